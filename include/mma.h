@@ -1,0 +1,287 @@
+/*
+ * mma.h -- Multipath Memory Access on one MI355X (gfx950): C ABI.
+ *
+ * One host<->GPU copy, tensor list or block-table KV transfer is split into
+ * micro-transfers that are driven concurrently over every path the GPU owns:
+ * its SDMA copy engines (submitted by a host engine thread) and CU-issued
+ * zero-copy loads/stores to pinned host memory (executed by the workgroups of
+ * a per-transfer "dummy-task" kernel). Paths pull work through per-path
+ * outstanding queues (backpressure, no link-state feedback); completion is
+ * aggregated through counters in device-visible memory, and the dummy-task
+ * kernel holds the caller's stream until every fragment has landed, so
+ * stream ordering is exactly that of the native copy it replaces.
+ *
+ * Paper: "Multipath Memory Access: Breaking Host--GPU Bandwidth Bottlenecks in
+ * LLM Serving" (arXiv 2512.16056). Section numbers below refer to it. The
+ * relay paths through peer GPUs (Section 3.4 relay scheduling, dual-pipeline
+ * relay) need a second GPU and are not part of this library.
+ *
+ * Conventions for every call:
+ *   - Returns mma_status_t: MMA_OK (0) or a negative error code. No call
+ *     aborts the process; details of the last error: mma_last_error().
+ *   - Argument validation happens before anything is enqueued: a call that
+ *     fails validation has no effect.
+ *   - bytes == 0 / n == 0 is an MMA_OK no-op (nothing is enqueued).
+ *   - `stream` is a hipStream_t (NULL = the device's null stream) of the
+ *     device passed to mma_init.
+ *   - Host buffers must be pinned and device-mapped (mma_host_alloc,
+ *     hipHostMalloc, or hipHostRegister with the mapped flag); pageable host
+ *     memory is rejected with MMA_ERR_NOT_PINNED. Device buffers must be
+ *     device memory of the initialised device.
+ *   - Descriptor arrays and block tables are copied before the call returns;
+ *     data buffers are borrowed until the stream has passed the transfer, as
+ *     with hipMemcpyAsync.
+ *   - Thread-safe: submissions are serialised internally.
+ *   - Asynchronous failures (an SDMA error, a wait-kernel watchdog timeout)
+ *     never hang the stream: the dummy-task kernel still exits, and every
+ *     later call returns the sticky MMA_ERR_TRANSFER_FAILED until
+ *     mma_clear_error().
+ */
+#ifndef MMA_H_
+#define MMA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t mma_status_t;
+
+#define MMA_OK 0
+#define MMA_ERR_NOT_INITIALIZED (-1)
+#define MMA_ERR_INVALID_ARG (-2)
+#define MMA_ERR_NOT_PINNED (-3)
+#define MMA_ERR_HIP (-4)
+#define MMA_ERR_HSA (-5)
+#define MMA_ERR_TRANSFER_FAILED (-6)
+#define MMA_ERR_ALREADY_INITIALIZED (-7)
+#define MMA_ERR_NO_MEMORY (-8)
+#define MMA_ERR_BUFFER_TOO_SMALL (-9)
+#define MMA_ERR_TIMEOUT (-10)
+
+/* Direction of a transfer. Only host<->device copies are handled (Section 3.2:
+ * GPU-to-GPU traffic is not intercepted). */
+#define MMA_H2D 0
+#define MMA_D2H 1
+
+/* Path mask bits: bit e (e < 16) = SDMA engine e; MMA_PATH_CU = the CU path. */
+#define MMA_PATH_CU 0x80000000u
+#define MMA_MAX_SDMA 16
+#define MMA_NUM_PATHS 17      /* stats index 16 = CU path */
+#define MMA_MAX_LAYERS 256    /* KV layers per call */
+
+/* Runtime tunables (Section 4, deployment: chunk size, thresholds and path
+ * set are configuration). Zero in any field selects its default. */
+typedef struct mma_config {
+  uint64_t chunk_bytes;     /* micro-task size; default 2 MiB (Section 3.4 Task Manager, 5.3) */
+  uint64_t fallback_bytes;  /* requests (or list tensors) below this are a single micro-task;
+                               default 2 * chunk_bytes (Section 3.2 fallback, 5.3 threshold) */
+  uint64_t small_bytes;     /* tensors below this are CU-path-only; default 64 KiB */
+  uint32_t queue_depth;     /* outstanding micro-tasks per SDMA engine; default 2 (Section 5.3) */
+  uint32_t cu_queue_depth;  /* outstanding micro-tasks on the CU path; default 2 */
+  uint32_t backoff_depth;   /* once a path's queue is full it pulls again only when its depth
+                               drops below this (Section 3.4 contention back-off);
+                               default = its queue depth (no extra back-off) */
+  uint32_t path_mask_h2d;   /* paths used host->device; default: CU path + the host-facing
+                               SDMA engines reported by ROCr */
+  uint32_t path_mask_d2h;   /* paths used device->host; same default */
+  uint32_t cu_workgroups;   /* max workgroups (4 wave64 each) of the dummy-task kernel; default 32 */
+  uint32_t cu_sub_bytes;    /* bytes one wave moves per CU claim; default 64 KiB */
+  uint32_t watchdog_ms;     /* wait-kernel gives up after this long without engine progress;
+                               default 20000 */
+  uint32_t reserved[4];
+} mma_config_t;
+
+typedef struct mma_copy_desc {
+  void* dst;
+  const void* src;
+  uint64_t bytes;
+} mma_copy_desc_t;
+
+/* Paged KV layout (Section 2.1 KV offload/fetch; the layout itself is a
+ * reading, the paper does not state it):
+ *   piece     = block_tokens * kv_heads * head_dim * elem_bytes bytes;
+ *   host pool = host_num_slots slots, slot s = [num_layers][2 (K,V)][piece];
+ *   GPU layer l (one pointer per layer) = [2 (K,V)][gpu_num_blocks][piece]. */
+typedef struct mma_kv_layout {
+  uint32_t num_layers;
+  uint32_t block_tokens;
+  uint32_t kv_heads;
+  uint32_t head_dim;
+  uint32_t elem_bytes;
+  uint32_t gpu_num_blocks;
+  uint32_t host_num_slots;
+  uint32_t reserved;
+} mma_kv_layout_t;
+
+typedef struct mma_stats {
+  uint64_t transfers;                     /* transfers retired */
+  uint64_t failed_transfers;
+  uint64_t path_bytes[MMA_NUM_PATHS];     /* payload bytes carried per path */
+  uint64_t path_tasks[MMA_NUM_PATHS];     /* micro-tasks carried per path */
+  uint64_t staging_bytes;                 /* HBM<->HBM bytes moved through SDMA staging */
+  uint64_t sdma_submit_failures;          /* submissions re-routed to the CU path */
+  uint64_t engine_cpu_ns;                 /* CPU time consumed by the engine threads */
+  uint64_t engine_wall_busy_ns;           /* wall time with at least one transfer active */
+  uint32_t sdma_engines_h2d;              /* masks actually in use */
+  uint32_t sdma_engines_d2h;
+  uint32_t cu_path_enabled;
+  uint32_t reserved;
+} mma_stats_t;
+
+/* One micro-task of a plan (host-only planner, exposed for verification).
+ * Linear/list plans: item = tensor index, offset = byte offset in the tensor,
+ * bytes = length, flags bit 0 = CU-path-only.
+ * KV plans: item = table index i, offset = first piece (2*l + k), bytes = piece count. */
+typedef struct mma_plan_entry {
+  uint64_t item;
+  uint64_t offset;
+  uint64_t bytes;
+  uint32_t flags;
+  uint32_t reserved;
+} mma_plan_entry_t;
+
+#define MMA_TASK_CU_ONLY 1u
+
+/* ---------------------------------------------------------------- lifecycle */
+
+/* Fill *out with the built-in defaults (no environment overrides, no GPU needed). */
+mma_status_t mma_config_default(mma_config_t* out);
+
+/* Initialise the library on HIP device `hip_device`: map it to its ROCr agent,
+ * discover its SDMA engines, allocate transfer records, and start one engine
+ * thread per direction (Section 4, Multipath Transfer Engine: separate H2D and
+ * D2H engines). cfg == NULL: defaults, then MMA_* environment overrides
+ * (MMA_CHUNK_BYTES, MMA_FALLBACK_BYTES, MMA_SMALL_BYTES, MMA_QUEUE_DEPTH,
+ * MMA_CU_QUEUE_DEPTH, MMA_BACKOFF_DEPTH, MMA_PATHS_H2D, MMA_PATHS_D2H,
+ * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS).
+ * Errors: MMA_ERR_ALREADY_INITIALIZED, MMA_ERR_INVALID_ARG (bad device or
+ * config), MMA_ERR_HIP / MMA_ERR_HSA. */
+mma_status_t mma_init(int hip_device, const mma_config_t* cfg);
+
+/* Wait for every submitted transfer to retire (bounded), stop the engine
+ * threads and release library resources. Returns MMA_ERR_TIMEOUT if in-flight
+ * transfers did not drain (their streams are then still blocked). */
+mma_status_t mma_finalize(void);
+
+/* The configuration in effect (after defaults and environment). */
+mma_status_t mma_get_config(mma_config_t* out);
+
+/* Host-side wait until every transfer submitted so far has retired, or
+ * timeout_ms elapsed (MMA_ERR_TIMEOUT). Does not synchronise any stream. */
+mma_status_t mma_synchronize(uint32_t timeout_ms);
+
+/* ------------------------------------------------------------ host memory */
+
+/* Pinned, device-mapped host memory, allocated on the GPU-local NUMA node when
+ * the platform reports one (Section 5.1 methodology: pinned host buffers).
+ * *out receives a pointer usable both by the host and as a kernel argument.
+ * Owned by the caller; free with mma_host_free. bytes == 0 -> *out = NULL. */
+mma_status_t mma_host_alloc(uint64_t bytes, void** out);
+mma_status_t mma_host_free(void* p);
+
+/* ---------------------------------------------------------------- transfers */
+
+/* Asynchronous copy of `bytes` bytes with hipMemcpyAsync semantics on `stream`
+ * (Section 3.1 workflow; Section 3.2 Transfer Task Interceptor; Section 3.3
+ * Sync Engine). dir = MMA_H2D: src pinned host, dst device; MMA_D2H: src
+ * device, dst pinned host. The stream-visible completion happens only after
+ * every micro-transfer has landed: work enqueued on `stream` after this call
+ * sees the whole copy, work before it is complete before any byte is read.
+ * Errors: MMA_ERR_INVALID_ARG (NULL with bytes > 0, bad dir, pointer of the
+ * wrong kind for dir), MMA_ERR_NOT_PINNED, MMA_ERR_HIP (launch failure),
+ * MMA_ERR_TRANSFER_FAILED (sticky), MMA_ERR_NOT_INITIALIZED. */
+mma_status_t mma_memcpy_async(void* dst, const void* src, uint64_t bytes, int32_t dir, void* stream);
+
+/* One logical transfer of a list of n independent copies, e.g. all weight
+ * tensors of a model (Section 2.1 model wake-up; Section 5.2.2). One dummy
+ * task covers the whole list. Each tensor is chunked on its own; tensors below
+ * small_bytes are CU-path-only. All copies share `dir`. Destination ranges
+ * must be pairwise disjoint (MMA_ERR_INVALID_ARG otherwise). `list` is copied
+ * before return. */
+mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t dir, void* stream);
+
+/* KV fetch, host pool -> paged GPU cache (Section 2.1 "fetching cached KV
+ * pages"; Section 5.2.1). For every i < n_blocks, l < num_layers, k in {K,V}:
+ *   gpu_layers[l][k][gpu_blocks[i]] = host_pool[host_slots[i]][l][k]
+ * Other GPU blocks are untouched. gpu_layers: num_layers device pointers, each
+ * to [2][gpu_num_blocks][piece]; host_pool: pinned, host_num_slots slots.
+ * Tables: int32, host_slots[i] in [0, host_num_slots), gpu_blocks[i] in
+ * [0, gpu_num_blocks), gpu_blocks distinct (MMA_ERR_INVALID_ARG otherwise).
+ * The pointer array and both tables are copied before return. */
+mma_status_t mma_kv_fetch(const mma_kv_layout_t* layout, const void* host_pool, void* const* gpu_layers,
+                          const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n_blocks,
+                          void* stream);
+
+/* KV offload, paged GPU cache -> host pool (Section 2.1 offload). For every
+ * j < n_blocks, l, k:  host_pool[host_slots[j]][l][k] = gpu_layers[l][k][gpu_blocks[j]].
+ * Other host slots are untouched. host_slots distinct; ranges as for fetch.
+ * Producer work enqueued on `stream` before this call is complete and visible
+ * before any byte is read. */
+mma_status_t mma_kv_offload(const mma_kv_layout_t* layout, void* host_pool, const void* const* gpu_layers,
+                            const int32_t* gpu_blocks, const int32_t* host_slots, uint64_t n_blocks,
+                            void* stream);
+
+/* Dependent HBM-bound check kernel (the mixed-contention workload's consumer):
+ * adds, modulo 2^64, digest = sum_i (w_i + 1) * (2i + 1) over the little-endian
+ * 32-bit words w_i of dev_ptr[0, bytes) (a trailing partial word is zero-
+ * padded) into *dev_out, ordered on `stream`. *dev_out is device memory the
+ * caller zeroed. Verifies that loads are visible to later stream work
+ * (Section 3.3 ordering requirement). */
+mma_status_t mma_digest_u32(const void* dev_ptr, uint64_t bytes, uint64_t* dev_out, void* stream);
+
+/* ------------------------------------------------------------------- status */
+
+mma_status_t mma_get_stats(mma_stats_t* out);
+mma_status_t mma_reset_stats(void);
+const char* mma_status_str(mma_status_t s);
+/* Thread-local text of the last error reported to this thread (never NULL). */
+const char* mma_last_error(void);
+/* Clear the sticky asynchronous-failure state. */
+mma_status_t mma_clear_error(void);
+
+/* ------------------------------------------------- host-only (no GPU needed) */
+
+/* The micro-task split of a tensor list (a single copy is a list of one):
+ * fixed chunks from offset 0, last one shorter; a tensor below `fallback` is
+ * one micro-task; below `small` it is CU-path-only (Section 3.4 Task Manager;
+ * Section 3.2 fallback). Writes up to `cap` entries to out and the total
+ * count to *n_out (MMA_ERR_BUFFER_TOO_SMALL if cap < total; out may then be
+ * NULL to query the count). */
+mma_status_t mma_plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, uint64_t fallback,
+                           uint64_t small, mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out);
+
+/* The micro-task split of a KV transfer: per table entry, consecutive pieces
+ * (piece index 2*l + k) in groups of max(1, chunk / piece_bytes). */
+mma_status_t mma_plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t piece_bytes, uint64_t chunk,
+                         mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out);
+
+/* Block-table check applied by mma_kv_fetch/offload: equal lengths implied,
+ * src[i] in [0, src_count), dst[i] in [0, dst_count), dst entries distinct.
+ * MMA_OK or MMA_ERR_INVALID_ARG. */
+mma_status_t mma_validate_kv_tables(const int32_t* src, uint32_t src_count, const int32_t* dst,
+                                    uint32_t dst_count, uint64_t n);
+
+/* ------------------------------------------------------------ test hooks */
+
+/* Faults forced from the host so that failure handling can be tested without
+ * any kernel faulting or hanging: every wait stays bounded.
+ *   MMA_FAULT_ENGINE_STALL_US: engine threads sleep `value` us before serving a
+ *     newly started transfer (stream must stay blocked, data stays correct).
+ *   MMA_FAULT_SDMA_SUBMIT_FAIL: the next `value` SDMA submissions fail; their
+ *     micro-tasks are re-routed to another path.
+ *   MMA_FAULT_ENGINE_IGNORE: while value != 0, engine threads do not serve newly
+ *     started transfers, so the wait kernel's watchdog must release the stream.
+ * value 0 clears a fault. */
+#define MMA_FAULT_ENGINE_STALL_US 1
+#define MMA_FAULT_SDMA_SUBMIT_FAIL 2
+#define MMA_FAULT_ENGINE_IGNORE 3
+mma_status_t mma_test_set_fault(int32_t kind, uint64_t value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MMA_H_ */

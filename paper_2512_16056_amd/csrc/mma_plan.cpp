@@ -1,0 +1,86 @@
+// Micro-transfer planner and argument checks (host-only).
+#include "mma_plan.h"
+
+#include <algorithm>
+
+#include "../../include/mma.h"
+
+namespace mma {
+
+void plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, uint64_t fallback, uint64_t small,
+               std::vector<PlanItem>& out) {
+  for (uint64_t t = 0; t < n; ++t) {
+    const uint64_t sz = sizes[t];
+    if (sz == 0) continue;
+    const uint32_t flags = sz < small ? kPlanCuOnly : 0u;
+    if (sz < fallback) {
+      out.push_back({t, 0, sz, flags});
+      continue;
+    }
+    for (uint64_t o = 0; o < sz; o += chunk) out.push_back({t, o, std::min(chunk, sz - o), flags});
+  }
+}
+
+void plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t piece_bytes, uint64_t chunk,
+             std::vector<PlanItem>& out) {
+  uint64_t per = piece_bytes ? chunk / piece_bytes : 1;
+  if (per < 1) per = 1;
+  for (uint64_t i = 0; i < n_blocks; ++i)
+    for (uint64_t p = 0; p < pieces_per_block; p += per)
+      out.push_back({i, p, std::min<uint64_t>(per, pieces_per_block - p), 0u});
+}
+
+bool tables_valid(const int32_t* src, uint32_t src_count, const int32_t* dst, uint32_t dst_count, uint64_t n) {
+  std::vector<uint8_t> seen(dst_count, 0);
+  for (uint64_t i = 0; i < n; ++i) {
+    if (src[i] < 0 || static_cast<uint32_t>(src[i]) >= src_count) return false;
+    if (dst[i] < 0 || static_cast<uint32_t>(dst[i]) >= dst_count) return false;
+    if (seen[dst[i]]) return false;
+    seen[dst[i]] = 1;
+  }
+  return true;
+}
+
+bool ranges_disjoint(std::vector<std::pair<uint64_t, uint64_t>> r) {
+  r.erase(std::remove_if(r.begin(), r.end(), [](const auto& x) { return x.second <= x.first; }), r.end());
+  std::sort(r.begin(), r.end());
+  for (size_t i = 1; i < r.size(); ++i)
+    if (r[i].first < r[i - 1].second) return false;
+  return true;
+}
+
+}  // namespace mma
+
+extern "C" {
+
+mma_status_t mma_plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, uint64_t fallback, uint64_t small,
+                           mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out) {
+  if (!n_out || chunk == 0 || (n && !sizes)) return MMA_ERR_INVALID_ARG;
+  std::vector<mma::PlanItem> v;
+  mma::plan_list(sizes, n, chunk, fallback, small, v);
+  *n_out = v.size();
+  if (!out) return cap == 0 ? MMA_OK : MMA_ERR_INVALID_ARG;
+  if (cap < v.size()) return MMA_ERR_BUFFER_TOO_SMALL;
+  for (size_t i = 0; i < v.size(); ++i) out[i] = {v[i].item, v[i].offset, v[i].bytes, v[i].flags, 0u};
+  return MMA_OK;
+}
+
+mma_status_t mma_plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t piece_bytes, uint64_t chunk,
+                         mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out) {
+  if (!n_out || chunk == 0 || piece_bytes == 0) return MMA_ERR_INVALID_ARG;
+  std::vector<mma::PlanItem> v;
+  mma::plan_kv(n_blocks, pieces_per_block, piece_bytes, chunk, v);
+  *n_out = v.size();
+  if (!out) return cap == 0 ? MMA_OK : MMA_ERR_INVALID_ARG;
+  if (cap < v.size()) return MMA_ERR_BUFFER_TOO_SMALL;
+  for (size_t i = 0; i < v.size(); ++i) out[i] = {v[i].item, v[i].offset, v[i].bytes, v[i].flags, 0u};
+  return MMA_OK;
+}
+
+mma_status_t mma_validate_kv_tables(const int32_t* src, uint32_t src_count, const int32_t* dst, uint32_t dst_count,
+                                    uint64_t n) {
+  if (n && (!src || !dst)) return MMA_ERR_INVALID_ARG;
+  return mma::tables_valid(src, src_count, dst, dst_count, n) ? MMA_OK : MMA_ERR_INVALID_ARG;
+}
+
+}  // extern "C"

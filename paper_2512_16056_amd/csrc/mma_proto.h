@@ -1,0 +1,104 @@
+// Host <-> GPU protocol of one transfer: the record that the host engine thread
+// and the dummy-task kernel share, and the kernel's launch arguments.
+//
+// A record lives in coherent (fine-grained) pinned host memory, mapped into the
+// GPU's address space. Every field has exactly one writer:
+//   host -> GPU : seq, closed, cu_total, complete, heartbeat, KV geometry,
+//                 ring entries (payload, then tag)
+//   GPU  -> host: started, released, status, done[]
+// Values are epoch-stamped with the transfer's sequence number, which never
+// repeats, so nothing is ever reset between uses of a record (no ABA).
+//
+// The CU ring is the CU path's outstanding queue (Section 3.4, Path Selector:
+// one outstanding queue per path). The engine thread appends entries; waves of
+// the dummy-task kernel claim them in ticket order with a device-memory atomic,
+// so the GPU side needs no PCIe atomics.
+#ifndef MMA_PROTO_H_
+#define MMA_PROTO_H_
+
+#include <stdint.h>
+
+namespace mma {
+
+constexpr uint32_t kRingSize = 1024;   // CU ring entries per record
+constexpr uint32_t kRecords = 128;     // records per direction (transfers in flight)
+constexpr uint32_t kMaxLayers = 256;   // KV layer pointers per record
+constexpr uint32_t kWave = 64;
+constexpr uint32_t kWavesPerWG = 4;
+constexpr uint32_t kBlock = kWave * kWavesPerWG;
+
+// Entry kinds. Kind and first piece share one 32-bit word: kind | p0 << 8.
+enum : uint32_t {
+  kEntryCopy = 1,       // a -> b, `count` bytes
+  kEntryToPaged = 2,    // contiguous pieces at a -> GPU layers, block b, pieces p0 .. p0+count
+  kEntryFromPaged = 3,  // GPU layers, block b, pieces p0 .. p0+count -> contiguous at a
+  kEntryKindMask = 0x7F,
+  // Flag: the source was written by a copy engine while the kernel runs (SDMA
+  // staging); the wave must acquire (invalidate its caches) before reading it.
+  kEntryAcquire = 0x80,
+};
+
+struct CuEntry {      // 32 bytes; `tag` is stored last, with release semantics
+  uint64_t a;
+  uint64_t b;
+  uint32_t count;
+  uint32_t kind_p0;
+  uint64_t tag;
+};
+
+struct alignas(64) RecordHdr {
+  // cache line 0: host -> GPU control
+  uint64_t seq;
+  uint64_t closed;       // == seq: no more ring entries will be appended
+  uint64_t cu_total;     // number of entries appended (valid once closed == seq)
+  uint64_t complete;     // == seq: every micro-task has landed; the wait may end
+  uint64_t heartbeat;    // bumped on engine progress; re-arms the kernel watchdog
+  uint64_t pad0[3];
+  // cache line 1: GPU -> host
+  uint64_t started;      // == seq once the stream reached the dummy task
+  uint64_t pad1[7];
+  // cache line 2: GPU -> host
+  uint64_t released;     // == seq once the kernel is done with this record
+  int32_t status;        // 0 ok, 1 watchdog expired
+  int32_t pad2a;
+  uint64_t pad2[6];
+  // cache line 3: KV geometry (host -> GPU, written before launch)
+  uint64_t kv_piece_bytes;
+  uint64_t kv_kstride;   // bytes between K and V halves of a GPU layer tensor
+  uint32_t kv_layers;
+  uint32_t pad3a;
+  uint64_t pad3[5];
+  uint64_t layer_ptr[kMaxLayers];
+};
+
+struct Record {
+  RecordHdr h;
+  CuEntry ring[kRingSize];
+  uint64_t done[kRingSize];  // GPU -> host: tag of the entry completed in this slot
+};
+
+// Per-record scratch in device memory, shared by the waves of one kernel.
+// The last wave to leave resets it before releasing the record.
+struct alignas(128) DevState {
+  uint64_t cursor;     // next ticket to claim
+  uint32_t arrived;    // waves that have started
+  uint32_t exited;     // waves that have finished claiming
+  uint32_t timed_out;  // a wave's watchdog expired
+  uint32_t pad[27];
+};
+
+struct KernelArgs {
+  Record* rec;              // device-visible address of the record
+  DevState* ds;
+  uint64_t seq;
+  uint64_t watchdog_ticks;  // wall-clock ticks without progress before giving up
+  uint32_t total_waves;
+  uint32_t release_each;    // 1: system-scope release before each done flag
+};
+
+// constexpr: usable from host and device code alike.
+constexpr uint64_t make_tag(uint64_t seq, uint64_t ticket) { return (seq << 32) | (ticket + 1); }
+
+}  // namespace mma
+
+#endif  // MMA_PROTO_H_

@@ -1,0 +1,105 @@
+"""Host-side checks of the C ABI (no GPU needed): symbol exports, one HIP runtime
+in the process, the planner and table validation against the oracle."""
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import kv as okv
+from oracle import plan as oplan
+
+mma = pytest.importorskip("paper_2512_16056_amd")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "mma.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:mma_status_t|const char\*)\s+(mma_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(mma.lib, n), n
+        assert n in mma._SIGNATURES, f"binding lacks {n}"
+
+
+def test_single_hip_runtime_in_process():
+    maps = open("/proc/self/maps").read()
+    hips = {line.split()[-1] for line in maps.splitlines() if "libamdhip64" in line}
+    assert len(hips) == 1, hips
+
+
+def test_status_strings_and_defaults():
+    assert mma.mma_status_str(0) == "MMA_OK"
+    assert mma.mma_status_str(-3) == "MMA_ERR_NOT_PINNED"
+    c = mma.mma_config_default()
+    assert c.chunk_bytes == 2 << 20 and c.queue_depth == 2 and c.cu_sub_bytes == 64 << 10
+    assert c.small_bytes == 64 << 10 and c.cu_workgroups > 0 and c.watchdog_ms > 0
+
+
+def test_calls_before_init_fail_cleanly():
+    with pytest.raises(mma.MMAError) as e:
+        mma.mma_memcpy_async(0, 0, 16, mma.MMA_H2D, 0)
+    assert e.value.name == "MMA_ERR_NOT_INITIALIZED"
+    with pytest.raises(mma.MMAError):
+        mma.mma_get_stats()
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd") and os.access("/dev/kfd", os.R_OK), reason="GPU present")
+def test_init_without_gpu_reports_error():
+    with pytest.raises(mma.MMAError) as e:
+        mma.mma_init(0)
+    assert e.value.name == "MMA_ERR_INVALID_ARG"
+
+
+def _as_oracle_list(entries):
+    return [(i, o, b, bool(f & mma.MMA_TASK_CU_ONLY)) for i, o, b, f in entries]
+
+
+@pytest.mark.parametrize("chunk,fallback,small", [(16, 32, 8), (7, 7, 1), (64, 200, 64), (4096, 8192, 1000)])
+def test_plan_list_matches_oracle(chunk, fallback, small):
+    r = np.random.default_rng(chunk)
+    for _ in range(30):
+        sizes = [int(x) for x in r.integers(0, 600, r.integers(1, 12))]
+        got = _as_oracle_list(mma.mma_plan_list(sizes, chunk, fallback, small))
+        assert got == oplan.plan_list(sizes, chunk, fallback, small)
+
+
+def test_plan_workload_counts_match_oracle():
+    M, K = W.MiB, W.KiB
+    sizes = W.weight_tensor_bytes()
+    for chunk in (2 * M, 256 * K, 5 * 1000 * 1000):
+        got = mma.mma_plan_list(sizes, chunk, 2 * chunk, 64 * K)
+        want = oplan.plan_list(sizes, chunk, 2 * chunk, 64 * K)
+        assert _as_oracle_list(got) == want
+    s = W.KV64K
+    for chunk in (2 * M, 256 * K, 100 * K, 16 * K):
+        got = mma.mma_plan_kv(4096, s.pieces_per_block, s.piece_bytes, chunk)
+        assert [(i, o, b) for i, o, b, _ in got] == oplan.plan_kv(4096, s.pieces_per_block, s.piece_bytes, chunk)
+        assert oplan.kv_covers_exactly_once([(i, o, b) for i, o, b, _ in got], 4096, s.pieces_per_block)
+
+
+def test_plan_linear_covers_exactly_once():
+    for n in list(range(0, 70)) + [4095, 4096, 4097, 1 << 20, (1 << 20) + 13]:
+        for chunk in (16, 48, 4096):
+            got = mma.mma_plan_list([n], chunk, 2 * chunk, 0)
+            assert (n == 0 and got == []) or oplan.covers_exactly_once([(o, b) for _, o, b, _ in got], n)
+
+
+def test_validate_tables_matches_oracle():
+    r = np.random.default_rng(4)
+    for _ in range(300):
+        n = int(r.integers(0, 8))
+        sc, dc = int(r.integers(1, 8)), int(r.integers(1, 8))
+        src = r.integers(-1, sc + 1, n)
+        dst = r.integers(-1, dc + 1, n)
+        assert mma.mma_validate_kv_tables(src, sc, dst, dc) == okv.validate_tables(src, sc, dst, dc)
+    for perm in itertools.permutations(range(4)):
+        assert mma.mma_validate_kv_tables([0, 1, 2, 3], 4, perm, 4)

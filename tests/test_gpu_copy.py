@@ -1,0 +1,172 @@
+"""GPU parity of single copies and tensor lists against the oracle (byte-exact).
+
+Every case calls the library through the C ABI (via the ctypes binding) and
+compares each destination byte -- inside and outside the copied ranges -- with
+oracle.copy on the same seeded inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import copy as ocopy
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU hosts too; every test here is gpu-marked
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2512_16056_amd as mma  # noqa: E402
+from gpu_helpers import PATHS, device_bytes, from_host, log, session, to_host  # noqa: E402
+
+SIZES = [0, 1, 2, 3, 15, 16, 17, 31, 32, 33, 63, 64, 65, 255, 256, 257, 1023, 1024, 1025, 4095, 4096]
+SRC_OFFS = [0, 1, 2, 3, 4, 7, 8, 9, 15]
+DST_OFFS = [0, 1, 7, 15]
+REGION = 8192
+
+
+def _cases():
+    return [(n, so, do) for n in SIZES for so in SRC_OFFS for do in DST_OFFS]
+
+
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+@pytest.mark.parametrize("chunk", [16, 48, 4096])
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_tiny_bruteforce(paths, chunk, direction):
+    log(f"tiny bruteforce paths={paths} chunk={chunk} dir={direction}")
+    cases = _cases()
+    src_np = np.ascontiguousarray(W.uniform_bytes(0, 0, chunk, REGION + 64))
+    poison = np.full(len(cases) * REGION, 0xFF, np.uint8)
+    # small_bytes=1: even the tiny copies may ride an SDMA engine
+    with session(paths, chunk_bytes=chunk, small_bytes=1):
+        if direction == mma.MMA_H2D:
+            src = mma.PinnedBuffer(src_np.size)
+            src.array[:] = src_np
+            dst = from_host(poison)
+            for k, (n, so, do) in enumerate(cases):
+                mma.mma_memcpy_async(dst.data_ptr() + k * REGION + do, src.ptr + so, n, direction)
+            torch.cuda.synchronize()
+            mma.mma_synchronize()
+            got = to_host(dst)
+        else:
+            src = from_host(src_np)
+            dst = mma.PinnedBuffer(poison.size)
+            dst.array[:] = poison
+            for k, (n, so, do) in enumerate(cases):
+                mma.mma_memcpy_async(dst.ptr + k * REGION + do, src.data_ptr() + so, n, direction)
+            torch.cuda.synchronize()
+            mma.mma_synchronize()
+            got = dst.array.copy()
+        stats = mma.mma_get_stats()
+    for k, (n, so, do) in enumerate(cases):
+        want = ocopy.memcpy(poison[k * REGION:(k + 1) * REGION], do, src_np, so, n)
+        assert np.array_equal(got[k * REGION:(k + 1) * REGION], want), (n, so, do)
+    assert stats["failed_transfers"] == 0
+    if paths == "cu":
+        assert sum(stats["path_bytes"][:16]) == 0
+    if paths == "sdma":
+        assert stats["path_bytes"][16] == 0
+
+
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_copy_64mib(paths, direction):
+    """The 64 MiB workload: one host->GPU copy split into 2 MiB micro-transfers (and its reverse)."""
+    log(f"64MiB copy paths={paths} dir={direction}")
+    n = W.COPY64_BYTES
+    src_np = np.ascontiguousarray(W.uniform_bytes(1, W.TAG_DATA, 0, n))
+    with session(paths, chunk_bytes=W.COPY64_CHUNK):
+        for rep in range(3):
+            if direction == mma.MMA_H2D:
+                src = mma.PinnedBuffer(n)
+                src.array[:] = src_np
+                dst = device_bytes(n, W.WEIGHT_POISON)
+                mma.mma_memcpy_async(dst, src, n, direction)
+                torch.cuda.synchronize()
+                got = to_host(dst)
+            else:
+                src = from_host(src_np)
+                dst = mma.PinnedBuffer(n)
+                dst.array[:] = W.WEIGHT_POISON
+                mma.mma_memcpy_async(dst, src, n, direction)
+                torch.cuda.synchronize()
+                got = dst.array.copy()
+            assert np.array_equal(got, ocopy.memcpy(np.full(n, W.WEIGHT_POISON, np.uint8), 0, src_np, 0, n))
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+    assert stats["failed_transfers"] == 0
+    total = sum(stats["path_bytes"])
+    assert total == 3 * n
+    log(f"  path bytes: cu={stats['path_bytes'][16]} sdma={stats['path_bytes'][:4]}")
+
+
+def _ragged_list(seed, count, max_size):
+    r = np.random.default_rng(seed)
+    sizes = [int(x) for x in r.integers(0, max_size, count)]
+    sizes[0] = 0
+    sizes[1] = 1
+    sizes[2] = 64 * 1024 - 1   # just below the CU-only threshold
+    sizes[3] = 64 * 1024       # at the threshold
+    return sizes
+
+
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_tensor_list_ragged(paths, direction):
+    log(f"tensor list paths={paths} dir={direction}")
+    sizes = _ragged_list(7 + direction, 40, 3 * 1024 * 1024)
+    src_offs, total = W.arena_offsets(sizes, 16)
+    # destinations interleaved with untouched 4 KiB gaps, some misaligned by 16 B
+    dst_offs, cur = [], 4096
+    for s in sizes:
+        dst_offs.append(cur)
+        cur += s + 4096 + 16
+    dtotal = cur
+    src_np = np.ascontiguousarray(W.uniform_bytes(2, W.TAG_DATA, 99, total))
+    poison = np.full(dtotal, W.WEIGHT_POISON, np.uint8)
+    with session(paths, chunk_bytes=256 * 1024):
+        if direction == mma.MMA_H2D:
+            src = mma.PinnedBuffer(total)
+            src.array[:] = src_np
+            dst = from_host(poison)
+            mma.mma_weights_load([(dst.data_ptr() + d, src.ptr + s, n) for d, s, n in zip(dst_offs, src_offs, sizes)],
+                                 direction)
+            torch.cuda.synchronize()
+            got = to_host(dst)
+        else:
+            src = from_host(src_np)
+            dst = mma.PinnedBuffer(dtotal)
+            dst.array[:] = poison
+            mma.mma_weights_load([(dst.ptr + d, src.data_ptr() + s, n) for d, s, n in zip(dst_offs, src_offs, sizes)],
+                                 direction)
+            torch.cuda.synchronize()
+            got = dst.array.copy()
+        mma.mma_synchronize()
+    want = ocopy.tensor_list(poison, src_np, list(zip(dst_offs, src_offs, sizes)))
+    assert np.array_equal(got, want)
+
+
+def test_rejects_bad_arguments():
+    with session("both"):
+        src = mma.PinnedBuffer(4096)
+        dst = device_bytes(4096)
+        pageable = np.zeros(4096, np.uint8)
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_memcpy_async(dst, pageable, 4096, mma.MMA_H2D)
+        assert e.value.name == "MMA_ERR_NOT_PINNED"
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_memcpy_async(dst, src, 4096, 7)
+        assert e.value.name == "MMA_ERR_INVALID_ARG"
+        with pytest.raises(mma.MMAError) as e:          # host range runs past the allocation
+            mma.mma_memcpy_async(dst, src, 8192, mma.MMA_H2D)
+        assert e.value.name in ("MMA_ERR_NOT_PINNED", "MMA_ERR_INVALID_ARG")
+        with pytest.raises(mma.MMAError) as e:          # device pointer where host memory is expected
+            mma.mma_memcpy_async(dst, dst, 16, mma.MMA_H2D)
+        assert e.value.name == "MMA_ERR_INVALID_ARG"
+        with pytest.raises(mma.MMAError) as e:          # overlapping destinations
+            mma.mma_weights_load([(dst, src, 64), (dst.data_ptr() + 32, src, 64)], mma.MMA_H2D)
+        assert e.value.name == "MMA_ERR_INVALID_ARG"
+        mma.mma_memcpy_async(dst, src, 0, mma.MMA_H2D)   # zero bytes: no-op
+        mma.mma_weights_load([], mma.MMA_H2D)
+        torch.cuda.synchronize()
+        src.free()

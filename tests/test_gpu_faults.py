@@ -1,0 +1,96 @@
+"""Failure handling, with every fault forced from the host: kernels still exit
+through their own bounded waits, nothing on the GPU faults or hangs."""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2512_16056_amd as mma  # noqa: E402
+from gpu_helpers import log, session, to_host  # noqa: E402
+
+
+def _copy_and_check(n, paths="both", **cfg):
+    src_np = np.ascontiguousarray(W.uniform_bytes(12, 0, n, n))
+    src = mma.PinnedBuffer(n)
+    src.array[:] = src_np
+    dst = torch.full((n,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
+    t0 = time.time()
+    mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D)
+    torch.cuda.synchronize()
+    dt = time.time() - t0
+    assert np.array_equal(to_host(dst), src_np)
+    src.free()
+    return dt
+
+
+def test_sdma_submit_failures_are_rerouted():
+    with session("both", chunk_bytes=1 << 20):
+        mma.mma_reset_stats()
+        mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 3)
+        _copy_and_check(32 << 20)
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+        mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 0)
+    log(f"  submit failures={st['sdma_submit_failures']} path bytes={st['path_bytes'][:2]}+cu {st['path_bytes'][16]}")
+    assert st["failed_transfers"] == 0
+    assert 1 <= st["sdma_submit_failures"] <= 3
+
+
+def test_sdma_only_submit_failures_fall_back_to_cu():
+    with session("sdma", chunk_bytes=1 << 20):
+        mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 1000000)
+        _copy_and_check(8 << 20)
+        mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 0)
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+    assert st["path_bytes"][16] == 8 << 20
+
+
+def test_engine_stall_keeps_stream_blocked():
+    with session("both", chunk_bytes=1 << 20):
+        mma.mma_test_set_fault(mma.MMA_FAULT_ENGINE_STALL_US, 200000)
+        try:
+            dt = _copy_and_check(16 << 20)
+        finally:
+            mma.mma_test_set_fault(mma.MMA_FAULT_ENGINE_STALL_US, 0)
+        mma.mma_synchronize()
+    log(f"  stalled copy took {dt * 1e3:.1f} ms")
+    assert dt >= 0.15
+
+
+def test_watchdog_releases_stream_and_error_is_sticky():
+    n = 8 << 20
+    with session("both", chunk_bytes=1 << 20, watchdog_ms=300):
+        src = mma.PinnedBuffer(n)
+        dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+        mma.mma_test_set_fault(mma.MMA_FAULT_ENGINE_IGNORE, 1)
+        try:
+            t0 = time.time()
+            mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D)
+            torch.cuda.synchronize()            # must return: the wait kernel's watchdog ends it
+            dt = time.time() - t0
+            deadline = time.time() + 10
+            while mma.mma_get_stats()["failed_transfers"] == 0 and time.time() < deadline:
+                time.sleep(0.01)
+        finally:
+            mma.mma_test_set_fault(mma.MMA_FAULT_ENGINE_IGNORE, 0)
+        log(f"  watchdog released the stream after {dt * 1e3:.0f} ms")
+        assert mma.mma_get_stats()["failed_transfers"] == 1
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D)
+        assert e.value.name == "MMA_ERR_TRANSFER_FAILED"
+        mma.mma_clear_error()
+        src.array[:] = 3
+        mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D)
+        torch.cuda.synchronize()
+        assert bool((dst == 3).all())
+        mma.mma_synchronize()
+        src.free()

@@ -1,0 +1,214 @@
+"""GPU parity of paged-KV fetch and offload against oracle.kv (byte-exact).
+
+Small shapes cover several micro-tasks, CU sub-entries and SDMA staging slots,
+ragged pieces (not a multiple of 16 bytes), every permutation of 4-entry tables,
+and both paths; the full 64k-token workloads are checked layer by layer / over the
+whole host pool.
+"""
+import itertools
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import kv as okv
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2512_16056_amd as mma  # noqa: E402
+from gpu_helpers import PATHS, device_bytes, log, session, to_host  # noqa: E402
+
+
+def layout_of(s: W.KVShape):
+    return mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                         s.host_num_slots)
+
+
+def _pool(s: W.KVShape, seed: int):
+    buf = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+    r = np.random.default_rng(seed)
+    buf.array[:] = r.integers(0, 256, buf.nbytes, dtype=np.uint8)
+    return buf
+
+
+def _layers(s: W.KVShape, fill=None, seed=None):
+    out = []
+    for l in range(s.layers):
+        t = device_bytes(s.layer_bytes, fill)
+        if seed is not None:
+            r = np.random.default_rng(seed + l)
+            t.copy_(torch.from_numpy(r.integers(0, 256, s.layer_bytes, dtype=np.uint8)))
+        out.append(t)
+    return out
+
+
+def _layer_views(s, layers):
+    return [to_host(t).reshape(2, s.gpu_num_blocks, s.piece_bytes) for t in layers]
+
+
+def check_fetch(s, pool, layers_before, layers_after, hs, gb):
+    pool_v = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+    for l in range(s.layers):
+        want = okv.kv_fetch_layer(pool_v, layers_before[l], l, s.layers, hs, gb)
+        got = to_host(layers_after[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
+        assert np.array_equal(got, want), f"layer {l}"
+
+
+SHAPES = {
+    "small": W.small_kv_shape(),
+    "ragged": W.KVShape(layers=3, block_tokens=1, kv_heads=1, head_dim=5, elem_bytes=2,
+                        gpu_num_blocks=50, host_num_slots=40, n_blocks=37),
+    "medium": W.KVShape(layers=4, block_tokens=16, kv_heads=2, head_dim=64, elem_bytes=2,
+                        gpu_num_blocks=300, host_num_slots=256, n_blocks=200),
+}
+
+
+@pytest.mark.parametrize("chunk", [4096, 65536])
+@pytest.mark.parametrize("shape", list(SHAPES))
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_kv_fetch_small(paths, shape, chunk):
+    s = SHAPES[shape]
+    log(f"kv fetch paths={paths} shape={shape} chunk={chunk}")
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
+        pool = _pool(s, 1)
+        layers = _layers(s, W.GPU_POISON)
+        before = _layer_views(s, layers)
+        mma.mma_kv_fetch(layout_of(s), pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+        check_fetch(s, pool, before, layers, hs, gb)
+    assert stats["failed_transfers"] == 0
+    assert sum(stats["path_bytes"]) == s.n_blocks * s.slot_bytes
+
+
+@pytest.mark.parametrize("chunk", [4096, 65536])
+@pytest.mark.parametrize("shape", list(SHAPES))
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_kv_offload_small(paths, shape, chunk):
+    s = SHAPES[shape]
+    log(f"kv offload paths={paths} shape={shape} chunk={chunk}")
+    plan = W.kv_offload_plan(s, cfg=4)
+    with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
+        pool = _pool(s, 2)
+        before = pool.array.copy()
+        layers = _layers(s, seed=100)
+        views = _layer_views(s, layers)
+        mma.mma_kv_offload(layout_of(s), pool, layers, plan.src_blocks, plan.dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        want = okv.kv_offload(before.reshape(s.host_num_slots, -1), views, plan.src_blocks, plan.dest)
+        assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
+
+
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_kv_all_permutations(paths):
+    s = W.KVShape(layers=2, block_tokens=2, kv_heads=1, head_dim=8, elem_bytes=2,
+                  gpu_num_blocks=6, host_num_slots=4, n_blocks=4)
+    with session(paths, chunk_bytes=64, cu_sub_bytes=256):
+        pool = _pool(s, 3)
+        src_layers = _layers(s, seed=7)
+        src_views = _layer_views(s, src_layers)
+        for perm in itertools.permutations(range(4)):
+            hs = list(perm)
+            gb = [5, 0, 3, 1]
+            layers = _layers(s, W.GPU_POISON)
+            before = _layer_views(s, layers)
+            mma.mma_kv_fetch(layout_of(s), pool, layers, hs, gb)
+            torch.cuda.synchronize()
+            check_fetch(s, pool, before, layers, hs, gb)
+            host = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+            host.array[:] = W.HOST_FREE_POISON
+            mma.mma_kv_offload(layout_of(s), host, src_layers, [2, 4, 0, 5], hs)
+            torch.cuda.synchronize()
+            want = okv.kv_offload(np.full((s.host_num_slots, s.slot_bytes), W.HOST_FREE_POISON, np.uint8),
+                                  src_views, [2, 4, 0, 5], hs)
+            assert np.array_equal(host.array.reshape(s.host_num_slots, -1), want), perm
+            host.free()
+        mma.mma_synchronize()
+
+
+def test_kv_rejects_bad_tables():
+    s = SHAPES["small"]
+    with session("both"):
+        pool = _pool(s, 1)
+        layers = _layers(s, 0)
+        lay = layout_of(s)
+        for hs, gb in [([0, 1], [3, 3]), ([0, s.host_num_slots], [0, 1]), ([0, 1], [0, s.gpu_num_blocks]),
+                       ([-1, 1], [0, 1])]:
+            with pytest.raises(mma.MMAError) as e:
+                mma.mma_kv_fetch(lay, pool, layers, hs, gb)
+            assert e.value.name == "MMA_ERR_INVALID_ARG"
+        with pytest.raises(mma.MMAError):  # duplicate destination slot on offload
+            mma.mma_kv_offload(lay, pool, layers, [0, 1], [2, 2])
+        mma.mma_kv_fetch(lay, pool, layers, [], [])  # empty: no-op
+        torch.cuda.synchronize()
+
+
+def _fill_pool_c3(pool: np.ndarray, s: W.KVShape, hs: np.ndarray):
+    v = pool.reshape(s.host_num_slots, s.slot_bytes)
+    for i in range(s.n_blocks):
+        v[hs[i]] = W.kv_block_bytes(3, i, s)
+
+
+@pytest.mark.slow
+def test_kv_fetch_64k_full():
+    """The 64k-token KV fetch workload (8 GiB), in the configuration the benchmark times."""
+    s = W.KV64K
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    with session("both"):
+        pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+        t0 = time.time()
+        _fill_pool_c3(pool.array, s, hs)
+        log(f"  pool generated in {time.time() - t0:.1f}s")
+        layers = _layers(s, W.GPU_POISON)
+        poison = np.full((2, s.gpu_num_blocks, s.piece_bytes), W.GPU_POISON, np.uint8)
+        mma.mma_kv_fetch(layout_of(s), pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+        log(f"  path bytes: cu={stats['path_bytes'][16]} sdma={stats['path_bytes'][:4]}")
+        pool_v = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+        for l in range(s.layers):
+            want = okv.kv_fetch_layer(pool_v, poison, l, s.layers, hs, gb)
+            got = to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
+            assert np.array_equal(got, want), f"layer {l}"
+        pool.free()
+    assert stats["failed_transfers"] == 0
+
+
+@pytest.mark.slow
+def test_kv_offload_64k_full():
+    """KV offload of a 50% dirty subset (4 GiB) into free host slots; the whole 8 GiB pool is verified."""
+    s = W.KV64K
+    plan = W.kv_offload_plan(s, cfg=4)
+    with session("both"):
+        pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+        pv = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+        for slot in plan.occupied:
+            pv[slot] = W.kv_occupied_bytes(4, int(slot), s)
+        pv[plan.free] = W.HOST_FREE_POISON
+        before = pv.copy()
+        layers = _layers(s, W.GPU_POISON)
+        # logical block i lives at GPU block gpu_blocks_all[i]
+        blocks = np.empty((s.n_blocks, s.layers, 2, s.piece_bytes), np.uint8)
+        for i in range(s.n_blocks):
+            blocks[i] = W.kv_block_bytes(4, i, s).reshape(s.layers, 2, s.piece_bytes)
+        for l in range(s.layers):
+            lay_np = np.full((2, s.gpu_num_blocks, s.piece_bytes), W.GPU_POISON, np.uint8)
+            lay_np[:, plan.gpu_blocks_all] = blocks[:, l].transpose(1, 0, 2)
+            layers[l].copy_(torch.from_numpy(lay_np.reshape(-1)))
+        del blocks
+        views = _layer_views(s, layers)
+        mma.mma_kv_offload(layout_of(s), pool, layers, plan.src_blocks, plan.dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        want = okv.kv_offload(before, views, plan.src_blocks, plan.dest)
+        assert np.array_equal(pv, want)
+        pool.free()
