@@ -793,18 +793,19 @@ mma_status_t check_ready() {
   return MMA_OK;
 }
 
-// [p, p + bytes) must lie inside the single allocation that contains p.
+// [p, p + bytes) must lie inside one allocation: its first and last byte carry
+// the same buffer id. (The runtime's RANGE_SIZE attribute is not used: it is
+// truncated to 32 bits for allocations of 4 GiB and more.)
 bool within_allocation(const void* p, uint64_t bytes) {
-  void* base = nullptr;
-  size_t size = 0;
-  hipDeviceptr_t dp = const_cast<void*>(p);
-  if (hipPointerGetAttribute(&base, HIP_POINTER_ATTRIBUTE_RANGE_START_ADDR, dp) != hipSuccess ||
-      hipPointerGetAttribute(&size, HIP_POINTER_ATTRIBUTE_RANGE_SIZE, dp) != hipSuccess) {
+  uint64_t id0 = 0, id1 = 0;
+  hipDeviceptr_t first = const_cast<void*>(p);
+  hipDeviceptr_t last = static_cast<uint8_t*>(const_cast<void*>(p)) + (bytes - 1);
+  if (hipPointerGetAttribute(&id0, HIP_POINTER_ATTRIBUTE_BUFFER_ID, first) != hipSuccess ||
+      hipPointerGetAttribute(&id1, HIP_POINTER_ATTRIBUTE_BUFFER_ID, last) != hipSuccess) {
     (void)hipGetLastError();
     return false;
   }
-  const uint64_t b = reinterpret_cast<uint64_t>(base), q = reinterpret_cast<uint64_t>(p);
-  return q >= b && bytes <= size && q - b <= size - bytes;
+  return id0 == id1 && id0 != 0;
 }
 
 // Pinned, device-mapped host range: returns the device-visible address of p.
