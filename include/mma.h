@@ -80,14 +80,15 @@ typedef struct mma_config {
                                default 2 * chunk_bytes (Section 3.2 fallback, 5.3 threshold) */
   uint64_t small_bytes;     /* tensors below this are CU-path-only; default 64 KiB */
   uint32_t queue_depth;     /* outstanding micro-tasks per SDMA engine; default 2 (Section 5.3) */
-  uint32_t cu_queue_depth;  /* outstanding micro-tasks on the CU path; default 2 */
+  uint32_t cu_queue_depth;  /* outstanding micro-tasks on the CU path; default 4 */
   uint32_t backoff_depth;   /* once a path's queue is full it pulls again only when its depth
                                drops below this (Section 3.4 contention back-off);
                                default = its queue depth (no extra back-off) */
   uint32_t path_mask_h2d;   /* paths used host->device; default: CU path + the host-facing
                                SDMA engines reported by ROCr */
   uint32_t path_mask_d2h;   /* paths used device->host; same default */
-  uint32_t cu_workgroups;   /* max workgroups (4 wave64 each) of the dummy-task kernel; default 32 */
+  uint32_t cu_workgroups;   /* max workgroups (4 wave64 each) of the dummy-task kernel; default 16,
+                               at most 256; chunk_bytes / cu_sub_bytes must not exceed 2048 */
   uint32_t cu_sub_bytes;    /* bytes one wave moves per CU claim; default 64 KiB */
   uint32_t watchdog_ms;     /* wait-kernel gives up after this long without engine progress;
                                default 20000 */
@@ -263,6 +264,33 @@ mma_status_t mma_plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t 
  * MMA_OK or MMA_ERR_INVALID_ARG. */
 mma_status_t mma_validate_kv_tables(const int32_t* src, uint32_t src_count, const int32_t* dst,
                                     uint32_t dst_count, uint64_t n);
+
+/* ------------------------------------------------------------------ tracing */
+
+/* Per-transfer timeline, recorded when a transfer retires (Section 5: transfer
+ * latency and per-path load). Timestamps are CLOCK_MONOTONIC nanoseconds of the
+ * host: API entry, submission (after validation and planning), first
+ * observation of the start signal, first SDMA
+ * submission (0 if none), last micro-task landed, `complete` published, and
+ * retirement (the dummy-task kernel has left the record). kind: 0 copy/list,
+ * 1 KV fetch, 2 KV offload. path_tasks: micro-tasks carried per path. */
+typedef struct mma_trace_rec {
+  uint64_t seq;
+  int32_t dir;
+  int32_t kind;
+  uint64_t bytes;
+  uint64_t tasks;
+  uint64_t t_api_ns, t_submit_ns, t_started_ns, t_first_sdma_ns, t_last_task_ns, t_complete_ns, t_retire_ns;
+  uint64_t path_tasks[MMA_NUM_PATHS];
+  int32_t failed;
+  int32_t reserved;
+} mma_trace_rec_t;
+
+/* Start (on != 0: the buffer is cleared) or stop recording. Also enabled by
+ * MMA_TRACE=1 at mma_init. At most 65536 records are kept (oldest dropped). */
+mma_status_t mma_trace_enable(int32_t on);
+/* Move up to cap of the oldest records into out; *n_out = number moved. */
+mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out);
 
 /* ------------------------------------------------------------ test hooks */
 

@@ -82,6 +82,21 @@ class mma_stats_t(ctypes.Structure):
         return d
 
 
+class mma_trace_rec_t(ctypes.Structure):
+    _fields_ = [("seq", ctypes.c_uint64), ("dir", ctypes.c_int32), ("kind", ctypes.c_int32),
+                ("bytes", ctypes.c_uint64), ("tasks", ctypes.c_uint64),
+                ("t_api_ns", ctypes.c_uint64), ("t_submit_ns", ctypes.c_uint64), ("t_started_ns", ctypes.c_uint64),
+                ("t_first_sdma_ns", ctypes.c_uint64), ("t_last_task_ns", ctypes.c_uint64),
+                ("t_complete_ns", ctypes.c_uint64), ("t_retire_ns", ctypes.c_uint64),
+                ("path_tasks", ctypes.c_uint64 * MMA_NUM_PATHS), ("failed", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+    def as_dict(self):
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k not in ("reserved", "path_tasks")}
+        d["path_tasks"] = list(self.path_tasks)
+        return d
+
+
 class mma_plan_entry_t(ctypes.Structure):
     _fields_ = [("item", ctypes.c_uint64), ("offset", ctypes.c_uint64), ("bytes", ctypes.c_uint64),
                 ("flags", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
@@ -118,6 +133,8 @@ _SIGNATURES = {
                        ctypes.POINTER(_U64)], _S),
     "mma_plan_kv": ([_U64, _U32, _U64, _U64, ctypes.POINTER(mma_plan_entry_t), _U64, ctypes.POINTER(_U64)], _S),
     "mma_validate_kv_tables": ([ctypes.POINTER(_I32), _U32, ctypes.POINTER(_I32), _U32, _U64], _S),
+    "mma_trace_enable": ([_I32], _S),
+    "mma_trace_read": ([ctypes.POINTER(mma_trace_rec_t), _U64, ctypes.POINTER(_U64)], _S),
     "mma_test_set_fault": ([_I32, _U64], _S),
 }
 
@@ -302,6 +319,17 @@ def mma_last_error() -> str:
 
 def mma_clear_error() -> None:
     _check(lib.mma_clear_error(), "mma_clear_error")
+
+
+def mma_trace_enable(on: bool = True) -> None:
+    _check(lib.mma_trace_enable(1 if on else 0), "mma_trace_enable")
+
+
+def mma_trace_read(cap: int = 65536) -> List[dict]:
+    buf = (mma_trace_rec_t * cap)()
+    n = _U64()
+    _check(lib.mma_trace_read(buf, cap, ctypes.byref(n)), "mma_trace_read")
+    return [buf[i].as_dict() for i in range(n.value)]
 
 
 def mma_test_set_fault(kind: int, value: int) -> None:

@@ -15,6 +15,11 @@
 //      of Section 4), with a bounded, progress-re-armed watchdog, then exits
 //      and releases downstream stream work.
 //
+// Every host-memory poll is a PCIe read that competes with the payload for the
+// link, so polls are few: one load instruction both checks and fetches a ring
+// entry, an idle wave backs off exponentially, and the close/heartbeat words
+// are read only every few polls.
+//
 // mma_digest_kernel is the dependent HBM-bound check kernel of the
 // mixed-contention workload.
 #include <hip/hip_runtime.h>
@@ -24,67 +29,96 @@
 namespace mma {
 namespace {
 
-constexpr int kUnroll = 16;  // 16 x 16 B loads in flight per lane (wave_copy spells them out)
-
 // Global-address-space views: global_load/global_store instead of flat ones
-// (no LDS counter waits on the copy path).
+// (no LDS-counter waits on the copy path).
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) u32x4 gu4;
 
 __device__ __forceinline__ uint64_t ld_sys(const uint64_t* p) {
   return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
-__device__ __forceinline__ uint32_t ld_sys32(const uint32_t* p) {
-  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-}
 __device__ __forceinline__ void st_sys(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
-// Wave-cooperative copy of n bytes. Consecutive lanes move consecutive 16-byte
-// units, so each load instruction covers one contiguous 1 KiB span; a lane keeps
-// kUnroll loads in flight before storing. Byte head/tail handle any alignment
-// when src and dst are equally aligned modulo 16; otherwise a byte loop is used.
-__device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
-                                          uint64_t n, uint32_t lane) {
-  if (((reinterpret_cast<uintptr_t>(src) ^ reinterpret_cast<uintptr_t>(dst)) & 15u) == 0) {
-    uint64_t head = (16u - (reinterpret_cast<uintptr_t>(src) & 15u)) & 15u;
-    if (head > n) head = n;
-    if (lane < head) dst[lane] = src[lane];
-    src += head;
-    dst += head;
-    n -= head;
-    const uint64_t n16 = n >> 4;
-    const gu4* s = (const gu4*)(src);  // generic -> global address space
-    gu4* d = (gu4*)(dst);
-    uint64_t i = lane;
-    for (; i + (kUnroll - 1) * kWave < n16; i += kUnroll * kWave) {
-#define MMA_LD(k) const u32x4 v##k = s[i + (k) * kWave];
-#define MMA_ST(k) d[i + (k) * kWave] = v##k;
-      MMA_LD(0) MMA_LD(1) MMA_LD(2) MMA_LD(3) MMA_LD(4) MMA_LD(5) MMA_LD(6) MMA_LD(7)
-      MMA_LD(8) MMA_LD(9) MMA_LD(10) MMA_LD(11) MMA_LD(12) MMA_LD(13) MMA_LD(14) MMA_LD(15)
-      // Keep every load of the batch in flight before the first store: the
-      // scheduler would otherwise pair each load with its store and expose the
-      // full PCIe latency once per 16 bytes.
-      __builtin_amdgcn_sched_barrier(0);
-      MMA_ST(0) MMA_ST(1) MMA_ST(2) MMA_ST(3) MMA_ST(4) MMA_ST(5) MMA_ST(6) MMA_ST(7)
-      MMA_ST(8) MMA_ST(9) MMA_ST(10) MMA_ST(11) MMA_ST(12) MMA_ST(13) MMA_ST(14) MMA_ST(15)
-#undef MMA_LD
-#undef MMA_ST
-    }
-    for (; i < n16; i += kWave) d[i] = s[i];
-    const uint64_t tail = n & 15u;
-    const uint64_t base = n16 << 4;
-    if (lane < tail) dst[base + lane] = src[base + lane];
-  } else {
-    for (uint64_t i = lane; i < n; i += kWave) dst[i] = src[i];
-  }
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(v), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(v >> 32), lane);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t bcast(uint64_t v) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
-  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
-  return (static_cast<uint64_t>(hi) << 32) | lo;
+__device__ __forceinline__ void backoff(uint32_t n) {
+  for (uint32_t k = 0; k < n; ++k) __builtin_amdgcn_s_sleep(8);  // ~512 cycles each
+}
+
+// One batch = 16 loads of 16 B per lane = 16 KiB per wave.
+constexpr uint64_t kBatch = 16 * kWave;  // in 16-byte units
+
+#define MMA_LOAD16(V, base)                                                                                \
+  V##0 = s[(base) + 0 * kWave]; V##1 = s[(base) + 1 * kWave]; V##2 = s[(base) + 2 * kWave];                \
+  V##3 = s[(base) + 3 * kWave]; V##4 = s[(base) + 4 * kWave]; V##5 = s[(base) + 5 * kWave];                \
+  V##6 = s[(base) + 6 * kWave]; V##7 = s[(base) + 7 * kWave]; V##8 = s[(base) + 8 * kWave];                \
+  V##9 = s[(base) + 9 * kWave]; V##10 = s[(base) + 10 * kWave]; V##11 = s[(base) + 11 * kWave];            \
+  V##12 = s[(base) + 12 * kWave]; V##13 = s[(base) + 13 * kWave]; V##14 = s[(base) + 14 * kWave];          \
+  V##15 = s[(base) + 15 * kWave];
+#define MMA_STORE16(V, base)                                                                               \
+  d[(base) + 0 * kWave] = V##0; d[(base) + 1 * kWave] = V##1; d[(base) + 2 * kWave] = V##2;                \
+  d[(base) + 3 * kWave] = V##3; d[(base) + 4 * kWave] = V##4; d[(base) + 5 * kWave] = V##5;                \
+  d[(base) + 6 * kWave] = V##6; d[(base) + 7 * kWave] = V##7; d[(base) + 8 * kWave] = V##8;                \
+  d[(base) + 9 * kWave] = V##9; d[(base) + 10 * kWave] = V##10; d[(base) + 11 * kWave] = V##11;            \
+  d[(base) + 12 * kWave] = V##12; d[(base) + 13 * kWave] = V##13; d[(base) + 14 * kWave] = V##14;          \
+  d[(base) + 15 * kWave] = V##15;
+
+// Wave-cooperative copy of n bytes. Consecutive lanes move consecutive 16-byte
+// units, so each load instruction covers one contiguous 1 KiB span. Two register
+// batches ping-pong: the loads of the next batch are issued before the current
+// batch is stored, so a wave keeps up to 32 KiB of reads in flight. Byte
+// head/tail handle any alignment when src and dst are equally aligned modulo
+// 16; otherwise a byte loop is used.
+__device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                          uint64_t n, uint32_t lane) {
+  if (((reinterpret_cast<uintptr_t>(src) ^ reinterpret_cast<uintptr_t>(dst)) & 15u) != 0) {
+    for (uint64_t i = lane; i < n; i += kWave) dst[i] = src[i];
+    return;
+  }
+  uint64_t head = (16u - (reinterpret_cast<uintptr_t>(src) & 15u)) & 15u;
+  if (head > n) head = n;
+  if (lane < head) dst[lane] = src[lane];
+  src += head;
+  dst += head;
+  n -= head;
+  const uint64_t n16 = n >> 4;
+  const gu4* s = (const gu4*)(src) + lane;  // generic -> global address space, this lane's unit
+  gu4* d = (gu4*)(dst) + lane;
+  const uint64_t nb = n16 / kBatch;         // full batches (wave-uniform)
+  if (nb > 0) {
+    u32x4 a0, a1, a2, a3, a4, a5, a6, a7, a8, a9, a10, a11, a12, a13, a14, a15;
+    u32x4 b0, b1, b2, b3, b4, b5, b6, b7, b8, b9, b10, b11, b12, b13, b14, b15;
+    MMA_LOAD16(a, 0)
+    uint64_t k = 0;  // batch held in registers `a` at the top of the loop
+    for (;;) {
+      if (k + 1 >= nb) {
+        MMA_STORE16(a, k * kBatch)
+        break;
+      }
+      MMA_LOAD16(b, (k + 1) * kBatch)
+      __builtin_amdgcn_sched_barrier(0);
+      MMA_STORE16(a, k * kBatch)
+      ++k;
+      if (k + 1 >= nb) {
+        MMA_STORE16(b, k * kBatch)
+        break;
+      }
+      MMA_LOAD16(a, (k + 1) * kBatch)
+      __builtin_amdgcn_sched_barrier(0);
+      MMA_STORE16(b, k * kBatch)
+      ++k;
+    }
+  }
+  for (uint64_t u = nb * kBatch; u + lane < n16; u += kWave) d[u] = s[u];
+  const uint64_t tail = n & 15u;
+  const uint64_t base = n16 << 4;
+  if (lane < tail) dst[base + lane] = src[base + lane];
 }
 
 }  // namespace
@@ -95,100 +129,97 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
   DevState* ds = a.ds;
   const uint32_t lane = threadIdx.x & (kWave - 1);
 
-  // KV geometry: one PCIe read per workgroup, then served from LDS.
-  uint32_t nl = ld_sys32(&rec->h.kv_layers);
-  if (nl > kMaxLayers) nl = kMaxLayers;
-  for (uint32_t i = threadIdx.x; i < nl; i += kBlock) s_layer[i] = ld_sys(&rec->h.layer_ptr[i]);
-  const uint64_t piece = ld_sys(&rec->h.kv_piece_bytes);
-  const uint64_t kstride = ld_sys(&rec->h.kv_kstride);
+  // KV layer table from the kernel arguments into LDS.
+  const uint32_t nl = a.kv_layers < kMaxLayers ? a.kv_layers : kMaxLayers;
+  for (uint32_t i = threadIdx.x; i < nl; i += kBlock) s_layer[i] = a.layer_ptr[i];
+  const uint64_t piece = a.kv_piece_bytes;
+  const uint64_t kstride = a.kv_kstride;
   __syncthreads();
-  // Writes that precede the transfer in stream order, and host data, are visible.
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
 
-  // 1. start signal (stream -> engine).
+  // 1. start signal (stream -> engine). Work that precedes this kernel in
+  // stream order is complete and visible (dispatch acquire/release).
   if (lane == 0) {
     const uint32_t first = __hip_atomic_fetch_add(&ds->arrived, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (first == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
-      st_sys(&rec->h.started, a.seq);
-    }
+    if (first == 0) st_sys(&rec->h.started, a.seq);
   }
 
-  // 2. CU-path worker loop. Lane 0 claims and polls; the wave copies.
+  // 2. CU-path worker loop. Lane 0 claims; lanes 0..4 fetch the entry with one
+  // load instruction; the wave copies.
   uint64_t hb = 0, t_prog = 0;
   uint32_t timed_out = 0;
-  if (lane == 0) {
-    hb = ld_sys(&rec->h.heartbeat);
-    t_prog = wall_clock64();
-  }
+  if (lane == 0) t_prog = wall_clock64();
   for (;;) {
-    uint64_t ea = 0, eb = 0, ck = 0, x = 0;
-    uint32_t state = 0;  // 1: entry ready, 2: no more entries, 3: watchdog
-    if (lane == 0) {
+    uint64_t x = 0;
+    if (lane == 0)
       x = __hip_atomic_fetch_add(&ds->cursor, static_cast<uint64_t>(1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const CuEntry* e = &rec->ring[x % kRingSize];
-      const uint64_t expect = make_tag(a.seq, x);
-      for (;;) {
-        if (ld_sys(&e->tag) == expect) {
-          state = 1;
-          break;
-        }
-        if (ld_sys(&rec->h.closed) == a.seq && x >= ld_sys(&rec->h.cu_total)) {
-          state = 2;
-          break;
-        }
-        const uint64_t now = wall_clock64();
-        const uint64_t hb2 = ld_sys(&rec->h.heartbeat);
-        if (hb2 != hb) {
-          hb = hb2;
-          t_prog = now;
-        } else if (now - t_prog > a.watchdog_ticks ||
-                   __hip_atomic_load(&ds->timed_out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
-          state = 3;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(4);
+    x = lane_u64(x, 0);
+    const uint64_t expect = make_tag(a.seq, x);
+    const uint64_t* ew = reinterpret_cast<const uint64_t*>(&rec->ring[x % kRingSize]);
+    uint32_t state = 0;  // 1: entry ready, 3: watchdog
+    uint64_t w1 = 0, w2 = 0, w3 = 0;
+    for (uint32_t polls = 0;; ++polls) {
+      const uint64_t w = lane < 5 ? ld_sys(ew + lane) : 0;
+      if (lane_u64(w, 0) == expect && lane_u64(w, 4) == expect) {
+        w1 = lane_u64(w, 1);
+        w2 = lane_u64(w, 2);
+        w3 = lane_u64(w, 3);
+        state = 1;
+        break;
       }
-      if (state == 1) {
-        ea = ld_sys(&e->a);
-        eb = ld_sys(&e->b);
-        ck = ld_sys(reinterpret_cast<const uint64_t*>(&e->count));
+      if ((polls & 7) == 7) {  // watchdog check every 8th poll
+        uint32_t st = 0;
+        if (lane == 0) {
+          const uint64_t now = wall_clock64();
+          const uint64_t hb2 = ld_sys(&rec->h.heartbeat);
+          if (hb2 != hb) {
+            hb = hb2;
+            t_prog = now;
+          } else if (now - t_prog > a.watchdog_ticks ||
+                     __hip_atomic_load(&ds->timed_out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+            st = 3;
+          }
+        }
+        st = __builtin_amdgcn_readfirstlane(st);
+        if (st) {
+          state = st;
+          break;
+        }
       }
+      backoff(polls < 4 ? 1u : (polls < 16 ? 4u : 8u));
     }
-    state = static_cast<uint32_t>(bcast(state));
     if (state != 1) {
       if (state == 3) timed_out = 1;
       break;
     }
-    x = bcast(x);
-    ea = bcast(ea);
-    eb = bcast(eb);
-    ck = bcast(ck);
-    const uint32_t count = static_cast<uint32_t>(ck);
-    const uint32_t kind = static_cast<uint32_t>(ck >> 32) & kEntryKindMask;
-    const uint32_t p0 = static_cast<uint32_t>(ck >> 40);
+    const uint32_t count = static_cast<uint32_t>(w3);
+    const uint32_t kind = static_cast<uint32_t>(w3 >> 32) & kEntryKindMask;
+    if (kind == kEntryEnd) break;  // the ring is closed and this ticket is past its end
+    const uint32_t p0 = static_cast<uint32_t>(w3 >> 40);
     // Data landed by an SDMA engine during this kernel: drop any stale copy of
     // it from this CU's vector L1 (and non-coherent L2 lines) before reading.
-    if ((ck >> 32) & kEntryAcquire) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+    if ((w3 >> 32) & kEntryAcquire) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
 
-    if (kind == kEntryCopy) {
-      wave_copy(reinterpret_cast<const uint8_t*>(ea), reinterpret_cast<uint8_t*>(eb), count, lane);
-    } else if (kind == kEntryToPaged) {
-      for (uint32_t j = 0; j < count; ++j) {
+    // One copy site for every kind (a linear entry is a single "piece"), so the
+    // copy loop is instantiated once.
+    const bool paged = kind != kEntryCopy;
+    const uint32_t npieces = paged ? count : 1u;
+    for (uint32_t j = 0; j < npieces; ++j) {
+      const uint8_t* src = reinterpret_cast<const uint8_t*>(w1);
+      uint8_t* dst = reinterpret_cast<uint8_t*>(w2);
+      uint64_t n = count;
+      if (paged) {
         const uint32_t p = p0 + j;
-        uint8_t* dst = reinterpret_cast<uint8_t*>(s_layer[p >> 1]) + (p & 1u) * kstride + eb * piece;
-        wave_copy(reinterpret_cast<const uint8_t*>(ea) + j * piece, dst, piece, lane);
+        uint8_t* pg = reinterpret_cast<uint8_t*>(s_layer[p >> 1]) + (p & 1u) * kstride + w2 * piece;
+        uint8_t* contig = reinterpret_cast<uint8_t*>(w1) + j * piece;
+        src = kind == kEntryToPaged ? contig : pg;
+        dst = kind == kEntryToPaged ? pg : contig;
+        n = piece;
       }
-    } else if (kind == kEntryFromPaged) {
-      for (uint32_t j = 0; j < count; ++j) {
-        const uint32_t p = p0 + j;
-        const uint8_t* src = reinterpret_cast<const uint8_t*>(s_layer[p >> 1]) + (p & 1u) * kstride + eb * piece;
-        wave_copy(src, reinterpret_cast<uint8_t*>(ea) + j * piece, piece, lane);
-      }
+      wave_copy(src, dst, n, lane);
     }
     if (a.release_each) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
     if (lane == 0) {
-      st_sys(&rec->done[x % kRingSize], make_tag(a.seq, x));
+      st_sys(&rec->done[x % kRingSize], expect);
       t_prog = wall_clock64();
     }
   }
@@ -254,8 +285,7 @@ __global__ __launch_bounds__(256) void mma_digest_kernel(const uint32_t* __restr
 }
 
 hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t stream) {
-  KernelArgs a = args;
-  void* params[] = {&a};
+  void* params[] = {const_cast<KernelArgs*>(&args)};
   return hipLaunchKernel(reinterpret_cast<const void*>(&mma_transfer_kernel), dim3(grid), dim3(kBlock), params, 0,
                          stream);
 }

@@ -20,8 +20,9 @@
 
 namespace mma {
 
-constexpr uint32_t kRingSize = 1024;   // CU ring entries per record
-constexpr uint32_t kRecords = 128;     // records per direction (transfers in flight)
+constexpr uint32_t kRingSize = 4096;   // CU ring entries per record
+constexpr uint32_t kRecords = 64;      // records per direction (transfers in flight)
+constexpr uint32_t kMaxWorkgroups = 256;  // dummy-task kernel size limit (ring keeps one slot per wave)
 constexpr uint32_t kMaxLayers = 256;   // KV layer pointers per record
 constexpr uint32_t kWave = 64;
 constexpr uint32_t kWavesPerWG = 4;
@@ -32,18 +33,25 @@ enum : uint32_t {
   kEntryCopy = 1,       // a -> b, `count` bytes
   kEntryToPaged = 2,    // contiguous pieces at a -> GPU layers, block b, pieces p0 .. p0+count
   kEntryFromPaged = 3,  // GPU layers, block b, pieces p0 .. p0+count -> contiguous at a
+  kEntryEnd = 4,        // no more work: the wave holding this ticket leaves
   kEntryKindMask = 0x7F,
   // Flag: the source was written by a copy engine while the kernel runs (SDMA
   // staging); the wave must acquire (invalidate its caches) before reading it.
   kEntryAcquire = 0x80,
 };
 
-struct CuEntry {      // 32 bytes; `tag` is stored last, with release semantics
+// One cache line. The engine writes the payload, then tag0 and tag1; a wave
+// reads words 0..4 with a single load instruction and accepts the entry only
+// if both tags carry the expected ticket, so one PCIe read both polls for the
+// entry and delivers it.
+struct alignas(64) CuEntry {
+  uint64_t tag0;
   uint64_t a;
   uint64_t b;
   uint32_t count;
   uint32_t kind_p0;
-  uint64_t tag;
+  uint64_t tag1;
+  uint64_t pad[3];
 };
 
 struct alignas(64) RecordHdr {
@@ -62,13 +70,6 @@ struct alignas(64) RecordHdr {
   int32_t status;        // 0 ok, 1 watchdog expired
   int32_t pad2a;
   uint64_t pad2[6];
-  // cache line 3: KV geometry (host -> GPU, written before launch)
-  uint64_t kv_piece_bytes;
-  uint64_t kv_kstride;   // bytes between K and V halves of a GPU layer tensor
-  uint32_t kv_layers;
-  uint32_t pad3a;
-  uint64_t pad3[5];
-  uint64_t layer_ptr[kMaxLayers];
 };
 
 struct Record {
@@ -94,6 +95,12 @@ struct KernelArgs {
   uint64_t watchdog_ticks;  // wall-clock ticks without progress before giving up
   uint32_t total_waves;
   uint32_t release_each;    // 1: system-scope release before each done flag
+  // KV geometry (unused by linear transfers)
+  uint64_t kv_piece_bytes;
+  uint64_t kv_kstride;      // bytes between the K and V halves of a GPU layer tensor
+  uint32_t kv_layers;
+  uint32_t pad;
+  uint64_t layer_ptr[kMaxLayers];
 };
 
 // constexpr: usable from host and device code alike.

@@ -112,6 +112,7 @@ struct Transfer {
   bool sdma_ok = true;         // SDMA may carry this transfer's tasks
   // CU ring bookkeeping
   uint64_t pushed = 0, done_upto = 0;
+  uint32_t waves = 0;          // waves of the dummy-task kernel
   int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
   uint8_t tdone[kRingSize];
   uint32_t cu_busy = 0;
@@ -119,6 +120,10 @@ struct Transfer {
   int sdma_cu_pending = 0;     // SDMA slots that will still append ring entries
   int sdma_refs = 0;           // SDMA slots referencing this transfer
   uint64_t heartbeat = 0;
+  uint64_t bytes = 0;          // payload bytes
+  // trace timestamps (CLOCK_MONOTONIC ns)
+  uint64_t t_api = 0, t_submit = 0, t_started = 0, t_first_sdma = 0, t_last_task = 0, t_complete = 0;
+  uint64_t path_tasks[MMA_NUM_PATHS] = {};
   bool started = false, closed = false, completed = false, failed = false, ignored = false, aborting = false;
   bool progress = false;
 };
@@ -173,6 +178,12 @@ struct Stats {
 };
 
 std::atomic<int> g_sticky{0};
+
+// Per-transfer trace records (MMA_TRACE=1 or mma_trace_enable): a bounded ring.
+std::atomic<int> g_trace{0};
+std::mutex g_trace_mu;
+std::deque<mma_trace_rec_t> g_trace_buf;
+constexpr size_t kTraceCap = 65536;
 std::atomic<uint64_t> g_fault_stall_us{0}, g_fault_submit_fail{0}, g_fault_ignore{0};
 
 class Engine {
@@ -221,6 +232,7 @@ class Engine {
       std::lock_guard<std::mutex> g(mu_);
       if (!thread_.joinable()) return;
       stop_ = true;
+      stop_flag_ = true;
     }
     cv_.notify_all();
     thread_.join();
@@ -272,6 +284,7 @@ class Engine {
       incoming_.push_back(std::move(x));
       ++inflight_;
     }
+    n_incoming_.fetch_add(1, std::memory_order_release);
     cv_.notify_all();
   }
 
@@ -294,7 +307,8 @@ class Engine {
       per = std::max<uint64_t>(1, cfg_.sub / x->piece);
     }
     ne = (count + per - 1) / per;
-    if (x->pushed + ne - x->done_upto > kRingSize) return 0;
+    // Keep one slot per wave free for the end markers written at close.
+    if (x->pushed + ne - x->done_upto > kRingSize - x->waves) return 0;
     Record* r = x->rec;
     for (uint64_t k = 0; k < ne; ++k) {
       const uint64_t t = x->pushed++;
@@ -313,13 +327,19 @@ class Engine {
       e->count = static_cast<uint32_t>(c);
       x->owner[slot] = owner;
       x->tdone[slot] = 0;
-      st_rel(&e->tag, make_tag(x->seq, t));
+      // Payload first, then both tags: a reader that sees either tag also sees
+      // the payload written before it (x86 stores are ordered).
+      const uint64_t tag = make_tag(x->seq, t);
+      st_rel(&e->tag0, tag);
+      st_rel(&e->tag1, tag);
     }
     return static_cast<uint32_t>(ne);
   }
 
   void task_done(Transfer* x, size_t i, int path_stat) {
     ++x->n_done;
+    ++x->path_tasks[path_stat];
+    if (x->n_done == x->tasks.size()) x->t_last_task = now_ns();
     const Task& t = x->tasks[i];
     const uint64_t bytes = x->kind == Kind::kLinear ? t.bytes : t.bytes * x->piece;
     st_->path_bytes[path_stat] += bytes;
@@ -390,6 +410,7 @@ class Engine {
     while (f > 0) {
       if (g_fault_submit_fail.compare_exchange_weak(f, f - 1)) return false;
     }
+    if (!s.x->t_first_sdma) s.x->t_first_sdma = now_ns();
     hsa_signal_store_screlease(s.sig, 1);
     const hsa_status_t r = hsa_amd_memory_async_copy_on_engine(
         dst, dst_agent, src, src_agent, bytes, 0, nullptr, s.sig,
@@ -574,6 +595,7 @@ class Engine {
         x->ignored = true;
       } else {
         x->started = true;
+        x->t_started = now_ns();
         const uint64_t us = g_fault_stall_us.load();
         if (us) std::this_thread::sleep_for(std::chrono::microseconds(us));
       }
@@ -591,6 +613,7 @@ class Engine {
     if (!x->closed && (x->n_claimed == x->tasks.size() || x->failed) && x->sdma_cu_pending == 0) {
       st_rel(&r->h.cu_total, x->pushed);
       st_rel(&r->h.closed, x->seq);
+      close_ring(x);
       x->closed = true;
       p = true;
     }
@@ -599,10 +622,50 @@ class Engine {
     const bool drained = x->failed && x->closed && x->sdma_refs == 0 && x->cu_busy == 0;
     if (!x->completed && (x->n_done == x->tasks.size() || drained)) {
       st_rel(&r->h.complete, x->seq);
+      x->t_complete = now_ns();
       x->completed = true;
       p = true;
     }
     return p;
+  }
+
+  void record_trace(const Transfer* x, bool bad) {
+    mma_trace_rec_t t{};
+    t.seq = x->seq;
+    t.dir = x->dir;
+    t.kind = static_cast<int32_t>(x->kind);
+    t.bytes = x->bytes;
+    t.tasks = x->tasks.size();
+    t.t_api_ns = x->t_api;
+    t.t_submit_ns = x->t_submit;
+    t.t_started_ns = x->t_started;
+    t.t_first_sdma_ns = x->t_first_sdma;
+    t.t_last_task_ns = x->t_last_task;
+    t.t_complete_ns = x->t_complete;
+    t.t_retire_ns = now_ns();
+    for (int i = 0; i < MMA_NUM_PATHS; ++i) t.path_tasks[i] = x->path_tasks[i];
+    t.failed = bad ? 1 : 0;
+    std::lock_guard<std::mutex> g(g_trace_mu);
+    if (g_trace_buf.size() >= kTraceCap) g_trace_buf.pop_front();
+    g_trace_buf.push_back(t);
+  }
+
+  // Every wave holds at most one claim beyond the last real ticket, so the
+  // tickets [pushed, pushed + waves) cover all of them: an end marker in each
+  // lets every waiting wave leave on its next poll. The slots are free because
+  // push_unit keeps `waves` slots in reserve.
+  void close_ring(Transfer* x) {
+    Record* r = x->rec;
+    for (uint64_t t = x->pushed; t < x->pushed + x->waves; ++t) {
+      CuEntry* e = &r->ring[t % kRingSize];
+      e->a = 0;
+      e->b = 0;
+      e->count = 0;
+      e->kind_p0 = kEntryEnd;
+      const uint64_t tag = make_tag(x->seq, t);
+      st_rel(&e->tag0, tag);
+      st_rel(&e->tag1, tag);
+    }
   }
 
   bool retire_ready(Transfer* x) {
@@ -613,19 +676,29 @@ class Engine {
   void loop() {
     uint64_t idle_spins = 0, busy_t0 = 0;
     for (;;) {
-      {
+      if (active_.empty()) {
+        if (busy_t0) {
+          st_->busy_ns += now_ns() - busy_t0;
+          busy_t0 = 0;
+        }
+        // Back-to-back transfers are common: poll for a while before sleeping,
+        // so that a new transfer does not pay a thread wake-up.
+        const uint64_t t0 = now_ns();
+        while (n_incoming_.load(std::memory_order_acquire) == 0 && !stop_flag_.load(std::memory_order_relaxed) &&
+               now_ns() - t0 < kIdleSpinNs)
+          cpu_relax();
         std::unique_lock<std::mutex> lk(mu_);
-        while (incoming_.empty() && active_.empty()) {
-          if (busy_t0) {
-            st_->busy_ns += now_ns() - busy_t0;
-            busy_t0 = 0;
-          }
+        while (incoming_.empty()) {
           if (stop_) return;
           cv_.wait_for(lk, std::chrono::milliseconds(100));
         }
+      }
+      if (n_incoming_.load(std::memory_order_acquire) > 0) {
+        std::lock_guard<std::mutex> g(mu_);
         while (!incoming_.empty()) {
           active_.push_back(std::move(incoming_.front()));
           incoming_.pop_front();
+          n_incoming_.fetch_sub(1, std::memory_order_relaxed);
         }
       }
       if (!busy_t0) busy_t0 = now_ns();
@@ -655,6 +728,7 @@ class Engine {
           st_->failed += 1;
         }
         st_->transfers += 1;
+        if (g_trace.load(std::memory_order_relaxed)) record_trace(x, bad);
         {
           std::lock_guard<std::mutex> g(mu_);
           free_recs_.push_back(x->rec_idx);
@@ -692,6 +766,9 @@ class Engine {
   std::deque<uint32_t> free_recs_;
   uint64_t inflight_ = 0;
   bool stop_ = false;
+  std::atomic<bool> stop_flag_{false};
+  std::atomic<uint64_t> n_incoming_{0};
+  static constexpr uint64_t kIdleSpinNs = 2000000;  // 2 ms
   std::thread thread_;
 };
 
@@ -838,17 +915,29 @@ mma_status_t device_range(const void* p, uint64_t bytes) {
   return MMA_OK;
 }
 
-uint32_t grid_for(const Runtime* rt, Engine* e, uint64_t bytes, bool needs_cu) {
+// Workgroups of the dummy-task kernel: one wave per ring entry that can be
+// outstanding at once (waves beyond that would only poll host memory, and
+// every poll is a PCIe read that competes with the payload).
+uint32_t grid_for(const Runtime* rt, Engine* e, uint64_t bytes, bool needs_cu, bool staged) {
   if (!needs_cu) return 1;
-  const uint64_t entries = (bytes + rt->cfg.sub - 1) / rt->cfg.sub;
-  uint64_t g = (entries + kWavesPerWG - 1) / kWavesPerWG;
-  if (!e->cu_enabled()) g = std::min<uint64_t>(g, 4);
-  g = std::max<uint64_t>(1, std::min<uint64_t>(g, rt->cfg.cu_wgs));
+  const Config& c = rt->cfg;
+  const uint64_t total = (bytes + c.sub - 1) / c.sub;
+  const uint64_t per_task = (c.chunk + c.sub - 1) / c.sub;
+  uint64_t inflight = e->cu_enabled() ? c.cu_depth * per_task : 0;
+  if (staged) inflight += static_cast<uint64_t>(__builtin_popcount(e->sdma_mask())) * c.depth * per_task;
+  uint64_t g = (std::max<uint64_t>(1, std::min(total, inflight)) + kWavesPerWG - 1) / kWavesPerWG;
+  g = std::max<uint64_t>(1, std::min<uint64_t>(g, c.cu_wgs));
   return static_cast<uint32_t>(g);
 }
 
 // Hand a planned transfer to its engine and enqueue the dummy task on the stream.
-mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* stream, const RecordHdr* kv) {
+struct KvGeom {
+  uint64_t piece = 0, kstride = 0;
+  uint32_t layers = 0;
+  uint64_t layer_ptr[kMaxLayers];
+};
+
+mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* stream, const KvGeom* kv) {
   Runtime* rt = g_rt;
   Engine* e = rt->eng[x->dir].get();
   x->claimed.assign(x->tasks.size(), 0);
@@ -856,26 +945,27 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   std::lock_guard<std::mutex> g(rt->submit_mu);
   if (!e->acquire_record(x.get(), 60000)) return fail(MMA_ERR_TIMEOUT, "no free transfer record for 60 s");
   x->seq = ++rt->seq;
+  x->t_submit = now_ns();
+  x->bytes = payload_bytes;
   Record* r = x->rec;
   r->h.seq = x->seq;
   r->h.status = 0;
-  r->h.kv_layers = 0;
-  r->h.kv_piece_bytes = 0;
-  r->h.kv_kstride = 0;
-  if (kv) {
-    r->h.kv_layers = kv->kv_layers;
-    r->h.kv_piece_bytes = kv->kv_piece_bytes;
-    r->h.kv_kstride = kv->kv_kstride;
-    memcpy(r->h.layer_ptr, kv->layer_ptr, sizeof(uint64_t) * kv->kv_layers);
-  }
   __atomic_thread_fence(__ATOMIC_RELEASE);
-  e->prefill(x.get());
   const bool staged = x->kind != Kind::kLinear && e->has_sdma() && x->sdma_ok;
   const bool needs_cu = e->cu_enabled() || staged ||
                         std::any_of(x->tasks.begin(), x->tasks.end(),
                                     [](const Task& t) { return (t.flags & kPlanCuOnly) != 0; });
-  const uint32_t grid = grid_for(rt, e, payload_bytes, needs_cu);
-  KernelArgs a{};
+  const uint32_t grid = grid_for(rt, e, payload_bytes, needs_cu, staged);
+  x->waves = grid * kWavesPerWG;
+  e->prefill(x.get());
+  static thread_local KernelArgs a;
+  memset(&a, 0, offsetof(KernelArgs, layer_ptr));
+  if (kv) {
+    a.kv_piece_bytes = kv->piece;
+    a.kv_kstride = kv->kstride;
+    a.kv_layers = kv->layers;
+    memcpy(a.layer_ptr, kv->layer_ptr, sizeof(uint64_t) * kv->layers);
+  }
   a.rec = e->rec_dev(x->rec_idx);
   a.ds = e->ds(x->rec_idx);
   a.seq = x->seq;
@@ -897,8 +987,8 @@ void fill_config(mma_config_t* c, bool use_env) {
   d.chunk_bytes = 2 * MiB;
   d.small_bytes = 64 * KiB;
   d.queue_depth = 2;
-  d.cu_queue_depth = 2;
-  d.cu_workgroups = 32;
+  d.cu_queue_depth = 4;
+  d.cu_workgroups = 16;
   d.cu_sub_bytes = 64 * KiB;
   d.watchdog_ms = 20000;
   if (use_env) {
@@ -954,8 +1044,11 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
     fill_config(&c, true);
   }
   if (!c.fallback_bytes) c.fallback_bytes = 2 * c.chunk_bytes;
+  // A micro-task's ring entries must fit the ring next to the end-marker
+  // reserve of one slot per wave.
   if (c.cu_sub_bytes % 16 || c.cu_sub_bytes < 256 || c.chunk_bytes % 16 || c.queue_depth > 16 ||
-      c.cu_workgroups > 1024 || c.cu_queue_depth > 64)
+      c.cu_workgroups > kMaxWorkgroups || c.cu_queue_depth > 64 ||
+      (c.chunk_bytes + c.cu_sub_bytes - 1) / c.cu_sub_bytes > kRingSize / 2)
     return fail(MMA_ERR_INVALID_ARG, "invalid configuration");
 
   std::unique_ptr<Runtime> rt(new Runtime());
@@ -1034,6 +1127,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
     }
     set_affinity_local(rt->eng[d]->native_handle(), hip_device);
   }
+  if (env_u64("MMA_TRACE", 0)) g_trace = 1;
   g_rt = rt.release();
   return MMA_OK;
 }
@@ -1100,6 +1194,7 @@ mma_status_t mma_memcpy_async(void* dst, const void* src, uint64_t bytes, int32_
 }
 
 mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t dir, void* stream) {
+  const uint64_t t_api = now_ns();
   mma_status_t s = check_ready();
   if (s) return s;
   if (dir != MMA_H2D && dir != MMA_D2H) return fail(MMA_ERR_INVALID_ARG, "dir must be MMA_H2D or MMA_D2H");
@@ -1131,6 +1226,7 @@ mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t d
   plan_list(sizes.data(), n, rt->cfg.chunk, rt->cfg.fallback, rt->cfg.small, plan);
   std::unique_ptr<Transfer> x(new Transfer());
   x->dir = dir;
+  x->t_api = t_api;
   x->kind = Kind::kLinear;
   x->tasks.reserve(plan.size());
   for (const PlanItem& p : plan) {
@@ -1150,6 +1246,7 @@ mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t d
 static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool, const void* const* layers,
                               const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n, int dir,
                               void* stream) {
+  const uint64_t t_api = now_ns();
   mma_status_t s = check_ready();
   if (s) return s;
   if (!n) return MMA_OK;
@@ -1171,10 +1268,10 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   DeviceGuard dg(rt->dev);
   uint64_t pool_cu = 0;
   if ((s = host_range(host_pool, pool_bytes, &pool_cu))) return s;
-  RecordHdr kv{};
-  kv.kv_layers = lay->num_layers;
-  kv.kv_piece_bytes = piece;
-  kv.kv_kstride = piece * lay->gpu_num_blocks;
+  KvGeom kv;
+  kv.layers = lay->num_layers;
+  kv.piece = piece;
+  kv.kstride = piece * lay->gpu_num_blocks;
   for (uint32_t l = 0; l < lay->num_layers; ++l) {
     if (!layers[l]) return fail(MMA_ERR_INVALID_ARG, "NULL layer pointer %u", l);
     if ((s = device_range(layers[l], layer_bytes))) return s;
@@ -1184,6 +1281,7 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   plan_kv(n, ppb, piece, rt->cfg.chunk, plan);
   std::unique_ptr<Transfer> x(new Transfer());
   x->dir = dir;
+  x->t_api = t_api;
   x->kind = dir == MMA_H2D ? Kind::kKvFetch : Kind::kKvOffload;
   x->piece = piece;
   Engine* e = rt->eng[dir].get();
@@ -1286,6 +1384,23 @@ const char* mma_last_error(void) { return t_err.c_str(); }
 mma_status_t mma_clear_error(void) {
   g_sticky.store(0);
   t_err.clear();
+  return MMA_OK;
+}
+
+mma_status_t mma_trace_enable(int32_t on) {
+  std::lock_guard<std::mutex> g(g_trace_mu);
+  if (on && !g_trace.load()) g_trace_buf.clear();
+  g_trace = on ? 1 : 0;
+  return MMA_OK;
+}
+
+mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out) {
+  if (!n_out || (cap && !out)) return fail(MMA_ERR_INVALID_ARG, "NULL argument");
+  std::lock_guard<std::mutex> g(g_trace_mu);
+  const uint64_t n = std::min<uint64_t>(cap, g_trace_buf.size());
+  for (uint64_t i = 0; i < n; ++i) out[i] = g_trace_buf[i];
+  g_trace_buf.erase(g_trace_buf.begin(), g_trace_buf.begin() + static_cast<long>(n));
+  *n_out = n;
   return MMA_OK;
 }
 
