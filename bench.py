@@ -259,9 +259,9 @@ def main():
         dst = torch.empty(n, dtype=torch.uint8, device="cuda")
         srct = torch.from_numpy(src.array)  # pinned memory seen by torch as a CPU tensor
 
-        def timed(fn, reps=50):
+        def timed(fn, reps=50, warm=5):
             ts = []
-            for _ in range(5):
+            for _ in range(min(warm, reps)):
                 fn()
             stream.synchronize()
             for _ in range(reps):
@@ -289,6 +289,49 @@ def main():
         if "measured_h2d_link_GBs" in extras:
             extras["copy64"]["frac_of_measured"] = round(n / mma_ms / 1e6 / extras["measured_h2d_link_GBs"], 4)
         src.free()
+
+        # KV offload (GPU -> host): the 50%-dirty subset of the cache just fetched, 2048 blocks (4 GiB),
+        # into a permutation of host slots; against 131,072 per-piece hipMemcpyAsync D2H.
+        plan = W.kv_offload_plan(s, cfg=4)
+        src_blocks = gb[plan.dirty].astype(np.int32)
+        off_bytes = len(plan.dirty) * s.slot_bytes
+
+        def offload():
+            mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, stream)
+
+        off_ms = timed(offload, reps=5)
+        fn = nat.native_kv_offload
+        fn.restype = ctypes.c_int
+        fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                       ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rc = fn(pool.ptr, lp, src_blocks.ctypes.data_as(ctypes.c_void_p), plan.dest.ctypes.data_as(ctypes.c_void_p),
+                len(plan.dirty), s.layers, s.piece_bytes, s.gpu_num_blocks, stream.cuda_stream)
+        stream.synchronize()
+        nat_off = (time.perf_counter() - t0) * 1e3 if rc == 0 else None
+        extras["kv_offload_2048_blocks"] = {"mma_ms": round(off_ms, 3), "mma_GBs": round(off_bytes / off_ms / 1e6, 2),
+                                            "native_per_piece_ms": round(nat_off, 2) if nat_off else None,
+                                            "speedup_vs_native": round(nat_off / off_ms, 2) if nat_off else None}
+
+        # Model wake-up: 291 Llama-3-8B-shaped bf16 tensors (16.06 GB) as one list, against 291 hipMemcpyAsync.
+        sizes = W.weight_tensor_bytes()
+        offs, wtotal = W.arena_offsets(sizes, 256)
+        arena = mma.PinnedBuffer(wtotal)
+        arena.array[:] = 0x3C
+        wdst = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in sizes]
+        lst = [(wdst[t], arena.ptr + offs[t], sizes[t]) for t in range(len(sizes))]
+        w_ms = timed(lambda: mma.mma_weights_load(lst, mma.MMA_H2D, stream), reps=3)
+        D = (ctypes.c_void_p * len(sizes))(*[t.data_ptr() for t in wdst])
+        S = (ctypes.c_void_p * len(sizes))(*[arena.ptr + o for o in offs])
+        Z = (ctypes.c_uint64 * len(sizes))(*sizes)
+        nat.native_list.restype = ctypes.c_int
+        w_nat = timed(lambda: nat.native_list(D, S, Z, ctypes.c_uint64(len(sizes)), 0,
+                                              ctypes.c_void_p(stream.cuda_stream)), reps=3)
+        extras["weights_wakeup_291"] = {"mma_ms": round(w_ms, 2), "mma_GBs": round(wtotal / w_ms / 1e6, 2),
+                                        "native_ms": round(w_nat, 2), "ratio_vs_native": round(w_nat / w_ms, 3)}
+        del wdst
+        arena.free()
         log("extras:", extras)
     out["extras"] = extras
 

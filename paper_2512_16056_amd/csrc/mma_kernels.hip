@@ -157,7 +157,13 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
     const uint64_t* ew = reinterpret_cast<const uint64_t*>(&rec->ring[x % kRingSize]);
     uint32_t state = 0;  // 1: entry ready, 3: watchdog
     uint64_t w1 = 0, w2 = 0, w3 = 0;
-    for (uint32_t polls = 0;; ++polls) {
+    if (x < a.n_pre) {  // first entries arrive with the launch: no PCIe round trip
+      w1 = a.pre[x][0];
+      w2 = a.pre[x][1];
+      w3 = a.pre[x][2];
+      state = 1;
+    }
+    for (uint32_t polls = 0; state == 0; ++polls) {
       const uint64_t w = lane < 5 ? ld_sys(ew + lane) : 0;
       if (lane_u64(w, 0) == expect && lane_u64(w, 4) == expect) {
         w1 = lane_u64(w, 1);

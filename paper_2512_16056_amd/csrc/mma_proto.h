@@ -23,6 +23,7 @@ namespace mma {
 constexpr uint32_t kRingSize = 4096;   // CU ring entries per record
 constexpr uint32_t kRecords = 64;      // records per direction (transfers in flight)
 constexpr uint32_t kMaxWorkgroups = 256;  // dummy-task kernel size limit (ring keeps one slot per wave)
+constexpr uint32_t kPrefill = 48;      // ring entries also passed in the kernel arguments (linear kinds)
 constexpr uint32_t kMaxLayers = 256;   // KV layer pointers per record
 constexpr uint32_t kWave = 64;
 constexpr uint32_t kWavesPerWG = 4;
@@ -99,8 +100,9 @@ struct KernelArgs {
   uint64_t kv_piece_bytes;
   uint64_t kv_kstride;      // bytes between the K and V halves of a GPU layer tensor
   uint32_t kv_layers;
-  uint32_t pad;
+  uint32_t n_pre;           // tickets [0, n_pre) are also given below: no first poll for them
   uint64_t layer_ptr[kMaxLayers];
+  uint64_t pre[kPrefill][3];  // words a, b, count|kind_p0 of the first ring entries
 };
 
 // constexpr: usable from host and device code alike.

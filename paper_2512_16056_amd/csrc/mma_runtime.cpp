@@ -619,8 +619,14 @@ class Engine {
     }
     // Complete: every micro-task landed -- or, after a failure, everything in
     // flight has drained, so the stream can be released (the error is sticky).
+    // The kernel's last wave starts waiting only after every wave has left the
+    // ring, i.e. after every appended entry is done; so once the ring is closed,
+    // only copy-engine operations can still be outstanding, and `complete` can
+    // be published as soon as none is -- without waiting to see the last CU
+    // done flags.
     const bool drained = x->failed && x->closed && x->sdma_refs == 0 && x->cu_busy == 0;
-    if (!x->completed && (x->n_done == x->tasks.size() || drained)) {
+    const bool landed = !x->failed && x->closed && sdma_ops_in_flight(x) == 0;
+    if (!x->completed && (x->n_done == x->tasks.size() || landed || drained)) {
       st_rel(&r->h.complete, x->seq);
       x->t_complete = now_ns();
       x->completed = true;
@@ -666,6 +672,15 @@ class Engine {
       st_rel(&e->tag0, tag);
       st_rel(&e->tag1, tag);
     }
+  }
+
+  // SDMA slots of x whose remaining work includes a copy-engine operation (a
+  // slot in kH2DScatter only waits for ring entries, which the kernel finishes).
+  int sdma_ops_in_flight(const Transfer* x) const {
+    int n = 0;
+    for (const auto& s : slots_)
+      if (s.x == x && s.state != kFree && s.state != kH2DScatter) ++n;
+    return n;
   }
 
   bool retire_ready(Transfer* x) {
@@ -958,8 +973,16 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   const uint32_t grid = grid_for(rt, e, payload_bytes, needs_cu, staged);
   x->waves = grid * kWavesPerWG;
   e->prefill(x.get());
+  const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
   static thread_local KernelArgs a;
   memset(&a, 0, offsetof(KernelArgs, layer_ptr));
+  a.n_pre = n_pre;
+  for (uint32_t t = 0; t < n_pre; ++t) {
+    const CuEntry& en = r->ring[t];
+    a.pre[t][0] = en.a;
+    a.pre[t][1] = en.b;
+    a.pre[t][2] = static_cast<uint64_t>(en.count) | (static_cast<uint64_t>(en.kind_p0) << 32);
+  }
   if (kv) {
     a.kv_piece_bytes = kv->piece;
     a.kv_kstride = kv->kstride;
