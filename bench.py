@@ -314,6 +314,22 @@ def main():
                                             "native_per_piece_ms": round(nat_off, 2) if nat_off else None,
                                             "speedup_vs_native": round(nat_off / off_ms, 2) if nat_off else None}
 
+        # The same gather with the pool resident in HBM: the CU gather/scatter code alone, HBM-bound.
+        dpool = torch.empty(s.host_num_slots * s.slot_bytes, dtype=torch.uint8, device="cuda")
+        dpool.copy_(torch.from_numpy(pool.array))
+        hbm_ms = timed(lambda: mma.mma_kv_fetch(lay, dpool, layers, hs, gb, stream), reps=5)
+        ok_hbm = True
+        for _ in range(16):
+            i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
+            off = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
+            ok_hbm &= bool(np.array_equal(layers[l][off:off + s.piece_bytes].cpu().numpy(),
+                                          pool.array.reshape(s.host_num_slots, s.layers, 2, -1)[hs[i], l, k]))
+        extras["kv_gather_hbm_pool"] = {"ms": round(hbm_ms, 3), "payload_GBs": round(total / hbm_ms / 1e6, 1),
+                                        "hbm_GBs_read_plus_write": round(2 * total / hbm_ms / 1e6, 1),
+                                        "frac_of_8TBs": round(2 * total / hbm_ms / 1e6 / 8000.0, 4),
+                                        "sampled_parity": ok_hbm}
+        del dpool
+
         # Model wake-up: 291 Llama-3-8B-shaped bf16 tensors (16.06 GB) as one list, against 291 hipMemcpyAsync.
         sizes = W.weight_tensor_bytes()
         offs, wtotal = W.arena_offsets(sizes, 256)

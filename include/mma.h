@@ -208,7 +208,9 @@ mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t d
  * pages"; Section 5.2.1). For every i < n_blocks, l < num_layers, k in {K,V}:
  *   gpu_layers[l][k][gpu_blocks[i]] = host_pool[host_slots[i]][l][k]
  * Other GPU blocks are untouched. gpu_layers: num_layers device pointers, each
- * to [2][gpu_num_blocks][piece]; host_pool: pinned, host_num_slots slots.
+ * to [2][gpu_num_blocks][piece]; host_pool: host_num_slots slots of pinned host
+ * memory -- or of device memory of this GPU (an HBM-resident KV tier), in which
+ * case the transfer is an HBM gather carried by the CU path alone.
  * Tables: int32, host_slots[i] in [0, host_num_slots), gpu_blocks[i] in
  * [0, gpu_num_blocks), gpu_blocks distinct (MMA_ERR_INVALID_ARG otherwise).
  * The pointer array and both tables are copied before return. */
@@ -218,7 +220,8 @@ mma_status_t mma_kv_fetch(const mma_kv_layout_t* layout, const void* host_pool, 
 
 /* KV offload, paged GPU cache -> host pool (Section 2.1 offload). For every
  * j < n_blocks, l, k:  host_pool[host_slots[j]][l][k] = gpu_layers[l][k][gpu_blocks[j]].
- * Other host slots are untouched. host_slots distinct; ranges as for fetch.
+ * Other host slots are untouched. host_slots distinct; ranges as for fetch; the
+ * pool may likewise be device memory (HBM scatter, CU path only).
  * Producer work enqueued on `stream` before this call is complete and visible
  * before any byte is read. */
 mma_status_t mma_kv_offload(const mma_kv_layout_t* layout, void* host_pool, const void* const* gpu_layers,

@@ -113,6 +113,7 @@ struct Transfer {
   // CU ring bookkeeping
   uint64_t pushed = 0, done_upto = 0;
   uint32_t waves = 0;          // waves of the dummy-task kernel
+  bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
   int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
   uint8_t tdone[kRingSize];
   uint32_t cu_busy = 0;
@@ -304,7 +305,9 @@ class Engine {
     if ((kind & kEntryKindMask) == kEntryCopy) {
       per = cfg_.sub;
     } else {
-      per = std::max<uint64_t>(1, cfg_.sub / x->piece);
+      // A wave's ring entry carries cu_sub_bytes of pieces across PCIe; for an
+      // HBM-resident pool (latency ~1 us instead of several) a whole micro-task.
+      per = x->pool_dev ? count : std::max<uint64_t>(1, cfg_.sub / x->piece);
     }
     ne = (count + per - 1) / per;
     // Keep one slot per wave free for the end markers written at close.
@@ -376,11 +379,13 @@ class Engine {
   // ---------------------------------------------------------------- CU path
   bool pull_cu(Transfer* x) {
     if (x->failed || x->ignored || x->aborting) return false;
-    const bool any = cu_enabled();
+    const bool any = cu_enabled() || x->pool_dev;
+    // An HBM-resident pool keeps every wave busy: two micro-tasks per wave outstanding.
+    const uint32_t depth = x->pool_dev ? 2 * x->waves : cfg_.cu_depth;
     bool p = false;
     while (true) {
-      if (x->cu_busy >= cfg_.cu_depth) x->cu_full = true;
-      if (x->cu_full && x->cu_busy < std::min(cfg_.backoff, cfg_.cu_depth)) x->cu_full = false;
+      if (x->cu_busy >= depth) x->cu_full = true;
+      if (x->cu_full && x->cu_busy < std::min(cfg_.backoff, depth)) x->cu_full = false;
       if (x->cu_full) break;
       size_t i = x->cur_cu;
       while (i < x->tasks.size() && (x->claimed[i] || (!any && !(x->tasks[i].flags & kPlanCuOnly)))) ++i;
@@ -933,8 +938,12 @@ mma_status_t device_range(const void* p, uint64_t bytes) {
 // Workgroups of the dummy-task kernel: one wave per ring entry that can be
 // outstanding at once (waves beyond that would only poll host memory, and
 // every poll is a PCIe read that competes with the payload).
-uint32_t grid_for(const Runtime* rt, Engine* e, uint64_t bytes, bool needs_cu, bool staged) {
+uint32_t grid_for(const Runtime* rt, Engine* e, uint64_t bytes, bool needs_cu, bool staged, bool pool_dev) {
   if (!needs_cu) return 1;
+  if (pool_dev) {  // HBM gather/scatter: as many waves as there are micro-tasks, up to the limit
+    const uint64_t tasks = (bytes + rt->cfg.chunk - 1) / rt->cfg.chunk;
+    return static_cast<uint32_t>(std::max<uint64_t>(1, std::min<uint64_t>((tasks + 3) / 4, kMaxWorkgroups)));
+  }
   const Config& c = rt->cfg;
   const uint64_t total = (bytes + c.sub - 1) / c.sub;
   const uint64_t per_task = (c.chunk + c.sub - 1) / c.sub;
@@ -970,7 +979,7 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   const bool needs_cu = e->cu_enabled() || staged ||
                         std::any_of(x->tasks.begin(), x->tasks.end(),
                                     [](const Task& t) { return (t.flags & kPlanCuOnly) != 0; });
-  const uint32_t grid = grid_for(rt, e, payload_bytes, needs_cu, staged);
+  const uint32_t grid = grid_for(rt, e, payload_bytes, needs_cu || x->pool_dev, staged, x->pool_dev);
   x->waves = grid * kWavesPerWG;
   e->prefill(x.get());
   const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
@@ -1289,8 +1298,19 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   if (!ok) return fail(MMA_ERR_INVALID_ARG, "block table entry out of range or duplicate destination");
   Runtime* rt = g_rt;
   DeviceGuard dg(rt->dev);
+  // The pool is pinned host memory, or device memory of this GPU (a KV tier
+  // in HBM): then the transfer is an HBM gather/scatter carried by the CU path.
   uint64_t pool_cu = 0;
-  if ((s = host_range(host_pool, pool_bytes, &pool_cu))) return s;
+  bool pool_dev = false;
+  if ((s = host_range(host_pool, pool_bytes, &pool_cu))) {
+    const std::string host_err = t_err;
+    if (s != MMA_ERR_INVALID_ARG || device_range(host_pool, pool_bytes) != MMA_OK) {
+      t_err = host_err;
+      return s;
+    }
+    pool_dev = true;
+    pool_cu = reinterpret_cast<uint64_t>(host_pool);
+  }
   KvGeom kv;
   kv.layers = lay->num_layers;
   kv.piece = piece;
@@ -1309,7 +1329,8 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   x->piece = piece;
   Engine* e = rt->eng[dir].get();
   const uint64_t per_task = std::max<uint64_t>(rt->cfg.chunk / piece, 1) * piece;
-  x->sdma_ok = per_task <= e->stage_bytes();
+  x->pool_dev = pool_dev;
+  x->sdma_ok = per_task <= e->stage_bytes() && !pool_dev;
   x->tasks.reserve(plan.size());
   const uint64_t host = reinterpret_cast<uint64_t>(host_pool);
   for (const PlanItem& p : plan) {

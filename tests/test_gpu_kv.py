@@ -134,6 +134,36 @@ def test_kv_all_permutations(paths):
         mma.mma_synchronize()
 
 
+@pytest.mark.parametrize("shape", ["small", "ragged", "medium"])
+def test_kv_device_pool(shape):
+    """A pool in device memory: the same gather/scatter runs HBM -> HBM on the CU path."""
+    s = SHAPES[shape]
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    plan = W.kv_offload_plan(s, cfg=4)
+    with session("both", chunk_bytes=4096):
+        r = np.random.default_rng(9)
+        pool_np = r.integers(0, 256, s.host_num_slots * s.slot_bytes, dtype=np.uint8)
+        pool = torch.from_numpy(pool_np.copy()).cuda()
+        layers = _layers(s, W.GPU_POISON)
+        before = _layer_views(s, layers)
+        mma.mma_kv_fetch(layout_of(s), pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        pv = pool_np.reshape(s.host_num_slots, s.slot_bytes)
+        for l in range(s.layers):
+            want = okv.kv_fetch_layer(pv, before[l], l, s.layers, hs, gb)
+            assert np.array_equal(to_host(layers[l]).reshape(want.shape), want), l
+        # offload back into the device pool
+        src = _layers(s, seed=500)
+        views = _layer_views(s, src)
+        mma.mma_kv_offload(layout_of(s), pool, src, plan.src_blocks, plan.dest)
+        torch.cuda.synchronize()
+        want = okv.kv_offload(pv, views, plan.src_blocks, plan.dest)
+        assert np.array_equal(to_host(pool).reshape(s.host_num_slots, -1), want)
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+    assert sum(st["path_bytes"][:16]) == 0 and st["failed_transfers"] == 0
+
+
 def test_kv_rejects_bad_tables():
     s = SHAPES["small"]
     with session("both"):
