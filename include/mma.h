@@ -92,7 +92,12 @@ typedef struct mma_config {
   uint32_t cu_sub_bytes;    /* bytes one wave moves per CU claim; default 64 KiB */
   uint32_t watchdog_ms;     /* wait-kernel gives up after this long without engine progress;
                                default 20000 */
-  uint32_t reserved[4];
+  uint32_t static_split;    /* 0 (default): pull-based path selection. 1: the baseline the paper
+                               compares against (Section 5.1.2) -- a fixed split decided at plan
+                               time: static_cu_percent of the micro-tasks (interleaved) go to the
+                               CU path, the rest to the SDMA engines (which share them by pulling) */
+  uint32_t static_cu_percent;
+  uint32_t reserved[2];
 } mma_config_t;
 
 typedef struct mma_copy_desc {
@@ -126,6 +131,8 @@ typedef struct mma_stats {
   uint64_t sdma_submit_failures;          /* submissions re-routed to the CU path */
   uint64_t engine_cpu_ns;                 /* CPU time consumed by the engine threads */
   uint64_t engine_wall_busy_ns;           /* wall time with at least one transfer active */
+  uint64_t sdma_foreign_busy_skips;       /* pulls skipped: engine busy with another component's copies */
+  uint64_t sdma_congestion_backoffs;      /* engines backed off after an overdue command */
   uint32_t sdma_engines_h2d;              /* masks actually in use */
   uint32_t sdma_engines_d2h;
   uint32_t cu_path_enabled;
@@ -145,6 +152,7 @@ typedef struct mma_plan_entry {
 } mma_plan_entry_t;
 
 #define MMA_TASK_CU_ONLY 1u
+#define MMA_TASK_SDMA_ONLY 2u
 
 /* ---------------------------------------------------------------- lifecycle */
 

@@ -29,6 +29,7 @@ MMA_FAULT_ENGINE_STALL_US = 1
 MMA_FAULT_SDMA_SUBMIT_FAIL = 2
 MMA_FAULT_ENGINE_IGNORE = 3
 MMA_TASK_CU_ONLY = 1
+MMA_TASK_SDMA_ONLY = 2
 
 STATUS = {
     0: "MMA_OK", -1: "MMA_ERR_NOT_INITIALIZED", -2: "MMA_ERR_INVALID_ARG", -3: "MMA_ERR_NOT_PINNED",
@@ -50,7 +51,8 @@ class mma_config_t(ctypes.Structure):
                 ("cu_queue_depth", ctypes.c_uint32), ("backoff_depth", ctypes.c_uint32),
                 ("path_mask_h2d", ctypes.c_uint32), ("path_mask_d2h", ctypes.c_uint32),
                 ("cu_workgroups", ctypes.c_uint32), ("cu_sub_bytes", ctypes.c_uint32),
-                ("watchdog_ms", ctypes.c_uint32), ("reserved", ctypes.c_uint32 * 4)]
+                ("watchdog_ms", ctypes.c_uint32), ("static_split", ctypes.c_uint32),
+                ("static_cu_percent", ctypes.c_uint32), ("reserved", ctypes.c_uint32 * 2)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
@@ -72,6 +74,7 @@ class mma_stats_t(ctypes.Structure):
                 ("path_bytes", ctypes.c_uint64 * MMA_NUM_PATHS), ("path_tasks", ctypes.c_uint64 * MMA_NUM_PATHS),
                 ("staging_bytes", ctypes.c_uint64), ("sdma_submit_failures", ctypes.c_uint64),
                 ("engine_cpu_ns", ctypes.c_uint64), ("engine_wall_busy_ns", ctypes.c_uint64),
+                ("sdma_foreign_busy_skips", ctypes.c_uint64), ("sdma_congestion_backoffs", ctypes.c_uint64),
                 ("sdma_engines_h2d", ctypes.c_uint32), ("sdma_engines_d2h", ctypes.c_uint32),
                 ("cu_path_enabled", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
 

@@ -18,6 +18,12 @@ struct PlanItem {
 };
 
 constexpr uint32_t kPlanCuOnly = 1u;
+constexpr uint32_t kPlanSdmaOnly = 2u;  // static-split baseline: reserved for the SDMA engines
+
+// Static-split baseline: task i of n goes to the CU path iff the running share
+// floor((i + 1) * pct / 100) grows at i, so exactly floor(n * pct / 100) tasks,
+// evenly interleaved, are CU tasks.
+inline bool static_cu_task(uint64_t i, uint32_t pct) { return (i + 1) * pct / 100 > i * pct / 100; }
 
 // Fixed chunks from offset 0 of each tensor, the last one shorter; a tensor below
 // `fallback` bytes is a single micro-task, below `small` it is CU-path-only.

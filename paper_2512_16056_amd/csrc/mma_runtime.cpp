@@ -149,6 +149,8 @@ struct SdmaSlot {
   uint32_t left = 0;      // ring entries outstanding
   uint64_t staging = 0;   // device address of this slot's staging buffer
   int path = 0;
+  uint64_t t_submit = 0;  // current copy-engine command: submission time and size
+  uint64_t op_bytes = 0;
 };
 
 struct SdmaPath {
@@ -156,23 +158,26 @@ struct SdmaPath {
   std::vector<int> slots;  // slot ids
   int busy = 0;
   bool full = false;
+  bool congested = false;  // a command is long overdue: pull nothing more until the engine drains
 };
 
 struct Config {
   uint64_t chunk, fallback, small, sub;
   uint32_t depth, cu_depth, backoff, cu_wgs, watchdog_ms;
   uint32_t mask[2];
+  uint32_t static_split, static_cu_percent;
 };
 
 struct Stats {
   std::atomic<uint64_t> transfers{0}, failed{0}, staging_bytes{0}, submit_failures{0}, busy_ns{0};
+  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0};
   std::atomic<uint64_t> path_bytes[MMA_NUM_PATHS], path_tasks[MMA_NUM_PATHS];
   Stats() {
     for (auto& v : path_bytes) v = 0;
     for (auto& v : path_tasks) v = 0;
   }
   void reset() {
-    transfers = failed = staging_bytes = submit_failures = busy_ns = 0;
+    transfers = failed = staging_bytes = submit_failures = busy_ns = foreign_skips = congestion_backoffs = 0;
     for (auto& v : path_bytes) v = 0;
     for (auto& v : path_tasks) v = 0;
   }
@@ -224,8 +229,43 @@ class Engine {
       }
       paths_.push_back(p);
     }
+    mma_status_t w = warm_up();
+    if (w != MMA_OK) return w;
     thread_ = std::thread([this] { loop(); });
     return MMA_OK;
+  }
+
+  // The first command on an engine makes ROCr create that engine's queue
+  // (milliseconds); do it here rather than inside the first transfer.
+  mma_status_t warm_up() {
+    if (paths_.empty()) return MMA_OK;
+    void* host = nullptr;
+    if (hipHostMalloc(&host, 4096, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
+      return fail(MMA_ERR_HIP, "hipHostMalloc(warm-up)");
+    mma_status_t rc = MMA_OK;
+    for (auto& path : paths_) {
+      SdmaSlot& s = slots_[path.slots[0]];
+      hsa_signal_store_screlease(s.sig, 1);
+      const auto eng = static_cast<hsa_amd_sdma_engine_id_t>(1u << path.engine);
+      hsa_status_t r = dir_ == MMA_H2D
+          ? hsa_amd_memory_async_copy_on_engine(reinterpret_cast<void*>(s.staging), gpu_, host, cpu_, 4096, 0,
+                                                nullptr, s.sig, eng, false)
+          : hsa_amd_memory_async_copy_on_engine(host, cpu_, reinterpret_cast<void*>(s.staging), gpu_, 4096, 0,
+                                                nullptr, s.sig, eng, false);
+      if (r != HSA_STATUS_SUCCESS) {
+        rc = fail(MMA_ERR_HSA, "SDMA engine %d rejected a warm-up copy", path.engine);
+        break;
+      }
+      const uint64_t t0 = now_ns();
+      hsa_signal_value_t v;
+      while ((v = hsa_signal_load_scacquire(s.sig)) > 0 && now_ns() - t0 < 10000000000ull) cpu_relax();
+      if (v != 0) {  // still in flight or failed: leave the engine out rather than reuse its signal
+        rc = fail(MMA_ERR_HSA, "SDMA engine %d did not complete a warm-up copy", path.engine);
+        break;
+      }
+    }
+    (void)hipHostFree(host);
+    return rc;
   }
 
   void shutdown() {
@@ -388,7 +428,9 @@ class Engine {
       if (x->cu_full && x->cu_busy < std::min(cfg_.backoff, depth)) x->cu_full = false;
       if (x->cu_full) break;
       size_t i = x->cur_cu;
-      while (i < x->tasks.size() && (x->claimed[i] || (!any && !(x->tasks[i].flags & kPlanCuOnly)))) ++i;
+      while (i < x->tasks.size() && (x->claimed[i] || (x->tasks[i].flags & kPlanSdmaOnly) ||
+                                      (!any && !(x->tasks[i].flags & kPlanCuOnly))))
+        ++i;
       x->cur_cu = i;
       if (i >= x->tasks.size()) break;
       const Task& t = x->tasks[i];
@@ -416,6 +458,8 @@ class Engine {
       if (g_fault_submit_fail.compare_exchange_weak(f, f - 1)) return false;
     }
     if (!s.x->t_first_sdma) s.x->t_first_sdma = now_ns();
+    s.t_submit = now_ns();
+    s.op_bytes = bytes;
     hsa_signal_store_screlease(s.sig, 1);
     const hsa_status_t r = hsa_amd_memory_async_copy_on_engine(
         dst, dst_agent, src, src_agent, bytes, 0, nullptr, s.sig,
@@ -537,11 +581,52 @@ class Engine {
     return false;
   }
 
+  // A copy-engine command is overdue when it has been in flight for four times
+  // what its size needs at 50 GB/s, plus 0.5 ms of slack.
+  bool overdue(const SdmaPath& path, uint64_t now) const {
+    for (int id : path.slots) {
+      const SdmaSlot& s = slots_[id];
+      if (s.state != kCopy && s.state != kH2DStage && s.state != kD2HStage) continue;
+      if (now - s.t_submit > 4 * s.op_bytes / 50 + 500000) return true;  // ns
+    }
+    return false;
+  }
+
+  // Paths that can make progress take work (Section 2.2; Section 3.4 contention
+  // back-off). ROCr keeps one in-order command queue per engine per process, so
+  // a command placed behind another component's copies waits for all of them:
+  // an engine that ROCr reports in use while none of our commands is on it is
+  // busy with foreign work and is skipped; an engine with an overdue command is
+  // backed off until it drains.
   bool pull_sdma() {
     bool p = false;
     const uint32_t bo = std::min(cfg_.backoff, cfg_.depth);
+    uint32_t free_mask = 0;
+    bool have_mask = false;
+    const uint64_t now = now_ns();
     for (size_t k = 0; k < paths_.size(); ++k) {
       SdmaPath& path = paths_[(k + rr_) % paths_.size()];
+      if (path.congested) {
+        if (path.busy > 0) continue;
+        path.congested = false;
+      } else if (path.busy > 0 && overdue(path, now)) {
+        path.congested = true;
+        st_->congestion_backoffs += 1;
+        continue;
+      }
+      if (path.busy == 0) {
+        if (!have_mask) {
+          if (dir_ == MMA_H2D)
+            hsa_amd_memory_copy_engine_status(gpu_, cpu_, &free_mask);
+          else
+            hsa_amd_memory_copy_engine_status(cpu_, gpu_, &free_mask);
+          have_mask = true;
+        }
+        if (!(free_mask & (1u << path.engine))) {
+          st_->foreign_skips += 1;
+          continue;
+        }
+      }
       for (int id : path.slots) {
         if (path.busy >= static_cast<int>(cfg_.depth)) path.full = true;
         if (path.full && path.busy < static_cast<int>(bo)) path.full = false;
@@ -579,7 +664,7 @@ class Engine {
           st_->submit_failures += 1;
           x->claimed[i] = 0;
           --x->n_claimed;
-          x->tasks[i].flags |= kPlanCuOnly;
+          x->tasks[i].flags = (x->tasks[i].flags & ~kPlanSdmaOnly) | kPlanCuOnly;
           x->cur_cu = std::min(x->cur_cu, i);
           free_slot(s);
         }
@@ -975,6 +1060,13 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   r->h.seq = x->seq;
   r->h.status = 0;
   __atomic_thread_fence(__ATOMIC_RELEASE);
+  if (rt->cfg.static_split && e->has_sdma() && x->sdma_ok) {
+    for (size_t i = 0; i < x->tasks.size(); ++i) {
+      uint32_t& f = x->tasks[i].flags;
+      if (f & kPlanCuOnly) continue;
+      f |= static_cu_task(i, rt->cfg.static_cu_percent) ? kPlanCuOnly : kPlanSdmaOnly;
+    }
+  }
   const bool staged = x->kind != Kind::kLinear && e->has_sdma() && x->sdma_ok;
   const bool needs_cu = e->cu_enabled() || staged ||
                         std::any_of(x->tasks.begin(), x->tasks.end(),
@@ -1127,6 +1219,9 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   k.watchdog_ms = c.watchdog_ms;
   k.mask[0] = mask[0];
   k.mask[1] = mask[1];
+  if (c.static_cu_percent > 100) return fail(MMA_ERR_INVALID_ARG, "static_cu_percent > 100");
+  k.static_split = c.static_split;
+  k.static_cu_percent = c.static_cu_percent;
 
   // SDMA staging for the KV kinds: one chunk per SDMA slot, in uncached device
   // memory (coherent between the copy engines and every XCD's L2 without
@@ -1386,6 +1481,8 @@ mma_status_t mma_get_stats(mma_stats_t* out) {
   out->staging_bytes = st.staging_bytes;
   out->sdma_submit_failures = st.submit_failures;
   out->engine_wall_busy_ns = st.busy_ns;
+  out->sdma_foreign_busy_skips = st.foreign_skips;
+  out->sdma_congestion_backoffs = st.congestion_backoffs;
   uint64_t cpu = 0;
   for (auto& e : g_rt->eng) {
     clockid_t cid;
