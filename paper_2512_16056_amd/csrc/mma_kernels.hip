@@ -115,7 +115,22 @@ __device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8
       ++k;
     }
   }
-  for (uint64_t u = nb * kBatch; u + lane < n16; u += kWave) d[u] = s[u];
+  // Remainder (< one batch): one predicated batch, all loads issued before the
+  // first store, so a short copy costs one round trip instead of one per 1 KiB.
+  const uint64_t r = nb * kBatch;
+  if (r < n16) {
+    const uint64_t left = n16 - r;  // units left for the whole wave, < kBatch
+    u32x4 c0, c1, c2, c3, c4, c5, c6, c7, c8, c9, c10, c11, c12, c13, c14, c15;
+#define MMA_PLD(k) if ((k) * kWave + lane < left) c##k = s[r + (k) * kWave];
+#define MMA_PST(k) if ((k) * kWave + lane < left) d[r + (k) * kWave] = c##k;
+    MMA_PLD(0) MMA_PLD(1) MMA_PLD(2) MMA_PLD(3) MMA_PLD(4) MMA_PLD(5) MMA_PLD(6) MMA_PLD(7)
+    MMA_PLD(8) MMA_PLD(9) MMA_PLD(10) MMA_PLD(11) MMA_PLD(12) MMA_PLD(13) MMA_PLD(14) MMA_PLD(15)
+    __builtin_amdgcn_sched_barrier(0);
+    MMA_PST(0) MMA_PST(1) MMA_PST(2) MMA_PST(3) MMA_PST(4) MMA_PST(5) MMA_PST(6) MMA_PST(7)
+    MMA_PST(8) MMA_PST(9) MMA_PST(10) MMA_PST(11) MMA_PST(12) MMA_PST(13) MMA_PST(14) MMA_PST(15)
+#undef MMA_PLD
+#undef MMA_PST
+  }
   const uint64_t tail = n & 15u;
   const uint64_t base = n16 << 4;
   if (lane < tail) dst[base + lane] = src[base + lane];
@@ -155,6 +170,7 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
     x = lane_u64(x, 0);
     const uint64_t expect = make_tag(a.seq, x);
     const uint64_t* ew = reinterpret_cast<const uint64_t*>(&rec->ring[x % kRingSize]);
+    if (a.self_contained && x >= a.n_pre) break;  // every entry came with the launch
     uint32_t state = 0;  // 1: entry ready, 3: watchdog
     uint64_t w1 = 0, w2 = 0, w3 = 0;
     if (x < a.n_pre) {  // first entries arrive with the launch: no PCIe round trip
@@ -238,7 +254,9 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
     const uint32_t n = __hip_atomic_fetch_add(&ds->exited, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (n == a.total_waves - 1) {
       uint32_t to = __hip_atomic_load(&ds->timed_out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      while (!to && ld_sys(&rec->h.complete) != a.seq) {
+      // Self-contained transfers have no copy-engine part: every wave has left,
+      // so every byte has been moved.
+      while (!to && !a.self_contained && ld_sys(&rec->h.complete) != a.seq) {
         const uint64_t now = wall_clock64();
         const uint64_t hb2 = ld_sys(&rec->h.heartbeat);
         if (hb2 != hb) {

@@ -114,6 +114,7 @@ struct Transfer {
   uint64_t pushed = 0, done_upto = 0;
   uint32_t waves = 0;          // waves of the dummy-task kernel
   bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
+  bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
   int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
   uint8_t tdone[kRingSize];
   uint32_t cu_busy = 0;
@@ -691,8 +692,9 @@ class Engine {
       }
       p = true;
     }
-    // The kernel leaves the record only after `complete`, or on its watchdog.
-    if (!x->completed && !x->aborting && ld_acq(&r->h.released) == x->seq) {
+    // The kernel leaves the record only after `complete`, or on its watchdog
+    // (a self-contained kernel leaves when its own entries are done).
+    if (!x->completed && !x->aborting && !x->self_contained && ld_acq(&r->h.released) == x->seq) {
       x->aborting = true;
       x->failed = true;
       p = true;
@@ -775,6 +777,10 @@ class Engine {
 
   bool retire_ready(Transfer* x) {
     if (ld_acq(&x->rec->h.released) != x->seq) return false;
+    if (x->self_contained && !x->completed) {  // its done tags may still be in flight
+      if (ld_acq(&x->rec->h.status) != 0) x->failed = true;
+      else return false;
+    }
     return x->sdma_refs == 0;
   }
 
@@ -1075,9 +1081,13 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   x->waves = grid * kWavesPerWG;
   e->prefill(x.get());
   const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
+  // Everything fits the launch: all tasks were claimed by the CU prefill (so no
+  // copy engine can take part) and all their entries are in the kernel args.
+  x->self_contained = !kv && x->n_claimed == x->tasks.size() && x->pushed == n_pre;
   static thread_local KernelArgs a;
   memset(&a, 0, offsetof(KernelArgs, layer_ptr));
   a.n_pre = n_pre;
+  a.self_contained = x->self_contained ? 1u : 0u;
   for (uint32_t t = 0; t < n_pre; ++t) {
     const CuEntry& en = r->ring[t];
     a.pre[t][0] = en.a;
