@@ -84,6 +84,266 @@ def recorded_traffic(root: str):
     return rec.get("traffic_bytes_per_launch")
 
 
+def _timed(stream, fn, reps, warm):
+    """Median (and p10/p90) of HIP-event-bracketed runs of fn on `stream`."""
+    import torch
+    for _ in range(warm):
+        fn()
+    stream.synchronize()
+    ts = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        b.synchronize()
+        ts.append(a.elapsed_time(b))
+    return _pcts(ts)
+
+
+def _pcts(ts):
+    ts = sorted(ts)
+
+    def q(p):
+        return ts[min(len(ts) - 1, int(round(p * (len(ts) - 1))))]
+    return {"p10": q(0.1), "p50": q(0.5), "p90": q(0.9), "mean": sum(ts) / len(ts), "n": len(ts)}
+
+
+def native_lib():
+    import ctypes
+    nat = ctypes.CDLL(os.path.join(ROOT, "paper_2512_16056_amd", "libmma_native.so"))
+    vp, u64, u32, i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int
+    kv_args = [vp, vp, vp, vp, u64, u32, u64, u64, vp]
+    for name, args in (("native_kv_fetch", kv_args), ("native_kv_fetch_batch", kv_args),
+                       ("native_kv_offload", kv_args), ("native_list", [vp, vp, vp, u64, i32, vp]),
+                       ("native_zero_copy", [vp, vp, u64, i32, u32, vp]),
+                       ("native_sdma_all", [vp, vp, u64, i32, u32, i32, ctypes.POINTER(u64)])):
+        fn = getattr(nat, name)
+        fn.restype = ctypes.c_int
+        fn.argtypes = args
+    return nat
+
+
+def link_peaks(mma, nat, stream, sdma_mask):
+    """Measured link peak M(dir): the best of three raw 1 GiB probes that bypass the multipath
+    planner -- one hipMemcpyAsync (median of 20), every host-facing SDMA engine at once over equal
+    parts (median of 5), and a bare zero-copy streaming kernel at the best grid of a sweep
+    (median of 3 per grid)."""
+    import ctypes
+
+    import torch
+    n = 1 << 30
+    hbuf = mma.PinnedBuffer(n)
+    hbuf.array[::4096] = 1
+    dbuf = torch.empty(n, dtype=torch.uint8, device="cuda")
+    res = {}
+    for d, name in ((0, "h2d"), (1, "d2h")):
+        dst, src = (dbuf.data_ptr(), hbuf.ptr) if d == 0 else (hbuf.ptr, dbuf.data_ptr())
+        D, S, Z = (ctypes.c_void_p * 1)(dst), (ctypes.c_void_p * 1)(src), (ctypes.c_uint64 * 1)(n)
+        memcpy = _timed(stream, lambda: nat.native_list(D, S, Z, 1, d, ctypes.c_void_p(stream.cuda_stream)),
+                        reps=20, warm=2)["p50"]
+        torch.cuda.synchronize()
+        ns = ctypes.c_uint64(0)
+        sd = []
+        for _ in range(6):
+            rc = nat.native_sdma_all(dst, src, n, d, sdma_mask, 0, ctypes.byref(ns))
+            if rc != 0:
+                sd = []
+                break
+            sd.append(ns.value / 1e6)
+        sdma = _pcts(sd[1:])["p50"] if sd else None
+        zc = {}
+        for grid in (16, 32, 64, 128, 256, 512, 1024):
+            zc[grid] = _timed(stream, lambda: nat.native_zero_copy(dst, src, n, d, grid,
+                                                                   ctypes.c_void_p(stream.cuda_stream)),
+                              reps=3, warm=1)["p50"]
+        best_grid = min(zc, key=zc.get)
+        rates = {"hipMemcpyAsync": n / memcpy / 1e6, "sdma_all": n / sdma / 1e6 if sdma else None,
+                 "zero_copy_kernel": n / zc[best_grid] / 1e6}
+        res[name] = {"peak_GBs": round(max(v for v in rates.values() if v), 2),
+                     **{k: (round(v, 2) if v else None) for k, v in rates.items()},
+                     "zero_copy_best_grid": best_grid,
+                     "sdma_mask": hex(sdma_mask)}
+    del dbuf
+    hbuf.free()
+    return res
+
+
+def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_step, total, out):
+    import ctypes
+    extras = {}
+    nat = native_lib()
+    cfg = mma.mma_get_config().as_dict()
+
+    peaks = link_peaks(mma, nat, stream, cfg["path_mask_h2d"] & 0xFFFF)
+    extras["measured_link"] = peaks
+    m_h2d, m_d2h = peaks["h2d"]["peak_GBs"], peaks["d2h"]["peak_GBs"]
+    out["roofline"]["measured_peak"] = m_h2d
+    out["roofline"]["frac_of_measured"] = round(out["roofline"]["achieved"] / m_h2d, 4)
+    log("measured link:", peaks)
+
+    # native per-piece hipMemcpyAsync KV fetch (262,144 copies), and the batched call if present
+    lp = (ctypes.c_void_p * s.layers)(*[t.data_ptr() for t in layers])
+    hs_c, gb_c = hs.ctypes.data_as(ctypes.c_void_p), gb.ctypes.data_as(ctypes.c_void_p)
+    for fn_name in ("native_kv_fetch", "native_kv_fetch_batch"):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        rc = getattr(nat, fn_name)(pool.ptr, lp, hs_c, gb_c, s.n_blocks, s.layers, s.piece_bytes, s.gpu_num_blocks,
+                                   ctypes.c_void_p(stream.cuda_stream))
+        stream.synchronize()
+        extras[f"{fn_name}_ms"] = round((time.perf_counter() - t0) * 1e3, 2) if rc == 0 else None
+    if extras.get("native_kv_fetch_ms"):
+        extras["kv_fetch_speedup_vs_native"] = round(extras["native_kv_fetch_ms"] / ms_per_step, 2)
+
+    # the 64 MiB single-copy workload: MMA vs one hipMemcpyAsync, 50 runs each after 5 warm-ups
+    n = W.COPY64_BYTES
+    src = mma.PinnedBuffer(n)
+    src.array[:] = W.uniform_bytes(1, W.TAG_DATA, 0, n)
+    dst = torch.full((n,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
+    m64 = _timed(stream, lambda: mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, stream), reps=50, warm=5)
+    ok64 = bool(np.array_equal(dst.cpu().numpy(), src.array))
+    D, S, Z = (ctypes.c_void_p * 1)(dst.data_ptr()), (ctypes.c_void_p * 1)(src.ptr), (ctypes.c_uint64 * 1)(n)
+    n64 = _timed(stream, lambda: nat.native_list(D, S, Z, 1, 0, ctypes.c_void_p(stream.cuda_stream)),
+                 reps=50, warm=5)
+    extras["copy64"] = {"mma_ms": round(m64["p50"], 4), "mma_ms_p10_p90": [round(m64["p10"], 4), round(m64["p90"], 4)],
+                        "mma_GBs": round(n / m64["p50"] / 1e6, 2),
+                        "native_ms": round(n64["p50"], 4),
+                        "native_ms_p10_p90": [round(n64["p10"], 4), round(n64["p90"], 4)],
+                        "native_GBs": round(n / n64["p50"] / 1e6, 2),
+                        "ratio_vs_native": round(n64["p50"] / m64["p50"], 3), "parity": ok64,
+                        "frac_of_pcie5": round(n / m64["p50"] / 1e6 / PCIE5_X16_GBS, 4),
+                        "frac_of_measured": round(n / m64["p50"] / 1e6 / m_h2d, 4)}
+    src.free()
+    del dst
+
+    # KV offload (GPU -> host): the 50%-dirty subset of the cache just fetched, 2048 blocks (4 GiB),
+    # into a permutation of host slots; against 131,072 per-piece hipMemcpyAsync D2H.
+    plan = W.kv_offload_plan(s, cfg=4)
+    src_blocks = gb[plan.dirty].astype(np.int32)
+    off_bytes = len(plan.dirty) * s.slot_bytes
+    off = _timed(stream, lambda: mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, stream), reps=5, warm=1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    rc = nat.native_kv_offload(pool.ptr, lp, src_blocks.ctypes.data_as(ctypes.c_void_p),
+                               plan.dest.ctypes.data_as(ctypes.c_void_p), len(plan.dirty), s.layers, s.piece_bytes,
+                               s.gpu_num_blocks, ctypes.c_void_p(stream.cuda_stream))
+    stream.synchronize()
+    nat_off = (time.perf_counter() - t0) * 1e3 if rc == 0 else None
+    extras["kv_offload_2048_blocks"] = {
+        "mma_ms": round(off["p50"], 3), "mma_ms_p10_p90": [round(off["p10"], 3), round(off["p90"], 3)],
+        "mma_GBs": round(off_bytes / off["p50"] / 1e6, 2),
+        "frac_of_measured_d2h": round(off_bytes / off["p50"] / 1e6 / m_d2h, 4),
+        "native_per_piece_ms": round(nat_off, 2) if nat_off else None,
+        "speedup_vs_native": round(nat_off / off["p50"], 2) if nat_off else None}
+
+    # The same gather with the pool resident in HBM: the CU gather/scatter code alone, HBM-bound.
+    r = np.random.default_rng(1)
+    dpool = torch.empty(s.host_num_slots * s.slot_bytes, dtype=torch.uint8, device="cuda")
+    dpool.copy_(torch.from_numpy(pool.array))
+    hbm = _timed(stream, lambda: mma.mma_kv_fetch(lay, dpool, layers, hs, gb, stream), reps=5, warm=1)
+    ok_hbm = True
+    pv4 = pool.array.reshape(s.host_num_slots, s.layers, 2, -1)
+    for _ in range(16):
+        i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
+        o = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
+        ok_hbm &= bool(np.array_equal(layers[l][o:o + s.piece_bytes].cpu().numpy(), pv4[hs[i], l, k]))
+    extras["kv_gather_hbm_pool"] = {"ms": round(hbm["p50"], 3), "payload_GBs": round(total / hbm["p50"] / 1e6, 1),
+                                    "hbm_GBs_read_plus_write": round(2 * total / hbm["p50"] / 1e6, 1),
+                                    "frac_of_8TBs": round(2 * total / hbm["p50"] / 1e6 / 8000.0, 4),
+                                    "sampled_parity": ok_hbm}
+    del dpool
+
+    # Model wake-up: 291 Llama-3-8B-shaped bf16 tensors (16.06 GB) as one list, against 291 hipMemcpyAsync.
+    sizes = W.weight_tensor_bytes()
+    offs, wtotal = W.arena_offsets(sizes, 256)
+    arena = mma.PinnedBuffer(wtotal)
+    arena.array[::4096] = 0x3C
+    wdst = [torch.empty(k, dtype=torch.uint8, device="cuda") for k in sizes]
+    lst = [(wdst[t], arena.ptr + offs[t], sizes[t]) for t in range(len(sizes))]
+    w = _timed(stream, lambda: mma.mma_weights_load(lst, mma.MMA_H2D, stream), reps=3, warm=1)
+    Dw = (ctypes.c_void_p * len(sizes))(*[t.data_ptr() for t in wdst])
+    Sw = (ctypes.c_void_p * len(sizes))(*[arena.ptr + o for o in offs])
+    Zw = (ctypes.c_uint64 * len(sizes))(*sizes)
+    wn = _timed(stream, lambda: nat.native_list(Dw, Sw, Zw, len(sizes), 0, ctypes.c_void_p(stream.cuda_stream)),
+                reps=3, warm=1)
+    extras["weights_wakeup_291"] = {"mma_ms": round(w["p50"], 2), "mma_GBs": round(wtotal / w["p50"] / 1e6, 2),
+                                    "native_ms": round(wn["p50"], 2), "ratio_vs_native": round(wn["p50"] / w["p50"], 3)}
+
+    # Mixed contention: the wake-up list as 34 groups on stream A, each followed by the dependent
+    # digest kernel over the group, while the 2048-block offload runs on stream B; 256 KiB chunks.
+    extras["mixed_contention"] = mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan,
+                                                  arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
+    del wdst
+    arena.free()
+    return extras
+
+
+def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan, arena, offs, sizes, wdst,
+                     Dw, Sw, Zw, lp):
+    import ctypes
+    groups = W.weight_groups()
+    assert all(list(g) == list(range(g[0], g[0] + len(g))) for g in groups)
+    digests = torch.zeros(len(sizes), dtype=torch.int64, device="cuda")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    res = {}
+
+    def schedule(use_mma):
+        ea = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        eb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ea[0].record(sa)
+        for g in groups:
+            if use_mma:
+                mma.mma_weights_load([(wdst[t], arena.ptr + offs[t], sizes[t]) for t in g], mma.MMA_H2D, sa)
+            else:  # a group is a contiguous run of the tensor list
+                o = 8 * g[0]
+                nat.native_list(ctypes.addressof(Dw) + o, ctypes.addressof(Sw) + o, ctypes.addressof(Zw) + o,
+                                len(g), 0, ctypes.c_void_p(sa.cuda_stream))
+            for t in g:
+                mma.mma_digest_u32(wdst[t], sizes[t], digests.data_ptr() + 8 * t, sa)
+        ea[1].record(sa)
+        eb[0].record(sb)
+        if use_mma:
+            mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, sb)
+        else:
+            nat.native_kv_offload(pool.ptr, lp, src_blocks.ctypes.data_as(ctypes.c_void_p),
+                                  plan.dest.ctypes.data_as(ctypes.c_void_p), len(src_blocks), s.layers,
+                                  s.piece_bytes, s.gpu_num_blocks, ctypes.c_void_p(sb.cuda_stream))
+        eb[1].record(sb)
+        torch.cuda.synchronize()
+        return ea[0].elapsed_time(ea[1]), eb[0].elapsed_time(eb[1])
+
+    cfg = mma.mma_get_config()
+    mma.mma_finalize()
+    c = mma.mma_config_default()
+    c.chunk_bytes = 256 << 10
+    mma.mma_init(0, c)
+    try:
+        for t in range(len(sizes)):
+            wdst[t].fill_(W.WEIGHT_POISON)
+        schedule(True)  # warm-up at this chunk size
+        for t in range(len(sizes)):
+            wdst[t].fill_(W.WEIGHT_POISON)
+        a_ms, b_ms = schedule(True)
+        mma.mma_synchronize()
+        r = np.random.default_rng(2)
+        ok = True
+        for t in [int(x) for x in r.integers(len(sizes), size=8)]:
+            ok &= bool(np.array_equal(wdst[t][:65536].cpu().numpy(), arena.array[offs[t]:offs[t] + min(65536, sizes[t])]))
+        res["mma"] = {"stream_a_weights_digests_ms": round(a_ms, 1), "stream_b_offload_ms": round(b_ms, 1),
+                      "makespan_ms": round(max(a_ms, b_ms), 1), "sampled_parity": ok,
+                      "failed_transfers": mma.mma_get_stats()["failed_transfers"]}
+    finally:
+        mma.mma_finalize()
+        mma.mma_init(0, cfg)
+    a_ms, b_ms = schedule(False)
+    res["native"] = {"stream_a_weights_digests_ms": round(a_ms, 1), "stream_b_offload_ms": round(b_ms, 1),
+                     "makespan_ms": round(max(a_ms, b_ms), 1)}
+    res["makespan_speedup_vs_native"] = round(res["native"]["makespan_ms"] / res["mma"]["makespan_ms"], 3)
+    res["chunk_bytes"] = 256 << 10
+    return res
+
+
 def main():
     args = parse()
     if args.calib:
@@ -150,6 +410,7 @@ def main():
     stats = mma.mma_get_stats()
     kernel_ms = [a.elapsed_time(b) for a, b in ev]
     avg_kernel_ms = sum(kernel_ms) / len(kernel_ms)
+    kp = _pcts(kernel_ms)
     ms_per_step = elapsed * 1e3 / args.steps
     value = total * args.steps / elapsed / 1e9
     achieved = total / (avg_kernel_ms * 1e-3) / 1e9
@@ -192,6 +453,7 @@ def main():
             "parallelism": "1 GPU (SDMA engines + CU zero-copy on its own PCIe link)",
         },
         "kv_fetch_latency_ms": round(avg_kernel_ms, 3),
+        "kv_fetch_latency_ms_p10_p50_p90": [round(kp[k], 3) for k in ("p10", "p50", "p90")],
         "sampled_parity": ok,
         "path_bytes": {"cu": stats["path_bytes"][16],
                        **{f"sdma{e}": stats["path_bytes"][e] for e in range(16) if stats["path_bytes"][e]}},
@@ -209,145 +471,7 @@ def main():
 
     extras = {}
     if not args.no_extras:
-        # measured link peak: native hipMemcpyAsync of 1 GiB from pinned memory
-        n = 1 << 30
-        hbuf = torch.empty(n, dtype=torch.uint8).pin_memory()
-        dbuf = torch.empty(n, dtype=torch.uint8, device="cuda")
-        times = []
-        for _ in range(6):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            with torch.cuda.stream(stream):
-                dbuf.copy_(hbuf, non_blocking=True)
-            b.record(stream)
-            b.synchronize()
-            times.append(a.elapsed_time(b))
-        link = n / (sorted(times[1:])[len(times[1:]) // 2] * 1e-3) / 1e9
-        extras["measured_h2d_link_GBs"] = round(link, 2)
-        out["roofline"]["measured_peak"] = round(link, 2)
-        out["roofline"]["frac_of_measured"] = round(achieved / link, 4)
-        del hbuf, dbuf
-
-        # native per-piece hipMemcpyAsync KV fetch (262,144 copies)
-        nat = ctypes.CDLL(os.path.join(ROOT, "paper_2512_16056_amd", "libmma_native.so"))
-        lp = (ctypes.c_void_p * s.layers)(*[t.data_ptr() for t in layers])
-        hs_c = hs.ctypes.data_as(ctypes.c_void_p)
-        gb_c = gb.ctypes.data_as(ctypes.c_void_p)
-        for fn_name in ("native_kv_fetch", "native_kv_fetch_batch"):
-            fn = getattr(nat, fn_name)
-            fn.restype = ctypes.c_int
-            fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
-                           ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p]
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            rc = fn(pool.ptr, lp, hs_c, gb_c, s.n_blocks, s.layers, s.piece_bytes, s.gpu_num_blocks,
-                    stream.cuda_stream)
-            stream.synchronize()
-            dt = time.perf_counter() - t0
-            if rc == 0:
-                extras[f"{fn_name}_ms"] = round(dt * 1e3, 2)
-            else:
-                extras[f"{fn_name}_ms"] = None
-        nat_ms = extras.get("native_kv_fetch_ms")
-        if nat_ms:
-            extras["kv_fetch_speedup_vs_native"] = round(nat_ms / ms_per_step, 2)
-
-        # the 64 MiB single-copy workload: MMA vs one hipMemcpyAsync
-        n = W.COPY64_BYTES
-        src = mma.PinnedBuffer(n)
-        src.array[:] = W.uniform_bytes(1, W.TAG_DATA, 0, n)
-        dst = torch.empty(n, dtype=torch.uint8, device="cuda")
-        srct = torch.from_numpy(src.array)  # pinned memory seen by torch as a CPU tensor
-
-        def timed(fn, reps=50, warm=5):
-            ts = []
-            for _ in range(min(warm, reps)):
-                fn()
-            stream.synchronize()
-            for _ in range(reps):
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record(stream)
-                fn()
-                b.record(stream)
-                b.synchronize()
-                ts.append(a.elapsed_time(b))
-            ts.sort()
-            return ts[len(ts) // 2]
-
-        mma_ms = timed(lambda: mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, stream))
-        ok64 = bool(np.array_equal(dst.cpu().numpy(), src.array))
-
-        def native():
-            with torch.cuda.stream(stream):
-                dst.copy_(srct, non_blocking=True)
-
-        nat64 = timed(native)
-        extras["copy64"] = {"mma_ms": round(mma_ms, 4), "mma_GBs": round(n / mma_ms / 1e6, 2),
-                            "native_ms": round(nat64, 4), "native_GBs": round(n / nat64 / 1e6, 2),
-                            "ratio_vs_native": round(nat64 / mma_ms, 3), "parity": ok64,
-                            "frac_of_pcie5": round(n / mma_ms / 1e6 / PCIE5_X16_GBS, 4)}
-        if "measured_h2d_link_GBs" in extras:
-            extras["copy64"]["frac_of_measured"] = round(n / mma_ms / 1e6 / extras["measured_h2d_link_GBs"], 4)
-        src.free()
-
-        # KV offload (GPU -> host): the 50%-dirty subset of the cache just fetched, 2048 blocks (4 GiB),
-        # into a permutation of host slots; against 131,072 per-piece hipMemcpyAsync D2H.
-        plan = W.kv_offload_plan(s, cfg=4)
-        src_blocks = gb[plan.dirty].astype(np.int32)
-        off_bytes = len(plan.dirty) * s.slot_bytes
-
-        def offload():
-            mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, stream)
-
-        off_ms = timed(offload, reps=5)
-        fn = nat.native_kv_offload
-        fn.restype = ctypes.c_int
-        fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
-                       ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        rc = fn(pool.ptr, lp, src_blocks.ctypes.data_as(ctypes.c_void_p), plan.dest.ctypes.data_as(ctypes.c_void_p),
-                len(plan.dirty), s.layers, s.piece_bytes, s.gpu_num_blocks, stream.cuda_stream)
-        stream.synchronize()
-        nat_off = (time.perf_counter() - t0) * 1e3 if rc == 0 else None
-        extras["kv_offload_2048_blocks"] = {"mma_ms": round(off_ms, 3), "mma_GBs": round(off_bytes / off_ms / 1e6, 2),
-                                            "native_per_piece_ms": round(nat_off, 2) if nat_off else None,
-                                            "speedup_vs_native": round(nat_off / off_ms, 2) if nat_off else None}
-
-        # The same gather with the pool resident in HBM: the CU gather/scatter code alone, HBM-bound.
-        dpool = torch.empty(s.host_num_slots * s.slot_bytes, dtype=torch.uint8, device="cuda")
-        dpool.copy_(torch.from_numpy(pool.array))
-        hbm_ms = timed(lambda: mma.mma_kv_fetch(lay, dpool, layers, hs, gb, stream), reps=5)
-        ok_hbm = True
-        for _ in range(16):
-            i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
-            off = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
-            ok_hbm &= bool(np.array_equal(layers[l][off:off + s.piece_bytes].cpu().numpy(),
-                                          pool.array.reshape(s.host_num_slots, s.layers, 2, -1)[hs[i], l, k]))
-        extras["kv_gather_hbm_pool"] = {"ms": round(hbm_ms, 3), "payload_GBs": round(total / hbm_ms / 1e6, 1),
-                                        "hbm_GBs_read_plus_write": round(2 * total / hbm_ms / 1e6, 1),
-                                        "frac_of_8TBs": round(2 * total / hbm_ms / 1e6 / 8000.0, 4),
-                                        "sampled_parity": ok_hbm}
-        del dpool
-
-        # Model wake-up: 291 Llama-3-8B-shaped bf16 tensors (16.06 GB) as one list, against 291 hipMemcpyAsync.
-        sizes = W.weight_tensor_bytes()
-        offs, wtotal = W.arena_offsets(sizes, 256)
-        arena = mma.PinnedBuffer(wtotal)
-        arena.array[:] = 0x3C
-        wdst = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in sizes]
-        lst = [(wdst[t], arena.ptr + offs[t], sizes[t]) for t in range(len(sizes))]
-        w_ms = timed(lambda: mma.mma_weights_load(lst, mma.MMA_H2D, stream), reps=3)
-        D = (ctypes.c_void_p * len(sizes))(*[t.data_ptr() for t in wdst])
-        S = (ctypes.c_void_p * len(sizes))(*[arena.ptr + o for o in offs])
-        Z = (ctypes.c_uint64 * len(sizes))(*sizes)
-        nat.native_list.restype = ctypes.c_int
-        w_nat = timed(lambda: nat.native_list(D, S, Z, ctypes.c_uint64(len(sizes)), 0,
-                                              ctypes.c_void_p(stream.cuda_stream)), reps=3)
-        extras["weights_wakeup_291"] = {"mma_ms": round(w_ms, 2), "mma_GBs": round(wtotal / w_ms / 1e6, 2),
-                                        "native_ms": round(w_nat, 2), "ratio_vs_native": round(w_nat / w_ms, 3)}
-        del wdst
-        arena.free()
+        extras = run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_step, total, out)
         log("extras:", extras)
     out["extras"] = extras
 
@@ -366,6 +490,25 @@ def main():
                                "kind": "oracle",
                                "sample": f"{reps} x the full 4096-block 64k-token KV fetch (oracle.kv.kv_fetch_layer "
                                          f"over 32 layers, numpy slice copies, one thread), {dt:.1f} s"}
+        # The same oracle calls spread over every core this process may use (one layer per task):
+        # context for the host's own copy bandwidth.
+        ncores = min(16, len(os.sched_getaffinity(0)))
+
+        def layer_task(l_):
+            okv.kv_fetch_layer(pv, poison, l_, s.layers, hs, gb)
+
+        reps, t0 = 0, time.perf_counter()
+        with ThreadPoolExecutor(ncores) as ex:
+            while True:
+                list(ex.map(layer_task, range(s.layers)))
+                reps += 1
+                if time.perf_counter() - t0 >= args.cpu_seconds / 2:
+                    break
+        dt = time.perf_counter() - t0
+        out["cpu_baseline_all_cores"] = {"value": round(total * reps / dt / 1e9, 3), "unit": "GB/s",
+                                         "cores": ncores, "kind": "oracle",
+                                         "sample": f"{reps} x the full fetch, 32 layer tasks over {ncores} threads, "
+                                                   f"{dt:.1f} s"}
     print(json.dumps(out), flush=True)
     pool.free()
     mma.mma_finalize()

@@ -54,9 +54,12 @@ def build(verbose: bool = False) -> str:
           f"-L{os.path.join(ROCM, 'lib')}", "-lhsa-runtime64", "-lpthread"])
     os.replace(tmp, LIB)
     tmp = NATIVE_LIB + ".tmp"
-    _run([HIPCC, "-x", "c++", "-D__HIP_PLATFORM_AMD__", f"-I{os.path.join(ROCM, 'include')}", *COMMON, "-shared",
-          os.path.join(CSRC, "native_baseline.cpp"), "-o", tmp, f"-L{os.path.join(ROCM, 'lib')}", "-lamdhip64",
-          "-ldl"])
+    nobj = [os.path.join(OBJ, "native_baseline.cpp.o"), os.path.join(OBJ, "native_probes.hip.o")]
+    _run([HIPCC, "-x", "c++", "-D__HIP_PLATFORM_AMD__", f"-I{os.path.join(ROCM, 'include')}", *COMMON, "-c",
+          os.path.join(CSRC, "native_baseline.cpp"), "-o", nobj[0]])
+    _run([HIPCC, *DEVICE, *COMMON, "-c", os.path.join(CSRC, "native_probes.hip"), "-o", nobj[1]])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *nobj, "-o", tmp, f"-L{os.path.join(ROCM, 'lib')}",
+          "-lamdhip64", "-lhsa-runtime64", "-ldl"])
     os.replace(tmp, NATIVE_LIB)
     return LIB
 
