@@ -97,7 +97,11 @@ typedef struct mma_config {
                                time: static_cu_percent of the micro-tasks (interleaved) go to the
                                CU path, the rest to the SDMA engines (which share them by pulling) */
   uint32_t static_cu_percent;
-  uint32_t reserved[2];
+  uint32_t sdma_merge_tasks; /* at most this many micro-tasks that follow each other in both
+                               address spaces (a linear run, or one KV block's consecutive pieces)
+                               go to an SDMA engine as one command; default: 8 MiB worth
+                               (max(1, 8 MiB / chunk_bytes)); 1 = one command per micro-task */
+  uint32_t reserved;
 } mma_config_t;
 
 typedef struct mma_copy_desc {
@@ -133,6 +137,8 @@ typedef struct mma_stats {
   uint64_t engine_wall_busy_ns;           /* wall time with at least one transfer active */
   uint64_t sdma_foreign_busy_skips;       /* pulls skipped: engine busy with another component's copies */
   uint64_t sdma_congestion_backoffs;      /* engines backed off after an overdue command */
+  uint64_t sdma_commands;                 /* copy-engine commands issued (a command may carry several
+                                             adjacent micro-tasks) */
   uint32_t sdma_engines_h2d;              /* masks actually in use */
   uint32_t sdma_engines_d2h;
   uint32_t cu_path_enabled;

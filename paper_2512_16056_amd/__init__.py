@@ -52,7 +52,8 @@ class mma_config_t(ctypes.Structure):
                 ("path_mask_h2d", ctypes.c_uint32), ("path_mask_d2h", ctypes.c_uint32),
                 ("cu_workgroups", ctypes.c_uint32), ("cu_sub_bytes", ctypes.c_uint32),
                 ("watchdog_ms", ctypes.c_uint32), ("static_split", ctypes.c_uint32),
-                ("static_cu_percent", ctypes.c_uint32), ("reserved", ctypes.c_uint32 * 2)]
+                ("static_cu_percent", ctypes.c_uint32), ("sdma_merge_tasks", ctypes.c_uint32),
+                ("reserved", ctypes.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
@@ -75,6 +76,7 @@ class mma_stats_t(ctypes.Structure):
                 ("staging_bytes", ctypes.c_uint64), ("sdma_submit_failures", ctypes.c_uint64),
                 ("engine_cpu_ns", ctypes.c_uint64), ("engine_wall_busy_ns", ctypes.c_uint64),
                 ("sdma_foreign_busy_skips", ctypes.c_uint64), ("sdma_congestion_backoffs", ctypes.c_uint64),
+                ("sdma_commands", ctypes.c_uint64),
                 ("sdma_engines_h2d", ctypes.c_uint32), ("sdma_engines_d2h", ctypes.c_uint32),
                 ("cu_path_enabled", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
 

@@ -146,7 +146,8 @@ struct SdmaSlot {
   hsa_signal_t sig{};
   int state = kFree;
   Transfer* x = nullptr;
-  size_t task = 0;
+  size_t task = 0, task_end = 0;  // micro-tasks [task, task_end) carried by this slot's command
+  uint64_t count = 0;     // their total: bytes (linear) or pieces (KV, one block's run)
   uint32_t left = 0;      // ring entries outstanding
   uint64_t staging = 0;   // device address of this slot's staging buffer
   int path = 0;
@@ -167,11 +168,12 @@ struct Config {
   uint32_t depth, cu_depth, backoff, cu_wgs, watchdog_ms;
   uint32_t mask[2];
   uint32_t static_split, static_cu_percent;
+  uint32_t merge;       // max micro-tasks per copy-engine command
 };
 
 struct Stats {
   std::atomic<uint64_t> transfers{0}, failed{0}, staging_bytes{0}, submit_failures{0}, busy_ns{0};
-  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0};
+  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0}, sdma_commands{0};
   std::atomic<uint64_t> path_bytes[MMA_NUM_PATHS], path_tasks[MMA_NUM_PATHS];
   Stats() {
     for (auto& v : path_bytes) v = 0;
@@ -179,6 +181,7 @@ struct Stats {
   }
   void reset() {
     transfers = failed = staging_bytes = submit_failures = busy_ns = foreign_skips = congestion_backoffs = 0;
+    sdma_commands = 0;
     for (auto& v : path_bytes) v = 0;
     for (auto& v : path_tasks) v = 0;
   }
@@ -220,8 +223,11 @@ class Engine {
       p.engine = eng;
       for (uint32_t d = 0; d < cfg_.depth; ++d) {
         SdmaSlot s;
-        if (hsa_signal_create(1, 0, nullptr, &s.sig) != HSA_STATUS_SUCCESS)
-          return fail(MMA_ERR_HSA, "hsa_signal_create failed");
+        // The GPU is the signal's only declared consumer, so ROCr makes it a
+        // plain memory signal: no completion interrupt per command (about 3 us
+        // of engine time each, measured). This thread only polls its value.
+        if (hsa_amd_signal_create(1, 1, &gpu_, 0, &s.sig) != HSA_STATUS_SUCCESS)
+          return fail(MMA_ERR_HSA, "hsa_amd_signal_create failed");
         s.staging = stage ? reinterpret_cast<uint64_t>(stage) : 0;
         if (stage) stage += stage_bytes;
         s.path = static_cast<int>(paths_.size());
@@ -465,6 +471,7 @@ class Engine {
     const hsa_status_t r = hsa_amd_memory_async_copy_on_engine(
         dst, dst_agent, src, src_agent, bytes, 0, nullptr, s.sig,
         static_cast<hsa_amd_sdma_engine_id_t>(1u << paths_[s.path].engine), false);
+    if (r == HSA_STATUS_SUCCESS) st_->sdma_commands += 1;
     return r == HSA_STATUS_SUCCESS;
   }
 
@@ -477,23 +484,27 @@ class Engine {
   }
 
   // The staged CU step of an SDMA-carried KV micro-task has landed.
+  void slot_tasks_done(SdmaSlot& s) {
+    for (size_t i = s.task; i < s.task_end; ++i) task_done(s.x, i, paths_[s.path].engine);
+  }
+
   void sdma_cu_stage_done(SdmaSlot& s) {
     Transfer* x = s.x;
     const Task& t = x->tasks[s.task];
     if (s.state == kH2DScatter) {
-      st_->staging_bytes += t.bytes * x->piece;
-      task_done(x, s.task, paths_[s.path].engine);
+      st_->staging_bytes += s.count * x->piece;
+      slot_tasks_done(s);
       free_slot(s);
     } else if (s.state == kD2HGather) {
-      st_->staging_bytes += t.bytes * x->piece;
+      st_->staging_bytes += s.count * x->piece;
       if (sdma_copy(s, reinterpret_cast<void*>(t.host_dma), cpu_, reinterpret_cast<void*>(s.staging), gpu_,
-                    t.bytes * x->piece)) {
+                    s.count * x->piece)) {
         s.state = kD2HStage;
       } else {
-        // The gathered bytes are in staging; finish them with a CU copy instead.
+        // The gathered bytes are in staging and cannot reach the host this way.
         st_->submit_failures += 1;
         x->failed = true;
-        task_done(x, s.task, paths_[s.path].engine);
+        slot_tasks_done(s);
         free_slot(s);
       }
     }
@@ -505,9 +516,9 @@ class Engine {
     const int32_t own = -1 - static_cast<int32_t>(&s - slots_.data());
     uint32_t ne;
     if (s.state == kH2DScatterPush)
-      ne = push_unit(x, own, kEntryToPaged | kEntryAcquire, s.staging, t.blk, t.bytes, t.p0);
+      ne = push_unit(x, own, kEntryToPaged | kEntryAcquire, s.staging, t.blk, s.count, t.p0);
     else
-      ne = push_unit(x, own, kEntryFromPaged, s.staging, t.blk, t.bytes, t.p0);
+      ne = push_unit(x, own, kEntryFromPaged, s.staging, t.blk, s.count, t.p0);
     if (!ne) return false;
     s.left = ne;
     s.state = s.state == kH2DScatterPush ? kH2DScatter : kD2HGather;
@@ -545,12 +556,12 @@ class Engine {
       if (v < 0) {
         x->failed = true;
         if (s.state == kH2DStage) --x->sdma_cu_pending;
-        task_done(x, s.task, paths_[s.path].engine);
+        slot_tasks_done(s);
         free_slot(s);
         continue;
       }
       if (s.state == kCopy || s.state == kD2HStage) {
-        task_done(x, s.task, paths_[s.path].engine);
+        slot_tasks_done(s);
         free_slot(s);
       } else {  // kH2DStage landed: scatter it on the CU side
         s.state = kH2DScatterPush;
@@ -580,6 +591,32 @@ class Engine {
       }
     }
     return false;
+  }
+
+  // One copy-engine command carries the claimed micro-task i and the unclaimed
+  // ones that directly follow it in both address spaces (a linear run, or one
+  // KV block's consecutive pieces that fit the staging slot), up to cfg.merge.
+  // Each ROCr copy command costs about 8 us of engine time (measured), so at
+  // small chunk sizes one command per micro-task would cap an engine well
+  // below the link.
+  size_t merge_run(const Transfer* x, size_t i) const {
+    const bool sdma_only = (x->tasks[i].flags & kPlanSdmaOnly) != 0;
+    uint64_t total = x->tasks[i].bytes;
+    size_t j = i + 1;
+    for (; j < x->tasks.size() && j - i < cfg_.merge; ++j) {
+      const Task& a = x->tasks[j - 1];
+      const Task& b = x->tasks[j];
+      if (x->claimed[j] || (b.flags & kPlanCuOnly) || ((b.flags & kPlanSdmaOnly) != 0) != sdma_only) break;
+      if (x->kind == Kind::kLinear) {
+        if (b.src_dma != a.src_dma + a.bytes || b.dst_dma != a.dst_dma + a.bytes) break;
+      } else {
+        if (b.blk != a.blk || b.p0 != a.p0 + a.bytes || b.host_dma != a.host_dma + a.bytes * x->piece ||
+            (total + b.bytes) * x->piece > stage_bytes_)
+          break;
+      }
+      total += b.bytes;
+    }
+    return j;
   }
 
   // A copy-engine command is overdue when it has been in flight for four times
@@ -638,21 +675,25 @@ class Engine {
         size_t i;
         if (!next_sdma_task(x, i)) return p;
         const Task& t = x->tasks[i];
-        x->claimed[i] = 1;
-        ++x->n_claimed;
+        const size_t end = merge_run(x, i);
+        for (size_t j = i; j < end; ++j) x->claimed[j] = 1;
+        x->n_claimed += end - i;
         s.x = x;
         s.task = i;
+        s.task_end = end;
+        s.count = 0;
+        for (size_t j = i; j < end; ++j) s.count += x->tasks[j].bytes;
         ++path.busy;
         ++x->sdma_refs;
         bool ok = true;
         if (x->kind == Kind::kLinear) {
           const bool h2d = dir_ == MMA_H2D;
           ok = sdma_copy(s, reinterpret_cast<void*>(t.dst_dma), h2d ? gpu_ : cpu_,
-                         reinterpret_cast<void*>(t.src_dma), h2d ? cpu_ : gpu_, t.bytes);
+                         reinterpret_cast<void*>(t.src_dma), h2d ? cpu_ : gpu_, s.count);
           s.state = kCopy;
         } else if (x->kind == Kind::kKvFetch) {
           ok = sdma_copy(s, reinterpret_cast<void*>(s.staging), gpu_, reinterpret_cast<void*>(t.host_dma), cpu_,
-                         t.bytes * x->piece);
+                         s.count * x->piece);
           s.state = kH2DStage;
           if (ok) ++x->sdma_cu_pending;
         } else {
@@ -661,11 +702,13 @@ class Engine {
           try_push_stage(s);
         }
         if (!ok) {
-          // Re-route: the task goes back to the queue, CU path only.
+          // Re-route: the tasks go back to the queue, CU path only.
           st_->submit_failures += 1;
-          x->claimed[i] = 0;
-          --x->n_claimed;
-          x->tasks[i].flags = (x->tasks[i].flags & ~kPlanSdmaOnly) | kPlanCuOnly;
+          for (size_t j = i; j < end; ++j) {
+            x->claimed[j] = 0;
+            x->tasks[j].flags = (x->tasks[j].flags & ~kPlanSdmaOnly) | kPlanCuOnly;
+          }
+          x->n_claimed -= end - i;
           x->cur_cu = std::min(x->cur_cu, i);
           free_slot(s);
         }
@@ -1137,6 +1180,7 @@ void fill_config(mma_config_t* c, bool use_env) {
     d.cu_workgroups = static_cast<uint32_t>(env_u64("MMA_CU_WGS", d.cu_workgroups));
     d.cu_sub_bytes = static_cast<uint32_t>(env_u64("MMA_CU_SUB_BYTES", d.cu_sub_bytes));
     d.watchdog_ms = static_cast<uint32_t>(env_u64("MMA_WATCHDOG_MS", d.watchdog_ms));
+    d.sdma_merge_tasks = static_cast<uint32_t>(env_u64("MMA_SDMA_MERGE_TASKS", 0));
   }
   *c = d;
 }
@@ -1232,6 +1276,8 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   if (c.static_cu_percent > 100) return fail(MMA_ERR_INVALID_ARG, "static_cu_percent > 100");
   k.static_split = c.static_split;
   k.static_cu_percent = c.static_cu_percent;
+  k.merge = c.sdma_merge_tasks ? c.sdma_merge_tasks
+                              : static_cast<uint32_t>(std::max<uint64_t>(1, 8 * MiB / c.chunk_bytes));
 
   // SDMA staging for the KV kinds: one chunk per SDMA slot, in uncached device
   // memory (coherent between the copy engines and every XCD's L2 without
@@ -1492,6 +1538,7 @@ mma_status_t mma_get_stats(mma_stats_t* out) {
   out->sdma_submit_failures = st.submit_failures;
   out->engine_wall_busy_ns = st.busy_ns;
   out->sdma_foreign_busy_skips = st.foreign_skips;
+  out->sdma_commands = st.sdma_commands;
   out->sdma_congestion_backoffs = st.congestion_backoffs;
   uint64_t cpu = 0;
   for (auto& e : g_rt->eng) {

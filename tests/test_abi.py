@@ -103,3 +103,31 @@ def test_validate_tables_matches_oracle():
         assert mma.mma_validate_kv_tables(src, sc, dst, dc) == okv.validate_tables(src, sc, dst, dc)
     for perm in itertools.permutations(range(4)):
         assert mma.mma_validate_kv_tables([0, 1, 2, 3], 4, perm, 4)
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """Every ctypes mirror has the size and field offsets that a C compiler gives the header's struct."""
+    import ctypes
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = ["mma_config_t", "mma_stats_t", "mma_copy_desc_t", "mma_kv_layout_t", "mma_trace_rec_t",
+               "mma_plan_entry_t"]
+    lines = ['#include "mma.h"', "#include <stdio.h>", "#include <stddef.h>", "int main(void) {"]
+    want = []
+    for sname in structs:
+        cls = getattr(mma, sname)
+        lines.append(f'  printf("%zu\\n", sizeof({sname}));')
+        want.append(ctypes.sizeof(cls))
+        for fname, _ in cls._fields_:
+            lines.append(f'  printf("%zu\\n", offsetof({sname}, {fname}));')
+            want.append(getattr(cls, fname).offset)
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c99", f"-I{os.path.join(ROOT, 'include')}", str(src), "-o", str(exe)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()]
+    assert got == want

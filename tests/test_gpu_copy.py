@@ -146,6 +146,55 @@ def test_tensor_list_ragged(paths, direction):
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+@pytest.mark.parametrize("merge", [1, 0, 5])
+def test_sdma_command_merging(merge, direction):
+    """Micro-tasks that follow each other in both address spaces go to a copy engine as one
+    command (at most sdma_merge_tasks of them; 0 = default). The bytes must not depend on it: a
+    ragged linear copy and a list of tensors packed back to back on both sides (so runs cross
+    tensor boundaries), on the SDMA engines only, against the oracle."""
+    log(f"sdma merging merge={merge} dir={direction}")
+    chunk = 256 << 10
+    n = 37 * chunk + 12345
+    sizes = _ragged_list(21 + direction, 24, 3 * chunk)
+    offs, ltotal = W.arena_offsets(sizes, 1)
+    src_np = np.ascontiguousarray(W.uniform_bytes(2, W.TAG_DATA, 123, n + ltotal))
+    with session("sdma", chunk_bytes=chunk, sdma_merge_tasks=merge, small_bytes=1):
+        mma.mma_reset_stats()
+        if direction == mma.MMA_H2D:
+            src = mma.PinnedBuffer(n + ltotal)
+            src.array[:] = src_np
+            dst = device_bytes(n + ltotal, W.WEIGHT_POISON)
+            mma.mma_memcpy_async(dst, src, n, direction)
+            mma.mma_weights_load([(dst.data_ptr() + n + o, src.ptr + n + o, k) for o, k in zip(offs, sizes)],
+                                 direction)
+            torch.cuda.synchronize()
+            got = to_host(dst)
+        else:
+            src = from_host(src_np)
+            dst = mma.PinnedBuffer(n + ltotal)
+            dst.array[:] = W.WEIGHT_POISON
+            mma.mma_memcpy_async(dst, src, n, direction)
+            mma.mma_weights_load([(dst.ptr + n + o, src.data_ptr() + n + o, k) for o, k in zip(offs, sizes)],
+                                 direction)
+            torch.cuda.synchronize()
+            got = dst.array.copy()
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+    poison = np.full(n + ltotal, W.WEIGHT_POISON, np.uint8)
+    want = ocopy.tensor_list(ocopy.memcpy(poison, 0, src_np, 0, n), src_np,
+                             [(n + o, n + o, k) for o, k in zip(offs, sizes)])
+    assert np.array_equal(got, want)
+    assert stats["failed_transfers"] == 0
+    sdma_tasks = sum(stats["path_tasks"][:16])
+    log(f"  sdma tasks={sdma_tasks} commands={stats['sdma_commands']} cu tasks={stats['path_tasks'][16]}")
+    assert sdma_tasks > 0
+    if merge == 1:
+        assert stats["sdma_commands"] == sdma_tasks
+    else:
+        assert stats["sdma_commands"] < sdma_tasks
+
+
 def test_rejects_bad_arguments():
     with session("both"):
         src = mma.PinnedBuffer(4096)

@@ -107,6 +107,40 @@ def test_kv_offload_small(paths, shape, chunk):
         assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
 
 
+@pytest.mark.parametrize("merge", [1, 0])
+def test_kv_sdma_merges_block_runs(merge):
+    """With micro-tasks smaller than a block, one copy-engine command carries a block's run of
+    consecutive pieces through staging (fetch) and back (offload); results stay byte-exact."""
+    s = SHAPES["medium"]
+    log(f"kv sdma merge={merge}")
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    plan = W.kv_offload_plan(s, cfg=4)
+    with session("sdma", chunk_bytes=2 * s.piece_bytes, cu_sub_bytes=1024, sdma_merge_tasks=merge):
+        mma.mma_reset_stats()
+        pool = _pool(s, 5)
+        layers = _layers(s, W.GPU_POISON)
+        before = _layer_views(s, layers)
+        mma.mma_kv_fetch(layout_of(s), pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        check_fetch(s, pool, before, layers, hs, gb)
+        pool_before = pool.array.copy()
+        views = _layer_views(s, layers)
+        mma.mma_kv_offload(layout_of(s), pool, layers, plan.src_blocks, plan.dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        want = okv.kv_offload(pool_before.reshape(s.host_num_slots, -1), views, plan.src_blocks, plan.dest)
+        assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
+        stats = mma.mma_get_stats()
+    sdma_tasks = sum(stats["path_tasks"][:16])
+    log(f"  sdma tasks={sdma_tasks} commands={stats['sdma_commands']}")
+    assert stats["failed_transfers"] == 0 and sdma_tasks > 0
+    if merge == 1:
+        assert stats["sdma_commands"] == sdma_tasks
+    else:
+        assert stats["sdma_commands"] < sdma_tasks
+
+
 @pytest.mark.parametrize("paths", list(PATHS))
 def test_kv_all_permutations(paths):
     s = W.KVShape(layers=2, block_tokens=2, kv_heads=1, head_dim=8, elem_bytes=2,
