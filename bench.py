@@ -236,6 +236,24 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
         "native_per_piece_ms": round(nat_off, 2) if nat_off else None,
         "speedup_vs_native": round(nat_off / off["p50"], 2) if nat_off else None}
 
+    # Measured HBM copy peak (read + write bytes): the runtime's device-to-device copy and the bare
+    # streaming kernel over device memory at the best grid, 2 GiB each way.
+    hb = 2 << 30
+    ha = torch.empty(hb, dtype=torch.uint8, device="cuda")
+    hbuf2 = torch.empty(hb, dtype=torch.uint8, device="cuda")
+    with torch.cuda.stream(stream):
+        d2d = _timed(stream, lambda: hbuf2.copy_(ha), reps=5, warm=1)["p50"]
+    zc = {g: _timed(stream, lambda: nat.native_zero_copy(hbuf2.data_ptr(), ha.data_ptr(), hb, 0, g,
+                                                         ctypes.c_void_p(stream.cuda_stream)), reps=5, warm=1)["p50"]
+          for g in (512, 1024, 2048, 4096, 8192)}
+    gbest = min(zc, key=zc.get)
+    hbm_peak = max(2 * hb / d2d / 1e6, 2 * hb / zc[gbest] / 1e6)
+    extras["measured_hbm_copy"] = {"peak_GBs_read_plus_write": round(hbm_peak, 1),
+                                   "device_copy_GBs": round(2 * hb / d2d / 1e6, 1),
+                                   "streaming_kernel_GBs": round(2 * hb / zc[gbest] / 1e6, 1),
+                                   "streaming_kernel_grid": gbest, "theoretical_GBs": 8000.0}
+    del ha, hbuf2
+
     # The same gather with the pool resident in HBM: the CU gather/scatter code alone, HBM-bound.
     r = np.random.default_rng(1)
     dpool = torch.empty(s.host_num_slots * s.slot_bytes, dtype=torch.uint8, device="cuda")
@@ -250,6 +268,7 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
     extras["kv_gather_hbm_pool"] = {"ms": round(hbm["p50"], 3), "payload_GBs": round(total / hbm["p50"] / 1e6, 1),
                                     "hbm_GBs_read_plus_write": round(2 * total / hbm["p50"] / 1e6, 1),
                                     "frac_of_8TBs": round(2 * total / hbm["p50"] / 1e6 / 8000.0, 4),
+                                    "frac_of_measured_copy": round(2 * total / hbm["p50"] / 1e6 / hbm_peak, 4),
                                     "sampled_parity": ok_hbm}
     del dpool
 

@@ -146,7 +146,7 @@ _SIGNATURES = {
 
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2512_16056_amd.build`")
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2512_16056_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     for name, (args, res) in _SIGNATURES.items():
         f = getattr(lib, name)

@@ -1,6 +1,6 @@
 """Build libmma.so in-tree for gfx950 with hipcc.
 
-Usage: python -m paper_2512_16056_amd.build   (or build() from Python).
+Usage: python paper_2512_16056_amd/build.py   (or __graft_entry__.build()).
 The library is placed next to this file so that it travels with the source tree.
 """
 from __future__ import annotations

@@ -69,7 +69,8 @@ hsa_status_t probe_agent_cb(hsa_agent_t a, void* d) {
 
 extern "C" {
 
-// dir 0: host -> device (src pinned host, dst device); 1: device -> host.
+// dir 0: host -> device (src pinned host, dst device); 1: device -> host. Both
+// pointers may also be device memory (an HBM-to-HBM streaming copy).
 // bytes must be a multiple of 16 and both pointers 16-byte aligned; grid > 0.
 // Returns 0 or the hipError_t of the launch.
 int native_zero_copy(void* dst, const void* src, uint64_t bytes, int dir, uint32_t grid, void* stream) {
