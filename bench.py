@@ -13,6 +13,8 @@ the same workload, native hipMemcpyAsync comparators, and the 64 MiB single-copy
 workload.
 
 Usage: python bench.py [--gpus 1] [--steps 10] [--warmup 2]
+       python bench.py --sweep sizes|chunks|contention|duplex   (JSON line per point)
+       python bench.py --calib                                  (counter-scaling kernels)
 """
 from __future__ import annotations
 
@@ -42,6 +44,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true", help="skip native comparators and the 64 MiB copy")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle timing window")
+    p.add_argument("--sweep", choices=["sizes", "chunks", "contention", "duplex"],
+                   help="instead of the benchmark, print one JSON line per point of a parameter sweep")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
     return p.parse_args()
@@ -287,6 +291,14 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
                 reps=3, warm=1)
     extras["weights_wakeup_291"] = {"mma_ms": round(w["p50"], 2), "mma_GBs": round(wtotal / w["p50"] / 1e6, 2),
                                     "native_ms": round(wn["p50"], 2), "ratio_vs_native": round(wn["p50"] / w["p50"], 3)}
+    # The reverse ("fall asleep"): the same 291 tensors device -> host into the arena.
+    back = [(arena.ptr + offs[t], wdst[t], sizes[t]) for t in range(len(sizes))]
+    ws = _timed(stream, lambda: mma.mma_weights_load(back, mma.MMA_D2H, stream), reps=3, warm=1)
+    wsn = _timed(stream, lambda: nat.native_list(Sw, Dw, Zw, len(sizes), 1, ctypes.c_void_p(stream.cuda_stream)),
+                 reps=3, warm=1)
+    extras["weights_sleep_291"] = {"mma_ms": round(ws["p50"], 2), "mma_GBs": round(wtotal / ws["p50"] / 1e6, 2),
+                                   "native_ms": round(wsn["p50"], 2),
+                                   "ratio_vs_native": round(wsn["p50"] / ws["p50"], 3)}
 
     # Mixed contention: the wake-up list as 34 groups on stream A, each followed by the dependent
     # digest kernel over the group, while the 2048-block offload runs on stream B; 256 KiB chunks.
@@ -363,10 +375,250 @@ def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, p
     return res
 
 
+# ---------------------------------------------------------------- sweeps (--sweep NAME)
+def _sweep_env():
+    import torch
+
+    import paper_2512_16056_amd as mma
+    torch.cuda.set_device(0)
+    return mma, torch, native_lib(), torch.cuda.Stream()
+
+
+def _emit(**rec):
+    print(json.dumps(rec), flush=True)
+
+
+def sweep_sizes():
+    """Bandwidth against transfer size, both directions, 1 KiB to 8 GiB (the paper's microbenchmark
+    range): the default multipath configuration against one hipMemcpyAsync of the same buffers.
+    Median of HIP-event-bracketed runs on the launch stream."""
+    import ctypes
+    mma, torch, nat, st = _sweep_env()
+    mma.mma_init(0)
+    top = 8 << 30
+    h = mma.PinnedBuffer(top)
+    h.array[::4096] = 1
+    d = torch.empty(top, dtype=torch.uint8, device="cuda")
+    for n in [1 << k for k in range(10, 34)]:
+        reps = 50 if n <= (64 << 20) else (10 if n <= (1 << 30) else 3)
+        row = {"bytes": n}
+        for dr, name in ((0, "h2d"), (1, "d2h")):
+            dst, src = (d.data_ptr(), h.ptr) if dr == 0 else (h.ptr, d.data_ptr())
+            D, S, Z = (ctypes.c_void_p * 1)(dst), (ctypes.c_void_p * 1)(src), (ctypes.c_uint64 * 1)(n)
+            t_nat = _timed(st, lambda: nat.native_list(D, S, Z, 1, dr, ctypes.c_void_p(st.cuda_stream)), reps, 3)
+            t_mma = _timed(st, lambda: mma.mma_memcpy_async(dst, src, n, dr, st), reps, 3)
+            row[name] = {"mma_us": round(t_mma["p50"] * 1e3, 2), "native_us": round(t_nat["p50"] * 1e3, 2),
+                         "mma_GBs": round(n / t_mma["p50"] / 1e6, 2), "native_GBs": round(n / t_nat["p50"] / 1e6, 2),
+                         "ratio_vs_native": round(t_nat["p50"] / t_mma["p50"], 3)}
+        _emit(sweep="sizes", **row)
+    h.free()
+    mma.mma_finalize()
+
+
+def sweep_chunks():
+    """Chunk size x outstanding-queue depth on a 512 MiB copy (the paper's sensitivity study,
+    Section 5.3): H2D and D2H GB/s, default path set."""
+    mma, torch, nat, st = _sweep_env()
+    n = 512 << 20
+    mma.mma_init(0)
+    h = mma.PinnedBuffer(n)
+    h.array[::4096] = 1
+    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+    mma.mma_finalize()
+    for chunk in (256 << 10, 512 << 10, 1 << 20, 2 << 20, 4 << 20, 8 << 20, 16 << 20):
+        for depth in (1, 2, 4):
+            c = mma.mma_config_default()
+            c.chunk_bytes, c.queue_depth = chunk, depth
+            mma.mma_init(0, c)
+            r = {}
+            for dr, name in ((0, "h2d"), (1, "d2h")):
+                dst, src = (d, h) if dr == 0 else (h, d)
+                t = _timed(st, lambda: mma.mma_memcpy_async(dst, src, n, dr, st), 8, 2)["p50"]
+                r[name + "_GBs"] = round(n / t / 1e6, 2)
+            mma.mma_finalize()
+            _emit(sweep="chunks", bytes=n, chunk=chunk, queue_depth=depth, **r)
+    h.free()
+
+
+def sweep_contention():
+    """Pull-based path selection against fixed CU:SDMA splits decided at plan time (the paper's
+    static-split comparison, Section 5.1.2) on a 1024-block KV fetch (2 GiB), with background load
+    on another stream: none, bf16 GEMMs on every CU, HBM-bound device copies, or competing native
+    host->GPU copies on the same link. Median of 3."""
+    import workloads as W
+    mma, torch, nat, ts = _sweep_env()
+    s = W.KV64K
+    nblk = 1024
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    hs, gb = hs[:nblk], gb[:nblk]
+    mma.mma_init(0)
+    pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+    pool.array[::4096] = 7
+    mma.mma_finalize()
+    layers = [torch.empty(s.layer_bytes, dtype=torch.uint8, device="cuda") for _ in range(s.layers)]
+    lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                        s.host_num_slots)
+    bs = torch.cuda.Stream()
+    A = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    B = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    C = torch.empty(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    H = torch.empty(1 << 30, dtype=torch.uint8).pin_memory()
+    Dv = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    X = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    Y = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+
+    def background(kind):
+        with torch.cuda.stream(bs):
+            if kind == "gemm":
+                for _ in range(300):
+                    torch.matmul(A, B, out=C)
+            elif kind == "native_h2d":
+                for _ in range(12):
+                    Dv.copy_(H, non_blocking=True)
+            elif kind == "hbm":
+                for _ in range(60):
+                    X.copy_(Y)
+
+    CU = mma.MMA_PATH_CU
+    policies = [("pull", {}), ("static_cu0", dict(path_mask_h2d=0x3)),
+                ("static_cu33", dict(static_split=1, static_cu_percent=33)),
+                ("static_cu50", dict(static_split=1, static_cu_percent=50)),
+                ("static_cu67", dict(static_split=1, static_cu_percent=67)),
+                ("static_cu100", dict(path_mask_h2d=CU))]
+    for kind in ("none", "gemm", "hbm", "native_h2d"):
+        for policy, kv in policies:
+            c = mma.mma_config_default()
+            for k, v in kv.items():
+                setattr(c, k, v)
+            mma.mma_init(0, c)
+            mma.mma_kv_fetch(lay, pool, layers, hs, gb, ts)
+            torch.cuda.synchronize()
+            res = []
+            for _ in range(3):
+                mma.mma_reset_stats()
+                background(kind)
+                time.sleep(0.003)
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(ts)
+                mma.mma_kv_fetch(lay, pool, layers, hs, gb, ts)
+                b.record(ts)
+                torch.cuda.synchronize()
+                mma.mma_synchronize()
+                stt = mma.mma_get_stats()
+                res.append((a.elapsed_time(b), stt["path_bytes"][16], sum(stt["path_bytes"][:16]), stt))
+            mma.mma_finalize()
+            res.sort(key=lambda x: x[0])
+            ms, cu, sd, stt = res[1]
+            _emit(sweep="contention", background=kind, policy=policy, ms=round(ms, 2),
+                  GBs=round(nblk * s.slot_bytes / ms / 1e6, 2), cu_share=round(cu / max(1, cu + sd), 3),
+                  foreign_skips=stt["sdma_foreign_busy_skips"], backoffs=stt["sdma_congestion_backoffs"])
+    pool.free()
+
+
+def sweep_duplex():
+    """Both directions at once on one link: 1 GiB each way with raw probes (one hipMemcpyAsync per
+    direction, one SDMA engine per direction, zero-copy kernels), then a 2 GiB KV fetch concurrent
+    with a 2 GiB KV offload through the multipath path."""
+    import ctypes
+    import threading
+
+    import numpy as np
+
+    import workloads as W
+    mma, torch, nat, sa = _sweep_env()
+    sb = torch.cuda.Stream()
+    mma.mma_init(0)
+    n = 1 << 30
+    h1, h2 = mma.PinnedBuffer(n), mma.PinnedBuffer(n)
+    d1 = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d2 = torch.empty(n, dtype=torch.uint8, device="cuda")
+
+    def both(fa, fb, nbytes_a, nbytes_b, reps=3):
+        out = []
+        for _ in range(reps + 1):
+            torch.cuda.synchronize()
+            ea = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            eb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ea[0].record(sa)
+            eb[0].record(sb)
+            fa()
+            ea[1].record(sa)
+            fb()
+            eb[1].record(sb)
+            torch.cuda.synchronize()
+            out.append((ea[0].elapsed_time(ea[1]), eb[0].elapsed_time(eb[1])))
+        a = sorted(x[0] for x in out[1:])[reps // 2]
+        b = sorted(x[1] for x in out[1:])[reps // 2]
+        return {"h2d_ms": round(a, 3), "d2h_ms": round(b, 3),
+                "aggregate_GBs": round(nbytes_a / a / 1e6 + nbytes_b / b / 1e6, 2)}
+
+    D1, S1, Z = (ctypes.c_void_p * 1)(d1.data_ptr()), (ctypes.c_void_p * 1)(h1.ptr), (ctypes.c_uint64 * 1)(n)
+    D2, S2 = (ctypes.c_void_p * 1)(h2.ptr), (ctypes.c_void_p * 1)(d2.data_ptr())
+    _emit(sweep="duplex", case="hipMemcpyAsync h2d || d2h",
+          **both(lambda: nat.native_list(D1, S1, Z, 1, 0, ctypes.c_void_p(sa.cuda_stream)),
+                 lambda: nat.native_list(D2, S2, Z, 1, 1, ctypes.c_void_p(sb.cuda_stream)), n, n))
+    _emit(sweep="duplex", case="zero-copy kernel h2d || d2h (64 WGs each)",
+          **both(lambda: nat.native_zero_copy(d1.data_ptr(), h1.ptr, n, 0, 64, ctypes.c_void_p(sa.cuda_stream)),
+                 lambda: nat.native_zero_copy(h2.ptr, d2.data_ptr(), n, 1, 64, ctypes.c_void_p(sb.cuda_stream)),
+                 n, n))
+    res = []
+    for _ in range(4):
+        ns = [ctypes.c_uint64(0), ctypes.c_uint64(0)]
+        th = [threading.Thread(target=lambda: nat.native_sdma_all(d1.data_ptr(), h1.ptr, n, 0, 1, 0,
+                                                                  ctypes.byref(ns[0]))),
+              threading.Thread(target=lambda: nat.native_sdma_all(h2.ptr, d2.data_ptr(), n, 1, 2, 0,
+                                                                  ctypes.byref(ns[1])))]
+        for t in th:
+            t.start()
+        for t in th:
+            t.join()
+        res.append((ns[0].value / 1e6, ns[1].value / 1e6))
+    a = sorted(x[0] for x in res[1:])[1]
+    b = sorted(x[1] for x in res[1:])[1]
+    _emit(sweep="duplex", case="SDMA engine 0 h2d || engine 1 d2h (host-timed)", h2d_ms=round(a, 3),
+          d2h_ms=round(b, 3), aggregate_GBs=round(n / a / 1e6 + n / b / 1e6, 2))
+    h1.free()
+    h2.free()
+    mma.mma_finalize()
+
+    s = W.KV64K
+    nb = 1024
+    mma.mma_init(0)
+    pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+    mma.mma_finalize()
+    layers = [torch.zeros(s.layer_bytes, dtype=torch.uint8, device="cuda") for _ in range(s.layers)]
+    lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                        s.host_num_slots)
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    hs1, gb1 = hs[:nb].astype(np.int32), gb[:nb].astype(np.int32)
+    hs2, gb2 = hs[nb:2 * nb].astype(np.int32), gb[nb:2 * nb].astype(np.int32)
+    kvb = nb * s.slot_bytes
+    CU = mma.MMA_PATH_CU
+    for name, kv in (("default", {}), ("cu only", dict(path_mask_h2d=CU, path_mask_d2h=CU)),
+                     ("d2h without cu", dict(path_mask_d2h=0x3)),
+                     ("engine 0 h2d, engine 1 d2h, no cu", dict(path_mask_h2d=1, path_mask_d2h=2))):
+        c = mma.mma_config_default()
+        for k, v in kv.items():
+            setattr(c, k, v)
+        mma.mma_init(0, c)
+        r = both(lambda: mma.mma_kv_fetch(lay, pool, layers, hs1, gb1, sa),
+                 lambda: mma.mma_kv_offload(lay, pool, layers, gb2, hs2, sb), kvb, kvb)
+        _emit(sweep="duplex", case=f"multipath kv fetch || kv offload: {name}", **r,
+              failed=mma.mma_get_stats()["failed_transfers"])
+        mma.mma_finalize()
+    pool.free()
+
+
+SWEEPS = {"sizes": sweep_sizes, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex}
+
+
 def main():
     args = parse()
     if args.calib:
         calibration_kernels()
+        return
+    if args.sweep:
+        SWEEPS[args.sweep]()
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the multipath path here is the single-GPU share (SDMA engines + "

@@ -151,9 +151,16 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
   const uint64_t kstride = a.kv_kstride;
   __syncthreads();
 
+  // A self-contained launch carries every entry of the transfer in its
+  // arguments and no copy engine takes part: wave w of the grid copies entry w
+  // and signals it. No start signal, ring, exit count or wait is needed, and
+  // the done tags are the kernel's last accesses to the record.
+  const bool sc = a.self_contained != 0;
+  bool sc_taken = false;
+
   // 1. start signal (stream -> engine). Work that precedes this kernel in
   // stream order is complete and visible (dispatch acquire/release).
-  if (lane == 0) {
+  if (!sc && lane == 0) {
     const uint32_t first = __hip_atomic_fetch_add(&ds->arrived, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (first == 0) st_sys(&rec->h.started, a.seq);
   }
@@ -165,12 +172,19 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
   if (lane == 0) t_prog = wall_clock64();
   for (;;) {
     uint64_t x = 0;
-    if (lane == 0)
-      x = __hip_atomic_fetch_add(&ds->cursor, static_cast<uint64_t>(1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    x = lane_u64(x, 0);
+    if (sc) {
+      if (sc_taken) break;
+      sc_taken = true;
+      x = static_cast<uint64_t>(blockIdx.x) * kWavesPerWG + threadIdx.x / kWave;
+      if (x >= a.n_pre) break;
+    } else {
+      if (lane == 0)
+        x = __hip_atomic_fetch_add(&ds->cursor, static_cast<uint64_t>(1), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+      x = lane_u64(x, 0);
+    }
     const uint64_t expect = make_tag(a.seq, x);
     const uint64_t* ew = reinterpret_cast<const uint64_t*>(&rec->ring[x % kRingSize]);
-    if (a.self_contained && x >= a.n_pre) break;  // every entry came with the launch
     uint32_t state = 0;  // 1: entry ready, 3: watchdog
     uint64_t w1 = 0, w2 = 0, w3 = 0;
     if (x < a.n_pre) {  // first entries arrive with the launch: no PCIe round trip
@@ -246,6 +260,8 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
     }
   }
 
+  if (sc) return;
+
   // 3. leave; the last wave out waits for completion of all paths.
   if (lane == 0) {
     if (timed_out) {
@@ -254,9 +270,7 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
     const uint32_t n = __hip_atomic_fetch_add(&ds->exited, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (n == a.total_waves - 1) {
       uint32_t to = __hip_atomic_load(&ds->timed_out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      // Self-contained transfers have no copy-engine part: every wave has left,
-      // so every byte has been moved.
-      while (!to && !a.self_contained && ld_sys(&rec->h.complete) != a.seq) {
+      while (!to && ld_sys(&rec->h.complete) != a.seq) {
         const uint64_t now = wall_clock64();
         const uint64_t hb2 = ld_sys(&rec->h.heartbeat);
         if (hb2 != hb) {

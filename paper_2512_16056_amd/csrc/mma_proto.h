@@ -102,7 +102,7 @@ struct KernelArgs {
   uint32_t kv_layers;
   uint32_t n_pre;           // tickets [0, n_pre) are also given below: no first poll for them
   uint32_t self_contained;  // 1: the n_pre entries are the whole transfer and no copy engine takes
-                            // part: no ring polling, no wait for the host's `complete`
+                            // part: wave w copies entry w; no start signal, ring, exit count or wait
   uint32_t pad;
   uint64_t layer_ptr[kMaxLayers];
   uint64_t pre[kPrefill][3];  // words a, b, count|kind_p0 of the first ring entries

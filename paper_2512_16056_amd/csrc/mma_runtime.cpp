@@ -84,6 +84,7 @@ uint64_t env_u64(const char* name, uint64_t dflt) {
 }
 
 constexpr uint64_t KiB = 1024, MiB = 1024 * 1024;
+constexpr uint64_t kSmallSub = 16 * KiB;  // one wave register batch
 
 // ------------------------------------------------------------------ transfer
 enum class Kind : uint8_t { kLinear, kKvFetch, kKvOffload };
@@ -115,6 +116,7 @@ struct Transfer {
   uint32_t waves = 0;          // waves of the dummy-task kernel
   bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
   bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
+  uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
   int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
   uint8_t tdone[kRingSize];
   uint32_t cu_busy = 0;
@@ -350,7 +352,7 @@ class Engine {
                      uint32_t p0) {
     uint64_t per, ne;
     if ((kind & kEntryKindMask) == kEntryCopy) {
-      per = cfg_.sub;
+      per = x->sub;
     } else {
       // A wave's ring entry carries cu_sub_bytes of pieces across PCIe; for an
       // HBM-resident pool (latency ~1 us instead of several) a whole micro-task.
@@ -819,11 +821,9 @@ class Engine {
   }
 
   bool retire_ready(Transfer* x) {
+    // A self-contained kernel's done tags are its last accesses to the record.
+    if (x->self_contained) return x->n_done == x->tasks.size();
     if (ld_acq(&x->rec->h.released) != x->seq) return false;
-    if (x->self_contained && !x->completed) {  // its done tags may still be in flight
-      if (ld_acq(&x->rec->h.status) != 0) x->failed = true;
-      else return false;
-    }
     return x->sdma_refs == 0;
   }
 
@@ -1072,15 +1072,16 @@ mma_status_t device_range(const void* p, uint64_t bytes) {
 // Workgroups of the dummy-task kernel: one wave per ring entry that can be
 // outstanding at once (waves beyond that would only poll host memory, and
 // every poll is a PCIe read that competes with the payload).
-uint32_t grid_for(const Runtime* rt, Engine* e, uint64_t bytes, bool needs_cu, bool staged, bool pool_dev) {
+uint32_t grid_for(const Runtime* rt, Engine* e, uint64_t bytes, uint64_t sub, bool needs_cu, bool staged,
+                  bool pool_dev) {
   if (!needs_cu) return 1;
   if (pool_dev) {  // HBM gather/scatter: as many waves as there are micro-tasks, up to the limit
     const uint64_t tasks = (bytes + rt->cfg.chunk - 1) / rt->cfg.chunk;
     return static_cast<uint32_t>(std::max<uint64_t>(1, std::min<uint64_t>((tasks + 3) / 4, kMaxWorkgroups)));
   }
   const Config& c = rt->cfg;
-  const uint64_t total = (bytes + c.sub - 1) / c.sub;
-  const uint64_t per_task = (c.chunk + c.sub - 1) / c.sub;
+  const uint64_t total = (bytes + sub - 1) / sub;
+  const uint64_t per_task = (c.chunk + sub - 1) / sub;
   uint64_t inflight = e->cu_enabled() ? c.cu_depth * per_task : 0;
   if (staged) inflight += static_cast<uint64_t>(__builtin_popcount(e->sdma_mask())) * c.depth * per_task;
   uint64_t g = (std::max<uint64_t>(1, std::min(total, inflight)) + kWavesPerWG - 1) / kWavesPerWG;
@@ -1120,13 +1121,29 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   const bool needs_cu = e->cu_enabled() || staged ||
                         std::any_of(x->tasks.begin(), x->tasks.end(),
                                     [](const Task& t) { return (t.flags & kPlanCuOnly) != 0; });
-  const uint32_t grid = grid_for(rt, e, payload_bytes, needs_cu || x->pool_dev, staged, x->pool_dev);
+  // CU ring entries of a linear transfer are cu_sub_bytes. A transfer that can
+  // fit the launch's prefilled entries is cut finer (16 KiB steps, one wave
+  // register batch), so that more waves share it and it costs about one PCIe
+  // round trip.
+  x->sub = rt->cfg.sub;
+  if (!kv && payload_bytes <= kPrefill * rt->cfg.sub) {
+    const uint64_t per = (payload_bytes + kPrefill - 1) / kPrefill;
+    x->sub = std::min<uint64_t>(rt->cfg.sub, std::max<uint64_t>(kSmallSub, (per + kSmallSub - 1) / kSmallSub * kSmallSub));
+  }
+  uint32_t grid = grid_for(rt, e, payload_bytes, x->sub, needs_cu || x->pool_dev, staged, x->pool_dev);
   x->waves = grid * kWavesPerWG;
   e->prefill(x.get());
   const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
   // Everything fits the launch: all tasks were claimed by the CU prefill (so no
   // copy engine can take part) and all their entries are in the kernel args.
+  // One wave per entry; the engine treats the transfer as started.
   x->self_contained = !kv && x->n_claimed == x->tasks.size() && x->pushed == n_pre;
+  if (x->self_contained) {
+    grid = (n_pre + kWavesPerWG - 1) / kWavesPerWG;
+    x->waves = grid * kWavesPerWG;
+    x->started = true;
+    x->t_started = x->t_submit;
+  }
   static thread_local KernelArgs a;
   memset(&a, 0, offsetof(KernelArgs, layer_ptr));
   a.n_pre = n_pre;
