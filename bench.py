@@ -13,7 +13,7 @@ the same workload, native hipMemcpyAsync comparators, and the 64 MiB single-copy
 workload.
 
 Usage: python bench.py [--gpus 1] [--steps 10] [--warmup 2]
-       python bench.py --sweep sizes|chunks|contention|duplex   (JSON line per point)
+       python bench.py --sweep sizes|chunks|contention|duplex|paths|footprint  (JSON per point)
        python bench.py --calib                                  (counter-scaling kernels)
 """
 from __future__ import annotations
@@ -44,7 +44,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true", help="skip native comparators and the 64 MiB copy")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle timing window")
-    p.add_argument("--sweep", choices=["sizes", "chunks", "contention", "duplex"],
+    p.add_argument("--sweep", choices=["sizes", "chunks", "contention", "duplex", "paths", "footprint"],
                    help="instead of the benchmark, print one JSON line per point of a parameter sweep")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
@@ -609,7 +609,139 @@ def sweep_duplex():
     pool.free()
 
 
-SWEEPS = {"sizes": sweep_sizes, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex}
+def sweep_paths():
+    """Bandwidth against the path set (single-GPU analog of the paper's bandwidth-vs-paths study):
+    a 1 GiB copy each way and a 1024-block (2 GiB) KV fetch with one engine, both host-facing
+    engines, the CU path alone, and combinations; `all16` adds the xGMI-facing engines 2-15."""
+    import workloads as W
+    mma, torch, nat, st = _sweep_env()
+    n = 1 << 30
+    mma.mma_init(0)
+    h = mma.PinnedBuffer(n)
+    h.array[::4096] = 1
+    s = W.KV64K
+    pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+    mma.mma_finalize()
+    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+    layers = [torch.empty(s.layer_bytes, dtype=torch.uint8, device="cuda") for _ in range(s.layers)]
+    lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                        s.host_num_slots)
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    hs, gb = hs[:1024], gb[:1024]
+    CU = mma.MMA_PATH_CU
+    for name, mask in (("sdma0", 0x1), ("sdma1", 0x2), ("sdma0+1", 0x3), ("cu", CU), ("cu+sdma0", CU | 0x1),
+                       ("cu+sdma0+1", CU | 0x3), ("cu+all16", CU | 0xFFFF)):
+        c = mma.mma_config_default()
+        c.path_mask_h2d = c.path_mask_d2h = mask
+        mma.mma_init(0, c)
+        used = mma.mma_get_stats()
+        r = {}
+        for dr, nm in ((0, "h2d"), (1, "d2h")):
+            dst, src = (d, h) if dr == 0 else (h, d)
+            t = _timed(st, lambda: mma.mma_memcpy_async(dst, src, n, dr, st), 5, 1)["p50"]
+            r[nm + "_GBs"] = round(n / t / 1e6, 2)
+        t = _timed(st, lambda: mma.mma_kv_fetch(lay, pool, layers, hs, gb, st), 3, 1)["p50"]
+        r["kv_fetch_GBs"] = round(1024 * s.slot_bytes / t / 1e6, 2)
+        _emit(sweep="paths", paths=name, engines_h2d=hex(used["sdma_engines_h2d"]),
+              cu=bool(used["cu_path_enabled"]), **r)
+        mma.mma_finalize()
+    h.free()
+    pool.free()
+
+
+def sweep_footprint():
+    """Cost of the dummy task to other work on the GPU (the paper's claim that its spin kernel has
+    a negligible footprint): 200 bf16 8192^3 matmuls alone, then next to back-to-back 1 GiB
+    host->GPU copies: native hipMemcpyAsync, then multipath through the copy engines only (the dummy
+    task is then a single waiting wave) and through the default path set (16 CU-path workgroups)."""
+    mma, torch, nat, st = _sweep_env()
+    n = 1 << 30
+    mma.mma_init(0)
+    h = mma.PinnedBuffer(n)
+    mma.mma_finalize()
+    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+    gs = torch.cuda.Stream()
+    A = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    B = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    C = torch.empty(8192, 8192, device="cuda", dtype=torch.bfloat16)
+
+    def gemms():
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(gs):
+            a.record(gs)
+            for _ in range(200):
+                torch.matmul(A, B, out=C)
+            b.record(gs)
+        return a, b
+
+    torch.cuda.synchronize()
+    gemms()
+    torch.cuda.synchronize()
+    a, b = gemms()
+    torch.cuda.synchronize()
+    alone = a.elapsed_time(b)
+    _emit(sweep="footprint", case="gemm alone", gemm_ms=round(alone, 2))
+    import ctypes
+    mma.mma_init(0)
+    D, S, Z = (ctypes.c_void_p * 1)(d.data_ptr()), (ctypes.c_void_p * 1)(h.ptr), (ctypes.c_uint64 * 1)(n)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(12):
+        nat.native_list(D, S, Z, 1, 0, ctypes.c_void_p(st.cuda_stream))
+    e1.record(st)
+    a, b = gemms()
+    torch.cuda.synchronize()
+    g = a.elapsed_time(b)
+    _emit(sweep="footprint", case="native hipMemcpyAsync copies (no dummy task)", gemm_ms=round(g, 2),
+          gemm_slowdown=round(g / alone - 1, 4), copy_GBs=round(12 * n / e0.elapsed_time(e1) / 1e6, 2))
+    mma.mma_finalize()
+    # Reference points: one resident sleeping wave of any kernel, and a stream held by the command
+    # processor (an event wait on a stream blocked in a host function): no wave resident.
+    with torch.cuda.stream(st):
+        torch.cuda._sleep(int(2.4e9 * 0.3))
+    a, b = gemms()
+    torch.cuda.synchronize()
+    g = a.elapsed_time(b)
+    _emit(sweep="footprint", case="one resident sleeping wave (torch.cuda._sleep)", gemm_ms=round(g, 2),
+          gemm_slowdown=round(g / alone - 1, 4))
+    hip = ctypes.CDLL("libamdhip64.so")
+    cbt = ctypes.CFUNCTYPE(None, ctypes.c_void_p)
+    hip.hipLaunchHostFunc.argtypes = [ctypes.c_void_p, cbt, ctypes.c_void_p]
+    hold = cbt(lambda _: time.sleep(0.3))
+    s3 = torch.cuda.Stream()
+    hip.hipLaunchHostFunc(ctypes.c_void_p(s3.cuda_stream), hold, None)
+    e3 = torch.cuda.Event()
+    e3.record(s3)
+    st.wait_event(e3)
+    a, b = gemms()
+    torch.cuda.synchronize()
+    g = a.elapsed_time(b)
+    _emit(sweep="footprint", case="stream held by the command processor (event wait, no wave)", gemm_ms=round(g, 2),
+          gemm_slowdown=round(g / alone - 1, 4))
+    for name, mask in (("copy engines only (dummy task = 1 waiting wave)", 0x3),
+                       ("default paths (16 CU-path workgroups)", 0)):
+        c = mma.mma_config_default()
+        c.path_mask_h2d = mask
+        mma.mma_init(0, c)
+        mma.mma_memcpy_async(d, h, n, mma.MMA_H2D, st)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(12):
+            mma.mma_memcpy_async(d, h, n, mma.MMA_H2D, st)
+        e1.record(st)
+        a, b = gemms()
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        g = a.elapsed_time(b)
+        _emit(sweep="footprint", case=name, gemm_ms=round(g, 2), gemm_slowdown=round(g / alone - 1, 4),
+              copy_GBs=round(12 * n / e0.elapsed_time(e1) / 1e6, 2),
+              failed=mma.mma_get_stats()["failed_transfers"])
+        mma.mma_finalize()
+    h.free()
+
+SWEEPS = {"sizes": sweep_sizes, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
+          "paths": sweep_paths, "footprint": sweep_footprint}
 
 
 def main():
