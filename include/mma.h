@@ -210,6 +210,16 @@ mma_status_t mma_host_free(void* p);
  * MMA_ERR_TRANSFER_FAILED (sticky), MMA_ERR_NOT_INITIALIZED. */
 mma_status_t mma_memcpy_async(void* dst, const void* src, uint64_t bytes, int32_t dir, void* stream);
 
+/* Synchronous copy with hipMemcpy semantics (Section 3.2: the blocking call
+ * returns once the data has arrived). The copy is enqueued on the legacy
+ * default stream, so it is ordered after earlier work there and on other
+ * blocking streams; the call returns after that stream has passed it and the
+ * engine has retired it, so a failure of this copy is returned here
+ * (MMA_ERR_TRANSFER_FAILED). Arguments, pinning rules and other errors as for
+ * mma_memcpy_async; MMA_ERR_TIMEOUT if the transfer is not retired within the
+ * watchdog period plus 10 s. */
+mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir);
+
 /* One logical transfer of a list of n independent copies, e.g. all weight
  * tensors of a model (Section 2.1 model wake-up; Section 5.2.2). One dummy
  * task covers the whole list. Each tensor is chunked on its own; tensors below

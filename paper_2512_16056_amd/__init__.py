@@ -123,6 +123,7 @@ _SIGNATURES = {
     "mma_host_alloc": ([_U64, ctypes.POINTER(_P)], _S),
     "mma_host_free": ([_P], _S),
     "mma_memcpy_async": ([_P, _P, _U64, _I32, _P], _S),
+    "mma_memcpy": ([_P, _P, _U64, _I32], _S),
     "mma_weights_load": ([ctypes.POINTER(mma_copy_desc_t), _U64, _I32, _P], _S),
     "mma_kv_fetch": ([ctypes.POINTER(mma_kv_layout_t), _P, ctypes.POINTER(_P), ctypes.POINTER(_I32),
                       ctypes.POINTER(_I32), _U64, _P], _S),
@@ -256,6 +257,11 @@ class PinnedBuffer:
 # ------------------------------------------------------------------ transfers
 def mma_memcpy_async(dst, src, nbytes: int, direction: int, stream=None) -> None:
     _check(lib.mma_memcpy_async(_ptr(dst), _ptr(src), nbytes, direction, _stream(stream)), "mma_memcpy_async")
+
+
+def mma_memcpy(dst, src, nbytes: int, direction: int) -> None:
+    """Blocking copy on the legacy default stream; returns once the data has arrived."""
+    _check(lib.mma_memcpy(_ptr(dst), _ptr(src), nbytes, direction), "mma_memcpy")
 
 
 def mma_weights_load(copies: Sequence[Tuple[object, object, int]], direction: int, stream=None) -> None:

@@ -89,6 +89,15 @@ constexpr uint64_t kSmallSub = 16 * KiB;  // one wave register batch
 // ------------------------------------------------------------------ transfer
 enum class Kind : uint8_t { kLinear, kKvFetch, kKvOffload };
 
+// Completion slot of one synchronous call (mma_memcpy): set by the engine
+// thread when it retires the transfer.
+struct Waiter {
+  std::mutex mu;
+  std::condition_variable cv;
+  bool submitted = false, done = false, failed = false;
+};
+thread_local std::shared_ptr<Waiter> tl_waiter;
+
 struct Task {
   uint64_t src_dma, dst_dma;  // addresses used by the SDMA engines (linear kinds)
   uint64_t src_cu, dst_cu;    // addresses used by CU loads/stores (linear kinds)
@@ -117,6 +126,7 @@ struct Transfer {
   bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
   bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
   uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
+  std::shared_ptr<Waiter> waiter;  // set for synchronous calls
   int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
   uint8_t tdone[kRingSize];
   uint32_t cu_busy = 0;
@@ -883,6 +893,12 @@ class Engine {
         }
         st_->transfers += 1;
         if (g_trace.load(std::memory_order_relaxed)) record_trace(x, bad);
+        if (x->waiter) {
+          std::lock_guard<std::mutex> g(x->waiter->mu);
+          x->waiter->done = true;
+          x->waiter->failed = bad;
+          x->waiter->cv.notify_all();
+        }
         {
           std::lock_guard<std::mutex> g(mu_);
           free_recs_.push_back(x->rec_idx);
@@ -1144,6 +1160,10 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
     x->started = true;
     x->t_started = x->t_submit;
   }
+  if (tl_waiter) {
+    x->waiter = tl_waiter;
+    tl_waiter->submitted = true;
+  }
   static thread_local KernelArgs a;
   memset(&a, 0, offsetof(KernelArgs, layer_ptr));
   a.n_pre = n_pre;
@@ -1391,6 +1411,27 @@ mma_status_t mma_memcpy_async(void* dst, const void* src, uint64_t bytes, int32_
   if (!dst || !src) return fail(MMA_ERR_INVALID_ARG, "NULL pointer with bytes > 0");
   mma_copy_desc_t d{dst, src, bytes};
   return mma_weights_load(&d, 1, dir, stream);
+}
+
+mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir) {
+  std::shared_ptr<Waiter> w = std::make_shared<Waiter>();
+  tl_waiter = w;
+  mma_status_t s = mma_memcpy_async(dst, src, bytes, dir, nullptr);
+  tl_waiter.reset();
+  if (s) return s;
+  if (!w->submitted) return MMA_OK;  // nothing to move
+  {
+    DeviceGuard dg(g_rt->dev);
+    const hipError_t e = hipStreamSynchronize(nullptr);
+    if (e != hipSuccess) return fail(MMA_ERR_HIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
+  }
+  // The stream has passed the dummy task; the engine retires the transfer
+  // right after, which is when its outcome is final.
+  std::unique_lock<std::mutex> lk(w->mu);
+  const uint64_t ms = static_cast<uint64_t>(g_rt->cfg.watchdog_ms) + 10000;
+  if (!w->cv.wait_for(lk, std::chrono::milliseconds(ms), [&] { return w->done; }))
+    return fail(MMA_ERR_TIMEOUT, "copy not retired");
+  return w->failed ? fail(MMA_ERR_TRANSFER_FAILED, "the copy failed") : MMA_OK;
 }
 
 mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t dir, void* stream) {

@@ -219,3 +219,31 @@ def test_rejects_bad_arguments():
         mma.mma_weights_load([], mma.MMA_H2D)
         torch.cuda.synchronize()
         src.free()
+
+
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+def test_sync_memcpy(direction):
+    """mma_memcpy returns only once the data has arrived, ordered after earlier work on the default
+    stream: a producer kernel on the default stream writes the source right before a D2H copy."""
+    with session("both", chunk_bytes=1 << 20):
+        for n in (0, 1, 4095, 1 << 20, (9 << 20) + 5):
+            src_np = np.ascontiguousarray(W.uniform_bytes(33, direction, n, n))
+            if direction == mma.MMA_H2D:
+                src = mma.PinnedBuffer(n)
+                src.array[:] = src_np
+                dst = device_bytes(n, W.WEIGHT_POISON)
+                mma.mma_memcpy(dst, src, n, direction)
+                got = to_host(dst)[:n]  # synchronising read; the copy itself already returned
+            else:
+                src = device_bytes(n, 0)
+                dev = device_bytes(n, 0)
+                if n:
+                    src[:n].copy_(torch.from_numpy(src_np.copy()))
+                    torch.cuda.synchronize()
+                    dev[:n].copy_(src[:n])  # producer on the default stream, not synchronised
+                dst = mma.PinnedBuffer(n)
+                dst.array[:] = W.WEIGHT_POISON
+                mma.mma_memcpy(dst, dev, n, direction)
+                got = dst.array[:n].copy()  # no synchronisation: mma_memcpy must have finished
+            assert np.array_equal(got, src_np), n
+        mma.mma_synchronize()

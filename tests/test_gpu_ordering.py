@@ -149,3 +149,58 @@ def test_kv_fetch_then_dependent_kernel():
             want = okv.kv_fetch_layer(pv, poison, l, s.layers, hs, gb)
             assert int(outs[l].cpu().numpy().view(np.uint64)[0]) == odigest.digest(want), l
         mma.mma_synchronize()
+
+
+def test_concurrent_submitters():
+    """Four host threads, each with its own stream, submit interleaved H2D copies, D2H copies and
+    tensor lists of mixed sizes (self-contained, CU+SDMA and SDMA-merged ones) at the same time;
+    each transfer is followed on its stream by the dependent digest kernel. Every destination and
+    every digest must equal the oracle's (submissions are serialised inside the library; streams
+    are independent)."""
+    from concurrent.futures import ThreadPoolExecutor
+    sizes = [12345, 1 << 20, (3 << 20) + 17, 9 << 20, 64 << 10]
+    with session("both", chunk_bytes=1 << 20):
+        def worker(tid):
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):  # torch's own allocations and fills go on this stream too
+                return _submitter(tid, stream)
+
+        def _submitter(tid, stream):
+            results = []
+            for rep in range(3):
+                for k, n in enumerate(sizes):
+                    src_np = np.ascontiguousarray(W.uniform_bytes(40 + tid, rep, k, n))
+                    h = mma.PinnedBuffer(n)
+                    h.array[:] = src_np
+                    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+                    out = torch.zeros(1, dtype=torch.int64, device="cuda")
+                    back = mma.PinnedBuffer(n)
+                    back.array[:] = W.WEIGHT_POISON
+                    half = n // 2
+                    if (rep + k) % 2:
+                        mma.mma_memcpy_async(d, h, n, mma.MMA_H2D, stream)
+                    else:
+                        mma.mma_weights_load([(d.data_ptr(), h.ptr, half), (d.data_ptr() + half, h.ptr + half, n - half)],
+                                             mma.MMA_H2D, stream)
+                    mma.mma_digest_u32(d, n, out, stream)
+                    mma.mma_memcpy_async(back, d, n, mma.MMA_D2H, stream)
+                    results.append((src_np, h, d, out, back))
+            stream.synchronize()
+            bad = []
+            for i, (src_np, h, d, out, back) in enumerate(results):
+                if not np.array_equal(back.array, src_np):
+                    bad.append(("d2h", i))
+                if int(out.cpu().numpy().view(np.uint64)[0]) != odigest.digest(src_np):
+                    bad.append(("digest", i))
+                h.free()
+                back.free()
+            return bad
+
+        with ThreadPoolExecutor(4) as ex:
+            bad = [b for r in ex.map(worker, range(4)) for b in r]
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+    assert not bad, bad[:10]
+    assert st["failed_transfers"] == 0
+    log(f"  transfers={st['transfers']} sdma commands={st['sdma_commands']} cu bytes={st['path_bytes'][16]}")
