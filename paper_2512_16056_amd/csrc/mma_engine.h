@@ -1,0 +1,1107 @@
+// Host engine of the multipath copy path, independent of the GPU runtime: the
+// transfer bookkeeping, the per-direction engine thread (Section 4: separate
+// H2D and D2H engine instances) with its path selector, copy-engine slots and
+// CU-ring protocol, and the micro-task builders. Everything that touches the
+// GPU goes through Backend: ROCr/HIP in mma_runtime.cpp, host threads in the
+// CPU engine test.
+//
+// Roles, mapped to the paper's components (Section 3, Figure "Overview"):
+//   Task Manager   -> make_*_transfer (plans from mma_plan.cpp) + per-task
+//                     completion accounting (Engine::task_done).
+//   Path Selector  -> Engine::pull_cu / Engine::pull_sdma: every path pulls the
+//                     next micro-task only while its outstanding queue has
+//                     room (backpressure).
+//   Task Launcher  -> Backend::copy (SDMA) and ring entries consumed by the
+//                     dummy-task kernel (CU path).
+//   Sync Engine    -> the record's started/complete words (Engine::advance).
+#ifndef MMA_ENGINE_H_
+#define MMA_ENGINE_H_
+
+#include <pthread.h>
+#include <time.h>
+
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstdarg>
+#include <cstddef>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <deque>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/mma.h"
+#include "mma_plan.h"
+#include "mma_proto.h"
+
+namespace mma {
+
+// ------------------------------------------------------------------ utilities
+inline thread_local std::string t_err;  // message of the calling thread's last error
+
+inline mma_status_t fail(mma_status_t s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return s;
+}
+
+inline uint64_t now_ns() {
+  timespec ts;
+  clock_gettime(CLOCK_MONOTONIC, &ts);
+  return static_cast<uint64_t>(ts.tv_sec) * 1000000000ull + ts.tv_nsec;
+}
+
+template <class T>
+inline T ld_acq(const T* p) {
+  return __atomic_load_n(p, __ATOMIC_ACQUIRE);
+}
+template <class T>
+inline void st_rel(T* p, T v) {
+  __atomic_store_n(p, v, __ATOMIC_RELEASE);
+}
+
+inline void cpu_relax() { __builtin_ia32_pause(); }
+
+inline uint64_t env_u64(const char* name, uint64_t dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  return strtoull(v, nullptr, 0);
+}
+
+constexpr uint64_t KiB = 1024, MiB = 1024 * 1024;
+constexpr uint64_t kSmallSub = 16 * KiB;  // one wave register batch
+
+// ------------------------------------------------------------------ transfer
+enum class Kind : uint8_t { kLinear, kKvFetch, kKvOffload };
+
+// Completion slot of one synchronous call (mma_memcpy): set by the engine
+// thread when it retires the transfer.
+struct Waiter {
+  std::mutex mu;
+  std::condition_variable cv;
+  bool submitted = false, done = false, failed = false;
+};
+inline thread_local std::shared_ptr<Waiter> tl_waiter;
+
+struct Task {
+  uint64_t src_dma, dst_dma;  // addresses used by the SDMA engines (linear kinds)
+  uint64_t src_cu, dst_cu;    // addresses used by CU loads/stores (linear kinds)
+  uint64_t host_dma, host_cu; // KV: contiguous host range of the task's pieces
+  uint64_t bytes;             // linear: bytes; KV: pieces
+  uint64_t blk;               // KV: GPU block index
+  uint32_t p0;                // KV: first piece (2*l + k)
+  uint32_t flags;             // kPlanCuOnly
+};
+
+struct Transfer {
+  uint64_t seq = 0;
+  int dir = MMA_H2D;
+  Kind kind = Kind::kLinear;
+  uint32_t rec_idx = 0;
+  Record* rec = nullptr;      // host address of the shared record
+  std::vector<Task> tasks;
+  std::vector<uint8_t> claimed;
+  std::vector<uint32_t> left;  // CU entries outstanding per CU-path task
+  size_t cur_cu = 0, cur_sdma = 0, n_claimed = 0, n_done = 0;
+  uint64_t piece = 0;
+  bool sdma_ok = true;         // SDMA may carry this transfer's tasks
+  // CU ring bookkeeping
+  uint64_t pushed = 0, done_upto = 0;
+  uint32_t waves = 0;          // waves of the dummy-task kernel
+  bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
+  bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
+  uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
+  std::shared_ptr<Waiter> waiter;  // set for synchronous calls
+  int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
+  uint8_t tdone[kRingSize];
+  uint32_t cu_busy = 0;
+  bool cu_full = false;
+  int sdma_cu_pending = 0;     // SDMA slots that will still append ring entries
+  int sdma_refs = 0;           // SDMA slots referencing this transfer
+  uint64_t heartbeat = 0;
+  uint64_t bytes = 0;          // payload bytes
+  // trace timestamps (CLOCK_MONOTONIC ns)
+  uint64_t t_api = 0, t_submit = 0, t_started = 0, t_first_sdma = 0, t_last_task = 0, t_complete = 0;
+  uint64_t path_tasks[MMA_NUM_PATHS] = {};
+  bool started = false, closed = false, completed = false, failed = false, ignored = false, aborting = false;
+  bool progress = false;
+};
+
+// ------------------------------------------------------------------ engine
+enum SlotState : int {
+  kFree = 0,
+  kCopy,            // SDMA: linear micro-task in flight
+  kH2DStage,        // SDMA: host slot range -> staging
+  kH2DScatterPush,  // waiting for ring room to append the staging scatter
+  kH2DScatter,      // CU: staging -> paged layout
+  kD2HGatherPush,   // waiting for ring room to append the staging gather
+  kD2HGather,       // CU: paged layout -> staging
+  kD2HStage,        // SDMA: staging -> host slot range
+};
+
+struct SdmaSlot {
+  uint64_t sig = 0;       // copy-engine completion signal (Backend handle)
+  int state = kFree;
+  Transfer* x = nullptr;
+  size_t task = 0, task_end = 0;  // micro-tasks [task, task_end) carried by this slot's command
+  uint64_t count = 0;     // their total: bytes (linear) or pieces (KV, one block's run)
+  uint32_t left = 0;      // ring entries outstanding
+  uint64_t staging = 0;   // device address of this slot's staging buffer
+  int path = 0;
+  uint64_t t_submit = 0;  // current copy-engine command: submission time and size
+  uint64_t op_bytes = 0;
+};
+
+struct SdmaPath {
+  int engine = 0;
+  std::vector<int> slots;  // slot ids
+  int busy = 0;
+  bool full = false;
+  bool congested = false;  // a command is long overdue: pull nothing more until the engine drains
+};
+
+struct Config {
+  uint64_t chunk, fallback, small, sub;
+  uint32_t depth, cu_depth, backoff, cu_wgs, watchdog_ms;
+  uint32_t mask[2];
+  uint32_t static_split, static_cu_percent;
+  uint32_t merge;       // max micro-tasks per copy-engine command
+};
+
+struct Stats {
+  std::atomic<uint64_t> transfers{0}, failed{0}, staging_bytes{0}, submit_failures{0}, busy_ns{0};
+  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0}, sdma_commands{0};
+  std::atomic<uint64_t> path_bytes[MMA_NUM_PATHS], path_tasks[MMA_NUM_PATHS];
+  Stats() {
+    for (auto& v : path_bytes) v = 0;
+    for (auto& v : path_tasks) v = 0;
+  }
+  void reset() {
+    transfers = failed = staging_bytes = submit_failures = busy_ns = foreign_skips = congestion_backoffs = 0;
+    sdma_commands = 0;
+    for (auto& v : path_bytes) v = 0;
+    for (auto& v : path_tasks) v = 0;
+  }
+};
+
+inline std::atomic<int> g_sticky{0};
+
+// Per-transfer trace records (MMA_TRACE=1 or mma_trace_enable): a bounded ring.
+inline std::atomic<int> g_trace{0};
+inline std::mutex g_trace_mu;
+inline std::deque<mma_trace_rec_t> g_trace_buf;
+constexpr size_t kTraceCap = 65536;
+inline std::atomic<uint64_t> g_fault_stall_us{0}, g_fault_submit_fail{0}, g_fault_ignore{0};
+
+// What the engine needs from the GPU side. The product backend is ROCr/HIP
+// (mma_runtime.cpp); a CPU test backend emulates it with host threads.
+struct Backend {
+  virtual ~Backend() = default;
+  // Coherent host memory that the device reads and writes (the records);
+  // *dev receives the device's address for it.
+  virtual mma_status_t alloc_records(uint64_t bytes, void** host, void** dev) = 0;
+  virtual void free_records(void* host) = 0;
+  // Zero-filled device memory (per-record device state).
+  virtual mma_status_t alloc_device_state(uint64_t bytes, void** dev) = 0;
+  virtual void free_device_state(void* dev) = 0;
+  virtual mma_status_t alloc_host_scratch(uint64_t bytes, void** host) = 0;
+  virtual void free_host_scratch(void* host) = 0;
+  // Completion signals of copy-engine commands: set to 1 before a command,
+  // 0 when it has landed, negative if it failed.
+  virtual bool signal_create(uint64_t* sig) = 0;
+  virtual void signal_destroy(uint64_t sig) = 0;
+  virtual void signal_store(uint64_t sig, int64_t value) = 0;
+  virtual int64_t signal_load(uint64_t sig) = 0;
+  // One command on copy engine `engine`; false if it was not accepted.
+  virtual bool copy(int engine, void* dst, bool dst_on_device, const void* src, bool src_on_device,
+                    uint64_t bytes, uint64_t sig) = 0;
+  // Bit e set: copy engine e has no command queued for direction `dir`.
+  virtual uint32_t engines_idle(int dir) = 0;
+};
+
+// KV geometry handed to the kernel: piece size, K-to-V stride in a layer
+// tensor, and the layer tensors' addresses.
+struct KvGeom {
+  uint64_t piece = 0, kstride = 0;
+  uint32_t layers = 0;
+  uint64_t layer_ptr[kMaxLayers];
+};
+
+class Engine {
+ public:
+  Engine(int dir, const Config& cfg, Backend* be, Stats* st) : dir_(dir), cfg_(cfg), be_(be), st_(st) {}
+  ~Engine() { shutdown(); }
+
+  mma_status_t init(uint32_t sdma_mask, uint64_t stage_bytes, void* staging_base) {
+    void *h = nullptr, *d = nullptr;
+    mma_status_t rc = be_->alloc_records(sizeof(Record) * kRecords, &h, &d);
+    if (rc != MMA_OK) return rc;
+    recs_ = static_cast<Record*>(h);
+    recs_dev_ = static_cast<Record*>(d);
+    memset(recs_, 0, sizeof(Record) * kRecords);
+    if ((rc = be_->alloc_device_state(sizeof(DevState) * kRecords, &d)) != MMA_OK) return rc;
+    ds_ = static_cast<DevState*>(d);
+    for (uint32_t i = 0; i < kRecords; ++i) free_recs_.push_back(i);
+    stage_bytes_ = stage_bytes;
+    uint8_t* stage = static_cast<uint8_t*>(staging_base);
+    for (int eng = 0; eng < MMA_MAX_SDMA; ++eng) {
+      if (!(sdma_mask & (1u << eng))) continue;
+      SdmaPath p;
+      p.engine = eng;
+      for (uint32_t d = 0; d < cfg_.depth; ++d) {
+        SdmaSlot s;
+        if (!be_->signal_create(&s.sig)) return fail(MMA_ERR_HSA, "copy-engine signal creation failed");
+        s.staging = stage ? reinterpret_cast<uint64_t>(stage) : 0;
+        if (stage) stage += stage_bytes;
+        s.path = static_cast<int>(paths_.size());
+        p.slots.push_back(static_cast<int>(slots_.size()));
+        slots_.push_back(s);
+      }
+      paths_.push_back(p);
+    }
+    mma_status_t w = warm_up();
+    if (w != MMA_OK) return w;
+    thread_ = std::thread([this] { loop(); });
+    return MMA_OK;
+  }
+
+  // The first command on an engine makes ROCr create that engine's queue
+  // (milliseconds); do it here rather than inside the first transfer.
+  mma_status_t warm_up() {
+    if (paths_.empty()) return MMA_OK;
+    void* host = nullptr;
+    mma_status_t rc = be_->alloc_host_scratch(4096, &host);
+    if (rc != MMA_OK) return rc;
+    for (auto& path : paths_) {
+      SdmaSlot& s = slots_[path.slots[0]];
+      be_->signal_store(s.sig, 1);
+      void* stage = reinterpret_cast<void*>(s.staging);
+      const bool ok = dir_ == MMA_H2D ? be_->copy(path.engine, stage, true, host, false, 4096, s.sig)
+                                      : be_->copy(path.engine, host, false, stage, true, 4096, s.sig);
+      if (!ok) {
+        rc = fail(MMA_ERR_HSA, "SDMA engine %d rejected a warm-up copy", path.engine);
+        break;
+      }
+      const uint64_t t0 = now_ns();
+      int64_t v;
+      while ((v = be_->signal_load(s.sig)) > 0 && now_ns() - t0 < 10000000000ull) cpu_relax();
+      if (v != 0) {  // still in flight or failed: leave the engine out rather than reuse its signal
+        rc = fail(MMA_ERR_HSA, "SDMA engine %d did not complete a warm-up copy", path.engine);
+        break;
+      }
+    }
+    be_->free_host_scratch(host);
+    return rc;
+  }
+
+  void shutdown() {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      if (!thread_.joinable()) return;
+      stop_ = true;
+      stop_flag_ = true;
+    }
+    cv_.notify_all();
+    thread_.join();
+    for (auto& s : slots_) be_->signal_destroy(s.sig);
+    slots_.clear();
+    if (ds_) be_->free_device_state(ds_);
+    if (recs_) be_->free_records(recs_);
+    ds_ = nullptr;
+    recs_ = nullptr;
+  }
+
+  pthread_t native_handle() { return thread_.native_handle(); }
+  uint32_t sdma_mask() const {
+    uint32_t m = 0;
+    for (auto& p : paths_) m |= 1u << p.engine;
+    return m;
+  }
+  bool cu_enabled() const { return (cfg_.mask[dir_] & MMA_PATH_CU) != 0; }
+  bool has_sdma() const { return !paths_.empty(); }
+  uint64_t stage_bytes() const { return stage_bytes_; }
+
+  // Blocks until a record is free (or the timeout passes). Called with the
+  // submission mutex held, never by the engine thread.
+  bool acquire_record(Transfer* x, uint64_t timeout_ms) {
+    std::unique_lock<std::mutex> lk(mu_);
+    if (!cv_done_.wait_for(lk, std::chrono::milliseconds(timeout_ms), [&] { return !free_recs_.empty(); }))
+      return false;
+    x->rec_idx = free_recs_.front();
+    free_recs_.pop_front();
+    x->rec = &recs_[x->rec_idx];
+    return true;
+  }
+  void release_record_unused(Transfer* x) {
+    std::lock_guard<std::mutex> g(mu_);
+    free_recs_.push_back(x->rec_idx);
+    cv_done_.notify_all();
+  }
+  Record* rec_dev(uint32_t i) const { return recs_dev_ + i; }
+  DevState* ds(uint32_t i) const { return ds_ + i; }
+
+  // CU path's first pulls, made before the transfer is handed to the engine
+  // thread (no concurrent access to x yet): the dummy task's workers can start
+  // copying as soon as the stream reaches them, without a host round trip.
+  void prefill(Transfer* x) { pull_cu(x); }
+
+  // Workgroups of the dummy-task kernel: one wave per ring entry that can be
+  // outstanding at once (waves beyond that would only poll host memory, and
+  // every poll is a PCIe read that competes with the payload).
+  uint32_t grid_for(uint64_t bytes, uint64_t sub, bool needs_cu, bool staged, bool pool_dev) const {
+    if (!needs_cu) return 1;
+    if (pool_dev) {  // HBM gather/scatter: as many waves as there are micro-tasks, up to the limit
+      const uint64_t tasks = (bytes + cfg_.chunk - 1) / cfg_.chunk;
+      return static_cast<uint32_t>(std::max<uint64_t>(1, std::min<uint64_t>((tasks + 3) / 4, kMaxWorkgroups)));
+    }
+    const uint64_t total = (bytes + sub - 1) / sub;
+    const uint64_t per_task = (cfg_.chunk + sub - 1) / sub;
+    uint64_t inflight = cu_enabled() ? cfg_.cu_depth * per_task : 0;
+    if (staged) inflight += static_cast<uint64_t>(__builtin_popcount(sdma_mask())) * cfg_.depth * per_task;
+    uint64_t g = (std::max<uint64_t>(1, std::min(total, inflight)) + kWavesPerWG - 1) / kWavesPerWG;
+    g = std::max<uint64_t>(1, std::min<uint64_t>(g, cfg_.cu_wgs));
+    return static_cast<uint32_t>(g);
+  }
+
+  // Everything between the plan and the kernel launch, for a transfer that
+  // holds a record: epoch, static-split flags, CU entry size, grid, the CU
+  // path's first pulls, the self-contained decision and the kernel
+  // arguments. Returns the grid in workgroups.
+  uint32_t prepare(Transfer* x, uint64_t seq, uint64_t payload_bytes, const KvGeom* kv, uint64_t watchdog_ticks,
+                   KernelArgs& a) {
+    x->claimed.assign(x->tasks.size(), 0);
+    x->left.assign(x->tasks.size(), 0);
+    x->seq = seq;
+    x->t_submit = now_ns();
+    x->bytes = payload_bytes;
+    Record* r = x->rec;
+    r->h.seq = x->seq;
+    r->h.status = 0;
+    __atomic_thread_fence(__ATOMIC_RELEASE);
+    if (cfg_.static_split && has_sdma() && x->sdma_ok) {
+      for (size_t i = 0; i < x->tasks.size(); ++i) {
+        uint32_t& f = x->tasks[i].flags;
+        if (f & kPlanCuOnly) continue;
+        f |= static_cu_task(i, cfg_.static_cu_percent) ? kPlanCuOnly : kPlanSdmaOnly;
+      }
+    }
+    const bool staged = x->kind != Kind::kLinear && has_sdma() && x->sdma_ok;
+    const bool needs_cu = cu_enabled() || staged ||
+                          std::any_of(x->tasks.begin(), x->tasks.end(),
+                                      [](const Task& t) { return (t.flags & kPlanCuOnly) != 0; });
+    // CU ring entries of a linear transfer are cu_sub_bytes. A transfer that can
+    // fit the launch's prefilled entries is cut finer (16 KiB steps, one wave
+    // register batch), so that more waves share it and it costs about one PCIe
+    // round trip.
+    x->sub = cfg_.sub;
+    if (!kv && payload_bytes <= kPrefill * cfg_.sub) {
+      const uint64_t per = (payload_bytes + kPrefill - 1) / kPrefill;
+      x->sub = std::min<uint64_t>(cfg_.sub,
+                                  std::max<uint64_t>(kSmallSub, (per + kSmallSub - 1) / kSmallSub * kSmallSub));
+    }
+    uint32_t grid = grid_for(payload_bytes, x->sub, needs_cu || x->pool_dev, staged, x->pool_dev);
+    x->waves = grid * kWavesPerWG;
+    prefill(x);
+    const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
+    // Everything fits the launch: all tasks were claimed by the CU prefill (so no
+    // copy engine can take part) and all their entries are in the kernel args.
+    // One wave per entry; the engine treats the transfer as started.
+    x->self_contained = !kv && x->n_claimed == x->tasks.size() && x->pushed == n_pre;
+    if (x->self_contained) {
+      grid = (n_pre + kWavesPerWG - 1) / kWavesPerWG;
+      x->waves = grid * kWavesPerWG;
+      x->started = true;
+      x->t_started = x->t_submit;
+    }
+    memset(&a, 0, offsetof(KernelArgs, layer_ptr));
+    a.n_pre = n_pre;
+    a.self_contained = x->self_contained ? 1u : 0u;
+    for (uint32_t t = 0; t < n_pre; ++t) {
+      const CuEntry& en = r->ring[t];
+      a.pre[t][0] = en.a;
+      a.pre[t][1] = en.b;
+      a.pre[t][2] = static_cast<uint64_t>(en.count) | (static_cast<uint64_t>(en.kind_p0) << 32);
+    }
+    if (kv) {
+      a.kv_piece_bytes = kv->piece;
+      a.kv_kstride = kv->kstride;
+      a.kv_layers = kv->layers;
+      memcpy(a.layer_ptr, kv->layer_ptr, sizeof(uint64_t) * kv->layers);
+    }
+    a.rec = rec_dev(x->rec_idx);
+    a.ds = ds(x->rec_idx);
+    a.seq = x->seq;
+    a.watchdog_ticks = watchdog_ticks;
+    a.total_waves = grid * kWavesPerWG;
+    a.release_each = x->dir == MMA_D2H ? 1u : 0u;
+    return grid;
+  }
+
+  void submit(std::unique_ptr<Transfer> x) {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      incoming_.push_back(std::move(x));
+      ++inflight_;
+    }
+    n_incoming_.fetch_add(1, std::memory_order_release);
+    cv_.notify_all();
+  }
+
+  bool wait_idle(uint64_t timeout_ms) {
+    std::unique_lock<std::mutex> lk(mu_);
+    return cv_done_.wait_for(lk, std::chrono::milliseconds(timeout_ms), [&] { return inflight_ == 0; });
+  }
+
+ private:
+  // ---------------------------------------------------------------- ring
+  // Append the ring entries of one unit of work. `a` is the contiguous side
+  // (linear: source; KV: host or staging range), `b` the other side (linear:
+  // destination; KV: GPU block). Returns the number appended, 0 if no room.
+  uint32_t push_unit(Transfer* x, int32_t owner, uint32_t kind, uint64_t a, uint64_t b, uint64_t count,
+                     uint32_t p0) {
+    uint64_t per, ne;
+    if ((kind & kEntryKindMask) == kEntryCopy) {
+      per = x->sub;
+    } else {
+      // A wave's ring entry carries cu_sub_bytes of pieces across PCIe; for an
+      // HBM-resident pool (latency ~1 us instead of several) a whole micro-task.
+      per = x->pool_dev ? count : std::max<uint64_t>(1, cfg_.sub / x->piece);
+    }
+    ne = (count + per - 1) / per;
+    // Keep one slot per wave free for the end markers written at close.
+    if (x->pushed + ne - x->done_upto > kRingSize - x->waves) return 0;
+    Record* r = x->rec;
+    for (uint64_t k = 0; k < ne; ++k) {
+      const uint64_t t = x->pushed++;
+      const uint32_t slot = static_cast<uint32_t>(t % kRingSize);
+      const uint64_t c = std::min(per, count - k * per);
+      CuEntry* e = &r->ring[slot];
+      if ((kind & kEntryKindMask) == kEntryCopy) {
+        e->a = a + k * per;
+        e->b = b + k * per;
+        e->kind_p0 = kind;
+      } else {
+        e->a = a + k * per * x->piece;
+        e->b = b;
+        e->kind_p0 = kind | ((p0 + static_cast<uint32_t>(k * per)) << 8);
+      }
+      e->count = static_cast<uint32_t>(c);
+      x->owner[slot] = owner;
+      x->tdone[slot] = 0;
+      // Payload first, then both tags: a reader that sees either tag also sees
+      // the payload written before it (x86 stores are ordered).
+      const uint64_t tag = make_tag(x->seq, t);
+      st_rel(&e->tag0, tag);
+      st_rel(&e->tag1, tag);
+    }
+    return static_cast<uint32_t>(ne);
+  }
+
+  void task_done(Transfer* x, size_t i, int path_stat) {
+    ++x->n_done;
+    ++x->path_tasks[path_stat];
+    if (x->n_done == x->tasks.size()) x->t_last_task = now_ns();
+    const Task& t = x->tasks[i];
+    const uint64_t bytes = x->kind == Kind::kLinear ? t.bytes : t.bytes * x->piece;
+    st_->path_bytes[path_stat] += bytes;
+    st_->path_tasks[path_stat] += 1;
+    x->progress = true;
+  }
+
+  bool scan_cu(Transfer* x) {
+    bool p = false;
+    Record* r = x->rec;
+    for (uint64_t t = x->done_upto; t < x->pushed; ++t) {
+      const uint32_t slot = static_cast<uint32_t>(t % kRingSize);
+      if (x->tdone[slot]) continue;
+      if (ld_acq(&r->done[slot]) != make_tag(x->seq, t)) continue;
+      x->tdone[slot] = 1;
+      p = true;
+      const int32_t own = x->owner[slot];
+      if (own >= 0) {
+        if (--x->left[own] == 0) {
+          --x->cu_busy;
+          task_done(x, static_cast<size_t>(own), MMA_NUM_PATHS - 1);
+        }
+      } else {
+        // Staging step of an SDMA slot; ignore it if the slot was released
+        // early because the transfer was aborted.
+        SdmaSlot& s = slots_[-own - 1];
+        if (s.x == x && (s.state == kH2DScatter || s.state == kD2HGather) && --s.left == 0) sdma_cu_stage_done(s);
+      }
+    }
+    while (x->done_upto < x->pushed && x->tdone[x->done_upto % kRingSize]) ++x->done_upto;
+    return p;
+  }
+
+  // ---------------------------------------------------------------- CU path
+  bool pull_cu(Transfer* x) {
+    if (x->failed || x->ignored || x->aborting) return false;
+    const bool any = cu_enabled() || x->pool_dev;
+    // An HBM-resident pool keeps every wave busy: two micro-tasks per wave outstanding.
+    const uint32_t depth = x->pool_dev ? 2 * x->waves : cfg_.cu_depth;
+    bool p = false;
+    while (true) {
+      if (x->cu_busy >= depth) x->cu_full = true;
+      if (x->cu_full && x->cu_busy < std::min(cfg_.backoff, depth)) x->cu_full = false;
+      if (x->cu_full) break;
+      size_t i = x->cur_cu;
+      while (i < x->tasks.size() && (x->claimed[i] || (x->tasks[i].flags & kPlanSdmaOnly) ||
+                                      (!any && !(x->tasks[i].flags & kPlanCuOnly))))
+        ++i;
+      x->cur_cu = i;
+      if (i >= x->tasks.size()) break;
+      const Task& t = x->tasks[i];
+      uint32_t ne;
+      if (x->kind == Kind::kLinear)
+        ne = push_unit(x, static_cast<int32_t>(i), kEntryCopy, t.src_cu, t.dst_cu, t.bytes, 0);
+      else
+        ne = push_unit(x, static_cast<int32_t>(i), x->kind == Kind::kKvFetch ? kEntryToPaged : kEntryFromPaged,
+                       t.host_cu, t.blk, t.bytes, t.p0);
+      if (!ne) break;
+      x->claimed[i] = 1;
+      ++x->n_claimed;
+      x->left[i] = ne;
+      ++x->cu_busy;
+      p = true;
+    }
+    return p;
+  }
+
+  // ---------------------------------------------------------------- SDMA path
+  bool sdma_copy(SdmaSlot& s, void* dst, bool dst_on_device, const void* src, bool src_on_device, uint64_t bytes) {
+    uint64_t f = g_fault_submit_fail.load();
+    while (f > 0) {
+      if (g_fault_submit_fail.compare_exchange_weak(f, f - 1)) return false;
+    }
+    if (!s.x->t_first_sdma) s.x->t_first_sdma = now_ns();
+    s.t_submit = now_ns();
+    s.op_bytes = bytes;
+    be_->signal_store(s.sig, 1);
+    const bool ok = be_->copy(paths_[s.path].engine, dst, dst_on_device, src, src_on_device, bytes, s.sig);
+    if (ok) st_->sdma_commands += 1;
+    return ok;
+  }
+
+  void free_slot(SdmaSlot& s) {
+    SdmaPath& p = paths_[s.path];
+    --p.busy;
+    if (s.x) --s.x->sdma_refs;
+    s.state = kFree;
+    s.x = nullptr;
+  }
+
+  // The staged CU step of an SDMA-carried KV micro-task has landed.
+  void slot_tasks_done(SdmaSlot& s) {
+    for (size_t i = s.task; i < s.task_end; ++i) task_done(s.x, i, paths_[s.path].engine);
+  }
+
+  void sdma_cu_stage_done(SdmaSlot& s) {
+    Transfer* x = s.x;
+    const Task& t = x->tasks[s.task];
+    if (s.state == kH2DScatter) {
+      st_->staging_bytes += s.count * x->piece;
+      slot_tasks_done(s);
+      free_slot(s);
+    } else if (s.state == kD2HGather) {
+      st_->staging_bytes += s.count * x->piece;
+      if (sdma_copy(s, reinterpret_cast<void*>(t.host_dma), false, reinterpret_cast<void*>(s.staging), true,
+                    s.count * x->piece)) {
+        s.state = kD2HStage;
+      } else {
+        // The gathered bytes are in staging and cannot reach the host this way.
+        st_->submit_failures += 1;
+        x->failed = true;
+        slot_tasks_done(s);
+        free_slot(s);
+      }
+    }
+  }
+
+  bool try_push_stage(SdmaSlot& s) {
+    Transfer* x = s.x;
+    const Task& t = x->tasks[s.task];
+    const int32_t own = -1 - static_cast<int32_t>(&s - slots_.data());
+    uint32_t ne;
+    if (s.state == kH2DScatterPush)
+      ne = push_unit(x, own, kEntryToPaged | kEntryAcquire, s.staging, t.blk, s.count, t.p0);
+    else
+      ne = push_unit(x, own, kEntryFromPaged, s.staging, t.blk, s.count, t.p0);
+    if (!ne) return false;
+    s.left = ne;
+    s.state = s.state == kH2DScatterPush ? kH2DScatter : kD2HGather;
+    --x->sdma_cu_pending;
+    return true;
+  }
+
+  bool poll_sdma() {
+    bool p = false;
+    for (auto& s : slots_) {
+      if (s.state == kH2DScatterPush || s.state == kD2HGatherPush) {
+        if (s.x->aborting) {
+          --s.x->sdma_cu_pending;
+          free_slot(s);
+          p = true;
+        } else if (try_push_stage(s)) {
+          s.x->progress = true;
+          p = true;
+        }
+        continue;
+      }
+      if (s.state == kH2DScatter || s.state == kD2HGather) {
+        if (s.x->aborting) {  // the kernel has left; its ring entries will never run
+          free_slot(s);
+          p = true;
+        }
+        continue;
+      }
+      if (s.state != kCopy && s.state != kH2DStage && s.state != kD2HStage) continue;
+      const int64_t v = be_->signal_load(s.sig);
+      if (v > 0) continue;
+      p = true;
+      Transfer* x = s.x;
+      x->progress = true;
+      if (v < 0) {
+        x->failed = true;
+        if (s.state == kH2DStage) --x->sdma_cu_pending;
+        slot_tasks_done(s);
+        free_slot(s);
+        continue;
+      }
+      if (s.state == kCopy || s.state == kD2HStage) {
+        slot_tasks_done(s);
+        free_slot(s);
+      } else {  // kH2DStage landed: scatter it on the CU side
+        s.state = kH2DScatterPush;
+        if (x->aborting) {
+          --x->sdma_cu_pending;
+          free_slot(s);
+        } else {
+          try_push_stage(s);
+        }
+      }
+    }
+    return p;
+  }
+
+  // Next SDMA-eligible task of the oldest started transfer.
+  bool next_sdma_task(Transfer*& out, size_t& idx) {
+    for (auto& up : active_) {
+      Transfer* x = up.get();
+      if (!x->started || x->failed || x->ignored || x->aborting || !x->sdma_ok) continue;
+      size_t i = x->cur_sdma;
+      while (i < x->tasks.size() && (x->claimed[i] || (x->tasks[i].flags & kPlanCuOnly))) ++i;
+      x->cur_sdma = i;
+      if (i < x->tasks.size()) {
+        out = x;
+        idx = i;
+        return true;
+      }
+    }
+    return false;
+  }
+
+  // One copy-engine command carries the claimed micro-task i and the unclaimed
+  // ones that directly follow it in both address spaces (a linear run, or one
+  // KV block's consecutive pieces that fit the staging slot), up to cfg.merge.
+  // Each ROCr copy command costs about 8 us of engine time (measured), so at
+  // small chunk sizes one command per micro-task would cap an engine well
+  // below the link.
+  size_t merge_run(const Transfer* x, size_t i) const {
+    const bool sdma_only = (x->tasks[i].flags & kPlanSdmaOnly) != 0;
+    uint64_t total = x->tasks[i].bytes;
+    size_t j = i + 1;
+    for (; j < x->tasks.size() && j - i < cfg_.merge; ++j) {
+      const Task& a = x->tasks[j - 1];
+      const Task& b = x->tasks[j];
+      if (x->claimed[j] || (b.flags & kPlanCuOnly) || ((b.flags & kPlanSdmaOnly) != 0) != sdma_only) break;
+      if (x->kind == Kind::kLinear) {
+        if (b.src_dma != a.src_dma + a.bytes || b.dst_dma != a.dst_dma + a.bytes) break;
+      } else {
+        if (b.blk != a.blk || b.p0 != a.p0 + a.bytes || b.host_dma != a.host_dma + a.bytes * x->piece ||
+            (total + b.bytes) * x->piece > stage_bytes_)
+          break;
+      }
+      total += b.bytes;
+    }
+    return j;
+  }
+
+  // A copy-engine command is overdue when it has been in flight for four times
+  // what its size needs at 50 GB/s, plus 0.5 ms of slack.
+  bool overdue(const SdmaPath& path, uint64_t now) const {
+    for (int id : path.slots) {
+      const SdmaSlot& s = slots_[id];
+      if (s.state != kCopy && s.state != kH2DStage && s.state != kD2HStage) continue;
+      if (now - s.t_submit > 4 * s.op_bytes / 50 + 500000) return true;  // ns
+    }
+    return false;
+  }
+
+  // Paths that can make progress take work (Section 2.2; Section 3.4 contention
+  // back-off). ROCr keeps one in-order command queue per engine per process, so
+  // a command placed behind another component's copies waits for all of them:
+  // an engine that ROCr reports in use while none of our commands is on it is
+  // busy with foreign work and is skipped; an engine with an overdue command is
+  // backed off until it drains.
+  bool pull_sdma() {
+    bool p = false;
+    const uint32_t bo = std::min(cfg_.backoff, cfg_.depth);
+    uint32_t free_mask = 0;
+    bool have_mask = false;
+    const uint64_t now = now_ns();
+    for (size_t k = 0; k < paths_.size(); ++k) {
+      SdmaPath& path = paths_[(k + rr_) % paths_.size()];
+      if (path.congested) {
+        if (path.busy > 0) continue;
+        path.congested = false;
+      } else if (path.busy > 0 && overdue(path, now)) {
+        path.congested = true;
+        st_->congestion_backoffs += 1;
+        continue;
+      }
+      if (path.busy == 0) {
+        if (!have_mask) {
+          free_mask = be_->engines_idle(dir_);
+          have_mask = true;
+        }
+        if (!(free_mask & (1u << path.engine))) {
+          st_->foreign_skips += 1;
+          continue;
+        }
+      }
+      for (int id : path.slots) {
+        if (path.busy >= static_cast<int>(cfg_.depth)) path.full = true;
+        if (path.full && path.busy < static_cast<int>(bo)) path.full = false;
+        if (path.full) break;
+        SdmaSlot& s = slots_[id];
+        if (s.state != kFree) continue;
+        Transfer* x;
+        size_t i;
+        if (!next_sdma_task(x, i)) return p;
+        const Task& t = x->tasks[i];
+        const size_t end = merge_run(x, i);
+        for (size_t j = i; j < end; ++j) x->claimed[j] = 1;
+        x->n_claimed += end - i;
+        s.x = x;
+        s.task = i;
+        s.task_end = end;
+        s.count = 0;
+        for (size_t j = i; j < end; ++j) s.count += x->tasks[j].bytes;
+        ++path.busy;
+        ++x->sdma_refs;
+        bool ok = true;
+        if (x->kind == Kind::kLinear) {
+          const bool h2d = dir_ == MMA_H2D;
+          ok = sdma_copy(s, reinterpret_cast<void*>(t.dst_dma), h2d, reinterpret_cast<void*>(t.src_dma), !h2d,
+                         s.count);
+          s.state = kCopy;
+        } else if (x->kind == Kind::kKvFetch) {
+          ok = sdma_copy(s, reinterpret_cast<void*>(s.staging), true, reinterpret_cast<void*>(t.host_dma), false,
+                         s.count * x->piece);
+          s.state = kH2DStage;
+          if (ok) ++x->sdma_cu_pending;
+        } else {
+          s.state = kD2HGatherPush;
+          ++x->sdma_cu_pending;
+          try_push_stage(s);
+        }
+        if (!ok) {
+          // Re-route: the tasks go back to the queue, CU path only.
+          st_->submit_failures += 1;
+          for (size_t j = i; j < end; ++j) {
+            x->claimed[j] = 0;
+            x->tasks[j].flags = (x->tasks[j].flags & ~kPlanSdmaOnly) | kPlanCuOnly;
+          }
+          x->n_claimed -= end - i;
+          x->cur_cu = std::min(x->cur_cu, i);
+          free_slot(s);
+        }
+        x->progress = true;
+        p = true;
+      }
+    }
+    ++rr_;
+    return p;
+  }
+
+  // ---------------------------------------------------------------- lifecycle
+  bool advance(Transfer* x) {
+    Record* r = x->rec;
+    bool p = false;
+    if (!x->started && !x->ignored && ld_acq(&r->h.started) == x->seq) {
+      if (g_fault_ignore.load()) {
+        x->ignored = true;
+      } else {
+        x->started = true;
+        x->t_started = now_ns();
+        const uint64_t us = g_fault_stall_us.load();
+        if (us) std::this_thread::sleep_for(std::chrono::microseconds(us));
+      }
+      p = true;
+    }
+    // The kernel leaves the record only after `complete`, or on its watchdog
+    // (a self-contained kernel leaves when its own entries are done).
+    if (!x->completed && !x->aborting && !x->self_contained && ld_acq(&r->h.released) == x->seq) {
+      x->aborting = true;
+      x->failed = true;
+      p = true;
+    }
+    if (x->ignored || x->aborting) return p;
+    // Closed: no more ring entries will ever be appended (every task claimed,
+    // or the transfer failed, and no SDMA slot still has a staging step to append).
+    if (!x->closed && (x->n_claimed == x->tasks.size() || x->failed) && x->sdma_cu_pending == 0) {
+      st_rel(&r->h.cu_total, x->pushed);
+      st_rel(&r->h.closed, x->seq);
+      close_ring(x);
+      x->closed = true;
+      p = true;
+    }
+    // Complete: every micro-task landed -- or, after a failure, everything in
+    // flight has drained, so the stream can be released (the error is sticky).
+    // The kernel's last wave starts waiting only after every wave has left the
+    // ring, i.e. after every appended entry is done; so once the ring is closed,
+    // only copy-engine operations can still be outstanding, and `complete` can
+    // be published as soon as none is -- without waiting to see the last CU
+    // done flags.
+    const bool drained = x->failed && x->closed && x->sdma_refs == 0 && x->cu_busy == 0;
+    const bool landed = !x->failed && x->closed && sdma_ops_in_flight(x) == 0;
+    if (!x->completed && (x->n_done == x->tasks.size() || landed || drained)) {
+      st_rel(&r->h.complete, x->seq);
+      x->t_complete = now_ns();
+      x->completed = true;
+      p = true;
+    }
+    return p;
+  }
+
+  void record_trace(const Transfer* x, bool bad) {
+    mma_trace_rec_t t{};
+    t.seq = x->seq;
+    t.dir = x->dir;
+    t.kind = static_cast<int32_t>(x->kind);
+    t.bytes = x->bytes;
+    t.tasks = x->tasks.size();
+    t.t_api_ns = x->t_api;
+    t.t_submit_ns = x->t_submit;
+    t.t_started_ns = x->t_started;
+    t.t_first_sdma_ns = x->t_first_sdma;
+    t.t_last_task_ns = x->t_last_task;
+    t.t_complete_ns = x->t_complete;
+    t.t_retire_ns = now_ns();
+    for (int i = 0; i < MMA_NUM_PATHS; ++i) t.path_tasks[i] = x->path_tasks[i];
+    t.failed = bad ? 1 : 0;
+    std::lock_guard<std::mutex> g(g_trace_mu);
+    if (g_trace_buf.size() >= kTraceCap) g_trace_buf.pop_front();
+    g_trace_buf.push_back(t);
+  }
+
+  // Every wave holds at most one claim beyond the last real ticket, so the
+  // tickets [pushed, pushed + waves) cover all of them: an end marker in each
+  // lets every waiting wave leave on its next poll. The slots are free because
+  // push_unit keeps `waves` slots in reserve.
+  void close_ring(Transfer* x) {
+    Record* r = x->rec;
+    for (uint64_t t = x->pushed; t < x->pushed + x->waves; ++t) {
+      CuEntry* e = &r->ring[t % kRingSize];
+      e->a = 0;
+      e->b = 0;
+      e->count = 0;
+      e->kind_p0 = kEntryEnd;
+      const uint64_t tag = make_tag(x->seq, t);
+      st_rel(&e->tag0, tag);
+      st_rel(&e->tag1, tag);
+    }
+  }
+
+  // SDMA slots of x whose remaining work includes a copy-engine operation (a
+  // slot in kH2DScatter only waits for ring entries, which the kernel finishes).
+  int sdma_ops_in_flight(const Transfer* x) const {
+    int n = 0;
+    for (const auto& s : slots_)
+      if (s.x == x && s.state != kFree && s.state != kH2DScatter) ++n;
+    return n;
+  }
+
+  bool retire_ready(Transfer* x) {
+    // A self-contained kernel's done tags are its last accesses to the record.
+    if (x->self_contained) return x->n_done == x->tasks.size();
+    if (ld_acq(&x->rec->h.released) != x->seq) return false;
+    return x->sdma_refs == 0;
+  }
+
+  void loop() {
+    uint64_t idle_spins = 0, busy_t0 = 0;
+    for (;;) {
+      if (active_.empty()) {
+        if (busy_t0) {
+          st_->busy_ns += now_ns() - busy_t0;
+          busy_t0 = 0;
+        }
+        // Back-to-back transfers are common: poll for a while before sleeping,
+        // so that a new transfer does not pay a thread wake-up.
+        const uint64_t t0 = now_ns();
+        while (n_incoming_.load(std::memory_order_acquire) == 0 && !stop_flag_.load(std::memory_order_relaxed) &&
+               now_ns() - t0 < kIdleSpinNs)
+          cpu_relax();
+        std::unique_lock<std::mutex> lk(mu_);
+        while (incoming_.empty()) {
+          if (stop_) return;
+          cv_.wait_for(lk, std::chrono::milliseconds(100));
+        }
+      }
+      if (n_incoming_.load(std::memory_order_acquire) > 0) {
+        std::lock_guard<std::mutex> g(mu_);
+        while (!incoming_.empty()) {
+          active_.push_back(std::move(incoming_.front()));
+          incoming_.pop_front();
+          n_incoming_.fetch_sub(1, std::memory_order_relaxed);
+        }
+      }
+      if (!busy_t0) busy_t0 = now_ns();
+      bool p = false;
+      for (auto& up : active_) {
+        up->progress = false;
+        p |= advance(up.get());
+        p |= scan_cu(up.get());
+      }
+      p |= poll_sdma();
+      for (auto& up : active_) p |= pull_cu(up.get());
+      p |= pull_sdma();
+      for (auto& up : active_) {
+        p |= advance(up.get());
+        if (up->progress && !up->ignored) st_rel(&up->rec->h.heartbeat, ++up->heartbeat);
+      }
+      // Retire transfers whose kernel has left the record.
+      for (size_t i = 0; i < active_.size();) {
+        Transfer* x = active_[i].get();
+        if (!retire_ready(x)) {
+          ++i;
+          continue;
+        }
+        const bool bad = x->failed || x->ignored || ld_acq(&x->rec->h.status) != 0;
+        if (bad) {
+          g_sticky.store(1);
+          st_->failed += 1;
+        }
+        st_->transfers += 1;
+        if (g_trace.load(std::memory_order_relaxed)) record_trace(x, bad);
+        if (x->waiter) {
+          std::lock_guard<std::mutex> g(x->waiter->mu);
+          x->waiter->done = true;
+          x->waiter->failed = bad;
+          x->waiter->cv.notify_all();
+        }
+        {
+          std::lock_guard<std::mutex> g(mu_);
+          free_recs_.push_back(x->rec_idx);
+          --inflight_;
+        }
+        cv_done_.notify_all();
+        active_.erase(active_.begin() + static_cast<long>(i));
+        p = true;
+      }
+      if (p) {
+        idle_spins = 0;
+      } else if (++idle_spins < 20000) {
+        cpu_relax();
+      } else {
+        std::this_thread::sleep_for(std::chrono::microseconds(20));
+      }
+    }
+  }
+
+  int dir_;
+  Config cfg_;
+  Backend* be_;
+  Stats* st_;
+  Record* recs_ = nullptr;
+  Record* recs_dev_ = nullptr;
+  DevState* ds_ = nullptr;
+  std::vector<SdmaSlot> slots_;
+  std::vector<SdmaPath> paths_;
+  uint64_t stage_bytes_ = 0;
+  size_t rr_ = 0;
+  std::mutex mu_;
+  std::condition_variable cv_, cv_done_;
+  std::deque<std::unique_ptr<Transfer>> incoming_;
+  std::vector<std::unique_ptr<Transfer>> active_;  // engine thread only
+  std::deque<uint32_t> free_recs_;
+  uint64_t inflight_ = 0;
+  bool stop_ = false;
+  std::atomic<bool> stop_flag_{false};
+  std::atomic<uint64_t> n_incoming_{0};
+  static constexpr uint64_t kIdleSpinNs = 2000000;  // 2 ms
+  std::thread thread_;
+};
+
+// Micro-tasks of a tensor list (Section 3.4 Task Manager). sizes[i] is tensor
+// i's byte count; src_cu/dst_cu are the addresses the CU path uses for it.
+inline std::unique_ptr<Transfer> make_list_transfer(int dir, const mma_copy_desc_t* list, uint64_t n,
+                                                    const uint64_t* sizes, const uint64_t* src_cu,
+                                                    const uint64_t* dst_cu, const Config& c) {
+  std::vector<PlanItem> plan;
+  plan_list(sizes, n, c.chunk, c.fallback, c.small, plan);
+  std::unique_ptr<Transfer> x(new Transfer());
+  x->dir = dir;
+  x->kind = Kind::kLinear;
+  x->tasks.reserve(plan.size());
+  for (const PlanItem& p : plan) {
+    const mma_copy_desc_t& d = list[p.item];
+    Task t{};
+    t.src_dma = reinterpret_cast<uint64_t>(d.src) + p.offset;
+    t.dst_dma = reinterpret_cast<uint64_t>(d.dst) + p.offset;
+    t.src_cu = src_cu[p.item] + p.offset;
+    t.dst_cu = dst_cu[p.item] + p.offset;
+    t.bytes = p.bytes;
+    t.flags = p.flags;
+    x->tasks.push_back(t);
+  }
+  return x;
+}
+
+// Micro-tasks of a block-table KV transfer: host slot host_slots[i] <-> GPU
+// block gpu_blocks[i], ppb pieces of `piece` bytes per block. `host` is the
+// pool's address for the copy engines, pool_cu the CU path's.
+inline std::unique_ptr<Transfer> make_kv_transfer(int dir, uint64_t piece, uint32_t ppb, uint64_t host,
+                                                  uint64_t pool_cu, bool pool_dev, bool sdma_ok,
+                                                  const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n,
+                                                  const Config& c) {
+  std::vector<PlanItem> plan;
+  plan_kv(n, ppb, piece, c.chunk, plan);
+  std::unique_ptr<Transfer> x(new Transfer());
+  x->dir = dir;
+  x->kind = dir == MMA_H2D ? Kind::kKvFetch : Kind::kKvOffload;
+  x->piece = piece;
+  x->pool_dev = pool_dev;
+  x->sdma_ok = sdma_ok;
+  x->tasks.reserve(plan.size());
+  const uint64_t slot_bytes = piece * ppb;
+  for (const PlanItem& p : plan) {
+    Task t{};
+    const uint64_t off = static_cast<uint64_t>(host_slots[p.item]) * slot_bytes + p.offset * piece;
+    t.host_dma = host + off;
+    t.host_cu = pool_cu + off;
+    t.blk = static_cast<uint64_t>(gpu_blocks[p.item]);
+    t.p0 = static_cast<uint32_t>(p.offset);
+    t.bytes = p.bytes;
+    t.flags = sdma_ok ? 0u : kPlanCuOnly;
+    x->tasks.push_back(t);
+  }
+  return x;
+}
+
+
+}  // namespace mma
+
+#endif  // MMA_ENGINE_H_
