@@ -132,6 +132,7 @@ struct Transfer {
   uint64_t bytes = 0;          // payload bytes
   // trace timestamps (CLOCK_MONOTONIC ns)
   uint64_t t_api = 0, t_submit = 0, t_started = 0, t_first_sdma = 0, t_last_task = 0, t_complete = 0;
+  uint64_t t_released = 0;     // when the kernel was seen to release the record with tags still missing
   uint64_t path_tasks[MMA_NUM_PATHS] = {};
   bool started = false, closed = false, completed = false, failed = false, ignored = false, aborting = false;
   bool progress = false;
@@ -937,6 +938,18 @@ class Engine {
     // A self-contained kernel's done tags are its last accesses to the record.
     if (x->self_contained) return x->n_done == x->tasks.size();
     if (ld_acq(&x->rec->h.released) != x->seq) return false;
+    // Every wave wrote its done tags before the last one released the record,
+    // but `complete` may have been published before this thread saw them (the
+    // early completion once only CU entries remain): credit them now, so that
+    // per-path accounting is exact. Tags still missing after a grace period
+    // mean a broken protocol; the transfer is then reported as failed.
+    scan_cu(x);
+    if (x->n_done != x->tasks.size() && !x->failed) {
+      const uint64_t now = now_ns();
+      if (!x->t_released) x->t_released = now;
+      if (now - x->t_released < kTagGraceNs) return false;
+      x->failed = true;
+    }
     return x->sdma_refs == 0;
   }
 
@@ -1042,6 +1055,7 @@ class Engine {
   std::atomic<bool> stop_flag_{false};
   std::atomic<uint64_t> n_incoming_{0};
   static constexpr uint64_t kIdleSpinNs = 2000000;  // 2 ms
+  static constexpr uint64_t kTagGraceNs = 100000000;  // 100 ms
   std::thread thread_;
 };
 

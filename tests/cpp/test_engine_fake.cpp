@@ -1,0 +1,689 @@
+// CPU test of the host engine on fake paths (no GPU). The engine code under
+// test is the product's (mma_engine.h): planner output, path selector,
+// copy-engine slots with merging, CU-ring protocol, completion and retirement.
+// Only the GPU side is replaced:
+//   - FakeBackend: "copy engines" are host threads that run commands in order,
+//     each taking bytes / rate plus a fixed per-command cost, then memcpy and
+//     drop the command's signal to 0;
+//   - the dummy-task kernel is emulated by host threads ("waves") that follow
+//     the record protocol of mma_proto.h: claim tickets with an atomic cursor,
+//     wait for tagged ring entries, copy (at a per-wave rate), write done tags,
+//     and the last wave out waits for `complete`, resets the device state and
+//     releases the record;
+//   - "device memory" is host memory.
+// Scenarios: byte-exact results for copies, tensor lists and paged-KV fetch /
+// offload through staging; every micro-task retired exactly once; a slower
+// copy engine receives proportionally fewer micro-tasks; merged commands;
+// submit failures re-routed; two streams in flight; and pull-based selection
+// against the best fixed split at 1:1 and 2:1 path-rate ratios (the paper's
+// static-split comparison, Section 5.1.2). Built twice by the pytest wrapper:
+// optimised, and with ThreadSanitizer (correctness scenarios only).
+//
+// Usage: test_engine_fake [--no-timing]
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <deque>
+#include <functional>
+#include <mutex>
+#include <random>
+#include <thread>
+#include <vector>
+
+#include "mma_engine.h"
+
+using namespace mma;
+
+namespace {
+
+int g_failures = 0;
+#define CHECK(cond, ...)                                          \
+  do {                                                            \
+    if (!(cond)) {                                                \
+      ++g_failures;                                               \
+      std::printf("FAIL %s:%d: %s -- ", __FILE__, __LINE__, #cond); \
+      std::printf(__VA_ARGS__);                                   \
+      std::printf("\n");                                          \
+    }                                                             \
+  } while (0)
+
+void sleep_ns(uint64_t ns) {
+  if (ns) std::this_thread::sleep_for(std::chrono::nanoseconds(ns));
+}
+
+// ------------------------------------------------------------ fake backend
+class FakeBackend final : public Backend {
+ public:
+  // rate in bytes per microsecond (1000 = 1 GB/s), cost per command in ns
+  FakeBackend(std::vector<double> rates, uint64_t cmd_ns) : cmd_ns_(cmd_ns) {
+    for (double r : rates) {
+      auto e = std::make_unique<Eng>();
+      e->rate = r;
+      engines_.push_back(std::move(e));
+    }
+    for (auto& e : engines_) {
+      Eng* p = e.get();
+      p->th = std::thread([this, p] { run(p); });
+    }
+  }
+  ~FakeBackend() override {
+    for (auto& e : engines_) {
+      {
+        std::lock_guard<std::mutex> g(e->mu);
+        e->stop = true;
+      }
+      e->cv.notify_all();
+      e->th.join();
+    }
+  }
+  mma_status_t alloc_records(uint64_t bytes, void** host, void** dev) override {
+    *host = *dev = std::aligned_alloc(4096, (bytes + 4095) & ~4095ull);
+    return *host ? MMA_OK : MMA_ERR_NO_MEMORY;
+  }
+  void free_records(void* host) override { std::free(host); }
+  mma_status_t alloc_device_state(uint64_t bytes, void** dev) override {
+    *dev = std::aligned_alloc(128, (bytes + 127) & ~127ull);
+    if (!*dev) return MMA_ERR_NO_MEMORY;
+    std::memset(*dev, 0, bytes);
+    return MMA_OK;
+  }
+  void free_device_state(void* dev) override { std::free(dev); }
+  mma_status_t alloc_host_scratch(uint64_t bytes, void** host) override {
+    *host = std::calloc(1, bytes);
+    return *host ? MMA_OK : MMA_ERR_NO_MEMORY;
+  }
+  void free_host_scratch(void* host) override { std::free(host); }
+  bool signal_create(uint64_t* sig) override {
+    *sig = reinterpret_cast<uint64_t>(new std::atomic<int64_t>(1));
+    return true;
+  }
+  void signal_destroy(uint64_t sig) override { delete reinterpret_cast<std::atomic<int64_t>*>(sig); }
+  void signal_store(uint64_t sig, int64_t v) override {
+    reinterpret_cast<std::atomic<int64_t>*>(sig)->store(v, std::memory_order_release);
+  }
+  int64_t signal_load(uint64_t sig) override {
+    return reinterpret_cast<std::atomic<int64_t>*>(sig)->load(std::memory_order_acquire);
+  }
+  bool copy(int engine, void* dst, bool, const void* src, bool, uint64_t bytes, uint64_t sig) override {
+    if (engine < 0 || engine >= static_cast<int>(engines_.size())) return false;
+    Eng* e = engines_[engine].get();
+    {
+      std::lock_guard<std::mutex> g(e->mu);
+      e->q.push_back({dst, src, bytes, sig});
+      e->pending.fetch_add(1);
+      e->bytes_total += bytes;
+      e->commands += 1;
+    }
+    e->cv.notify_all();
+    return true;
+  }
+  uint32_t engines_idle(int) override {
+    uint32_t m = 0;
+    for (size_t i = 0; i < engines_.size(); ++i)
+      if (engines_[i]->pending.load() == 0) m |= 1u << i;
+    return m;
+  }
+  uint64_t engine_bytes(int e) {
+    std::lock_guard<std::mutex> g(engines_[e]->mu);
+    return engines_[e]->bytes_total;
+  }
+
+ private:
+  struct Cmd {
+    void* dst;
+    const void* src;
+    uint64_t bytes;
+    uint64_t sig;
+  };
+  struct Eng {
+    double rate = 1000;
+    std::mutex mu;
+    std::condition_variable cv;
+    std::deque<Cmd> q;
+    std::atomic<int> pending{0};
+    uint64_t bytes_total = 0, commands = 0;
+    bool stop = false;
+    std::thread th;
+  };
+  void run(Eng* e) {
+    for (;;) {
+      Cmd c;
+      {
+        std::unique_lock<std::mutex> lk(e->mu);
+        e->cv.wait(lk, [&] { return e->stop || !e->q.empty(); });
+        if (e->q.empty()) return;
+        c = e->q.front();
+        e->q.pop_front();
+      }
+      sleep_ns(cmd_ns_ + static_cast<uint64_t>(c.bytes * 1000.0 / e->rate));
+      std::memcpy(c.dst, c.src, c.bytes);
+      e->pending.fetch_sub(1);
+      signal_store(c.sig, 0);
+    }
+  }
+  uint64_t cmd_ns_;
+  std::vector<std::unique_ptr<Eng>> engines_;
+};
+
+// ------------------------------------------------------------ fake GPU stream
+// Kernels on one stream run one after another; each is a set of wave threads.
+class FakeStream {
+ public:
+  FakeStream() : th_([this] { run(); }) {}
+  ~FakeStream() {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    th_.join();
+  }
+  void launch(std::function<void()> k) {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      q_.push_back(std::move(k));
+      ++pending_;
+    }
+    cv_.notify_all();
+  }
+  void synchronize() {
+    std::unique_lock<std::mutex> lk(mu_);
+    done_cv_.wait(lk, [&] { return pending_ == 0; });
+  }
+
+ private:
+  void run() {
+    for (;;) {
+      std::function<void()> k;
+      {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_.wait(lk, [&] { return stop_ || !q_.empty(); });
+        if (q_.empty()) return;
+        k = std::move(q_.front());
+        q_.pop_front();
+      }
+      k();
+      {
+        std::lock_guard<std::mutex> g(mu_);
+        --pending_;
+      }
+      done_cv_.notify_all();
+    }
+  }
+  std::mutex mu_;
+  std::condition_variable cv_, done_cv_;
+  std::deque<std::function<void()>> q_;
+  int pending_ = 0;
+  bool stop_ = false;
+  std::thread th_;
+};
+
+// One wave of the dummy-task kernel, following the record protocol.
+template <class T>
+T aload(const T* p) {
+  return __atomic_load_n(p, __ATOMIC_ACQUIRE);
+}
+template <class T>
+void astore(T* p, T v) {
+  __atomic_store_n(p, v, __ATOMIC_RELEASE);
+}
+
+void copy_at_rate(void* dst, const void* src, uint64_t n, double wave_rate) {
+  sleep_ns(static_cast<uint64_t>(n * 1000.0 / wave_rate));
+  std::memcpy(dst, src, n);
+}
+
+void wave(const KernelArgs a, uint32_t w, double wave_rate) {
+  Record* rec = a.rec;
+  DevState* ds = a.ds;
+  const bool sc = a.self_contained != 0;
+  if (!sc && __atomic_fetch_add(&ds->arrived, 1u, __ATOMIC_RELAXED) == 0) astore(&rec->h.started, a.seq);
+  uint64_t hb = 0, t_prog = now_ns();
+  bool timed_out = false, sc_taken = false;
+  for (;;) {
+    uint64_t x;
+    if (sc) {
+      if (sc_taken) break;
+      sc_taken = true;
+      x = w;
+      if (x >= a.n_pre) break;
+    } else {
+      x = __atomic_fetch_add(&ds->cursor, 1ull, __ATOMIC_RELAXED);
+    }
+    const uint64_t expect = make_tag(a.seq, x);
+    uint64_t w1, w2, w3;
+    if (x < a.n_pre) {
+      w1 = a.pre[x][0];
+      w2 = a.pre[x][1];
+      w3 = a.pre[x][2];
+    } else {
+      CuEntry* e = &rec->ring[x % kRingSize];
+      bool ready = false;
+      while (!ready) {
+        if (aload(&e->tag0) == expect && aload(&e->tag1) == expect) {
+          ready = true;
+          break;
+        }
+        const uint64_t hb2 = aload(&rec->h.heartbeat);
+        if (hb2 != hb) {
+          hb = hb2;
+          t_prog = now_ns();
+        } else if (now_ns() - t_prog > a.watchdog_ticks || __atomic_load_n(&ds->timed_out, __ATOMIC_RELAXED)) {
+          break;
+        }
+        std::this_thread::yield();
+      }
+      if (!ready) {
+        timed_out = true;
+        break;
+      }
+      w1 = e->a;
+      w2 = e->b;
+      w3 = static_cast<uint64_t>(e->count) | (static_cast<uint64_t>(e->kind_p0) << 32);
+    }
+    const uint32_t count = static_cast<uint32_t>(w3);
+    const uint32_t kind = static_cast<uint32_t>(w3 >> 32) & kEntryKindMask;
+    if (kind == kEntryEnd) break;
+    const uint32_t p0 = static_cast<uint32_t>(w3 >> 40);
+    if (kind == kEntryCopy) {
+      copy_at_rate(reinterpret_cast<void*>(w2), reinterpret_cast<const void*>(w1), count, wave_rate);
+    } else {
+      for (uint32_t j = 0; j < count; ++j) {
+        const uint32_t p = p0 + j;
+        uint8_t* pg = reinterpret_cast<uint8_t*>(a.layer_ptr[p >> 1]) + (p & 1u) * a.kv_kstride + w2 * a.kv_piece_bytes;
+        uint8_t* contig = reinterpret_cast<uint8_t*>(w1) + j * a.kv_piece_bytes;
+        if (kind == kEntryToPaged)
+          copy_at_rate(pg, contig, a.kv_piece_bytes, wave_rate);
+        else
+          copy_at_rate(contig, pg, a.kv_piece_bytes, wave_rate);
+      }
+    }
+    astore(&rec->done[x % kRingSize], expect);
+    t_prog = now_ns();
+  }
+  if (sc) return;
+  if (timed_out) __atomic_store_n(&ds->timed_out, 1u, __ATOMIC_RELAXED);
+  const uint32_t n = __atomic_fetch_add(&ds->exited, 1u, __ATOMIC_ACQ_REL);
+  if (n == a.total_waves - 1) {
+    bool to = __atomic_load_n(&ds->timed_out, __ATOMIC_RELAXED) != 0;
+    while (!to && aload(&rec->h.complete) != a.seq) {
+      const uint64_t hb2 = aload(&rec->h.heartbeat);
+      if (hb2 != hb) {
+        hb = hb2;
+        t_prog = now_ns();
+      } else if (now_ns() - t_prog > a.watchdog_ticks) {
+        to = true;
+      }
+      std::this_thread::yield();
+    }
+    if (to) astore(&rec->h.status, 1);
+    __atomic_store_n(&ds->cursor, 0ull, __ATOMIC_RELAXED);
+    __atomic_store_n(&ds->arrived, 0u, __ATOMIC_RELAXED);
+    __atomic_store_n(&ds->exited, 0u, __ATOMIC_RELAXED);
+    __atomic_store_n(&ds->timed_out, 0u, __ATOMIC_RELAXED);
+    astore(&rec->h.released, a.seq);
+  }
+}
+
+// ------------------------------------------------------------ harness
+struct Setup {
+  std::vector<double> engine_rates{2000, 2000};  // bytes/us
+  double wave_rate = 250;                          // bytes/us per wave
+  uint64_t cmd_ns = 20000;
+  uint32_t mask = MMA_PATH_CU | 0x3;
+  Config cfg{};
+};
+
+Config default_config() {
+  Config c{};
+  c.chunk = 256 * 1024;
+  c.fallback = 2 * c.chunk;
+  c.small = 16 * 1024;
+  c.sub = 64 * 1024;
+  c.depth = 2;
+  c.cu_depth = 4;
+  c.backoff = 2;
+  c.cu_wgs = 2;
+  c.watchdog_ms = 20000;
+  c.mask[0] = c.mask[1] = MMA_PATH_CU | 0x3;
+  c.static_split = 0;
+  c.static_cu_percent = 0;
+  c.merge = 4;
+  return c;
+}
+
+class Harness {
+ public:
+  explicit Harness(const Setup& s) : s_(s), be_(s.engine_rates, s.cmd_ns) {
+    Config c = s.cfg;
+    c.mask[0] = c.mask[1] = s.mask;
+    stage_bytes_ = std::max<uint64_t>(c.chunk, 2 * 1024 * 1024);
+    const uint32_t engines = static_cast<uint32_t>(__builtin_popcount(s.mask & 0xFFFFu));
+    staging_.assign(2 * engines * c.depth * stage_bytes_ + 1, 0);
+    for (int d = 0; d < 2; ++d) {
+      eng_[d].reset(new Engine(d, c, &be_, &stats_));
+      void* base = engines ? staging_.data() + d * engines * c.depth * stage_bytes_ : nullptr;
+      const mma_status_t rc = eng_[d]->init(s.mask & 0xFFFFu, stage_bytes_, base);
+      CHECK(rc == MMA_OK, "engine init %d: %s", rc, t_err.c_str());
+    }
+    cfg_ = c;
+  }
+  ~Harness() {
+    for (auto& e : eng_) e.reset();
+  }
+  // The runtime's submit(), with the fake stream in place of the kernel launch.
+  void submit(std::unique_ptr<Transfer> x, uint64_t payload, FakeStream& st, const KvGeom* kv = nullptr) {
+    Engine* e = eng_[x->dir].get();
+    std::lock_guard<std::mutex> g(submit_mu_);
+    CHECK(e->acquire_record(x.get(), 60000), "record");
+    KernelArgs a;
+    const uint32_t grid = e->prepare(x.get(), ++seq_, payload, kv, 20000ull * 1000000ull, a);
+    const uint32_t waves = grid * kWavesPerWG;
+    const double rate = s_.wave_rate;
+    st.launch([a, waves, rate] {
+      std::vector<std::thread> ts;
+      for (uint32_t w = 0; w < waves; ++w) ts.emplace_back(wave, a, w, rate);
+      for (auto& t : ts) t.join();
+    });
+    e->submit(std::move(x));
+  }
+  bool sync() { return eng_[0]->wait_idle(60000) && eng_[1]->wait_idle(60000); }
+  const Config& cfg() const { return cfg_; }
+  Stats& stats() { return stats_; }
+  FakeBackend& backend() { return be_; }
+  Engine* engine(int d) { return eng_[d].get(); }
+
+ private:
+  Setup s_;
+  FakeBackend be_;
+  Stats stats_;
+  std::unique_ptr<Engine> eng_[2];
+  std::vector<uint8_t> staging_;
+  uint64_t stage_bytes_ = 0;
+  Config cfg_{};
+  std::mutex submit_mu_;
+  uint64_t seq_ = 0;
+};
+
+std::vector<uint8_t> random_bytes(size_t n, uint32_t seed) {
+  std::vector<uint8_t> v(n);
+  std::mt19937 r(seed);
+  for (auto& b : v) b = static_cast<uint8_t>(r());
+  return v;
+}
+
+uint64_t sum_tasks(Stats& s, int from, int to) {
+  uint64_t t = 0;
+  for (int i = from; i < to; ++i) t += s.path_tasks[i].load();
+  return t;
+}
+
+std::unique_ptr<Transfer> linear(int dir, void* dst, const void* src, uint64_t n, const Config& c) {
+  mma_copy_desc_t d{dst, src, n};
+  const uint64_t s = reinterpret_cast<uint64_t>(src), t = reinterpret_cast<uint64_t>(dst);
+  return make_list_transfer(dir, &d, 1, &n, &s, &t, c);
+}
+
+// ------------------------------------------------------------ scenarios
+void copies_are_exact(uint32_t mask, const char* name) {
+  Setup s;
+  s.cfg = default_config();
+  s.mask = mask;
+  Harness h(s);
+  FakeStream st;
+  for (int dir = 0; dir < 2; ++dir) {
+    for (uint64_t n : {1ull, 777ull, 64ull * 1024, 300ull * 1024 + 5, 3ull * 1024 * 1024 + 123}) {
+      auto src = random_bytes(n, static_cast<uint32_t>(n + dir));
+      std::vector<uint8_t> dst(n + 64, 0xA5);
+      auto x = linear(dir, dst.data() + 32, src.data(), n, h.cfg());
+      const size_t tasks = x->tasks.size();
+      const uint64_t before = sum_tasks(h.stats(), 0, MMA_NUM_PATHS);
+      h.submit(std::move(x), n, st);
+      st.synchronize();
+      CHECK(h.sync(), "sync");
+      CHECK(std::memcmp(dst.data() + 32, src.data(), n) == 0, "%s dir=%d n=%llu: bytes differ", name, dir,
+            (unsigned long long)n);
+      CHECK(dst[31] == 0xA5 && dst[32 + n] == 0xA5, "%s: bytes outside the destination changed", name);
+      CHECK(sum_tasks(h.stats(), 0, MMA_NUM_PATHS) - before == tasks, "%s: tasks retired %llu != %zu", name,
+            (unsigned long long)(sum_tasks(h.stats(), 0, MMA_NUM_PATHS) - before), tasks);
+    }
+  }
+  CHECK(h.stats().failed.load() == 0, "%s: failed transfers", name);
+  std::printf("ok   copies exact, every micro-task retired once (%s): cu tasks %llu, sdma tasks %llu\n", name,
+              (unsigned long long)h.stats().path_tasks[16].load(), (unsigned long long)sum_tasks(h.stats(), 0, 16));
+}
+
+void list_with_merging() {
+  Setup s;
+  s.cfg = default_config();
+  s.mask = 0x3;  // copy engines only: every micro-task goes through a command
+  Harness h(s);
+  FakeStream st;
+  std::vector<uint64_t> sizes = {5, 300 * 1024, 1024 * 1024 + 17, 0, 70 * 1024, 2 * 1024 * 1024};
+  uint64_t total = 0;
+  for (auto z : sizes) total += z;
+  auto src = random_bytes(total, 7);
+  std::vector<uint8_t> dst(total, 0);
+  std::vector<mma_copy_desc_t> list;
+  std::vector<uint64_t> s_cu, d_cu;
+  uint64_t off = 0;
+  for (auto z : sizes) {  // back to back on both sides: runs cross tensor boundaries
+    list.push_back({dst.data() + off, src.data() + off, z});
+    s_cu.push_back(reinterpret_cast<uint64_t>(src.data() + off));
+    d_cu.push_back(reinterpret_cast<uint64_t>(dst.data() + off));
+    off += z;
+  }
+  auto x = make_list_transfer(MMA_H2D, list.data(), list.size(), sizes.data(), s_cu.data(), d_cu.data(), h.cfg());
+  const size_t tasks = x->tasks.size();
+  h.submit(std::move(x), total, st);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(std::memcmp(dst.data(), src.data(), total) == 0, "list bytes differ");
+  const uint64_t cmds = h.stats().sdma_commands.load();
+  const uint64_t sdma_tasks = sum_tasks(h.stats(), 0, 16);
+  CHECK(sdma_tasks + h.stats().path_tasks[16].load() == tasks, "tasks retired");
+  CHECK(cmds < sdma_tasks, "merging: %llu commands for %llu micro-tasks", (unsigned long long)cmds,
+        (unsigned long long)sdma_tasks);
+  std::printf("ok   tensor list, merged commands: %llu commands for %llu copy-engine micro-tasks\n",
+              (unsigned long long)cmds, (unsigned long long)sdma_tasks);
+}
+
+void kv_roundtrip(uint32_t mask, const char* name) {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.chunk = 8 * 1024;  // 4 pieces per micro-task
+  s.mask = mask;
+  Harness h(s);
+  FakeStream st;
+  const uint32_t L = 3, ppb = 2 * L, slots = 24, nb = 30;
+  const uint64_t piece = 2048, slot_bytes = piece * ppb;
+  std::vector<uint8_t> pool = random_bytes(slots * slot_bytes, 11);
+  std::vector<std::vector<uint8_t>> layers(L, std::vector<uint8_t>(2 * nb * piece, 0xA5));
+  KvGeom kv;
+  kv.piece = piece;
+  kv.kstride = piece * nb;
+  kv.layers = L;
+  for (uint32_t l = 0; l < L; ++l) kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l].data());
+  std::vector<int32_t> hs = {5, 0, 17, 3, 22, 9, 11, 1, 14, 20}, gb = {2, 29, 7, 0, 13, 21, 4, 26, 9, 15};
+  const uint64_t host = reinterpret_cast<uint64_t>(pool.data());
+  const bool sdma_ok = (mask & 0xFFFFu) != 0;
+  auto x = make_kv_transfer(MMA_H2D, piece, ppb, host, host, false, sdma_ok, hs.data(), gb.data(), hs.size(), h.cfg());
+  h.submit(std::move(x), hs.size() * slot_bytes, st, &kv);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  bool ok = true;
+  for (size_t i = 0; i < hs.size(); ++i)
+    for (uint32_t l = 0; l < L; ++l)
+      for (uint32_t k = 0; k < 2; ++k)
+        ok &= std::memcmp(layers[l].data() + (k * nb + gb[i]) * piece,
+                          pool.data() + hs[i] * slot_bytes + (2 * l + k) * piece, piece) == 0;
+  size_t untouched = 0;
+  for (uint32_t l = 0; l < L; ++l)
+    for (uint32_t k = 0; k < 2; ++k)
+      for (uint32_t b = 0; b < nb; ++b)
+        if (std::find(gb.begin(), gb.end(), static_cast<int32_t>(b)) == gb.end())
+          untouched += layers[l][(k * nb + b) * piece] == 0xA5 && layers[l][(k * nb + b + 1) * piece - 1] == 0xA5;
+  CHECK(ok, "%s: fetched pieces differ", name);
+  CHECK(untouched == L * 2 * (nb - hs.size()), "%s: untouched blocks changed", name);
+  // offload the same blocks into other slots
+  std::vector<int32_t> dest = {23, 2, 4, 6, 8, 10, 12, 13, 15, 16};
+  auto before = pool;
+  auto y = make_kv_transfer(MMA_D2H, piece, ppb, host, host, false, sdma_ok, dest.data(), gb.data(), gb.size(),
+                            h.cfg());
+  h.submit(std::move(y), gb.size() * slot_bytes, st, &kv);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  auto want = before;
+  for (size_t j = 0; j < gb.size(); ++j)
+    for (uint32_t l = 0; l < L; ++l)
+      for (uint32_t k = 0; k < 2; ++k)
+        std::memcpy(want.data() + dest[j] * slot_bytes + (2 * l + k) * piece,
+                    layers[l].data() + (k * nb + gb[j]) * piece, piece);
+  CHECK(pool == want, "%s: offloaded pool differs", name);
+  CHECK(h.stats().failed.load() == 0, "%s: failed", name);
+  std::printf("ok   paged-KV fetch and offload (%s): staging bytes %llu, sdma commands %llu\n", name,
+              (unsigned long long)h.stats().staging_bytes.load(), (unsigned long long)h.stats().sdma_commands.load());
+}
+
+void slow_engine_gets_fewer_tasks() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.merge = 1;
+  s.engine_rates = {3000, 750};  // 4:1
+  s.mask = 0x3;
+  s.cmd_ns = 5000;
+  Harness h(s);
+  FakeStream st;
+  const uint64_t n = 24 * 1024 * 1024;
+  auto src = random_bytes(n, 3);
+  std::vector<uint8_t> dst(n);
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst == src, "bytes differ");
+  const double t0 = static_cast<double>(h.stats().path_tasks[0].load());
+  const double t1 = static_cast<double>(h.stats().path_tasks[1].load());
+  CHECK(t1 > 0 && t0 / t1 > 2.0, "fast engine %g tasks, slow engine %g tasks", t0, t1);
+  std::printf("ok   a 4x slower copy engine pulls fewer micro-tasks: %g vs %g\n", t0, t1);
+}
+
+void submit_failures_rerouted() {
+  Setup s;
+  s.cfg = default_config();
+  Harness h(s);
+  FakeStream st;
+  const uint64_t n = 4 * 1024 * 1024;
+  auto src = random_bytes(n, 5);
+  std::vector<uint8_t> dst(n);
+  g_fault_submit_fail = 3;
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  g_fault_submit_fail = 0;
+  CHECK(dst == src, "bytes differ");
+  CHECK(h.stats().submit_failures.load() >= 1 && h.stats().failed.load() == 0, "re-route");
+  std::printf("ok   copy-engine submit failures re-routed to the CU path (%llu)\n",
+              (unsigned long long)h.stats().submit_failures.load());
+}
+
+void two_streams_both_directions() {
+  Setup s;
+  s.cfg = default_config();
+  Harness h(s);
+  FakeStream a, b;
+  const uint64_t n = 6 * 1024 * 1024 + 3;
+  std::vector<std::vector<uint8_t>> srcs, dsts;
+  for (int i = 0; i < 6; ++i) {
+    srcs.push_back(random_bytes(n, 100 + i));
+    dsts.emplace_back(n, 0);
+  }
+  for (int i = 0; i < 6; ++i) {
+    FakeStream& st = i % 2 ? b : a;
+    h.submit(linear(i % 2, dsts[i].data(), srcs[i].data(), n, h.cfg()), n, st);
+  }
+  a.synchronize();
+  b.synchronize();
+  CHECK(h.sync(), "sync");
+  for (int i = 0; i < 6; ++i) CHECK(dsts[i] == srcs[i], "stream transfer %d differs", i);
+  std::printf("ok   six transfers on two streams, both directions\n");
+}
+
+// Pull-based selection against fixed splits decided at plan time, on two
+// paths (the CU path and one copy engine) with a given rate ratio.
+double timed_copy(double cu_rate, double eng_rate, uint32_t static_cu_percent, bool pull) {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.cu_wgs = 1;
+  s.cfg.merge = 1;
+  s.cmd_ns = 0;
+  s.engine_rates = {eng_rate};
+  s.wave_rate = cu_rate / 4;  // 4 waves
+  s.mask = MMA_PATH_CU | 0x1;
+  if (!pull) {
+    s.cfg.static_split = 1;
+    s.cfg.static_cu_percent = static_cu_percent;
+  }
+  Harness h(s);
+  FakeStream st;
+  const uint64_t n = 32 * 1024 * 1024;
+  std::vector<uint8_t> src(n, 1), dst(n);
+  const auto t0 = std::chrono::steady_clock::now();
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  const double ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  CHECK(dst == src, "bytes differ");
+  return ms;
+}
+
+void pull_tracks_best_static_split() {
+  for (double ratio : {1.0, 2.0}) {
+    const double eng = 1000, cu = 1000 * ratio;  // CU path ratio x faster
+    double best = 1e30;
+    std::printf("     rate ratio CU:SDMA = %g:1 -- static", ratio);
+    // best of three runs each: the fake paths are host threads that sleep
+    auto best_of3 = [&](uint32_t pct, bool pull) {
+      double t = 1e30;
+      for (int r = 0; r < 3; ++r) t = std::min(t, timed_copy(cu, eng, pct, pull));
+      return t;
+    };
+    for (uint32_t pct : {0u, 33u, 50u, 67u, 100u}) {
+      const double t = best_of3(pct, false);
+      best = std::min(best, t);
+      std::printf(" %u%%=%.1fms", pct, t);
+    }
+    const double p = best_of3(0, true);
+    std::printf(" | pull=%.1fms\n", p);
+    // Quiet machines give pull <= best static; the bound leaves room for a busy host's sleep jitter.
+    CHECK(p <= best * 1.15, "pull %.1f ms vs best static %.1f ms at ratio %g", p, best, ratio);
+    std::printf("     pull / best static = %.3f\n", p / best);
+  }
+  std::printf("ok   pull-based selection tracks the best fixed split at 1:1 and 2:1\n");
+}
+
+}  // namespace
+
+int main(int argc, char** argv) {
+  const bool timing = !(argc > 1 && std::strcmp(argv[1], "--no-timing") == 0);
+  copies_are_exact(MMA_PATH_CU | 0x3, "CU + 2 engines");
+  copies_are_exact(0x3, "2 engines");
+  copies_are_exact(MMA_PATH_CU, "CU only");
+  list_with_merging();
+  kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging");
+  kv_roundtrip(MMA_PATH_CU, "CU only");
+  submit_failures_rerouted();
+  two_streams_both_directions();
+  if (timing) {
+    slow_engine_gets_fewer_tasks();
+    pull_tracks_best_static_split();
+  }
+  if (g_failures) {
+    std::printf("FAILED: %d check(s)\n", g_failures);
+    return 1;
+  }
+  std::printf("ALL OK\n");
+  return 0;
+}
