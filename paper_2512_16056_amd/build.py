@@ -16,6 +16,8 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(HERE, "libmma.so")
 NATIVE_LIB = os.path.join(HERE, "libmma_native.so")  # hipMemcpyAsync comparators for the benchmark
+INTERPOSE_LIB = os.path.join(HERE, "libmma_interpose.so")  # LD_PRELOAD: hipMemcpy* -> libmma
+CXX = os.environ.get("CXX", "g++")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
@@ -61,6 +63,13 @@ def build(verbose: bool = False) -> str:
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *nobj, "-o", tmp, f"-L{os.path.join(ROCM, 'lib')}",
           "-lamdhip64", "-lhsa-runtime64", "-ldl"])
     os.replace(tmp, NATIVE_LIB)
+    # LD_PRELOAD interposer: host C++ only, linked against neither the HIP runtime nor libmma.so
+    # (both are resolved at run time inside the process).
+    tmp = INTERPOSE_LIB + ".tmp"
+    _run([CXX, "-std=c++17", "-O2", "-fPIC", "-shared", "-Wall", "-D__HIP_PLATFORM_AMD__",
+          f"-I{os.path.join(ROCM, 'include')}", f"-I{os.path.join(ROOT, 'include')}",
+          os.path.join(CSRC, "mma_interpose.cpp"), "-o", tmp, "-ldl"])
+    os.replace(tmp, INTERPOSE_LIB)
     return LIB
 
 

@@ -131,3 +131,17 @@ def test_struct_layouts_match_header(tmp_path):
     subprocess.run([cc, "-std=c99", f"-I{os.path.join(ROOT, 'include')}", str(src), "-o", str(exe)], check=True)
     got = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()]
     assert got == want
+
+
+def test_interposer_exports_and_links_no_runtime():
+    """libmma_interpose.so exports the three intercepted HIP copies and links neither the HIP
+    runtime nor libmma.so (both are resolved inside the process at the first call)."""
+    import subprocess
+    lib = os.path.join(ROOT, "paper_2512_16056_amd", "libmma_interpose.so")
+    if not os.path.exists(lib):
+        pytest.skip("interposer not built")
+    syms = subprocess.run(["nm", "-D", "--defined-only", lib], capture_output=True, text=True).stdout
+    for name in ("hipMemcpyAsync", "hipMemcpy", "hipMemcpyWithStream"):
+        assert re.search(rf"\bT {name}$", syms, flags=re.M), name
+    needed = subprocess.run(["readelf", "-d", lib], capture_output=True, text=True).stdout
+    assert "libamdhip64" not in needed and "libmma.so" not in needed
