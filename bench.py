@@ -105,6 +105,11 @@ def _timed(stream, fn, reps, warm):
     return _pcts(ts)
 
 
+def _ok(rc):
+    if rc != 0:
+        raise RuntimeError(f"library call failed with status {rc}")
+
+
 def _pcts(ts):
     ts = sorted(ts)
 
@@ -204,11 +209,15 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
     src = mma.PinnedBuffer(n)
     src.array[:] = W.uniform_bytes(1, W.TAG_DATA, 0, n)
     dst = torch.full((n,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
-    m64 = _timed(stream, lambda: mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, stream), reps=50, warm=5)
+    # Both sides are called straight through ctypes with prepared arguments, so neither pays
+    # Python-level argument conversion inside the timed region.
+    margs = (ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.ptr), ctypes.c_uint64(n), mma.MMA_H2D,
+             ctypes.c_void_p(stream.cuda_stream))
+    m64 = _timed(stream, lambda: _ok(mma.lib.mma_memcpy_async(*margs)), reps=50, warm=5)
     ok64 = bool(np.array_equal(dst.cpu().numpy(), src.array))
     D, S, Z = (ctypes.c_void_p * 1)(dst.data_ptr()), (ctypes.c_void_p * 1)(src.ptr), (ctypes.c_uint64 * 1)(n)
-    n64 = _timed(stream, lambda: nat.native_list(D, S, Z, 1, 0, ctypes.c_void_p(stream.cuda_stream)),
-                 reps=50, warm=5)
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    n64 = _timed(stream, lambda: nat.native_list(D, S, Z, 1, 0, sp), reps=50, warm=5)
     extras["copy64"] = {"mma_ms": round(m64["p50"], 4), "mma_ms_p10_p90": [round(m64["p10"], 4), round(m64["p90"], 4)],
                         "mma_GBs": round(n / m64["p50"] / 1e6, 2),
                         "native_ms": round(n64["p50"], 4),
@@ -405,8 +414,10 @@ def sweep_sizes():
         for dr, name in ((0, "h2d"), (1, "d2h")):
             dst, src = (d.data_ptr(), h.ptr) if dr == 0 else (h.ptr, d.data_ptr())
             D, S, Z = (ctypes.c_void_p * 1)(dst), (ctypes.c_void_p * 1)(src), (ctypes.c_uint64 * 1)(n)
-            t_nat = _timed(st, lambda: nat.native_list(D, S, Z, 1, dr, ctypes.c_void_p(st.cuda_stream)), reps, 3)
-            t_mma = _timed(st, lambda: mma.mma_memcpy_async(dst, src, n, dr, st), reps, 3)
+            sp = ctypes.c_void_p(st.cuda_stream)
+            t_nat = _timed(st, lambda: nat.native_list(D, S, Z, 1, dr, sp), reps, 3)
+            margs = (ctypes.c_void_p(dst), ctypes.c_void_p(src), ctypes.c_uint64(n), dr, sp)
+            t_mma = _timed(st, lambda: _ok(mma.lib.mma_memcpy_async(*margs)), reps, 3)
             row[name] = {"mma_us": round(t_mma["p50"] * 1e3, 2), "native_us": round(t_nat["p50"] * 1e3, 2),
                          "mma_GBs": round(n / t_mma["p50"] / 1e6, 2), "native_GBs": round(n / t_nat["p50"] / 1e6, 2),
                          "ratio_vs_native": round(t_nat["p50"] / t_mma["p50"], 3)}

@@ -122,8 +122,9 @@ struct Transfer {
   bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
   uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
   std::shared_ptr<Waiter> waiter;  // set for synchronous calls
+  // Per ring slot, set when an entry is appended (left uninitialised until then):
   int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
-  uint8_t tdone[kRingSize];
+  uint8_t tdone[kRingSize];    // its done tag has been seen
   uint32_t cu_busy = 0;
   bool cu_full = false;
   int sdma_cu_pending = 0;     // SDMA slots that will still append ring entries
@@ -1066,7 +1067,7 @@ inline std::unique_ptr<Transfer> make_list_transfer(int dir, const mma_copy_desc
                                                     const uint64_t* dst_cu, const Config& c) {
   std::vector<PlanItem> plan;
   plan_list(sizes, n, c.chunk, c.fallback, c.small, plan);
-  std::unique_ptr<Transfer> x(new Transfer());
+  std::unique_ptr<Transfer> x(new Transfer);  // owner/tdone are written before they are read
   x->dir = dir;
   x->kind = Kind::kLinear;
   x->tasks.reserve(plan.size());
@@ -1093,7 +1094,7 @@ inline std::unique_ptr<Transfer> make_kv_transfer(int dir, uint64_t piece, uint3
                                                   const Config& c) {
   std::vector<PlanItem> plan;
   plan_kv(n, ppb, piece, c.chunk, plan);
-  std::unique_ptr<Transfer> x(new Transfer());
+  std::unique_ptr<Transfer> x(new Transfer);  // owner/tdone are written before they are read
   x->dir = dir;
   x->kind = dir == MMA_H2D ? Kind::kKvFetch : Kind::kKvOffload;
   x->piece = piece;

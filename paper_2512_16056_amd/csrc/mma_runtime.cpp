@@ -196,8 +196,79 @@ bool within_allocation(const void* p, uint64_t bytes) {
   return id0 == id1 && id0 != 0;
 }
 
+// Allocations validated before, by the runtime's buffer id (unique for the
+// life of the process, so an entry can never describe a different live
+// allocation): a later range inside one of them needs one attribute query
+// instead of three.
+class RangeCache {
+ public:
+  struct Entry {
+    uint64_t id = 0, base = 0, size = 0;
+    int64_t dev_off = 0;  // host kind: device address - host address
+    bool host = false;
+  };
+  bool find(uint64_t id, bool host, uint64_t p, uint64_t bytes, Entry* out) {
+    std::lock_guard<std::mutex> g(mu_);
+    for (const Entry& e : e_)
+      if (e.id == id && e.host == host && p >= e.base && p + bytes <= e.base + e.size) {
+        *out = e;
+        return true;
+      }
+    return false;
+  }
+  void insert(const Entry& e) {
+    std::lock_guard<std::mutex> g(mu_);
+    e_[next_++ % kEntries] = e;
+  }
+  void clear() {
+    std::lock_guard<std::mutex> g(mu_);
+    for (Entry& e : e_) e = Entry{};
+  }
+
+ private:
+  static constexpr size_t kEntries = 64;
+  std::mutex mu_;
+  Entry e_[kEntries];
+  size_t next_ = 0;
+};
+RangeCache g_ranges;
+
+uint64_t buffer_id(const void* p) {
+  uint64_t id = 0;
+  if (hipPointerGetAttribute(&id, HIP_POINTER_ATTRIBUTE_BUFFER_ID, const_cast<void*>(p)) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return id;
+}
+
+// After a full check of [p, p + bytes): remember the whole allocation.
+void remember(uint64_t id, bool host, const void* p, uint64_t bytes, int64_t dev_off) {
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (!id || hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess) {
+    (void)hipGetLastError();
+    return;
+  }
+  const uint64_t b = reinterpret_cast<uint64_t>(base), q = reinterpret_cast<uint64_t>(p);
+  if (q < b || q + bytes > b + size) return;  // inconsistent answer: do not rely on it
+  RangeCache::Entry e;
+  e.id = id;
+  e.base = b;
+  e.size = size;
+  e.dev_off = dev_off;
+  e.host = host;
+  g_ranges.insert(e);
+}
+
 // Pinned, device-mapped host range: returns the device-visible address of p.
 mma_status_t host_range(const void* p, uint64_t bytes, uint64_t* dev_addr) {
+  const uint64_t id = buffer_id(p);
+  RangeCache::Entry e;
+  if (id && g_ranges.find(id, true, reinterpret_cast<uint64_t>(p), bytes, &e)) {
+    *dev_addr = static_cast<uint64_t>(reinterpret_cast<int64_t>(p) + e.dev_off);
+    return MMA_OK;
+  }
   hipPointerAttribute_t a{};
   if (hipPointerGetAttributes(&a, p) != hipSuccess) {
     (void)hipGetLastError();
@@ -210,10 +281,14 @@ mma_status_t host_range(const void* p, uint64_t bytes, uint64_t* dev_addr) {
     return fail(MMA_ERR_NOT_PINNED, "host range [%p, +%llu) is not inside one pinned allocation", p,
                 static_cast<unsigned long long>(bytes));
   *dev_addr = reinterpret_cast<uint64_t>(a.devicePointer);
+  remember(id, true, p, bytes, reinterpret_cast<int64_t>(a.devicePointer) - reinterpret_cast<int64_t>(p));
   return MMA_OK;
 }
 
 mma_status_t device_range(const void* p, uint64_t bytes) {
+  const uint64_t id = buffer_id(p);
+  RangeCache::Entry e;
+  if (id && g_ranges.find(id, false, reinterpret_cast<uint64_t>(p), bytes, &e)) return MMA_OK;
   hipPointerAttribute_t a{};
   if (hipPointerGetAttributes(&a, p) != hipSuccess || a.type != hipMemoryTypeDevice) {
     (void)hipGetLastError();
@@ -223,6 +298,7 @@ mma_status_t device_range(const void* p, uint64_t bytes) {
   if (!within_allocation(p, bytes))
     return fail(MMA_ERR_INVALID_ARG, "device range [%p, +%llu) is not inside one allocation", p,
                 static_cast<unsigned long long>(bytes));
+  remember(id, false, p, bytes, 0);
   return MMA_OK;
 }
 
@@ -291,6 +367,7 @@ mma_status_t mma_config_default(mma_config_t* out) {
 mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   std::lock_guard<std::mutex> g(g_init_mu);
   if (g_rt) return fail(MMA_ERR_ALREADY_INITIALIZED, "already initialised");
+  g_ranges.clear();  // device entries were checked against the previous device
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || hip_device < 0 || hip_device >= ndev) {
     (void)hipGetLastError();
