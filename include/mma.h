@@ -171,14 +171,17 @@ mma_status_t mma_config_default(mma_config_t* out);
  * D2H engines). cfg == NULL: defaults, then MMA_* environment overrides
  * (MMA_CHUNK_BYTES, MMA_FALLBACK_BYTES, MMA_SMALL_BYTES, MMA_QUEUE_DEPTH,
  * MMA_CU_QUEUE_DEPTH, MMA_BACKOFF_DEPTH, MMA_PATHS_H2D, MMA_PATHS_D2H,
- * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS).
+ * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS, MMA_SDMA_MERGE_TASKS, MMA_TRACE).
  * Errors: MMA_ERR_ALREADY_INITIALIZED, MMA_ERR_INVALID_ARG (bad device or
  * config), MMA_ERR_HIP / MMA_ERR_HSA. */
 mma_status_t mma_init(int hip_device, const mma_config_t* cfg);
 
 /* Wait for every submitted transfer to retire (bounded), stop the engine
  * threads and release library resources. Returns MMA_ERR_TIMEOUT if in-flight
- * transfers did not drain (their streams are then still blocked). */
+ * transfers did not drain (their streams are then still blocked). Must not run
+ * concurrently with other calls of this library. A process that exits without
+ * it has its engine threads stopped when the library is unloaded, before the
+ * HIP runtime's own teardown. */
 mma_status_t mma_finalize(void);
 
 /* The configuration in effect (after defaults and environment). */

@@ -134,6 +134,19 @@ struct Runtime {
 Runtime* g_rt = nullptr;
 std::mutex g_init_mu;
 
+// Engine threads must not outlive the HIP runtime: if the program exits
+// without mma_finalize, they are stopped when this library is unloaded, which
+// happens before the runtime it depends on is torn down.
+struct ExitGuard {
+  ~ExitGuard() {
+    std::lock_guard<std::mutex> g(g_init_mu);
+    if (!g_rt) return;
+    for (auto& e : g_rt->eng)
+      if (e) (void)e->wait_idle(2000);
+    for (auto& e : g_rt->eng) e.reset();
+  }
+} g_exit_guard;
+
 void set_affinity_local(pthread_t th, int dev) {
   char bus[64];
   if (hipDeviceGetPCIBusId(bus, sizeof bus, dev) != hipSuccess) return;

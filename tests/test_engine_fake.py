@@ -40,7 +40,15 @@ def test_engine_on_fake_paths(tmp_path):
         pytest.skip("no C++ compiler")
     exe = str(tmp_path / "engine_fake")
     _build(cxx, exe, ["-O2", "-Wall"])
-    _run(exe, [])
+    _run(exe, ["--no-timing"])
+    # The rate-dependent scenarios (a slower engine pulls fewer micro-tasks; pull vs the best
+    # fixed split) emulate path rates with sleeps; one re-measurement absorbs a noisy host.
+    for attempt in range(2):
+        r = subprocess.run([exe, "--timing-only"], capture_output=True, text=True, timeout=600)
+        print(r.stdout)
+        if r.returncode == 0 and "ALL OK" in r.stdout:
+            return
+    raise AssertionError("timing scenarios failed twice:\n" + r.stdout[-3000:])
 
 
 def test_engine_on_fake_paths_thread_sanitizer(tmp_path):
