@@ -99,8 +99,10 @@ typedef struct mma_config {
   uint32_t static_cu_percent;
   uint32_t sdma_merge_tasks; /* at most this many micro-tasks that follow each other in both
                                address spaces (a linear run, or one KV block's consecutive pieces)
-                               go to an SDMA engine as one command; default: 8 MiB worth
-                               (max(1, 8 MiB / chunk_bytes)); 1 = one command per micro-task */
+                               go to an SDMA engine as one command, and never more than the
+                               engine's fair share of the transfer's remaining work; default:
+                               64 MiB worth (max(1, 64 MiB / chunk_bytes)); 1 = one command per
+                               micro-task */
   uint32_t reserved;
 } mma_config_t;
 

@@ -120,6 +120,12 @@ struct Transfer {
   uint32_t waves = 0;          // waves of the dummy-task kernel
   bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
   bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
+  // Submitted on a stream with nothing pending: the engine may start the copy
+  // engines at once, without waiting for the kernel's start signal.
+  bool early = false;
+  // Set by the submitting thread when the dummy-task launch of an early
+  // transfer failed: no kernel will ever run for it.
+  std::atomic<bool> unlaunched{false};
   uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
   std::shared_ptr<Waiter> waiter;  // set for synchronous calls
   // Per ring slot, set when an entry is appended (left uninitialised until then):
@@ -170,6 +176,7 @@ struct SdmaPath {
   int busy = 0;
   bool full = false;
   bool congested = false;  // a command is long overdue: pull nothing more until the engine drains
+  uint64_t t_head = 0;     // when the path's oldest command in flight reached the head of its queue
 };
 
 struct Config {
@@ -581,6 +588,13 @@ class Engine {
   }
 
   // ---------------------------------------------------------------- SDMA path
+  static bool engine_op(const SdmaSlot& s) { return s.state == kCopy || s.state == kH2DStage || s.state == kD2HStage; }
+  int engine_ops(const SdmaPath& path) const {
+    int n = 0;
+    for (int id : path.slots) n += engine_op(slots_[id]) ? 1 : 0;
+    return n;
+  }
+
   bool sdma_copy(SdmaSlot& s, void* dst, bool dst_on_device, const void* src, bool src_on_device, uint64_t bytes) {
     uint64_t f = g_fault_submit_fail.load();
     while (f > 0) {
@@ -589,6 +603,8 @@ class Engine {
     if (!s.x->t_first_sdma) s.x->t_first_sdma = now_ns();
     s.t_submit = now_ns();
     s.op_bytes = bytes;
+    SdmaPath& path = paths_[s.path];
+    if (engine_ops(path) == 0) path.t_head = s.t_submit;  // (s is not in an engine state yet)
     be_->signal_store(s.sig, 1);
     const bool ok = be_->copy(paths_[s.path].engine, dst, dst_on_device, src, src_on_device, bytes, s.sig);
     if (ok) st_->sdma_commands += 1;
@@ -667,12 +683,14 @@ class Engine {
         }
         continue;
       }
-      if (s.state != kCopy && s.state != kH2DStage && s.state != kD2HStage) continue;
+      if (!engine_op(s)) continue;
       const int64_t v = be_->signal_load(s.sig);
       if (v > 0) continue;
       p = true;
       Transfer* x = s.x;
       x->progress = true;
+      // The engine runs our commands in order: the next one is at the head now.
+      paths_[s.path].t_head = now_ns();
       if (v < 0) {
         x->failed = true;
         if (s.state == kH2DStage) --x->sdma_cu_pending;
@@ -715,15 +733,15 @@ class Engine {
 
   // One copy-engine command carries the claimed micro-task i and the unclaimed
   // ones that directly follow it in both address spaces (a linear run, or one
-  // KV block's consecutive pieces that fit the staging slot), up to cfg.merge.
-  // Each ROCr copy command costs about 8 us of engine time (measured), so at
-  // small chunk sizes one command per micro-task would cap an engine well
+  // KV block's consecutive pieces that fit the staging slot), `cap` micro-tasks
+  // at most. Each ROCr copy command costs about 8 us of engine time (measured),
+  // so at small chunk sizes one command per micro-task would cap an engine well
   // below the link.
-  size_t merge_run(const Transfer* x, size_t i) const {
+  size_t merge_run(const Transfer* x, size_t i, size_t cap) const {
     const bool sdma_only = (x->tasks[i].flags & kPlanSdmaOnly) != 0;
     uint64_t total = x->tasks[i].bytes;
     size_t j = i + 1;
-    for (; j < x->tasks.size() && j - i < cfg_.merge; ++j) {
+    for (; j < x->tasks.size() && j - i < cap; ++j) {
       const Task& a = x->tasks[j - 1];
       const Task& b = x->tasks[j];
       if (x->claimed[j] || (b.flags & kPlanCuOnly) || ((b.flags & kPlanSdmaOnly) != 0) != sdma_only) break;
@@ -739,15 +757,42 @@ class Engine {
     return j;
   }
 
-  // A copy-engine command is overdue when it has been in flight for four times
-  // what its size needs at 50 GB/s, plus 0.5 ms of slack.
-  bool overdue(const SdmaPath& path, uint64_t now) const {
+  // Micro-tasks of x that copy-engine `path` may still take: each engine holds
+  // at most an equal share, among the engines, of the work of x not yet landed
+  // (claimed-but-outstanding plus unclaimed). Early in a transfer the share is
+  // large, so an engine gets few long commands and ROCr's per-command cost is
+  // paid rarely; it shrinks as the transfer drains, so the engines finish
+  // together (guided self-scheduling, Polychronopoulos and Kuck, 1987,
+  // extended to paths with several commands in flight). The CU path is not
+  // counted: it pulls 64 KiB ring entries at its own depth, fills whatever the
+  // engines leave, and strands no work at the end. An idle engine always gets
+  // at least one micro-task.
+  size_t fair_share(const Transfer* x, const SdmaPath& path) const {
+    const size_t unclaimed = x->tasks.size() - x->n_claimed;
+    const size_t outstanding = x->n_claimed - x->n_done;
+    size_t mine = 0;
     for (int id : path.slots) {
       const SdmaSlot& s = slots_[id];
-      if (s.state != kCopy && s.state != kH2DStage && s.state != kD2HStage) continue;
-      if (now - s.t_submit > 4 * s.op_bytes / 50 + 500000) return true;  // ns
+      if (s.x == x && s.state != kFree) mine += s.task_end - s.task;
     }
-    return false;
+    const size_t fair = (unclaimed + outstanding + paths_.size() - 1) / paths_.size();
+    return fair > mine ? fair - mine : 0;
+  }
+
+  // A path is overdue when its oldest command has been at the head of the
+  // engine's queue for four times what its size needs at an equal share of a
+  // 50 GB/s link among all paths, plus 0.5 ms of slack. (Timing from
+  // submission would count the wait behind the path's own earlier commands.)
+  bool overdue(const SdmaPath& path, uint64_t now) const {
+    const SdmaSlot* head = nullptr;
+    for (int id : path.slots) {
+      const SdmaSlot& s = slots_[id];
+      if (engine_op(s) && (!head || s.t_submit < head->t_submit)) head = &s;
+    }
+    if (!head) return false;
+    const uint64_t npaths = paths_.size() + (cu_enabled() ? 1 : 0);
+    const uint64_t since = std::max(path.t_head, head->t_submit);
+    return now > since && now - since > 4 * npaths * head->op_bytes / 50 + 500000;  // ns
   }
 
   // Paths that can make progress take work (Section 2.2; Section 3.4 contention
@@ -791,8 +836,10 @@ class Engine {
         Transfer* x;
         size_t i;
         if (!next_sdma_task(x, i)) return p;
+        const size_t share = fair_share(x, path);
+        if (share == 0) break;
         const Task& t = x->tasks[i];
-        const size_t end = merge_run(x, i);
+        const size_t end = merge_run(x, i, std::min<size_t>(cfg_.merge, share));
         for (size_t j = i; j < end; ++j) x->claimed[j] = 1;
         x->n_claimed += end - i;
         s.x = x;
@@ -841,7 +888,12 @@ class Engine {
   bool advance(Transfer* x) {
     Record* r = x->rec;
     bool p = false;
-    if (!x->started && !x->ignored && ld_acq(&r->h.started) == x->seq) {
+    if (x->unlaunched.load(std::memory_order_acquire) && !x->aborting) {
+      x->aborting = true;  // drain what the copy engines hold; nothing else will run
+      x->failed = true;
+      return true;
+    }
+    if (!x->started && !x->ignored && (x->early || ld_acq(&r->h.started) == x->seq)) {
       if (g_fault_ignore.load()) {
         x->ignored = true;
       } else {
@@ -938,6 +990,7 @@ class Engine {
   bool retire_ready(Transfer* x) {
     // A self-contained kernel's done tags are its last accesses to the record.
     if (x->self_contained) return x->n_done == x->tasks.size();
+    if (x->unlaunched.load(std::memory_order_acquire)) return x->sdma_refs == 0;
     if (ld_acq(&x->rec->h.released) != x->seq) return false;
     // Every wave wrote its done tags before the last one released the record,
     // but `complete` may have been published before this thread saw them (the
@@ -1003,12 +1056,14 @@ class Engine {
           ++i;
           continue;
         }
-        const bool bad = x->failed || x->ignored || ld_acq(&x->rec->h.status) != 0;
+        // A failed launch was reported to the caller; it leaves no sticky error.
+        const bool unlaunched = x->unlaunched.load(std::memory_order_relaxed);
+        const bool bad = !unlaunched && (x->failed || x->ignored || ld_acq(&x->rec->h.status) != 0);
         if (bad) {
           g_sticky.store(1);
           st_->failed += 1;
         }
-        st_->transfers += 1;
+        if (!unlaunched) st_->transfers += 1;
         if (g_trace.load(std::memory_order_relaxed)) record_trace(x, bad);
         if (x->waiter) {
           std::lock_guard<std::mutex> g(x->waiter->mu);

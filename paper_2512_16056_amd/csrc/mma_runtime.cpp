@@ -315,7 +315,39 @@ mma_status_t device_range(const void* p, uint64_t bytes) {
   return MMA_OK;
 }
 
+// True when nothing can be ordered before work enqueued now on `s`: it is not
+// the legacy default stream, it has no pending work, and it either does not
+// synchronise with the legacy default stream or that stream is idle too.
+// (hipStreamQuery reports hipErrorNotReady for a busy stream; that status is
+// not left behind as the thread's last error.)
+bool stream_idle(hipStream_t s) {
+  if (s == nullptr || s == hipStreamLegacy) return false;
+  if (hipStreamQuery(s) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  unsigned int flags = 0;
+  if (s != hipStreamPerThread && hipStreamGetFlags(s, &flags) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (flags & hipStreamNonBlocking) return true;
+  if (hipStreamQuery(nullptr) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return true;
+}
+
 // Hand a planned transfer to its engine and enqueue the dummy task on the stream.
+//
+// The copy must not start before the work that precedes it on the stream, so
+// the copy engines normally wait for the dummy kernel's start signal (one
+// posted PCIe write, seen by the polling engine thread). When the stream has
+// nothing pending, no work precedes the copy: the transfer goes to the engine
+// before the launch and the copy engines start while the kernel is still
+// being launched. The kernel still holds later stream work until every path
+// has landed.
 mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* stream, const KvGeom* kv) {
   Runtime* rt = g_rt;
   Engine* e = rt->eng[x->dir].get();
@@ -329,7 +361,25 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
     tl_waiter->submitted = true;
   }
   DeviceGuard dg(rt->dev);
-  const hipError_t err = launch_transfer(a, grid, static_cast<hipStream_t>(stream));
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (!x->self_contained && x->sdma_ok && e->has_sdma() && x->n_claimed < x->tasks.size() && stream_idle(hs)) {
+    x->early = true;
+    // If the launch fails, the copy engines may already hold part of the
+    // transfer: the call returns only after they have drained.
+    std::shared_ptr<Waiter> w = std::make_shared<Waiter>();
+    x->waiter = w;
+    Transfer* raw = x.get();  // the engine retires it only after the kernel (or `unlaunched`) releases it
+    e->submit(std::move(x));
+    const hipError_t err = launch_transfer(a, grid, hs);
+    if (err != hipSuccess) {
+      raw->unlaunched.store(true, std::memory_order_release);
+      std::unique_lock<std::mutex> lk(w->mu);
+      w->cv.wait(lk, [&] { return w->done; });
+      return fail(MMA_ERR_HIP, "dummy-task kernel launch failed: %s", hipGetErrorString(err));
+    }
+    return MMA_OK;
+  }
+  const hipError_t err = launch_transfer(a, grid, hs);
   if (err != hipSuccess) {
     e->release_record_unused(x.get());
     return fail(MMA_ERR_HIP, "dummy-task kernel launch failed: %s", hipGetErrorString(err));
@@ -457,7 +507,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   k.static_split = c.static_split;
   k.static_cu_percent = c.static_cu_percent;
   k.merge = c.sdma_merge_tasks ? c.sdma_merge_tasks
-                              : static_cast<uint32_t>(std::max<uint64_t>(1, 8 * MiB / c.chunk_bytes));
+                              : static_cast<uint32_t>(std::max<uint64_t>(1, 64 * MiB / c.chunk_bytes));
 
   // SDMA staging for the KV kinds: one chunk per SDMA slot, in uncached device
   // memory (coherent between the copy engines and every XCD's L2 without

@@ -377,7 +377,11 @@ class Harness {
     for (auto& e : eng_) e.reset();
   }
   // The runtime's submit(), with the fake stream in place of the kernel launch.
-  void submit(std::unique_ptr<Transfer> x, uint64_t payload, FakeStream& st, const KvGeom* kv = nullptr) {
+  // early: the stream is taken to be idle, so the transfer goes to the engine
+  // before the launch (the copy engines may start at once); with launch =
+  // false the launch then "fails" and the transfer is marked unlaunched.
+  void submit(std::unique_ptr<Transfer> x, uint64_t payload, FakeStream& st, const KvGeom* kv = nullptr,
+              bool early = false, bool launch = true) {
     Engine* e = eng_[x->dir].get();
     std::lock_guard<std::mutex> g(submit_mu_);
     CHECK(e->acquire_record(x.get(), 60000), "record");
@@ -385,12 +389,21 @@ class Harness {
     const uint32_t grid = e->prepare(x.get(), ++seq_, payload, kv, 20000ull * 1000000ull, a);
     const uint32_t waves = grid * kWavesPerWG;
     const double rate = s_.wave_rate;
+    Transfer* raw = x.get();
+    if (early && !x->self_contained) {
+      x->early = true;
+      e->submit(std::move(x));
+    }
+    if (!launch) {
+      raw->unlaunched.store(true, std::memory_order_release);
+      return;
+    }
     st.launch([a, waves, rate] {
       std::vector<std::thread> ts;
       for (uint32_t w = 0; w < waves; ++w) ts.emplace_back(wave, a, w, rate);
       for (auto& t : ts) t.join();
     });
-    e->submit(std::move(x));
+    if (x) e->submit(std::move(x));
   }
   bool sync() { return eng_[0]->wait_idle(60000) && eng_[1]->wait_idle(60000); }
   const Config& cfg() const { return cfg_; }
@@ -430,7 +443,7 @@ std::unique_ptr<Transfer> linear(int dir, void* dst, const void* src, uint64_t n
 }
 
 // ------------------------------------------------------------ scenarios
-void copies_are_exact(uint32_t mask, const char* name) {
+void copies_are_exact(uint32_t mask, const char* name, bool early = false) {
   Setup s;
   s.cfg = default_config();
   s.mask = mask;
@@ -443,7 +456,7 @@ void copies_are_exact(uint32_t mask, const char* name) {
       auto x = linear(dir, dst.data() + 32, src.data(), n, h.cfg());
       const size_t tasks = x->tasks.size();
       const uint64_t before = sum_tasks(h.stats(), 0, MMA_NUM_PATHS);
-      h.submit(std::move(x), n, st);
+      h.submit(std::move(x), n, st, nullptr, early);
       st.synchronize();
       CHECK(h.sync(), "sync");
       CHECK(std::memcmp(dst.data() + 32, src.data(), n) == 0, "%s dir=%d n=%llu: bytes differ", name, dir,
@@ -493,7 +506,7 @@ void list_with_merging() {
               (unsigned long long)cmds, (unsigned long long)sdma_tasks);
 }
 
-void kv_roundtrip(uint32_t mask, const char* name) {
+void kv_roundtrip(uint32_t mask, const char* name, bool early = false) {
   Setup s;
   s.cfg = default_config();
   s.cfg.chunk = 8 * 1024;  // 4 pieces per micro-task
@@ -513,7 +526,7 @@ void kv_roundtrip(uint32_t mask, const char* name) {
   const uint64_t host = reinterpret_cast<uint64_t>(pool.data());
   const bool sdma_ok = (mask & 0xFFFFu) != 0;
   auto x = make_kv_transfer(MMA_H2D, piece, ppb, host, host, false, sdma_ok, hs.data(), gb.data(), hs.size(), h.cfg());
-  h.submit(std::move(x), hs.size() * slot_bytes, st, &kv);
+  h.submit(std::move(x), hs.size() * slot_bytes, st, &kv, early);
   st.synchronize();
   CHECK(h.sync(), "sync");
   bool ok = true;
@@ -535,7 +548,7 @@ void kv_roundtrip(uint32_t mask, const char* name) {
   auto before = pool;
   auto y = make_kv_transfer(MMA_D2H, piece, ppb, host, host, false, sdma_ok, dest.data(), gb.data(), gb.size(),
                             h.cfg());
-  h.submit(std::move(y), gb.size() * slot_bytes, st, &kv);
+  h.submit(std::move(y), gb.size() * slot_bytes, st, &kv, early);
   st.synchronize();
   CHECK(h.sync(), "sync");
   auto want = before;
@@ -548,6 +561,30 @@ void kv_roundtrip(uint32_t mask, const char* name) {
   CHECK(h.stats().failed.load() == 0, "%s: failed", name);
   std::printf("ok   paged-KV fetch and offload (%s): staging bytes %llu, sdma commands %llu\n", name,
               (unsigned long long)h.stats().staging_bytes.load(), (unsigned long long)h.stats().sdma_commands.load());
+}
+
+// An early transfer whose dummy-task launch failed: the copy engines drain what
+// they hold, the record is retired without a kernel, no sticky error is left,
+// and the next transfer runs normally.
+void unlaunched_transfer_drains() {
+  Setup s;
+  s.cfg = default_config();
+  s.mask = MMA_PATH_CU | 0x3;
+  Harness h(s);
+  FakeStream st;
+  const uint64_t n = 8 * 1024 * 1024;
+  auto src = random_bytes(n, 5);
+  std::vector<uint8_t> dst(n, 0);
+  g_sticky.store(0);
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st, nullptr, true, false);
+  CHECK(h.sync(), "an unlaunched transfer must be retired once its copy-engine commands drained");
+  CHECK(g_sticky.load() == 0, "an unlaunched transfer must not leave a sticky error");
+  CHECK(h.stats().failed.load() == 0 && h.stats().transfers.load() == 0, "unlaunched transfers are not counted");
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st, nullptr, true);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst == src, "the transfer after an unlaunched one differs");
+  std::printf("ok   an early transfer whose launch failed drains and retires without a sticky error\n");
 }
 
 void slow_engine_gets_fewer_tasks() {
@@ -679,6 +716,10 @@ int main(int argc, char** argv) {
     list_with_merging();
     kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging");
     kv_roundtrip(MMA_PATH_CU, "CU only");
+    copies_are_exact(MMA_PATH_CU | 0x3, "CU + 2 engines, idle-stream early start", true);
+    copies_are_exact(0x3, "2 engines, idle-stream early start", true);
+    kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging, idle-stream early start", true);
+    unlaunched_transfer_drains();
     submit_failures_rerouted();
     two_streams_both_directions();
   }
