@@ -103,6 +103,15 @@ typedef struct mma_config {
                                engine's fair share of the transfer's remaining work; default:
                                64 MiB worth (max(1, 64 MiB / chunk_bytes)); 1 = one command per
                                micro-task */
+  uint32_t cu_whole_bytes;  /* host->device: a copy or tensor list of at most this many bytes,
+                               whose micro-tasks fit one launch (at most 48 CU entries), is carried
+                               by the CU path alone in a dummy-task launch that needs no host round
+                               trip (no start signal, no completion wait) -- below this size the
+                               setup of several paths costs more than it gains (Section 3.2
+                               fallback); default 24 MiB; 1 keeps every transfer on the multipath
+                               engine */
+  uint32_t cu_whole_bytes_d2h; /* the same for device->host; default 8 MiB (CU stores to host
+                               memory reach the link less efficiently than CU loads, measured) */
   uint32_t reserved;
 } mma_config_t;
 

@@ -53,6 +53,7 @@ class mma_config_t(ctypes.Structure):
                 ("cu_workgroups", ctypes.c_uint32), ("cu_sub_bytes", ctypes.c_uint32),
                 ("watchdog_ms", ctypes.c_uint32), ("static_split", ctypes.c_uint32),
                 ("static_cu_percent", ctypes.c_uint32), ("sdma_merge_tasks", ctypes.c_uint32),
+                ("cu_whole_bytes", ctypes.c_uint32), ("cu_whole_bytes_d2h", ctypes.c_uint32),
                 ("reserved", ctypes.c_uint32)]
 
     def as_dict(self):

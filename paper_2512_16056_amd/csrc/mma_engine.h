@@ -80,6 +80,9 @@ inline uint64_t env_u64(const char* name, uint64_t dflt) {
 
 constexpr uint64_t KiB = 1024, MiB = 1024 * 1024;
 constexpr uint64_t kSmallSub = 16 * KiB;  // one wave register batch
+// CU entry size behind the default size limit of transfers taken whole by the
+// CU path: kPrefill entries of this size travel in the launch arguments (24 MiB).
+constexpr uint64_t kWholeMaxSub = 512 * KiB;
 
 // ------------------------------------------------------------------ transfer
 enum class Kind : uint8_t { kLinear, kKvFetch, kKvOffload };
@@ -120,6 +123,7 @@ struct Transfer {
   uint32_t waves = 0;          // waves of the dummy-task kernel
   bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
   bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
+  bool whole = false;          // the CU path claims every micro-task at prefill
   // Submitted on a stream with nothing pending: the engine may start the copy
   // engines at once, without waiting for the kernel's start signal.
   bool early = false;
@@ -185,6 +189,7 @@ struct Config {
   uint32_t mask[2];
   uint32_t static_split, static_cu_percent;
   uint32_t merge;       // max micro-tasks per copy-engine command
+  uint64_t whole[2];    // per direction: transfers up to this size may be taken whole by the CU path (0: never)
 };
 
 struct Stats {
@@ -408,12 +413,25 @@ class Engine {
     const bool needs_cu = cu_enabled() || staged ||
                           std::any_of(x->tasks.begin(), x->tasks.end(),
                                       [](const Task& t) { return (t.flags & kPlanCuOnly) != 0; });
-    // CU ring entries of a linear transfer are cu_sub_bytes. A transfer that can
-    // fit the launch's prefilled entries is cut finer (16 KiB steps, one wave
-    // register batch), so that more waves share it and it costs about one PCIe
-    // round trip.
+    // CU ring entries of a linear transfer are cu_sub_bytes. A transfer of at
+    // most cfg.whole[dir] bytes whose micro-tasks can all travel in the launch's
+    // arguments (at most kPrefill entries) is taken whole by the CU path, each
+    // micro-task cut into at most kPrefill / tasks entries of whole 16 KiB steps
+    // (one wave register batch): the kernel is then the transfer's only copy
+    // engine and needs no host round trip at all -- no start signal, no ring, no
+    // wait for `complete` -- which at these sizes is worth more than the copy
+    // engines' slightly better link efficiency. Otherwise a transfer that fits
+    // the prefilled entries is still cut into 16 KiB steps, so that more waves
+    // share it.
     x->sub = cfg_.sub;
-    if (!kv && payload_bytes <= kPrefill * cfg_.sub) {
+    if (!kv && cu_enabled() && !cfg_.static_split && x->tasks.size() <= kPrefill && payload_bytes <= cfg_.whole[dir_]) {
+      const uint64_t per_task = kPrefill / x->tasks.size();
+      uint64_t biggest = 0;
+      for (const Task& t : x->tasks) biggest = std::max(biggest, t.bytes);
+      const uint64_t sub = (biggest + per_task - 1) / per_task;
+      x->sub = std::max<uint64_t>(kSmallSub, (sub + kSmallSub - 1) / kSmallSub * kSmallSub);
+      x->whole = true;
+    } else if (!kv && payload_bytes <= kPrefill * cfg_.sub) {
       const uint64_t per = (payload_bytes + kPrefill - 1) / kPrefill;
       x->sub = std::min<uint64_t>(cfg_.sub,
                                   std::max<uint64_t>(kSmallSub, (per + kSmallSub - 1) / kSmallSub * kSmallSub));
@@ -558,7 +576,7 @@ class Engine {
     if (x->failed || x->ignored || x->aborting) return false;
     const bool any = cu_enabled() || x->pool_dev;
     // An HBM-resident pool keeps every wave busy: two micro-tasks per wave outstanding.
-    const uint32_t depth = x->pool_dev ? 2 * x->waves : cfg_.cu_depth;
+    const uint32_t depth = x->whole ? ~0u : (x->pool_dev ? 2 * x->waves : cfg_.cu_depth);
     bool p = false;
     while (true) {
       if (x->cu_busy >= depth) x->cu_full = true;

@@ -397,6 +397,8 @@ void fill_config(mma_config_t* c, bool use_env) {
   d.cu_workgroups = 16;
   d.cu_sub_bytes = 64 * KiB;
   d.watchdog_ms = 20000;
+  d.cu_whole_bytes = static_cast<uint32_t>(kPrefill * kWholeMaxSub);
+  d.cu_whole_bytes_d2h = static_cast<uint32_t>(8 * MiB);
   if (use_env) {
     d.chunk_bytes = env_u64("MMA_CHUNK_BYTES", d.chunk_bytes);
     d.fallback_bytes = env_u64("MMA_FALLBACK_BYTES", 0);
@@ -410,6 +412,8 @@ void fill_config(mma_config_t* c, bool use_env) {
     d.cu_sub_bytes = static_cast<uint32_t>(env_u64("MMA_CU_SUB_BYTES", d.cu_sub_bytes));
     d.watchdog_ms = static_cast<uint32_t>(env_u64("MMA_WATCHDOG_MS", d.watchdog_ms));
     d.sdma_merge_tasks = static_cast<uint32_t>(env_u64("MMA_SDMA_MERGE_TASKS", 0));
+    d.cu_whole_bytes = static_cast<uint32_t>(env_u64("MMA_CU_WHOLE_BYTES", d.cu_whole_bytes));
+    d.cu_whole_bytes_d2h = static_cast<uint32_t>(env_u64("MMA_CU_WHOLE_BYTES_D2H", d.cu_whole_bytes_d2h));
   }
   *c = d;
 }
@@ -448,6 +452,8 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
     if (!c.cu_workgroups) c.cu_workgroups = d.cu_workgroups;
     if (!c.cu_sub_bytes) c.cu_sub_bytes = d.cu_sub_bytes;
     if (!c.watchdog_ms) c.watchdog_ms = d.watchdog_ms;
+    if (!c.cu_whole_bytes) c.cu_whole_bytes = d.cu_whole_bytes;
+    if (!c.cu_whole_bytes_d2h) c.cu_whole_bytes_d2h = d.cu_whole_bytes_d2h;
   } else {
     fill_config(&c, true);
   }
@@ -506,6 +512,8 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   if (c.static_cu_percent > 100) return fail(MMA_ERR_INVALID_ARG, "static_cu_percent > 100");
   k.static_split = c.static_split;
   k.static_cu_percent = c.static_cu_percent;
+  k.whole[MMA_H2D] = c.cu_whole_bytes;
+  k.whole[MMA_D2H] = c.cu_whole_bytes_d2h;
   k.merge = c.sdma_merge_tasks ? c.sdma_merge_tasks
                               : static_cast<uint32_t>(std::max<uint64_t>(1, 64 * MiB / c.chunk_bytes));
 

@@ -563,6 +563,45 @@ void kv_roundtrip(uint32_t mask, const char* name, bool early = false) {
               (unsigned long long)h.stats().staging_bytes.load(), (unsigned long long)h.stats().sdma_commands.load());
 }
 
+// Transfers up to cfg.whole bytes whose micro-tasks fit one launch are taken
+// whole by the CU path: self-contained launches, no copy-engine command, one
+// wave per entry, at most kPrefill entries; larger ones still use every path.
+void whole_transfers_on_cu() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.whole[0] = s.cfg.whole[1] = 4 * 1024 * 1024;
+  s.mask = MMA_PATH_CU | 0x3;
+  Harness h(s);
+  FakeStream st;
+  for (int dir = 0; dir < 2; ++dir) {
+    for (uint64_t n : {1ull, 100000ull, 3ull * 1024 * 1024 + 7, 4ull * 1024 * 1024}) {
+      auto src = random_bytes(n, static_cast<uint32_t>(n + 3 * dir));
+      std::vector<uint8_t> dst(n + 64, 0xA5);
+      const uint64_t cmds = h.stats().sdma_commands.load();
+      auto x = linear(dir, dst.data() + 32, src.data(), n, h.cfg());
+      h.submit(std::move(x), n, st);
+      st.synchronize();
+      CHECK(h.sync(), "sync");
+      CHECK(std::memcmp(dst.data() + 32, src.data(), n) == 0, "whole dir=%d n=%llu: bytes differ", dir,
+            (unsigned long long)n);
+      CHECK(dst[31] == 0xA5 && dst[32 + n] == 0xA5, "whole: bytes outside the destination changed");
+      CHECK(h.stats().sdma_commands.load() == cmds, "whole dir=%d n=%llu: a copy engine took part", dir,
+            (unsigned long long)n);
+    }
+  }
+  // Above the limit every path takes part again.
+  const uint64_t n = 6 * 1024 * 1024;
+  auto src = random_bytes(n, 99);
+  std::vector<uint8_t> dst(n, 0);
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst == src, "6 MiB copy differs");
+  CHECK(h.stats().sdma_commands.load() > 0, "above the whole-transfer limit the copy engines take part");
+  CHECK(h.stats().failed.load() == 0, "whole: failed transfers");
+  std::printf("ok   transfers up to the whole-transfer limit run as self-contained CU launches\n");
+}
+
 // An early transfer whose dummy-task launch failed: the copy engines drain what
 // they hold, the record is retired without a kernel, no sticky error is left,
 // and the next transfer runs normally.
@@ -720,6 +759,7 @@ int main(int argc, char** argv) {
     copies_are_exact(0x3, "2 engines, idle-stream early start", true);
     kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging, idle-stream early start", true);
     unlaunched_transfer_drains();
+    whole_transfers_on_cu();
     submit_failures_rerouted();
     two_streams_both_directions();
   }

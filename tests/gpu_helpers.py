@@ -10,11 +10,13 @@ import torch
 
 import paper_2512_16056_amd as mma
 
-# Path sets exercised by the parity tests: CU path only, SDMA engines only, both.
+# Path sets exercised by the parity tests: CU path only (small transfers then run as
+# self-contained launches), SDMA engines only, both -- with every transfer kept on the
+# multipath engine (cu_whole_bytes[_d2h]=1), so that small cases still mix the paths.
 PATHS = {
     "cu": dict(path_mask_h2d=mma.MMA_PATH_CU, path_mask_d2h=mma.MMA_PATH_CU),
     "sdma": dict(path_mask_h2d=0x3, path_mask_d2h=0x3),
-    "both": dict(),
+    "both": dict(cu_whole_bytes=1, cu_whole_bytes_d2h=1),
 }
 
 

@@ -100,6 +100,84 @@ def test_copy_64mib(paths, direction):
     log(f"  path bytes: cu={stats['path_bytes'][16]} sdma={stats['path_bytes'][:4]}")
 
 
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+def test_whole_transfers_on_cu_path(direction):
+    """Default configuration around the size limit of transfers taken whole by the CU path
+    (24 MiB host->device, 8 MiB device->host, and at most 48 CU entries): below it no copy
+    engine takes part, above it they do; every byte matches the oracle, poison outside the
+    destination stays."""
+    limit = (24 << 20) if direction == mma.MMA_H2D else (8 << 20)
+    cases = [(3 << 20) + 1, 4 << 20, limit - 5, limit, limit + 1]
+    pad = 4096
+    with session("both", cu_whole_bytes=0, cu_whole_bytes_d2h=0):  # 0: the default limits
+        cfg = mma.mma_get_config()
+        assert (cfg.cu_whole_bytes, cfg.cu_whole_bytes_d2h) == (24 << 20, 8 << 20)
+        for n in cases:
+            log(f"whole transfer n={n} dir={direction}")
+            src_np = np.ascontiguousarray(W.uniform_bytes(13, direction, n, n + 16))
+            mma.mma_synchronize()
+            mma.mma_reset_stats()
+            if direction == mma.MMA_H2D:
+                src = mma.PinnedBuffer(n + 16)
+                src.array[:] = src_np
+                dst = device_bytes(n + 2 * pad, W.WEIGHT_POISON)
+                mma.mma_memcpy_async(dst.data_ptr() + pad + 3, src.ptr + 3, n, direction)
+                torch.cuda.synchronize()
+                got = to_host(dst)
+            else:
+                src = from_host(src_np)
+                dst = mma.PinnedBuffer(n + 2 * pad)
+                dst.array[:] = W.WEIGHT_POISON
+                mma.mma_memcpy_async(dst.ptr + pad + 3, src.data_ptr() + 3, n, direction)
+                torch.cuda.synchronize()
+                got = dst.array.copy()
+            mma.mma_synchronize()
+            st = mma.mma_get_stats()
+            want = ocopy.memcpy(np.full(n + 2 * pad, W.WEIGHT_POISON, np.uint8), pad + 3, src_np, 3, n)
+            assert np.array_equal(got, want), n
+            assert st["failed_transfers"] == 0
+            if n <= limit:
+                assert st["sdma_commands"] == 0 and st["path_bytes"][16] == n, (n, st["path_bytes"])
+            else:
+                assert st["sdma_commands"] > 0, n
+            if direction == mma.MMA_D2H:
+                dst.free()
+            else:
+                src.free()
+        # tensor lists: 48 tensors fit one launch, 49 do not
+        for count in (48, 49):
+            sizes = [100 * 1024 + 16 * k for k in range(count)]
+            offs, total = W.arena_offsets(sizes, 256)
+            host = mma.PinnedBuffer(total)
+            host.array[:] = W.uniform_bytes(14, count, direction, total)
+            devs = [device_bytes(z + 64, W.WEIGHT_POISON) for z in sizes]
+            mma.mma_synchronize()
+            mma.mma_reset_stats()
+            if direction == mma.MMA_H2D:
+                mma.mma_weights_load([(devs[t], host.ptr + offs[t], z) for t, z in enumerate(sizes)], direction)
+            else:
+                for t, z in enumerate(sizes):
+                    devs[t][:z] = torch.from_numpy(host.array[offs[t]:offs[t] + z].copy()).cuda()
+                back = mma.PinnedBuffer(total)
+                back.array[:] = W.WEIGHT_POISON
+                mma.mma_weights_load([(back.ptr + offs[t], devs[t], z) for t, z in enumerate(sizes)], direction)
+            torch.cuda.synchronize()
+            mma.mma_synchronize()
+            st = mma.mma_get_stats()
+            for t, z in enumerate(sizes):
+                if direction == mma.MMA_H2D:
+                    got = to_host(devs[t])
+                    want = ocopy.memcpy(np.full(z + 64, W.WEIGHT_POISON, np.uint8), 0, host.array, offs[t], z)
+                else:
+                    got = back.array[offs[t]:offs[t] + z]
+                    want = host.array[offs[t]:offs[t] + z]
+                assert np.array_equal(got, want), (count, t)
+            assert (st["sdma_commands"] == 0) == (count == 48), (count, st["sdma_commands"])
+            host.free()
+            if direction == mma.MMA_D2H:
+                back.free()
+
+
 def _ragged_list(seed, count, max_size):
     r = np.random.default_rng(seed)
     sizes = [int(x) for x in r.integers(0, max_size, count)]
