@@ -13,7 +13,7 @@ the same workload, native hipMemcpyAsync comparators, and the 64 MiB single-copy
 workload.
 
 Usage: python bench.py [--gpus 1] [--steps 10] [--warmup 2]
-       python bench.py --sweep sizes|chunks|contention|duplex|paths|footprint  (JSON per point)
+       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint  (JSON per point)
        python bench.py --calib                                  (counter-scaling kernels)
 """
 from __future__ import annotations
@@ -44,7 +44,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true", help="skip native comparators and the 64 MiB copy")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle timing window")
-    p.add_argument("--sweep", choices=["sizes", "chunks", "contention", "duplex", "paths", "footprint"],
+    p.add_argument("--sweep", choices=["sizes", "idle", "chunks", "contention", "duplex", "paths", "footprint"],
                    help="instead of the benchmark, print one JSON line per point of a parameter sweep")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
@@ -426,6 +426,52 @@ def sweep_sizes():
     mma.mma_finalize()
 
 
+def sweep_idle():
+    """Host wall time from the call to the return of hipStreamSynchronize, on a stream with nothing
+    pending (the case of the idle-stream early start), for the default multipath configuration and
+    one hipMemcpyAsync, alternating; median of 50 after 10 discarded. Also the share of transfers
+    whose copy engines started before the kernel's start signal (trace: started < 3 us after
+    submission)."""
+    import ctypes
+    import numpy as np
+    mma, torch, nat, st = _sweep_env()
+    mma.mma_init(0)
+    top = 64 << 20
+    h = mma.PinnedBuffer(top)
+    h.array[::4096] = 1
+    d = torch.empty(top, dtype=torch.uint8, device="cuda")
+    sp = ctypes.c_void_p(st.cuda_stream)
+    for n in (4 << 20, 8 << 20, 16 << 20, 32 << 20, 64 << 20):
+        row = {"bytes": n}
+        for dr, name in ((0, "h2d"), (1, "d2h")):
+            dst, src = (d.data_ptr(), h.ptr) if dr == 0 else (h.ptr, d.data_ptr())
+            D, S, Z = (ctypes.c_void_p * 1)(dst), (ctypes.c_void_p * 1)(src), (ctypes.c_uint64 * 1)(n)
+            margs = (ctypes.c_void_p(dst), ctypes.c_void_p(src), ctypes.c_uint64(n), dr, sp)
+            tn, tm = [], []
+            mma.mma_trace_enable(True)
+            for _ in range(60):
+                st.synchronize()
+                t0 = time.perf_counter()
+                nat.native_list(D, S, Z, 1, dr, sp)
+                st.synchronize()
+                tn.append((time.perf_counter() - t0) * 1e6)
+                time.sleep(0.0002)
+                t0 = time.perf_counter()
+                _ok(mma.lib.mma_memcpy_async(*margs))
+                st.synchronize()
+                tm.append((time.perf_counter() - t0) * 1e6)
+            mma.mma_synchronize()
+            tr = mma.mma_trace_read()[-60:]
+            mma.mma_trace_enable(False)
+            early = sum(1 for r in tr if r["t_started_ns"] and r["t_started_ns"] - r["t_submit_ns"] < 3000)
+            m, nt = float(np.median(tm[10:])), float(np.median(tn[10:]))
+            row[name] = {"mma_us": round(m, 1), "native_us": round(nt, 1), "ratio_vs_native": round(nt / m, 3),
+                         "early_start_frac": round(early / max(1, len(tr)), 2)}
+        _emit(sweep="idle", **row)
+    h.free()
+    mma.mma_finalize()
+
+
 def sweep_chunks():
     """Chunk size x outstanding-queue depth on a 512 MiB copy (the paper's sensitivity study,
     Section 5.3): H2D and D2H GB/s, default path set."""
@@ -751,7 +797,7 @@ def sweep_footprint():
         mma.mma_finalize()
     h.free()
 
-SWEEPS = {"sizes": sweep_sizes, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
+SWEEPS = {"sizes": sweep_sizes, "idle": sweep_idle, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
           "paths": sweep_paths, "footprint": sweep_footprint}
 
 
