@@ -23,6 +23,18 @@ Every other GPU block (fetch) or host slot (offload) is unchanged. Table validit
 reading; the paper is silent): entries in range, and no destination named twice,
 since two sources racing into one block would make the result path-dependent.
 Sources may repeat.
+
+GPU block layouts (``layout``; the host side is always token-major
+``[block_tokens][kv_heads][head_dim]`` per piece):
+
+* ``LAYOUT_PIECE`` (0): the GPU block holds the piece exactly as the host does;
+* ``LAYOUT_XPACKED`` (1): the layout of paged-attention decode kernels, where a
+  block's key is ``[kv_heads][head_dim / x][block_tokens][x]`` with ``x = 16 //
+  elem_bytes`` (16-byte groups of consecutive dims, token-minor), and its value is
+  ``[kv_heads][head_dim][block_tokens]`` (token-minor). ``head_dim * elem_bytes``
+  must be a multiple of 16.
+
+Both are readings: the paper names the KV-cache systems but not their layouts.
 """
 from __future__ import annotations
 
@@ -47,13 +59,54 @@ def validate_tables(src_idx: Sequence[int], src_count: int,
     return True
 
 
+LAYOUT_PIECE = 0
+LAYOUT_XPACKED = 1
+
+
+def piece_to_block(piece: np.ndarray, k: int, layout: int, geom) -> np.ndarray:
+    """GPU block bytes of one layer's K (k=0) or V (k=1) piece given in the host's
+    token-major layout. ``geom`` = (block_tokens, kv_heads, head_dim, elem_bytes)."""
+    piece = np.asarray(piece, dtype=np.uint8).reshape(-1)
+    if layout == LAYOUT_PIECE:
+        return piece.copy()
+    if layout != LAYOUT_XPACKED:
+        raise ValueError("unknown layout")
+    B, H, D, E = geom
+    if (D * E) % 16:
+        raise ValueError("head_dim * elem_bytes must be a multiple of 16")
+    x = 16 // E
+    a = piece.reshape(B, H, D, E)
+    if k == 0:  # key: [H][D/x][B][x]
+        return np.ascontiguousarray(a.reshape(B, H, D // x, x, E).transpose(1, 2, 0, 3, 4)).reshape(-1)
+    return np.ascontiguousarray(a.transpose(1, 2, 0, 3)).reshape(-1)  # value: [H][D][B]
+
+
+def block_to_piece(block: np.ndarray, k: int, layout: int, geom) -> np.ndarray:
+    """Inverse of piece_to_block: the host (token-major) bytes of a GPU block's K or V."""
+    block = np.asarray(block, dtype=np.uint8).reshape(-1)
+    if layout == LAYOUT_PIECE:
+        return block.copy()
+    if layout != LAYOUT_XPACKED:
+        raise ValueError("unknown layout")
+    B, H, D, E = geom
+    if (D * E) % 16:
+        raise ValueError("head_dim * elem_bytes must be a multiple of 16")
+    x = 16 // E
+    if k == 0:
+        a = block.reshape(H, D // x, B, x, E).transpose(2, 0, 1, 3, 4)
+    else:
+        a = block.reshape(H, D, B, E).transpose(2, 0, 1, 3)
+    return np.ascontiguousarray(a).reshape(-1)
+
+
 def _pool_view(host_pool: np.ndarray, layers: int) -> np.ndarray:
     slots = host_pool.shape[0]
     return host_pool.reshape(slots, layers, 2, -1)
 
 
 def kv_fetch_layer(host_pool: np.ndarray, layer_before: np.ndarray, l: int, layers: int,
-                   host_slots: Sequence[int], gpu_blocks: Sequence[int]) -> np.ndarray:
+                   host_slots: Sequence[int], gpu_blocks: Sequence[int],
+                   layout: int = LAYOUT_PIECE, geom=None) -> np.ndarray:
     """Expected GPU layer tensor ``l`` (shape [2, NB, piece]) after a fetch."""
     pool = _pool_view(host_pool, layers)
     nb = layer_before.shape[1]
@@ -62,19 +115,22 @@ def kv_fetch_layer(host_pool: np.ndarray, layer_before: np.ndarray, l: int, laye
     out = np.array(layer_before, dtype=np.uint8, copy=True)
     for i in range(len(host_slots)):
         for k in (0, 1):
-            out[k, int(gpu_blocks[i])] = pool[int(host_slots[i]), l, k]
+            out[k, int(gpu_blocks[i])] = piece_to_block(pool[int(host_slots[i]), l, k], k, layout, geom)
     return out
 
 
 def kv_fetch(host_pool: np.ndarray, layers_before: List[np.ndarray],
-             host_slots: Sequence[int], gpu_blocks: Sequence[int]) -> List[np.ndarray]:
+             host_slots: Sequence[int], gpu_blocks: Sequence[int],
+             layout: int = LAYOUT_PIECE, geom=None) -> List[np.ndarray]:
     """Expected GPU layer tensors after a fetch (all layers)."""
     L = len(layers_before)
-    return [kv_fetch_layer(host_pool, layers_before[l], l, L, host_slots, gpu_blocks) for l in range(L)]
+    return [kv_fetch_layer(host_pool, layers_before[l], l, L, host_slots, gpu_blocks, layout, geom)
+            for l in range(L)]
 
 
 def kv_offload(host_pool_before: np.ndarray, layers: List[np.ndarray],
-               gpu_blocks: Sequence[int], host_slots: Sequence[int]) -> np.ndarray:
+               gpu_blocks: Sequence[int], host_slots: Sequence[int],
+               layout: int = LAYOUT_PIECE, geom=None) -> np.ndarray:
     """Expected host pool (shape [S, slot_bytes]) after an offload."""
     L = len(layers)
     nb = layers[0].shape[1]
@@ -85,7 +141,7 @@ def kv_offload(host_pool_before: np.ndarray, layers: List[np.ndarray],
     for j in range(len(host_slots)):
         for l in range(L):
             for k in (0, 1):
-                pool[int(host_slots[j]), l, k] = layers[l][k, int(gpu_blocks[j])]
+                pool[int(host_slots[j]), l, k] = block_to_piece(layers[l][k, int(gpu_blocks[j])], k, layout, geom)
     return out
 
 

@@ -188,6 +188,96 @@ def test_kv_offload_slot_layout():
     assert slot.tolist() == [x for l in range(L) for x in pieces[l].reshape(-1).tolist()]
 
 
+# ----------------------------------------------------------------------------- x-packed KV layout
+XP = okv.LAYOUT_XPACKED
+
+
+@pytest.mark.parametrize("name", ["bytes1", "elem2"])
+def test_kv_xpacked_golden(golden_dir, name):
+    g = parse_golden(os.path.join(golden_dir, "kv_xpacked_tiny.txt"))[name]
+    geom = (g["B"], g["H"], g["D"], g["E"])
+    host = np.array(g["host"], np.uint8)
+    assert okv.piece_to_block(host, 0, XP, geom).tolist() == g["key"]
+    assert okv.piece_to_block(host, 1, XP, geom).tolist() == g["value"]
+    assert okv.block_to_piece(np.array(g["key"], np.uint8), 0, XP, geom).tolist() == g["host"]
+    assert okv.block_to_piece(np.array(g["value"], np.uint8), 1, XP, geom).tolist() == g["host"]
+
+
+XP_SHAPES = [(1, 2, 1, 8, 2), (2, 2, 2, 16, 2), (1, 3, 2, 16, 1), (2, 4, 1, 4, 4), (1, 16, 2, 8, 2), (1, 5, 3, 32, 1)]
+
+
+@pytest.mark.parametrize("shape", XP_SHAPES)
+def test_kv_xpacked_matches_naive(shape):
+    L, B, H, D, E = shape
+    S, NB = 3, 4
+    host, layers = _tiny(L, B, H, D, E, S, NB, seed=7 + sum(shape))
+    slots, blocks = [2, 0, 1], [3, 1, 0]
+    geom = (B, H, D, E)
+    got = okv.kv_fetch(host, layers, slots, blocks, XP, geom)
+    want = onaive.fetch(host.tobytes(), [x.tobytes() for x in layers], slots, blocks, L, B, H, D, E, NB, layout=1)
+    assert all(got[l].tobytes() == bytes(want[l]) for l in range(L))
+    got = okv.kv_offload(host, layers, blocks, slots, XP, geom)
+    want = onaive.offload(host.tobytes(), [x.tobytes() for x in layers], blocks, slots, L, B, H, D, E, NB, layout=1)
+    assert got.tobytes() == bytes(want)
+
+
+def test_kv_xpacked_all_permutations_naive():
+    L, B, H, D, E, S, NB = 1, 2, 2, 8, 2, 4, 5
+    host, layers = _tiny(L, B, H, D, E, S, NB, seed=21)
+    geom = (B, H, D, E)
+    for perm in itertools.permutations(range(4)):
+        got = okv.kv_fetch(host, layers, list(perm), [4, 0, 2, 3], XP, geom)
+        want = onaive.fetch(host.tobytes(), [x.tobytes() for x in layers], list(perm), [4, 0, 2, 3],
+                            L, B, H, D, E, NB, layout=1)
+        assert got[0].tobytes() == bytes(want[0])
+
+
+def test_kv_xpacked_single_token_block_is_the_host_layout():
+    # With one token per block, [H][D/x][1][x] and [H][D][1] are the host order [1][H][D].
+    r = np.random.default_rng(5)
+    for H, D, E in [(1, 8, 2), (4, 16, 2), (3, 16, 1), (2, 4, 4)]:
+        piece = r.integers(0, 256, H * D * E, dtype=np.uint8)
+        for k in (0, 1):
+            assert np.array_equal(okv.piece_to_block(piece, k, XP, (1, H, D, E)), piece)
+
+
+def test_kv_xpacked_value_is_a_per_head_transpose():
+    # Per head, the value block [D][B] is the transpose of the host's [B][D] rows taken at
+    # stride H*D elements -- written with explicit Python loops over elements.
+    B, H, D, E = 4, 3, 8, 2
+    r = np.random.default_rng(9)
+    piece = r.integers(0, 256, B * H * D * E, dtype=np.uint8)
+    blk = okv.piece_to_block(piece, 1, XP, (B, H, D, E))
+    for h in range(H):
+        for d in range(D):
+            for t in range(B):
+                src = ((t * H + h) * D + d) * E
+                dst = ((h * D + d) * B + t) * E
+                assert blk[dst:dst + E].tolist() == piece[src:src + E].tolist()
+
+
+def test_kv_xpacked_roundtrip_and_rejects():
+    r = np.random.default_rng(13)
+    for B, H, D, E in [(16, 8, 128, 2), (3, 2, 16, 1), (2, 2, 8, 4)]:
+        piece = r.integers(0, 256, B * H * D * E, dtype=np.uint8)
+        for k in (0, 1):
+            blk = okv.piece_to_block(piece, k, XP, (B, H, D, E))
+            assert sorted(blk.tolist()) == sorted(piece.tolist())
+            assert np.array_equal(okv.block_to_piece(blk, k, XP, (B, H, D, E)), piece)
+    with pytest.raises(ValueError):
+        okv.piece_to_block(np.zeros(2 * 1 * 6 * 2, np.uint8), 0, XP, (2, 1, 6, 2))  # 12-byte rows
+    s = W.small_kv_shape(head_dim=16)
+    geom = (s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes)
+    host = r.integers(0, 256, (s.host_num_slots, s.slot_bytes), dtype=np.uint8)
+    layers = [np.full((2, s.gpu_num_blocks, s.piece_bytes), W.GPU_POISON, np.uint8) for _ in range(s.layers)]
+    slots, blocks = W.kv_fetch_tables(s)
+    fetched = okv.kv_fetch(host, layers, slots, blocks, XP, geom)
+    untouched = np.setdiff1d(np.arange(s.gpu_num_blocks), blocks)
+    assert all(np.all(fetched[l][:, untouched] == W.GPU_POISON) for l in range(s.layers))
+    back = okv.kv_offload(np.zeros_like(host), fetched, blocks, slots, XP, geom)
+    assert np.array_equal(back[slots], host[slots])
+
+
 # ----------------------------------------------------------------------------- plan
 def test_plan_counts_golden(golden_dir):
     g = dict(parse_pairs(os.path.join(golden_dir, "plan_counts.txt")))
