@@ -121,11 +121,24 @@ typedef struct mma_copy_desc {
   uint64_t bytes;
 } mma_copy_desc_t;
 
-/* Paged KV layout (Section 2.1 KV offload/fetch; the layout itself is a
- * reading, the paper does not state it):
- *   piece     = block_tokens * kv_heads * head_dim * elem_bytes bytes;
+/* Paged KV layout (Section 2.1 KV offload/fetch; the layouts themselves are
+ * readings, the paper does not state them):
+ *   piece     = block_tokens * kv_heads * head_dim * elem_bytes bytes: one layer's
+ *               K or V of one block, token-major [block_tokens][kv_heads][head_dim]
+ *               in host memory;
  *   host pool = host_num_slots slots, slot s = [num_layers][2 (K,V)][piece];
- *   GPU layer l (one pointer per layer) = [2 (K,V)][gpu_num_blocks][piece]. */
+ *   GPU layer l (one pointer per layer) = [2 (K,V)][gpu_num_blocks][block], where a
+ *               block holds one piece in the GPU block layout `gpu_layout`:
+ *     MMA_KV_LAYOUT_PIECE   (0): as in host memory;
+ *     MMA_KV_LAYOUT_XPACKED (1): the layout of paged-attention decode kernels --
+ *               key [kv_heads][head_dim / x][block_tokens][x] with x = 16 / elem_bytes,
+ *               value [kv_heads][head_dim][block_tokens]. Needs elem_bytes in
+ *               {1, 2, 4, 8}, head_dim * elem_bytes and block_tokens * elem_bytes
+ *               multiples of 16, a 16-byte-aligned pool and layer tensors, and
+ *               block_tokens * (head_dim * elem_bytes + 16) <= 36 KiB (one head of
+ *               one block fits a wave's LDS tile); otherwise MMA_ERR_INVALID_ARG. */
+#define MMA_KV_LAYOUT_PIECE 0u
+#define MMA_KV_LAYOUT_XPACKED 1u
 typedef struct mma_kv_layout {
   uint32_t num_layers;
   uint32_t block_tokens;
@@ -134,7 +147,7 @@ typedef struct mma_kv_layout {
   uint32_t elem_bytes;
   uint32_t gpu_num_blocks;
   uint32_t host_num_slots;
-  uint32_t reserved;
+  uint32_t gpu_layout;    /* MMA_KV_LAYOUT_PIECE (0) or MMA_KV_LAYOUT_XPACKED */
 } mma_kv_layout_t;
 
 typedef struct mma_stats {

@@ -24,6 +24,8 @@ MMA_OK = 0
 MMA_H2D = 0
 MMA_D2H = 1
 MMA_PATH_CU = 0x80000000
+MMA_KV_LAYOUT_PIECE = 0
+MMA_KV_LAYOUT_XPACKED = 1
 MMA_NUM_PATHS = 17
 MMA_FAULT_ENGINE_STALL_US = 1
 MMA_FAULT_SDMA_SUBMIT_FAIL = 2
@@ -68,7 +70,7 @@ class mma_kv_layout_t(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_uint32), ("block_tokens", ctypes.c_uint32),
                 ("kv_heads", ctypes.c_uint32), ("head_dim", ctypes.c_uint32),
                 ("elem_bytes", ctypes.c_uint32), ("gpu_num_blocks", ctypes.c_uint32),
-                ("host_num_slots", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+                ("host_num_slots", ctypes.c_uint32), ("gpu_layout", ctypes.c_uint32)]
 
 
 class mma_stats_t(ctypes.Structure):
@@ -274,10 +276,10 @@ def mma_weights_load(copies: Sequence[Tuple[object, object, int]], direction: in
     _check(lib.mma_weights_load(arr, n, direction, _stream(stream)), "mma_weights_load")
 
 
-def kv_layout(num_layers, block_tokens, kv_heads, head_dim, elem_bytes, gpu_num_blocks, host_num_slots
-              ) -> mma_kv_layout_t:
+def kv_layout(num_layers, block_tokens, kv_heads, head_dim, elem_bytes, gpu_num_blocks, host_num_slots,
+              gpu_layout: int = 0) -> mma_kv_layout_t:
     return mma_kv_layout_t(num_layers, block_tokens, kv_heads, head_dim, elem_bytes, gpu_num_blocks,
-                           host_num_slots, 0)
+                           host_num_slots, gpu_layout)
 
 
 def _layers(gpu_layers) -> ctypes.Array:

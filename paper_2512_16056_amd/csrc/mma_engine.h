@@ -248,6 +248,8 @@ struct Backend {
 struct KvGeom {
   uint64_t piece = 0, kstride = 0;
   uint32_t layers = 0;
+  uint32_t layout = kKvLayoutPiece;
+  uint32_t tokens = 0, heads = 0, row_bytes = 0, elem = 0, lds_wave = 0;  // x-packed layout
   uint64_t layer_ptr[kMaxLayers];
 };
 
@@ -463,6 +465,12 @@ class Engine {
       a.kv_piece_bytes = kv->piece;
       a.kv_kstride = kv->kstride;
       a.kv_layers = kv->layers;
+      a.kv_layout = kv->layout;
+      a.kv_tokens = kv->tokens;
+      a.kv_heads = kv->heads;
+      a.kv_row_bytes = kv->row_bytes;
+      a.kv_elem = kv->elem;
+      a.kv_lds_wave = kv->lds_wave;
       memcpy(a.layer_ptr, kv->layer_ptr, sizeof(uint64_t) * kv->layers);
     }
     a.rec = rec_dev(x->rec_idx);

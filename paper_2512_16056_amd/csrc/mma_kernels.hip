@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 
 #include "mma_proto.h"
+#include "mma_xpacked.h"
 
 namespace mma {
 namespace {
@@ -136,9 +137,160 @@ __device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8
   if (lane < tail) dst[base + lane] = src[base + lane];
 }
 
-}  // namespace
+// ---------------------------------------------------------------- x-packed KV layout
+// A paged-KV piece in the x-packed layout: key [H][R/16][B][16 bytes], value
+// [H][D][B] elements, while the host keeps every piece token-major [B][H][R]
+// (R = head_dim * elem bytes per token row of one head). Both transforms
+// permute the piece at 16-byte (key) or element (value) granularity, so one
+// side of a direct copy would be read or written in scattered 16-byte or
+// smaller pieces -- across PCIe, requests that small waste most of each
+// transaction. Each wave therefore stages a group of whole heads in its slice
+// of LDS: it reads the group coalesced in the source's order, then writes it
+// coalesced in the destination's order, gathering from LDS. Rows in LDS are
+// padded by 16 bytes to spread the column reads over the banks.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef __attribute__((address_space(3))) u32x4 lu4;
 
-__global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
+// Make LDS writes of the wave visible to its other lanes (the wave-level
+// barrier idiom: release, wave barrier, acquire).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// 16-byte units [0, n) moved by one wave: map(u) gives the unit's source and
+// destination offsets, get(source offset) reads it, put(destination offset, v)
+// writes it. kUnits units per lane are read before the first is written; their
+// offsets are computed once and kept in registers.
+constexpr uint32_t kUnits = 8;
+struct UnitOffs {
+  uint32_t src, dst;
+};
+template <class Map, class Get, class Put>
+__device__ __forceinline__ void wave_units(uint32_t n, uint32_t lane, Map map, Get get, Put put) {
+  for (uint32_t base = 0; base < n; base += kUnits * kWave) {
+    u32x4 v[kUnits];
+    UnitOffs o[kUnits];
+#pragma unroll
+    for (uint32_t i = 0; i < kUnits; ++i) {
+      const uint32_t u = base + i * kWave + lane;
+      if (u < n) {
+        o[i] = map(u);
+        v[i] = get(o[i].src);
+      }
+    }
+#pragma unroll
+    for (uint32_t i = 0; i < kUnits; ++i) {
+      const uint32_t u = base + i * kWave + lane;
+      if (u < n) put(o[i].dst, v[i]);
+    }
+  }
+}
+
+// 16 bytes made of 16 / E elements of E bytes, element j at p + j * stride (LDS).
+template <uint32_t E>
+__device__ __forceinline__ u32x4 gather16(const lds_u8* p, uint32_t stride) {
+  u32x4 r;
+  if constexpr (E == 1) {
+#pragma unroll
+    for (uint32_t w = 0; w < 4; ++w) {
+      const lds_u8* q = p + 4 * w * stride;
+      r[w] = static_cast<uint32_t>(q[0]) | (static_cast<uint32_t>(q[stride]) << 8) |
+             (static_cast<uint32_t>(q[2 * stride]) << 16) | (static_cast<uint32_t>(q[3 * stride]) << 24);
+    }
+  } else if constexpr (E == 2) {
+#pragma unroll
+    for (uint32_t w = 0; w < 4; ++w) {
+      const auto* q0 = reinterpret_cast<const __attribute__((address_space(3))) uint16_t*>(p + 2 * w * stride);
+      const auto* q1 = reinterpret_cast<const __attribute__((address_space(3))) uint16_t*>(p + (2 * w + 1) * stride);
+      r[w] = static_cast<uint32_t>(*q0) | (static_cast<uint32_t>(*q1) << 16);
+    }
+  } else if constexpr (E == 4) {
+#pragma unroll
+    for (uint32_t w = 0; w < 4; ++w) r[w] = *reinterpret_cast<const __attribute__((address_space(3))) uint32_t*>(p + w * stride);
+  } else {
+#pragma unroll
+    for (uint32_t w = 0; w < 2; ++w) {
+      const auto* q = reinterpret_cast<const __attribute__((address_space(3))) uint32_t*>(p + w * stride);
+      r[2 * w] = q[0];
+      r[2 * w + 1] = q[1];
+    }
+  }
+  return r;
+}
+
+// host (token-major) piece `src` -> x-packed block `dst`; k = 0 key, 1 value.
+template <uint32_t E>
+__device__ void xpacked_to_block(const uint8_t* src, uint8_t* dst, uint32_t k, const XGeom& g, lds_u8* lds,
+                                 uint32_t lane) {
+  const uint32_t G = xp_to_heads(g);
+  auto to_lds = [&](uint32_t o, u32x4 v) { *reinterpret_cast<lu4*>(lds + o) = v; };
+  for (uint32_t h0 = 0; h0 < g.H; h0 += G) {
+    const uint32_t gh = xp_min(G, g.H - h0), rs = xp_to_row_stride(g, gh);
+    wave_units(xp_to_load_count(g, gh), lane,
+               [&](uint32_t u) {
+                 UnitOffs o;
+                 xp_to_load(g, h0, gh, u, &o.src, &o.dst);
+                 return o;
+               },
+               [&](uint32_t o) -> u32x4 { return *(const gu4*)(src + o); }, to_lds);
+    wave_sync();
+    uint8_t* out = dst + h0 * g.B * g.R;  // heads are the block's outermost dimension
+    auto to_out = [&](uint32_t o, u32x4 v) { *(gu4*)(out + o) = v; };
+    if (k == 0)
+      wave_units(xp_to_key_count(g, gh), lane, [&](uint32_t v) { return UnitOffs{xp_to_key_lds(g, gh, v), v * 16}; },
+                 [&](uint32_t o) -> u32x4 { return *reinterpret_cast<const lu4*>(lds + o); }, to_out);
+    else
+      wave_units(xp_to_val_count(g, gh), lane, [&](uint32_t v) { return UnitOffs{xp_to_val_lds(g, gh, v), v * 16}; },
+                 [&](uint32_t o) -> u32x4 { return gather16<E>(lds + o, rs); }, to_out);
+    wave_sync();  // the tile is read before the next group overwrites it
+  }
+}
+
+// x-packed block `src` -> host (token-major) piece `dst`; k = 0 key, 1 value.
+template <uint32_t E>
+__device__ void xpacked_from_block(const uint8_t* src, uint8_t* dst, uint32_t k, const XGeom& g, lds_u8* lds,
+                                   uint32_t lane) {
+  const uint32_t G = xp_from_heads(g, k), rs = xp_from_row_stride(g, k);
+  auto to_lds = [&](uint32_t o, u32x4 v) { *reinterpret_cast<lu4*>(lds + o) = v; };
+  auto to_dst = [&](uint32_t o, u32x4 v) { *(gu4*)(dst + o) = v; };
+  for (uint32_t h0 = 0; h0 < g.H; h0 += G) {
+    const uint32_t gh = xp_min(G, g.H - h0);
+    const uint8_t* in = src + h0 * g.B * g.R;  // the group is one contiguous range of the block
+    wave_units(xp_from_load_count(g, k, gh), lane,
+               [&](uint32_t v) { return UnitOffs{v * 16, xp_from_load_lds(g, k, v)}; },
+               [&](uint32_t o) -> u32x4 { return *(const gu4*)(in + o); }, to_lds);
+    wave_sync();
+    if (k == 0)
+      wave_units(xp_from_store_count(g, gh), lane,
+                 [&](uint32_t u) { return UnitOffs{xp_from_store_lds(g, 0, gh, u), xp_from_store_dst(g, h0, gh, u)}; },
+                 [&](uint32_t o) -> u32x4 { return *reinterpret_cast<const lu4*>(lds + o); }, to_dst);
+    else
+      wave_units(xp_from_store_count(g, gh), lane,
+                 [&](uint32_t u) { return UnitOffs{xp_from_store_lds(g, 1, gh, u), xp_from_store_dst(g, h0, gh, u)}; },
+                 [&](uint32_t o) -> u32x4 { return gather16<E>(lds + o, rs); }, to_dst);
+    wave_sync();
+  }
+}
+
+template <uint32_t E>
+__device__ __forceinline__ void xpacked_piece(const uint8_t* src, uint8_t* dst, bool to_block, uint32_t k,
+                                              const XGeom& g, lds_u8* lds, uint32_t lane) {
+  if (to_block)
+    xpacked_to_block<E>(src, dst, k, g, lds, lane);
+  else
+    xpacked_from_block<E>(src, dst, k, g, lds, lane);
+}
+
+extern __shared__ __attribute__((aligned(16))) uint8_t mma_dyn_lds[];
+
+// The dummy-task kernel's body. kXE = 0: paged-KV blocks hold pieces as the
+// host does. kXE = element bytes: the x-packed GPU block layout through LDS --
+// one kernel per element size, so that no launch carries the registers or LDS
+// of a transform it does not run.
+template <uint32_t kXE>
+__device__ __forceinline__ void transfer_body(const KernelArgs& a) {
   __shared__ uint64_t s_layer[kMaxLayers];
   Record* rec = a.rec;
   DevState* ds = a.ds;
@@ -149,6 +301,8 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
   for (uint32_t i = threadIdx.x; i < nl; i += kBlock) s_layer[i] = a.layer_ptr[i];
   const uint64_t piece = a.kv_piece_bytes;
   const uint64_t kstride = a.kv_kstride;
+  const XGeom xg{a.kv_tokens, a.kv_heads, a.kv_row_bytes, a.kv_elem, a.kv_lds_wave};
+  lds_u8* wave_lds = (lds_u8*)(mma_dyn_lds) + (threadIdx.x / kWave) * a.kv_lds_wave;
   __syncthreads();
 
   // A self-contained launch carries every entry of the transfer in its
@@ -250,6 +404,10 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
         src = kind == kEntryToPaged ? contig : pg;
         dst = kind == kEntryToPaged ? pg : contig;
         n = piece;
+        if constexpr (kXE != 0) {
+          xpacked_piece<kXE>(src, dst, kind == kEntryToPaged, p & 1u, xg, wave_lds, lane);
+          continue;
+        }
       }
       wave_copy(src, dst, n, lane);
     }
@@ -292,6 +450,15 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) {
   }
 }
 
+}  // namespace
+
+__global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) { transfer_body<0>(a); }
+
+template <uint32_t E>
+__global__ __launch_bounds__(kBlock) void mma_transfer_xpacked_kernel(KernelArgs a) {
+  transfer_body<E>(a);
+}
+
 // digest += sum_i (w_i + 1) * (2i + 1) mod 2^64 over nw words (+ one zero-padded
 // tail word of tail_len bytes at tail). vec4: w is 16-byte aligned.
 __global__ __launch_bounds__(256) void mma_digest_kernel(const uint32_t* __restrict__ w, uint64_t nw,
@@ -324,6 +491,15 @@ __global__ __launch_bounds__(256) void mma_digest_kernel(const uint32_t* __restr
 
 hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t stream) {
   void* params[] = {const_cast<KernelArgs*>(&args)};
+  // Only x-packed KV transfers stage through LDS; every other launch asks for
+  // none, so it can share CUs with kernels that use most of theirs.
+  if (args.kv_layout == kKvLayoutXPacked) {
+    const void* k = args.kv_elem == 1   ? reinterpret_cast<const void*>(&mma_transfer_xpacked_kernel<1>)
+                    : args.kv_elem == 2 ? reinterpret_cast<const void*>(&mma_transfer_xpacked_kernel<2>)
+                    : args.kv_elem == 4 ? reinterpret_cast<const void*>(&mma_transfer_xpacked_kernel<4>)
+                                        : reinterpret_cast<const void*>(&mma_transfer_xpacked_kernel<8>);
+    return hipLaunchKernel(k, dim3(grid), dim3(kBlock), params, kWavesPerWG * args.kv_lds_wave, stream);
+  }
   return hipLaunchKernel(reinterpret_cast<const void*>(&mma_transfer_kernel), dim3(grid), dim3(kBlock), params, 0,
                          stream);
 }

@@ -25,9 +25,17 @@ constexpr uint32_t kRecords = 64;      // records per direction (transfers in fl
 constexpr uint32_t kMaxWorkgroups = 256;  // dummy-task kernel size limit (ring keeps one slot per wave)
 constexpr uint32_t kPrefill = 48;      // ring entries also passed in the kernel arguments (linear kinds)
 constexpr uint32_t kMaxLayers = 256;   // KV layer pointers per record
+constexpr uint32_t kMaxLdsPerWave = 36 * 1024;  // x-packed KV tiles: 4 waves x 36 KiB + 2 KiB of a CU's 160 KiB
 constexpr uint32_t kWave = 64;
 constexpr uint32_t kWavesPerWG = 4;
 constexpr uint32_t kBlock = kWave * kWavesPerWG;
+
+// GPU block layouts of a paged-KV piece (one layer's K or V of one block). The
+// host side is always token-major [tokens][heads][head_dim].
+enum : uint32_t {
+  kKvLayoutPiece = 0,    // the GPU block holds the piece as the host does
+  kKvLayoutXPacked = 1,  // key [heads][head_dim/x][tokens][x], x = 16 / elem; value [heads][head_dim][tokens]
+};
 
 // Entry kinds. Kind and first piece share one 32-bit word: kind | p0 << 8.
 enum : uint32_t {
@@ -103,7 +111,12 @@ struct KernelArgs {
   uint32_t n_pre;           // tickets [0, n_pre) are also given below: no first poll for them
   uint32_t self_contained;  // 1: the n_pre entries are the whole transfer and no copy engine takes
                             // part: wave w copies entry w; no start signal, ring, exit count or wait
-  uint32_t pad;
+  // GPU block layout of paged-KV pieces: kKvLayoutPiece (as in host memory) or
+  // kKvLayoutXPacked, whose geometry follows (a row is one token's head_dim
+  // elements of one head: head_dim * elem bytes).
+  uint32_t kv_layout;
+  uint32_t kv_tokens, kv_heads, kv_row_bytes, kv_elem;
+  uint32_t kv_lds_wave;     // kKvLayoutXPacked: dynamic LDS bytes per wave (the launch asks for 4x)
   uint64_t layer_ptr[kMaxLayers];
   uint64_t pre[kPrefill][3];  // words a, b, count|kind_p0 of the first ring entries
 };

@@ -684,6 +684,31 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
     return fail(MMA_ERR_INVALID_ARG, "invalid KV layout");
   const uint64_t piece = static_cast<uint64_t>(lay->block_tokens) * lay->kv_heads * lay->head_dim * lay->elem_bytes;
   if (piece > (1ull << 32)) return fail(MMA_ERR_INVALID_ARG, "KV piece too large");
+  KvGeom kv;
+  kv.layout = lay->gpu_layout;
+  if (lay->gpu_layout == MMA_KV_LAYOUT_XPACKED) {
+    // One wave stages whole heads of one piece in LDS: the tile must hold at
+    // least one head's rows (with 16 bytes of padding per row) in every
+    // staging order the kernel uses.
+    const uint64_t E = lay->elem_bytes, B = lay->block_tokens, R = static_cast<uint64_t>(lay->head_dim) * E;
+    if ((E != 1 && E != 2 && E != 4 && E != 8) || R % 16 || (B * E) % 16)
+      return fail(MMA_ERR_INVALID_ARG, "x-packed KV layout needs elem_bytes in {1,2,4,8} and head_dim*elem_bytes, "
+                                       "block_tokens*elem_bytes multiples of 16");
+    const uint64_t need = std::max({B * (R + 16), (R / 16) * (B * 16 + 16), (R / E) * (B * E + 16)});
+    const uint64_t lds_wave = std::max<uint64_t>(need, 16 * KiB);
+    if (need > kMaxLdsPerWave)
+      return fail(MMA_ERR_INVALID_ARG, "x-packed KV layout: one head of one block needs %llu bytes of LDS (max %llu)",
+                  static_cast<unsigned long long>(need), static_cast<unsigned long long>(kMaxLdsPerWave));
+    if ((reinterpret_cast<uintptr_t>(host_pool) & 15u) != 0)
+      return fail(MMA_ERR_INVALID_ARG, "x-packed KV layout needs a 16-byte-aligned pool");
+    kv.tokens = lay->block_tokens;
+    kv.heads = lay->kv_heads;
+    kv.row_bytes = static_cast<uint32_t>(R);
+    kv.elem = lay->elem_bytes;
+    kv.lds_wave = static_cast<uint32_t>((lds_wave + 15) & ~15ull);
+  } else if (lay->gpu_layout != MMA_KV_LAYOUT_PIECE) {
+    return fail(MMA_ERR_INVALID_ARG, "unknown GPU KV layout %u", lay->gpu_layout);
+  }
   const uint32_t ppb = 2 * lay->num_layers;
   const uint64_t slot_bytes = piece * ppb;
   const uint64_t pool_bytes = slot_bytes * lay->host_num_slots;
@@ -706,13 +731,14 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
     pool_dev = true;
     pool_cu = reinterpret_cast<uint64_t>(host_pool);
   }
-  KvGeom kv;
   kv.layers = lay->num_layers;
   kv.piece = piece;
   kv.kstride = piece * lay->gpu_num_blocks;
   for (uint32_t l = 0; l < lay->num_layers; ++l) {
     if (!layers[l]) return fail(MMA_ERR_INVALID_ARG, "NULL layer pointer %u", l);
     if ((s = device_range(layers[l], layer_bytes))) return s;
+    if (kv.layout == MMA_KV_LAYOUT_XPACKED && (reinterpret_cast<uintptr_t>(layers[l]) & 15u) != 0)
+      return fail(MMA_ERR_INVALID_ARG, "x-packed KV layout needs 16-byte-aligned layer tensors (layer %u)", l);
     kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l]);
   }
   const uint64_t per_task = std::max<uint64_t>(rt->cfg.chunk / piece, 1) * piece;

@@ -215,6 +215,129 @@ def test_kv_rejects_bad_tables():
         torch.cuda.synchronize()
 
 
+# ----------------------------------------------------------------------------- x-packed GPU block layout
+XP = okv.LAYOUT_XPACKED
+XP_SHAPES = {
+    # block_tokens * elem_bytes and head_dim * elem_bytes are multiples of 16
+    "bf16": W.KVShape(layers=2, block_tokens=16, kv_heads=2, head_dim=16, elem_bytes=2,
+                      gpu_num_blocks=40, host_num_slots=32, n_blocks=24),
+    "fp8": W.KVShape(layers=3, block_tokens=16, kv_heads=3, head_dim=32, elem_bytes=1,
+                     gpu_num_blocks=50, host_num_slots=40, n_blocks=30),
+    "fp32": W.KVShape(layers=2, block_tokens=8, kv_heads=5, head_dim=16, elem_bytes=4,
+                      gpu_num_blocks=33, host_num_slots=30, n_blocks=29),
+    "fp64": W.KVShape(layers=1, block_tokens=2, kv_heads=3, head_dim=8, elem_bytes=8,
+                      gpu_num_blocks=20, host_num_slots=20, n_blocks=17),
+    "llama": W.KVShape(layers=4, block_tokens=16, kv_heads=8, head_dim=128, elem_bytes=2,
+                       gpu_num_blocks=300, host_num_slots=256, n_blocks=200),
+}
+
+
+def xp_layout_of(s: W.KVShape):
+    return mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                         s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED)
+
+
+def _geom(s: W.KVShape):
+    return (s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes)
+
+
+@pytest.mark.parametrize("chunk", [4096, 1 << 21])
+@pytest.mark.parametrize("shape", list(XP_SHAPES))
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_kv_xpacked_fetch(paths, shape, chunk):
+    s = XP_SHAPES[shape]
+    log(f"kv fetch x-packed paths={paths} shape={shape} chunk={chunk}")
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
+        pool = _pool(s, 5)
+        layers = _layers(s, W.GPU_POISON)
+        before = _layer_views(s, layers)
+        mma.mma_kv_fetch(xp_layout_of(s), pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+        pool_v = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+        for l in range(s.layers):
+            want = okv.kv_fetch_layer(pool_v, before[l], l, s.layers, hs, gb, XP, _geom(s))
+            got = to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
+            assert np.array_equal(got, want), f"layer {l}"
+    assert stats["failed_transfers"] == 0
+    assert sum(stats["path_bytes"]) == s.n_blocks * s.slot_bytes
+
+
+@pytest.mark.parametrize("chunk", [4096, 1 << 21])
+@pytest.mark.parametrize("shape", list(XP_SHAPES))
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_kv_xpacked_offload(paths, shape, chunk):
+    s = XP_SHAPES[shape]
+    log(f"kv offload x-packed paths={paths} shape={shape} chunk={chunk}")
+    plan = W.kv_offload_plan(s, cfg=4)
+    with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
+        pool = _pool(s, 6)
+        before = pool.array.copy()
+        layers = _layers(s, seed=200)
+        views = _layer_views(s, layers)
+        mma.mma_kv_offload(xp_layout_of(s), pool, layers, plan.src_blocks, plan.dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        want = okv.kv_offload(before.reshape(s.host_num_slots, -1), views, plan.src_blocks, plan.dest, XP, _geom(s))
+        assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
+
+
+@pytest.mark.parametrize("shape", ["bf16", "llama"])
+def test_kv_xpacked_device_pool_roundtrip(shape):
+    """An HBM-resident pool (CU gather/scatter in HBM) with the x-packed layout: fetch, then offload
+    the same blocks into other slots; both against the oracle."""
+    s = XP_SHAPES[shape]
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    with session("both", chunk_bytes=4096):
+        r = np.random.default_rng(8)
+        pool_np = r.integers(0, 256, s.host_num_slots * s.slot_bytes, dtype=np.uint8)
+        dpool = torch.from_numpy(pool_np.copy()).cuda()
+        layers = _layers(s, W.GPU_POISON)
+        before = _layer_views(s, layers)
+        mma.mma_kv_fetch(xp_layout_of(s), dpool, layers, hs, gb)
+        torch.cuda.synchronize()
+        pv = pool_np.reshape(s.host_num_slots, s.slot_bytes)
+        for l in range(s.layers):
+            want = okv.kv_fetch_layer(pv, before[l], l, s.layers, hs, gb, XP, _geom(s))
+            assert np.array_equal(to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes), want), l
+        dest = np.roll(hs, 1).astype(np.int32)
+        views = _layer_views(s, layers)
+        mma.mma_kv_offload(xp_layout_of(s), dpool, layers, gb, dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        want = okv.kv_offload(pv, views, gb, dest, XP, _geom(s))
+        assert np.array_equal(to_host(dpool).reshape(s.host_num_slots, -1), want)
+
+
+def test_kv_xpacked_rejects_unsupported_geometry():
+    with session("both"):
+        for s in [W.KVShape(layers=1, block_tokens=16, kv_heads=1, head_dim=12, elem_bytes=2,
+                            gpu_num_blocks=4, host_num_slots=4, n_blocks=2),   # head row of 24 bytes
+                  W.KVShape(layers=1, block_tokens=4, kv_heads=1, head_dim=16, elem_bytes=2,
+                            gpu_num_blocks=4, host_num_slots=4, n_blocks=2),   # 8-byte token column
+                  W.KVShape(layers=1, block_tokens=16, kv_heads=1, head_dim=24, elem_bytes=3,
+                            gpu_num_blocks=4, host_num_slots=4, n_blocks=2),   # 3-byte elements
+                  W.KVShape(layers=1, block_tokens=256, kv_heads=1, head_dim=128, elem_bytes=2,
+                            gpu_num_blocks=4, host_num_slots=4, n_blocks=2)]:  # one head > the LDS tile
+            pool = _pool(s, 1)
+            layers = _layers(s, 0)
+            with pytest.raises(mma.MMAError) as e:
+                mma.mma_kv_fetch(xp_layout_of(s), pool, layers, [0, 1], [0, 1])
+            assert e.value.name == "MMA_ERR_INVALID_ARG"
+            pool.free()
+        s = XP_SHAPES["bf16"]
+        pool = _pool(s, 1)
+        layers = _layers(s, 0)
+        bad = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                            s.host_num_slots, 7)
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_kv_fetch(bad, pool, layers, [0], [0])
+        assert e.value.name == "MMA_ERR_INVALID_ARG"
+        torch.cuda.synchronize()
+
+
 def _fill_pool_c3(pool: np.ndarray, s: W.KVShape, hs: np.ndarray):
     v = pool.reshape(s.host_num_slots, s.slot_bytes)
     for i in range(s.n_blocks):
@@ -276,3 +399,46 @@ def test_kv_offload_64k_full():
         want = okv.kv_offload(before, views, plan.src_blocks, plan.dest)
         assert np.array_equal(pv, want)
         pool.free()
+
+
+@pytest.mark.slow
+def test_kv_xpacked_fetch_offload_64k():
+    """The 64k-token KV fetch (8 GiB) into the x-packed GPU layout, in the configuration the benchmark
+    times, then the offload of every fetched block into the host slots in reverse order (a poisoned
+    pool). For 512 sampled logical blocks every GPU block is checked against the oracle in every
+    layer, and the offloaded slot must hold the block's original bytes; every untouched GPU block
+    stays poison."""
+    s = W.KV64K
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    geom = _geom(s)
+    sample = np.random.default_rng(17).permutation(s.n_blocks)[:512]
+    with session("both", cu_whole_bytes=0):
+        pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+        _fill_pool_c3(pool.array, s, hs)
+        layers = _layers(s, W.GPU_POISON)
+        lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                            s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED)
+        mma.mma_kv_fetch(lay, pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        pool_v = pool.array.reshape(s.host_num_slots, s.layers, 2, s.piece_bytes)
+        untouched = np.setdiff1d(np.arange(s.gpu_num_blocks), gb)
+        for l in range(s.layers):
+            got = to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
+            for i in sample:
+                for k in (0, 1):
+                    want = okv.piece_to_block(pool_v[hs[i], l, k], k, XP, geom)
+                    assert np.array_equal(got[k, gb[i]], want), (l, int(i), k)
+            assert np.all(got[:, untouched] == W.GPU_POISON), l
+        log("  x-packed fetch verified on the sample")
+        dest = hs[::-1].copy()
+        pool.array[:] = W.HOST_FREE_POISON
+        mma.mma_kv_offload(lay, pool, layers, gb, dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        for i in sample:
+            want = W.kv_block_bytes(3, int(i), s).reshape(s.layers, 2, s.piece_bytes)
+            assert np.array_equal(pool_v[dest[i]], want), int(i)
+        st = mma.mma_get_stats()
+        pool.free()
+    assert st["failed_transfers"] == 0
