@@ -249,6 +249,34 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
         "native_per_piece_ms": round(nat_off, 2) if nat_off else None,
         "speedup_vs_native": round(nat_off / off["p50"], 2) if nat_off else None}
 
+    # The same 64k-token fetch, and the 2048-block offload, with the GPU cache in the x-packed block
+    # layout of paged-attention decode kernels (key [H][D/x][B][x], value [H][D][B]): the CU path
+    # transforms every piece through LDS. Sampled parity against the layout's definition.
+    xlay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                         s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED)
+    xf = _timed(stream, lambda: mma.mma_kv_fetch(xlay, pool, layers, hs, gb, stream), reps=5, warm=1)
+    B_, H_, D_, E_ = s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes
+    x_ = 16 // E_
+    pv4 = pool.array.reshape(s.host_num_slots, s.layers, 2, s.piece_bytes)
+    r = np.random.default_rng(1)
+    ok_x = True
+    for _ in range(32):
+        i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
+        o = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
+        got = layers[l][o:o + s.piece_bytes].cpu().numpy()
+        src = pv4[hs[i], l, k].reshape(B_, H_, D_, E_)
+        want = (src.reshape(B_, H_, D_ // x_, x_, E_).transpose(1, 2, 0, 3, 4) if k == 0
+                else src.transpose(1, 2, 0, 3)).reshape(-1)
+        ok_x &= bool(np.array_equal(got, want))
+    xo = _timed(stream, lambda: mma.mma_kv_offload(xlay, pool, layers, src_blocks, plan.dest, stream), reps=5, warm=1)
+    extras["kv_xpacked_layout"] = {
+        "fetch_ms": round(xf["p50"], 3), "fetch_GBs": round(total / xf["p50"] / 1e6, 2),
+        "fetch_frac_of_measured": round(total / xf["p50"] / 1e6 / m_h2d, 4),
+        "offload_2048_ms": round(xo["p50"], 3), "offload_GBs": round(off_bytes / xo["p50"] / 1e6, 2),
+        "offload_frac_of_measured_d2h": round(off_bytes / xo["p50"] / 1e6 / m_d2h, 4),
+        "sampled_parity": ok_x}
+    log("x-packed layout:", extras["kv_xpacked_layout"])
+
     # Measured HBM copy peak (read + write bytes): the runtime's device-to-device copy and the bare
     # streaming kernel over device memory at the best grid, 2 GiB each way.
     hb = 2 << 30

@@ -374,7 +374,11 @@ class Engine {
   // Workgroups of the dummy-task kernel: one wave per ring entry that can be
   // outstanding at once (waves beyond that would only poll host memory, and
   // every poll is a PCIe read that competes with the payload).
-  uint32_t grid_for(uint64_t bytes, uint64_t sub, bool needs_cu, bool staged, bool pool_dev) const {
+  // x-packed KV pieces: a wave alternates between reading a head group into its
+  // LDS tile and writing it out, with no reads in flight during the second
+  // phase, so twice the waves keep the same bytes in flight (measured on the
+  // 64k-token fetch: 54.6 GB/s at 16 workgroups, 57.0 at 32).
+  uint32_t grid_for(uint64_t bytes, uint64_t sub, bool needs_cu, bool staged, bool pool_dev, bool xpacked) const {
     if (!needs_cu) return 1;
     if (pool_dev) {  // HBM gather/scatter: as many waves as there are micro-tasks, up to the limit
       const uint64_t tasks = (bytes + cfg_.chunk - 1) / cfg_.chunk;
@@ -385,7 +389,8 @@ class Engine {
     uint64_t inflight = cu_enabled() ? cfg_.cu_depth * per_task : 0;
     if (staged) inflight += static_cast<uint64_t>(__builtin_popcount(sdma_mask())) * cfg_.depth * per_task;
     uint64_t g = (std::max<uint64_t>(1, std::min(total, inflight)) + kWavesPerWG - 1) / kWavesPerWG;
-    g = std::max<uint64_t>(1, std::min<uint64_t>(g, cfg_.cu_wgs));
+    const uint64_t cap = std::min<uint64_t>(xpacked ? 2ull * cfg_.cu_wgs : cfg_.cu_wgs, kMaxWorkgroups);
+    g = std::max<uint64_t>(1, std::min<uint64_t>(g, cap));
     return static_cast<uint32_t>(g);
   }
 
@@ -438,7 +443,8 @@ class Engine {
       x->sub = std::min<uint64_t>(cfg_.sub,
                                   std::max<uint64_t>(kSmallSub, (per + kSmallSub - 1) / kSmallSub * kSmallSub));
     }
-    uint32_t grid = grid_for(payload_bytes, x->sub, needs_cu || x->pool_dev, staged, x->pool_dev);
+    uint32_t grid = grid_for(payload_bytes, x->sub, needs_cu || x->pool_dev, staged, x->pool_dev,
+                             kv && kv->layout == kKvLayoutXPacked);
     x->waves = grid * kWavesPerWG;
     prefill(x);
     const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
