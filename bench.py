@@ -41,6 +41,9 @@ def parse():
     p.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--kv-layout", choices=["piece", "xpacked"], default="piece",
+                   help="GPU block layout of the timed KV fetch: pieces as in host memory (default), or the "
+                        "x-packed layout of paged-attention decode kernels (transformed through LDS)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true", help="skip native comparators and the 64 MiB copy")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle timing window")
@@ -72,11 +75,11 @@ def calibration_kernels():
                                                               "copyBuffer: read N + write N"]}}), flush=True)
 
 
-def recorded_traffic(root: str):
+def recorded_traffic(root: str, kernel: str = "mma_transfer_kernel"):
     """HBM/EA bytes per launch of the transfer kernel from the committed rocprofv3 --pmc summary,
     valid only while the kernel source is the one that was profiled."""
     import hashlib
-    path = os.path.join(root, "profiles", "mma_transfer_kernel__kv_fetch_64k.traffic.json")
+    path = os.path.join(root, "profiles", f"{kernel}__kv_fetch_64k.traffic.json")
     src = os.path.join(root, "paper_2512_16056_amd", "csrc", "mma_kernels.hip")
     try:
         rec = json.load(open(path))
@@ -871,8 +874,10 @@ def main():
     with ThreadPoolExecutor(16) as ex:
         list(ex.map(fill, range(s.n_blocks)))
     layers = [torch.full((s.layer_bytes,), W.GPU_POISON, dtype=torch.uint8, device="cuda") for _ in range(s.layers)]
+    xpacked = args.kv_layout == "xpacked"
     lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
-                        s.host_num_slots)
+                        s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED if xpacked else mma.MMA_KV_LAYOUT_PIECE)
+    kernel_name = "mma_transfer_xpacked_kernel" if xpacked else "mma_transfer_kernel"
     torch.cuda.synchronize()
     log(f"inputs ready in {time.time() - t0:.1f}s")
 
@@ -909,11 +914,16 @@ def main():
     r = np.random.default_rng(0)
     ok = True
     host = {}
+    B_, H_, D_, E_ = s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes
     for _ in range(64):
         i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
         off = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
         got = layers[l][off:off + s.piece_bytes].cpu().numpy()
         want = pv[hs[i]].reshape(s.layers, 2, s.piece_bytes)[l, k]
+        if xpacked:  # key [H][D/x][B][x], value [H][D][B]
+            w = want.reshape(B_, H_, D_, E_)
+            want = (w.reshape(B_, H_, D_ * E_ // 16, 16 // E_, E_).transpose(1, 2, 0, 3, 4) if k == 0
+                    else w.transpose(1, 2, 0, 3)).reshape(-1)
         ok &= bool(np.array_equal(got, want))
     log(f"sampled parity: {'ok' if ok else 'MISMATCH'}")
 
@@ -932,7 +942,9 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": "kv_fetch_64k_tokens: 4096 blocks x 16 tokens, 32 layers x K,V x 8 kv heads x 128 dim bf16 "
-                        "(8 GiB) pinned host pool -> paged GPU cache via block table",
+                        "(8 GiB) pinned host pool -> paged GPU cache via block table"
+                        + (" (x-packed GPU block layout)" if xpacked else ""),
+            "gpu_block_layout": args.kv_layout,
             "bytes_per_step": total,
             "pieces_per_step": s.n_blocks * s.pieces_per_block,
             "chunk_bytes": cfg["chunk_bytes"],
@@ -947,13 +959,13 @@ def main():
                        **{f"sdma{e}": stats["path_bytes"][e] for e in range(16) if stats["path_bytes"][e]}},
         "engine_cpu_ms_per_step": round(stats["engine_cpu_ns"] / 1e6 / max(1, args.steps + args.warmup), 3),
         "roofline": {
-            "kernel": "mma_transfer_kernel (dummy task: CU gather + stream wait)",
+            "kernel": f"{kernel_name} (dummy task: CU gather + stream wait)",
             "bound": "pcie",
             "achieved": round(achieved, 3),
             "peak": round(PCIE5_X16_GBS, 2),
             "unit": "GB/s",
             "frac": round(achieved / PCIE5_X16_GBS, 4),
-            "traffic": recorded_traffic(ROOT),
+            "traffic": recorded_traffic(ROOT, kernel_name),
         },
     }
 
