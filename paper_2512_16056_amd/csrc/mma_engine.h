@@ -137,7 +137,8 @@ struct Transfer {
   uint8_t tdone[kRingSize];    // its done tag has been seen
   uint32_t cu_busy = 0;
   bool cu_full = false;
-  int sdma_cu_pending = 0;     // SDMA slots that will still append ring entries
+  int sdma_cu_pending = 0;     // SDMA slots that may still append ring entries (a staging step, or a
+                               // re-route of their micro-tasks to the CU path)
   int sdma_refs = 0;           // SDMA slots referencing this transfer
   uint64_t heartbeat = 0;
   uint64_t bytes = 0;          // payload bytes
@@ -669,13 +670,26 @@ class Engine {
                     s.count * x->piece)) {
         s.state = kD2HStage;
       } else {
-        // The gathered bytes are in staging and cannot reach the host this way.
+        // The copy engine refused the command. The source blocks are untouched, so the
+        // micro-tasks go back to the queue for the CU path, which moves them straight to
+        // host memory; the ring is still open for them (this slot kept it open).
         st_->submit_failures += 1;
-        x->failed = true;
-        slot_tasks_done(s);
+        requeue_cu(x, s.task, s.task_end);
         free_slot(s);
       }
+      --x->sdma_cu_pending;
     }
+  }
+
+  // Micro-tasks [i, end) of x go back to the queue, CU path only.
+  void requeue_cu(Transfer* x, size_t i, size_t end) {
+    for (size_t j = i; j < end; ++j) {
+      x->claimed[j] = 0;
+      x->tasks[j].flags = (x->tasks[j].flags & ~kPlanSdmaOnly) | kPlanCuOnly;
+    }
+    x->n_claimed -= end - i;
+    x->cur_cu = std::min(x->cur_cu, i);
+    x->progress = true;
   }
 
   bool try_push_stage(SdmaSlot& s) {
@@ -689,8 +703,12 @@ class Engine {
       ne = push_unit(x, own, kEntryFromPaged, s.staging, t.blk, s.count, t.p0);
     if (!ne) return false;
     s.left = ne;
-    s.state = s.state == kH2DScatterPush ? kH2DScatter : kD2HGather;
-    --x->sdma_cu_pending;
+    if (s.state == kH2DScatterPush) {
+      s.state = kH2DScatter;
+      --x->sdma_cu_pending;
+    } else {
+      s.state = kD2HGather;  // still pending until its copy-engine command is accepted
+    }
     return true;
   }
 
@@ -710,6 +728,7 @@ class Engine {
       }
       if (s.state == kH2DScatter || s.state == kD2HGather) {
         if (s.x->aborting) {  // the kernel has left; its ring entries will never run
+          if (s.state == kD2HGather) --s.x->sdma_cu_pending;
           free_slot(s);
           p = true;
         }
@@ -900,12 +919,7 @@ class Engine {
         if (!ok) {
           // Re-route: the tasks go back to the queue, CU path only.
           st_->submit_failures += 1;
-          for (size_t j = i; j < end; ++j) {
-            x->claimed[j] = 0;
-            x->tasks[j].flags = (x->tasks[j].flags & ~kPlanSdmaOnly) | kPlanCuOnly;
-          }
-          x->n_claimed -= end - i;
-          x->cur_cu = std::min(x->cur_cu, i);
+          requeue_cu(x, i, end);
           free_slot(s);
         }
         x->progress = true;

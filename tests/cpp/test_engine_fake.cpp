@@ -668,6 +668,63 @@ void submit_failures_rerouted() {
               (unsigned long long)h.stats().submit_failures.load());
 }
 
+// Copy-engine commands refused during paged-KV transfers: a fetch's host->staging
+// command (before anything moved) and an offload's staging->host command (after the
+// CU gather into staging) both send their micro-tasks back to the CU path; the
+// results are exact and no transfer fails.
+void kv_submit_failures_rerouted() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.chunk = 8 * 1024;  // 4 pieces per micro-task
+  s.mask = 0x3;            // copy engines only: every micro-task starts on an engine
+  Harness h(s);
+  FakeStream st;
+  const uint32_t L = 2, ppb = 2 * L, slots = 16, nb = 20;
+  const uint64_t piece = 2048, slot_bytes = piece * ppb;
+  std::vector<uint8_t> pool = random_bytes(slots * slot_bytes, 21);
+  std::vector<std::vector<uint8_t>> layers(L, std::vector<uint8_t>(2 * nb * piece, 0xA5));
+  KvGeom kv;
+  kv.piece = piece;
+  kv.kstride = piece * nb;
+  kv.layers = L;
+  for (uint32_t l = 0; l < L; ++l) kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l].data());
+  std::vector<int32_t> hs = {3, 7, 0, 12, 9, 15}, gb = {19, 2, 8, 5, 11, 0};
+  const uint64_t host = reinterpret_cast<uint64_t>(pool.data());
+  g_fault_submit_fail = 2;
+  h.submit(make_kv_transfer(MMA_H2D, piece, ppb, host, host, false, true, hs.data(), gb.data(), hs.size(), h.cfg()),
+           hs.size() * slot_bytes, st, &kv);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  bool ok = true;
+  for (size_t i = 0; i < hs.size(); ++i)
+    for (uint32_t l = 0; l < L; ++l)
+      for (uint32_t k = 0; k < 2; ++k)
+        ok &= std::memcmp(layers[l].data() + (k * nb + gb[i]) * piece,
+                          pool.data() + hs[i] * slot_bytes + (2 * l + k) * piece, piece) == 0;
+  CHECK(ok, "fetch with refused commands: pieces differ");
+  const uint64_t after_fetch = h.stats().submit_failures.load();
+  CHECK(after_fetch >= 1, "no refused command during the fetch");
+  std::vector<int32_t> dest = {1, 2, 4, 5, 6, 8};
+  auto want = pool;
+  for (size_t j = 0; j < gb.size(); ++j)
+    for (uint32_t l = 0; l < L; ++l)
+      for (uint32_t k = 0; k < 2; ++k)
+        std::memcpy(want.data() + dest[j] * slot_bytes + (2 * l + k) * piece,
+                    layers[l].data() + (k * nb + gb[j]) * piece, piece);
+  g_fault_submit_fail = 2;
+  h.submit(make_kv_transfer(MMA_D2H, piece, ppb, host, host, false, true, dest.data(), gb.data(), gb.size(),
+                            h.cfg()),
+           gb.size() * slot_bytes, st, &kv);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  g_fault_submit_fail = 0;
+  CHECK(pool == want, "offload with refused commands: pool differs");
+  CHECK(h.stats().submit_failures.load() > after_fetch, "no refused command during the offload");
+  CHECK(h.stats().failed.load() == 0 && g_sticky.load() == 0, "a refused command failed the transfer");
+  std::printf("ok   refused copy-engine commands of KV fetch and offload re-routed to the CU path (%llu)\n",
+              (unsigned long long)h.stats().submit_failures.load());
+}
+
 void two_streams_both_directions() {
   Setup s;
   s.cfg = default_config();
@@ -761,6 +818,7 @@ int main(int argc, char** argv) {
     unlaunched_transfer_drains();
     whole_transfers_on_cu();
     submit_failures_rerouted();
+    kv_submit_failures_rerouted();
     two_streams_both_directions();
   }
   if (timing) {

@@ -44,6 +44,56 @@ def test_sdma_submit_failures_are_rerouted():
     assert 1 <= st["sdma_submit_failures"] <= 3
 
 
+@pytest.mark.parametrize("layout", [mma.MMA_KV_LAYOUT_PIECE, mma.MMA_KV_LAYOUT_XPACKED])
+def test_kv_sdma_submit_failures_are_rerouted(layout):
+    """Refused copy-engine commands during a KV fetch (host -> staging) and a KV offload
+    (staging -> host, after the CU gather into staging): the micro-tasks go back to the CU path
+    and both results match the oracle; no transfer fails."""
+    from oracle import kv as okv
+    s = W.KVShape(layers=3, block_tokens=16, kv_heads=2, head_dim=64, elem_bytes=2, gpu_num_blocks=40,
+                  host_num_slots=32, n_blocks=24)
+    geom = (s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes)
+    ol = okv.LAYOUT_XPACKED if layout else okv.LAYOUT_PIECE
+    lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                        s.host_num_slots, layout)
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    with session("sdma", chunk_bytes=4 * s.piece_bytes):
+        pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+        pool.array[:] = np.random.default_rng(3).integers(0, 256, pool.nbytes, dtype=np.uint8)
+        pool_np = pool.array.reshape(s.host_num_slots, -1).copy()
+        layers = [torch.full((s.layer_bytes,), W.GPU_POISON, dtype=torch.uint8, device="cuda") for _ in range(s.layers)]
+        before = [to_host(t).reshape(2, s.gpu_num_blocks, s.piece_bytes) for t in layers]
+        mma.mma_reset_stats()
+        mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 3)
+        try:
+            mma.mma_kv_fetch(lay, pool, layers, hs, gb)
+            torch.cuda.synchronize()
+            mma.mma_synchronize()
+        finally:
+            mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 0)
+        st_fetch = mma.mma_get_stats()
+        want = okv.kv_fetch(pool_np, before, hs, gb, ol, geom)
+        for l in range(s.layers):
+            assert np.array_equal(to_host(layers[l]).reshape(want[l].shape), want[l]), l
+        views = [to_host(t).reshape(2, s.gpu_num_blocks, s.piece_bytes) for t in layers]
+        dest = np.roll(hs, 3).astype(np.int32)
+        mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 3)
+        try:
+            mma.mma_kv_offload(lay, pool, layers, gb, dest)
+            torch.cuda.synchronize()
+            mma.mma_synchronize()
+        finally:
+            mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 0)
+        st = mma.mma_get_stats()
+        want = okv.kv_offload(pool_np, views, gb, dest, ol, geom)
+        assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
+        pool.free()
+    log(f"  refused commands: fetch {st_fetch['sdma_submit_failures']}, total {st['sdma_submit_failures']}")
+    assert st_fetch["sdma_submit_failures"] >= 1
+    assert st["sdma_submit_failures"] > st_fetch["sdma_submit_failures"]
+    assert st["failed_transfers"] == 0
+
+
 def test_sdma_only_submit_failures_fall_back_to_cu():
     with session("sdma", chunk_bytes=1 << 20):
         mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 1000000)
