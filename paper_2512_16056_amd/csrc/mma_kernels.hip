@@ -116,13 +116,17 @@ __device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8
       ++k;
     }
   }
-  // Remainder (< one batch): one predicated batch, all loads issued before the
-  // first store, so a short copy costs one round trip instead of one per 1 KiB.
+  // Remainder (< one batch): one batch, all loads issued before the first
+  // store, so a short copy costs one round trip instead of one per 1 KiB. The
+  // loads are unconditional -- a lane past the end re-reads the last unit -- and
+  // only the stores are predicated: a predicated load makes the compiler wait
+  // for it before the next one, one PCIe round trip each.
   const uint64_t r = nb * kBatch;
   if (r < n16) {
     const uint64_t left = n16 - r;  // units left for the whole wave, < kBatch
+    const gu4* sl = s - lane;       // the wave's first unit
     u32x4 c0, c1, c2, c3, c4, c5, c6, c7, c8, c9, c10, c11, c12, c13, c14, c15;
-#define MMA_PLD(k) if ((k) * kWave + lane < left) c##k = s[r + (k) * kWave];
+#define MMA_PLD(k) c##k = sl[r + min(static_cast<uint64_t>((k) * kWave + lane), left - 1)];
 #define MMA_PST(k) if ((k) * kWave + lane < left) d[r + (k) * kWave] = c##k;
     MMA_PLD(0) MMA_PLD(1) MMA_PLD(2) MMA_PLD(3) MMA_PLD(4) MMA_PLD(5) MMA_PLD(6) MMA_PLD(7)
     MMA_PLD(8) MMA_PLD(9) MMA_PLD(10) MMA_PLD(11) MMA_PLD(12) MMA_PLD(13) MMA_PLD(14) MMA_PLD(15)
@@ -167,6 +171,8 @@ constexpr uint32_t kUnits = 8;
 struct UnitOffs {
   uint32_t src, dst;
 };
+// Reads are unconditional (a lane past the end reads unit n - 1 again): a
+// predicated read would make the compiler wait for it before issuing the next.
 template <class Map, class Get, class Put>
 __device__ __forceinline__ void wave_units(uint32_t n, uint32_t lane, Map map, Get get, Put put) {
   for (uint32_t base = 0; base < n; base += kUnits * kWave) {
@@ -174,16 +180,12 @@ __device__ __forceinline__ void wave_units(uint32_t n, uint32_t lane, Map map, G
     UnitOffs o[kUnits];
 #pragma unroll
     for (uint32_t i = 0; i < kUnits; ++i) {
-      const uint32_t u = base + i * kWave + lane;
-      if (u < n) {
-        o[i] = map(u);
-        v[i] = get(o[i].src);
-      }
+      o[i] = map(min(base + i * kWave + lane, n - 1));
+      v[i] = get(o[i].src);
     }
 #pragma unroll
     for (uint32_t i = 0; i < kUnits; ++i) {
-      const uint32_t u = base + i * kWave + lane;
-      if (u < n) put(o[i].dst, v[i]);
+      if (base + i * kWave + lane < n) put(o[i].dst, v[i]);
     }
   }
 }
