@@ -111,7 +111,10 @@ struct Transfer {
   int dir = MMA_H2D;
   Kind kind = Kind::kLinear;
   uint32_t rec_idx = 0;
-  Record* rec = nullptr;      // host address of the shared record
+  Record* rec = nullptr;      // host address of the shared record; null for a light slot
+  int32_t light = -1;         // light slot (a whole self-contained transfer), or -1
+  CuEntry* ring = nullptr;    // where the engine writes ring entries (the record's, or a scratch ring)
+  uint64_t* done_host = nullptr;  // done tags the kernel writes
   std::vector<Task> tasks;
   std::vector<uint8_t> claimed;
   std::vector<uint32_t> left;  // CU entries outstanding per CU-path task
@@ -269,6 +272,12 @@ class Engine {
     if ((rc = be_->alloc_device_state(sizeof(DevState) * kRecords, &d)) != MMA_OK) return rc;
     ds_ = static_cast<DevState*>(d);
     for (uint32_t i = 0; i < kRecords; ++i) free_recs_.push_back(i);
+    if ((rc = be_->alloc_records(sizeof(uint64_t) * kPrefill * kLightSlots, &h, &d)) != MMA_OK) return rc;
+    light_ = static_cast<uint64_t*>(h);
+    light_dev_ = static_cast<uint64_t*>(d);
+    memset(light_, 0, sizeof(uint64_t) * kPrefill * kLightSlots);
+    for (uint32_t i = 0; i < kLightSlots; ++i) free_light_.push_back(i);
+    light_ring_.reset(new CuEntry[kPrefill + kRingSize]);
     stage_bytes_ = stage_bytes;
     uint8_t* stage = static_cast<uint8_t*>(staging_base);
     for (int eng = 0; eng < MMA_MAX_SDMA; ++eng) {
@@ -334,8 +343,10 @@ class Engine {
     slots_.clear();
     if (ds_) be_->free_device_state(ds_);
     if (recs_) be_->free_records(recs_);
+    if (light_) be_->free_records(light_);
     ds_ = nullptr;
     recs_ = nullptr;
+    light_ = nullptr;
   }
 
   pthread_t native_handle() { return thread_.native_handle(); }
@@ -348,20 +359,45 @@ class Engine {
   bool has_sdma() const { return !paths_.empty(); }
   uint64_t stage_bytes() const { return stage_bytes_; }
 
-  // Blocks until a record is free (or the timeout passes). Called with the
-  // submission mutex held, never by the engine thread.
-  bool acquire_record(Transfer* x, uint64_t timeout_ms) {
+  // A linear transfer that the CU path takes whole (see prepare): it runs as
+  // one self-contained launch and needs a light slot, not a record.
+  bool whole_eligible(const Transfer* x, uint64_t payload_bytes, bool kv) const {
+    return !kv && cu_enabled() && !cfg_.static_split && !x->tasks.empty() && x->tasks.size() <= kPrefill &&
+           payload_bytes <= cfg_.whole[dir_];
+  }
+
+  // Takes a light slot for a whole transfer, else a record; blocks until one is
+  // free (or the timeout passes). Called with the submission mutex held, never
+  // by the engine thread. Light slots outnumber records 64 to 1, so a deep
+  // queue of small transfers on a stream does not wait for the GPU.
+  bool acquire(Transfer* x, uint64_t payload_bytes, bool kv, uint64_t timeout_ms) {
+    const bool light = whole_eligible(x, payload_bytes, kv);
     std::unique_lock<std::mutex> lk(mu_);
-    if (!cv_done_.wait_for(lk, std::chrono::milliseconds(timeout_ms), [&] { return !free_recs_.empty(); }))
+    std::deque<uint32_t>& pool = light ? free_light_ : free_recs_;
+    if (pool.empty() &&
+        !cv_done_.wait_for(lk, std::chrono::milliseconds(timeout_ms), [&] { return !pool.empty(); }))
       return false;
-    x->rec_idx = free_recs_.front();
-    free_recs_.pop_front();
-    x->rec = &recs_[x->rec_idx];
+    const uint32_t i = pool.front();
+    pool.pop_front();
+    if (light) {
+      x->light = static_cast<int32_t>(i);
+      x->rec = nullptr;
+      x->ring = light_ring_.get();
+      x->done_host = light_ + static_cast<uint64_t>(i) * kPrefill;
+    } else {
+      x->rec_idx = i;
+      x->rec = &recs_[i];
+      x->ring = x->rec->ring;
+      x->done_host = x->rec->done;
+    }
     return true;
   }
-  void release_record_unused(Transfer* x) {
+  void release_unused(Transfer* x) {
     std::lock_guard<std::mutex> g(mu_);
-    free_recs_.push_back(x->rec_idx);
+    if (x->light >= 0)
+      free_light_.push_back(static_cast<uint32_t>(x->light));
+    else
+      free_recs_.push_back(x->rec_idx);
     cv_done_.notify_all();
   }
   Record* rec_dev(uint32_t i) const { return recs_dev_ + i; }
@@ -406,10 +442,11 @@ class Engine {
     x->seq = seq;
     x->t_submit = now_ns();
     x->bytes = payload_bytes;
-    Record* r = x->rec;
-    r->h.seq = x->seq;
-    r->h.status = 0;
-    __atomic_thread_fence(__ATOMIC_RELEASE);
+    if (Record* r = x->rec) {
+      r->h.seq = x->seq;
+      r->h.status = 0;
+      __atomic_thread_fence(__ATOMIC_RELEASE);
+    }
     if (cfg_.static_split && has_sdma() && x->sdma_ok) {
       for (size_t i = 0; i < x->tasks.size(); ++i) {
         uint32_t& f = x->tasks[i].flags;
@@ -432,7 +469,7 @@ class Engine {
     // the prefilled entries is still cut into 16 KiB steps, so that more waves
     // share it.
     x->sub = cfg_.sub;
-    if (!kv && cu_enabled() && !cfg_.static_split && x->tasks.size() <= kPrefill && payload_bytes <= cfg_.whole[dir_]) {
+    if (whole_eligible(x, payload_bytes, kv != nullptr)) {
       const uint64_t per_task = kPrefill / x->tasks.size();
       uint64_t biggest = 0;
       for (const Task& t : x->tasks) biggest = std::max(biggest, t.bytes);
@@ -459,11 +496,15 @@ class Engine {
       x->started = true;
       x->t_started = x->t_submit;
     }
+    if (x->light >= 0) {  // whole, hence self-contained: nothing to close or publish in a record
+      x->closed = x->completed = true;
+      x->t_complete = x->t_submit;
+    }
     memset(&a, 0, offsetof(KernelArgs, layer_ptr));
     a.n_pre = n_pre;
     a.self_contained = x->self_contained ? 1u : 0u;
     for (uint32_t t = 0; t < n_pre; ++t) {
-      const CuEntry& en = r->ring[t];
+      const CuEntry& en = x->ring[t];
       a.pre[t][0] = en.a;
       a.pre[t][1] = en.b;
       a.pre[t][2] = static_cast<uint64_t>(en.count) | (static_cast<uint64_t>(en.kind_p0) << 32);
@@ -480,8 +521,15 @@ class Engine {
       a.kv_lds_wave = kv->lds_wave;
       memcpy(a.layer_ptr, kv->layer_ptr, sizeof(uint64_t) * kv->layers);
     }
-    a.rec = rec_dev(x->rec_idx);
-    a.ds = ds(x->rec_idx);
+    if (x->light >= 0) {
+      a.rec = nullptr;
+      a.ds = nullptr;
+      a.done = light_dev_ + static_cast<uint64_t>(x->light) * kPrefill;
+    } else {
+      a.rec = rec_dev(x->rec_idx);
+      a.ds = ds(x->rec_idx);
+      a.done = a.rec->done;
+    }
     a.seq = x->seq;
     a.watchdog_ticks = watchdog_ticks;
     a.total_waves = grid * kWavesPerWG;
@@ -522,12 +570,11 @@ class Engine {
     ne = (count + per - 1) / per;
     // Keep one slot per wave free for the end markers written at close.
     if (x->pushed + ne - x->done_upto > kRingSize - x->waves) return 0;
-    Record* r = x->rec;
     for (uint64_t k = 0; k < ne; ++k) {
       const uint64_t t = x->pushed++;
       const uint32_t slot = static_cast<uint32_t>(t % kRingSize);
       const uint64_t c = std::min(per, count - k * per);
-      CuEntry* e = &r->ring[slot];
+      CuEntry* e = &x->ring[slot];
       if ((kind & kEntryKindMask) == kEntryCopy) {
         e->a = a + k * per;
         e->b = b + k * per;
@@ -562,11 +609,10 @@ class Engine {
 
   bool scan_cu(Transfer* x) {
     bool p = false;
-    Record* r = x->rec;
     for (uint64_t t = x->done_upto; t < x->pushed; ++t) {
       const uint32_t slot = static_cast<uint32_t>(t % kRingSize);
       if (x->tdone[slot]) continue;
-      if (ld_acq(&r->done[slot]) != make_tag(x->seq, t)) continue;
+      if (ld_acq(&x->done_host[slot]) != make_tag(x->seq, t)) continue;
       x->tdone[slot] = 1;
       p = true;
       const int32_t own = x->owner[slot];
@@ -1011,9 +1057,8 @@ class Engine {
   // lets every waiting wave leave on its next poll. The slots are free because
   // push_unit keeps `waves` slots in reserve.
   void close_ring(Transfer* x) {
-    Record* r = x->rec;
     for (uint64_t t = x->pushed; t < x->pushed + x->waves; ++t) {
-      CuEntry* e = &r->ring[t % kRingSize];
+      CuEntry* e = &x->ring[t % kRingSize];
       e->a = 0;
       e->b = 0;
       e->count = 0;
@@ -1093,7 +1138,7 @@ class Engine {
       p |= pull_sdma();
       for (auto& up : active_) {
         p |= advance(up.get());
-        if (up->progress && !up->ignored) st_rel(&up->rec->h.heartbeat, ++up->heartbeat);
+        if (up->progress && !up->ignored && up->rec) st_rel(&up->rec->h.heartbeat, ++up->heartbeat);
       }
       // Retire transfers whose kernel has left the record.
       for (size_t i = 0; i < active_.size();) {
@@ -1104,7 +1149,8 @@ class Engine {
         }
         // A failed launch was reported to the caller; it leaves no sticky error.
         const bool unlaunched = x->unlaunched.load(std::memory_order_relaxed);
-        const bool bad = !unlaunched && (x->failed || x->ignored || ld_acq(&x->rec->h.status) != 0);
+        const bool bad =
+            !unlaunched && (x->failed || x->ignored || (x->rec && ld_acq(&x->rec->h.status) != 0));
         if (bad) {
           g_sticky.store(1);
           st_->failed += 1;
@@ -1119,7 +1165,10 @@ class Engine {
         }
         {
           std::lock_guard<std::mutex> g(mu_);
-          free_recs_.push_back(x->rec_idx);
+          if (x->light >= 0)
+            free_light_.push_back(static_cast<uint32_t>(x->light));
+          else
+            free_recs_.push_back(x->rec_idx);
           --inflight_;
         }
         cv_done_.notify_all();
@@ -1142,6 +1191,9 @@ class Engine {
   Stats* st_;
   Record* recs_ = nullptr;
   Record* recs_dev_ = nullptr;
+  uint64_t* light_ = nullptr;      // light slots' done tags, kPrefill per slot (host address)
+  uint64_t* light_dev_ = nullptr;  // the same, device address
+  std::unique_ptr<CuEntry[]> light_ring_;  // scratch ring: light transfers' entries go to the kernel args
   DevState* ds_ = nullptr;
   std::vector<SdmaSlot> slots_;
   std::vector<SdmaPath> paths_;
@@ -1151,7 +1203,7 @@ class Engine {
   std::condition_variable cv_, cv_done_;
   std::deque<std::unique_ptr<Transfer>> incoming_;
   std::vector<std::unique_ptr<Transfer>> active_;  // engine thread only
-  std::deque<uint32_t> free_recs_;
+  std::deque<uint32_t> free_recs_, free_light_;
   uint64_t inflight_ = 0;
   bool stop_ = false;
   std::atomic<bool> stop_flag_{false};

@@ -307,16 +307,9 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
   lds_u8* wave_lds = (lds_u8*)(mma_dyn_lds) + (threadIdx.x / kWave) * a.kv_lds_wave;
   __syncthreads();
 
-  // A self-contained launch carries every entry of the transfer in its
-  // arguments and no copy engine takes part: wave w of the grid copies entry w
-  // and signals it. No start signal, ring, exit count or wait is needed, and
-  // the done tags are the kernel's last accesses to the record.
-  const bool sc = a.self_contained != 0;
-  bool sc_taken = false;
-
   // 1. start signal (stream -> engine). Work that precedes this kernel in
   // stream order is complete and visible (dispatch acquire/release).
-  if (!sc && lane == 0) {
+  if (lane == 0) {
     const uint32_t first = __hip_atomic_fetch_add(&ds->arrived, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (first == 0) st_sys(&rec->h.started, a.seq);
   }
@@ -328,17 +321,9 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
   if (lane == 0) t_prog = wall_clock64();
   for (;;) {
     uint64_t x = 0;
-    if (sc) {
-      if (sc_taken) break;
-      sc_taken = true;
-      x = static_cast<uint64_t>(blockIdx.x) * kWavesPerWG + threadIdx.x / kWave;
-      if (x >= a.n_pre) break;
-    } else {
-      if (lane == 0)
-        x = __hip_atomic_fetch_add(&ds->cursor, static_cast<uint64_t>(1), __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-      x = lane_u64(x, 0);
-    }
+    if (lane == 0)
+      x = __hip_atomic_fetch_add(&ds->cursor, static_cast<uint64_t>(1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    x = lane_u64(x, 0);
     const uint64_t expect = make_tag(a.seq, x);
     const uint64_t* ew = reinterpret_cast<const uint64_t*>(&rec->ring[x % kRingSize]);
     uint32_t state = 0;  // 1: entry ready, 3: watchdog
@@ -415,12 +400,10 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
     }
     if (a.release_each) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
     if (lane == 0) {
-      st_sys(&rec->done[x % kRingSize], expect);
+      st_sys(&a.done[x % kRingSize], expect);
       t_prog = wall_clock64();
     }
   }
-
-  if (sc) return;
 
   // 3. leave; the last wave out waits for completion of all paths.
   if (lane == 0) {
@@ -455,6 +438,22 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
 }  // namespace
 
 __global__ __launch_bounds__(kBlock) void mma_transfer_kernel(KernelArgs a) { transfer_body<0>(a); }
+
+// A self-contained launch: every entry of a linear transfer travels in the
+// arguments and no copy engine takes part, so wave w of the grid copies entry w
+// and writes its done tag -- no start signal, ring, exit count or wait. The
+// arguments hold only the entries (N of them), so a deep queue of small
+// transfers on one stream uses little of the runtime's kernel-argument pool.
+template <uint32_t N>
+__global__ __launch_bounds__(kBlock) void mma_whole_kernel(WholeArgs<N> a) {
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  const uint32_t w = blockIdx.x * kWavesPerWG + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  if (w >= a.n) return;
+  wave_copy(reinterpret_cast<const uint8_t*>(a.e[w][0]), reinterpret_cast<uint8_t*>(a.e[w][1]),
+            static_cast<uint32_t>(a.e[w][2]), lane);
+  if (a.release_each) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+  if (lane == 0) st_sys(&a.done[w], make_tag(a.seq, w));
+}
 
 template <uint32_t E>
 __global__ __launch_bounds__(kBlock) void mma_transfer_xpacked_kernel(KernelArgs a) {
@@ -491,7 +490,26 @@ __global__ __launch_bounds__(256) void mma_digest_kernel(const uint32_t* __restr
   if ((threadIdx.x & (kWave - 1)) == 0 && acc) atomicAdd(out, static_cast<unsigned long long>(acc));
 }
 
+template <uint32_t N>
+hipError_t launch_whole(const KernelArgs& args, uint32_t grid, hipStream_t stream) {
+  WholeArgs<N> w;
+  w.done = args.done;
+  w.seq = args.seq;
+  w.n = args.n_pre;
+  w.release_each = args.release_each;
+  for (uint32_t i = 0; i < args.n_pre; ++i)
+    for (int k = 0; k < 3; ++k) w.e[i][k] = args.pre[i][k];
+  void* params[] = {&w};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&mma_whole_kernel<N>), dim3(grid), dim3(kBlock), params, 0,
+                         stream);
+}
+
 hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t stream) {
+  if (args.self_contained) {
+    if (args.n_pre <= 4) return launch_whole<4>(args, grid, stream);
+    if (args.n_pre <= 16) return launch_whole<16>(args, grid, stream);
+    return launch_whole<kPrefill>(args, grid, stream);
+  }
   void* params[] = {const_cast<KernelArgs*>(&args)};
   // Only x-packed KV transfers stage through LDS; every other launch asks for
   // none, so it can share CUs with kernels that use most of theirs.

@@ -22,6 +22,9 @@ namespace mma {
 
 constexpr uint32_t kRingSize = 4096;   // CU ring entries per record
 constexpr uint32_t kRecords = 64;      // records per direction (transfers in flight)
+// Light slots per direction: a transfer carried whole by one self-contained
+// launch needs no record, only its done tags (at most kPrefill).
+constexpr uint32_t kLightSlots = 4096;
 constexpr uint32_t kMaxWorkgroups = 256;  // dummy-task kernel size limit (ring keeps one slot per wave)
 constexpr uint32_t kPrefill = 48;      // ring entries also passed in the kernel arguments (linear kinds)
 constexpr uint32_t kMaxLayers = 256;   // KV layer pointers per record
@@ -98,8 +101,9 @@ struct alignas(128) DevState {
 };
 
 struct KernelArgs {
-  Record* rec;              // device-visible address of the record
+  Record* rec;              // device-visible address of the record (null for a light slot)
   DevState* ds;
+  uint64_t* done;           // device-visible done tags: the record's, or a light slot's kPrefill
   uint64_t seq;
   uint64_t watchdog_ticks;  // wall-clock ticks without progress before giving up
   uint32_t total_waves;
@@ -110,7 +114,7 @@ struct KernelArgs {
   uint32_t kv_layers;
   uint32_t n_pre;           // tickets [0, n_pre) are also given below: no first poll for them
   uint32_t self_contained;  // 1: the n_pre entries are the whole transfer and no copy engine takes
-                            // part: wave w copies entry w; no start signal, ring, exit count or wait
+                            // part: launched as mma_whole_kernel with WholeArgs instead
   // GPU block layout of paged-KV pieces: kKvLayoutPiece (as in host memory) or
   // kKvLayoutXPacked, whose geometry follows (a row is one token's head_dim
   // elements of one head: head_dim * elem bytes).
@@ -119,6 +123,18 @@ struct KernelArgs {
   uint32_t kv_lds_wave;     // kKvLayoutXPacked: dynamic LDS bytes per wave (the launch asks for 4x)
   uint64_t layer_ptr[kMaxLayers];
   uint64_t pre[kPrefill][3];  // words a, b, count|kind_p0 of the first ring entries
+};
+
+// Arguments of a self-contained launch (every entry of a linear transfer, no
+// copy engine): entry w = {source, destination, bytes} goes to wave w, whose
+// done tag is done[w]. N is the capacity, n the entries used.
+template <uint32_t N>
+struct WholeArgs {
+  uint64_t* done;
+  uint64_t seq;
+  uint32_t n;
+  uint32_t release_each;    // 1: system-scope release before each done tag
+  uint64_t e[N][3];
 };
 
 // constexpr: usable from host and device code alike.

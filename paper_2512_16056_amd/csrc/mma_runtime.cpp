@@ -352,7 +352,8 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   Runtime* rt = g_rt;
   Engine* e = rt->eng[x->dir].get();
   std::lock_guard<std::mutex> g(rt->submit_mu);
-  if (!e->acquire_record(x.get(), 60000)) return fail(MMA_ERR_TIMEOUT, "no free transfer record for 60 s");
+  if (!e->acquire(x.get(), payload_bytes, kv != nullptr, 60000))
+    return fail(MMA_ERR_TIMEOUT, "no free transfer record for 60 s");
   static thread_local KernelArgs a;
   const uint32_t grid = e->prepare(x.get(), ++rt->seq, payload_bytes, kv,
                                    static_cast<uint64_t>(rt->cfg.watchdog_ms) * rt->wallclock_khz, a);
@@ -381,7 +382,7 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   }
   const hipError_t err = launch_transfer(a, grid, hs);
   if (err != hipSuccess) {
-    e->release_record_unused(x.get());
+    e->release_unused(x.get());
     return fail(MMA_ERR_HIP, "dummy-task kernel launch failed: %s", hipGetErrorString(err));
   }
   e->submit(std::move(x));

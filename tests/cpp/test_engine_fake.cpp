@@ -30,6 +30,7 @@
 #include <cstring>
 #include <deque>
 #include <functional>
+#include <future>
 #include <mutex>
 #include <random>
 #include <thread>
@@ -303,7 +304,7 @@ void wave(const KernelArgs a, uint32_t w, double wave_rate) {
           copy_at_rate(contig, pg, a.kv_piece_bytes, wave_rate);
       }
     }
-    astore(&rec->done[x % kRingSize], expect);
+    astore(&a.done[x % kRingSize], expect);
     t_prog = now_ns();
   }
   if (sc) return;
@@ -384,7 +385,7 @@ class Harness {
               bool early = false, bool launch = true) {
     Engine* e = eng_[x->dir].get();
     std::lock_guard<std::mutex> g(submit_mu_);
-    CHECK(e->acquire_record(x.get(), 60000), "record");
+    CHECK(e->acquire(x.get(), payload, kv != nullptr, 60000), "record");
     KernelArgs a;
     const uint32_t grid = e->prepare(x.get(), ++seq_, payload, kv, 20000ull * 1000000ull, a);
     const uint32_t waves = grid * kWavesPerWG;
@@ -602,6 +603,37 @@ void whole_transfers_on_cu() {
   std::printf("ok   transfers up to the whole-transfer limit run as self-contained CU launches\n");
 }
 
+// A deep queue of whole transfers on a stream that cannot progress yet: they
+// take light slots, so submission does not wait for the stream (records alone
+// would run out after 64), and every transfer lands once the stream runs.
+void deep_queue_does_not_block() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.whole[0] = s.cfg.whole[1] = 4 * 1024 * 1024;
+  Harness h(s);
+  FakeStream st;
+  std::promise<void> gate;
+  std::shared_future<void> open = gate.get_future().share();
+  st.launch([open] { open.wait(); });  // holds the stream
+  const int n = 600;
+  const uint64_t sz = 4096 + 16;
+  auto src = random_bytes(sz * n, 8);
+  std::vector<uint8_t> dst(sz * n, 0);
+  auto submitted = std::async(std::launch::async, [&] {
+    for (int i = 0; i < n; ++i)
+      h.submit(linear(MMA_H2D, dst.data() + i * sz, src.data() + i * sz, sz, h.cfg()), sz, st);
+  });
+  const bool quick = submitted.wait_for(std::chrono::seconds(20)) == std::future_status::ready;
+  CHECK(quick, "submitting %d whole transfers waited for the stream", n);
+  gate.set_value();
+  submitted.wait();
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst == src, "deep queue: bytes differ");
+  CHECK(h.stats().failed.load() == 0, "deep queue: failed transfers");
+  std::printf("ok   %d whole transfers queued behind a held stream without waiting for it\n", n);
+}
+
 // An early transfer whose dummy-task launch failed: the copy engines drain what
 // they hold, the record is retired without a kernel, no sticky error is left,
 // and the next transfer runs normally.
@@ -817,6 +849,7 @@ int main(int argc, char** argv) {
     kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging, idle-stream early start", true);
     unlaunched_transfer_drains();
     whole_transfers_on_cu();
+    deep_queue_does_not_block();
     submit_failures_rerouted();
     kv_submit_failures_rerouted();
     two_streams_both_directions();

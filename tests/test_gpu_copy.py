@@ -4,6 +4,8 @@ Every case calls the library through the C ABI (via the ctypes binding) and
 compares each destination byte -- inside and outside the copied ranges -- with
 oracle.copy on the same seeded inputs.
 """
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -176,6 +178,46 @@ def test_whole_transfers_on_cu_path(direction):
             host.free()
             if direction == mma.MMA_D2H:
                 back.free()
+
+
+def test_deep_queue_does_not_wait_for_the_stream():
+    """600 small copies queued on a stream held by a long-running kernel: they take light slots
+    (a whole self-contained launch needs no transfer record), so the calls return while the
+    stream is still held -- as hipMemcpyAsync would -- and every copy lands afterwards."""
+    n, sz = 600, 64 << 10
+    with session("both", cu_whole_bytes=0, cu_whole_bytes_d2h=0):
+        st = torch.cuda.Stream()
+        # a spin kernel of about 0.5 s holds the stream (calibrated on this GPU's clock)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        with torch.cuda.stream(st):
+            torch.cuda._sleep(10_000_000)
+        b.record(st)
+        b.synchronize()
+        cycles = int(10_000_000 * 500.0 / max(a.elapsed_time(b), 1e-3))
+        src_np = np.ascontiguousarray(W.uniform_bytes(15, 0, 0, n * sz))
+        src = mma.PinnedBuffer(n * sz)
+        src.array[:] = src_np
+        dst = device_bytes(n * sz, W.WEIGHT_POISON)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        with torch.cuda.stream(st):
+            torch.cuda._sleep(cycles)
+        e1.record(st)
+        t0 = time.perf_counter()
+        for i in range(n):
+            mma.mma_memcpy_async(dst.data_ptr() + i * sz, src.ptr + i * sz, sz, mma.MMA_H2D, st)
+        t_submit = time.perf_counter() - t0
+        held = not e1.query()  # the spin kernel is still running
+        st.synchronize()
+        spin_ms = e0.elapsed_time(e1)
+        log(f"  {n} submissions took {t_submit * 1e3:.1f} ms behind a {spin_ms:.0f} ms spin kernel")
+        assert held and t_submit * 1e3 < 0.5 * spin_ms, (t_submit, spin_ms)
+        assert np.array_equal(to_host(dst), src_np)
+        mma.mma_synchronize()
+        assert mma.mma_get_stats()["failed_transfers"] == 0
+        src.free()
 
 
 def _ragged_list(seed, count, max_size):
