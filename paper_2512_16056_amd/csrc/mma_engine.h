@@ -135,9 +135,10 @@ struct Transfer {
   std::atomic<bool> unlaunched{false};
   uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
   std::shared_ptr<Waiter> waiter;  // set for synchronous calls
-  // Per ring slot, set when an entry is appended (left uninitialised until then):
-  int32_t owner[kRingSize];    // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
-  uint8_t tdone[kRingSize];    // its done tag has been seen
+  // Per ring slot (kRingSize of them for a record, kPrefill for a light slot), set
+  // when an entry is appended (left uninitialised until then):
+  std::unique_ptr<int32_t[]> owner;  // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
+  std::unique_ptr<uint8_t[]> tdone;  // its done tag has been seen
   uint32_t cu_busy = 0;
   bool cu_full = false;
   int sdma_cu_pending = 0;     // SDMA slots that may still append ring entries (a staging step, or a
@@ -379,6 +380,10 @@ class Engine {
       return false;
     const uint32_t i = pool.front();
     pool.pop_front();
+    lk.unlock();
+    const uint32_t slots = light ? kPrefill : kRingSize;
+    x->owner.reset(new int32_t[slots]);
+    x->tdone.reset(new uint8_t[slots]);
     if (light) {
       x->light = static_cast<int32_t>(i);
       x->rec = nullptr;
@@ -538,13 +543,15 @@ class Engine {
   }
 
   void submit(std::unique_ptr<Transfer> x) {
+    bool wake;
     {
       std::lock_guard<std::mutex> g(mu_);
       incoming_.push_back(std::move(x));
       ++inflight_;
+      wake = engine_waiting_;
     }
     n_incoming_.fetch_add(1, std::memory_order_release);
-    cv_.notify_all();
+    if (wake) cv_.notify_all();  // the engine thread sleeps only after 2 ms without work
   }
 
   bool wait_idle(uint64_t timeout_ms) {
@@ -1115,7 +1122,9 @@ class Engine {
         std::unique_lock<std::mutex> lk(mu_);
         while (incoming_.empty()) {
           if (stop_) return;
+          engine_waiting_ = true;
           cv_.wait_for(lk, std::chrono::milliseconds(100));
+          engine_waiting_ = false;
         }
       }
       if (n_incoming_.load(std::memory_order_acquire) > 0) {
@@ -1206,6 +1215,7 @@ class Engine {
   std::deque<uint32_t> free_recs_, free_light_;
   uint64_t inflight_ = 0;
   bool stop_ = false;
+  bool engine_waiting_ = false;  // the engine thread waits on cv_ (guarded by mu_)
   std::atomic<bool> stop_flag_{false};
   std::atomic<uint64_t> n_incoming_{0};
   static constexpr uint64_t kIdleSpinNs = 2000000;  // 2 ms
