@@ -75,18 +75,30 @@ def calibration_kernels():
                                                               "copyBuffer: read N + write N"]}}), flush=True)
 
 
+# Every source file that the device code is compiled from, in a fixed order.
+KERNEL_SOURCES = ("mma_kernels.hip", "mma_proto.h", "mma_xpacked.h")
+
+
+def kernel_sources_sha256(root: str) -> str:
+    """SHA-256 over the device sources (each file's bytes, in KERNEL_SOURCES order)."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(root, "paper_2512_16056_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def recorded_traffic(root: str, kernel: str = "mma_transfer_kernel"):
     """HBM/EA bytes per launch of the transfer kernel from the committed rocprofv3 --pmc summary,
-    valid only while the kernel source is the one that was profiled."""
-    import hashlib
+    valid only while the device sources are the ones that were profiled."""
     path = os.path.join(root, "profiles", f"{kernel}__kv_fetch_64k.traffic.json")
-    src = os.path.join(root, "paper_2512_16056_amd", "csrc", "mma_kernels.hip")
     try:
         rec = json.load(open(path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        sha = kernel_sources_sha256(root)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_sha256") != sha:
+    if rec.get("kernel_sources_sha256") != sha:
         return None
     return rec.get("traffic_bytes_per_launch")
 
