@@ -98,7 +98,8 @@ typedef struct mma_config {
                                compares against (Section 5.1.2) -- a fixed split decided at plan
                                time: static_cu_percent of the micro-tasks (interleaved) go to the
                                CU path, the rest to the SDMA engines (which share them by pulling) */
-  uint32_t static_cu_percent;
+  uint32_t static_cu_percent; /* also, under MMA_CONTROL_DEVICE, the CU path's share of a linear
+                               transfer's bytes when the copy engines take part (0: 60) */
   uint32_t sdma_merge_tasks; /* at most this many micro-tasks that follow each other in both
                                address spaces (a linear run, or one KV block's consecutive pieces)
                                go to an SDMA engine as one command, and never more than the
@@ -114,7 +115,20 @@ typedef struct mma_config {
                                engine */
   uint32_t cu_whole_bytes_d2h; /* the same for device->host; default 8 MiB (CU stores to host
                                memory reach the link less efficiently than CU loads, measured) */
-  uint32_t reserved;
+  uint32_t control;         /* who drives a transfer once it is submitted (Section 6, Current
+                               limitations: a CPU-driven control plane costs fine-grained
+                               transfers scheduling time):
+                               MMA_CONTROL_HOST (0, default): the engine thread of the direction
+                                 pulls micro-tasks for every path while the transfer runs;
+                               MMA_CONTROL_DEVICE (1): the calling thread plans the whole transfer
+                                 at submission -- every CU-path entry is published before the
+                                 launch, and on a stream with nothing pending the copy engines get
+                                 a fixed share of a linear transfer at once -- and the dummy-task
+                                 kernel alone tracks completion; no host thread works on the
+                                 transfer afterwards (records are recycled by later calls). On a
+                                 stream with work pending, and for KV transfers, the CU path
+                                 carries the transfer alone. A transfer of more than 4096
+                                 micro-tasks still goes to the engine thread. */
 } mma_config_t;
 
 typedef struct mma_copy_desc {
@@ -139,6 +153,9 @@ typedef struct mma_copy_desc {
  *               multiples of 16, a 16-byte-aligned pool and layer tensors, and
  *               block_tokens * (head_dim * elem_bytes + 16) <= 36 KiB (one head of
  *               one block fits a wave's LDS tile); otherwise MMA_ERR_INVALID_ARG. */
+#define MMA_CONTROL_HOST 0u
+#define MMA_CONTROL_DEVICE 1u
+
 #define MMA_KV_LAYOUT_PIECE 0u
 #define MMA_KV_LAYOUT_XPACKED 1u
 typedef struct mma_kv_layout {

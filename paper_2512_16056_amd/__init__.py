@@ -26,6 +26,8 @@ MMA_D2H = 1
 MMA_PATH_CU = 0x80000000
 MMA_KV_LAYOUT_PIECE = 0
 MMA_KV_LAYOUT_XPACKED = 1
+MMA_CONTROL_HOST = 0
+MMA_CONTROL_DEVICE = 1
 MMA_NUM_PATHS = 17
 MMA_FAULT_ENGINE_STALL_US = 1
 MMA_FAULT_SDMA_SUBMIT_FAIL = 2
@@ -56,7 +58,7 @@ class mma_config_t(ctypes.Structure):
                 ("watchdog_ms", ctypes.c_uint32), ("static_split", ctypes.c_uint32),
                 ("static_cu_percent", ctypes.c_uint32), ("sdma_merge_tasks", ctypes.c_uint32),
                 ("cu_whole_bytes", ctypes.c_uint32), ("cu_whole_bytes_d2h", ctypes.c_uint32),
-                ("reserved", ctypes.c_uint32)]
+                ("control", ctypes.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}

@@ -14,6 +14,9 @@
 //   Task Launcher  -> Backend::copy (SDMA) and ring entries consumed by the
 //                     dummy-task kernel (CU path).
 //   Sync Engine    -> the record's started/complete words (Engine::advance).
+// Under device control (Engine::prepare_device) the submitting thread plans
+// the whole transfer and the kernel tracks its completion: no engine-thread
+// work per transfer.
 #ifndef MMA_ENGINE_H_
 #define MMA_ENGINE_H_
 
@@ -83,6 +86,9 @@ constexpr uint64_t kSmallSub = 16 * KiB;  // one wave register batch
 // CU entry size behind the default size limit of transfers taken whole by the
 // CU path: kPrefill entries of this size travel in the launch arguments (24 MiB).
 constexpr uint64_t kWholeMaxSub = 512 * KiB;
+// Device control: default CU-path share of a linear transfer's bytes when the
+// copy engines take part (the rest is split between the engines).
+constexpr uint32_t kDeviceCuPercent = 60;
 
 // ------------------------------------------------------------------ transfer
 enum class Kind : uint8_t { kLinear, kKvFetch, kKvOffload };
@@ -134,6 +140,11 @@ struct Transfer {
   // transfer failed: no kernel will ever run for it.
   std::atomic<bool> unlaunched{false};
   uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
+  uint64_t kv_per = 0;         // pieces per CU ring entry of a KV transfer (0: the engine thread's rule)
+  // Device control: planned in full at submission, retired by reap_device.
+  bool device = false;
+  uint32_t dev_cmds = 0;           // copy-engine commands counted by the record's device signal
+  std::vector<uint8_t> dev_path;   // path (stats index) that carries each micro-task
   std::shared_ptr<Waiter> waiter;  // set for synchronous calls
   // Per ring slot (kRingSize of them for a record, kPrefill for a light slot), set
   // when an entry is appended (left uninitialised until then):
@@ -195,6 +206,8 @@ struct Config {
   uint32_t static_split, static_cu_percent;
   uint32_t merge;       // max micro-tasks per copy-engine command
   uint64_t whole[2];    // per direction: transfers up to this size may be taken whole by the CU path (0: never)
+  uint32_t device;      // 1: device control (no engine thread in the loop)
+  uint32_t device_cu_percent;  // device control: the CU path's share of a linear transfer's bytes
 };
 
 struct Stats {
@@ -241,9 +254,15 @@ struct Backend {
   virtual void signal_destroy(uint64_t sig) = 0;
   virtual void signal_store(uint64_t sig, int64_t value) = 0;
   virtual int64_t signal_load(uint64_t sig) = 0;
-  // One command on copy engine `engine`; false if it was not accepted.
+  // One command on copy engine `engine`; false if it was not accepted. The
+  // command decrements `sig` by one when it has landed.
   virtual bool copy(int engine, void* dst, bool dst_on_device, const void* src, bool src_on_device,
                     uint64_t bytes, uint64_t sig) = 0;
+  // Device control: a completion signal that kernels poll; *value receives the
+  // device-visible address of its 64-bit value. false: not available.
+  virtual bool signal_create_polled(uint64_t* sig, const int64_t** value) = 0;
+  // Atomically subtracts v from the signal's value.
+  virtual void signal_sub(uint64_t sig, int64_t v) = 0;
   // Bit e set: copy engine e has no command queued for direction `dir`.
   virtual uint32_t engines_idle(int dir) = 0;
 };
@@ -296,6 +315,23 @@ class Engine {
       }
       paths_.push_back(p);
     }
+    // Device control: one polled completion signal per record for the copy
+    // engines' share. Without them the CU path carries device-controlled
+    // transfers alone.
+    if (cfg_.device && !paths_.empty()) {
+      for (uint32_t i = 0; i < kRecords; ++i) {
+        uint64_t sig = 0;
+        const int64_t* val = nullptr;
+        if (!be_->signal_create_polled(&sig, &val)) break;
+        dev_sig_.push_back(sig);
+        dev_sig_val_.push_back(val);
+      }
+      if (dev_sig_.size() != kRecords) {
+        for (uint64_t sig : dev_sig_) be_->signal_destroy(sig);
+        dev_sig_.clear();
+        dev_sig_val_.clear();
+      }
+    }
     mma_status_t w = warm_up();
     if (w != MMA_OK) return w;
     thread_ = std::thread([this] { loop(); });
@@ -342,6 +378,9 @@ class Engine {
     thread_.join();
     for (auto& s : slots_) be_->signal_destroy(s.sig);
     slots_.clear();
+    for (uint64_t sig : dev_sig_) be_->signal_destroy(sig);
+    dev_sig_.clear();
+    dev_sig_val_.clear();
     if (ds_) be_->free_device_state(ds_);
     if (recs_) be_->free_records(recs_);
     if (light_) be_->free_records(light_);
@@ -357,6 +396,7 @@ class Engine {
     return m;
   }
   bool cu_enabled() const { return (cfg_.mask[dir_] & MMA_PATH_CU) != 0; }
+  bool device_control() const { return cfg_.device != 0; }
   bool has_sdma() const { return !paths_.empty(); }
   uint64_t stage_bytes() const { return stage_bytes_; }
 
@@ -373,11 +413,10 @@ class Engine {
   // queue of small transfers on a stream does not wait for the GPU.
   bool acquire(Transfer* x, uint64_t payload_bytes, bool kv, uint64_t timeout_ms) {
     const bool light = whole_eligible(x, payload_bytes, kv);
+    if (cfg_.device) reap_device();
     std::unique_lock<std::mutex> lk(mu_);
     std::deque<uint32_t>& pool = light ? free_light_ : free_recs_;
-    if (pool.empty() &&
-        !cv_done_.wait_for(lk, std::chrono::milliseconds(timeout_ms), [&] { return !pool.empty(); }))
-      return false;
+    if (pool.empty() && !wait_for_pool(lk, pool, timeout_ms)) return false;
     const uint32_t i = pool.front();
     pool.pop_front();
     lk.unlock();
@@ -397,6 +436,26 @@ class Engine {
     }
     return true;
   }
+  // Waits (lk held on entry and exit) until `pool` has a free entry. Under
+  // device control no thread signals a recycled record, so this thread reaps.
+  bool wait_for_pool(std::unique_lock<std::mutex>& lk, const std::deque<uint32_t>& pool, uint64_t timeout_ms) {
+    const auto deadline = std::chrono::steady_clock::now() + std::chrono::milliseconds(timeout_ms);
+    while (pool.empty()) {
+      const auto now = std::chrono::steady_clock::now();
+      if (now >= deadline) return false;
+      if (cfg_.device) {
+        lk.unlock();
+        reap_device();
+        lk.lock();
+        if (!pool.empty()) break;
+        cv_done_.wait_for(lk, std::chrono::microseconds(20));
+      } else {
+        cv_done_.wait_until(lk, deadline);
+      }
+    }
+    return true;
+  }
+
   void release_unused(Transfer* x) {
     std::lock_guard<std::mutex> g(mu_);
     if (x->light >= 0)
@@ -505,6 +564,13 @@ class Engine {
       x->closed = x->completed = true;
       x->t_complete = x->t_submit;
     }
+    fill_args(x, kv, n_pre, grid, watchdog_ticks, a);
+    return grid;
+  }
+
+  // Kernel arguments common to both control modes.
+  void fill_args(const Transfer* x, const KvGeom* kv, uint32_t n_pre, uint32_t grid, uint64_t watchdog_ticks,
+                 KernelArgs& a) const {
     memset(&a, 0, offsetof(KernelArgs, layer_ptr));
     a.n_pre = n_pre;
     a.self_contained = x->self_contained ? 1u : 0u;
@@ -539,7 +605,217 @@ class Engine {
     a.watchdog_ticks = watchdog_ticks;
     a.total_waves = grid * kWavesPerWG;
     a.release_each = x->dir == MMA_D2H ? 1u : 0u;
+  }
+
+  // ---------------------------------------------------------------- device control
+  // A control plane with no host thread in the loop -- the direction Section 6
+  // (Current limitations) gives for the cost of a CPU-driven control plane on
+  // fine-grained transfers. The submitting thread plans the whole transfer
+  // before the launch:
+  //   - the CU path's share goes into the record's ring in full, so the
+  //     kernel's waves claim every entry with their device atomic and nothing
+  //     is ever appended later;
+  //   - on a stream with nothing pending, a fixed share of a linear transfer
+  //     (the last 100 - device_cu_percent % of its bytes) goes to the copy
+  //     engines at once, split between them, all commands counting down one
+  //     polled completion signal.
+  // The kernel's last wave waits for that signal instead of the engine
+  // thread's `complete` word, and the submitting thread recycles the record
+  // once the kernel has released it (reap_device). Against the engine thread
+  // this gives up pulling and back-off on the copy engines, whose share is
+  // fixed at submission, and copy engines on a stream with work pending: a
+  // command that waited for the stream would hold the head of the engine's
+  // in-order queue, which every other copy of the process shares. KV
+  // transfers run on the CU path alone (their copy-engine share would need
+  // staging slots recycled between commands). Returns the grid, or 0 if the
+  // transfer has more micro-tasks than the ring has entries; the caller then
+  // hands it to the engine thread.
+  uint32_t prepare_device(Transfer* x, uint64_t seq, uint64_t payload_bytes, const KvGeom* kv,
+                          uint64_t watchdog_ticks, bool stream_idle, KernelArgs& a) {
+    const size_t n = x->tasks.size();
+    if (n == 0 || n > kRingSize || !x->rec) return 0;
+    const bool linear = x->kind == Kind::kLinear;
+    // CU entry size: the engine thread's, grown until every micro-task would
+    // fit the ring, so that the tasks of a command the runtime refuses can
+    // still go to the CU path.
+    uint64_t per, biggest = 0;
+    for (const Task& t : x->tasks) biggest = std::max(biggest, t.bytes);
+    if (linear) {
+      per = cfg_.sub;
+      if (payload_bytes <= kPrefill * cfg_.sub) {
+        const uint64_t p = (payload_bytes + kPrefill - 1) / kPrefill;
+        per = std::min<uint64_t>(cfg_.sub, std::max<uint64_t>(kSmallSub, (p + kSmallSub - 1) / kSmallSub * kSmallSub));
+      }
+    } else {
+      per = x->pool_dev ? biggest : std::max<uint64_t>(1, cfg_.sub / x->piece);
+    }
+    auto entries = [&](uint64_t p) {
+      uint64_t e = 0;
+      for (const Task& t : x->tasks) e += (t.bytes + p - 1) / p;
+      return e;
+    };
+    while (per < biggest && entries(per) > kRingSize) per = std::min(biggest, 2 * per);
+    if (entries(per) > kRingSize) return 0;
+    if (linear)
+      x->sub = per;
+    else
+      x->kv_per = per;
+
+    x->claimed.assign(n, 0);
+    x->left.assign(n, 0);
+    x->dev_path.assign(n, static_cast<uint8_t>(MMA_NUM_PATHS - 1));
+    x->seq = seq;
+    x->t_submit = x->t_started = now_ns();
+    x->bytes = payload_bytes;
+    x->device = x->started = x->closed = true;
+    Record* r = x->rec;
+    r->h.seq = seq;
+    r->h.status = 0;
+    __atomic_thread_fence(__ATOMIC_RELEASE);
+
+    // The copy engines' share: the last micro-tasks, by bytes.
+    std::vector<size_t> eng_tasks;
+    if (stream_idle && linear && x->sdma_ok && !dev_sig_.empty()) {
+      const uint64_t cu_pct = cu_enabled() ? cfg_.device_cu_percent : 0;
+      const uint64_t want = payload_bytes / 100 * (100 - cu_pct) + payload_bytes % 100 * (100 - cu_pct) / 100;
+      uint64_t got = 0;
+      for (size_t i = n; i-- > 0 && got < want;) {
+        if (x->tasks[i].flags & kPlanCuOnly) continue;
+        eng_tasks.push_back(i);
+        got += x->tasks[i].bytes;
+      }
+      std::reverse(eng_tasks.begin(), eng_tasks.end());
+      for (size_t i : eng_tasks) x->claimed[i] = 1;
+    }
+    // The CU path's share, in task order.
+    x->pushed = 0;
+    for (size_t i = 0; i < n; ++i)
+      if (!x->claimed[i]) push_device(x, i);
+    // Engine k takes the engine tasks whose first byte falls in the k-th equal
+    // part of their bytes; runs that follow each other in both address spaces
+    // go as one command.
+    struct Cmd {
+      int path;
+      size_t first, end;
+      uint64_t bytes;
+    };
+    std::vector<Cmd> cmds;
+    uint64_t total = 0, at = 0;
+    for (size_t i : eng_tasks) total += x->tasks[i].bytes;
+    for (size_t k = 0; k < eng_tasks.size(); ++k) {
+      const size_t i = eng_tasks[k];
+      const Task& t = x->tasks[i];
+      const int path = static_cast<int>(at * paths_.size() / std::max<uint64_t>(total, 1));
+      at += t.bytes;
+      if (!cmds.empty()) {
+        Cmd& c = cmds.back();
+        const Task& prev = x->tasks[c.end - 1];
+        if (c.path == path && c.end == i && t.src_dma == prev.src_dma + prev.bytes &&
+            t.dst_dma == prev.dst_dma + prev.bytes) {
+          c.end = i + 1;
+          c.bytes += t.bytes;
+          continue;
+        }
+      }
+      cmds.push_back(Cmd{path, i, i + 1, t.bytes});
+    }
+    const uint64_t sig = cmds.empty() ? 0 : dev_sig_[x->rec_idx];
+    if (!cmds.empty()) be_->signal_store(sig, static_cast<int64_t>(cmds.size()));
+    const bool h2d = dir_ == MMA_H2D;
+    for (const Cmd& c : cmds) {
+      const Task& t = x->tasks[c.first];
+      bool ok = true;
+      uint64_t f = g_fault_submit_fail.load();
+      while (ok && f > 0)
+        if (g_fault_submit_fail.compare_exchange_weak(f, f - 1)) ok = false;
+      ok = ok && be_->copy(paths_[c.path].engine, reinterpret_cast<void*>(t.dst_dma), h2d,
+                           reinterpret_cast<void*>(t.src_dma), !h2d, c.bytes, sig);
+      if (ok) {
+        st_->sdma_commands += 1;
+        if (!x->t_first_sdma) x->t_first_sdma = now_ns();
+        for (size_t i = c.first; i < c.end; ++i) x->dev_path[i] = static_cast<uint8_t>(paths_[c.path].engine);
+      } else {
+        // Refused: its tasks go to the CU path (the ring has room for them).
+        st_->submit_failures += 1;
+        be_->signal_sub(sig, 1);
+        for (size_t i = c.first; i < c.end; ++i) push_device(x, i);
+      }
+    }
+    x->dev_cmds = static_cast<uint32_t>(cmds.size());
+
+    uint32_t grid;
+    if (x->pool_dev) {
+      grid = grid_for(payload_bytes, x->sub, true, false, true, false);
+    } else {
+      const uint64_t cap = std::min<uint64_t>(
+          kv && kv->layout == kKvLayoutXPacked ? 2ull * cfg_.cu_wgs : cfg_.cu_wgs, kMaxWorkgroups);
+      grid = static_cast<uint32_t>(
+          std::max<uint64_t>(1, std::min<uint64_t>((x->pushed + kWavesPerWG - 1) / kWavesPerWG, cap)));
+    }
+    x->waves = grid * kWavesPerWG;
+    const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
+    fill_args(x, kv, n_pre, grid, watchdog_ticks, a);
+    a.device_ctl = 1;
+    a.n_total = static_cast<uint32_t>(x->pushed);
+    a.sdma_left = x->dev_cmds ? dev_sig_val_[x->rec_idx] : nullptr;
     return grid;
+  }
+
+  // Device control: track a launched transfer (prepare_device, or a whole
+  // transfer in a light slot) until reap_device retires it.
+  void add_device(std::unique_ptr<Transfer> x) {
+    x->device = true;
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      ++inflight_;
+    }
+    std::lock_guard<std::mutex> g(dev_mu_);
+    dev_active_.push_back(std::move(x));
+  }
+
+  // Device control: the dummy-task launch failed after the copy engines were
+  // given their share. Waits for them (they write the caller's buffers), then
+  // frees the record; one that does not drain is never reused.
+  void abandon_device(Transfer* x, uint64_t timeout_ms) {
+    if (x->dev_cmds) {
+      const uint64_t sig = dev_sig_[x->rec_idx];
+      const uint64_t t0 = now_ns();
+      while (be_->signal_load(sig) > 0) {
+        if (now_ns() - t0 > timeout_ms * 1000000ull) return;
+        std::this_thread::sleep_for(std::chrono::microseconds(20));
+      }
+    }
+    release_unused(x);
+  }
+
+  // Device control: retire tracked transfers whose kernel has finished with
+  // their record (and whose copy-engine commands have all landed, even after a
+  // watchdog). Any thread may call it. Only the oldest kReapWindow transfers
+  // are looked at, so a deep queue costs each submission a bounded scan;
+  // transfers on one stream finish in order, so the oldest go first.
+  void reap_device() {
+    std::lock_guard<std::mutex> g(dev_mu_);
+    for (size_t k = 0; k < dev_active_.size() && k < kReapWindow;) {
+      Transfer* x = dev_active_[k].get();
+      if (!device_done(x)) {
+        ++k;
+        continue;
+      }
+      bool bad = false;
+      if (x->rec) bad = ld_acq(&x->rec->h.status) != 0;
+      if (x->dev_cmds && be_->signal_load(dev_sig_[x->rec_idx]) < 0) bad = true;
+      x->t_last_task = x->t_complete = now_ns();
+      for (size_t i = 0; i < x->tasks.size(); ++i) {
+        const int path = x->dev_path.empty() ? MMA_NUM_PATHS - 1 : x->dev_path[i];
+        const Task& t = x->tasks[i];
+        st_->path_bytes[path] += x->kind == Kind::kLinear ? t.bytes : t.bytes * x->piece;
+        st_->path_tasks[path] += 1;
+        ++x->path_tasks[path];
+      }
+      x->n_done = x->tasks.size();
+      finish(x, bad, true);
+      dev_active_.erase(dev_active_.begin() + static_cast<long>(k));
+    }
   }
 
   void submit(std::unique_ptr<Transfer> x) {
@@ -555,8 +831,18 @@ class Engine {
   }
 
   bool wait_idle(uint64_t timeout_ms) {
-    std::unique_lock<std::mutex> lk(mu_);
-    return cv_done_.wait_for(lk, std::chrono::milliseconds(timeout_ms), [&] { return inflight_ == 0; });
+    const auto deadline = std::chrono::steady_clock::now() + std::chrono::milliseconds(timeout_ms);
+    for (;;) {
+      if (cfg_.device) reap_device();
+      std::unique_lock<std::mutex> lk(mu_);
+      if (inflight_ == 0) return true;
+      const auto now = std::chrono::steady_clock::now();
+      if (now >= deadline) return false;
+      if (cfg_.device)
+        cv_done_.wait_for(lk, std::chrono::microseconds(50));
+      else
+        cv_done_.wait_until(lk, deadline);
+    }
   }
 
  private:
@@ -566,7 +852,7 @@ class Engine {
   // destination; KV: GPU block). Returns the number appended, 0 if no room.
   uint32_t push_unit(Transfer* x, int32_t owner, uint32_t kind, uint64_t a, uint64_t b, uint64_t count,
                      uint32_t p0) {
-    uint64_t per, ne;
+    uint64_t per;
     if ((kind & kEntryKindMask) == kEntryCopy) {
       per = x->sub;
     } else {
@@ -574,9 +860,17 @@ class Engine {
       // HBM-resident pool (latency ~1 us instead of several) a whole micro-task.
       per = x->pool_dev ? count : std::max<uint64_t>(1, cfg_.sub / x->piece);
     }
-    ne = (count + per - 1) / per;
+    const uint64_t ne = (count + per - 1) / per;
     // Keep one slot per wave free for the end markers written at close.
     if (x->pushed + ne - x->done_upto > kRingSize - x->waves) return 0;
+    return append(x, owner, kind, a, b, count, p0, per);
+  }
+
+  // Appends the entries of one unit of work, `per` bytes (linear) or pieces
+  // (KV) each; the caller has checked that they fit the ring.
+  uint32_t append(Transfer* x, int32_t owner, uint32_t kind, uint64_t a, uint64_t b, uint64_t count, uint32_t p0,
+                  uint64_t per) {
+    const uint64_t ne = (count + per - 1) / per;
     for (uint64_t k = 0; k < ne; ++k) {
       const uint64_t t = x->pushed++;
       const uint32_t slot = static_cast<uint32_t>(t % kRingSize);
@@ -637,6 +931,55 @@ class Engine {
     }
     while (x->done_upto < x->pushed && x->tdone[x->done_upto % kRingSize]) ++x->done_upto;
     return p;
+  }
+
+  // Device control: all CU ring entries of micro-task i (prepare_device has
+  // sized them so that every task fits the ring).
+  void push_device(Transfer* x, size_t i) {
+    const Task& t = x->tasks[i];
+    if (x->kind == Kind::kLinear)
+      append(x, static_cast<int32_t>(i), kEntryCopy, t.src_cu, t.dst_cu, t.bytes, 0, x->sub);
+    else
+      append(x, static_cast<int32_t>(i), x->kind == Kind::kKvFetch ? kEntryToPaged : kEntryFromPaged, t.host_cu,
+             t.blk, t.bytes, t.p0, x->kv_per);
+    x->claimed[i] = 1;
+    x->dev_path[i] = static_cast<uint8_t>(MMA_NUM_PATHS - 1);
+  }
+
+  // Device control: the kernel is done with the transfer's record or light slot.
+  bool device_done(const Transfer* x) const {
+    if (x->light >= 0) {  // a whole transfer: every entry's done tag is in
+      for (uint64_t t = 0; t < x->pushed; ++t)
+        if (ld_acq(&x->done_host[t]) != make_tag(x->seq, t)) return false;
+      return true;
+    }
+    if (ld_acq(&x->rec->h.released) != x->seq) return false;
+    return !x->dev_cmds || be_->signal_load(dev_sig_[x->rec_idx]) <= 0;
+  }
+
+  // Outcome, trace and waiter of a retired transfer; frees its record or light slot.
+  void finish(Transfer* x, bool bad, bool counted) {
+    if (bad) {
+      g_sticky.store(1);
+      st_->failed += 1;
+    }
+    if (counted) st_->transfers += 1;
+    if (g_trace.load(std::memory_order_relaxed)) record_trace(x, bad);
+    if (x->waiter) {
+      std::lock_guard<std::mutex> g(x->waiter->mu);
+      x->waiter->done = true;
+      x->waiter->failed = bad;
+      x->waiter->cv.notify_all();
+    }
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      if (x->light >= 0)
+        free_light_.push_back(static_cast<uint32_t>(x->light));
+      else
+        free_recs_.push_back(x->rec_idx);
+      --inflight_;
+    }
+    cv_done_.notify_all();
   }
 
   // ---------------------------------------------------------------- CU path
@@ -1160,27 +1503,7 @@ class Engine {
         const bool unlaunched = x->unlaunched.load(std::memory_order_relaxed);
         const bool bad =
             !unlaunched && (x->failed || x->ignored || (x->rec && ld_acq(&x->rec->h.status) != 0));
-        if (bad) {
-          g_sticky.store(1);
-          st_->failed += 1;
-        }
-        if (!unlaunched) st_->transfers += 1;
-        if (g_trace.load(std::memory_order_relaxed)) record_trace(x, bad);
-        if (x->waiter) {
-          std::lock_guard<std::mutex> g(x->waiter->mu);
-          x->waiter->done = true;
-          x->waiter->failed = bad;
-          x->waiter->cv.notify_all();
-        }
-        {
-          std::lock_guard<std::mutex> g(mu_);
-          if (x->light >= 0)
-            free_light_.push_back(static_cast<uint32_t>(x->light));
-          else
-            free_recs_.push_back(x->rec_idx);
-          --inflight_;
-        }
-        cv_done_.notify_all();
+        finish(x, bad, !unlaunched);
         active_.erase(active_.begin() + static_cast<long>(i));
         p = true;
       }
@@ -1213,6 +1536,12 @@ class Engine {
   std::deque<std::unique_ptr<Transfer>> incoming_;
   std::vector<std::unique_ptr<Transfer>> active_;  // engine thread only
   std::deque<uint32_t> free_recs_, free_light_;
+  // Device control: per record, the copy engines' polled completion signal and
+  // its device-visible value; transfers launched and not yet retired.
+  std::vector<uint64_t> dev_sig_;
+  std::vector<const int64_t*> dev_sig_val_;
+  std::mutex dev_mu_;  // taken before mu_, never after it
+  std::deque<std::unique_ptr<Transfer>> dev_active_;
   uint64_t inflight_ = 0;
   bool stop_ = false;
   bool engine_waiting_ = false;  // the engine thread waits on cv_ (guarded by mu_)
@@ -1220,6 +1549,7 @@ class Engine {
   std::atomic<uint64_t> n_incoming_{0};
   static constexpr uint64_t kIdleSpinNs = 2000000;  // 2 ms
   static constexpr uint64_t kTagGraceNs = 100000000;  // 100 ms
+  static constexpr size_t kReapWindow = 512;
   std::thread thread_;
 };
 

@@ -324,6 +324,7 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
     if (lane == 0)
       x = __hip_atomic_fetch_add(&ds->cursor, static_cast<uint64_t>(1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     x = lane_u64(x, 0);
+    if (a.device_ctl && x >= a.n_total) break;  // the whole CU share was in the ring at launch
     const uint64_t expect = make_tag(a.seq, x);
     const uint64_t* ew = reinterpret_cast<const uint64_t*>(&rec->ring[x % kRingSize]);
     uint32_t state = 0;  // 1: entry ready, 3: watchdog
@@ -413,18 +414,34 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
     const uint32_t n = __hip_atomic_fetch_add(&ds->exited, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (n == a.total_waves - 1) {
       uint32_t to = __hip_atomic_load(&ds->timed_out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      while (!to && ld_sys(&rec->h.complete) != a.seq) {
-        const uint64_t now = wall_clock64();
-        const uint64_t hb2 = ld_sys(&rec->h.heartbeat);
-        if (hb2 != hb) {
-          hb = hb2;
-          t_prog = now;
-        } else if (now - t_prog > a.watchdog_ticks) {
-          to = 1;
+      int32_t status = 0;
+      if (a.device_ctl) {
+        // Every wave has left, so the CU share has landed; the copy engines'
+        // share has when their completion signal reaches 0. Nothing re-arms
+        // the watchdog here: it runs from this wave's last completion.
+        int64_t left = 0;
+        while (!to && a.sdma_left &&
+               (left = __hip_atomic_load(const_cast<int64_t*>(a.sdma_left), __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_SYSTEM)) > 0) {
+          if (wall_clock64() - t_prog > a.watchdog_ticks) to = 1;
+          __builtin_amdgcn_s_sleep(8);
         }
-        __builtin_amdgcn_s_sleep(8);
+        if (left < 0) status = 2;
+      } else {
+        while (!to && ld_sys(&rec->h.complete) != a.seq) {
+          const uint64_t now = wall_clock64();
+          const uint64_t hb2 = ld_sys(&rec->h.heartbeat);
+          if (hb2 != hb) {
+            hb = hb2;
+            t_prog = now;
+          } else if (now - t_prog > a.watchdog_ticks) {
+            to = 1;
+          }
+          __builtin_amdgcn_s_sleep(8);
+        }
       }
-      if (to) __hip_atomic_store(&rec->h.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      if (to) status = 1;
+      if (status) __hip_atomic_store(&rec->h.status, status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       __hip_atomic_store(&ds->cursor, static_cast<uint64_t>(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&ds->arrived, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&ds->exited, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

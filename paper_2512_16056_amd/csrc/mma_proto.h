@@ -79,7 +79,7 @@ struct alignas(64) RecordHdr {
   uint64_t pad1[7];
   // cache line 2: GPU -> host
   uint64_t released;     // == seq once the kernel is done with this record
-  int32_t status;        // 0 ok, 1 watchdog expired
+  int32_t status;        // 0 ok, 1 watchdog expired, 2 a copy-engine command failed (device control)
   int32_t pad2a;
   uint64_t pad2[6];
 };
@@ -108,6 +108,14 @@ struct KernelArgs {
   uint64_t watchdog_ticks;  // wall-clock ticks without progress before giving up
   uint32_t total_waves;
   uint32_t release_each;    // 1: system-scope release before each done flag
+  // Device control (no engine thread in the loop): every CU entry is in the
+  // ring before the launch, so tickets [0, n_total) are the whole CU share and
+  // a ticket past it ends a wave's claims; the last wave then waits until the
+  // copy engines' completion signal, whose value sdma_left points at (null if
+  // they carry nothing), has counted down to 0 -- negative if a command failed.
+  const int64_t* sdma_left;
+  uint32_t device_ctl;
+  uint32_t n_total;
   // KV geometry (unused by linear transfers)
   uint64_t kv_piece_bytes;
   uint64_t kv_kstride;      // bytes between the K and V halves of a GPU layer tensor

@@ -95,6 +95,24 @@ class HsaBackend final : public Backend {
   void signal_destroy(uint64_t sig) override { hsa_signal_destroy(hsa_signal_t{sig}); }
   void signal_store(uint64_t sig, int64_t v) override { hsa_signal_store_screlease(hsa_signal_t{sig}, v); }
   int64_t signal_load(uint64_t sig) override { return hsa_signal_load_scacquire(hsa_signal_t{sig}); }
+  // A signal consumed by GPUs only, whose value a kernel may poll. The value
+  // must be the one inside the signal object that the copy engines decrement
+  // (the handle is that object's address and the value follows its 8-byte
+  // kind); anything else and the copy engines stay out of device control.
+  bool signal_create_polled(uint64_t* sig, const int64_t** value) override {
+    hsa_signal_t s;
+    if (hsa_amd_signal_create(0, 0, nullptr, HSA_AMD_SIGNAL_AMD_GPU_ONLY, &s) != HSA_STATUS_SUCCESS) return false;
+    volatile hsa_signal_value_t* v = nullptr;
+    if (hsa_amd_signal_value_pointer(s, &v) != HSA_STATUS_SUCCESS || !v ||
+        reinterpret_cast<uint64_t>(v) != s.handle + 8) {
+      hsa_signal_destroy(s);
+      return false;
+    }
+    *sig = s.handle;
+    *value = const_cast<const int64_t*>(reinterpret_cast<volatile int64_t*>(v));
+    return true;
+  }
+  void signal_sub(uint64_t sig, int64_t v) override { hsa_signal_subtract_screlease(hsa_signal_t{sig}, v); }
   bool copy(int engine, void* dst, bool dst_on_device, const void* src, bool src_on_device, uint64_t bytes,
             uint64_t sig) override {
     return hsa_amd_memory_async_copy_on_engine(dst, dst_on_device ? gpu_ : cpu_, src, src_on_device ? gpu_ : cpu_,
@@ -355,14 +373,34 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   if (!e->acquire(x.get(), payload_bytes, kv != nullptr, 60000))
     return fail(MMA_ERR_TIMEOUT, "no free transfer record for 60 s");
   static thread_local KernelArgs a;
-  const uint32_t grid = e->prepare(x.get(), ++rt->seq, payload_bytes, kv,
-                                   static_cast<uint64_t>(rt->cfg.watchdog_ms) * rt->wallclock_khz, a);
+  const uint64_t wd = static_cast<uint64_t>(rt->cfg.watchdog_ms) * rt->wallclock_khz;
   if (tl_waiter) {
     x->waiter = tl_waiter;
     tl_waiter->submitted = true;
   }
   DeviceGuard dg(rt->dev);
   const hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (e->device_control()) {
+    // Device control: the transfer is planned in full here and the kernel
+    // tracks its completion; no engine-thread work. A transfer with more
+    // micro-tasks than a ring holds goes to the engine thread instead.
+    const uint32_t grid = x->light >= 0 ? e->prepare(x.get(), ++rt->seq, payload_bytes, kv, wd, a)
+                                        : e->prepare_device(x.get(), ++rt->seq, payload_bytes, kv, wd,
+                                                            stream_idle(hs), a);
+    if (grid) {
+      const hipError_t err = launch_transfer(a, grid, hs);
+      if (err != hipSuccess) {
+        if (x->light >= 0)
+          e->release_unused(x.get());
+        else
+          e->abandon_device(x.get(), rt->cfg.watchdog_ms + 10000ull);
+        return fail(MMA_ERR_HIP, "dummy-task kernel launch failed: %s", hipGetErrorString(err));
+      }
+      e->add_device(std::move(x));
+      return MMA_OK;
+    }
+  }
+  const uint32_t grid = e->prepare(x.get(), ++rt->seq, payload_bytes, kv, wd, a);
   if (!x->self_contained && x->sdma_ok && e->has_sdma() && x->n_claimed < x->tasks.size() && stream_idle(hs)) {
     x->early = true;
     // If the launch fails, the copy engines may already hold part of the
@@ -400,7 +438,10 @@ void fill_config(mma_config_t* c, bool use_env) {
   d.watchdog_ms = 20000;
   d.cu_whole_bytes = static_cast<uint32_t>(kPrefill * kWholeMaxSub);
   d.cu_whole_bytes_d2h = static_cast<uint32_t>(8 * MiB);
+  d.control = MMA_CONTROL_HOST;
   if (use_env) {
+    d.control = static_cast<uint32_t>(env_u64("MMA_CONTROL", d.control));
+    d.static_cu_percent = static_cast<uint32_t>(env_u64("MMA_STATIC_CU_PERCENT", 0));
     d.chunk_bytes = env_u64("MMA_CHUNK_BYTES", d.chunk_bytes);
     d.fallback_bytes = env_u64("MMA_FALLBACK_BYTES", 0);
     d.small_bytes = env_u64("MMA_SMALL_BYTES", d.small_bytes);
@@ -511,6 +552,9 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   k.mask[0] = mask[0];
   k.mask[1] = mask[1];
   if (c.static_cu_percent > 100) return fail(MMA_ERR_INVALID_ARG, "static_cu_percent > 100");
+  if (c.control > MMA_CONTROL_DEVICE) return fail(MMA_ERR_INVALID_ARG, "unknown control mode %u", c.control);
+  k.device = c.control == MMA_CONTROL_DEVICE ? 1u : 0u;
+  k.device_cu_percent = c.static_cu_percent ? c.static_cu_percent : kDeviceCuPercent;
   k.static_split = c.static_split;
   k.static_cu_percent = c.static_cu_percent;
   k.whole[MMA_H2D] = c.cu_whole_bytes;
@@ -629,11 +673,23 @@ mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir)
     if (e != hipSuccess) return fail(MMA_ERR_HIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
   }
   // The stream has passed the dummy task; the engine retires the transfer
-  // right after, which is when its outcome is final.
+  // right after (under device control, this thread does), which is when its
+  // outcome is final.
+  Engine* e = g_rt->eng[dir].get();
   std::unique_lock<std::mutex> lk(w->mu);
-  const uint64_t ms = static_cast<uint64_t>(g_rt->cfg.watchdog_ms) + 10000;
-  if (!w->cv.wait_for(lk, std::chrono::milliseconds(ms), [&] { return w->done; }))
-    return fail(MMA_ERR_TIMEOUT, "copy not retired");
+  const auto deadline = std::chrono::steady_clock::now() +
+                        std::chrono::milliseconds(static_cast<uint64_t>(g_rt->cfg.watchdog_ms) + 10000);
+  while (!w->done) {
+    if (std::chrono::steady_clock::now() >= deadline) return fail(MMA_ERR_TIMEOUT, "copy not retired");
+    if (e->device_control()) {
+      lk.unlock();
+      e->reap_device();
+      lk.lock();
+      if (!w->done) w->cv.wait_for(lk, std::chrono::microseconds(20));
+    } else {
+      w->cv.wait_until(lk, deadline);
+    }
+  }
   return w->failed ? fail(MMA_ERR_TRANSFER_FAILED, "the copy failed") : MMA_OK;
 }
 

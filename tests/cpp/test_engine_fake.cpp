@@ -110,6 +110,17 @@ class FakeBackend final : public Backend {
   int64_t signal_load(uint64_t sig) override {
     return reinterpret_cast<std::atomic<int64_t>*>(sig)->load(std::memory_order_acquire);
   }
+  bool signal_create_polled(uint64_t* sig, const int64_t** value) override {
+    if (!polled_) return false;
+    auto* a = new std::atomic<int64_t>(0);
+    *sig = reinterpret_cast<uint64_t>(a);
+    *value = reinterpret_cast<const int64_t*>(a);
+    return true;
+  }
+  void signal_sub(uint64_t sig, int64_t v) override {
+    reinterpret_cast<std::atomic<int64_t>*>(sig)->fetch_sub(v, std::memory_order_acq_rel);
+  }
+  void set_polled(bool on) { polled_ = on; }
   bool copy(int engine, void* dst, bool, const void* src, bool, uint64_t bytes, uint64_t sig) override {
     if (engine < 0 || engine >= static_cast<int>(engines_.size())) return false;
     Eng* e = engines_[engine].get();
@@ -164,10 +175,11 @@ class FakeBackend final : public Backend {
       sleep_ns(cmd_ns_ + static_cast<uint64_t>(c.bytes * 1000.0 / e->rate));
       std::memcpy(c.dst, c.src, c.bytes);
       e->pending.fetch_sub(1);
-      signal_store(c.sig, 0);
+      signal_sub(c.sig, 1);  // a landed command decrements its signal
     }
   }
   uint64_t cmd_ns_;
+  bool polled_ = true;
   std::vector<std::unique_ptr<Eng>> engines_;
 };
 
@@ -255,6 +267,7 @@ void wave(const KernelArgs a, uint32_t w, double wave_rate) {
       if (x >= a.n_pre) break;
     } else {
       x = __atomic_fetch_add(&ds->cursor, 1ull, __ATOMIC_RELAXED);
+      if (a.device_ctl && x >= a.n_total) break;
     }
     const uint64_t expect = make_tag(a.seq, x);
     uint64_t w1, w2, w3;
@@ -312,17 +325,28 @@ void wave(const KernelArgs a, uint32_t w, double wave_rate) {
   const uint32_t n = __atomic_fetch_add(&ds->exited, 1u, __ATOMIC_ACQ_REL);
   if (n == a.total_waves - 1) {
     bool to = __atomic_load_n(&ds->timed_out, __ATOMIC_RELAXED) != 0;
-    while (!to && aload(&rec->h.complete) != a.seq) {
-      const uint64_t hb2 = aload(&rec->h.heartbeat);
-      if (hb2 != hb) {
-        hb = hb2;
-        t_prog = now_ns();
-      } else if (now_ns() - t_prog > a.watchdog_ticks) {
-        to = true;
+    int32_t status = 0;
+    if (a.device_ctl) {
+      int64_t left = 0;
+      while (!to && a.sdma_left && (left = aload(a.sdma_left)) > 0) {
+        if (now_ns() - t_prog > a.watchdog_ticks) to = true;
+        std::this_thread::yield();
       }
-      std::this_thread::yield();
+      if (left < 0) status = 2;
+    } else {
+      while (!to && aload(&rec->h.complete) != a.seq) {
+        const uint64_t hb2 = aload(&rec->h.heartbeat);
+        if (hb2 != hb) {
+          hb = hb2;
+          t_prog = now_ns();
+        } else if (now_ns() - t_prog > a.watchdog_ticks) {
+          to = true;
+        }
+        std::this_thread::yield();
+      }
     }
-    if (to) astore(&rec->h.status, 1);
+    if (to) status = 1;
+    if (status) astore(&rec->h.status, status);
     __atomic_store_n(&ds->cursor, 0ull, __ATOMIC_RELAXED);
     __atomic_store_n(&ds->arrived, 0u, __ATOMIC_RELAXED);
     __atomic_store_n(&ds->exited, 0u, __ATOMIC_RELAXED);
@@ -405,6 +429,43 @@ class Harness {
       for (auto& t : ts) t.join();
     });
     if (x) e->submit(std::move(x));
+  }
+  // The runtime's submit() under device control: light (whole) transfers and
+  // transfers that fit a ring are planned in full and launched; the engine
+  // thread never sees them. Others fall back to submit(). idle: the stream is
+  // taken to have nothing pending; launch = false: the launch "fails".
+  void submit_device(std::unique_ptr<Transfer> x, uint64_t payload, FakeStream& st, const KvGeom* kv, bool idle,
+                     bool launch = true) {
+    Engine* e = eng_[x->dir].get();
+    std::unique_lock<std::mutex> g(submit_mu_);
+    CHECK(e->acquire(x.get(), payload, kv != nullptr, 60000), "record");
+    KernelArgs a;
+    const uint64_t wd = 20000ull * 1000000ull;
+    const uint32_t grid = x->light >= 0 ? e->prepare(x.get(), ++seq_, payload, kv, wd, a)
+                                        : e->prepare_device(x.get(), ++seq_, payload, kv, wd, idle, a);
+    if (!grid) {  // too many micro-tasks for a ring: the engine thread takes it
+      e->release_unused(x.get());
+      x->rec = nullptr;
+      x->light = -1;
+      g.unlock();
+      submit(std::move(x), payload, st, kv);
+      return;
+    }
+    if (!launch) {
+      if (x->light >= 0)
+        e->release_unused(x.get());
+      else
+        e->abandon_device(x.get(), 60000);
+      return;
+    }
+    const uint32_t waves = grid * kWavesPerWG;
+    const double rate = s_.wave_rate;
+    st.launch([a, waves, rate] {
+      std::vector<std::thread> ts;
+      for (uint32_t w = 0; w < waves; ++w) ts.emplace_back(wave, a, w, rate);
+      for (auto& t : ts) t.join();
+    });
+    e->add_device(std::move(x));
   }
   bool sync() { return eng_[0]->wait_idle(60000) && eng_[1]->wait_idle(60000); }
   const Config& cfg() const { return cfg_; }
@@ -779,6 +840,193 @@ void two_streams_both_directions() {
   std::printf("ok   six transfers on two streams, both directions\n");
 }
 
+// ------------------------------------------------------------ device control
+Setup device_setup() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.device = 1;
+  s.cfg.device_cu_percent = 60;
+  return s;
+}
+
+// Linear copies under device control, both directions: exact, every micro-task
+// retired once; on an idle stream the copy engines carry their fixed share, on
+// a stream with work pending none; the engine thread never runs.
+void device_copies(bool idle) {
+  Setup s = device_setup();
+  Harness h(s);
+  FakeStream st;
+  for (int dir = 0; dir < 2; ++dir) {
+    for (uint64_t n : {1ull, 777ull, 64ull * 1024, 300ull * 1024 + 5, 3ull * 1024 * 1024 + 123}) {
+      auto src = random_bytes(n, static_cast<uint32_t>(n + 7 * dir));
+      std::vector<uint8_t> dst(n + 64, 0xA5);
+      auto x = linear(dir, dst.data() + 32, src.data(), n, h.cfg());
+      const size_t tasks = x->tasks.size();
+      const uint64_t before = sum_tasks(h.stats(), 0, MMA_NUM_PATHS);
+      const uint64_t cmds = h.stats().sdma_commands.load();
+      h.submit_device(std::move(x), n, st, nullptr, idle);
+      st.synchronize();
+      CHECK(h.sync(), "sync");
+      CHECK(std::memcmp(dst.data() + 32, src.data(), n) == 0, "device dir=%d n=%llu idle=%d: bytes differ", dir,
+            (unsigned long long)n, idle);
+      CHECK(dst[31] == 0xA5 && dst[32 + n] == 0xA5, "device: bytes outside the destination changed");
+      CHECK(sum_tasks(h.stats(), 0, MMA_NUM_PATHS) - before == tasks, "device: tasks retired");
+      const uint64_t issued = h.stats().sdma_commands.load() - cmds;
+      if (!idle) CHECK(issued == 0, "device: copy engines took part on a busy stream");
+      if (idle && tasks >= 4) CHECK(issued >= 2, "device: the copy engines took no share (%llu commands)",
+                                    (unsigned long long)issued);
+    }
+  }
+  CHECK(h.stats().failed.load() == 0, "device: failed transfers");
+  CHECK(h.stats().busy_ns.load() == 0, "device: the engine thread worked on a transfer");
+  std::printf("ok   device control, %s stream: copies exact, cu tasks %llu, engine tasks %llu, no engine-thread work\n",
+              idle ? "idle" : "busy", (unsigned long long)h.stats().path_tasks[MMA_NUM_PATHS - 1].load(),
+              (unsigned long long)sum_tasks(h.stats(), 0, 16));
+}
+
+// Paged-KV fetch then offload under device control: the CU path alone.
+void device_kv_roundtrip() {
+  Setup s = device_setup();
+  s.cfg.chunk = 8 * 1024;
+  Harness h(s);
+  FakeStream st;
+  const uint32_t L = 3, ppb = 2 * L, slots = 24, nb = 30;
+  const uint64_t piece = 2048, slot_bytes = piece * ppb;
+  std::vector<uint8_t> pool = random_bytes(slots * slot_bytes, 41);
+  std::vector<std::vector<uint8_t>> layers(L, std::vector<uint8_t>(2 * nb * piece, 0xA5));
+  KvGeom kv;
+  kv.piece = piece;
+  kv.kstride = piece * nb;
+  kv.layers = L;
+  for (uint32_t l = 0; l < L; ++l) kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l].data());
+  std::vector<int32_t> hs = {5, 0, 17, 3, 22, 9, 11}, gb = {2, 29, 7, 0, 13, 21, 4};
+  const uint64_t host = reinterpret_cast<uint64_t>(pool.data());
+  h.submit_device(make_kv_transfer(MMA_H2D, piece, ppb, host, host, false, true, hs.data(), gb.data(), hs.size(),
+                                   h.cfg()),
+                  hs.size() * slot_bytes, st, &kv, true);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  bool ok = true;
+  for (size_t i = 0; i < hs.size(); ++i)
+    for (uint32_t l = 0; l < L; ++l)
+      for (uint32_t k = 0; k < 2; ++k)
+        ok &= std::memcmp(layers[l].data() + (k * nb + gb[i]) * piece,
+                          pool.data() + hs[i] * slot_bytes + (2 * l + k) * piece, piece) == 0;
+  CHECK(ok, "device KV fetch: pieces differ");
+  std::vector<int32_t> dest = {23, 2, 4, 6, 8, 10, 12};
+  auto want = pool;
+  for (size_t j = 0; j < gb.size(); ++j)
+    for (uint32_t l = 0; l < L; ++l)
+      for (uint32_t k = 0; k < 2; ++k)
+        std::memcpy(want.data() + dest[j] * slot_bytes + (2 * l + k) * piece,
+                    layers[l].data() + (k * nb + gb[j]) * piece, piece);
+  h.submit_device(make_kv_transfer(MMA_D2H, piece, ppb, host, host, false, true, dest.data(), gb.data(), gb.size(),
+                                   h.cfg()),
+                  gb.size() * slot_bytes, st, &kv, true);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(pool == want, "device KV offload: pool differs");
+  CHECK(h.stats().sdma_commands.load() == 0, "device KV: a copy engine took part");
+  CHECK(h.stats().failed.load() == 0 && h.stats().busy_ns.load() == 0, "device KV: failed or engine-thread work");
+  std::printf("ok   device control: paged-KV fetch and offload exact on the CU path alone\n");
+}
+
+// More transfers than records, back to back on one stream: each submission
+// recycles the records of retired transfers itself. Copy-engine commands that
+// the runtime refuses go to the CU path. A transfer with more micro-tasks than
+// a ring holds falls back to the engine thread.
+void device_recycling_and_refusals() {
+  Setup s = device_setup();
+  Harness h(s);
+  FakeStream st;
+  const uint64_t n = 1024 * 1024 + 48;
+  const int count = 3 * static_cast<int>(kRecords);
+  auto src = random_bytes(n * count, 12);
+  std::vector<uint8_t> dst(n * count, 0);
+  for (int i = 0; i < count; ++i)
+    h.submit_device(linear(i % 2, i % 2 ? src.data() + i * n : dst.data() + i * n,
+                           i % 2 ? dst.data() + i * n : src.data() + i * n, n, h.cfg()),
+                    n, st, nullptr, i % 3 != 0);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  for (int i = 0; i < count; ++i)
+    CHECK(std::memcmp(dst.data() + i * n, src.data() + i * n, n) == 0, "device recycled transfer %d differs", i);
+  CHECK(h.stats().transfers.load() == static_cast<uint64_t>(count), "device: %llu transfers retired",
+        (unsigned long long)h.stats().transfers.load());
+  // refused commands
+  const uint64_t m = 6 * 1024 * 1024 + 9;
+  auto src2 = random_bytes(m, 13);
+  std::vector<uint8_t> dst2(m, 0);
+  g_fault_submit_fail = 1;
+  h.submit_device(linear(MMA_H2D, dst2.data(), src2.data(), m, h.cfg()), m, st, nullptr, true);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  g_fault_submit_fail = 0;
+  CHECK(dst2 == src2, "device: refused command, bytes differ");
+  CHECK(h.stats().submit_failures.load() == 1, "device: refused command not counted");
+  CHECK(h.stats().failed.load() == 0 && g_sticky.load() == 0, "device: a refused command failed the transfer");
+  CHECK(h.stats().busy_ns.load() == 0, "device: the engine thread worked on a transfer");
+  // more micro-tasks than ring entries
+  Setup s2 = device_setup();
+  s2.cfg.chunk = 4 * 1024;
+  s2.cfg.fallback = 8 * 1024;
+  Harness h2(s2);
+  const uint64_t big = (kRingSize + 3) * 4 * 1024ull + 5;
+  auto src3 = random_bytes(big, 14);
+  std::vector<uint8_t> dst3(big, 0);
+  h2.submit_device(linear(MMA_H2D, dst3.data(), src3.data(), big, h2.cfg()), big, st, nullptr, true);
+  st.synchronize();
+  CHECK(h2.sync(), "sync");
+  CHECK(dst3 == src3, "device fallback: bytes differ");
+  CHECK(h2.stats().busy_ns.load() > 0, "device fallback: the engine thread did not take the transfer");
+  std::printf("ok   device control: %d transfers recycle %u records, refused commands re-routed, "
+              "a transfer beyond the ring falls back to the engine thread\n", count, kRecords);
+}
+
+// Device control with a launch that fails after the copy engines took their
+// share: the call waits for them, frees the record, leaves no sticky error.
+// Whole transfers in light slots are retired by later calls too.
+void device_unlaunched_and_whole() {
+  Setup s = device_setup();
+  s.cfg.whole[0] = s.cfg.whole[1] = 1024 * 1024;
+  Harness h(s);
+  FakeStream st;
+  const uint64_t n = 8 * 1024 * 1024;
+  auto src = random_bytes(n, 15);
+  std::vector<uint8_t> dst(n, 0);
+  g_sticky.store(0);
+  h.submit_device(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st, nullptr, true, false);
+  CHECK(h.sync(), "sync after an unlaunched device transfer");
+  CHECK(g_sticky.load() == 0 && h.stats().transfers.load() == 0, "unlaunched device transfer counted or sticky");
+  h.submit_device(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st, nullptr, true);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst == src, "device: transfer after an unlaunched one differs");
+  // whole transfers behind a held stream
+  std::promise<void> gate;
+  std::shared_future<void> open = gate.get_future().share();
+  st.launch([open] { open.wait(); });
+  const int k = 300;
+  const uint64_t sz = 20000;
+  auto src2 = random_bytes(sz * k, 16);
+  std::vector<uint8_t> dst2(sz * k, 0);
+  auto submitted = std::async(std::launch::async, [&] {
+    for (int i = 0; i < k; ++i)
+      h.submit_device(linear(MMA_H2D, dst2.data() + i * sz, src2.data() + i * sz, sz, h.cfg()), sz, st, nullptr,
+                      false);
+  });
+  CHECK(submitted.wait_for(std::chrono::seconds(20)) == std::future_status::ready,
+        "device: whole transfers waited for the stream");
+  gate.set_value();
+  submitted.wait();
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst2 == src2, "device whole transfers differ");
+  CHECK(h.stats().failed.load() == 0 && h.stats().busy_ns.load() == 0, "device whole: failed or engine-thread work");
+  std::printf("ok   device control: a failed launch drains the copy engines; %d whole transfers retired by later calls\n",
+              k);
+}
+
 // Pull-based selection against fixed splits decided at plan time, on two
 // paths (the CU path and one copy engine) with a given rate ratio.
 double timed_copy(double cu_rate, double eng_rate, uint32_t static_cu_percent, bool pull) {
@@ -853,6 +1101,11 @@ int main(int argc, char** argv) {
     submit_failures_rerouted();
     kv_submit_failures_rerouted();
     two_streams_both_directions();
+    device_copies(true);
+    device_copies(false);
+    device_kv_roundtrip();
+    device_recycling_and_refusals();
+    device_unlaunched_and_whole();
   }
   if (timing) {
     slow_engine_gets_fewer_tasks();

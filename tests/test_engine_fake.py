@@ -7,7 +7,11 @@ byte-exact copies, tensor lists and paged-KV fetch/offload through staging, that
 micro-task is retired once, merged copy-engine commands, re-routed submit failures, two
 streams in flight, that a slower engine pulls fewer micro-tasks, and that pull-based
 selection tracks the best fixed split (the paper's static-split comparison, Section 5.1.2).
-It is built optimised, and with ThreadSanitizer for the correctness scenarios.
+Under device control (no engine thread in the loop) it checks exact copies on idle streams
+(copy engines and CU path) and busy ones (CU path only), KV fetch and offload, records
+recycled by later submissions, refused commands re-routed, a transfer larger than a ring
+handed to the engine thread, a failed launch draining the copy engines, and queued whole
+transfers. It is built optimised, and with ThreadSanitizer for the correctness scenarios.
 """
 import os
 import shutil
