@@ -47,7 +47,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true", help="skip native comparators and the 64 MiB copy")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle timing window")
-    p.add_argument("--sweep", choices=["sizes", "idle", "chunks", "contention", "duplex", "paths", "footprint"],
+    p.add_argument("--control", choices=["host", "device"], default=None,
+                   help="who drives transfers after submission (default: the library's, MMA_CONTROL)")
+    p.add_argument("--sweep", choices=["sizes", "idle", "chunks", "contention", "duplex", "paths", "footprint",
+                                       "control"],
                    help="instead of the benchmark, print one JSON line per point of a parameter sweep")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
@@ -358,7 +361,33 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
                                                   arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
     del wdst
     arena.free()
+
+    extras["device_control"] = device_control_leg(mma, torch, pool, layers, lay, hs, gb, stream, total)
     return extras
+
+
+def device_control_leg(mma, torch, pool, layers, lay, hs, gb, stream, total):
+    """The 64k-token fetch again under device control (the calling thread plans the transfer, the
+    dummy-task kernel alone tracks it; the stream has the start event pending, so the CU path
+    carries it), with the engine threads' CPU time per step; then the default session again."""
+    mma.mma_synchronize()
+    mma.mma_finalize()
+    cfg = mma.mma_config_default()
+    cfg.control = mma.MMA_CONTROL_DEVICE
+    mma.mma_init(0, cfg)
+    try:
+        t = _timed(stream, lambda: mma.mma_kv_fetch(lay, pool, layers, hs, gb, stream), reps=5, warm=1)
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+        res = {"kv_fetch_ms": round(t["p50"], 3), "kv_fetch_ms_p10_p90": [round(t["p10"], 3), round(t["p90"], 3)],
+               "kv_fetch_GBs": round(total / t["p50"] / 1e6, 2),
+               "engine_cpu_ms_per_step": round(st["engine_cpu_ns"] / 1e6 / 6, 3),
+               "failed_transfers": st["failed_transfers"]}
+    finally:
+        mma.mma_finalize()
+        mma.mma_init(0)
+    log("device control:", res)
+    return res
 
 
 def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan, arena, offs, sizes, wdst,
@@ -513,6 +542,105 @@ def sweep_idle():
         _emit(sweep="idle", **row)
     h.free()
     mma.mma_finalize()
+
+
+def _busy_timed(torch, st, fn, reps, warm):
+    """HIP-event time of fn() queued behind about a millisecond of other work on `st`: the
+    stream has work pending when fn is called. Median and the list, in ms."""
+    ts = []
+    for i in range(reps + warm):
+        with torch.cuda.stream(st):
+            torch.cuda._sleep(2_000_000)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        fn()
+        e1.record(st)
+        e1.synchronize()
+        if i >= warm:
+            ts.append(e0.elapsed_time(e1))
+    ts.sort()
+    return ts[len(ts) // 2]
+
+
+def sweep_control():
+    """Host control (the direction's engine thread pulls micro-tasks for every path) against
+    device control (the calling thread plans the whole transfer, the dummy-task kernel alone
+    tracks completion), on the same copies, both directions. Per mode:
+      idle_us   host wall time from the call to the return of hipStreamSynchronize on a stream
+                with nothing pending (both modes use the copy engines), median;
+      api_us    time spent inside the call itself on that idle stream, median;
+      busy_GBs  HIP-event rate of the copy queued behind other work on its stream (device
+                control: the CU path alone);
+      engine_cpu_us_per_transfer  CPU time of the engine threads over both legs / transfers.
+    Then device control's CU-path share (static_cu_percent) on 1 GiB idle-stream copies."""
+    import ctypes
+    import numpy as np
+    mma, torch, nat, st = _sweep_env()
+    top = 1 << 30
+    sp = ctypes.c_void_p(st.cuda_stream)
+    sizes = [64 << 10, 1 << 20, 4 << 20, 16 << 20, 64 << 20, 256 << 20, 1 << 30]
+
+    def idle_leg(margs, reps, warm):
+        tw, ta = [], []
+        for i in range(reps + warm):
+            st.synchronize()
+            t0 = time.perf_counter()
+            _ok(mma.lib.mma_memcpy_async(*margs))
+            t1 = time.perf_counter()
+            st.synchronize()
+            t2 = time.perf_counter()
+            if i >= warm:
+                tw.append((t2 - t0) * 1e6)
+                ta.append((t1 - t0) * 1e6)
+        return float(np.median(tw)), float(np.median(ta))
+
+    rows = {}
+    for mode, name in ((mma.MMA_CONTROL_HOST, "host"), (mma.MMA_CONTROL_DEVICE, "device")):
+        cfg = mma.mma_config_default()
+        cfg.control = mode
+        mma.mma_init(0, cfg)
+        h = mma.PinnedBuffer(top)
+        h.array[::4096] = 1
+        d = torch.empty(top, dtype=torch.uint8, device="cuda")
+        for n in sizes:
+            reps = 30 if n <= (64 << 20) else 8
+            for dr, dname in ((0, "h2d"), (1, "d2h")):
+                dst, src = (d.data_ptr(), h.ptr) if dr == 0 else (h.ptr, d.data_ptr())
+                margs = (ctypes.c_void_p(dst), ctypes.c_void_p(src), ctypes.c_uint64(n), dr, sp)
+                mma.mma_synchronize()
+                cpu0 = mma.mma_get_stats()["engine_cpu_ns"]
+                idle_us, api_us = idle_leg(margs, reps, 3)
+                busy_ms = _busy_timed(torch, st, lambda: _ok(mma.lib.mma_memcpy_async(*margs)), reps, 2)
+                mma.mma_synchronize()
+                cpu1 = mma.mma_get_stats()["engine_cpu_ns"]
+                rows.setdefault((n, dname), {})[name] = {
+                    "idle_us": round(idle_us, 1), "idle_GBs": round(n / idle_us / 1e3, 2),
+                    "api_us": round(api_us, 2), "busy_GBs": round(n / busy_ms / 1e6, 2),
+                    "engine_cpu_us_per_transfer": round((cpu1 - cpu0) / 1e3 / (2 * reps + 5), 1)}
+        h.free()
+        del d
+        mma.mma_finalize()
+    for (n, dname), r in rows.items():
+        _emit(sweep="control", bytes=n, dir=dname, **r)
+
+    for pct in (40, 50, 60, 70, 80, 100):
+        cfg = mma.mma_config_default()
+        cfg.control = mma.MMA_CONTROL_DEVICE
+        cfg.static_cu_percent = pct
+        mma.mma_init(0, cfg)
+        h = mma.PinnedBuffer(top)
+        h.array[::4096] = 1
+        d = torch.empty(top, dtype=torch.uint8, device="cuda")
+        row = {"cu_percent": pct}
+        for dr, dname in ((0, "h2d"), (1, "d2h")):
+            dst, src = (d.data_ptr(), h.ptr) if dr == 0 else (h.ptr, d.data_ptr())
+            margs = (ctypes.c_void_p(dst), ctypes.c_void_p(src), ctypes.c_uint64(top), dr, sp)
+            idle_us, _ = idle_leg(margs, 8, 2)
+            row[dname + "_GBs"] = round(top / idle_us / 1e3, 2)
+        h.free()
+        del d
+        mma.mma_finalize()
+        _emit(sweep="control_cu_share", **row)
 
 
 def sweep_chunks():
@@ -841,11 +969,13 @@ def sweep_footprint():
     h.free()
 
 SWEEPS = {"sizes": sweep_sizes, "idle": sweep_idle, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
-          "paths": sweep_paths, "footprint": sweep_footprint}
+          "paths": sweep_paths, "footprint": sweep_footprint, "control": sweep_control}
 
 
 def main():
     args = parse()
+    if args.control:
+        os.environ["MMA_CONTROL"] = "1" if args.control == "device" else "0"
     if args.calib:
         calibration_kernels()
         return
@@ -962,6 +1092,7 @@ def main():
             "chunk_bytes": cfg["chunk_bytes"],
             "paths_h2d": hex(cfg["path_mask_h2d"]),
             "cu_workgroups": cfg["cu_workgroups"],
+            "control": "device" if cfg["control"] == mma.MMA_CONTROL_DEVICE else "host",
             "parallelism": "1 GPU (SDMA engines + CU zero-copy on its own PCIe link)",
         },
         "kv_fetch_latency_ms": round(avg_kernel_ms, 3),

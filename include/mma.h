@@ -99,7 +99,7 @@ typedef struct mma_config {
                                time: static_cu_percent of the micro-tasks (interleaved) go to the
                                CU path, the rest to the SDMA engines (which share them by pulling) */
   uint32_t static_cu_percent; /* also, under MMA_CONTROL_DEVICE, the CU path's share of a linear
-                               transfer's bytes when the copy engines take part (0: 60) */
+                               transfer's bytes when the copy engines take part (0: 40) */
   uint32_t sdma_merge_tasks; /* at most this many micro-tasks that follow each other in both
                                address spaces (a linear run, or one KV block's consecutive pieces)
                                go to an SDMA engine as one command, and never more than the
