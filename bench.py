@@ -1101,6 +1101,14 @@ def main():
         "path_bytes": {"cu": stats["path_bytes"][16],
                        **{f"sdma{e}": stats["path_bytes"][e] for e in range(16) if stats["path_bytes"][e]}},
         "engine_cpu_ms_per_step": round(stats["engine_cpu_ns"] / 1e6 / max(1, args.steps + args.warmup), 3),
+        # SDMA share of the fetch: host slot -> HBM staging (copy engine), then the CU scatter
+        # staging -> paged blocks reads and writes each byte once more in HBM.
+        "staging_scatter": {
+            "bytes_per_step": stats["staging_bytes"] // args.steps,
+            "hbm_bytes_per_step": 2 * stats["staging_bytes"] // args.steps,
+            "hbm_GBs_avg_over_step": round(2 * stats["staging_bytes"] / args.steps / (ms_per_step * 1e-3) / 1e9, 2),
+            "frac_of_8TBs": round(2 * stats["staging_bytes"] / args.steps / (ms_per_step * 1e-3) / 8e12, 5),
+        },
         "roofline": {
             "kernel": f"{kernel_name} (dummy task: CU gather + stream wait)",
             "bound": "pcie",
