@@ -88,8 +88,8 @@ typedef struct mma_config {
                                SDMA engines reported by ROCr */
   uint32_t path_mask_d2h;   /* paths used device->host; same default */
   uint32_t cu_workgroups;   /* max workgroups (4 wave64 each) of the dummy-task kernel; default 16,
-                               at most 256 (x-packed KV transfers use up to twice this: their
-                               waves spend half their time writing out an LDS tile);
+                               at most 256 (x-packed KV transfers use up to 1.5 times this:
+                               their waves spend part of their time writing out an LDS tile);
                                chunk_bytes / cu_sub_bytes must not exceed 2048 */
   uint32_t cu_sub_bytes;    /* bytes one wave moves per CU claim; default 64 KiB */
   uint32_t watchdog_ms;     /* wait-kernel gives up after this long without engine progress;

@@ -479,8 +479,7 @@ class Engine {
   // every poll is a PCIe read that competes with the payload).
   // x-packed KV pieces: a wave alternates between reading a head group into its
   // LDS tile and writing it out, with no reads in flight during the second
-  // phase, so twice the waves keep the same bytes in flight (measured on the
-  // 64k-token fetch: 54.6 GB/s at 16 workgroups, 57.0 at 32).
+  // phase, so more waves are needed for the same bytes in flight.
   uint32_t grid_for(uint64_t bytes, uint64_t sub, bool needs_cu, bool staged, bool pool_dev, bool xpacked) const {
     if (!needs_cu) return 1;
     if (pool_dev) {  // HBM gather/scatter: as many waves as there are micro-tasks, up to the limit
@@ -492,9 +491,19 @@ class Engine {
     uint64_t inflight = cu_enabled() ? cfg_.cu_depth * per_task : 0;
     if (staged) inflight += static_cast<uint64_t>(__builtin_popcount(sdma_mask())) * cfg_.depth * per_task;
     uint64_t g = (std::max<uint64_t>(1, std::min(total, inflight)) + kWavesPerWG - 1) / kWavesPerWG;
-    const uint64_t cap = std::min<uint64_t>(xpacked ? 2ull * cfg_.cu_wgs : cfg_.cu_wgs, kMaxWorkgroups);
-    g = std::max<uint64_t>(1, std::min<uint64_t>(g, cap));
+    g = std::max<uint64_t>(1, std::min<uint64_t>(g, wg_cap(xpacked)));
     return static_cast<uint32_t>(g);
+  }
+
+  // Workgroup limit of one launch. x-packed launches get 1.5x cu_workgroups:
+  // on the 64k-token workload (fetch / offload GB/s at the default 16) 16
+  // workgroups gave 54.6 / 49.1, 20 gave 57.27 / 56.93, 24 gave 57.33 / 56.85,
+  // 28 gave 57.14 / 56.82, 32 gave 56.97 / 56.42, 40 and 48 gave 56.4 and 55.8
+  // on the fetch: past about 24, the waves' polls and LDS phases cost more
+  // than their extra reads in flight gain.
+  uint64_t wg_cap(bool xpacked) const {
+    const uint64_t w = xpacked ? (3ull * cfg_.cu_wgs + 1) / 2 : cfg_.cu_wgs;
+    return std::min<uint64_t>(w, kMaxWorkgroups);
   }
 
   // Everything between the plan and the kernel launch, for a transfer that
@@ -749,8 +758,7 @@ class Engine {
     if (x->pool_dev) {
       grid = grid_for(payload_bytes, x->sub, true, false, true, false);
     } else {
-      const uint64_t cap = std::min<uint64_t>(
-          kv && kv->layout == kKvLayoutXPacked ? 2ull * cfg_.cu_wgs : cfg_.cu_wgs, kMaxWorkgroups);
+      const uint64_t cap = wg_cap(kv && kv->layout == kKvLayoutXPacked);
       grid = static_cast<uint32_t>(
           std::max<uint64_t>(1, std::min<uint64_t>((x->pushed + kWavesPerWG - 1) / kWavesPerWG, cap)));
     }

@@ -144,3 +144,33 @@ def test_watchdog_releases_stream_and_error_is_sticky():
         assert bool((dst == 3).all())
         mma.mma_synchronize()
         src.free()
+
+
+@pytest.mark.parametrize("refused", [1, 2, 1000000])
+def test_device_control_refused_commands_go_to_cu(refused):
+    """Device control on an idle stream: copy-engine commands refused at submission move their
+    micro-tasks to the CU path before the launch; the copy is exact and nothing fails."""
+    n = (48 << 20) + 5
+    src_np = np.ascontiguousarray(W.uniform_bytes(12, 1, n, n))
+    stream = torch.cuda.Stream()
+    with session("both", control=mma.MMA_CONTROL_DEVICE):
+        src = mma.PinnedBuffer(n)
+        src.array[:] = src_np
+        dst = torch.full((n,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        mma.mma_reset_stats()
+        mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, refused)
+        try:
+            mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, stream)
+            stream.synchronize()
+        finally:
+            mma.mma_test_set_fault(mma.MMA_FAULT_SDMA_SUBMIT_FAIL, 0)
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+        assert np.array_equal(to_host(dst), src_np)
+        src.free()
+    log(f"  refused={st['sdma_submit_failures']} commands={st['sdma_commands']} cu bytes={st['path_bytes'][16]}")
+    assert st["failed_transfers"] == 0
+    assert 1 <= st["sdma_submit_failures"] <= refused
+    if refused > 2:  # every command refused: the CU path carried everything
+        assert st["path_bytes"][16] == n
