@@ -308,6 +308,9 @@ mma_status_t mma_digest_u32(const void* dev_ptr, uint64_t bytes, uint64_t* dev_o
 
 /* ------------------------------------------------------------------- status */
 
+/* Counters since mma_init or mma_reset_stats. They cover every transfer retired so far;
+ * this call first retires the transfers whose kernel has finished and that no engine
+ * thread watches (whole transfers, and every transfer under MMA_CONTROL_DEVICE). */
 mma_status_t mma_get_stats(mma_stats_t* out);
 mma_status_t mma_reset_stats(void);
 const char* mma_status_str(mma_status_t s);

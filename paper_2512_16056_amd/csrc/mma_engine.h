@@ -143,7 +143,7 @@ struct Transfer {
   std::atomic<bool> unlaunched{false};
   uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
   uint64_t kv_per = 0;         // pieces per CU ring entry of a KV transfer (0: the engine thread's rule)
-  // Device control: planned in full at submission, retired by reap_device.
+  // Device control: planned in full at submission, retired by reap.
   bool device = false;
   uint32_t dev_cmds = 0;           // copy-engine commands counted by the record's device signal
   std::vector<uint8_t> dev_path;   // path (stats index) that carries each micro-task
@@ -399,6 +399,8 @@ class Engine {
   }
   bool cu_enabled() const { return (cfg_.mask[dir_] & MMA_PATH_CU) != 0; }
   bool device_control() const { return cfg_.device != 0; }
+  // Transfers tracked by the submitting threads are in flight (see track).
+  bool tracked() const { return n_tracked_.load(std::memory_order_acquire) != 0; }
   bool has_sdma() const { return !paths_.empty(); }
   uint64_t stage_bytes() const { return stage_bytes_; }
 
@@ -415,7 +417,7 @@ class Engine {
   // queue of small transfers on a stream does not wait for the GPU.
   bool acquire(Transfer* x, uint64_t payload_bytes, bool kv, uint64_t timeout_ms) {
     const bool light = whole_eligible(x, payload_bytes, kv);
-    if (cfg_.device) reap_device();
+    reap();
     std::unique_lock<std::mutex> lk(mu_);
     std::deque<uint32_t>& pool = light ? free_light_ : free_recs_;
     if (pool.empty() && !wait_for_pool(lk, pool, timeout_ms)) return false;
@@ -438,22 +440,18 @@ class Engine {
     }
     return true;
   }
-  // Waits (lk held on entry and exit) until `pool` has a free entry. Under
-  // device control no thread signals a recycled record, so this thread reaps.
+  // Waits (lk held on entry and exit) until `pool` has a free entry. Slots of
+  // transfers that the submitting threads track themselves (track) come back
+  // only when one of them reaps, so this thread reaps while it waits.
   bool wait_for_pool(std::unique_lock<std::mutex>& lk, const std::deque<uint32_t>& pool, uint64_t timeout_ms) {
     const auto deadline = std::chrono::steady_clock::now() + std::chrono::milliseconds(timeout_ms);
     while (pool.empty()) {
-      const auto now = std::chrono::steady_clock::now();
-      if (now >= deadline) return false;
-      if (cfg_.device) {
-        lk.unlock();
-        reap_device();
-        lk.lock();
-        if (!pool.empty()) break;
-        cv_done_.wait_for(lk, std::chrono::microseconds(20));
-      } else {
-        cv_done_.wait_until(lk, deadline);
-      }
+      if (std::chrono::steady_clock::now() >= deadline) return false;
+      lk.unlock();
+      reap();
+      lk.lock();
+      if (!pool.empty()) break;
+      cv_done_.wait_for(lk, std::chrono::microseconds(20));
     }
     return true;
   }
@@ -632,7 +630,7 @@ class Engine {
   //     polled completion signal.
   // The kernel's last wave waits for that signal instead of the engine
   // thread's `complete` word, and the submitting thread recycles the record
-  // once the kernel has released it (reap_device). Against the engine thread
+  // once the kernel has released it (reap). Against the engine thread
   // this gives up pulling and back-off on the copy engines, whose share is
   // fixed at submission, and copy engines on a stream with work pending: a
   // command that waited for the stream would hold the head of the engine's
@@ -771,16 +769,18 @@ class Engine {
     return grid;
   }
 
-  // Device control: track a launched transfer (prepare_device, or a whole
-  // transfer in a light slot) until reap_device retires it.
-  void add_device(std::unique_ptr<Transfer> x) {
-    x->device = true;
+  // A launched transfer that needs no engine-thread work -- every transfer
+  // under device control, and a whole transfer in a light slot in either mode
+  // (the kernel is its only copy engine) -- is tracked by the submitting
+  // threads until reap retires it; the engine thread is not woken for it.
+  void track(std::unique_ptr<Transfer> x) {
     {
       std::lock_guard<std::mutex> g(mu_);
       ++inflight_;
     }
     std::lock_guard<std::mutex> g(dev_mu_);
-    dev_active_.push_back(std::move(x));
+    tracked_.push_back(std::move(x));
+    n_tracked_.fetch_add(1, std::memory_order_release);
   }
 
   // Device control: the dummy-task launch failed after the copy engines were
@@ -798,16 +798,17 @@ class Engine {
     release_unused(x);
   }
 
-  // Device control: retire tracked transfers whose kernel has finished with
-  // their record (and whose copy-engine commands have all landed, even after a
+  // Retires tracked transfers whose kernel has finished with their record or
+  // light slot (and whose copy-engine commands have all landed, even after a
   // watchdog). Any thread may call it. Only the oldest kReapWindow transfers
   // are looked at, so a deep queue costs each submission a bounded scan;
   // transfers on one stream finish in order, so the oldest go first.
-  void reap_device() {
+  void reap() {
+    if (!tracked()) return;
     std::lock_guard<std::mutex> g(dev_mu_);
-    for (size_t k = 0; k < dev_active_.size() && k < kReapWindow;) {
-      Transfer* x = dev_active_[k].get();
-      if (!device_done(x)) {
+    for (size_t k = 0; k < tracked_.size() && k < kReapWindow;) {
+      Transfer* x = tracked_[k].get();
+      if (!tracked_done(x)) {
         ++k;
         continue;
       }
@@ -824,7 +825,8 @@ class Engine {
       }
       x->n_done = x->tasks.size();
       finish(x, bad, true);
-      dev_active_.erase(dev_active_.begin() + static_cast<long>(k));
+      tracked_.erase(tracked_.begin() + static_cast<long>(k));
+      n_tracked_.fetch_sub(1, std::memory_order_release);
     }
   }
 
@@ -843,12 +845,11 @@ class Engine {
   bool wait_idle(uint64_t timeout_ms) {
     const auto deadline = std::chrono::steady_clock::now() + std::chrono::milliseconds(timeout_ms);
     for (;;) {
-      if (cfg_.device) reap_device();
+      reap();
       std::unique_lock<std::mutex> lk(mu_);
       if (inflight_ == 0) return true;
-      const auto now = std::chrono::steady_clock::now();
-      if (now >= deadline) return false;
-      if (cfg_.device)
+      if (std::chrono::steady_clock::now() >= deadline) return false;
+      if (tracked())
         cv_done_.wait_for(lk, std::chrono::microseconds(50));
       else
         cv_done_.wait_until(lk, deadline);
@@ -956,8 +957,8 @@ class Engine {
     x->dev_path[i] = static_cast<uint8_t>(MMA_NUM_PATHS - 1);
   }
 
-  // Device control: the kernel is done with the transfer's record or light slot.
-  bool device_done(const Transfer* x) const {
+  // A tracked transfer's kernel is done with its record or light slot.
+  bool tracked_done(const Transfer* x) const {
     if (x->light >= 0) {  // a whole transfer: every entry's done tag is in
       for (uint64_t t = 0; t < x->pushed; ++t)
         if (ld_acq(&x->done_host[t]) != make_tag(x->seq, t)) return false;
@@ -1547,11 +1548,13 @@ class Engine {
   std::vector<std::unique_ptr<Transfer>> active_;  // engine thread only
   std::deque<uint32_t> free_recs_, free_light_;
   // Device control: per record, the copy engines' polled completion signal and
-  // its device-visible value; transfers launched and not yet retired.
+  // its device-visible value. Transfers tracked by the submitting threads (see
+  // track) that are launched and not yet retired.
   std::vector<uint64_t> dev_sig_;
   std::vector<const int64_t*> dev_sig_val_;
   std::mutex dev_mu_;  // taken before mu_, never after it
-  std::deque<std::unique_ptr<Transfer>> dev_active_;
+  std::deque<std::unique_ptr<Transfer>> tracked_;
+  std::atomic<uint64_t> n_tracked_{0};
   uint64_t inflight_ = 0;
   bool stop_ = false;
   bool engine_waiting_ = false;  // the engine thread waits on cv_ (guarded by mu_)

@@ -396,7 +396,7 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
           e->abandon_device(x.get(), rt->cfg.watchdog_ms + 10000ull);
         return fail(MMA_ERR_HIP, "dummy-task kernel launch failed: %s", hipGetErrorString(err));
       }
-      e->add_device(std::move(x));
+      e->track(std::move(x));
       return MMA_OK;
     }
   }
@@ -423,7 +423,12 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
     e->release_unused(x.get());
     return fail(MMA_ERR_HIP, "dummy-task kernel launch failed: %s", hipGetErrorString(err));
   }
-  e->submit(std::move(x));
+  // A whole transfer needs nothing from the engine thread but retirement:
+  // submitting threads retire it later, and the engine thread is not woken.
+  if (x->light >= 0)
+    e->track(std::move(x));
+  else
+    e->submit(std::move(x));
   return MMA_OK;
 }
 
@@ -672,23 +677,19 @@ mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir)
     const hipError_t e = hipStreamSynchronize(nullptr);
     if (e != hipSuccess) return fail(MMA_ERR_HIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
   }
-  // The stream has passed the dummy task; the engine retires the transfer
-  // right after (under device control, this thread does), which is when its
-  // outcome is final.
+  // The stream has passed the dummy task; the engine thread retires the
+  // transfer right after (or this thread does, for a transfer the submitting
+  // threads track), which is when its outcome is final.
   Engine* e = g_rt->eng[dir].get();
   std::unique_lock<std::mutex> lk(w->mu);
   const auto deadline = std::chrono::steady_clock::now() +
                         std::chrono::milliseconds(static_cast<uint64_t>(g_rt->cfg.watchdog_ms) + 10000);
   while (!w->done) {
     if (std::chrono::steady_clock::now() >= deadline) return fail(MMA_ERR_TIMEOUT, "copy not retired");
-    if (e->device_control()) {
-      lk.unlock();
-      e->reap_device();
-      lk.lock();
-      if (!w->done) w->cv.wait_for(lk, std::chrono::microseconds(20));
-    } else {
-      w->cv.wait_until(lk, deadline);
-    }
+    lk.unlock();
+    e->reap();
+    lk.lock();
+    if (!w->done) w->cv.wait_for(lk, std::chrono::microseconds(20));
   }
   return w->failed ? fail(MMA_ERR_TRANSFER_FAILED, "the copy failed") : MMA_OK;
 }
@@ -834,6 +835,9 @@ mma_status_t mma_digest_u32(const void* dev_ptr, uint64_t bytes, uint64_t* dev_o
 mma_status_t mma_get_stats(mma_stats_t* out) {
   if (!out) return fail(MMA_ERR_INVALID_ARG, "NULL out");
   if (!g_rt) return fail(MMA_ERR_NOT_INITIALIZED, "not initialised");
+  // Transfers that the submitting threads track are retired when a thread
+  // reaps: do it here, so the figures cover every transfer whose kernel is done.
+  for (auto& e : g_rt->eng) e->reap();
   memset(out, 0, sizeof *out);
   Stats& st = g_rt->stats;
   out->transfers = st.transfers;
@@ -902,6 +906,8 @@ mma_status_t mma_trace_enable(int32_t on) {
 
 mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out) {
   if (!n_out || (cap && !out)) return fail(MMA_ERR_INVALID_ARG, "NULL argument");
+  if (g_rt)
+    for (auto& e : g_rt->eng) e->reap();  // records of tracked transfers are written when they retire
   std::lock_guard<std::mutex> g(g_trace_mu);
   const uint64_t n = std::min<uint64_t>(cap, g_trace_buf.size());
   for (uint64_t i = 0; i < n; ++i) out[i] = g_trace_buf[i];

@@ -179,8 +179,9 @@ def test_device_kv_roundtrip(shape, chunk):
 def test_device_stream_ordering(rep):
     """A 256 MiB host->device copy on an idle stream (the copy engines carry their share), then
     the digest kernel on the same stream: its digest equals the oracle's digest of the source,
-    so the stream waited for every path. Then the reverse: a kernel writes the source, the
-    device->host copy follows on the stream and must see the kernel's bytes."""
+    so the stream waited for every path. Then the reverse: a kernel writes the source and the
+    device->host copy follows on the stream, queued behind it or after it has finished (then the
+    copy engines take part); either way it must see the kernel's bytes."""
     n = 256 << 20
     src_np = np.ascontiguousarray(W.uniform_bytes(23, rep, 0, n))
     stream = torch.cuda.Stream()
@@ -198,16 +199,24 @@ def test_device_stream_ordering(rep):
         assert got == odigest.digest(src_np)
         mid = mma.mma_get_stats()
         log(f"  h2d copy-engine bytes {sum(mid['path_bytes'][:16]) - sum(before['path_bytes'][:16])}")
-        # device -> host after a kernel that wrote the source on the same stream
+        # device -> host after a kernel that wrote the source on the same stream: queued right
+        # behind it (CU path), and after it has finished (idle stream: the copy engines read
+        # what the kernel wrote)
         host = mma.PinnedBuffer(n)
-        host.array[:] = W.WEIGHT_POISON
-        torch.cuda.synchronize()
-        with torch.cuda.stream(stream):
-            dst.fill_(0x3C)
-        mma.mma_memcpy_async(host, dst, n, mma.MMA_D2H, stream)
-        stream.synchronize()
-        assert np.all(host.array == 0x3C)
-        mma.mma_synchronize()
+        for idle, val in ((False, 0x3C), (True, 0xC3)):
+            host.array[:] = W.WEIGHT_POISON
+            torch.cuda.synchronize()
+            with torch.cuda.stream(stream):
+                dst.fill_(val)
+            if idle:
+                stream.synchronize()
+            b0 = mma.mma_get_stats()
+            mma.mma_memcpy_async(host, dst, n, mma.MMA_D2H, stream)
+            stream.synchronize()
+            mma.mma_synchronize()
+            b1 = mma.mma_get_stats()
+            assert np.all(host.array == val), idle
+            log(f"  d2h idle={idle} copy-engine bytes {sum(b1['path_bytes'][:16]) - sum(b0['path_bytes'][:16])}")
         assert mma.mma_get_stats()["failed_transfers"] == 0
 
 
