@@ -19,9 +19,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 LIB = os.path.join(ROOT, "paper_2512_16056_amd", "libmma_interpose.so")
 
 
-def test_torch_copies_through_interposer():
+@pytest.mark.parametrize("control", ["0", "1"])
+def test_torch_copies_through_interposer(control):
     assert os.path.exists(LIB), "build with python paper_2512_16056_amd/build.py"
     env = dict(os.environ)
+    env["MMA_CONTROL"] = control  # the interposer initialises the library from the environment
     # keep whatever is preloaded already; add the interposer after it
     env["LD_PRELOAD"] = (env.get("LD_PRELOAD", "") + " " + LIB).strip()
     env["MMA_WATCHDOG_MS"] = "5000"

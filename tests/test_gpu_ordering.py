@@ -96,10 +96,11 @@ def test_producer_then_d2h(paths):
         mma.mma_synchronize()
 
 
-def test_two_streams_concurrent():
+@pytest.mark.parametrize("control", [mma.MMA_CONTROL_HOST, mma.MMA_CONTROL_DEVICE])
+def test_two_streams_concurrent(control):
     """An H2D stream and a D2H stream with dependent work on each, interleaved."""
     n = 32 << 20
-    with session("both", chunk_bytes=256 << 10):
+    with session("both", chunk_bytes=256 << 10, control=control):
         sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
         src = mma.PinnedBuffer(n)
         src.array[:] = W.uniform_bytes(11, 0, 0, n)
@@ -151,7 +152,8 @@ def test_kv_fetch_then_dependent_kernel():
         mma.mma_synchronize()
 
 
-def test_concurrent_submitters():
+@pytest.mark.parametrize("control", [mma.MMA_CONTROL_HOST, mma.MMA_CONTROL_DEVICE])
+def test_concurrent_submitters(control):
     """Four host threads, each with its own stream, submit interleaved H2D copies, D2H copies and
     tensor lists of mixed sizes (self-contained, CU+SDMA and SDMA-merged ones) at the same time;
     each transfer is followed on its stream by the dependent digest kernel. Every destination and
@@ -159,7 +161,7 @@ def test_concurrent_submitters():
     are independent)."""
     from concurrent.futures import ThreadPoolExecutor
     sizes = [12345, 1 << 20, (3 << 20) + 17, 9 << 20, 64 << 10]
-    with session("both", chunk_bytes=1 << 20):
+    with session("both", chunk_bytes=1 << 20, control=control):
         def worker(tid):
             stream = torch.cuda.Stream()
             with torch.cuda.stream(stream):  # torch's own allocations and fills go on this stream too

@@ -55,11 +55,12 @@ def _size(r):
     return int(np.exp(r.uniform(0, np.log(12 << 20))))
 
 
+@pytest.mark.parametrize("control", [mma.MMA_CONTROL_HOST, mma.MMA_CONTROL_DEVICE])
 @pytest.mark.parametrize("seed", [1, 2])
-def test_random_mixed_schedule(seed):
+def test_random_mixed_schedule(seed, control):
     r = np.random.default_rng(seed)
     HOST, DEV = 256 << 20, 256 << 20
-    with session("both", cu_whole_bytes=0, cu_whole_bytes_d2h=0, chunk_bytes=1 << 20):
+    with session("both", cu_whole_bytes=0, cu_whole_bytes_d2h=0, chunk_bytes=1 << 20, control=control):
         src_h = mma.PinnedBuffer(32 << 20)                   # read-only host source
         src_h.array[:] = r.integers(0, 256, src_h.nbytes, dtype=np.uint8)
         src_d_np = r.integers(0, 256, 32 << 20, dtype=np.uint8)
