@@ -143,8 +143,7 @@ struct Transfer {
   std::atomic<bool> unlaunched{false};
   uint64_t sub = 0;            // bytes per CU ring entry of a linear transfer
   uint64_t kv_per = 0;         // pieces per CU ring entry of a KV transfer (0: the engine thread's rule)
-  // Device control: planned in full at submission, retired by reap.
-  bool device = false;
+  // Device control: planned in full at submission (prepare_device), retired by reap.
   uint32_t dev_cmds = 0;           // copy-engine commands counted by the record's device signal
   std::vector<uint8_t> dev_path;   // path (stats index) that carries each micro-task
   std::shared_ptr<Waiter> waiter;  // set for synchronous calls
@@ -676,7 +675,7 @@ class Engine {
     x->seq = seq;
     x->t_submit = x->t_started = now_ns();
     x->bytes = payload_bytes;
-    x->device = x->started = x->closed = true;
+    x->started = x->closed = true;
     Record* r = x->rec;
     r->h.seq = seq;
     r->h.status = 0;
