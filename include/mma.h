@@ -378,10 +378,16 @@ mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out)
  *     micro-tasks are re-routed to another path.
  *   MMA_FAULT_ENGINE_IGNORE: while value != 0, engine threads do not serve newly
  *     started transfers, so the wait kernel's watchdog must release the stream.
+ *   MMA_FAULT_DEVICE_SIGNAL_HOLD: under MMA_CONTROL_DEVICE, the next `value`
+ *     transfers that give the copy engines a share count one command more than
+ *     they submit, so the kernel's wait never sees the engines finish and its
+ *     watchdog must release the stream; the count is taken back once the kernel
+ *     has left, and the transfer fails (sticky).
  * value 0 clears a fault. */
 #define MMA_FAULT_ENGINE_STALL_US 1
 #define MMA_FAULT_SDMA_SUBMIT_FAIL 2
 #define MMA_FAULT_ENGINE_IGNORE 3
+#define MMA_FAULT_DEVICE_SIGNAL_HOLD 4
 mma_status_t mma_test_set_fault(int32_t kind, uint64_t value);
 
 #ifdef __cplusplus

@@ -32,6 +32,7 @@ MMA_NUM_PATHS = 17
 MMA_FAULT_ENGINE_STALL_US = 1
 MMA_FAULT_SDMA_SUBMIT_FAIL = 2
 MMA_FAULT_ENGINE_IGNORE = 3
+MMA_FAULT_DEVICE_SIGNAL_HOLD = 4
 MMA_TASK_CU_ONLY = 1
 MMA_TASK_SDMA_ONLY = 2
 

@@ -145,6 +145,7 @@ struct Transfer {
   uint64_t kv_per = 0;         // pieces per CU ring entry of a KV transfer (0: the engine thread's rule)
   // Device control: planned in full at submission (prepare_device), retired by reap.
   uint32_t dev_cmds = 0;           // copy-engine commands counted by the record's device signal
+  bool dev_hold = false;           // test fault: the signal counts one command too many until reaped
   std::vector<uint8_t> dev_path;   // path (stats index) that carries each micro-task
   std::shared_ptr<Waiter> waiter;  // set for synchronous calls
   // Per ring slot (kRingSize of them for a record, kPrefill for a light slot), set
@@ -235,6 +236,7 @@ inline std::mutex g_trace_mu;
 inline std::deque<mma_trace_rec_t> g_trace_buf;
 constexpr size_t kTraceCap = 65536;
 inline std::atomic<uint64_t> g_fault_stall_us{0}, g_fault_submit_fail{0}, g_fault_ignore{0};
+inline std::atomic<uint64_t> g_fault_signal_hold{0};
 
 // What the engine needs from the GPU side. The product backend is ROCr/HIP
 // (mma_runtime.cpp); a CPU test backend emulates it with host threads.
@@ -728,7 +730,12 @@ class Engine {
       cmds.push_back(Cmd{path, i, i + 1, t.bytes});
     }
     const uint64_t sig = cmds.empty() ? 0 : dev_sig_[x->rec_idx];
-    if (!cmds.empty()) be_->signal_store(sig, static_cast<int64_t>(cmds.size()));
+    if (!cmds.empty()) {
+      uint64_t f = g_fault_signal_hold.load();
+      while (f > 0 && !x->dev_hold)
+        if (g_fault_signal_hold.compare_exchange_weak(f, f - 1)) x->dev_hold = true;
+      be_->signal_store(sig, static_cast<int64_t>(cmds.size()) + (x->dev_hold ? 1 : 0));
+    }
     const bool h2d = dir_ == MMA_H2D;
     for (const Cmd& c : cmds) {
       const Task& t = x->tasks[c.first];
@@ -788,6 +795,10 @@ class Engine {
   void abandon_device(Transfer* x, uint64_t timeout_ms) {
     if (x->dev_cmds) {
       const uint64_t sig = dev_sig_[x->rec_idx];
+      if (x->dev_hold) {
+        be_->signal_sub(sig, 1);
+        x->dev_hold = false;
+      }
       const uint64_t t0 = now_ns();
       while (be_->signal_load(sig) > 0) {
         if (now_ns() - t0 > timeout_ms * 1000000ull) return;
@@ -957,13 +968,17 @@ class Engine {
   }
 
   // A tracked transfer's kernel is done with its record or light slot.
-  bool tracked_done(const Transfer* x) const {
+  bool tracked_done(Transfer* x) {
     if (x->light >= 0) {  // a whole transfer: every entry's done tag is in
       for (uint64_t t = 0; t < x->pushed; ++t)
         if (ld_acq(&x->done_host[t]) != make_tag(x->seq, t)) return false;
       return true;
     }
     if (ld_acq(&x->rec->h.released) != x->seq) return false;
+    if (x->dev_hold) {  // the kernel has left: take back the count the fault added
+      be_->signal_sub(dev_sig_[x->rec_idx], 1);
+      x->dev_hold = false;
+    }
     return !x->dev_cmds || be_->signal_load(dev_sig_[x->rec_idx]) <= 0;
   }
 

@@ -921,6 +921,7 @@ mma_status_t mma_test_set_fault(int32_t kind, uint64_t value) {
     case MMA_FAULT_ENGINE_STALL_US: g_fault_stall_us = value; return MMA_OK;
     case MMA_FAULT_SDMA_SUBMIT_FAIL: g_fault_submit_fail = value; return MMA_OK;
     case MMA_FAULT_ENGINE_IGNORE: g_fault_ignore = value; return MMA_OK;
+    case MMA_FAULT_DEVICE_SIGNAL_HOLD: g_fault_signal_hold = value; return MMA_OK;
     default: return fail(MMA_ERR_INVALID_ARG, "unknown fault kind %d", kind);
   }
 }

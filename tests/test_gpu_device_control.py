@@ -175,6 +175,37 @@ def test_device_kv_roundtrip(shape, chunk):
     assert sum(stats["path_bytes"][:16]) == 0, "copy engines took part in a KV transfer under device control"
 
 
+@pytest.mark.parametrize("shape", list(KV_SHAPES))
+def test_device_kv_hbm_pool(shape):
+    """A KV pool in HBM (the CU path gathers and scatters within HBM): fetch, then offload the
+    same blocks into other slots, both against the oracle."""
+    s, layout = KV_SHAPES[shape]
+    geom = (s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes)
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    plan = W.kv_offload_plan(s, cfg=4)
+    stream = torch.cuda.Stream()
+    with session("both", chunk_bytes=1 << 20, **DEVICE):
+        r = np.random.default_rng(33)
+        pool_np = r.integers(0, 256, s.host_num_slots * s.slot_bytes, dtype=np.uint8)
+        dpool = torch.from_numpy(pool_np.copy()).cuda()
+        layers = [device_bytes(s.layer_bytes, W.GPU_POISON) for _ in range(s.layers)]
+        before = [to_host(t).reshape(2, s.gpu_num_blocks, s.piece_bytes) for t in layers]
+        torch.cuda.synchronize()
+        mma.mma_kv_fetch(_kv_layout(s, layout), dpool, layers, hs, gb, stream)
+        stream.synchronize()
+        pool_v = pool_np.reshape(s.host_num_slots, s.slot_bytes)
+        for l in range(s.layers):
+            want = okv.kv_fetch_layer(pool_v, before[l], l, s.layers, hs, gb, layout, geom)
+            assert np.array_equal(to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes), want), l
+        views = [to_host(t).reshape(2, s.gpu_num_blocks, s.piece_bytes) for t in layers]
+        mma.mma_kv_offload(_kv_layout(s, layout), dpool, layers, plan.src_blocks, plan.dest, stream)
+        stream.synchronize()
+        want = okv.kv_offload(pool_v, views, plan.src_blocks, plan.dest, layout, geom)
+        assert np.array_equal(to_host(dpool).reshape(s.host_num_slots, -1), want)
+        mma.mma_synchronize()
+        assert mma.mma_get_stats()["failed_transfers"] == 0
+
+
 @pytest.mark.parametrize("rep", range(3))
 def test_device_stream_ordering(rep):
     """A 256 MiB host->device copy on an idle stream (the copy engines carry their share), then

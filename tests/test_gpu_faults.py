@@ -174,3 +174,44 @@ def test_device_control_refused_commands_go_to_cu(refused):
     assert 1 <= st["sdma_submit_failures"] <= refused
     if refused > 2:  # every command refused: the CU path carried everything
         assert st["path_bytes"][16] == n
+
+
+def test_device_control_watchdog_releases_stream_and_error_is_sticky():
+    """Device control on an idle stream with the copy engines' completion signal held one count
+    above their commands: the kernel's last wave never sees them finish, its watchdog releases
+    the stream, the transfer is reported failed and the error is sticky. The data itself has
+    landed (every real command completed)."""
+    n = (64 << 20) + 3
+    src_np = np.ascontiguousarray(W.uniform_bytes(12, 2, n, n))
+    stream = torch.cuda.Stream()
+    with session("both", control=mma.MMA_CONTROL_DEVICE, watchdog_ms=300):
+        src = mma.PinnedBuffer(n)
+        src.array[:] = src_np
+        dst = torch.full((n,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        mma.mma_test_set_fault(mma.MMA_FAULT_DEVICE_SIGNAL_HOLD, 1)
+        try:
+            t0 = time.time()
+            mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, stream)
+            stream.synchronize()                # must return: the wait's watchdog ends it
+            dt = time.time() - t0
+        finally:
+            mma.mma_test_set_fault(mma.MMA_FAULT_DEVICE_SIGNAL_HOLD, 0)
+        deadline = time.time() + 10
+        while mma.mma_get_stats()["failed_transfers"] == 0 and time.time() < deadline:
+            time.sleep(0.01)
+        log(f"  watchdog released the stream after {dt * 1e3:.0f} ms")
+        assert dt >= 0.25
+        assert mma.mma_get_stats()["failed_transfers"] == 1
+        assert np.array_equal(to_host(dst), src_np)
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, stream)
+        assert e.value.name == "MMA_ERR_TRANSFER_FAILED"
+        mma.mma_clear_error()
+        # the record came back: later transfers run normally
+        for _ in range(70):
+            mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, stream)
+        stream.synchronize()
+        mma.mma_synchronize()
+        assert mma.mma_get_stats()["failed_transfers"] == 1
+        src.free()
