@@ -14,6 +14,13 @@
 //      reports that every micro-task of every path has landed (the spin wait
 //      of Section 4), with a bounded, progress-re-armed watchdog, then exits
 //      and releases downstream stream work.
+// Under device control the whole CU share is in the ring before the launch
+// (a ticket past it ends a wave's claims) and the last wave waits for the copy
+// engines' own completion signal instead of the engine's word: no host thread
+// takes part once the kernel runs. mma_transfer_xpacked_kernel<E> is the same
+// kernel for the x-packed GPU block layout (an LDS transform per piece), and
+// mma_whole_kernel<N> a self-contained launch whose N entries travel in its
+// arguments.
 //
 // Every host-memory poll is a PCIe read that competes with the payload for the
 // link, so polls are few: one load instruction both checks and fetches a ring
