@@ -824,7 +824,11 @@ def sweep_duplex():
     CU = mma.MMA_PATH_CU
     for name, kv in (("default", {}), ("cu only", dict(path_mask_h2d=CU, path_mask_d2h=CU)),
                      ("d2h without cu", dict(path_mask_d2h=0x3)),
-                     ("engine 0 h2d, engine 1 d2h, no cu", dict(path_mask_h2d=1, path_mask_d2h=2))):
+                     ("h2d without cu", dict(path_mask_h2d=0x3)),
+                     ("no cu either way", dict(path_mask_h2d=0x3, path_mask_d2h=0x3)),
+                     ("engine 0 h2d, engine 1 d2h, no cu", dict(path_mask_h2d=1, path_mask_d2h=2)),
+                     ("engine 0 + cu h2d, engine 1 + cu d2h", dict(path_mask_h2d=CU | 1, path_mask_d2h=CU | 2)),
+                     ("engine 0 h2d, engine 1 + cu d2h", dict(path_mask_h2d=1, path_mask_d2h=CU | 2))):
         c = mma.mma_config_default()
         for k, v in kv.items():
             setattr(c, k, v)
