@@ -370,7 +370,11 @@ class Engine {
     return rc;
   }
 
-  void shutdown() {
+  // Stops the engine thread and frees what the GPU side shares with it. With
+  // release = false (transfers still in flight: a kernel may still read its
+  // record, a copy engine still decrement a signal) that memory and those
+  // signals are left alone rather than unmapped under them.
+  void shutdown(bool release = true) {
     {
       std::lock_guard<std::mutex> g(mu_);
       if (!thread_.joinable()) return;
@@ -379,6 +383,15 @@ class Engine {
     }
     cv_.notify_all();
     thread_.join();
+    if (!release) {
+      slots_.clear();
+      dev_sig_.clear();
+      dev_sig_val_.clear();
+      ds_ = nullptr;
+      recs_ = nullptr;
+      light_ = nullptr;
+      return;
+    }
     for (auto& s : slots_) be_->signal_destroy(s.sig);
     slots_.clear();
     for (uint64_t sig : dev_sig_) be_->signal_destroy(sig);

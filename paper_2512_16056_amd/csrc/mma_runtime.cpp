@@ -159,8 +159,11 @@ struct ExitGuard {
   ~ExitGuard() {
     std::lock_guard<std::mutex> g(g_init_mu);
     if (!g_rt) return;
+    // Transfers still in flight after the wait keep their records and signals:
+    // the process is ending, and freeing them could unmap memory that a
+    // running kernel still polls.
     for (auto& e : g_rt->eng)
-      if (e) (void)e->wait_idle(2000);
+      if (e) e->shutdown(e->wait_idle(2000));
     for (auto& e : g_rt->eng) e.reset();
   }
 } g_exit_guard;

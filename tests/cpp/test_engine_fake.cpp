@@ -86,14 +86,21 @@ class FakeBackend final : public Backend {
     *host = *dev = std::aligned_alloc(4096, (bytes + 4095) & ~4095ull);
     return *host ? MMA_OK : MMA_ERR_NO_MEMORY;
   }
-  void free_records(void* host) override { std::free(host); }
+  void free_records(void* host) override {
+    frees_.fetch_add(1);
+    std::free(host);
+  }
+  int frees() const { return frees_.load(); }
   mma_status_t alloc_device_state(uint64_t bytes, void** dev) override {
     *dev = std::aligned_alloc(128, (bytes + 127) & ~127ull);
     if (!*dev) return MMA_ERR_NO_MEMORY;
     std::memset(*dev, 0, bytes);
     return MMA_OK;
   }
-  void free_device_state(void* dev) override { std::free(dev); }
+  void free_device_state(void* dev) override {
+    frees_.fetch_add(1);
+    std::free(dev);
+  }
   mma_status_t alloc_host_scratch(uint64_t bytes, void** host) override {
     *host = std::calloc(1, bytes);
     return *host ? MMA_OK : MMA_ERR_NO_MEMORY;
@@ -180,6 +187,7 @@ class FakeBackend final : public Backend {
   }
   uint64_t cmd_ns_;
   bool polled_ = true;
+  std::atomic<int> frees_{0};
   std::vector<std::unique_ptr<Eng>> engines_;
 };
 
@@ -1033,6 +1041,35 @@ void device_unlaunched_and_whole() {
               k);
 }
 
+// Shutting an engine down while a transfer is still in flight (process exit
+// with a stream that has not reached the transfer): the memory the kernel
+// shares with the engine stays allocated, and the kernel, once it runs, still
+// finds its record and done tags.
+void shutdown_in_flight_keeps_shared_memory() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.whole[0] = s.cfg.whole[1] = 4 * 1024 * 1024;
+  Harness h(s);
+  FakeStream st;
+  std::promise<void> gate;
+  std::shared_future<void> open = gate.get_future().share();
+  st.launch([open] { open.wait(); });  // holds the stream
+  const uint64_t n = 64 * 1024 + 7;
+  auto src = random_bytes(n, 31);
+  std::vector<uint8_t> dst(n, 0);
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st);
+  Engine* e = h.engine(MMA_H2D);
+  const bool idle = e->wait_idle(50);
+  CHECK(!idle, "a transfer behind a held stream reported idle");
+  const int frees = h.backend().frees();
+  e->shutdown(idle);
+  CHECK(h.backend().frees() == frees, "shared memory freed with a transfer in flight");
+  gate.set_value();
+  st.synchronize();
+  CHECK(dst == src, "the transfer after an unreleased shutdown differs");
+  std::printf("ok   shutdown with a transfer in flight keeps the memory its kernel uses\n");
+}
+
 // Pull-based selection against fixed splits decided at plan time, on two
 // paths (the CU path and one copy engine) with a given rate ratio.
 double timed_copy(double cu_rate, double eng_rate, uint32_t static_cu_percent, bool pull) {
@@ -1112,6 +1149,7 @@ int main(int argc, char** argv) {
     device_kv_roundtrip();
     device_recycling_and_refusals();
     device_unlaunched_and_whole();
+    shutdown_in_flight_keeps_shared_memory();
   }
   if (timing) {
     slow_engine_gets_fewer_tasks();

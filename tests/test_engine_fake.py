@@ -11,7 +11,8 @@ Under device control (no engine thread in the loop) it checks exact copies on id
 (copy engines and CU path) and busy ones (CU path only), KV fetch and offload, records
 recycled by later submissions, refused commands re-routed, a transfer larger than a ring
 handed to the engine thread, a failed launch draining the copy engines, and queued whole
-transfers. It is built optimised, and with ThreadSanitizer for the correctness scenarios.
+transfers, and a shutdown with a transfer in flight that keeps the memory its kernel uses. It
+is built optimised, and with ThreadSanitizer and AddressSanitizer for the correctness scenarios.
 """
 import os
 import shutil
@@ -63,4 +64,16 @@ def test_engine_on_fake_paths_thread_sanitizer(tmp_path):
     exe = str(tmp_path / "engine_fake_tsan")
     _build(cxx, exe, ["-O1", "-fsanitize=thread"])
     env = dict(os.environ, TSAN_OPTIONS="halt_on_error=1 exitcode=66")
+    _run(exe, ["--no-timing"], env)
+
+
+def test_engine_on_fake_paths_address_sanitizer(tmp_path):
+    # host code only (g++); leak checks are off because a shutdown with transfers in flight
+    # keeps the memory their kernels use, on purpose
+    cxx = shutil.which("g++")
+    if cxx is None:
+        pytest.skip("no g++")
+    exe = str(tmp_path / "engine_fake_asan")
+    _build(cxx, exe, ["-O1", "-fsanitize=address", "-fno-omit-frame-pointer"])
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0 halt_on_error=1 exitcode=67")
     _run(exe, ["--no-timing"], env)
