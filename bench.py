@@ -366,6 +366,27 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
     return extras
 
 
+def sampled_fetch_parity(s, pv, layers, hs, gb, xpacked, samples=64, seed=0):
+    """64 random (block, layer, K/V) pieces of the GPU cache against the pool bytes they were
+    fetched from: the piece itself, or for the x-packed layout its key [H][D/x][B][x] / value
+    [H][D][B] arrangement."""
+    import numpy as np
+    r = np.random.default_rng(seed)
+    ok = True
+    B_, H_, D_, E_ = s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes
+    for _ in range(samples):
+        i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
+        off = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
+        got = layers[l][off:off + s.piece_bytes].cpu().numpy()
+        want = pv[hs[i]].reshape(s.layers, 2, s.piece_bytes)[l, k]
+        if xpacked:
+            w = want.reshape(B_, H_, D_, E_)
+            want = (w.reshape(B_, H_, D_ * E_ // 16, 16 // E_, E_).transpose(1, 2, 0, 3, 4) if k == 0
+                    else w.transpose(1, 2, 0, 3)).reshape(-1)
+        ok &= bool(np.array_equal(got, want))
+    return ok
+
+
 def device_control_leg(mma, torch, pool, layers, lay, hs, gb, stream, total):
     """The 64k-token fetch again under device control (the calling thread plans the transfer, the
     dummy-task kernel alone tracks it; the stream has the start event pending, so the CU path
@@ -376,13 +397,20 @@ def device_control_leg(mma, torch, pool, layers, lay, hs, gb, stream, total):
     cfg.control = mma.MMA_CONTROL_DEVICE
     mma.mma_init(0, cfg)
     try:
+        import workloads as W
+        for t_ in layers:  # poison the cache so that the parity check sees this leg's bytes
+            t_.fill_(W.GPU_POISON)
+        torch.cuda.synchronize()
         t = _timed(stream, lambda: mma.mma_kv_fetch(lay, pool, layers, hs, gb, stream), reps=5, warm=1)
         mma.mma_synchronize()
         st = mma.mma_get_stats()
+        s = W.KV64K
+        pv = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+        ok = sampled_fetch_parity(s, pv, layers, hs, gb, lay.gpu_layout == mma.MMA_KV_LAYOUT_XPACKED, seed=1)
         res = {"kv_fetch_ms": round(t["p50"], 3), "kv_fetch_ms_p10_p90": [round(t["p10"], 3), round(t["p90"], 3)],
                "kv_fetch_GBs": round(total / t["p50"] / 1e6, 2),
                "engine_cpu_ms_per_step": round(st["engine_cpu_ns"] / 1e6 / 6, 3),
-               "failed_transfers": st["failed_transfers"]}
+               "failed_transfers": st["failed_transfers"], "sampled_parity": ok}
     finally:
         mma.mma_finalize()
         mma.mma_init(0)
@@ -1056,21 +1084,8 @@ def main():
     log(f"kv fetch: {ms_per_step:.2f} ms/step, {value:.2f} GB/s wall; kernel avg {avg_kernel_ms:.2f} ms "
         f"(min {min(kernel_ms):.2f}, max {max(kernel_ms):.2f}) = {achieved:.2f} GB/s")
 
-    # ---- sampled parity against the oracle definition (full parity lives in the tests)
-    r = np.random.default_rng(0)
-    ok = True
-    host = {}
-    B_, H_, D_, E_ = s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes
-    for _ in range(64):
-        i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
-        off = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
-        got = layers[l][off:off + s.piece_bytes].cpu().numpy()
-        want = pv[hs[i]].reshape(s.layers, 2, s.piece_bytes)[l, k]
-        if xpacked:  # key [H][D/x][B][x], value [H][D][B]
-            w = want.reshape(B_, H_, D_, E_)
-            want = (w.reshape(B_, H_, D_ * E_ // 16, 16 // E_, E_).transpose(1, 2, 0, 3, 4) if k == 0
-                    else w.transpose(1, 2, 0, 3)).reshape(-1)
-        ok &= bool(np.array_equal(got, want))
+    # ---- sampled parity against the definition of the fetch (full parity lives in the tests)
+    ok = sampled_fetch_parity(s, pv, layers, hs, gb, xpacked)
     log(f"sampled parity: {'ok' if ok else 'MISMATCH'}")
 
     out = {

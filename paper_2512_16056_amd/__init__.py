@@ -62,7 +62,7 @@ class mma_config_t(ctypes.Structure):
                 ("control", ctypes.c_uint32)]
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        return {k: getattr(self, k) for k, _ in self._fields_}
 
 
 class mma_copy_desc_t(ctypes.Structure):
