@@ -32,9 +32,12 @@ GPU block layouts (``layout``; the host side is always token-major
   block's key is ``[kv_heads][head_dim / x][block_tokens][x]`` with ``x = 16 //
   elem_bytes`` (16-byte groups of consecutive dims, token-minor), and its value is
   ``[kv_heads][head_dim][block_tokens]`` (token-minor). ``head_dim * elem_bytes``
-  must be a multiple of 16.
+  must be a multiple of 16;
+* ``LAYOUT_HND`` (2): head-major, the transposed layout of some attention kernels: K
+  and V blocks are both ``[kv_heads][block_tokens][head_dim]``, i.e. the piece's
+  (token, head) rows of ``head_dim`` elements, transposed to (head, token) order.
 
-Both are readings: the paper names the KV-cache systems but not their layouts.
+All three are readings: the paper names the KV-cache systems but not their layouts.
 """
 from __future__ import annotations
 
@@ -61,6 +64,7 @@ def validate_tables(src_idx: Sequence[int], src_count: int,
 
 LAYOUT_PIECE = 0
 LAYOUT_XPACKED = 1
+LAYOUT_HND = 2
 
 
 def piece_to_block(piece: np.ndarray, k: int, layout: int, geom) -> np.ndarray:
@@ -69,6 +73,9 @@ def piece_to_block(piece: np.ndarray, k: int, layout: int, geom) -> np.ndarray:
     piece = np.asarray(piece, dtype=np.uint8).reshape(-1)
     if layout == LAYOUT_PIECE:
         return piece.copy()
+    if layout == LAYOUT_HND:  # K and V alike: [B][H][row] -> [H][B][row]
+        B, H, D, E = geom
+        return np.ascontiguousarray(piece.reshape(B, H, D * E).transpose(1, 0, 2)).reshape(-1)
     if layout != LAYOUT_XPACKED:
         raise ValueError("unknown layout")
     B, H, D, E = geom
@@ -86,6 +93,9 @@ def block_to_piece(block: np.ndarray, k: int, layout: int, geom) -> np.ndarray:
     block = np.asarray(block, dtype=np.uint8).reshape(-1)
     if layout == LAYOUT_PIECE:
         return block.copy()
+    if layout == LAYOUT_HND:  # [H][B][row] -> [B][H][row]
+        B, H, D, E = geom
+        return np.ascontiguousarray(block.reshape(H, B, D * E).transpose(1, 0, 2)).reshape(-1)
     if layout != LAYOUT_XPACKED:
         raise ValueError("unknown layout")
     B, H, D, E = geom

@@ -17,6 +17,10 @@ block layout 1 (x-packed key, token-minor value; x = 16 // E elements)::
 
     key   (k=0): ((((k*NB + g)*H + h)*(D//x) + d//x)*B + t)*x + d%x) * E + b
     value (k=1): ((((k*NB + g)*H + h)*D + d)*B + t) * E + b
+
+block layout 2 (head-major, K and V alike)::
+
+    gpu_off  = ((((k*NB + g)*H + h)*B + t)*D + d)*E + b
 """
 from __future__ import annotations
 
@@ -30,6 +34,8 @@ def host_offset(s, l, k, t, h, d, b, L, B, H, D, E):
 def gpu_offset(k, g, t, h, d, b, NB, B, H, D, E, layout=0):
     if layout == 0:
         return ((((k * NB + g) * B + t) * H + h) * D + d) * E + b
+    if layout == 2:
+        return ((((k * NB + g) * H + h) * B + t) * D + d) * E + b
     x = 16 // E
     if k == 0:
         return (((((k * NB + g) * H + h) * (D // x) + d // x) * B + t) * x + d % x) * E + b

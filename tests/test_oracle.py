@@ -278,6 +278,71 @@ def test_kv_xpacked_roundtrip_and_rejects():
     assert np.array_equal(back[slots], host[slots])
 
 
+# ----------------------------------------------------------------------------- head-major (HND) KV layout
+HND = okv.LAYOUT_HND
+
+
+@pytest.mark.parametrize("name", ["rows16", "rows3"])
+def test_kv_hnd_golden(golden_dir, name):
+    g = parse_golden(os.path.join(golden_dir, "kv_hnd_tiny.txt"))[name]
+    geom = (g["B"], g["H"], g["D"], g["E"])
+    host = np.array(g["host"], np.uint8)
+    for k in (0, 1):  # K and V share the layout
+        assert okv.piece_to_block(host, k, HND, geom).tolist() == g["block"]
+        assert okv.block_to_piece(np.array(g["block"], np.uint8), k, HND, geom).tolist() == g["host"]
+
+
+HND_SHAPES = [(1, 2, 2, 8, 2), (2, 3, 2, 8, 2), (1, 2, 3, 16, 1), (2, 1, 4, 4, 4), (1, 4, 1, 8, 2), (1, 3, 5, 2, 1)]
+
+
+@pytest.mark.parametrize("shape", HND_SHAPES)
+def test_kv_hnd_matches_naive(shape):
+    L, B, H, D, E = shape
+    S, NB = 3, 4
+    host, layers = _tiny(L, B, H, D, E, S, NB, seed=11 + sum(shape))
+    slots, blocks = [1, 2, 0], [0, 3, 2]
+    geom = (B, H, D, E)
+    got = okv.kv_fetch(host, layers, slots, blocks, HND, geom)
+    want = onaive.fetch(host.tobytes(), [x.tobytes() for x in layers], slots, blocks, L, B, H, D, E, NB, layout=2)
+    assert all(got[l].tobytes() == bytes(want[l]) for l in range(L))
+    got = okv.kv_offload(host, layers, blocks, slots, HND, geom)
+    want = onaive.offload(host.tobytes(), [x.tobytes() for x in layers], blocks, slots, L, B, H, D, E, NB, layout=2)
+    assert got.tobytes() == bytes(want)
+
+
+def test_kv_hnd_all_permutations_naive():
+    L, B, H, D, E, S, NB = 1, 2, 3, 8, 2, 4, 5
+    host, layers = _tiny(L, B, H, D, E, S, NB, seed=23)
+    geom = (B, H, D, E)
+    for perm in itertools.permutations(range(4)):
+        got = okv.kv_fetch(host, layers, list(perm), [1, 4, 0, 2], HND, geom)
+        want = onaive.fetch(host.tobytes(), [x.tobytes() for x in layers], list(perm), [1, 4, 0, 2],
+                            L, B, H, D, E, NB, layout=2)
+        assert got[0].tobytes() == bytes(want[0])
+
+
+def test_kv_hnd_one_token_or_one_head_is_the_host_layout():
+    # [H][1][D] and [1][B][D] are the host's [1][H][D] and [B][1][D].
+    r = np.random.default_rng(17)
+    for B, H, D, E in [(1, 4, 8, 2), (1, 3, 16, 1), (5, 1, 8, 2), (16, 1, 128, 2)]:
+        piece = r.integers(0, 256, B * H * D * E, dtype=np.uint8)
+        for k in (0, 1):
+            assert np.array_equal(okv.piece_to_block(piece, k, HND, (B, H, D, E)), piece)
+
+
+def test_kv_hnd_rows_move_whole():
+    # Every (token, head) row of D*E bytes lands intact at row (head, token) -- explicit loops.
+    B, H, D, E = 4, 3, 8, 2
+    R = D * E
+    r = np.random.default_rng(19)
+    piece = r.integers(0, 256, B * H * R, dtype=np.uint8)
+    blk = okv.piece_to_block(piece, 0, HND, (B, H, D, E))
+    for t in range(B):
+        for h in range(H):
+            assert blk[(h * B + t) * R:(h * B + t + 1) * R].tolist() == piece[(t * H + h) * R:(t * H + h + 1) * R].tolist()
+    assert np.array_equal(okv.block_to_piece(blk, 1, HND, (B, H, D, E)), piece)
+
+
 # ----------------------------------------------------------------------------- plan
 def test_plan_counts_golden(golden_dir):
     g = dict(parse_pairs(os.path.join(golden_dir, "plan_counts.txt")))
