@@ -41,9 +41,10 @@ def parse():
     p.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
-    p.add_argument("--kv-layout", choices=["piece", "xpacked"], default="piece",
-                   help="GPU block layout of the timed KV fetch: pieces as in host memory (default), or the "
-                        "x-packed layout of paged-attention decode kernels (transformed through LDS)")
+    p.add_argument("--kv-layout", choices=["piece", "xpacked", "hnd"], default="piece",
+                   help="GPU block layout of the timed KV fetch: pieces as in host memory (default), the "
+                        "x-packed layout of paged-attention decode kernels (transformed through LDS), or "
+                        "head-major blocks [heads][tokens][head_dim] (a row permutation)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true", help="skip native comparators and the 64 MiB copy")
     p.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle timing window")
@@ -270,30 +271,22 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
     # The same 64k-token fetch, and the 2048-block offload, with the GPU cache in the x-packed block
     # layout of paged-attention decode kernels (key [H][D/x][B][x], value [H][D][B]): the CU path
     # transforms every piece through LDS. Sampled parity against the layout's definition.
-    xlay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
-                         s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED)
-    xf = _timed(stream, lambda: mma.mma_kv_fetch(xlay, pool, layers, hs, gb, stream), reps=5, warm=1)
-    B_, H_, D_, E_ = s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes
-    x_ = 16 // E_
-    pv4 = pool.array.reshape(s.host_num_slots, s.layers, 2, s.piece_bytes)
-    r = np.random.default_rng(1)
-    ok_x = True
-    for _ in range(32):
-        i, l, k = int(r.integers(s.n_blocks)), int(r.integers(s.layers)), int(r.integers(2))
-        o = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
-        got = layers[l][o:o + s.piece_bytes].cpu().numpy()
-        src = pv4[hs[i], l, k].reshape(B_, H_, D_, E_)
-        want = (src.reshape(B_, H_, D_ // x_, x_, E_).transpose(1, 2, 0, 3, 4) if k == 0
-                else src.transpose(1, 2, 0, 3)).reshape(-1)
-        ok_x &= bool(np.array_equal(got, want))
-    xo = _timed(stream, lambda: mma.mma_kv_offload(xlay, pool, layers, src_blocks, plan.dest, stream), reps=5, warm=1)
-    extras["kv_xpacked_layout"] = {
-        "fetch_ms": round(xf["p50"], 3), "fetch_GBs": round(total / xf["p50"] / 1e6, 2),
-        "fetch_frac_of_measured": round(total / xf["p50"] / 1e6 / m_h2d, 4),
-        "offload_2048_ms": round(xo["p50"], 3), "offload_GBs": round(off_bytes / xo["p50"] / 1e6, 2),
-        "offload_frac_of_measured_d2h": round(off_bytes / xo["p50"] / 1e6 / m_d2h, 4),
-        "sampled_parity": ok_x}
-    log("x-packed layout:", extras["kv_xpacked_layout"])
+    # The same fetch and offload into the transformed GPU block layouts.
+    pv = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+    for key, code in (("kv_xpacked_layout", mma.MMA_KV_LAYOUT_XPACKED), ("kv_hnd_layout", mma.MMA_KV_LAYOUT_HND)):
+        xlay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                             s.host_num_slots, code)
+        xf = _timed(stream, lambda: mma.mma_kv_fetch(xlay, pool, layers, hs, gb, stream), reps=5, warm=1)
+        ok_x = sampled_fetch_parity(s, pv, layers, hs, gb, code, samples=32, seed=1)
+        xo = _timed(stream, lambda: mma.mma_kv_offload(xlay, pool, layers, src_blocks, plan.dest, stream), reps=5,
+                    warm=1)
+        extras[key] = {
+            "fetch_ms": round(xf["p50"], 3), "fetch_GBs": round(total / xf["p50"] / 1e6, 2),
+            "fetch_frac_of_measured": round(total / xf["p50"] / 1e6 / m_h2d, 4),
+            "offload_2048_ms": round(xo["p50"], 3), "offload_GBs": round(off_bytes / xo["p50"] / 1e6, 2),
+            "offload_frac_of_measured_d2h": round(off_bytes / xo["p50"] / 1e6 / m_d2h, 4),
+            "sampled_parity": ok_x}
+        log(key, extras[key])
 
     # Measured HBM copy peak (read + write bytes): the runtime's device-to-device copy and the bare
     # streaming kernel over device memory at the best grid, 2 GiB each way.
@@ -366,10 +359,10 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
     return extras
 
 
-def sampled_fetch_parity(s, pv, layers, hs, gb, xpacked, samples=64, seed=0):
-    """64 random (block, layer, K/V) pieces of the GPU cache against the pool bytes they were
-    fetched from: the piece itself, or for the x-packed layout its key [H][D/x][B][x] / value
-    [H][D][B] arrangement."""
+def sampled_fetch_parity(s, pv, layers, hs, gb, gpu_layout, samples=64, seed=0):
+    """Random (block, layer, K/V) pieces of the GPU cache against the pool bytes they were
+    fetched from: the piece itself (gpu_layout 0), its x-packed key [H][D/x][B][x] / value
+    [H][D][B] arrangement (1), or its head-major [H][B][D] arrangement (2)."""
     import numpy as np
     r = np.random.default_rng(seed)
     ok = True
@@ -379,10 +372,12 @@ def sampled_fetch_parity(s, pv, layers, hs, gb, xpacked, samples=64, seed=0):
         off = (k * s.gpu_num_blocks + int(gb[i])) * s.piece_bytes
         got = layers[l][off:off + s.piece_bytes].cpu().numpy()
         want = pv[hs[i]].reshape(s.layers, 2, s.piece_bytes)[l, k]
-        if xpacked:
+        if gpu_layout == 1:
             w = want.reshape(B_, H_, D_, E_)
             want = (w.reshape(B_, H_, D_ * E_ // 16, 16 // E_, E_).transpose(1, 2, 0, 3, 4) if k == 0
                     else w.transpose(1, 2, 0, 3)).reshape(-1)
+        elif gpu_layout == 2:
+            want = want.reshape(B_, H_, D_ * E_).transpose(1, 0, 2).reshape(-1)
         ok &= bool(np.array_equal(got, want))
     return ok
 
@@ -406,7 +401,7 @@ def device_control_leg(mma, torch, pool, layers, lay, hs, gb, stream, total):
         st = mma.mma_get_stats()
         s = W.KV64K
         pv = pool.array.reshape(s.host_num_slots, s.slot_bytes)
-        ok = sampled_fetch_parity(s, pv, layers, hs, gb, lay.gpu_layout == mma.MMA_KV_LAYOUT_XPACKED, seed=1)
+        ok = sampled_fetch_parity(s, pv, layers, hs, gb, lay.gpu_layout, seed=1)
         res = {"kv_fetch_ms": round(t["p50"], 3), "kv_fetch_ms_p10_p90": [round(t["p10"], 3), round(t["p90"], 3)],
                "kv_fetch_GBs": round(total / t["p50"] / 1e6, 2),
                "engine_cpu_ms_per_step": round(st["engine_cpu_ns"] / 1e6 / 6, 3),
@@ -1048,10 +1043,11 @@ def main():
     with ThreadPoolExecutor(16) as ex:
         list(ex.map(fill, range(s.n_blocks)))
     layers = [torch.full((s.layer_bytes,), W.GPU_POISON, dtype=torch.uint8, device="cuda") for _ in range(s.layers)]
-    xpacked = args.kv_layout == "xpacked"
+    gl = {"piece": mma.MMA_KV_LAYOUT_PIECE, "xpacked": mma.MMA_KV_LAYOUT_XPACKED, "hnd": mma.MMA_KV_LAYOUT_HND}
     lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
-                        s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED if xpacked else mma.MMA_KV_LAYOUT_PIECE)
-    kernel_name = "mma_transfer_xpacked_kernel" if xpacked else "mma_transfer_kernel"
+                        s.host_num_slots, gl[args.kv_layout])
+    kernel_name = {"piece": "mma_transfer_kernel", "xpacked": "mma_transfer_xpacked_kernel",
+                   "hnd": "mma_transfer_hnd_kernel"}[args.kv_layout]
     torch.cuda.synchronize()
     log(f"inputs ready in {time.time() - t0:.1f}s")
 
@@ -1085,7 +1081,7 @@ def main():
         f"(min {min(kernel_ms):.2f}, max {max(kernel_ms):.2f}) = {achieved:.2f} GB/s")
 
     # ---- sampled parity against the definition of the fetch (full parity lives in the tests)
-    ok = sampled_fetch_parity(s, pv, layers, hs, gb, xpacked)
+    ok = sampled_fetch_parity(s, pv, layers, hs, gb, lay.gpu_layout)
     log(f"sampled parity: {'ok' if ok else 'MISMATCH'}")
 
     out = {
@@ -1104,7 +1100,8 @@ def main():
         "config": {
             "workload": "kv_fetch_64k_tokens: 4096 blocks x 16 tokens, 32 layers x K,V x 8 kv heads x 128 dim bf16 "
                         "(8 GiB) pinned host pool -> paged GPU cache via block table"
-                        + (" (x-packed GPU block layout)" if xpacked else ""),
+                        + {"piece": "", "xpacked": " (x-packed GPU block layout)",
+                           "hnd": " (head-major GPU block layout)"}[args.kv_layout],
             "gpu_block_layout": args.kv_layout,
             "bytes_per_step": total,
             "pieces_per_step": s.n_blocks * s.pieces_per_block,

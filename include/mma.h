@@ -152,12 +152,17 @@ typedef struct mma_copy_desc {
  *               {1, 2, 4, 8}, head_dim * elem_bytes and block_tokens * elem_bytes
  *               multiples of 16, a 16-byte-aligned pool and layer tensors, and
  *               block_tokens * (head_dim * elem_bytes + 16) <= 36 KiB (one head of
- *               one block fits a wave's LDS tile); otherwise MMA_ERR_INVALID_ARG. */
+ *               one block fits a wave's LDS tile); otherwise MMA_ERR_INVALID_ARG.
+ *     MMA_KV_LAYOUT_HND     (2): head-major, K and V alike [kv_heads][block_tokens][head_dim]
+ *               (the transposed layout of some attention kernels). Needs
+ *               head_dim * elem_bytes a multiple of 16 and a 16-byte-aligned pool and
+ *               layer tensors; otherwise MMA_ERR_INVALID_ARG. */
 #define MMA_CONTROL_HOST 0u
 #define MMA_CONTROL_DEVICE 1u
 
 #define MMA_KV_LAYOUT_PIECE 0u
 #define MMA_KV_LAYOUT_XPACKED 1u
+#define MMA_KV_LAYOUT_HND 2u
 typedef struct mma_kv_layout {
   uint32_t num_layers;
   uint32_t block_tokens;
@@ -166,7 +171,7 @@ typedef struct mma_kv_layout {
   uint32_t elem_bytes;
   uint32_t gpu_num_blocks;
   uint32_t host_num_slots;
-  uint32_t gpu_layout;    /* MMA_KV_LAYOUT_PIECE (0) or MMA_KV_LAYOUT_XPACKED */
+  uint32_t gpu_layout;    /* MMA_KV_LAYOUT_PIECE (0), MMA_KV_LAYOUT_XPACKED (1) or MMA_KV_LAYOUT_HND (2) */
 } mma_kv_layout_t;
 
 typedef struct mma_stats {

@@ -26,6 +26,7 @@ MMA_D2H = 1
 MMA_PATH_CU = 0x80000000
 MMA_KV_LAYOUT_PIECE = 0
 MMA_KV_LAYOUT_XPACKED = 1
+MMA_KV_LAYOUT_HND = 2
 MMA_CONTROL_HOST = 0
 MMA_CONTROL_DEVICE = 1
 MMA_NUM_PATHS = 17

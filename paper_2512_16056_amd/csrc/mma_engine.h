@@ -492,7 +492,7 @@ class Engine {
   // x-packed KV pieces: a wave alternates between reading a head group into its
   // LDS tile and writing it out, with no reads in flight during the second
   // phase, so more waves are needed for the same bytes in flight.
-  uint32_t grid_for(uint64_t bytes, uint64_t sub, bool needs_cu, bool staged, bool pool_dev, bool xpacked) const {
+  uint32_t grid_for(uint64_t bytes, uint64_t sub, bool needs_cu, bool staged, bool pool_dev, bool wide) const {
     if (!needs_cu) return 1;
     if (pool_dev) {  // HBM gather/scatter: as many waves as there are micro-tasks, up to the limit
       const uint64_t tasks = (bytes + cfg_.chunk - 1) / cfg_.chunk;
@@ -503,18 +503,20 @@ class Engine {
     uint64_t inflight = cu_enabled() ? cfg_.cu_depth * per_task : 0;
     if (staged) inflight += static_cast<uint64_t>(__builtin_popcount(sdma_mask())) * cfg_.depth * per_task;
     uint64_t g = (std::max<uint64_t>(1, std::min(total, inflight)) + kWavesPerWG - 1) / kWavesPerWG;
-    g = std::max<uint64_t>(1, std::min<uint64_t>(g, wg_cap(xpacked)));
+    g = std::max<uint64_t>(1, std::min<uint64_t>(g, wg_cap(wide)));
     return static_cast<uint32_t>(g);
   }
 
-  // Workgroup limit of one launch. x-packed launches get 1.5x cu_workgroups:
+  // Workgroup limit of one launch. x-packed and head-major launches (their
+  // waves move 8 KiB per batch through 16-byte units, against the plain copy's
+  // two 16 KiB batches) get 1.5x cu_workgroups. For x-packed,
   // on the 64k-token workload (fetch / offload GB/s at the default 16) 16
   // workgroups gave 54.6 / 49.1, 20 gave 57.27 / 56.93, 24 gave 57.33 / 56.85,
   // 28 gave 57.14 / 56.82, 32 gave 56.97 / 56.42, 40 and 48 gave 56.4 and 55.8
   // on the fetch: past about 24, the waves' polls and LDS phases cost more
   // than their extra reads in flight gain.
-  uint64_t wg_cap(bool xpacked) const {
-    const uint64_t w = xpacked ? (3ull * cfg_.cu_wgs + 1) / 2 : cfg_.cu_wgs;
+  uint64_t wg_cap(bool wide) const {
+    const uint64_t w = wide ? (3ull * cfg_.cu_wgs + 1) / 2 : cfg_.cu_wgs;
     return std::min<uint64_t>(w, kMaxWorkgroups);
   }
 
@@ -569,7 +571,7 @@ class Engine {
                                   std::max<uint64_t>(kSmallSub, (per + kSmallSub - 1) / kSmallSub * kSmallSub));
     }
     uint32_t grid = grid_for(payload_bytes, x->sub, needs_cu || x->pool_dev, staged, x->pool_dev,
-                             kv && kv->layout == kKvLayoutXPacked);
+                             kv && kv->layout != kKvLayoutPiece);
     x->waves = grid * kWavesPerWG;
     prefill(x);
     const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
@@ -775,7 +777,7 @@ class Engine {
     if (x->pool_dev) {
       grid = grid_for(payload_bytes, x->sub, true, false, true, false);
     } else {
-      const uint64_t cap = wg_cap(kv && kv->layout == kKvLayoutXPacked);
+      const uint64_t cap = wg_cap(kv && kv->layout != kKvLayoutPiece);
       grid = static_cast<uint32_t>(
           std::max<uint64_t>(1, std::min<uint64_t>((x->pushed + kWavesPerWG - 1) / kWavesPerWG, cap)));
     }

@@ -18,7 +18,8 @@
 // (a ticket past it ends a wave's claims) and the last wave waits for the copy
 // engines' own completion signal instead of the engine's word: no host thread
 // takes part once the kernel runs. mma_transfer_xpacked_kernel<E> is the same
-// kernel for the x-packed GPU block layout (an LDS transform per piece), and
+// kernel for the x-packed GPU block layout (an LDS transform per piece),
+// mma_transfer_hnd_kernel for the head-major one (a row permutation), and
 // mma_whole_kernel<N> a self-contained launch whose N entries travel in its
 // arguments.
 //
@@ -292,10 +293,31 @@ __device__ __forceinline__ void xpacked_piece(const uint8_t* src, uint8_t* dst, 
     xpacked_from_block<E>(src, dst, k, g, lds, lane);
 }
 
+// ---------------------------------------------------------------- head-major KV layout
+// A paged-KV piece in the head-major (HND) layout: the block is [H][B][R], the
+// host piece [B][H][R]. Whole rows move, so there is no LDS stage: units are
+// taken in host order, which keeps the PCIe side (host reads of a fetch, host
+// writes of an offload) contiguous, and the HBM side is read or written in whole
+// rows (256 bytes for the 64k-token workload).
+__device__ __forceinline__ void hnd_piece(const uint8_t* src, uint8_t* dst, bool to_block, const XGeom& g,
+                                          uint32_t lane) {
+  auto get = [&](uint32_t o) -> u32x4 { return *(const gu4*)(src + o); };
+  auto put = [&](uint32_t o, u32x4 v) { *(gu4*)(dst + o) = v; };
+  if (to_block)
+    wave_units(hnd_count(g), lane, [&](uint32_t u) { return UnitOffs{u * 16, hnd_block_off(g, u)}; }, get, put);
+  else
+    wave_units(hnd_count(g), lane, [&](uint32_t u) { return UnitOffs{hnd_block_off(g, u), u * 16}; }, get, put);
+}
+
+// Template value of transfer_body for the head-major layout (the x-packed ones
+// are the element sizes 1, 2, 4, 8).
+constexpr uint32_t kXeHnd = 0x100;
+
 extern __shared__ __attribute__((aligned(16))) uint8_t mma_dyn_lds[];
 
 // The dummy-task kernel's body. kXE = 0: paged-KV blocks hold pieces as the
-// host does. kXE = element bytes: the x-packed GPU block layout through LDS --
+// host does. kXE = kXeHnd: head-major blocks (a row permutation, no LDS).
+// kXE = element bytes: the x-packed GPU block layout through LDS --
 // one kernel per element size, so that no launch carries the registers or LDS
 // of a transform it does not run.
 template <uint32_t kXE>
@@ -399,7 +421,10 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
         src = kind == kEntryToPaged ? contig : pg;
         dst = kind == kEntryToPaged ? pg : contig;
         n = piece;
-        if constexpr (kXE != 0) {
+        if constexpr (kXE == kXeHnd) {
+          hnd_piece(src, dst, kind == kEntryToPaged, xg, lane);
+          continue;
+        } else if constexpr (kXE != 0) {
           xpacked_piece<kXE>(src, dst, kind == kEntryToPaged, p & 1u, xg, wave_lds, lane);
           continue;
         }
@@ -479,6 +504,8 @@ __global__ __launch_bounds__(kBlock) void mma_whole_kernel(WholeArgs<N> a) {
   if (lane == 0) st_sys(&a.done[w], make_tag(a.seq, w));
 }
 
+__global__ __launch_bounds__(kBlock) void mma_transfer_hnd_kernel(KernelArgs a) { transfer_body<kXeHnd>(a); }
+
 template <uint32_t E>
 __global__ __launch_bounds__(kBlock) void mma_transfer_xpacked_kernel(KernelArgs a) {
   transfer_body<E>(a);
@@ -544,6 +571,9 @@ hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t st
                                         : reinterpret_cast<const void*>(&mma_transfer_xpacked_kernel<8>);
     return hipLaunchKernel(k, dim3(grid), dim3(kBlock), params, kWavesPerWG * args.kv_lds_wave, stream);
   }
+  if (args.kv_layout == kKvLayoutHnd)
+    return hipLaunchKernel(reinterpret_cast<const void*>(&mma_transfer_hnd_kernel), dim3(grid), dim3(kBlock), params,
+                           0, stream);
   return hipLaunchKernel(reinterpret_cast<const void*>(&mma_transfer_kernel), dim3(grid), dim3(kBlock), params, 0,
                          stream);
 }

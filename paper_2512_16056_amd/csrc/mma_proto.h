@@ -38,6 +38,7 @@ constexpr uint32_t kBlock = kWave * kWavesPerWG;
 enum : uint32_t {
   kKvLayoutPiece = 0,    // the GPU block holds the piece as the host does
   kKvLayoutXPacked = 1,  // key [heads][head_dim/x][tokens][x], x = 16 / elem; value [heads][head_dim][tokens]
+  kKvLayoutHnd = 2,      // head-major: K and V [heads][tokens][head_dim]
 };
 
 // Entry kinds. Kind and first piece share one 32-bit word: kind | p0 << 8.

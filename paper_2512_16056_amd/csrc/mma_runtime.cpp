@@ -767,6 +767,17 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
     kv.row_bytes = static_cast<uint32_t>(R);
     kv.elem = lay->elem_bytes;
     kv.lds_wave = static_cast<uint32_t>((lds_wave + 15) & ~15ull);
+  } else if (lay->gpu_layout == MMA_KV_LAYOUT_HND) {
+    // Rows of head_dim elements move whole, in 16-byte units.
+    const uint64_t R = static_cast<uint64_t>(lay->head_dim) * lay->elem_bytes;
+    if (R % 16)
+      return fail(MMA_ERR_INVALID_ARG, "head-major KV layout needs head_dim*elem_bytes a multiple of 16");
+    if ((reinterpret_cast<uintptr_t>(host_pool) & 15u) != 0)
+      return fail(MMA_ERR_INVALID_ARG, "head-major KV layout needs a 16-byte-aligned pool");
+    kv.tokens = lay->block_tokens;
+    kv.heads = lay->kv_heads;
+    kv.row_bytes = static_cast<uint32_t>(R);
+    kv.elem = lay->elem_bytes;
   } else if (lay->gpu_layout != MMA_KV_LAYOUT_PIECE) {
     return fail(MMA_ERR_INVALID_ARG, "unknown GPU KV layout %u", lay->gpu_layout);
   }
@@ -798,8 +809,9 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   for (uint32_t l = 0; l < lay->num_layers; ++l) {
     if (!layers[l]) return fail(MMA_ERR_INVALID_ARG, "NULL layer pointer %u", l);
     if ((s = device_range(layers[l], layer_bytes))) return s;
-    if (kv.layout == MMA_KV_LAYOUT_XPACKED && (reinterpret_cast<uintptr_t>(layers[l]) & 15u) != 0)
-      return fail(MMA_ERR_INVALID_ARG, "x-packed KV layout needs 16-byte-aligned layer tensors (layer %u)", l);
+    if (kv.layout != MMA_KV_LAYOUT_PIECE && (reinterpret_cast<uintptr_t>(layers[l]) & 15u) != 0)
+      return fail(MMA_ERR_INVALID_ARG, "x-packed and head-major KV layouts need 16-byte-aligned layer tensors "
+                                       "(layer %u)", l);
     kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l]);
   }
   const uint64_t per_task = std::max<uint64_t>(rt->cfg.chunk / piece, 1) * piece;

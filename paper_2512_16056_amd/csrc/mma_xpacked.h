@@ -1,11 +1,12 @@
-// Index maps of the x-packed paged-KV block transform (key [H][R/16][B][16 bytes],
+// Index maps of the paged-KV block transforms: x-packed (key [H][R/16][B][16 bytes],
 // value [H][D][B] elements; the host piece is token-major [B][H][R], R = head_dim *
 // elem bytes). The dummy-task kernel stages a group of whole heads of one piece in
 // a wave's LDS tile: a load phase reads 16-byte units of the group in the source's
 // order into the tile, a store phase writes 16-byte units in the destination's
 // order, each assembled from the tile. These functions give, for unit number u of
 // a phase, the global and LDS byte offsets it touches; they are plain arithmetic,
-// shared by the kernel and by a CPU test that emulates a wave over them.
+// shared by the kernel and by a CPU test that emulates a wave over them. The
+// head-major (HND) map at the end needs no tile.
 #ifndef MMA_XPACKED_H_
 #define MMA_XPACKED_H_
 
@@ -82,6 +83,16 @@ MMA_HD inline uint32_t xp_from_store_lds(const XGeom& g, uint32_t k, uint32_t gh
   if (k == 0) return rem * xp_from_row_stride(g, 0) + b * 16;
   const uint32_t hl = rem / C, dq = rem - hl * C, D = g.R / g.E;
   return (hl * D + dq * (16 / g.E)) * xp_from_row_stride(g, 1) + b * g.E;
+}
+
+// ---- head-major (HND) blocks: the block is [H][B][R], the host piece [B][H][R].
+// Whole rows move, so there is no LDS stage: 16-byte unit u of the piece in host
+// order (row u / (R/16) = t * H + h, column u % (R/16)) lives in the block at row
+// h * B + t, same column.
+MMA_HD inline uint32_t hnd_count(const XGeom& g) { return g.B * g.H * (g.R / 16); }
+MMA_HD inline uint32_t hnd_block_off(const XGeom& g, uint32_t u) {
+  const uint32_t C = g.R / 16, row = u / C, c = u - row * C, t = row / g.H, h = row - t * g.H;
+  return (h * g.B + t) * g.R + c * 16;
 }
 
 }  // namespace mma

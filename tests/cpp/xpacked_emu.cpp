@@ -85,3 +85,22 @@ extern "C" int emu_xpacked(const uint8_t* src, uint8_t* dst, int to_block, int k
     if (written[i] != 1) bad = 3;
   return bad;
 }
+
+// Head-major blocks: every unit of the piece in host order, read from and written
+// to the offsets hnd_block_off gives, each access checked against the piece.
+extern "C" int emu_hnd(const uint8_t* src, uint8_t* dst, int to_block, uint32_t B, uint32_t H, uint32_t R) {
+  const XGeom g{B, H, R, 0, 0};
+  const uint64_t piece = static_cast<uint64_t>(B) * H * R;
+  std::vector<uint8_t> written(piece, 0);
+  if (static_cast<uint64_t>(hnd_count(g)) * 16 != piece) return 3;
+  for (uint32_t u = 0; u < hnd_count(g); ++u) {
+    const uint64_t host = u * 16ull, blk = hnd_block_off(g, u);
+    if (blk + 16 > piece || host + 16 > piece) return 1;
+    const uint64_t so = to_block ? host : blk, d = to_block ? blk : host;
+    std::memcpy(dst + d, src + so, 16);
+    for (uint32_t i = 0; i < 16; ++i) written[d + i] += 1;
+  }
+  for (uint64_t i = 0; i < piece; ++i)
+    if (written[i] != 1) return 4;
+  return 0;
+}

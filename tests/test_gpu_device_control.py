@@ -129,11 +129,14 @@ KV_SHAPES = {
                         gpu_num_blocks=300, host_num_slots=256, n_blocks=200), okv.LAYOUT_PIECE),
     "xpacked": (W.KVShape(layers=4, block_tokens=16, kv_heads=8, head_dim=128, elem_bytes=2,
                           gpu_num_blocks=300, host_num_slots=256, n_blocks=200), okv.LAYOUT_XPACKED),
+    "hnd": (W.KVShape(layers=4, block_tokens=16, kv_heads=8, head_dim=128, elem_bytes=2,
+                      gpu_num_blocks=300, host_num_slots=256, n_blocks=200), okv.LAYOUT_HND),
 }
 
 
 def _kv_layout(s, layout):
-    gl = mma.MMA_KV_LAYOUT_XPACKED if layout == okv.LAYOUT_XPACKED else mma.MMA_KV_LAYOUT_PIECE
+    gl = {okv.LAYOUT_PIECE: mma.MMA_KV_LAYOUT_PIECE, okv.LAYOUT_XPACKED: mma.MMA_KV_LAYOUT_XPACKED,
+          okv.LAYOUT_HND: mma.MMA_KV_LAYOUT_HND}[layout]
     return mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
                          s.host_num_slots, gl)
 

@@ -338,6 +338,118 @@ def test_kv_xpacked_rejects_unsupported_geometry():
         torch.cuda.synchronize()
 
 
+# ----------------------------------------------------------------------------- head-major GPU block layout
+HND = okv.LAYOUT_HND
+HND_SHAPES = {
+    # head_dim * elem_bytes is a multiple of 16; any token count
+    "bf16": W.KVShape(layers=2, block_tokens=16, kv_heads=2, head_dim=16, elem_bytes=2,
+                      gpu_num_blocks=40, host_num_slots=32, n_blocks=24),
+    "fp8": W.KVShape(layers=3, block_tokens=16, kv_heads=3, head_dim=32, elem_bytes=1,
+                     gpu_num_blocks=50, host_num_slots=40, n_blocks=30),
+    "fp32_5tok": W.KVShape(layers=2, block_tokens=5, kv_heads=3, head_dim=4, elem_bytes=4,
+                           gpu_num_blocks=33, host_num_slots=30, n_blocks=29),
+    "one_head": W.KVShape(layers=2, block_tokens=16, kv_heads=1, head_dim=64, elem_bytes=2,
+                          gpu_num_blocks=20, host_num_slots=20, n_blocks=17),
+    "llama": W.KVShape(layers=4, block_tokens=16, kv_heads=8, head_dim=128, elem_bytes=2,
+                       gpu_num_blocks=300, host_num_slots=256, n_blocks=200),
+}
+
+
+def hnd_layout_of(s: W.KVShape):
+    return mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                         s.host_num_slots, mma.MMA_KV_LAYOUT_HND)
+
+
+@pytest.mark.parametrize("chunk", [4096, 1 << 21])
+@pytest.mark.parametrize("shape", list(HND_SHAPES))
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_kv_hnd_fetch(paths, shape, chunk):
+    s = HND_SHAPES[shape]
+    log(f"kv fetch head-major paths={paths} shape={shape} chunk={chunk}")
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
+        pool = _pool(s, 9)
+        layers = _layers(s, W.GPU_POISON)
+        before = _layer_views(s, layers)
+        mma.mma_kv_fetch(hnd_layout_of(s), pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+        pool_v = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+        for l in range(s.layers):
+            want = okv.kv_fetch_layer(pool_v, before[l], l, s.layers, hs, gb, HND, _geom(s))
+            got = to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
+            assert np.array_equal(got, want), f"layer {l}"
+    assert stats["failed_transfers"] == 0
+    assert sum(stats["path_bytes"]) == s.n_blocks * s.slot_bytes
+
+
+@pytest.mark.parametrize("chunk", [4096, 1 << 21])
+@pytest.mark.parametrize("shape", list(HND_SHAPES))
+@pytest.mark.parametrize("paths", list(PATHS))
+def test_kv_hnd_offload(paths, shape, chunk):
+    s = HND_SHAPES[shape]
+    log(f"kv offload head-major paths={paths} shape={shape} chunk={chunk}")
+    plan = W.kv_offload_plan(s, cfg=4)
+    with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
+        pool = _pool(s, 10)
+        before = pool.array.copy()
+        layers = _layers(s, seed=300)
+        views = _layer_views(s, layers)
+        mma.mma_kv_offload(hnd_layout_of(s), pool, layers, plan.src_blocks, plan.dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        want = okv.kv_offload(before.reshape(s.host_num_slots, -1), views, plan.src_blocks, plan.dest, HND, _geom(s))
+        assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
+
+
+@pytest.mark.parametrize("shape", ["fp32_5tok", "llama"])
+def test_kv_hnd_device_pool_roundtrip(shape):
+    """An HBM-resident pool with the head-major layout: fetch, then offload the same blocks into
+    other slots; both against the oracle."""
+    s = HND_SHAPES[shape]
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    with session("both", chunk_bytes=4096):
+        r = np.random.default_rng(18)
+        pool_np = r.integers(0, 256, s.host_num_slots * s.slot_bytes, dtype=np.uint8)
+        dpool = torch.from_numpy(pool_np.copy()).cuda()
+        layers = _layers(s, W.GPU_POISON)
+        before = _layer_views(s, layers)
+        mma.mma_kv_fetch(hnd_layout_of(s), dpool, layers, hs, gb)
+        torch.cuda.synchronize()
+        pv = pool_np.reshape(s.host_num_slots, s.slot_bytes)
+        for l in range(s.layers):
+            want = okv.kv_fetch_layer(pv, before[l], l, s.layers, hs, gb, HND, _geom(s))
+            assert np.array_equal(to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes), want), l
+        dest = np.roll(hs, 1).astype(np.int32)
+        views = _layer_views(s, layers)
+        mma.mma_kv_offload(hnd_layout_of(s), dpool, layers, gb, dest)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        want = okv.kv_offload(pv, views, gb, dest, HND, _geom(s))
+        assert np.array_equal(to_host(dpool).reshape(s.host_num_slots, -1), want)
+
+
+def test_kv_hnd_rejects_unsupported_geometry():
+    with session("both"):
+        s = W.KVShape(layers=1, block_tokens=16, kv_heads=2, head_dim=12, elem_bytes=2,
+                      gpu_num_blocks=4, host_num_slots=4, n_blocks=2)  # head row of 24 bytes
+        pool = _pool(s, 1)
+        layers = _layers(s, 0)
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_kv_fetch(hnd_layout_of(s), pool, layers, [0, 1], [0, 1])
+        assert e.value.name == "MMA_ERR_INVALID_ARG"
+        pool.free()
+        s = HND_SHAPES["bf16"]
+        big = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes + 64)  # a pool 8 bytes off alignment
+        layers = _layers(s, 0)
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_kv_fetch(hnd_layout_of(s), big.ptr + 8, layers, [0], [0])
+        assert e.value.name == "MMA_ERR_INVALID_ARG"
+        big.free()
+        torch.cuda.synchronize()
+
+
 def _fill_pool_c3(pool: np.ndarray, s: W.KVShape, hs: np.ndarray):
     v = pool.reshape(s.host_num_slots, s.slot_bytes)
     for i in range(s.n_blocks):
@@ -402,12 +514,15 @@ def test_kv_offload_64k_full():
 
 
 @pytest.mark.slow
-def test_kv_xpacked_fetch_offload_64k():
-    """The 64k-token KV fetch (8 GiB) into the x-packed GPU layout, in the configuration the benchmark
-    times, then the offload of every fetched block into the host slots in reverse order (a poisoned
-    pool). For 512 sampled logical blocks every GPU block is checked against the oracle in every
-    layer, and the offloaded slot must hold the block's original bytes; every untouched GPU block
-    stays poison."""
+@pytest.mark.parametrize("gpu_layout", ["xpacked", "hnd"])
+def test_kv_xpacked_fetch_offload_64k(gpu_layout):
+    """The 64k-token KV fetch (8 GiB) into the x-packed or head-major GPU layout, in the
+    configuration the benchmark times, then the offload of every fetched block into the host slots
+    in reverse order (a poisoned pool). For 512 sampled logical blocks every GPU block is checked
+    against the oracle in every layer, and the offloaded slot must hold the block's original bytes;
+    every untouched GPU block stays poison."""
+    LAY, GL = ((XP, mma.MMA_KV_LAYOUT_XPACKED) if gpu_layout == "xpacked"
+               else (okv.LAYOUT_HND, mma.MMA_KV_LAYOUT_HND))
     s = W.KV64K
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     geom = _geom(s)
@@ -417,7 +532,7 @@ def test_kv_xpacked_fetch_offload_64k():
         _fill_pool_c3(pool.array, s, hs)
         layers = _layers(s, W.GPU_POISON)
         lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
-                            s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED)
+                            s.host_num_slots, GL)
         mma.mma_kv_fetch(lay, pool, layers, hs, gb)
         torch.cuda.synchronize()
         mma.mma_synchronize()
@@ -427,10 +542,10 @@ def test_kv_xpacked_fetch_offload_64k():
             got = to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
             for i in sample:
                 for k in (0, 1):
-                    want = okv.piece_to_block(pool_v[hs[i], l, k], k, XP, geom)
+                    want = okv.piece_to_block(pool_v[hs[i], l, k], k, LAY, geom)
                     assert np.array_equal(got[k, gb[i]], want), (l, int(i), k)
             assert np.all(got[:, untouched] == W.GPU_POISON), l
-        log("  x-packed fetch verified on the sample")
+        log(f"  {gpu_layout} fetch verified on the sample")
         dest = hs[::-1].copy()
         pool.array[:] = W.HOST_FREE_POISON
         mma.mma_kv_offload(lay, pool, layers, gb, dest)

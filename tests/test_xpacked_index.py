@@ -1,4 +1,4 @@
-"""The x-packed KV transform's index maps, emulated on the CPU (no GPU).
+"""The x-packed and head-major KV transforms' index maps, emulated on the CPU (no GPU).
 
 tests/cpp/xpacked_emu.cpp runs one wave of the dummy-task kernel's x-packed
 transform over the kernel's own index maps (mma_xpacked.h): it checks that every
@@ -39,6 +39,10 @@ def emu(tmp_path_factory):
     f = lib.emu_xpacked
     f.restype = ctypes.c_int
     f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int] + [ctypes.c_uint32] * 5
+    h = lib.emu_hnd
+    h.restype = ctypes.c_int
+    h.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int] + [ctypes.c_uint32] * 3
+    f.hnd = h
     return f
 
 
@@ -76,3 +80,22 @@ def test_emulator_catches_a_wrong_map(emu):
     piece = np.zeros(B * H * D * E, np.uint8)
     got = np.zeros_like(piece)
     assert emu(piece.ctypes.data, got.ctypes.data, 1, 1, B, H, D * E, E, 1024) != 0
+
+
+HND_SHAPES = [(16, 8, 128, 2), (16, 8, 64, 2), (16, 1, 128, 2), (1, 8, 128, 2), (32, 8, 128, 1), (8, 3, 16, 2),
+              (2, 5, 8, 8), (64, 2, 128, 1), (3, 7, 16, 4)]
+
+
+@pytest.mark.parametrize("shape", HND_SHAPES)
+def test_hnd_index_map_matches_oracle(emu, shape):
+    """The head-major map: every access inside the piece, every byte written once, and the
+    result equal to the oracle's, in both directions."""
+    B, H, D, E = shape
+    r = np.random.default_rng(sum(shape) + 1)
+    piece = np.ascontiguousarray(r.integers(0, 256, B * H * D * E, dtype=np.uint8))
+    blk = np.zeros_like(piece)
+    assert emu.hnd(piece.ctypes.data, blk.ctypes.data, 1, B, H, D * E) == 0
+    assert np.array_equal(blk, okv.piece_to_block(piece, 0, okv.LAYOUT_HND, (B, H, D, E)))
+    back = np.zeros_like(piece)
+    assert emu.hnd(blk.ctypes.data, back.ctypes.data, 0, B, H, D * E) == 0
+    assert np.array_equal(back, piece)
