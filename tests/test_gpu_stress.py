@@ -3,7 +3,7 @@
 One schedule of ~150 operations is drawn from a seed: single copies and tensor lists in both
 directions (1 byte to 12 MiB, odd offsets, self-contained launches, whole-CU transfers, early
 starts on idle streams, multipath transfers with merged copy-engine commands) and paged-KV
-fetches and offloads in both GPU block layouts, issued in random order over four streams
+fetches and offloads in all three GPU block layouts, issued in random order over four streams
 (including the legacy default stream). Every operation writes its own destination range and
 reads a read-only source, so the final state is unique whatever the interleaving; each
 destination (and the poison around it) is compared byte-exact with oracle.copy / oracle.kv.
@@ -106,9 +106,9 @@ def test_random_mixed_schedule(seed, control):
                 expect += [("h" if d2h else "d", do, so, n) for do, so, n in items]
             else:
                 s = KV_SHAPES[int(r.integers(len(KV_SHAPES)))]
-                xp = bool(r.integers(2))
+                xp = int(r.integers(3))  # GPU block layout: 0 piece, 1 x-packed, 2 head-major
                 lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
-                                    s.host_num_slots, mma.MMA_KV_LAYOUT_XPACKED if xp else 0)
+                                    s.host_num_slots, xp)
                 pool_np = r.integers(0, 256, (s.host_num_slots, s.slot_bytes), dtype=np.uint8)
                 pool = mma.PinnedBuffer(pool_np.size)
                 pool.array[:] = pool_np.reshape(-1)
@@ -143,7 +143,7 @@ def test_random_mixed_schedule(seed, control):
             assert np.all(got[side][~covered[side]] == POISON), side
         for s, xp, d2h, pool, pool_np, layers, layers_np, a, b in kv_jobs:
             geom = (s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes)
-            layout = okv.LAYOUT_XPACKED if xp else okv.LAYOUT_PIECE
+            layout = (okv.LAYOUT_PIECE, okv.LAYOUT_XPACKED, okv.LAYOUT_HND)[xp]
             if d2h:
                 want = okv.kv_offload(pool_np, layers_np, b, a, layout, geom)
                 assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
