@@ -418,11 +418,27 @@ class Engine {
   bool has_sdma() const { return !paths_.empty(); }
   uint64_t stage_bytes() const { return stage_bytes_; }
 
-  // A linear transfer that the CU path takes whole (see prepare): it runs as
-  // one self-contained launch and needs a light slot, not a record.
+  // A transfer that the CU path takes whole (see prepare): it runs as one
+  // self-contained launch and needs a light slot, not a record.
   bool whole_eligible(const Transfer* x, uint64_t payload_bytes, bool kv) const {
-    return !kv && cu_enabled() && !cfg_.static_split && !x->tasks.empty() && x->tasks.size() <= kPrefill &&
-           payload_bytes <= cfg_.whole[dir_];
+    if (!cu_enabled() || cfg_.static_split || x->tasks.empty() || payload_bytes > cfg_.whole[dir_]) return false;
+    if (kv) return !x->pool_dev && whole_kv_per(x) != 0;
+    return x->tasks.size() <= kPrefill;
+  }
+
+  // Pieces per CU entry of a whole KV transfer: the engine thread's entry size,
+  // grown until all of the transfer's entries fit the launch arguments (one
+  // entry never spans two micro-tasks, i.e. two blocks); 0 if they cannot.
+  uint64_t whole_kv_per(const Transfer* x) const {
+    uint64_t per = std::max<uint64_t>(1, cfg_.sub / x->piece), biggest = 0;
+    for (const Task& t : x->tasks) biggest = std::max(biggest, t.bytes);
+    for (;;) {
+      uint64_t e = 0;
+      for (const Task& t : x->tasks) e += (t.bytes + per - 1) / per;
+      if (e <= kPrefill) return per;
+      if (per >= biggest) return 0;
+      per = std::min(biggest, 2 * per);
+    }
   }
 
   // Takes a light slot for a whole transfer, else a record; blocks until one is
@@ -558,7 +574,10 @@ class Engine {
     // the prefilled entries is still cut into 16 KiB steps, so that more waves
     // share it.
     x->sub = cfg_.sub;
-    if (whole_eligible(x, payload_bytes, kv != nullptr)) {
+    if (kv && x->light >= 0) {  // a whole KV transfer (acquire gave it a light slot)
+      x->kv_per = whole_kv_per(x);
+      x->whole = true;
+    } else if (!kv && whole_eligible(x, payload_bytes, false)) {
       const uint64_t per_task = kPrefill / x->tasks.size();
       uint64_t biggest = 0;
       for (const Task& t : x->tasks) biggest = std::max(biggest, t.bytes);
@@ -574,11 +593,12 @@ class Engine {
                              kv && kv->layout != kKvLayoutPiece);
     x->waves = grid * kWavesPerWG;
     prefill(x);
-    const uint32_t n_pre = kv ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
+    const uint32_t n_pre =
+        kv && !x->whole ? 0u : static_cast<uint32_t>(std::min<uint64_t>(x->pushed, kPrefill));
     // Everything fits the launch: all tasks were claimed by the CU prefill (so no
     // copy engine can take part) and all their entries are in the kernel args.
     // One wave per entry; the engine treats the transfer as started.
-    x->self_contained = !kv && x->n_claimed == x->tasks.size() && x->pushed == n_pre;
+    x->self_contained = (!kv || x->whole) && x->n_claimed == x->tasks.size() && x->pushed == n_pre;
     if (x->self_contained) {
       grid = (n_pre + kWavesPerWG - 1) / kWavesPerWG;
       x->waves = grid * kWavesPerWG;
@@ -892,9 +912,10 @@ class Engine {
     if ((kind & kEntryKindMask) == kEntryCopy) {
       per = x->sub;
     } else {
-      // A wave's ring entry carries cu_sub_bytes of pieces across PCIe; for an
+      // A wave's ring entry carries cu_sub_bytes of pieces across PCIe (more for
+      // a whole transfer, whose entries must fit the launch); for an
       // HBM-resident pool (latency ~1 us instead of several) a whole micro-task.
-      per = x->pool_dev ? count : std::max<uint64_t>(1, cfg_.sub / x->piece);
+      per = x->kv_per ? x->kv_per : x->pool_dev ? count : std::max<uint64_t>(1, cfg_.sub / x->piece);
     }
     const uint64_t ne = (count + per - 1) / per;
     // Keep one slot per wave free for the end markers written at close.

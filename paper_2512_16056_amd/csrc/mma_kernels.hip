@@ -336,6 +336,54 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
   lds_u8* wave_lds = (lds_u8*)(mma_dyn_lds) + (threadIdx.x / kWave) * a.kv_lds_wave;
   __syncthreads();
 
+  // One ring entry: words a, b and count | kind_p0 (see CuEntry). One copy site
+  // for every kind (a linear entry is a single "piece"), so the copy loop is
+  // instantiated once.
+  auto run_entry = [&](uint64_t w1, uint64_t w2, uint64_t w3) {
+    const uint32_t count = static_cast<uint32_t>(w3);
+    const uint32_t kind = static_cast<uint32_t>(w3 >> 32) & kEntryKindMask;
+    const uint32_t p0 = static_cast<uint32_t>(w3 >> 40);
+    // Data landed by an SDMA engine during this kernel: drop any stale copy of
+    // it from this CU's vector L1 (and non-coherent L2 lines) before reading.
+    if ((w3 >> 32) & kEntryAcquire) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+    const bool paged = kind != kEntryCopy;
+    const uint32_t npieces = paged ? count : 1u;
+    for (uint32_t j = 0; j < npieces; ++j) {
+      const uint8_t* src = reinterpret_cast<const uint8_t*>(w1);
+      uint8_t* dst = reinterpret_cast<uint8_t*>(w2);
+      uint64_t n = count;
+      if (paged) {
+        const uint32_t p = p0 + j;
+        uint8_t* pg = reinterpret_cast<uint8_t*>(s_layer[p >> 1]) + (p & 1u) * kstride + w2 * piece;
+        uint8_t* contig = reinterpret_cast<uint8_t*>(w1) + j * piece;
+        src = kind == kEntryToPaged ? contig : pg;
+        dst = kind == kEntryToPaged ? pg : contig;
+        n = piece;
+        if constexpr (kXE == kXeHnd) {
+          hnd_piece(src, dst, kind == kEntryToPaged, xg, lane);
+          continue;
+        } else if constexpr (kXE != 0) {
+          xpacked_piece<kXE>(src, dst, kind == kEntryToPaged, p & 1u, xg, wave_lds, lane);
+          continue;
+        }
+      }
+      wave_copy(src, dst, n, lane);
+    }
+  };
+
+  // A self-contained launch of a whole KV transfer (linear ones use
+  // mma_whole_kernel): wave w copies entry w of the arguments and writes its
+  // done tag -- no start signal, record, ring or wait.
+  if (a.self_contained) {
+    const uint32_t w = blockIdx.x * kWavesPerWG + threadIdx.x / kWave;
+    if (w < a.n_pre) {
+      run_entry(a.pre[w][0], a.pre[w][1], a.pre[w][2]);
+      if (a.release_each) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+      if (lane == 0) st_sys(&a.done[w], make_tag(a.seq, w));
+    }
+    return;
+  }
+
   // 1. start signal (stream -> engine). Work that precedes this kernel in
   // stream order is complete and visible (dispatch acquire/release).
   if (lane == 0) {
@@ -398,39 +446,9 @@ __device__ __forceinline__ void transfer_body(const KernelArgs& a) {
       if (state == 3) timed_out = 1;
       break;
     }
-    const uint32_t count = static_cast<uint32_t>(w3);
-    const uint32_t kind = static_cast<uint32_t>(w3 >> 32) & kEntryKindMask;
-    if (kind == kEntryEnd) break;  // the ring is closed and this ticket is past its end
-    const uint32_t p0 = static_cast<uint32_t>(w3 >> 40);
-    // Data landed by an SDMA engine during this kernel: drop any stale copy of
-    // it from this CU's vector L1 (and non-coherent L2 lines) before reading.
-    if ((w3 >> 32) & kEntryAcquire) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
-
-    // One copy site for every kind (a linear entry is a single "piece"), so the
-    // copy loop is instantiated once.
-    const bool paged = kind != kEntryCopy;
-    const uint32_t npieces = paged ? count : 1u;
-    for (uint32_t j = 0; j < npieces; ++j) {
-      const uint8_t* src = reinterpret_cast<const uint8_t*>(w1);
-      uint8_t* dst = reinterpret_cast<uint8_t*>(w2);
-      uint64_t n = count;
-      if (paged) {
-        const uint32_t p = p0 + j;
-        uint8_t* pg = reinterpret_cast<uint8_t*>(s_layer[p >> 1]) + (p & 1u) * kstride + w2 * piece;
-        uint8_t* contig = reinterpret_cast<uint8_t*>(w1) + j * piece;
-        src = kind == kEntryToPaged ? contig : pg;
-        dst = kind == kEntryToPaged ? pg : contig;
-        n = piece;
-        if constexpr (kXE == kXeHnd) {
-          hnd_piece(src, dst, kind == kEntryToPaged, xg, lane);
-          continue;
-        } else if constexpr (kXE != 0) {
-          xpacked_piece<kXE>(src, dst, kind == kEntryToPaged, p & 1u, xg, wave_lds, lane);
-          continue;
-        }
-      }
-      wave_copy(src, dst, n, lane);
-    }
+    if ((static_cast<uint32_t>(w3 >> 32) & kEntryKindMask) == kEntryEnd)
+      break;  // the ring is closed and this ticket is past its end
+    run_entry(w1, w2, w3);
     if (a.release_each) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
     if (lane == 0) {
       st_sys(&a.done[x % kRingSize], expect);
@@ -556,7 +574,7 @@ hipError_t launch_whole(const KernelArgs& args, uint32_t grid, hipStream_t strea
 }
 
 hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t stream) {
-  if (args.self_contained) {
+  if (args.self_contained && args.kv_layers == 0) {  // linear: the lean kernel; KV: below, by layout
     if (args.n_pre <= 4) return launch_whole<4>(args, grid, stream);
     if (args.n_pre <= 16) return launch_whole<16>(args, grid, stream);
     return launch_whole<kPrefill>(args, grid, stream);

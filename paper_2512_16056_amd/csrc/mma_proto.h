@@ -123,7 +123,8 @@ struct KernelArgs {
   uint32_t kv_layers;
   uint32_t n_pre;           // tickets [0, n_pre) are also given below: no first poll for them
   uint32_t self_contained;  // 1: the n_pre entries are the whole transfer and no copy engine takes
-                            // part: launched as mma_whole_kernel with WholeArgs instead
+                            // part: wave w runs entry w and writes done[w]; a linear one is
+                            // launched as mma_whole_kernel with WholeArgs instead
   // GPU block layout of paged-KV pieces: kKvLayoutPiece (as in host memory) or
   // kKvLayoutXPacked, whose geometry follows (a row is one token's head_dim
   // elements of one head: head_dim * elem bytes).

@@ -678,6 +678,70 @@ void whole_transfers_on_cu() {
               "engine thread\n");
 }
 
+// Small paged-KV fetches and offloads taken whole by the CU path: one
+// self-contained launch each (entries in the arguments), exact, no copy-engine
+// command, no engine-thread work; a larger one still uses every path.
+void whole_kv_transfers() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.chunk = 8 * 1024;  // 4 pieces per micro-task
+  s.cfg.whole[0] = s.cfg.whole[1] = 64 * 1024;
+  Harness h(s);
+  FakeStream st;
+  const uint32_t L = 2, ppb = 2 * L, slots = 40, nb = 48;
+  const uint64_t piece = 2048, slot_bytes = piece * ppb;  // 8 KiB slots
+  std::vector<uint8_t> pool = random_bytes(slots * slot_bytes, 51);
+  std::vector<std::vector<uint8_t>> layers(L, std::vector<uint8_t>(2 * nb * piece, 0xA5));
+  KvGeom kv;
+  kv.piece = piece;
+  kv.kstride = piece * nb;
+  kv.layers = L;
+  for (uint32_t l = 0; l < L; ++l) kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l].data());
+  const uint64_t host = reinterpret_cast<uint64_t>(pool.data());
+  for (int n : {1, 3, 8, 20}) {  // 8, 24, 64 and 160 KiB: the last is above the whole-transfer limit
+    std::vector<int32_t> hs(n), gb(n);
+    for (int i = 0; i < n; ++i) {
+      hs[i] = (7 * i + 3) % static_cast<int>(slots);
+      gb[i] = (5 * i + 1) % static_cast<int>(nb);
+    }
+    const uint64_t cmds = h.stats().sdma_commands.load();
+    h.submit(make_kv_transfer(MMA_H2D, piece, ppb, host, host, false, true, hs.data(), gb.data(), n, h.cfg()),
+             n * slot_bytes, st, &kv);
+    st.synchronize();
+    CHECK(h.sync(), "sync");
+    bool ok = true;
+    for (int i = 0; i < n; ++i)
+      for (uint32_t l = 0; l < L; ++l)
+        for (uint32_t k = 0; k < 2; ++k)
+          ok &= std::memcmp(layers[l].data() + (k * nb + gb[i]) * piece,
+                            pool.data() + hs[i] * slot_bytes + (2 * l + k) * piece, piece) == 0;
+    CHECK(ok, "whole KV fetch of %d blocks differs", n);
+    const bool whole = n * slot_bytes <= 64 * 1024;
+    if (whole) CHECK(h.stats().sdma_commands.load() == cmds, "whole KV fetch of %d blocks used a copy engine", n);
+    if (!whole) CHECK(h.stats().sdma_commands.load() > cmds, "a KV fetch above the limit used no copy engine");
+    // offload the same blocks into other slots
+    std::vector<int32_t> dest(n);
+    for (int i = 0; i < n; ++i) dest[i] = (hs[i] + 1) % static_cast<int>(slots);
+    std::vector<bool> taken(slots, false);
+    bool distinct = true;
+    for (int i = 0; i < n; ++i) distinct &= !taken[dest[i]], taken[dest[i]] = true;
+    if (!distinct) continue;
+    auto want = pool;
+    for (int j = 0; j < n; ++j)
+      for (uint32_t l = 0; l < L; ++l)
+        for (uint32_t k = 0; k < 2; ++k)
+          std::memcpy(want.data() + dest[j] * slot_bytes + (2 * l + k) * piece,
+                      layers[l].data() + (k * nb + gb[j]) * piece, piece);
+    h.submit(make_kv_transfer(MMA_D2H, piece, ppb, host, host, false, true, dest.data(), gb.data(), n, h.cfg()),
+             n * slot_bytes, st, &kv);
+    st.synchronize();
+    CHECK(h.sync(), "sync");
+    CHECK(pool == want, "whole KV offload of %d blocks: pool differs", n);
+  }
+  CHECK(h.stats().failed.load() == 0, "whole KV: failed transfers");
+  std::printf("ok   small KV fetches and offloads taken whole by the CU path; larger ones use every path\n");
+}
+
 // A deep queue of whole transfers on a stream that cannot progress yet: they
 // take light slots, so submission does not wait for the stream (records alone
 // would run out after 64), and every transfer lands once the stream runs.
@@ -1140,6 +1204,7 @@ int main(int argc, char** argv) {
     kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging, idle-stream early start", true);
     unlaunched_transfer_drains();
     whole_transfers_on_cu();
+    whole_kv_transfers();
     deep_queue_does_not_block();
     submit_failures_rerouted();
     kv_submit_failures_rerouted();

@@ -450,6 +450,58 @@ def test_kv_hnd_rejects_unsupported_geometry():
         torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("gpu_layout", [0, 1, 2])
+def test_kv_whole_transfers(gpu_layout):
+    """Default size limits: KV fetches of up to 24 MiB (12 blocks of the 64k workload's shape) and
+    offloads of up to 8 MiB (4 blocks) are taken whole by the CU path -- one self-contained launch,
+    no copy engine -- and larger ones use every path; all three GPU block layouts, every byte
+    against the oracle."""
+    LAYOUTS = (okv.LAYOUT_PIECE, okv.LAYOUT_XPACKED, okv.LAYOUT_HND)
+    base = W.KV64K
+    with session("both", cu_whole_bytes=0, cu_whole_bytes_d2h=0):  # 0: the default limits
+        for n in (1, 4, 5, 12, 13):
+            s = W.KVShape(layers=base.layers, block_tokens=base.block_tokens, kv_heads=base.kv_heads,
+                          head_dim=base.head_dim, elem_bytes=base.elem_bytes, gpu_num_blocks=20,
+                          host_num_slots=16, n_blocks=n)
+            log(f"whole kv layout={gpu_layout} blocks={n}")
+            geom = _geom(s)
+            lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                                s.host_num_slots, gpu_layout)
+            r = np.random.default_rng(60 + n)
+            hs = r.permutation(s.host_num_slots)[:n].astype(np.int32)
+            gb = r.permutation(s.gpu_num_blocks)[:n].astype(np.int32)
+            pool = _pool(s, 70 + n)
+            layers = _layers(s, W.GPU_POISON)
+            before = _layer_views(s, layers)
+            mma.mma_synchronize()
+            st0 = mma.mma_get_stats()
+            mma.mma_kv_fetch(lay, pool, layers, hs, gb)
+            torch.cuda.synchronize()
+            mma.mma_synchronize()
+            st1 = mma.mma_get_stats()
+            pool_v = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+            for l in range(s.layers):
+                want = okv.kv_fetch_layer(pool_v, before[l], l, s.layers, hs, gb, LAYOUTS[gpu_layout], geom)
+                got = to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
+                assert np.array_equal(got, want), (n, l)
+            eng = sum(st1["path_bytes"][:16]) - sum(st0["path_bytes"][:16])
+            assert (eng == 0) == (n <= 12), (n, eng)
+            dest = np.roll(hs, 1).astype(np.int32)
+            views = _layer_views(s, layers)
+            pool_before = pool.array.copy()
+            mma.mma_kv_offload(lay, pool, layers, gb, dest)
+            torch.cuda.synchronize()
+            mma.mma_synchronize()
+            st2 = mma.mma_get_stats()
+            want = okv.kv_offload(pool_before.reshape(s.host_num_slots, -1), views, gb, dest, LAYOUTS[gpu_layout],
+                                  geom)
+            assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want), n
+            eng = sum(st2["path_bytes"][:16]) - sum(st1["path_bytes"][:16])
+            assert (eng == 0) == (n <= 4), (n, eng)
+            assert st2["failed_transfers"] == 0
+            pool.free()
+
+
 def _fill_pool_c3(pool: np.ndarray, s: W.KVShape, hs: np.ndarray):
     v = pool.reshape(s.host_num_slots, s.slot_bytes)
     for i in range(s.n_blocks):
