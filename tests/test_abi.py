@@ -146,3 +146,16 @@ def test_interposer_exports_and_links_no_runtime():
         assert re.search(rf"\bT {name}$", syms, flags=re.M), name
     needed = subprocess.run(["readelf", "-d", lib], capture_output=True, text=True).stdout
     assert "libamdhip64" not in needed and "libmma.so" not in needed
+
+
+def test_layer_table_addresses_and_reuse():
+    """The KV calls' layer array: one address per layer in order, and a table built once is
+    passed through unchanged (no per-call rebuild)."""
+    import ctypes
+    import torch
+    ts = [torch.empty(64, dtype=torch.uint8) for _ in range(5)]
+    lt = mma.layer_table(ts)
+    assert [lt[i] for i in range(5)] == [t.data_ptr() for t in ts]
+    assert mma.layer_table(lt) is lt
+    assert list(mma.layer_table([7, 0x1000])) == [7, 0x1000]
+    assert isinstance(mma.layer_table([]), ctypes.Array)
