@@ -133,6 +133,14 @@ struct Transfer {
   uint64_t pushed = 0, done_upto = 0;
   uint32_t waves = 0;          // waves of the dummy-task kernel
   bool pool_dev = false;       // KV pool in device memory: HBM gather/scatter, one entry per task
+  // HBM pool launch: the transfer is one launch of the pool kernel, which reads
+  // the block table (pool slot | GPU block << 32 per block) from the engine's
+  // table arena, segments [tab_seg, tab_seg + tab_nseg).
+  bool pool_launch = false;
+  uint64_t pool_base = 0;
+  std::vector<uint64_t> pool_pairs;
+  int32_t tab_seg = -1;
+  uint32_t tab_nseg = 0;
   bool self_contained = false; // whole transfer in the kernel args; the kernel does not wait on the host
   bool whole = false;          // the CU path claims every micro-task at prefill
   // Submitted on a stream with nothing pending: the engine may start the copy
@@ -301,6 +309,12 @@ class Engine {
     memset(light_, 0, sizeof(uint64_t) * kPrefill * kLightSlots);
     for (uint32_t i = 0; i < kLightSlots; ++i) free_light_.push_back(i);
     light_ring_.reset(new CuEntry[kPrefill + kRingSize]);
+    if ((rc = be_->alloc_records(sizeof(uint64_t) * kPoolTabEntries, &h, &d)) != MMA_OK) return rc;
+    pool_tab_ = static_cast<uint64_t*>(h);
+    pool_tab_dev_ = static_cast<uint64_t*>(d);
+    if ((rc = be_->alloc_device_state(sizeof(uint32_t) * kLightSlots, &d)) != MMA_OK) return rc;
+    pool_ctr_ = static_cast<uint32_t*>(d);
+    seg_used_.assign(kPoolTabEntries / kPoolTabSeg, 0);
     stage_bytes_ = stage_bytes;
     uint8_t* stage = static_cast<uint8_t*>(staging_base);
     for (int eng = 0; eng < MMA_MAX_SDMA; ++eng) {
@@ -390,6 +404,8 @@ class Engine {
       ds_ = nullptr;
       recs_ = nullptr;
       light_ = nullptr;
+      pool_tab_ = nullptr;
+      pool_ctr_ = nullptr;
       return;
     }
     for (auto& s : slots_) be_->signal_destroy(s.sig);
@@ -400,9 +416,13 @@ class Engine {
     if (ds_) be_->free_device_state(ds_);
     if (recs_) be_->free_records(recs_);
     if (light_) be_->free_records(light_);
+    if (pool_tab_) be_->free_records(pool_tab_);
+    if (pool_ctr_) be_->free_device_state(pool_ctr_);
     ds_ = nullptr;
     recs_ = nullptr;
     light_ = nullptr;
+    pool_tab_ = nullptr;
+    pool_ctr_ = nullptr;
   }
 
   pthread_t native_handle() { return thread_.native_handle(); }
@@ -446,11 +466,17 @@ class Engine {
   // by the engine thread. Light slots outnumber records 64 to 1, so a deep
   // queue of small transfers on a stream does not wait for the GPU.
   bool acquire(Transfer* x, uint64_t payload_bytes, bool kv, uint64_t timeout_ms) {
-    const bool light = whole_eligible(x, payload_bytes, kv);
+    bool light = whole_eligible(x, payload_bytes, kv);
     reap();
     std::unique_lock<std::mutex> lk(mu_);
+    // An HBM pool launch needs room for its table in the arena; without it the
+    // transfer takes the ring path like any other.
+    if (x->pool_launch) light = x->pool_launch = take_tab(x);
     std::deque<uint32_t>& pool = light ? free_light_ : free_recs_;
-    if (pool.empty() && !wait_for_pool(lk, pool, timeout_ms)) return false;
+    if (pool.empty() && !wait_for_pool(lk, pool, timeout_ms)) {
+      give_tab(x);
+      return false;
+    }
     const uint32_t i = pool.front();
     pool.pop_front();
     lk.unlock();
@@ -488,11 +514,36 @@ class Engine {
 
   void release_unused(Transfer* x) {
     std::lock_guard<std::mutex> g(mu_);
+    give_tab(x);
     if (x->light >= 0)
       free_light_.push_back(static_cast<uint32_t>(x->light));
     else
       free_recs_.push_back(x->rec_idx);
     cv_done_.notify_all();
+  }
+  // Table arena segments for an HBM pool launch (mu_ held): the first run of
+  // free segments that holds the table, or false if there is none.
+  bool take_tab(Transfer* x) {
+    if (!pool_tab_) return false;
+    const uint64_t need = (x->pool_pairs.size() + kPoolTabSeg - 1) / kPoolTabSeg;
+    if (need == 0 || need > seg_used_.size()) return false;
+    for (size_t i = 0, run = 0; i < seg_used_.size(); ++i) {
+      run = seg_used_[i] ? 0 : run + 1;
+      if (run == need) {
+        const size_t first = i + 1 - need;
+        std::fill(seg_used_.begin() + static_cast<long>(first), seg_used_.begin() + static_cast<long>(i) + 1, 1);
+        x->tab_seg = static_cast<int32_t>(first);
+        x->tab_nseg = static_cast<uint32_t>(need);
+        return true;
+      }
+    }
+    return false;
+  }
+  void give_tab(Transfer* x) {  // mu_ held
+    if (x->tab_seg < 0) return;
+    std::fill(seg_used_.begin() + x->tab_seg, seg_used_.begin() + x->tab_seg + x->tab_nseg, 0);
+    x->tab_seg = -1;
+    x->tab_nseg = 0;
   }
   Record* rec_dev(uint32_t i) const { return recs_dev_ + i; }
   DevState* ds(uint32_t i) const { return ds_ + i; }
@@ -552,6 +603,7 @@ class Engine {
       r->h.status = 0;
       __atomic_thread_fence(__ATOMIC_RELEASE);
     }
+    if (x->pool_launch) return prepare_pool(x, kv, a);
     if (cfg_.static_split && has_sdma() && x->sdma_ok) {
       for (size_t i = 0; i < x->tasks.size(); ++i) {
         uint32_t& f = x->tasks[i].flags;
@@ -611,6 +663,38 @@ class Engine {
     }
     fill_args(x, kv, n_pre, grid, watchdog_ticks, a);
     return grid;
+  }
+
+  // An HBM pool launch: the table goes to the arena, the grid is sized to
+  // the spans (at least one per wave, at most kPoolMaxWorkgroups workgroups),
+  // and the kernel is the transfer's only copy engine. Returns the grid.
+  uint32_t prepare_pool(Transfer* x, const KvGeom* kv, KernelArgs& a) {
+    const uint64_t nblk = x->pool_pairs.size();
+    memcpy(pool_tab_ + static_cast<uint64_t>(x->tab_seg) * kPoolTabSeg, x->pool_pairs.data(),
+           nblk * sizeof(uint64_t));
+    __atomic_thread_fence(__ATOMIC_RELEASE);
+    std::fill(x->claimed.begin(), x->claimed.end(), 1);
+    x->n_claimed = x->tasks.size();
+    x->pushed = 1;
+    x->whole = x->self_contained = true;
+    x->started = x->closed = x->completed = true;
+    x->t_started = x->t_complete = x->t_submit;
+    const uint64_t spans = (kv->piece + kPoolSpan - 1) / kPoolSpan;
+    const uint64_t units = nblk * 2 * kv->layers * spans;
+    uint64_t grid = std::min<uint64_t>(kPoolMaxWorkgroups, (units + kWavesPerWG - 1) / kWavesPerWG);
+    const uint64_t per_wg = (units + grid - 1) / grid;
+    grid = (units + per_wg - 1) / per_wg;
+    x->waves = static_cast<uint32_t>(grid) * kWavesPerWG;
+    fill_args(x, kv, 0, static_cast<uint32_t>(grid), 0, a);
+    a.self_contained = 1;
+    a.pool_tab = pool_tab_dev_ + static_cast<uint64_t>(x->tab_seg) * kPoolTabSeg;
+    a.pool_ctr = pool_ctr_ + x->light;
+    a.pool_base = x->pool_base;
+    a.pool_units = units;
+    a.pool_per_wg = per_wg;
+    a.pool_spans = static_cast<uint32_t>(spans);
+    a.pool_to_paged = x->kind == Kind::kKvFetch ? 1u : 0u;
+    return static_cast<uint32_t>(grid);
   }
 
   // Kernel arguments common to both control modes.
@@ -1034,6 +1118,7 @@ class Engine {
     }
     {
       std::lock_guard<std::mutex> g(mu_);
+      give_tab(x);
       if (x->light >= 0)
         free_light_.push_back(static_cast<uint32_t>(x->light));
       else
@@ -1587,6 +1672,10 @@ class Engine {
   uint64_t* light_ = nullptr;      // light slots' done tags, kPrefill per slot (host address)
   uint64_t* light_dev_ = nullptr;  // the same, device address
   std::unique_ptr<CuEntry[]> light_ring_;  // scratch ring: light transfers' entries go to the kernel args
+  uint64_t* pool_tab_ = nullptr;      // HBM pool launches' table arena (host address)
+  uint64_t* pool_tab_dev_ = nullptr;  // the same, device address
+  uint32_t* pool_ctr_ = nullptr;      // per light slot: finished workgroups of its pool launch (device)
+  std::vector<uint8_t> seg_used_;     // arena segments in use (mu_)
   DevState* ds_ = nullptr;
   std::vector<SdmaSlot> slots_;
   std::vector<SdmaPath> paths_;
@@ -1656,6 +1745,12 @@ inline std::unique_ptr<Transfer> make_kv_transfer(int dir, uint64_t piece, uint3
   x->piece = piece;
   x->pool_dev = pool_dev;
   x->sdma_ok = sdma_ok;
+  if (pool_dev) {
+    x->pool_base = host;
+    x->pool_pairs.resize(n);
+    for (uint64_t i = 0; i < n; ++i)
+      x->pool_pairs[i] = static_cast<uint32_t>(host_slots[i]) | static_cast<uint64_t>(gpu_blocks[i]) << 32;
+  }
   x->tasks.reserve(plan.size());
   const uint64_t slot_bytes = piece * ppb;
   for (const PlanItem& p : plan) {

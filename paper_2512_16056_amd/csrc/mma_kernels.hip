@@ -524,6 +524,82 @@ __global__ __launch_bounds__(kBlock) void mma_whole_kernel(WholeArgs<N> a) {
 
 __global__ __launch_bounds__(kBlock) void mma_transfer_hnd_kernel(KernelArgs a) { transfer_body<kXeHnd>(a); }
 
+// One span of an HBM pool launch: n <= kPoolSpan bytes. A full, 16-byte
+// aligned span is read whole into registers before the first store, with
+// nontemporal loads and stores (every byte is moved once, so caching it would
+// only evict other data); a piece's shorter last span and misaligned spans
+// take plain loops.
+constexpr uint32_t kPoolVec = kPoolSpan / (kWave * 16);
+__device__ __forceinline__ void pool_span(const uint8_t* src, uint8_t* dst, uint32_t n, uint32_t lane) {
+  const uintptr_t mis = (reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15u;
+  if (mis == 0 && n == kPoolSpan) {
+    const gu4* s = (const gu4*)(src) + lane;
+    gu4* d = (gu4*)(dst) + lane;
+    u32x4 v[kPoolVec];
+#pragma unroll
+    for (uint32_t i = 0; i < kPoolVec; ++i) v[i] = __builtin_nontemporal_load(s + i * kWave);
+#pragma unroll
+    for (uint32_t i = 0; i < kPoolVec; ++i) __builtin_nontemporal_store(v[i], d + i * kWave);
+    return;
+  }
+  if (mis == 0) {
+    const uint32_t n16 = n >> 4;
+    const gu4* s = (const gu4*)(src);
+    gu4* d = (gu4*)(dst);
+    for (uint32_t i = lane; i < n16; i += kWave) d[i] = s[i];
+    for (uint32_t i = (n16 << 4) + lane; i < n; i += kWave) dst[i] = src[i];
+    return;
+  }
+  for (uint32_t i = lane; i < n; i += kWave) dst[i] = src[i];
+}
+
+// A paged-KV transfer between a pool in this GPU's memory and the paged layer
+// tensors (piece layout): HBM-bound, so the launch is sized to the bytes, up
+// to kPoolMaxWorkgroups workgroups, with no ring and no host round trip. A
+// workgroup's spans are contiguous and its waves interleave over them, so a
+// wave meets one or two blocks and reads each one's table entry once. The
+// counter only orders the done tag after every workgroup has finished with its
+// table entries: the data itself becomes visible to later work through the
+// stream, when the kernel ends, as for any kernel (a device-wide release per
+// workgroup would write back the L2 of its XCD each time).
+__global__ __launch_bounds__(kBlock) void mma_kv_pool_kernel(PoolArgs a) {
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const uint64_t u0 = static_cast<uint64_t>(blockIdx.x) * a.per_wg;
+  const uint64_t u1 = min(a.units, u0 + a.per_wg);
+  const uint64_t per_blk = static_cast<uint64_t>(a.ppb) * a.spans;
+  uint64_t cur = ~0ull, pooled = 0, paged_off = 0;
+  for (uint64_t u = u0 + wave; u < u1; u += kWavesPerWG) {
+    const uint64_t i = u / per_blk;
+    const uint32_t r = static_cast<uint32_t>(u - i * per_blk);
+    const uint32_t p = r / a.spans;
+    const uint32_t sp = r - p * a.spans;
+    if (i != cur) {
+      cur = i;
+      const uint64_t e = ld_sys(&a.tab[i]);
+      pooled = a.pool + (e & 0xffffffffull) * a.slot_bytes;
+      paged_off = (e >> 32) * a.piece;
+    }
+    const uint64_t off = static_cast<uint64_t>(sp) * kPoolSpan;
+    const uint32_t n = static_cast<uint32_t>(min(static_cast<uint64_t>(kPoolSpan), a.piece - off));
+    uint8_t* host_side = reinterpret_cast<uint8_t*>(pooled + static_cast<uint64_t>(p) * a.piece + off);
+    uint8_t* gpu_side = reinterpret_cast<uint8_t*>(a.layer_ptr[p >> 1] + (p & 1u) * a.kstride + paged_off + off);
+    if (a.to_paged)
+      pool_span(host_side, gpu_side, n, lane);
+    else
+      pool_span(gpu_side, host_side, n, lane);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t prev = __hip_atomic_fetch_add(a.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == gridDim.x - 1) {
+      __hip_atomic_store(a.ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      st_sys(a.done, make_tag(a.seq, 0));
+    }
+  }
+}
+
 template <uint32_t E>
 __global__ __launch_bounds__(kBlock) void mma_transfer_xpacked_kernel(KernelArgs a) {
   transfer_body<E>(a);
@@ -573,7 +649,30 @@ hipError_t launch_whole(const KernelArgs& args, uint32_t grid, hipStream_t strea
                          stream);
 }
 
+hipError_t launch_pool(const KernelArgs& args, uint32_t grid, hipStream_t stream) {
+  PoolArgs p;
+  p.done = args.done;
+  p.seq = args.seq;
+  p.ctr = args.pool_ctr;
+  p.tab = args.pool_tab;
+  p.pool = args.pool_base;
+  p.units = args.pool_units;
+  p.per_wg = args.pool_per_wg;
+  p.ppb = 2 * args.kv_layers;
+  p.piece = args.kv_piece_bytes;
+  p.slot_bytes = p.piece * p.ppb;
+  p.kstride = args.kv_kstride;
+  p.spans = args.pool_spans;
+  p.to_paged = args.pool_to_paged;
+  p.layers = args.kv_layers;
+  for (uint32_t l = 0; l < args.kv_layers; ++l) p.layer_ptr[l] = args.layer_ptr[l];
+  void* params[] = {&p};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&mma_kv_pool_kernel), dim3(grid), dim3(kBlock), params, 0,
+                         stream);
+}
+
 hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t stream) {
+  if (args.pool_tab) return launch_pool(args, grid, stream);
   if (args.self_contained && args.kv_layers == 0) {  // linear: the lean kernel; KV: below, by layout
     if (args.n_pre <= 4) return launch_whole<4>(args, grid, stream);
     if (args.n_pre <= 16) return launch_whole<16>(args, grid, stream);

@@ -32,6 +32,15 @@ constexpr uint32_t kMaxLdsPerWave = 36 * 1024;  // x-packed KV tiles: 4 waves x 
 constexpr uint32_t kWave = 64;
 constexpr uint32_t kWavesPerWG = 4;
 constexpr uint32_t kBlock = kWave * kWavesPerWG;
+// HBM pool launches (a paged-KV transfer whose pool is in device memory): a
+// piece is moved in spans of kPoolSpan bytes, one 16-byte unit per lane and
+// register, at most kPoolMaxWorkgroups workgroups per launch. The block table
+// goes to the kernel through an arena of kPoolTabEntries 8-byte entries in
+// device-visible host memory, handed out in segments of kPoolTabSeg entries.
+constexpr uint32_t kPoolSpan = 8 * 1024;
+constexpr uint32_t kPoolMaxWorkgroups = 8192;
+constexpr uint32_t kPoolTabEntries = 1u << 19;
+constexpr uint32_t kPoolTabSeg = 512;
 
 // GPU block layouts of a paged-KV piece (one layer's K or V of one block). The
 // host side is always token-major [tokens][heads][head_dim].
@@ -131,8 +140,34 @@ struct KernelArgs {
   uint32_t kv_layout;
   uint32_t kv_tokens, kv_heads, kv_row_bytes, kv_elem;
   uint32_t kv_lds_wave;     // kKvLayoutXPacked: dynamic LDS bytes per wave (the launch asks for 4x)
+  // HBM pool launch (pool_tab non-null): the whole transfer is one launch of
+  // mma_kv_pool_kernel, converted from these arguments (see PoolArgs).
+  const uint64_t* pool_tab;  // per block: pool slot | GPU block << 32 (device-visible host memory)
+  uint32_t* pool_ctr;        // device counter of finished workgroups, 0 between launches
+  uint64_t pool_base;        // device address of the pool
+  uint64_t pool_units;       // spans in the transfer
+  uint64_t pool_per_wg;      // spans per workgroup
+  uint32_t pool_spans;       // spans per piece
+  uint32_t pool_to_paged;    // 1: pool -> layers (fetch); 0: layers -> pool (offload)
   uint64_t layer_ptr[kMaxLayers];
   uint64_t pre[kPrefill][3];  // words a, b, count|kind_p0 of the first ring entries
+};
+
+// Arguments of an HBM pool launch. Span u is span s of piece p of block i,
+// u = (i * ppb + p) * spans + s (ppb = 2 * layers pieces per block, piece p =
+// layer p / 2, K for even p and V for odd); workgroup g takes spans
+// [g * per_wg, (g + 1) * per_wg). The workgroup that finishes last writes
+// done[0] = make_tag(seq, 0) and returns the counter to 0.
+struct PoolArgs {
+  uint64_t* done;
+  uint64_t seq;
+  uint32_t* ctr;
+  const uint64_t* tab;
+  uint64_t pool;
+  uint64_t units, per_wg;
+  uint64_t slot_bytes, piece, kstride;
+  uint32_t ppb, spans, to_paged, layers;
+  uint64_t layer_ptr[kMaxLayers];
 };
 
 // Arguments of a self-contained launch (every entry of a linear transfer, no

@@ -5,7 +5,9 @@
 //                       pinned host memory, or stores to it), grid chosen by
 //                       the caller's sweep;
 //   native_sdma_all   - the buffer split evenly over a set of SDMA engines,
-//                       one ROCr command each, all in flight at once.
+//                       one ROCr command each, all in flight at once;
+//   native_hbm_copy   - for the measured HBM peak: a device-to-device streaming
+//                       copy in wave-contiguous spans.
 // Together with one plain hipMemcpyAsync they bound what the link delivers on
 // this machine (the paper quotes 52-60 GB/s typical for a 64 GB/s PCIe 5.0 x16
 // link, Section 2.2). Built into libmma_native.so, not into libmma.so.
@@ -38,6 +40,29 @@ __global__ __launch_bounds__(256) void zero_copy_stream_kernel(const v4u* __rest
     dst[i + 7 * stride] = r7;
   }
   for (; i < n16; i += stride) dst[i] = src[i];
+}
+
+// HBM-to-HBM streaming copy for the measured HBM peak: each wave moves whole
+// 16 KiB spans (16 independent 16-byte loads per lane, nontemporal, before the
+// matching stores), spans strided over the grid; units past the last whole span
+// go one per lane.
+__global__ __launch_bounds__(256) void hbm_span_copy_kernel(const v4u* __restrict__ src, v4u* __restrict__ dst,
+                                                            uint64_t n16) {
+  constexpr uint32_t kV = 16;
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint64_t wave = static_cast<uint64_t>(blockIdx.x) * 4 + threadIdx.x / 64;
+  const uint64_t waves = static_cast<uint64_t>(gridDim.x) * 4;
+  const uint64_t span = kV * 64ull;
+  const uint64_t full = n16 / span;
+  for (uint64_t c = wave; c < full; c += waves) {
+    const uint64_t b = c * span + lane;
+    v4u v[kV];
+#pragma unroll
+    for (uint32_t i = 0; i < kV; ++i) v[i] = __builtin_nontemporal_load(src + b + i * 64);
+#pragma unroll
+    for (uint32_t i = 0; i < kV; ++i) __builtin_nontemporal_store(v[i], dst + b + i * 64);
+  }
+  for (uint64_t i = full * span + wave * 64 + lane; i < n16; i += waves * 64) dst[i] = src[i];
 }
 
 struct ProbeAgents {
@@ -80,6 +105,17 @@ int native_zero_copy(void* dst, const void* src, uint64_t bytes, int dir, uint32
     return static_cast<int>(hipErrorInvalidValue);
   zero_copy_stream_kernel<<<grid, 256, 0, static_cast<hipStream_t>(stream)>>>(static_cast<const v4u*>(src),
                                                                               static_cast<v4u*>(dst), bytes >> 4);
+  return static_cast<int>(hipGetLastError());
+}
+
+// HBM-to-HBM copy with hbm_span_copy_kernel on `grid` workgroups of 256
+// threads; the same argument rules and return value as native_zero_copy.
+int native_hbm_copy(void* dst, const void* src, uint64_t bytes, uint32_t grid, void* stream) {
+  if ((bytes & 15u) || (reinterpret_cast<uintptr_t>(dst) & 15u) || (reinterpret_cast<uintptr_t>(src) & 15u) ||
+      grid == 0)
+    return static_cast<int>(hipErrorInvalidValue);
+  hbm_span_copy_kernel<<<grid, 256, 0, static_cast<hipStream_t>(stream)>>>(static_cast<const v4u*>(src),
+                                                                           static_cast<v4u*>(dst), bytes >> 4);
   return static_cast<int>(hipGetLastError());
 }
 

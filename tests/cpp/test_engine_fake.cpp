@@ -259,6 +259,45 @@ void copy_at_rate(void* dst, const void* src, uint64_t n, double wave_rate) {
   std::memcpy(dst, src, n);
 }
 
+// The HBM pool kernel: workgroup g moves spans [g * per_wg, (g + 1) * per_wg)
+// from the table entries, then counts itself done; the last one resets the
+// counter and writes the done tag.
+void pool_workgroup(const KernelArgs& a, uint32_t g, uint32_t grid) {
+  const uint64_t per_blk = 2ull * a.kv_layers * a.pool_spans;
+  const uint64_t slot_bytes = 2ull * a.kv_layers * a.kv_piece_bytes;
+  const uint64_t u0 = static_cast<uint64_t>(g) * a.pool_per_wg;
+  const uint64_t u1 = std::min(a.pool_units, u0 + a.pool_per_wg);
+  for (uint64_t u = u0; u < u1; ++u) {
+    const uint64_t i = u / per_blk, r = u % per_blk;
+    const uint64_t p = r / a.pool_spans, off = (r % a.pool_spans) * kPoolSpan;
+    const uint64_t e = aload(&a.pool_tab[i]);
+    const uint64_t n = std::min<uint64_t>(kPoolSpan, a.kv_piece_bytes - off);
+    uint8_t* pooled = reinterpret_cast<uint8_t*>(a.pool_base + (e & 0xffffffffull) * slot_bytes + p * a.kv_piece_bytes + off);
+    uint8_t* paged = reinterpret_cast<uint8_t*>(a.layer_ptr[p >> 1] + (p & 1u) * a.kv_kstride + (e >> 32) * a.kv_piece_bytes + off);
+    if (a.pool_to_paged)
+      std::memcpy(paged, pooled, n);
+    else
+      std::memcpy(pooled, paged, n);
+  }
+  if (__atomic_fetch_add(a.pool_ctr, 1u, __ATOMIC_ACQ_REL) == grid - 1) {
+    __atomic_store_n(a.pool_ctr, 0u, __ATOMIC_RELAXED);
+    astore(a.done, make_tag(a.seq, 0));
+  }
+}
+
+// A pool launch on the fake stream: a few host threads share its workgroups.
+void pool_launch(FakeStream& st, const KernelArgs& a, uint32_t grid) {
+  st.launch([a, grid] {
+    const uint32_t nt = std::min<uint32_t>(grid, 4);
+    std::vector<std::thread> ts;
+    for (uint32_t t = 0; t < nt; ++t)
+      ts.emplace_back([&a, grid, t, nt] {
+        for (uint32_t g = t; g < grid; g += nt) pool_workgroup(a, g, grid);
+      });
+    for (auto& t : ts) t.join();
+  });
+}
+
 void wave(const KernelArgs a, uint32_t w, double wave_rate) {
   Record* rec = a.rec;
   DevState* ds = a.ds;
@@ -428,14 +467,22 @@ class Harness {
       e->submit(std::move(x));
     }
     if (!launch) {
+      if (x && x->light >= 0) {
+        e->release_unused(x.get());
+        return;
+      }
       raw->unlaunched.store(true, std::memory_order_release);
       return;
     }
-    st.launch([a, waves, rate] {
-      std::vector<std::thread> ts;
-      for (uint32_t w = 0; w < waves; ++w) ts.emplace_back(wave, a, w, rate);
-      for (auto& t : ts) t.join();
-    });
+    if (a.pool_tab) {
+      pool_launch(st, a, grid);
+    } else {
+      st.launch([a, waves, rate] {
+        std::vector<std::thread> ts;
+        for (uint32_t w = 0; w < waves; ++w) ts.emplace_back(wave, a, w, rate);
+        for (auto& t : ts) t.join();
+      });
+    }
     if (!x) return;
     if (x->light >= 0)
       e->track(std::move(x));  // as the runtime: whole transfers never reach the engine thread
@@ -472,11 +519,15 @@ class Harness {
     }
     const uint32_t waves = grid * kWavesPerWG;
     const double rate = s_.wave_rate;
-    st.launch([a, waves, rate] {
-      std::vector<std::thread> ts;
-      for (uint32_t w = 0; w < waves; ++w) ts.emplace_back(wave, a, w, rate);
-      for (auto& t : ts) t.join();
-    });
+    if (a.pool_tab) {
+      pool_launch(st, a, grid);
+    } else {
+      st.launch([a, waves, rate] {
+        std::vector<std::thread> ts;
+        for (uint32_t w = 0; w < waves; ++w) ts.emplace_back(wave, a, w, rate);
+        for (auto& t : ts) t.join();
+      });
+    }
     e->track(std::move(x));
   }
   bool sync() { return eng_[0]->wait_idle(60000) && eng_[1]->wait_idle(60000); }
@@ -740,6 +791,118 @@ void whole_kv_transfers() {
   }
   CHECK(h.stats().failed.load() == 0, "whole KV: failed transfers");
   std::printf("ok   small KV fetches and offloads taken whole by the CU path; larger ones use every path\n");
+}
+
+// KV transfers between a pool in device memory and the paged layers (piece
+// layout) run as pool launches: one launch, table from the arena, no ring and
+// no copy engine. Pieces of 8 KiB + 48 bytes end in a short span. Launches
+// queued back to back on one stream reuse light slots and counters. With the
+// stream held, a transfer whose table finds no room in the arena takes the
+// ring path instead, and all of them land once the stream runs.
+void hbm_pool_launches() {
+  Setup s;
+  s.cfg = default_config();
+  Harness h(s);
+  {
+    FakeStream st;
+    const uint32_t L = 2, ppb = 2 * L, slots = 300, nb = 320;
+    const uint64_t piece = 8192 + 48, slot_bytes = piece * ppb;
+    std::vector<uint8_t> pool = random_bytes(slots * slot_bytes, 61);
+    std::vector<std::vector<uint8_t>> layers(L, std::vector<uint8_t>(2 * nb * piece, 0xA5));
+    KvGeom kv;
+    kv.piece = piece;
+    kv.kstride = piece * nb;
+    kv.layers = L;
+    for (uint32_t l = 0; l < L; ++l) kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l].data());
+    const uint64_t base = reinterpret_cast<uint64_t>(pool.data());
+    const uint64_t cmds = h.stats().sdma_commands.load();
+    for (int n : {1, 7, 300}) {
+      std::vector<int32_t> hs(n), gb(n);
+      for (int i = 0; i < n; ++i) {
+        hs[i] = (7 * i + 3) % static_cast<int>(slots);
+        gb[i] = (11 * i + 1) % static_cast<int>(nb);
+      }
+      for (int rep = 0; rep < 3; ++rep) {  // queued back to back: light slots and counters reused
+        std::unique_ptr<Transfer> x =
+            make_kv_transfer(MMA_H2D, piece, ppb, base, base, true, false, hs.data(), gb.data(), n, h.cfg());
+        x->pool_launch = true;
+        h.submit(std::move(x), n * slot_bytes, st, &kv);
+      }
+      st.synchronize();
+      CHECK(h.sync(), "sync");
+      bool ok = true;
+      for (int i = 0; i < n; ++i)
+        for (uint32_t l = 0; l < L; ++l)
+          for (uint32_t k = 0; k < 2; ++k)
+            ok &= std::memcmp(layers[l].data() + (k * nb + gb[i]) * piece,
+                              pool.data() + hs[i] * slot_bytes + (2 * l + k) * piece, piece) == 0;
+      CHECK(ok, "pool fetch of %d blocks differs", n);
+      // offload the fetched blocks back into other slots
+      std::vector<int32_t> dest(n);
+      for (int i = 0; i < n; ++i) dest[i] = (hs[i] + 1) % static_cast<int>(slots);
+      auto want = pool;
+      for (int j = 0; j < n; ++j)
+        for (uint32_t l = 0; l < L; ++l)
+          for (uint32_t k = 0; k < 2; ++k)
+            std::memcpy(want.data() + dest[j] * slot_bytes + (2 * l + k) * piece,
+                        layers[l].data() + (k * nb + gb[j]) * piece, piece);
+      std::unique_ptr<Transfer> x =
+          make_kv_transfer(MMA_D2H, piece, ppb, base, base, true, false, dest.data(), gb.data(), n, h.cfg());
+      x->pool_launch = true;
+      h.submit(std::move(x), n * slot_bytes, st, &kv);
+      st.synchronize();
+      CHECK(h.sync(), "sync");
+      CHECK(pool == want, "pool offload of %d blocks: pool differs", n);
+    }
+    CHECK(h.stats().sdma_commands.load() == cmds, "a pool launch used a copy engine");
+  }
+  {
+    // Arena room: 16-byte pieces, one layer. A takes all but one segment, C
+    // the last one, so B finds no room and goes through a record and the ring.
+    FakeStream st;
+    const uint64_t piece = 16, slot_bytes = 2 * piece;
+    const uint32_t na = (kPoolTabEntries / kPoolTabSeg - 1) * kPoolTabSeg, nc = kPoolTabSeg, nbb = 3;
+    const uint32_t total = na + nc + nbb;
+    std::vector<uint8_t> pool = random_bytes(static_cast<uint64_t>(total) * slot_bytes, 62);
+    std::vector<uint8_t> layer(2ull * total * piece, 0xA5);
+    KvGeom kv;
+    kv.piece = piece;
+    kv.kstride = piece * total;
+    kv.layers = 1;
+    kv.layer_ptr[0] = reinterpret_cast<uint64_t>(layer.data());
+    std::vector<int32_t> hs(total), gb(total);
+    for (uint32_t i = 0; i < total; ++i) {
+      hs[i] = static_cast<int32_t>((i * 7919ull) % total);  // 7919 is prime and does not divide total
+      gb[i] = static_cast<int32_t>(total - 1 - i);
+    }
+    std::promise<void> gate;
+    std::shared_future<void> open = gate.get_future().share();
+    st.launch([open] { open.wait(); });  // holds the stream
+    const uint32_t first[3] = {0, na, na + nc}, count[3] = {na, nc, nbb};
+    bool launched[3];
+    for (int t = 0; t < 3; ++t) {
+      std::unique_ptr<Transfer> x = make_kv_transfer(MMA_H2D, piece, 2, reinterpret_cast<uint64_t>(pool.data()),
+                                                     reinterpret_cast<uint64_t>(pool.data()), true, false,
+                                                     hs.data() + first[t], gb.data() + first[t], count[t], h.cfg());
+      x->pool_launch = true;
+      Transfer* raw = x.get();
+      h.submit(std::move(x), static_cast<uint64_t>(count[t]) * slot_bytes, st, &kv);
+      launched[t] = raw->pool_launch;  // set by acquire; the held stream keeps the transfer alive
+    }
+    CHECK(launched[0] && launched[1] && !launched[2], "arena: expected launches A and C, ring for B (%d %d %d)",
+          launched[0], launched[1], launched[2]);
+    gate.set_value();
+    st.synchronize();
+    CHECK(h.sync(), "sync");
+    bool ok = true;
+    for (uint32_t i = 0; i < total; ++i)
+      for (uint32_t k = 0; k < 2; ++k)
+        ok &= std::memcmp(layer.data() + (k * total + gb[i]) * piece, pool.data() + hs[i] * slot_bytes + k * piece,
+                          piece) == 0;
+    CHECK(ok, "arena-bound pool fetches differ");
+  }
+  CHECK(h.stats().failed.load() == 0, "pool launches: failed transfers");
+  std::printf("ok   HBM pool KV transfers run as one launch each; without arena room a transfer takes the ring\n");
 }
 
 // A deep queue of whole transfers on a stream that cannot progress yet: they
@@ -1205,6 +1368,7 @@ int main(int argc, char** argv) {
     unlaunched_transfer_drains();
     whole_transfers_on_cu();
     whole_kv_transfers();
+    hbm_pool_launches();
     deep_queue_does_not_block();
     submit_failures_rerouted();
     kv_submit_failures_rerouted();

@@ -168,10 +168,24 @@ def test_kv_all_permutations(paths):
         mma.mma_synchronize()
 
 
-@pytest.mark.parametrize("shape", ["small", "ragged", "medium"])
+POOL_SHAPES = {
+    **SHAPES,
+    # pieces of 8 KiB + 48 bytes: one full span of the pool kernel and a short one
+    "span_tail": W.KVShape(layers=2, block_tokens=16, kv_heads=1, head_dim=515, elem_bytes=1,
+                           gpu_num_blocks=90, host_num_slots=80, n_blocks=70),
+    # 32 KiB pieces, 3000 blocks: the launch's full 8192 workgroups, 12 spans each, so waves
+    # move several spans and cross from one block into the next
+    "wide": W.KVShape(layers=4, block_tokens=16, kv_heads=8, head_dim=128, elem_bytes=2,
+                      gpu_num_blocks=3300, host_num_slots=3072, n_blocks=3000),
+}
+
+
+@pytest.mark.parametrize("shape", ["small", "ragged", "medium", "span_tail", "wide"])
 def test_kv_device_pool(shape):
-    """A pool in device memory: the same gather/scatter runs HBM -> HBM on the CU path."""
-    s = SHAPES[shape]
+    """A pool in device memory: the same gather/scatter runs HBM -> HBM on the CU path
+    (one pool-kernel launch per transfer in the piece layout)."""
+    s = POOL_SHAPES[shape]
+    log(f"device pool {shape}: {s}")
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     plan = W.kv_offload_plan(s, cfg=4)
     with session("both", chunk_bytes=4096):
@@ -196,6 +210,37 @@ def test_kv_device_pool(shape):
         mma.mma_synchronize()
         st = mma.mma_get_stats()
     assert sum(st["path_bytes"][:16]) == 0 and st["failed_transfers"] == 0
+
+
+def test_kv_device_pool_queued_launches():
+    """Pool launches queued back to back on two streams, with no synchronisation between them:
+    each stream's fetches land in order (the last one wins) and every launch retires."""
+    s = POOL_SHAPES["span_tail"]
+    lay = layout_of(s)
+    with session("both"):
+        r = np.random.default_rng(21)
+        pools = [r.integers(0, 256, s.host_num_slots * s.slot_bytes, dtype=np.uint8) for _ in range(3)]
+        dpools = [torch.from_numpy(p.copy()).cuda() for p in pools]
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        hs, gb = W.kv_fetch_tables(s, cfg=3)
+        outs = []
+        for k, st in enumerate(streams):
+            layers = _layers(s, W.GPU_POISON)
+            before = _layer_views(s, layers)
+            torch.cuda.synchronize()
+            lt = mma.layer_table(layers)
+            for rep in range(6):  # pools 0, 1, 2, 0, 1, 2 (k = 0) or 1, 2, 0, ... (k = 1)
+                mma.mma_kv_fetch(lay, dpools[(rep + k) % 3], lt, hs, gb, st)
+            outs.append((layers, before, (5 + k) % 3))
+        torch.cuda.synchronize()
+        for layers, before, last in outs:
+            pv = pools[last].reshape(s.host_num_slots, s.slot_bytes)
+            for l in range(s.layers):
+                want = okv.kv_fetch_layer(pv, before[l], l, s.layers, hs, gb)
+                assert np.array_equal(to_host(layers[l]).reshape(want.shape), want), l
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+    assert st["transfers"] == 12 and st["failed_transfers"] == 0
 
 
 def test_kv_rejects_bad_tables():
