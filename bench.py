@@ -13,7 +13,7 @@ the same workload, native hipMemcpyAsync comparators, and the 64 MiB single-copy
 workload.
 
 Usage: python bench.py [--gpus 1] [--steps 10] [--warmup 2]
-       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint  (JSON per point)
+       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint|control|hbmpool  (JSON per point)
        python bench.py --calib                                  (counter-scaling kernels)
 """
 from __future__ import annotations
@@ -51,7 +51,7 @@ def parse():
     p.add_argument("--control", choices=["host", "device"], default=None,
                    help="who drives transfers after submission (default: the library's, MMA_CONTROL)")
     p.add_argument("--sweep", choices=["sizes", "idle", "chunks", "contention", "duplex", "paths", "footprint",
-                                       "control"],
+                                       "control", "hbmpool"],
                    help="instead of the benchmark, print one JSON line per point of a parameter sweep")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
@@ -1002,8 +1002,52 @@ def sweep_footprint():
         mma.mma_finalize()
     h.free()
 
+def sweep_hbmpool():
+    """The 64k-token KV fetch (4096 blocks) and the 2048-block offload with the pool resident in HBM:
+    one pool-kernel launch per call in the piece layout. Reports HBM read+write TB/s per call (median
+    of 5) and checks 32 sampled pieces of each direction against the other side."""
+    import numpy as np
+
+    import workloads as W
+    mma, torch, nat, st = _sweep_env()
+    s = W.KV64K
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    plan = W.kv_offload_plan(s, cfg=4)
+    mma.mma_init(0)
+    lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                        s.host_num_slots)
+    torch.manual_seed(1)
+    dpool = torch.empty(s.host_num_slots * s.slot_bytes, dtype=torch.uint8, device="cuda").random_(0, 256)
+    layers = [torch.empty(s.layer_bytes, dtype=torch.uint8, device="cuda").random_(0, 256) for _ in range(s.layers)]
+    lt = mma.layer_table(layers)
+    torch.cuda.synchronize()
+    r = np.random.default_rng(2)
+
+    def pieces_equal(slots, blocks):
+        ok = True
+        for _ in range(32):
+            j, l, k = int(r.integers(len(slots))), int(r.integers(s.layers)), int(r.integers(2))
+            po = int(slots[j]) * s.slot_bytes + (2 * l + k) * s.piece_bytes
+            go = (k * s.gpu_num_blocks + int(blocks[j])) * s.piece_bytes
+            ok &= bool(torch.equal(dpool[po:po + s.piece_bytes], layers[l][go:go + s.piece_bytes]))
+        return ok
+
+    for case, fn, slots, blocks in (
+            ("fetch", lambda: mma.mma_kv_fetch(lay, dpool, lt, hs, gb, st), hs, gb),
+            ("offload", lambda: mma.mma_kv_offload(lay, dpool, lt, plan.src_blocks, plan.dest, st),
+             plan.dest, plan.src_blocks)):
+        t = _timed(st, fn, reps=5, warm=1)
+        st.synchronize()
+        payload = len(slots) * s.slot_bytes
+        _emit(sweep="hbmpool", case=case, blocks=len(slots), payload_bytes=payload, ms=round(t["p50"], 3),
+              ms_p10_p90=[round(t["p10"], 3), round(t["p90"], 3)],
+              hbm_TBs_read_plus_write=round(2 * payload / t["p50"] / 1e9, 3),
+              frac_of_8TBs=round(2 * payload / t["p50"] / 1e9 / 8.0, 4), sampled_parity=pieces_equal(slots, blocks))
+    mma.mma_finalize()
+
+
 SWEEPS = {"sizes": sweep_sizes, "idle": sweep_idle, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
-          "paths": sweep_paths, "footprint": sweep_footprint, "control": sweep_control}
+          "paths": sweep_paths, "footprint": sweep_footprint, "control": sweep_control, "hbmpool": sweep_hbmpool}
 
 
 def main():
