@@ -3,7 +3,8 @@
 One schedule of ~150 operations is drawn from a seed: single copies and tensor lists in both
 directions (1 byte to 12 MiB, odd offsets, self-contained launches, whole-CU transfers, early
 starts on idle streams, multipath transfers with merged copy-engine commands) and paged-KV
-fetches and offloads in all three GPU block layouts, issued in random order over four streams
+fetches and offloads in all three GPU block layouts, a third of them with the pool in HBM (pool
+launches in the piece layout, the ring otherwise), issued in random order over four streams
 (including the legacy default stream). Every operation writes its own destination range and
 reads a read-only source, so the final state is unique whatever the interleaving; each
 destination (and the poison around it) is compared byte-exact with oracle.copy / oracle.kv.
@@ -110,8 +111,11 @@ def test_random_mixed_schedule(seed, control):
                 lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
                                     s.host_num_slots, xp)
                 pool_np = r.integers(0, 256, (s.host_num_slots, s.slot_bytes), dtype=np.uint8)
-                pool = mma.PinnedBuffer(pool_np.size)
-                pool.array[:] = pool_np.reshape(-1)
+                if r.integers(3) == 0:  # a pool in HBM: one pool-kernel launch (piece layout) or the ring
+                    pool = torch.from_numpy(pool_np.reshape(-1).copy()).cuda()
+                else:
+                    pool = mma.PinnedBuffer(pool_np.size)
+                    pool.array[:] = pool_np.reshape(-1)
                 layers_np = [r.integers(0, 256, (2, s.gpu_num_blocks, s.piece_bytes), dtype=np.uint8)
                              for _ in range(s.layers)]
                 layers = [torch.from_numpy(x.reshape(-1).copy()).cuda() for x in layers_np]
@@ -144,14 +148,17 @@ def test_random_mixed_schedule(seed, control):
         for s, xp, d2h, pool, pool_np, layers, layers_np, a, b in kv_jobs:
             geom = (s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes)
             layout = (okv.LAYOUT_PIECE, okv.LAYOUT_XPACKED, okv.LAYOUT_HND)[xp]
+            on_dev = isinstance(pool, torch.Tensor)
             if d2h:
                 want = okv.kv_offload(pool_np, layers_np, b, a, layout, geom)
-                assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
+                got_pool = to_host(pool) if on_dev else pool.array
+                assert np.array_equal(got_pool.reshape(s.host_num_slots, -1), want), (xp, on_dev)
             else:
                 want = okv.kv_fetch(pool_np, layers_np, a, b, layout, geom)
                 for l in range(s.layers):
-                    assert np.array_equal(to_host(layers[l]).reshape(want[l].shape), want[l]), l
-            pool.free()
+                    assert np.array_equal(to_host(layers[l]).reshape(want[l].shape), want[l]), (l, xp, on_dev)
+            if not on_dev:
+                pool.free()
         src_h.free()
         dst_h.free()
     assert stats["failed_transfers"] == 0
