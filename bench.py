@@ -1004,8 +1004,10 @@ def sweep_footprint():
 
 def sweep_hbmpool():
     """The 64k-token KV fetch (4096 blocks) and the 2048-block offload with the pool resident in HBM:
-    one pool-kernel launch per call in the piece layout. Reports HBM read+write TB/s per call (median
-    of 5) and checks 32 sampled pieces of each direction against the other side."""
+    one pool-kernel launch per call, GPU blocks in the piece and in the head-major layout. Reports
+    HBM read+write TB/s per call (median of 5). Piece layout: 32 sampled pieces of each direction
+    are compared with the other side. Head-major: the fetched blocks are offloaded back into their
+    own slots, which must leave the pool unchanged."""
     import numpy as np
 
     import workloads as W
@@ -1014,8 +1016,6 @@ def sweep_hbmpool():
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     plan = W.kv_offload_plan(s, cfg=4)
     mma.mma_init(0)
-    lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
-                        s.host_num_slots)
     torch.manual_seed(1)
     dpool = torch.empty(s.host_num_slots * s.slot_bytes, dtype=torch.uint8, device="cuda").random_(0, 256)
     layers = [torch.empty(s.layer_bytes, dtype=torch.uint8, device="cuda").random_(0, 256) for _ in range(s.layers)]
@@ -1032,17 +1032,34 @@ def sweep_hbmpool():
             ok &= bool(torch.equal(dpool[po:po + s.piece_bytes], layers[l][go:go + s.piece_bytes]))
         return ok
 
-    for case, fn, slots, blocks in (
-            ("fetch", lambda: mma.mma_kv_fetch(lay, dpool, lt, hs, gb, st), hs, gb),
-            ("offload", lambda: mma.mma_kv_offload(lay, dpool, lt, plan.src_blocks, plan.dest, st),
-             plan.dest, plan.src_blocks)):
-        t = _timed(st, fn, reps=5, warm=1)
+    def round_trip(lay):
+        before = dpool.clone()
+        mma.mma_kv_offload(lay, dpool, lt, gb, hs, st)
         st.synchronize()
-        payload = len(slots) * s.slot_bytes
-        _emit(sweep="hbmpool", case=case, blocks=len(slots), payload_bytes=payload, ms=round(t["p50"], 3),
-              ms_p10_p90=[round(t["p10"], 3), round(t["p90"], 3)],
-              hbm_TBs_read_plus_write=round(2 * payload / t["p50"] / 1e9, 3),
-              frac_of_8TBs=round(2 * payload / t["p50"] / 1e9 / 8.0, 4), sampled_parity=pieces_equal(slots, blocks))
+        ok = bool(torch.equal(before, dpool))
+        del before
+        return ok
+
+    for name, code in (("piece", mma.MMA_KV_LAYOUT_PIECE), ("hnd", mma.MMA_KV_LAYOUT_HND)):
+        lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                            s.host_num_slots, code)
+        for case, fn, slots, blocks in (
+                ("fetch", lambda: mma.mma_kv_fetch(lay, dpool, lt, hs, gb, st), hs, gb),
+                ("offload", lambda: mma.mma_kv_offload(lay, dpool, lt, plan.src_blocks, plan.dest, st),
+                 plan.dest, plan.src_blocks)):
+            t = _timed(st, fn, reps=5, warm=1)
+            st.synchronize()
+            if code == mma.MMA_KV_LAYOUT_PIECE:
+                check = pieces_equal(slots, blocks)
+            else:
+                check = round_trip(lay) if case == "fetch" else None
+            payload = len(slots) * s.slot_bytes
+            _emit(sweep="hbmpool", layout=name, case=case, blocks=len(slots), payload_bytes=payload,
+                  ms=round(t["p50"], 3), ms_p10_p90=[round(t["p10"], 3), round(t["p90"], 3)],
+                  hbm_TBs_read_plus_write=round(2 * payload / t["p50"] / 1e9, 3),
+                  frac_of_8TBs=round(2 * payload / t["p50"] / 1e9 / 8.0, 4),
+                  check="sampled pieces" if code == mma.MMA_KV_LAYOUT_PIECE else "round trip after the fetch",
+                  check_ok=check)
     mma.mma_finalize()
 
 

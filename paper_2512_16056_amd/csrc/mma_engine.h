@@ -666,7 +666,8 @@ class Engine {
   }
 
   // An HBM pool launch: the table goes to the arena, the grid is sized to
-  // the spans (at least one per wave, at most kPoolMaxWorkgroups workgroups),
+  // the spans (whole pieces for head-major blocks; at least one per wave, at
+  // most kPoolMaxWorkgroups workgroups),
   // and the kernel is the transfer's only copy engine. Returns the grid.
   uint32_t prepare_pool(Transfer* x, const KvGeom* kv, KernelArgs& a) {
     const uint64_t nblk = x->pool_pairs.size();
@@ -679,7 +680,7 @@ class Engine {
     x->whole = x->self_contained = true;
     x->started = x->closed = x->completed = true;
     x->t_started = x->t_complete = x->t_submit;
-    const uint64_t spans = (kv->piece + kPoolSpan - 1) / kPoolSpan;
+    const uint64_t spans = kv->layout == kKvLayoutHnd ? 1 : (kv->piece + kPoolSpan - 1) / kPoolSpan;
     const uint64_t units = nblk * 2 * kv->layers * spans;
     uint64_t grid = std::min<uint64_t>(kPoolMaxWorkgroups, (units + kWavesPerWG - 1) / kWavesPerWG);
     const uint64_t per_wg = (units + grid - 1) / grid;

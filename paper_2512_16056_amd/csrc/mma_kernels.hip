@@ -562,6 +562,9 @@ __device__ __forceinline__ void pool_span(const uint8_t* src, uint8_t* dst, uint
 // table entries: the data itself becomes visible to later work through the
 // stream, when the kernel ends, as for any kernel (a device-wide release per
 // workgroup would write back the L2 of its XCD each time).
+// kHnd: GPU blocks in the head-major layout; a span is then a whole piece,
+// permuted row by row on its way (hnd_piece).
+template <bool kHnd>
 __global__ __launch_bounds__(kBlock) void mma_kv_pool_kernel(PoolArgs a) {
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -584,7 +587,13 @@ __global__ __launch_bounds__(kBlock) void mma_kv_pool_kernel(PoolArgs a) {
     const uint32_t n = static_cast<uint32_t>(min(static_cast<uint64_t>(kPoolSpan), a.piece - off));
     uint8_t* host_side = reinterpret_cast<uint8_t*>(pooled + static_cast<uint64_t>(p) * a.piece + off);
     uint8_t* gpu_side = reinterpret_cast<uint8_t*>(a.layer_ptr[p >> 1] + (p & 1u) * a.kstride + paged_off + off);
-    if (a.to_paged)
+    if constexpr (kHnd) {
+      const XGeom g{a.tokens, a.heads, a.row_bytes, a.elem, 0};
+      if (a.to_paged)
+        hnd_piece(host_side, gpu_side, true, g, lane);
+      else
+        hnd_piece(gpu_side, host_side, false, g, lane);
+    } else if (a.to_paged)
       pool_span(host_side, gpu_side, n, lane);
     else
       pool_span(gpu_side, host_side, n, lane);
@@ -665,10 +674,15 @@ hipError_t launch_pool(const KernelArgs& args, uint32_t grid, hipStream_t stream
   p.spans = args.pool_spans;
   p.to_paged = args.pool_to_paged;
   p.layers = args.kv_layers;
+  p.tokens = args.kv_tokens;
+  p.heads = args.kv_heads;
+  p.row_bytes = args.kv_row_bytes;
+  p.elem = args.kv_elem;
   for (uint32_t l = 0; l < args.kv_layers; ++l) p.layer_ptr[l] = args.layer_ptr[l];
   void* params[] = {&p};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&mma_kv_pool_kernel), dim3(grid), dim3(kBlock), params, 0,
-                         stream);
+  const void* k = args.kv_layout == kKvLayoutHnd ? reinterpret_cast<const void*>(&mma_kv_pool_kernel<true>)
+                                                 : reinterpret_cast<const void*>(&mma_kv_pool_kernel<false>);
+  return hipLaunchKernel(k, dim3(grid), dim3(kBlock), params, 0, stream);
 }
 
 hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t stream) {

@@ -153,7 +153,8 @@ struct KernelArgs {
   uint64_t pre[kPrefill][3];  // words a, b, count|kind_p0 of the first ring entries
 };
 
-// Arguments of an HBM pool launch. Span u is span s of piece p of block i,
+// Arguments of an HBM pool launch (GPU blocks in the piece or the head-major
+// layout). Span u is span s of piece p of block i,
 // u = (i * ppb + p) * spans + s (ppb = 2 * layers pieces per block, piece p =
 // layer p / 2, K for even p and V for odd); workgroup g takes spans
 // [g * per_wg, (g + 1) * per_wg). The workgroup that finishes last writes
@@ -167,6 +168,7 @@ struct PoolArgs {
   uint64_t units, per_wg;
   uint64_t slot_bytes, piece, kstride;
   uint32_t ppb, spans, to_paged, layers;
+  uint32_t tokens, heads, row_bytes, elem;  // head-major blocks: a piece is one unit (spans = 1)
   uint64_t layer_ptr[kMaxLayers];
 };
 

@@ -818,9 +818,10 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   const bool sdma_ok = per_task <= rt->eng[dir]->stage_bytes() && !pool_dev;
   std::unique_ptr<Transfer> x = make_kv_transfer(dir, piece, ppb, reinterpret_cast<uint64_t>(host_pool), pool_cu,
                                                  pool_dev, sdma_ok, host_slots, gpu_blocks, n, rt->cfg);
-  // A pool in HBM, GPU blocks in the piece layout: one launch of the pool
-  // kernel sized to the bytes, if the table finds room (acquire).
-  x->pool_launch = pool_dev && kv.layout == MMA_KV_LAYOUT_PIECE;
+  // A pool in HBM, GPU blocks in the piece or the head-major layout: one
+  // launch of the pool kernel sized to the bytes, if the table finds room
+  // (acquire). x-packed blocks need the LDS transform of the ring path.
+  x->pool_launch = pool_dev && (kv.layout == MMA_KV_LAYOUT_PIECE || kv.layout == MMA_KV_LAYOUT_HND);
   x->t_api = t_api;
   return submit(std::move(x), n * slot_bytes, stream, &kv);
 }
