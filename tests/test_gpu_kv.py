@@ -448,11 +448,20 @@ def test_kv_hnd_offload(paths, shape, chunk):
         assert np.array_equal(pool.array.reshape(s.host_num_slots, -1), want)
 
 
-@pytest.mark.parametrize("shape", ["fp32_5tok", "llama"])
+HND_POOL_SHAPES = {
+    **HND_SHAPES,
+    # 9000 blocks of 512-byte pieces: a pool launch of 7200 workgroups with 5 pieces each, so
+    # waves move several pieces and cross from one block into the next
+    "many_small": W.KVShape(layers=2, block_tokens=16, kv_heads=1, head_dim=16, elem_bytes=2,
+                            gpu_num_blocks=9500, host_num_slots=9216, n_blocks=9000),
+}
+
+
+@pytest.mark.parametrize("shape", ["fp32_5tok", "llama", "many_small"])
 def test_kv_hnd_device_pool_roundtrip(shape):
-    """An HBM-resident pool with the head-major layout: fetch, then offload the same blocks into
-    other slots; both against the oracle."""
-    s = HND_SHAPES[shape]
+    """An HBM-resident pool with the head-major layout (one pool-kernel launch per call): fetch,
+    then offload the same blocks into other slots; both against the oracle."""
+    s = HND_POOL_SHAPES[shape]
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     with session("both", chunk_bytes=4096):
         r = np.random.default_rng(18)
