@@ -13,7 +13,8 @@ the same workload, native hipMemcpyAsync comparators, and the 64 MiB single-copy
 workload.
 
 Usage: python bench.py [--gpus 1] [--steps 10] [--warmup 2]
-       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint|control|hbmpool  (JSON per point)
+       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint|control|hbmpool|misaligned
+                                                                (JSON per point)
        python bench.py --calib                                  (counter-scaling kernels)
 """
 from __future__ import annotations
@@ -51,7 +52,7 @@ def parse():
     p.add_argument("--control", choices=["host", "device"], default=None,
                    help="who drives transfers after submission (default: the library's, MMA_CONTROL)")
     p.add_argument("--sweep", choices=["sizes", "idle", "chunks", "contention", "duplex", "paths", "footprint",
-                                       "control", "hbmpool"],
+                                       "control", "hbmpool", "misaligned"],
                    help="instead of the benchmark, print one JSON line per point of a parameter sweep")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
@@ -524,6 +525,43 @@ def sweep_sizes():
                          "mma_GBs": round(n / t_mma["p50"] / 1e6, 2), "native_GBs": round(n / t_nat["p50"] / 1e6, 2),
                          "ratio_vs_native": round(t_nat["p50"] / t_mma["p50"], 3)}
         _emit(sweep="sizes", **row)
+    h.free()
+    mma.mma_finalize()
+
+
+def sweep_misaligned():
+    """Copies whose two ends differ in alignment modulo 16 (source at +1, destination at +0, and the
+    reverse), 64 KiB to 64 MiB, both directions: the default multipath configuration against the
+    same copy with both ends aligned and against one hipMemcpyAsync of the misaligned buffers.
+    Median of HIP-event-bracketed runs on the launch stream."""
+    import ctypes
+    mma, torch, nat, st = _sweep_env()
+    mma.mma_init(0)
+    top = (64 << 20) + 64
+    h = mma.PinnedBuffer(top)
+    h.array[::4096] = 1
+    d = torch.empty(top, dtype=torch.uint8, device="cuda")
+    sp = ctypes.c_void_p(st.cuda_stream)
+    for n in [1 << k for k in range(16, 27)]:
+        reps = 30 if n <= (16 << 20) else 10
+        row = {"bytes": n}
+        for dr, name in ((0, "h2d"), (1, "d2h")):
+            res = {}
+            for tag, (so, do) in (("aligned", (0, 0)), ("src+1", (1, 0)), ("dst+1", (0, 1)), ("src+5,dst+9", (5, 9))):
+                hp, dp = (h.ptr + so, d.data_ptr() + do) if dr == 0 else (h.ptr + do, d.data_ptr() + so)
+                dst, src = (dp, hp) if dr == 0 else (hp, dp)
+                margs = (ctypes.c_void_p(dst), ctypes.c_void_p(src), ctypes.c_uint64(n), dr, sp)
+                t_mma = _timed(st, lambda: _ok(mma.lib.mma_memcpy_async(*margs)), reps, 3)
+                ent = {"mma_us": round(t_mma["p50"] * 1e3, 2), "mma_GBs": round(n / t_mma["p50"] / 1e6, 2)}
+                if tag != "aligned":
+                    D, S, Z = (ctypes.c_void_p * 1)(dst), (ctypes.c_void_p * 1)(src), (ctypes.c_uint64 * 1)(n)
+                    t_nat = _timed(st, lambda: nat.native_list(D, S, Z, 1, dr, sp), reps, 3)
+                    ent["native_us"] = round(t_nat["p50"] * 1e3, 2)
+                    ent["ratio_vs_native"] = round(t_nat["p50"] / t_mma["p50"], 3)
+                    ent["ratio_vs_aligned"] = round(res["aligned"]["mma_us"] / ent["mma_us"], 3)
+                res[tag] = ent
+            row[name] = res
+        _emit(sweep="misaligned", **row)
     h.free()
     mma.mma_finalize()
 
@@ -1064,7 +1102,8 @@ def sweep_hbmpool():
 
 
 SWEEPS = {"sizes": sweep_sizes, "idle": sweep_idle, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
-          "paths": sweep_paths, "footprint": sweep_footprint, "control": sweep_control, "hbmpool": sweep_hbmpool}
+          "paths": sweep_paths, "footprint": sweep_footprint, "control": sweep_control, "hbmpool": sweep_hbmpool,
+          "misaligned": sweep_misaligned}
 
 
 def main():

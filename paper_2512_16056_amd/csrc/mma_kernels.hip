@@ -78,28 +78,16 @@ constexpr uint64_t kBatch = 16 * kWave;  // in 16-byte units
   d[(base) + 12 * kWave] = V##12; d[(base) + 13 * kWave] = V##13; d[(base) + 14 * kWave] = V##14;          \
   d[(base) + 15 * kWave] = V##15;
 
-// Wave-cooperative copy of n bytes. Consecutive lanes move consecutive 16-byte
-// units, so each load instruction covers one contiguous 1 KiB span. Two register
-// batches ping-pong: the loads of the next batch are issued before the current
-// batch is stored, so a wave keeps up to 32 KiB of reads in flight. Byte
-// head/tail handle any alignment when src and dst are equally aligned modulo
-// 16; otherwise a byte loop is used.
-__device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
-                                          uint64_t n, uint32_t lane) {
-  if (((reinterpret_cast<uintptr_t>(src) ^ reinterpret_cast<uintptr_t>(dst)) & 15u) != 0) {
-    for (uint64_t i = lane; i < n; i += kWave) dst[i] = src[i];
-    return;
-  }
-  uint64_t head = (16u - (reinterpret_cast<uintptr_t>(src) & 15u)) & 15u;
-  if (head > n) head = n;
-  if (lane < head) dst[lane] = src[lane];
-  src += head;
-  dst += head;
-  n -= head;
-  const uint64_t n16 = n >> 4;
-  const gu4* s = (const gu4*)(src) + lane;  // generic -> global address space, this lane's unit
-  gu4* d = (gu4*)(dst) + lane;
-  const uint64_t nb = n16 / kBatch;         // full batches (wave-uniform)
+// n16 16-byte units s[0, n16) -> d[0, n16), both aligned. Consecutive lanes
+// move consecutive units, so each load instruction covers one contiguous 1 KiB
+// span. Two register batches ping-pong: the loads of the next batch are issued
+// before the current batch is stored, so a wave keeps up to 32 KiB of reads in
+// flight.
+__device__ __forceinline__ void aligned_units(const gu4* __restrict__ s0, gu4* __restrict__ d0, uint64_t n16,
+                                              uint32_t lane) {
+  const gu4* s = s0 + lane;  // this lane's unit
+  gu4* d = d0 + lane;
+  const uint64_t nb = n16 / kBatch;  // full batches (wave-uniform)
   if (nb > 0) {
     u32x4 a0, a1, a2, a3, a4, a5, a6, a7, a8, a9, a10, a11, a12, a13, a14, a15;
     u32x4 b0, b1, b2, b3, b4, b5, b6, b7, b8, b9, b10, b11, b12, b13, b14, b15;
@@ -132,9 +120,8 @@ __device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8
   const uint64_t r = nb * kBatch;
   if (r < n16) {
     const uint64_t left = n16 - r;  // units left for the whole wave, < kBatch
-    const gu4* sl = s - lane;       // the wave's first unit
     u32x4 c0, c1, c2, c3, c4, c5, c6, c7, c8, c9, c10, c11, c12, c13, c14, c15;
-#define MMA_PLD(k) c##k = sl[r + min(static_cast<uint64_t>((k) * kWave + lane), left - 1)];
+#define MMA_PLD(k) c##k = s0[r + min(static_cast<uint64_t>((k) * kWave + lane), left - 1)];
 #define MMA_PST(k) if ((k) * kWave + lane < left) d[r + (k) * kWave] = c##k;
     MMA_PLD(0) MMA_PLD(1) MMA_PLD(2) MMA_PLD(3) MMA_PLD(4) MMA_PLD(5) MMA_PLD(6) MMA_PLD(7)
     MMA_PLD(8) MMA_PLD(9) MMA_PLD(10) MMA_PLD(11) MMA_PLD(12) MMA_PLD(13) MMA_PLD(14) MMA_PLD(15)
@@ -144,9 +131,138 @@ __device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8
 #undef MMA_PLD
 #undef MMA_PST
   }
-  const uint64_t tail = n & 15u;
-  const uint64_t base = n16 << 4;
-  if (lane < tail) dst[base + lane] = src[base + lane];
+}
+
+// Bytes [4Q + r, 4Q + r + 16) of the 32 bytes lo|hi (little-endian), r < 4:
+// v_alignbyte_b32 takes 4 bytes at a byte offset out of two adjacent words.
+template <uint32_t Q>
+__device__ __forceinline__ u32x4 funnel16(const u32x4& lo, const u32x4& hi, uint32_t r) {
+  const uint32_t w[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  u32x4 o;
+  o[0] = __builtin_amdgcn_alignbyte(w[Q + 1], w[Q], r);
+  o[1] = __builtin_amdgcn_alignbyte(w[Q + 2], w[Q + 1], r);
+  o[2] = __builtin_amdgcn_alignbyte(w[Q + 3], w[Q + 2], r);
+  o[3] = __builtin_amdgcn_alignbyte(w[Q + 4], w[Q + 3], r);
+  return o;
+}
+
+// One batch of a realigning copy: rows v[0..15] hold source units
+// base + i * 64 + lane; `next` is unit base + kBatch, the same in every lane.
+// A lane's unit k + 1 is its right neighbour's unit k (ds_bpermute); lane
+// 63's is lane 0's of the next row (readlane), or `next` for the last row.
+template <uint32_t Q>
+__device__ __forceinline__ void realign_store(const u32x4 (&v)[16], const u32x4& next, gu4* __restrict__ d,
+                                              uint64_t base, uint64_t n16, uint32_t r, uint32_t lane, int right) {
+#pragma unroll
+  for (uint32_t i = 0; i < 16; ++i) {
+    u32x4 hi;
+#pragma unroll
+    for (uint32_t w = 0; w < 4; ++w) {
+      const uint32_t nb = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(right, static_cast<int>(v[i][w])));
+      const uint32_t l0 = i < 15 ? __builtin_amdgcn_readlane(v[i + 1][w], 0) : next[w];
+      hi[w] = lane == kWave - 1 ? l0 : nb;
+    }
+    const uint64_t u = base + i * kWave + lane;
+    if (u < n16) d[u] = funnel16<Q>(v[i], hi, r);
+  }
+}
+
+// n16 aligned destination units d[0, n16) from a source that starts
+// s = 4Q + r bytes (1 <= s <= 15) past the aligned unit sa[0]: unit k is bytes
+// [s, s + 16) of the aligned source units k and k + 1. Every load and store is
+// an aligned 16-byte unit; the shift happens in registers. Source units
+// [0, n16] each hold at least one byte of the source range, and loads past
+// the end are clamped to unit n16, so no load leaves the aligned units the
+// range touches; stores are predicated.
+// kDeep = false: one 16 KiB batch in flight per wave; a batch's `next` unit is
+// one more load that every lane makes at the same address (one request).
+// kDeep = true: batches ping-pong as in aligned_units -- the next batch's loads
+// are issued before this one is stored, and its first unit is this batch's
+// `next` -- for 32 KiB in flight per wave; the last batch's `next`, unit n16,
+// is read once at the start. It needs 64 more VGPRs, which only the lean
+// self-contained kernel has to spare.
+template <uint32_t Q, bool kDeep>
+__device__ void realign_units(const gu4* __restrict__ sa, gu4* __restrict__ d, uint64_t n16, uint32_t r,
+                              uint32_t lane) {
+  const int right = static_cast<int>(((lane + 1) & (kWave - 1)) << 2);  // ds_bpermute byte address
+  auto load = [&](u32x4 (&v)[16], uint64_t base) {
+#pragma unroll
+    for (uint32_t i = 0; i < 16; ++i) v[i] = sa[min(base + i * kWave + lane, n16)];
+  };
+  if constexpr (!kDeep) {
+    for (uint64_t base = 0; base < n16; base += kBatch) {
+      u32x4 v[16];
+      load(v, base);
+      const u32x4 next = sa[min(base + kBatch, n16)];
+      __builtin_amdgcn_sched_barrier(0);
+      realign_store<Q>(v, next, d, base, n16, r, lane, right);
+    }
+  } else {
+    const u32x4 last = sa[n16];
+    auto first = [&](const u32x4& v0) {
+      u32x4 x;
+#pragma unroll
+      for (uint32_t w = 0; w < 4; ++w) x[w] = __builtin_amdgcn_readlane(v0[w], 0);
+      return x;
+    };
+    u32x4 a[16], b[16];
+    load(a, 0);
+    for (uint64_t base = 0;;) {
+      if (base + kBatch >= n16) {
+        realign_store<Q>(a, last, d, base, n16, r, lane, right);
+        break;
+      }
+      load(b, base + kBatch);
+      __builtin_amdgcn_sched_barrier(0);
+      realign_store<Q>(a, first(b[0]), d, base, n16, r, lane, right);
+      base += kBatch;
+      if (base + kBatch >= n16) {
+        realign_store<Q>(b, last, d, base, n16, r, lane, right);
+        break;
+      }
+      load(a, base + kBatch);
+      __builtin_amdgcn_sched_barrier(0);
+      realign_store<Q>(b, first(a[0]), d, base, n16, r, lane, right);
+      base += kBatch;
+    }
+  }
+}
+
+// Wave-cooperative copy of n bytes. A byte head brings the destination to a
+// 16-byte boundary; the aligned middle moves in 16-byte units -- straight
+// (aligned_units) when source and destination are equally aligned modulo 16,
+// else realigned in registers (realign_units); a byte tail finishes. The head
+// and tail bytes are read first, with unconditional clamped loads, and
+// written last, so their round trips overlap the middle's instead of
+// preceding it. kDeep: see realign_units.
+template <bool kDeep = false>
+__device__ __forceinline__ void wave_copy(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                          uint64_t n, uint32_t lane) {
+  const bool rel = ((reinterpret_cast<uintptr_t>(src) ^ reinterpret_cast<uintptr_t>(dst)) & 15u) != 0;
+  uint64_t head = (16u - (reinterpret_cast<uintptr_t>(dst) & 15u)) & 15u;
+  if (head > n) head = n;
+  const uint64_t n16 = (n - head) >> 4, tail = (n - head) & 15u, tb = head + (n16 << 4);
+  uint8_t hv = 0, tv = 0;
+  if (head) hv = src[min(static_cast<uint64_t>(lane), head - 1)];
+  if (tail) tv = src[tb + min(static_cast<uint64_t>(lane), tail - 1)];
+  if (n16) {
+    const uint8_t* s = src + head;
+    gu4* d = (gu4*)(dst + head);
+    if (!rel) {
+      aligned_units((const gu4*)(s), d, n16, lane);
+    } else {
+      const uint32_t sh = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(s) & 15u);
+      const gu4* sa = (const gu4*)(s - sh);
+      switch (sh >> 2) {
+        case 0: realign_units<0, kDeep>(sa, d, n16, sh & 3u, lane); break;
+        case 1: realign_units<1, kDeep>(sa, d, n16, sh & 3u, lane); break;
+        case 2: realign_units<2, kDeep>(sa, d, n16, sh & 3u, lane); break;
+        default: realign_units<3, kDeep>(sa, d, n16, sh & 3u, lane); break;
+      }
+    }
+  }
+  if (lane < head) dst[lane] = hv;
+  if (lane < tail) dst[tb + lane] = tv;
 }
 
 // ---------------------------------------------------------------- x-packed KV layout
@@ -516,8 +632,8 @@ __global__ __launch_bounds__(kBlock) void mma_whole_kernel(WholeArgs<N> a) {
   const uint32_t lane = threadIdx.x & (kWave - 1);
   const uint32_t w = blockIdx.x * kWavesPerWG + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (w >= a.n) return;
-  wave_copy(reinterpret_cast<const uint8_t*>(a.e[w][0]), reinterpret_cast<uint8_t*>(a.e[w][1]),
-            static_cast<uint32_t>(a.e[w][2]), lane);
+  wave_copy<true>(reinterpret_cast<const uint8_t*>(a.e[w][0]), reinterpret_cast<uint8_t*>(a.e[w][1]),
+                  static_cast<uint32_t>(a.e[w][2]), lane);
   if (a.release_each) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
   if (lane == 0) st_sys(&a.done[w], make_tag(a.seq, w));
 }
@@ -722,5 +838,6 @@ hipError_t launch_digest(const void* ptr, uint64_t bytes, uint64_t* out, hipStre
   return hipLaunchKernel(reinterpret_cast<const void*>(&mma_digest_kernel), dim3(grid), dim3(256), params, 0,
                          stream);
 }
+
 
 }  // namespace mma

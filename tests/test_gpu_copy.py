@@ -367,3 +367,50 @@ def test_sync_memcpy(direction):
                 got = dst.array[:n].copy()  # no synchronisation: mma_memcpy must have finished
             assert np.array_equal(got, src_np), n
         mma.mma_synchronize()
+
+
+MISALIGNED = [(1, 0), (0, 1), (5, 9), (15, 2)]  # (source, destination) offsets modulo 16
+
+
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+@pytest.mark.parametrize("paths", ["default", *PATHS])
+def test_misaligned_large(paths, direction):
+    """Copies whose ends differ in alignment modulo 16, 1-40 MiB: whole CU-path launches below
+    the size limit and multipath transfers above it (default paths), and each path set alone.
+    The CU path realigns in registers; every byte matches the oracle and the poison around the
+    destination stays."""
+    sizes = [(1 << 20) + 3, (8 << 20) - 1, (24 << 20) - 7, (40 << 20) + 11]
+    pad = 4096
+    top = max(sizes) + 2 * pad
+    src_np = np.ascontiguousarray(W.uniform_bytes(14, direction, 0, top))
+    opts = {} if paths == "default" else PATHS[paths]
+    with session("both", **{"cu_whole_bytes": 0, "cu_whole_bytes_d2h": 0, **opts}):
+        if direction == mma.MMA_H2D:
+            src = mma.PinnedBuffer(top)
+            src.array[:] = src_np
+        else:
+            src = from_host(src_np)
+        for n in sizes:
+            for so, do in MISALIGNED:
+                log(f"misaligned paths={paths} dir={direction} n={n} src+{so} dst+{do}")
+                if direction == mma.MMA_H2D:
+                    dst = device_bytes(top, W.WEIGHT_POISON)
+                    mma.mma_memcpy_async(dst.data_ptr() + pad + do, src.ptr + so, n, direction)
+                    torch.cuda.synchronize()
+                    got = to_host(dst)
+                else:
+                    dst = mma.PinnedBuffer(top)
+                    dst.array[:] = W.WEIGHT_POISON
+                    mma.mma_memcpy_async(dst.ptr + pad + do, src.data_ptr() + so, n, direction)
+                    torch.cuda.synchronize()
+                    got = dst.array.copy()
+                    dst.free()
+                want = ocopy.memcpy(np.full(top, W.WEIGHT_POISON, np.uint8), pad + do, src_np, so, n)
+                assert np.array_equal(got, want), (n, so, do)
+        mma.mma_synchronize()
+        st = mma.mma_get_stats()
+    assert st["failed_transfers"] == 0
+    if paths == "cu":
+        assert sum(st["path_bytes"][:16]) == 0
+    if paths == "sdma":
+        assert st["path_bytes"][16] == 0
