@@ -303,6 +303,27 @@ mma_status_t mma_kv_offload(const mma_kv_layout_t* layout, void* host_pool, cons
                             const int32_t* gpu_blocks, const int32_t* host_slots, uint64_t n_blocks,
                             void* stream);
 
+/* KV fetch that allocates nothing, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. The same operation, arguments, validation and errors as
+ * mma_kv_fetch (every GPU block layout; a pinned host pool or a pool in this
+ * GPU's memory), and the same bytes in the GPU cache. It makes no hipMalloc,
+ * hipHostMalloc or hipFree call and uses no buffer of the engine: the block
+ * table and a claim counter live in `scratch`, a fixed array of the library's
+ * device code (256 B + 8 B per block, 512 KiB + 256 B in all per GPU, held
+ * until the process ends), whose address mma_init looks up. The table reaches
+ * it through the arguments of ceil(n_blocks / 448) small kernel launches on
+ * `stream`, then one launch carries every piece on the CU path alone (no copy
+ * engine, no engine thread); the transfer is complete when that launch
+ * completes on the stream, and it does not appear in mma_get_stats.
+ * n_blocks at most 65536: larger calls return MMA_ERR_INVALID_ARG and enqueue
+ * nothing. Every call on one GPU shares its scratch array, which keeps the
+ * last call's table: calls that may overlap on one GPU (other streams, other
+ * threads) race and must be ordered by the caller (one stream, or events). */
+mma_status_t mma_kv_fetch_noalloc(const mma_kv_layout_t* layout, const void* host_pool, void* const* gpu_layers,
+                                  const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n_blocks,
+                                  void* stream);
+
 /* Dependent HBM-bound check kernel (the mixed-contention workload's consumer):
  * adds, modulo 2^64, digest = sum_i (w_i + 1) * (2i + 1) over the little-endian
  * 32-bit words w_i of dev_ptr[0, bytes) (a trailing partial word is zero-

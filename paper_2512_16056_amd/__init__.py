@@ -21,6 +21,12 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmma.so")
 
 MMA_OK = 0
+MMA_ERR_NOT_INITIALIZED = -1
+MMA_ERR_INVALID_ARG = -2
+MMA_ERR_NOT_PINNED = -3
+MMA_ERR_HIP = -4
+MMA_ERR_TRANSFER_FAILED = -6
+MMA_ERR_TIMEOUT = -10
 MMA_H2D = 0
 MMA_D2H = 1
 MMA_PATH_CU = 0x80000000
@@ -136,6 +142,7 @@ _SIGNATURES = {
     # microseconds per call, as much as a small transfer's whole host-side set-up
     "mma_kv_fetch": ([ctypes.POINTER(mma_kv_layout_t), _P, _P, _P, _P, _U64, _P], _S),
     "mma_kv_offload": ([ctypes.POINTER(mma_kv_layout_t), _P, _P, _P, _P, _U64, _P], _S),
+    "mma_kv_fetch_noalloc": ([ctypes.POINTER(mma_kv_layout_t), _P, _P, _P, _P, _U64, _P], _S),
     "mma_digest_u32": ([_P, _U64, _P, _P], _S),
     "mma_get_stats": ([ctypes.POINTER(mma_stats_t)], _S),
     "mma_reset_stats": ([], _S),
@@ -303,6 +310,17 @@ def mma_kv_fetch(layout: mma_kv_layout_t, host_pool, gpu_layers, host_slots, gpu
     lt = layer_table(gpu_layers)  # a local, so the array outlives the call
     _check(lib.mma_kv_fetch(ctypes.byref(layout), _ptr(host_pool), lt,
                             hs.ctypes.data, gb.ctypes.data, hs.size, _stream(stream)), "mma_kv_fetch")
+
+
+def mma_kv_fetch_noalloc(layout: mma_kv_layout_t, host_pool, gpu_layers, host_slots, gpu_blocks,
+                         stream=None) -> None:
+    hs, gb = _i32(host_slots), _i32(gpu_blocks)
+    if hs.size != gb.size:
+        raise ValueError("host_slots and gpu_blocks differ in length")
+    lt = layer_table(gpu_layers)  # a local, so the array outlives the call
+    _check(lib.mma_kv_fetch_noalloc(ctypes.byref(layout), _ptr(host_pool), lt,
+                                    hs.ctypes.data, gb.ctypes.data, hs.size, _stream(stream)),
+           "mma_kv_fetch_noalloc")
 
 
 def mma_kv_offload(layout: mma_kv_layout_t, host_pool, gpu_layers, gpu_blocks, host_slots, stream=None) -> None:

@@ -730,6 +730,53 @@ __global__ __launch_bounds__(kBlock) void mma_transfer_xpacked_kernel(KernelArgs
   transfer_body<E>(a);
 }
 
+// ------------------------------------------------------- KV fetch that allocates nothing
+// Table chunk of a no-alloc KV fetch: entries [first, first + count) of the
+// call's block table from the arguments into the scratch array; the first
+// chunk of a call also returns the claim counter to 0.
+__global__ __launch_bounds__(kBlock) void mma_kv_noalloc_table_kernel(NoallocTabArgs a) {
+  uint64_t* tab = a.scratch + kNoallocTabOffset / 8;
+  for (uint32_t j = threadIdx.x; j < a.count; j += kBlock) tab[a.first + j] = a.e[j];
+  if (a.reset && threadIdx.x == 0) a.scratch[0] = 0;
+}
+
+// The pieces of a no-alloc KV fetch, carried by the CU path alone: a wave
+// claims per_claim consecutive pieces (piece u is piece u % ppb of table entry
+// u / ppb) from the counter in the scratch array, looks up their block, and
+// copies host slot -> paged layer in the GPU block layout of kXE (as for
+// transfer_body: 0 pieces as on the host, kXeHnd head-major, else the x-packed
+// element size). No ring, no record, no host thread: the data is complete
+// when the kernel ends, and the stream orders it for later work.
+template <uint32_t kXE>
+__global__ __launch_bounds__(kBlock) void mma_kv_noalloc_kernel(NoallocArgs a) {
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  const XGeom xg{a.tokens, a.heads, a.row_bytes, a.elem, a.lds_wave};
+  lds_u8* wave_lds = (lds_u8*)(mma_dyn_lds) + (threadIdx.x / kWave) * a.lds_wave;
+  const uint64_t* tab = a.scratch + kNoallocTabOffset / 8;
+  for (;;) {
+    uint64_t c = 0;
+    if (lane == 0)
+      c = __hip_atomic_fetch_add(a.scratch, static_cast<uint64_t>(1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    c = lane_u64(c, 0);
+    const uint64_t u0 = c * a.per_claim;
+    if (u0 >= a.units) break;
+    const uint64_t u1 = min(u0 + a.per_claim, a.units);
+    for (uint64_t u = u0; u < u1; ++u) {
+      const uint64_t i = u / a.ppb;
+      const uint32_t p = static_cast<uint32_t>(u - i * a.ppb);
+      const uint64_t e = lane_u64(tab[i], 0);
+      const uint8_t* src = reinterpret_cast<const uint8_t*>(a.pool + (e & 0xffffffffull) * a.slot_bytes + p * a.piece);
+      uint8_t* dst = reinterpret_cast<uint8_t*>(a.layer_ptr[p >> 1] + (p & 1u) * a.kstride + (e >> 32) * a.piece);
+      if constexpr (kXE == kXeHnd)
+        hnd_piece(src, dst, true, xg, lane);
+      else if constexpr (kXE != 0)
+        xpacked_piece<kXE>(src, dst, true, p & 1u, xg, wave_lds, lane);
+      else
+        wave_copy(src, dst, a.piece, lane);
+    }
+  }
+}
+
 // digest += sum_i (w_i + 1) * (2i + 1) mod 2^64 over nw words (+ one zero-padded
 // tail word of tail_len bytes at tail). vec4: w is 16-byte aligned.
 __global__ __launch_bounds__(256) void mma_digest_kernel(const uint32_t* __restrict__ w, uint64_t nw,
@@ -839,5 +886,54 @@ hipError_t launch_digest(const void* ptr, uint64_t bytes, uint64_t* out, hipStre
                          stream);
 }
 
+
+// ------------------------------------------------------- KV fetch that allocates nothing
+// The no-alloc KV fetch's claim counter and block table: a fixed array of this
+// library's device code, so that the call needs no allocation. Every GPU the
+// library runs on holds its own copy, at its own address, until the process
+// ends. In host code the array's name is only a stand-in: its device address
+// is looked up once per device (noalloc_setup, called by mma_init with that
+// device current) and only that address is used.
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+
+namespace {
+constexpr int kNoallocDevices = 64;
+uint64_t* g_scratch_dev[kNoallocDevices] = {};
+}  // namespace
+
+hipError_t noalloc_setup(int dev) {
+  if (dev < 0 || dev >= kNoallocDevices) return hipErrorInvalidDevice;
+  if (g_scratch_dev[dev]) return hipSuccess;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  if (!p || (reinterpret_cast<uintptr_t>(p) & 255u) != 0) return hipErrorInvalidSymbol;
+  g_scratch_dev[dev] = static_cast<uint64_t*>(p);
+  return hipSuccess;
+}
+
+uint64_t* noalloc_scratch(int dev) { return dev >= 0 && dev < kNoallocDevices ? g_scratch_dev[dev] : nullptr; }
+
+hipError_t launch_noalloc_table(const NoallocTabArgs& t, hipStream_t stream) {
+  void* params[] = {const_cast<NoallocTabArgs*>(&t)};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&mma_kv_noalloc_table_kernel), dim3(1), dim3(kBlock), params,
+                         0, stream);
+}
+
+hipError_t launch_noalloc(const NoallocArgs& a, uint32_t grid, hipStream_t stream) {
+  void* params[] = {const_cast<NoallocArgs*>(&a)};
+  const void* k = reinterpret_cast<const void*>(&mma_kv_noalloc_kernel<0>);
+  uint32_t lds = 0;
+  if (a.layout == kKvLayoutHnd) {
+    k = reinterpret_cast<const void*>(&mma_kv_noalloc_kernel<kXeHnd>);
+  } else if (a.layout == kKvLayoutXPacked) {
+    k = a.elem == 1   ? reinterpret_cast<const void*>(&mma_kv_noalloc_kernel<1>)
+        : a.elem == 2 ? reinterpret_cast<const void*>(&mma_kv_noalloc_kernel<2>)
+        : a.elem == 4 ? reinterpret_cast<const void*>(&mma_kv_noalloc_kernel<4>)
+                      : reinterpret_cast<const void*>(&mma_kv_noalloc_kernel<8>);
+    lds = kWavesPerWG * a.lds_wave;
+  }
+  return hipLaunchKernel(k, dim3(grid), dim3(kBlock), params, lds, stream);
+}
 
 }  // namespace mma

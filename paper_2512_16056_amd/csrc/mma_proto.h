@@ -184,6 +184,39 @@ struct WholeArgs {
   uint64_t e[N][3];
 };
 
+// KV fetch that allocates nothing (mma_kv_fetch_noalloc): its block table and
+// claim counter live in one array of the library's device code, `scratch`, of
+// kNoallocScratchBytes per GPU: word 0 is the claim counter, the table (host
+// slot | GPU block << 32 per block) starts at byte kNoallocTabOffset. The table
+// reaches it through launches of mma_kv_noalloc_table_kernel whose arguments
+// carry kNoallocTabChunk entries each; then one launch of
+// mma_kv_noalloc_kernel moves the pieces, its waves claiming per_claim pieces
+// at a time from the counter.
+constexpr uint32_t kNoallocMaxBlocks = 65536;
+constexpr uint32_t kNoallocTabOffset = 256;
+constexpr uint64_t kNoallocScratchBytes = kNoallocTabOffset + 8ull * kNoallocMaxBlocks;
+constexpr uint32_t kNoallocTabChunk = 448;
+
+struct NoallocTabArgs {
+  uint64_t* scratch;  // device address of the scratch array
+  uint32_t first;     // table entries [first, first + count)
+  uint32_t count;
+  uint32_t reset;     // 1: also return the claim counter to 0 (the first launch of a call)
+  uint32_t pad;
+  uint64_t e[kNoallocTabChunk];
+};
+
+struct NoallocArgs {
+  uint64_t* scratch;
+  uint64_t pool;        // device address of the pool
+  uint64_t slot_bytes, piece, kstride;
+  uint64_t units;       // pieces to move: blocks * ppb
+  uint32_t ppb;         // pieces per block (2 per layer: K, V)
+  uint32_t per_claim;   // pieces per claim
+  uint32_t layout, tokens, heads, row_bytes, elem, lds_wave;  // GPU block layout and its geometry
+  uint64_t layer_ptr[kMaxLayers];
+};
+
 // constexpr: usable from host and device code alike.
 constexpr uint64_t make_tag(uint64_t seq, uint64_t ticket) { return (seq << 32) | (ticket + 1); }
 

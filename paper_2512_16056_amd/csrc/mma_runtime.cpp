@@ -16,6 +16,10 @@ namespace mma {
 
 hipError_t launch_transfer(const KernelArgs& args, uint32_t grid, hipStream_t stream);
 hipError_t launch_digest(const void* ptr, uint64_t bytes, uint64_t* out, hipStream_t stream);
+hipError_t noalloc_setup(int dev);
+uint64_t* noalloc_scratch(int dev);
+hipError_t launch_noalloc_table(const NoallocTabArgs& t, hipStream_t stream);
+hipError_t launch_noalloc(const NoallocArgs& a, uint32_t grid, hipStream_t stream);
 
 namespace {
 
@@ -296,7 +300,9 @@ void remember(uint64_t id, bool host, const void* p, uint64_t bytes, int64_t dev
 }
 
 // Pinned, device-mapped host range: returns the device-visible address of p.
-mma_status_t host_range(const void* p, uint64_t bytes, uint64_t* dev_addr) {
+// If p is device memory and is_device is given, *is_device is set and
+// MMA_ERR_INVALID_ARG returned without an error message.
+mma_status_t host_range(const void* p, uint64_t bytes, uint64_t* dev_addr, bool* is_device = nullptr) {
   const uint64_t id = buffer_id(p);
   RangeCache::Entry e;
   if (id && g_ranges.find(id, true, reinterpret_cast<uint64_t>(p), bytes, &e)) {
@@ -308,7 +314,13 @@ mma_status_t host_range(const void* p, uint64_t bytes, uint64_t* dev_addr) {
     (void)hipGetLastError();
     return fail(MMA_ERR_NOT_PINNED, "host pointer %p is not pinned host memory", p);
   }
-  if (a.type == hipMemoryTypeDevice) return fail(MMA_ERR_INVALID_ARG, "%p is device memory, host memory expected", p);
+  if (a.type == hipMemoryTypeDevice) {
+    if (is_device) {
+      *is_device = true;
+      return MMA_ERR_INVALID_ARG;
+    }
+    return fail(MMA_ERR_INVALID_ARG, "%p is device memory, host memory expected", p);
+  }
   if (a.type != hipMemoryTypeHost || !a.devicePointer)
     return fail(MMA_ERR_NOT_PINNED, "host pointer %p is not pinned, device-mapped host memory", p);
   if (!within_allocation(p, bytes))
@@ -590,6 +602,16 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
       sc.bytes = need;
     }
   }
+  // The no-alloc KV fetch's scratch array: its address on this device, looked
+  // up once with the device current.
+  {
+    const hipError_t e = noalloc_setup(hip_device);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      hsa_shut_down();
+      return fail(MMA_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    }
+  }
   rt->backend.reset(new HsaBackend(rt->ag.gpu, rt->ag.cpu));
   for (int d = 0; d < 2; ++d) {
     rt->eng[d].reset(new Engine(d, k, rt->backend.get(), &rt->stats));
@@ -731,13 +753,26 @@ mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t d
   return submit(std::move(x), total, stream, nullptr);
 }
 
-static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool, const void* const* layers,
-                              const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n, int dir,
-                              void* stream) {
-  const uint64_t t_api = now_ns();
-  mma_status_t s = check_ready();
-  if (s) return s;
-  if (!n) return MMA_OK;
+// A validated KV call: geometry handed to the kernels, and where the pool is.
+struct KvCall {
+  KvGeom kv;
+  uint64_t piece = 0, slot_bytes = 0;
+  uint32_t ppb = 0;
+  uint64_t pool_cu = 0;  // the pool's device-visible address
+  bool pool_dev = false; // the pool is device memory of this GPU
+};
+
+typedef bool (*tables_check_fn)(const int32_t* src, uint32_t src_count, const int32_t* dst, uint32_t dst_count,
+                                uint64_t n);
+
+// Validation shared by the KV calls (nothing enqueued): layout, GPU block
+// layout geometry, tables (in range, distinct destinations), the pool (pinned
+// host memory, or device memory of this GPU) and the layer tensors. n > 0 and
+// the library initialised.
+static mma_status_t kv_check(const mma_kv_layout_t* lay, const void* host_pool, const void* const* layers,
+                             const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n, int dir,
+                             tables_check_fn tables, KvCall* out) {
+  mma_status_t s;
   if (!lay || !host_pool || !layers || !host_slots || !gpu_blocks)
     return fail(MMA_ERR_INVALID_ARG, "NULL argument");
   if (!lay->num_layers || lay->num_layers > kMaxLayers || !lay->block_tokens || !lay->kv_heads || !lay->head_dim ||
@@ -745,7 +780,7 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
     return fail(MMA_ERR_INVALID_ARG, "invalid KV layout");
   const uint64_t piece = static_cast<uint64_t>(lay->block_tokens) * lay->kv_heads * lay->head_dim * lay->elem_bytes;
   if (piece > (1ull << 32)) return fail(MMA_ERR_INVALID_ARG, "KV piece too large");
-  KvGeom kv;
+  KvGeom& kv = out->kv;
   kv.layout = lay->gpu_layout;
   if (lay->gpu_layout == MMA_KV_LAYOUT_XPACKED) {
     // One wave stages whole heads of one piece in LDS: the tile must hold at
@@ -785,24 +820,19 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   const uint64_t slot_bytes = piece * ppb;
   const uint64_t pool_bytes = slot_bytes * lay->host_num_slots;
   const uint64_t layer_bytes = 2 * piece * lay->gpu_num_blocks;
-  bool ok = dir == MMA_H2D ? tables_valid(host_slots, lay->host_num_slots, gpu_blocks, lay->gpu_num_blocks, n)
-                           : tables_valid(gpu_blocks, lay->gpu_num_blocks, host_slots, lay->host_num_slots, n);
+  bool ok = dir == MMA_H2D ? tables(host_slots, lay->host_num_slots, gpu_blocks, lay->gpu_num_blocks, n)
+                           : tables(gpu_blocks, lay->gpu_num_blocks, host_slots, lay->host_num_slots, n);
   if (!ok) return fail(MMA_ERR_INVALID_ARG, "block table entry out of range or duplicate destination");
-  Runtime* rt = g_rt;
-  DeviceGuard dg(rt->dev);
   // The pool is pinned host memory, or device memory of this GPU (a KV tier
   // in HBM): then the transfer is an HBM gather/scatter carried by the CU path.
   uint64_t pool_cu = 0;
   bool pool_dev = false;
-  if ((s = host_range(host_pool, pool_bytes, &pool_cu))) {
-    const std::string host_err = t_err;
-    if (s != MMA_ERR_INVALID_ARG || device_range(host_pool, pool_bytes) != MMA_OK) {
-      t_err = host_err;
-      return s;
-    }
-    pool_dev = true;
+  s = host_range(host_pool, pool_bytes, &pool_cu, &pool_dev);
+  if (pool_dev) {
+    s = device_range(host_pool, pool_bytes);
     pool_cu = reinterpret_cast<uint64_t>(host_pool);
   }
+  if (s) return s;
   kv.layers = lay->num_layers;
   kv.piece = piece;
   kv.kstride = piece * lay->gpu_num_blocks;
@@ -814,16 +844,71 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
                                        "(layer %u)", l);
     kv.layer_ptr[l] = reinterpret_cast<uint64_t>(layers[l]);
   }
-  const uint64_t per_task = std::max<uint64_t>(rt->cfg.chunk / piece, 1) * piece;
-  const bool sdma_ok = per_task <= rt->eng[dir]->stage_bytes() && !pool_dev;
-  std::unique_ptr<Transfer> x = make_kv_transfer(dir, piece, ppb, reinterpret_cast<uint64_t>(host_pool), pool_cu,
-                                                 pool_dev, sdma_ok, host_slots, gpu_blocks, n, rt->cfg);
+  out->piece = piece;
+  out->slot_bytes = slot_bytes;
+  out->ppb = ppb;
+  out->pool_cu = pool_cu;
+  out->pool_dev = pool_dev;
+  return MMA_OK;
+}
+
+static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool, const void* const* layers,
+                              const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n, int dir,
+                              void* stream) {
+  const uint64_t t_api = now_ns();
+  mma_status_t s = check_ready();
+  if (s) return s;
+  if (!n) return MMA_OK;
+  Runtime* rt = g_rt;
+  DeviceGuard dg(rt->dev);
+  KvCall c;
+  if ((s = kv_check(lay, host_pool, layers, host_slots, gpu_blocks, n, dir, tables_valid, &c))) return s;
+  const uint64_t per_task = std::max<uint64_t>(rt->cfg.chunk / c.piece, 1) * c.piece;
+  const bool sdma_ok = per_task <= rt->eng[dir]->stage_bytes() && !c.pool_dev;
+  std::unique_ptr<Transfer> x = make_kv_transfer(dir, c.piece, c.ppb, reinterpret_cast<uint64_t>(host_pool),
+                                                 c.pool_cu, c.pool_dev, sdma_ok, host_slots, gpu_blocks, n, rt->cfg);
   // A pool in HBM, GPU blocks in the piece or the head-major layout: one
   // launch of the pool kernel sized to the bytes, if the table finds room
   // (acquire). x-packed blocks need the LDS transform of the ring path.
-  x->pool_launch = pool_dev && (kv.layout == MMA_KV_LAYOUT_PIECE || kv.layout == MMA_KV_LAYOUT_HND);
+  x->pool_launch = c.pool_dev && (c.kv.layout == MMA_KV_LAYOUT_PIECE || c.kv.layout == MMA_KV_LAYOUT_HND);
   x->t_api = t_api;
-  return submit(std::move(x), n * slot_bytes, stream, &kv);
+  return submit(std::move(x), n * c.slot_bytes, stream, &c.kv);
+}
+
+// Table check of the no-alloc KV fetch: the same rule as tables_valid, with
+// fixed storage instead of a buffer per call (a bitmap over destination
+// blocks, cleared again after use, or a sorted copy for very large caches).
+std::mutex g_noalloc_mu;
+constexpr uint32_t kNoallocBitmapBits = 1u << 24;
+uint64_t g_noalloc_seen[kNoallocBitmapBits / 64];
+int32_t g_noalloc_sorted[kNoallocMaxBlocks];
+
+bool noalloc_tables_valid(const int32_t* src, uint32_t src_count, const int32_t* dst, uint32_t dst_count,
+                          uint64_t n) {
+  if (n > kNoallocMaxBlocks) return false;
+  for (uint64_t i = 0; i < n; ++i) {
+    if (src[i] < 0 || static_cast<uint32_t>(src[i]) >= src_count) return false;
+    if (dst[i] < 0 || static_cast<uint32_t>(dst[i]) >= dst_count) return false;
+  }
+  std::lock_guard<std::mutex> g(g_noalloc_mu);
+  if (dst_count <= kNoallocBitmapBits) {
+    uint64_t i = 0;
+    bool ok = true;
+    for (; i < n; ++i) {
+      uint64_t& w = g_noalloc_seen[static_cast<uint32_t>(dst[i]) >> 6];
+      const uint64_t bit = 1ull << (static_cast<uint32_t>(dst[i]) & 63u);
+      if (w & bit) {
+        ok = false;
+        break;
+      }
+      w |= bit;
+    }
+    for (uint64_t j = 0; j < i; ++j) g_noalloc_seen[static_cast<uint32_t>(dst[j]) >> 6] = 0;
+    return ok;
+  }
+  std::copy(dst, dst + n, g_noalloc_sorted);
+  std::sort(g_noalloc_sorted, g_noalloc_sorted + n);
+  return std::adjacent_find(g_noalloc_sorted, g_noalloc_sorted + n) == g_noalloc_sorted + n;
 }
 
 mma_status_t mma_kv_fetch(const mma_kv_layout_t* layout, const void* host_pool, void* const* gpu_layers,
@@ -835,6 +920,69 @@ mma_status_t mma_kv_fetch(const mma_kv_layout_t* layout, const void* host_pool, 
 mma_status_t mma_kv_offload(const mma_kv_layout_t* layout, void* host_pool, const void* const* gpu_layers,
                             const int32_t* gpu_blocks, const int32_t* host_slots, uint64_t n_blocks, void* stream) {
   return kv_common(layout, host_pool, gpu_layers, host_slots, gpu_blocks, n_blocks, MMA_D2H, stream);
+}
+
+mma_status_t mma_kv_fetch_noalloc(const mma_kv_layout_t* layout, const void* host_pool, void* const* gpu_layers,
+                                  const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n_blocks,
+                                  void* stream) {
+  mma_status_t s = check_ready();
+  if (s) return s;
+  if (!n_blocks) return MMA_OK;
+  if (n_blocks > kNoallocMaxBlocks)
+    return fail(MMA_ERR_INVALID_ARG, "mma_kv_fetch_noalloc: %llu blocks in one call, at most %u (its fixed table)",
+                static_cast<unsigned long long>(n_blocks), kNoallocMaxBlocks);
+  Runtime* rt = g_rt;
+  DeviceGuard dg(rt->dev);
+  uint64_t* scratch = noalloc_scratch(rt->dev);
+  if (!scratch) return fail(MMA_ERR_NOT_INITIALIZED, "no scratch array address for device %d", rt->dev);
+  KvCall c;
+  if ((s = kv_check(layout, host_pool, const_cast<const void* const*>(gpu_layers), host_slots, gpu_blocks, n_blocks,
+                    MMA_H2D, noalloc_tables_valid, &c)))
+    return s;
+  NoallocArgs a;
+  memset(&a, 0, sizeof a);
+  a.scratch = scratch;
+  a.pool = c.pool_cu;
+  a.slot_bytes = c.slot_bytes;
+  a.piece = c.piece;
+  a.kstride = c.kv.kstride;
+  a.ppb = c.ppb;
+  a.units = n_blocks * c.ppb;
+  a.per_claim = static_cast<uint32_t>(std::max<uint64_t>(1, rt->cfg.sub / c.piece));
+  a.layout = c.kv.layout;
+  a.tokens = c.kv.tokens;
+  a.heads = c.kv.heads;
+  a.row_bytes = c.kv.row_bytes;
+  a.elem = c.kv.elem;
+  a.lds_wave = c.kv.lds_wave;
+  memcpy(a.layer_ptr, c.kv.layer_ptr, sizeof(uint64_t) * c.kv.layers);
+  const hipStream_t hs = static_cast<hipStream_t>(stream);
+  // The table goes into the scratch array through kernel arguments, chunk by
+  // chunk, on the caller's stream: no copy call and no staging buffer.
+  NoallocTabArgs t;
+  memset(&t, 0, offsetof(NoallocTabArgs, e));
+  t.scratch = scratch;
+  for (uint64_t first = 0; first < n_blocks; first += kNoallocTabChunk) {
+    const uint32_t count = static_cast<uint32_t>(std::min<uint64_t>(kNoallocTabChunk, n_blocks - first));
+    t.first = static_cast<uint32_t>(first);
+    t.count = count;
+    t.reset = first == 0 ? 1u : 0u;
+    for (uint32_t j = 0; j < count; ++j)
+      t.e[j] = static_cast<uint64_t>(static_cast<uint32_t>(host_slots[first + j])) |
+               (static_cast<uint64_t>(static_cast<uint32_t>(gpu_blocks[first + j])) << 32);
+    const hipError_t err = launch_noalloc_table(t, hs);
+    if (err != hipSuccess) return fail(MMA_ERR_HIP, "no-alloc table launch failed: %s", hipGetErrorString(err));
+  }
+  // CU path alone: the engine thread's workgroup limit for a transfer over
+  // PCIe (1.5x for the transformed layouts); a pool in HBM gets a grid sized
+  // for HBM rates.
+  const uint64_t claims = (a.units + a.per_claim - 1) / a.per_claim;
+  const uint64_t wgs = c.kv.layout == MMA_KV_LAYOUT_PIECE ? rt->cfg.cu_wgs : (3ull * rt->cfg.cu_wgs + 1) / 2;
+  const uint64_t cap = c.pool_dev ? 2048 : std::min<uint64_t>(wgs, kMaxWorkgroups);
+  const uint32_t grid =
+      static_cast<uint32_t>(std::max<uint64_t>(1, std::min<uint64_t>((claims + kWavesPerWG - 1) / kWavesPerWG, cap)));
+  const hipError_t err = launch_noalloc(a, grid, hs);
+  return err == hipSuccess ? MMA_OK : fail(MMA_ERR_HIP, "no-alloc KV fetch launch failed: %s", hipGetErrorString(err));
 }
 
 mma_status_t mma_digest_u32(const void* dev_ptr, uint64_t bytes, uint64_t* dev_out, void* stream) {
