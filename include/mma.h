@@ -191,6 +191,8 @@ typedef struct mma_stats {
   uint32_t sdma_engines_d2h;
   uint32_t cu_path_enabled;
   uint32_t reserved;
+  uint64_t pool_launches;                 /* KV transfers with the pool in this GPU's memory carried by
+                                             one pool-kernel launch (the others took the ring path) */
 } mma_stats_t;
 
 /* One micro-task of a plan (host-only planner, exposed for verification).
@@ -236,7 +238,15 @@ mma_status_t mma_finalize(void);
 mma_status_t mma_get_config(mma_config_t* out);
 
 /* Host-side wait until every transfer submitted so far has retired, or
- * timeout_ms elapsed (MMA_ERR_TIMEOUT). Does not synchronise any stream. */
+ * timeout_ms elapsed (MMA_ERR_TIMEOUT). Does not synchronise any stream.
+ * Retired means that no path of the library touches the transfer's buffers
+ * any more. Device-to-host data is then in host memory (every wave releases
+ * at system scope before its done tag). Data written to this GPU's memory is
+ * ordered for later work by the transfer's stream, as for any copy or kernel:
+ * work on another stream must wait for that stream (an event) -- a retired
+ * transfer does not make it visible there, in particular not a KV transfer
+ * with its pool in this GPU's memory, whose workgroups release nothing when
+ * they finish (a device-wide release per workgroup costs HBM bandwidth). */
 mma_status_t mma_synchronize(uint32_t timeout_ms);
 
 /* ------------------------------------------------------------ host memory */
@@ -268,8 +278,31 @@ mma_status_t mma_memcpy_async(void* dst, const void* src, uint64_t bytes, int32_
  * engine has retired it, so a failure of this copy is returned here
  * (MMA_ERR_TRANSFER_FAILED). Arguments, pinning rules and other errors as for
  * mma_memcpy_async; MMA_ERR_TIMEOUT if the transfer is not retired within the
- * watchdog period plus 10 s. */
+ * watchdog period plus 10 s. Equal to mma_memcpy_stream(..., NULL, NULL). */
 mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir);
+
+/* What happened to the copy of a synchronous call (mma_memcpy_stream's
+ * `outcome`): NOT_ENQUEUED -- refused, or its launch failed; no part of it is
+ * in flight (an MMA_ERR_TRANSFER_FAILED here is the sticky failure of an
+ * earlier transfer). RETIRED -- every path has finished with it: MMA_OK, or
+ * MMA_ERR_TRANSFER_FAILED if this copy failed (its destination may then hold
+ * partial data, and nothing writes it any more). IN_FLIGHT -- enqueued and
+ * not retired within the limit (MMA_ERR_TIMEOUT, or MMA_ERR_HIP from the
+ * stream wait): parts of it may still be moving. */
+#define MMA_COPY_NOT_ENQUEUED 0
+#define MMA_COPY_RETIRED 1
+#define MMA_COPY_IN_FLIGHT 2
+
+/* Synchronous copy ordered on `stream`, with hipMemcpyWithStream semantics
+ * (Section 3.2: a blocking copy returns once the data has arrived): enqueued on
+ * `stream` like mma_memcpy_async, then the call waits until the stream has
+ * passed it and the engine has retired it, so this copy's own failure is
+ * returned here (MMA_ERR_TRANSFER_FAILED). If `outcome` is not NULL, it
+ * receives one of MMA_COPY_* above, which tells a caller that wants to retry
+ * the copy some other way whether that is safe (only when nothing of it is in
+ * flight). Arguments, pinning rules and other errors as for mma_memcpy. */
+mma_status_t mma_memcpy_stream(void* dst, const void* src, uint64_t bytes, int32_t dir, void* stream,
+                               int32_t* outcome);
 
 /* One logical transfer of a list of n independent copies, e.g. all weight
  * tensors of a model (Section 2.1 model wake-up; Section 5.2.2). One dummy
@@ -409,11 +442,15 @@ mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out)
  *     they submit, so the kernel's wait never sees the engines finish and its
  *     watchdog must release the stream; the count is taken back once the kernel
  *     has left, and the transfer fails (sticky).
+ *   MMA_FAULT_POOL_NO_TABLE: while value != 0, a KV transfer whose pool is in
+ *     this GPU's memory finds no room for its table in the pool kernel's table
+ *     arena, so it takes the ring path (as when the arena is full).
  * value 0 clears a fault. */
 #define MMA_FAULT_ENGINE_STALL_US 1
 #define MMA_FAULT_SDMA_SUBMIT_FAIL 2
 #define MMA_FAULT_ENGINE_IGNORE 3
 #define MMA_FAULT_DEVICE_SIGNAL_HOLD 4
+#define MMA_FAULT_POOL_NO_TABLE 5
 mma_status_t mma_test_set_fault(int32_t kind, uint64_t value);
 
 #ifdef __cplusplus

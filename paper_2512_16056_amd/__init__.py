@@ -40,6 +40,10 @@ MMA_FAULT_ENGINE_STALL_US = 1
 MMA_FAULT_SDMA_SUBMIT_FAIL = 2
 MMA_FAULT_ENGINE_IGNORE = 3
 MMA_FAULT_DEVICE_SIGNAL_HOLD = 4
+MMA_FAULT_POOL_NO_TABLE = 5
+MMA_COPY_NOT_ENQUEUED = 0
+MMA_COPY_RETIRED = 1
+MMA_COPY_IN_FLIGHT = 2
 MMA_TASK_CU_ONLY = 1
 MMA_TASK_SDMA_ONLY = 2
 
@@ -91,7 +95,8 @@ class mma_stats_t(ctypes.Structure):
                 ("sdma_foreign_busy_skips", ctypes.c_uint64), ("sdma_congestion_backoffs", ctypes.c_uint64),
                 ("sdma_commands", ctypes.c_uint64),
                 ("sdma_engines_h2d", ctypes.c_uint32), ("sdma_engines_d2h", ctypes.c_uint32),
-                ("cu_path_enabled", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+                ("cu_path_enabled", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("pool_launches", ctypes.c_uint64)]
 
     def as_dict(self):
         d = {k: getattr(self, k) for k, _ in self._fields_ if k not in ("reserved", "path_bytes", "path_tasks")}
@@ -137,6 +142,7 @@ _SIGNATURES = {
     "mma_host_free": ([_P], _S),
     "mma_memcpy_async": ([_P, _P, _U64, _I32, _P], _S),
     "mma_memcpy": ([_P, _P, _U64, _I32], _S),
+    "mma_memcpy_stream": ([_P, _P, _U64, _I32, _P, ctypes.POINTER(_I32)], _S),
     "mma_weights_load": ([ctypes.POINTER(mma_copy_desc_t), _U64, _I32, _P], _S),
     # the layer array and the two tables go as plain addresses: a ctypes pointer cast costs
     # microseconds per call, as much as a small transfer's whole host-side set-up
@@ -276,6 +282,19 @@ def mma_memcpy_async(dst, src, nbytes: int, direction: int, stream=None) -> None
 def mma_memcpy(dst, src, nbytes: int, direction: int) -> None:
     """Blocking copy on the legacy default stream; returns once the data has arrived."""
     _check(lib.mma_memcpy(_ptr(dst), _ptr(src), nbytes, direction), "mma_memcpy")
+
+
+def mma_memcpy_stream(dst, src, nbytes: int, direction: int, stream=None) -> int:
+    """Blocking copy ordered on `stream`; returns the outcome (MMA_COPY_*). A failure raises MMAError,
+    whose `outcome` attribute is set."""
+    out = ctypes.c_int32(-1)
+    st = lib.mma_memcpy_stream(_ptr(dst), _ptr(src), nbytes, direction, _stream(stream), ctypes.byref(out))
+    try:
+        _check(st, "mma_memcpy_stream")
+    except MMAError as e:
+        e.outcome = out.value
+        raise
+    return out.value
 
 
 def mma_weights_load(copies: Sequence[Tuple[object, object, int]], direction: int, stream=None) -> None:

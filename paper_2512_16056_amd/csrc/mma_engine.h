@@ -222,7 +222,7 @@ struct Config {
 
 struct Stats {
   std::atomic<uint64_t> transfers{0}, failed{0}, staging_bytes{0}, submit_failures{0}, busy_ns{0};
-  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0}, sdma_commands{0};
+  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0}, sdma_commands{0}, pool_launches{0};
   std::atomic<uint64_t> path_bytes[MMA_NUM_PATHS], path_tasks[MMA_NUM_PATHS];
   Stats() {
     for (auto& v : path_bytes) v = 0;
@@ -230,7 +230,7 @@ struct Stats {
   }
   void reset() {
     transfers = failed = staging_bytes = submit_failures = busy_ns = foreign_skips = congestion_backoffs = 0;
-    sdma_commands = 0;
+    sdma_commands = pool_launches = 0;
     for (auto& v : path_bytes) v = 0;
     for (auto& v : path_tasks) v = 0;
   }
@@ -244,7 +244,7 @@ inline std::mutex g_trace_mu;
 inline std::deque<mma_trace_rec_t> g_trace_buf;
 constexpr size_t kTraceCap = 65536;
 inline std::atomic<uint64_t> g_fault_stall_us{0}, g_fault_submit_fail{0}, g_fault_ignore{0};
-inline std::atomic<uint64_t> g_fault_signal_hold{0};
+inline std::atomic<uint64_t> g_fault_signal_hold{0}, g_fault_pool_no_table{0};
 
 // What the engine needs from the GPU side. The product backend is ROCr/HIP
 // (mma_runtime.cpp); a CPU test backend emulates it with host threads.
@@ -471,7 +471,7 @@ class Engine {
     std::unique_lock<std::mutex> lk(mu_);
     // An HBM pool launch needs room for its table in the arena; without it the
     // transfer takes the ring path like any other.
-    if (x->pool_launch) light = x->pool_launch = take_tab(x);
+    if (x->pool_launch) light = x->pool_launch = !g_fault_pool_no_table.load() && take_tab(x);
     std::deque<uint32_t>& pool = light ? free_light_ : free_recs_;
     if (pool.empty() && !wait_for_pool(lk, pool, timeout_ms)) {
       give_tab(x);
@@ -1110,6 +1110,7 @@ class Engine {
       st_->failed += 1;
     }
     if (counted) st_->transfers += 1;
+    if (x->pool_launch) st_->pool_launches += 1;
     if (g_trace.load(std::memory_order_relaxed)) record_trace(x, bad);
     if (x->waiter) {
       std::lock_guard<std::mutex> g(x->waiter->mu);

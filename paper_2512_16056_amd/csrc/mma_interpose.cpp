@@ -1,11 +1,21 @@
 // Transparent interposition (Section 3.2, Transfer Task Interceptor): loaded
 // with LD_PRELOAD, this library exports hipMemcpyAsync, hipMemcpy and
 // hipMemcpyWithStream. A host<->device copy of at least MMA_INTERPOSE_MIN_BYTES
-// (default 32 KiB, where the multipath copy starts to beat one runtime copy on
-// MI355X) goes through libmma.so; everything else, and every copy that libmma
-// refuses (pageable host memory, another device, a sticky earlier failure),
-// goes to the runtime's own function. The application is not changed and not
-// relinked.
+// (default 32 KiB) goes through libmma.so; everything else, and every copy that
+// libmma refuses before any of it is enqueued (pageable host memory, another
+// device), goes to the runtime's own function. The application is not changed
+// and not relinked.
+//
+// Failures are never silent, and a copy is never issued twice over the same
+// bytes while part of it may still be moving:
+//   - a synchronous copy (hipMemcpy, hipMemcpyWithStream) that libmma reports
+//     failed and retired -- no path writes its destination any more -- is
+//     re-issued with the runtime's copy, and the failure is written to stderr;
+//     one that is not retired within libmma's limit returns hipErrorUnknown;
+//   - an asynchronous copy fails after its call has returned, so libmma keeps
+//     the failure (sticky) and the next interposed call reports it: that call
+//     returns hipErrorUnknown and writes the failure to stderr, and libmma's
+//     sticky state is cleared so that later copies go through it again.
 //
 // The library links neither the HIP runtime nor libmma.so: both are resolved
 // at the first intercepted call, so the process keeps using the HIP runtime it
@@ -15,6 +25,7 @@
 #include <dlfcn.h>
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
+#include <stdio.h>
 #include <stdlib.h>
 
 #include <mutex>
@@ -28,7 +39,6 @@ typedef hipError_t (*async_fn)(void*, const void*, size_t, hipMemcpyKind, hipStr
 typedef hipError_t (*sync_fn)(void*, const void*, size_t, hipMemcpyKind);
 typedef hipError_t (*get_device_fn)(int*);
 typedef hipError_t (*attrs_fn)(hipPointerAttribute_t*, const void*);
-typedef hipError_t (*stream_sync_fn)(hipStream_t);
 
 struct Real {
   async_fn memcpy_async = nullptr;
@@ -36,14 +46,15 @@ struct Real {
   async_fn memcpy_with_stream = nullptr;
   get_device_fn get_device = nullptr;
   attrs_fn pointer_attributes = nullptr;
-  stream_sync_fn stream_synchronize = nullptr;
 };
 
 struct Lib {
   mma_status_t (*init)(int, const mma_config_t*) = nullptr;
   mma_status_t (*finalize)(void) = nullptr;
   mma_status_t (*memcpy_async)(void*, const void*, uint64_t, int32_t, void*) = nullptr;
-  mma_status_t (*memcpy)(void*, const void*, uint64_t, int32_t) = nullptr;
+  mma_status_t (*memcpy_stream)(void*, const void*, uint64_t, int32_t, void*, int32_t*) = nullptr;
+  mma_status_t (*clear_error)(void) = nullptr;
+  const char* (*last_error)(void) = nullptr;
 };
 
 std::once_flag g_real_once, g_lib_once;
@@ -72,7 +83,6 @@ void resolve_real() {
   g_real.memcpy_with_stream = reinterpret_cast<async_fn>(runtime_symbol(rt, "hipMemcpyWithStream"));
   g_real.get_device = reinterpret_cast<get_device_fn>(runtime_symbol(rt, "hipGetDevice"));
   g_real.pointer_attributes = reinterpret_cast<attrs_fn>(runtime_symbol(rt, "hipPointerGetAttributes"));
-  g_real.stream_synchronize = reinterpret_cast<stream_sync_fn>(runtime_symbol(rt, "hipStreamSynchronize"));
 }
 
 void finalize_at_exit() {
@@ -99,8 +109,12 @@ void load_lib() {
   g_lib.init = reinterpret_cast<decltype(g_lib.init)>(dlsym(h, "mma_init"));
   g_lib.finalize = reinterpret_cast<decltype(g_lib.finalize)>(dlsym(h, "mma_finalize"));
   g_lib.memcpy_async = reinterpret_cast<decltype(g_lib.memcpy_async)>(dlsym(h, "mma_memcpy_async"));
-  g_lib.memcpy = reinterpret_cast<decltype(g_lib.memcpy)>(dlsym(h, "mma_memcpy"));
-  if (!g_lib.init || !g_lib.finalize || !g_lib.memcpy_async || !g_lib.memcpy) return;
+  g_lib.memcpy_stream = reinterpret_cast<decltype(g_lib.memcpy_stream)>(dlsym(h, "mma_memcpy_stream"));
+  g_lib.clear_error = reinterpret_cast<decltype(g_lib.clear_error)>(dlsym(h, "mma_clear_error"));
+  g_lib.last_error = reinterpret_cast<decltype(g_lib.last_error)>(dlsym(h, "mma_last_error"));
+  if (!g_lib.init || !g_lib.finalize || !g_lib.memcpy_async || !g_lib.memcpy_stream || !g_lib.clear_error ||
+      !g_lib.last_error)
+    return;
   const mma_status_t s = g_lib.init(g_dev, nullptr);
   if (s != MMA_OK && s != MMA_ERR_ALREADY_INITIALIZED) return;
   g_on = true;
@@ -127,20 +141,63 @@ int route(void* dst, const void* src, size_t bytes, hipMemcpyKind kind) {
   return -1;
 }
 
+// An earlier asynchronous copy failed (libmma's sticky state): report it as
+// this call's error and clear it, so that later copies go through libmma again.
+hipError_t report_earlier_failure(const char* api) {
+  fprintf(stderr, "[mma_interpose] %s: an earlier copy through libmma failed, its destination may be incomplete: "
+                  "%s\n", api, g_lib.last_error());
+  g_lib.clear_error();
+  return hipErrorUnknown;
+}
+
+// A blocking copy through libmma on `stream`; falls back to the runtime copy
+// only when nothing of the libmma copy is in flight.
+hipError_t sync_copy(const char* api, void* dst, const void* src, size_t bytes, hipMemcpyKind kind, int dir,
+                     hipStream_t stream, bool* use_runtime) {
+  int32_t outcome = MMA_COPY_NOT_ENQUEUED;
+  const mma_status_t s = g_lib.memcpy_stream(dst, src, bytes, dir, stream, &outcome);
+  *use_runtime = false;
+  if (s == MMA_OK) return hipSuccess;
+  if (outcome == MMA_COPY_NOT_ENQUEUED) {
+    if (s == MMA_ERR_TRANSFER_FAILED) return report_earlier_failure(api);
+    *use_runtime = true;  // refused: the runtime copies it
+    return hipSuccess;
+  }
+  if (outcome == MMA_COPY_RETIRED) {  // this copy failed, and nothing writes its destination any more
+    fprintf(stderr, "[mma_interpose] %s: copy of %zu bytes failed in libmma (%s); copied again by the runtime\n",
+            api, bytes, g_lib.last_error());
+    g_lib.clear_error();
+    *use_runtime = true;
+    return hipSuccess;
+  }
+  fprintf(stderr, "[mma_interpose] %s: copy of %zu bytes (kind %d) did not finish in libmma (%s)\n", api, bytes,
+          static_cast<int>(kind), g_lib.last_error());
+  return hipErrorUnknown;  // parts may still be moving: a second copy could interleave with them
+}
+
 }  // namespace
 
 extern "C" {
 
 hipError_t hipMemcpyAsync(void* dst, const void* src, size_t bytes, hipMemcpyKind kind, hipStream_t stream) {
   const int dir = route(dst, src, bytes, kind);
-  if (dir >= 0 && g_lib.memcpy_async(dst, src, bytes, dir, stream) == MMA_OK) return hipSuccess;
+  if (dir >= 0) {
+    const mma_status_t s = g_lib.memcpy_async(dst, src, bytes, dir, stream);
+    if (s == MMA_OK) return hipSuccess;
+    if (s == MMA_ERR_TRANSFER_FAILED) return report_earlier_failure("hipMemcpyAsync");
+    // refused, or its launch failed: nothing of it is in flight
+  }
   if (!g_real.memcpy_async) return hipErrorNotSupported;
   return g_real.memcpy_async(dst, src, bytes, kind, stream);
 }
 
 hipError_t hipMemcpy(void* dst, const void* src, size_t bytes, hipMemcpyKind kind) {
   const int dir = route(dst, src, bytes, kind);
-  if (dir >= 0 && g_lib.memcpy(dst, src, bytes, dir) == MMA_OK) return hipSuccess;
+  if (dir >= 0) {
+    bool use_runtime = false;
+    const hipError_t e = sync_copy("hipMemcpy", dst, src, bytes, kind, dir, nullptr, &use_runtime);
+    if (!use_runtime) return e;
+  }
   if (!g_real.memcpy) return hipErrorNotSupported;
   return g_real.memcpy(dst, src, bytes, kind);
 }
@@ -148,8 +205,11 @@ hipError_t hipMemcpy(void* dst, const void* src, size_t bytes, hipMemcpyKind kin
 // Synchronous with respect to the host, ordered on `stream`.
 hipError_t hipMemcpyWithStream(void* dst, const void* src, size_t bytes, hipMemcpyKind kind, hipStream_t stream) {
   const int dir = route(dst, src, bytes, kind);
-  if (dir >= 0 && g_real.stream_synchronize && g_lib.memcpy_async(dst, src, bytes, dir, stream) == MMA_OK)
-    return g_real.stream_synchronize(stream);
+  if (dir >= 0) {
+    bool use_runtime = false;
+    const hipError_t e = sync_copy("hipMemcpyWithStream", dst, src, bytes, kind, dir, stream, &use_runtime);
+    if (!use_runtime) return e;
+  }
   if (!g_real.memcpy_with_stream) return hipErrorNotSupported;
   return g_real.memcpy_with_stream(dst, src, bytes, kind, stream);
 }

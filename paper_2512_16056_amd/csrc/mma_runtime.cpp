@@ -690,16 +690,22 @@ mma_status_t mma_memcpy_async(void* dst, const void* src, uint64_t bytes, int32_
   return mma_weights_load(&d, 1, dir, stream);
 }
 
-mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir) {
+mma_status_t mma_memcpy_stream(void* dst, const void* src, uint64_t bytes, int32_t dir, void* stream,
+                               int32_t* outcome) {
+  if (outcome) *outcome = MMA_COPY_NOT_ENQUEUED;
   std::shared_ptr<Waiter> w = std::make_shared<Waiter>();
   tl_waiter = w;
-  mma_status_t s = mma_memcpy_async(dst, src, bytes, dir, nullptr);
+  mma_status_t s = mma_memcpy_async(dst, src, bytes, dir, stream);
   tl_waiter.reset();
-  if (s) return s;
-  if (!w->submitted) return MMA_OK;  // nothing to move
+  if (s) return s;  // refused; or a failed launch, after which nothing of the copy is in flight
+  if (!w->submitted) {  // nothing to move
+    if (outcome) *outcome = MMA_COPY_RETIRED;
+    return MMA_OK;
+  }
+  if (outcome) *outcome = MMA_COPY_IN_FLIGHT;
   {
     DeviceGuard dg(g_rt->dev);
-    const hipError_t e = hipStreamSynchronize(nullptr);
+    const hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(MMA_ERR_HIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
   }
   // The stream has passed the dummy task; the engine thread retires the
@@ -716,7 +722,12 @@ mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir)
     lk.lock();
     if (!w->done) w->cv.wait_for(lk, std::chrono::microseconds(20));
   }
+  if (outcome) *outcome = MMA_COPY_RETIRED;
   return w->failed ? fail(MMA_ERR_TRANSFER_FAILED, "the copy failed") : MMA_OK;
+}
+
+mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir) {
+  return mma_memcpy_stream(dst, src, bytes, dir, nullptr, nullptr);
 }
 
 mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t dir, void* stream) {
@@ -1018,6 +1029,7 @@ mma_status_t mma_get_stats(mma_stats_t* out) {
   out->engine_wall_busy_ns = st.busy_ns;
   out->sdma_foreign_busy_skips = st.foreign_skips;
   out->sdma_commands = st.sdma_commands;
+  out->pool_launches = st.pool_launches;
   out->sdma_congestion_backoffs = st.congestion_backoffs;
   uint64_t cpu = 0;
   for (auto& e : g_rt->eng) {
@@ -1089,6 +1101,7 @@ mma_status_t mma_test_set_fault(int32_t kind, uint64_t value) {
     case MMA_FAULT_SDMA_SUBMIT_FAIL: g_fault_submit_fail = value; return MMA_OK;
     case MMA_FAULT_ENGINE_IGNORE: g_fault_ignore = value; return MMA_OK;
     case MMA_FAULT_DEVICE_SIGNAL_HOLD: g_fault_signal_hold = value; return MMA_OK;
+    case MMA_FAULT_POOL_NO_TABLE: g_fault_pool_no_table = value; return MMA_OK;
     default: return fail(MMA_ERR_INVALID_ARG, "unknown fault kind %d", kind);
   }
 }

@@ -180,15 +180,18 @@ POOL_SHAPES = {
 }
 
 
+@pytest.mark.parametrize("route", ["pool", "ring"])
 @pytest.mark.parametrize("shape", ["small", "ragged", "medium", "span_tail", "wide"])
-def test_kv_device_pool(shape):
-    """A pool in device memory: the same gather/scatter runs HBM -> HBM on the CU path
-    (one pool-kernel launch per transfer in the piece layout)."""
+def test_kv_device_pool(shape, route):
+    """A pool in device memory: the same gather/scatter runs HBM -> HBM on the CU path -- one
+    pool-kernel launch per transfer in the piece layout, or, when the pool kernel's table arena
+    has no room (forced from the host), the transfer kernel's ring path."""
     s = POOL_SHAPES[shape]
-    log(f"device pool {shape}: {s}")
+    log(f"device pool {shape} route={route}: {s}")
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     plan = W.kv_offload_plan(s, cfg=4)
     with session("both", chunk_bytes=4096):
+        mma.mma_test_set_fault(mma.MMA_FAULT_POOL_NO_TABLE, 1 if route == "ring" else 0)
         r = np.random.default_rng(9)
         pool_np = r.integers(0, 256, s.host_num_slots * s.slot_bytes, dtype=np.uint8)
         pool = torch.from_numpy(pool_np.copy()).cuda()
@@ -209,7 +212,9 @@ def test_kv_device_pool(shape):
         assert np.array_equal(to_host(pool).reshape(s.host_num_slots, -1), want)
         mma.mma_synchronize()
         st = mma.mma_get_stats()
+        mma.mma_test_set_fault(mma.MMA_FAULT_POOL_NO_TABLE, 0)
     assert sum(st["path_bytes"][:16]) == 0 and st["failed_transfers"] == 0
+    assert st["transfers"] == 2 and st["pool_launches"] == (2 if route == "pool" else 0), st
 
 
 def test_kv_device_pool_queued_launches():
@@ -457,13 +462,17 @@ HND_POOL_SHAPES = {
 }
 
 
+@pytest.mark.parametrize("route", ["pool", "ring"])
 @pytest.mark.parametrize("shape", ["fp32_5tok", "llama", "many_small"])
-def test_kv_hnd_device_pool_roundtrip(shape):
-    """An HBM-resident pool with the head-major layout (one pool-kernel launch per call): fetch,
-    then offload the same blocks into other slots; both against the oracle."""
+def test_kv_hnd_device_pool_roundtrip(shape, route):
+    """An HBM-resident pool with the head-major layout (one pool-kernel launch per call, or the
+    ring path when the table arena has no room, forced from the host): fetch, then offload the
+    same blocks into other slots; both against the oracle."""
     s = HND_POOL_SHAPES[shape]
+    log(f"head-major device pool {shape} route={route}")
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     with session("both", chunk_bytes=4096):
+        mma.mma_test_set_fault(mma.MMA_FAULT_POOL_NO_TABLE, 1 if route == "ring" else 0)
         r = np.random.default_rng(18)
         pool_np = r.integers(0, 256, s.host_num_slots * s.slot_bytes, dtype=np.uint8)
         dpool = torch.from_numpy(pool_np.copy()).cuda()
@@ -482,6 +491,10 @@ def test_kv_hnd_device_pool_roundtrip(shape):
         mma.mma_synchronize()
         want = okv.kv_offload(pv, views, gb, dest, HND, _geom(s))
         assert np.array_equal(to_host(dpool).reshape(s.host_num_slots, -1), want)
+        st = mma.mma_get_stats()
+        mma.mma_test_set_fault(mma.MMA_FAULT_POOL_NO_TABLE, 0)
+    assert st["failed_transfers"] == 0
+    assert st["transfers"] == 2 and st["pool_launches"] == (2 if route == "pool" else 0), st
 
 
 def test_kv_hnd_rejects_unsupported_geometry():
@@ -624,15 +637,13 @@ def test_kv_offload_64k_full():
 def test_kv_xpacked_fetch_offload_64k(gpu_layout):
     """The 64k-token KV fetch (8 GiB) into the x-packed or head-major GPU layout, in the
     configuration the benchmark times, then the offload of every fetched block into the host slots
-    in reverse order (a poisoned pool). For 512 sampled logical blocks every GPU block is checked
-    against the oracle in every layer, and the offloaded slot must hold the block's original bytes;
-    every untouched GPU block stays poison."""
+    in reverse order (a poisoned pool). Every layer of the GPU cache (all 4096 fetched blocks and the
+    untouched ones) and the whole 8 GiB pool after the offload are compared with the oracle."""
     LAY, GL = ((XP, mma.MMA_KV_LAYOUT_XPACKED) if gpu_layout == "xpacked"
                else (okv.LAYOUT_HND, mma.MMA_KV_LAYOUT_HND))
     s = W.KV64K
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     geom = _geom(s)
-    sample = np.random.default_rng(17).permutation(s.n_blocks)[:512]
     with session("both", cu_whole_bytes=0):
         pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
         _fill_pool_c3(pool.array, s, hs)
@@ -642,24 +653,26 @@ def test_kv_xpacked_fetch_offload_64k(gpu_layout):
         mma.mma_kv_fetch(lay, pool, layers, hs, gb)
         torch.cuda.synchronize()
         mma.mma_synchronize()
-        pool_v = pool.array.reshape(s.host_num_slots, s.layers, 2, s.piece_bytes)
-        untouched = np.setdiff1d(np.arange(s.gpu_num_blocks), gb)
+        pool_v = pool.array.reshape(s.host_num_slots, s.slot_bytes)
+        poison = np.full((2, s.gpu_num_blocks, s.piece_bytes), W.GPU_POISON, np.uint8)
         for l in range(s.layers):
+            want = okv.kv_fetch_layer(pool_v, poison, l, s.layers, hs, gb, LAY, geom)
             got = to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes)
-            for i in sample:
-                for k in (0, 1):
-                    want = okv.piece_to_block(pool_v[hs[i], l, k], k, LAY, geom)
-                    assert np.array_equal(got[k, gb[i]], want), (l, int(i), k)
-            assert np.all(got[:, untouched] == W.GPU_POISON), l
-        log(f"  {gpu_layout} fetch verified on the sample")
+            assert np.array_equal(got, want), l
+            if l % 8 == 7:
+                log(f"  {gpu_layout} fetch: layers 0..{l} match the oracle")
+        views = _layer_views(s, layers)
         dest = hs[::-1].copy()
         pool.array[:] = W.HOST_FREE_POISON
+        before = np.full((s.host_num_slots, s.slot_bytes), W.HOST_FREE_POISON, np.uint8)
         mma.mma_kv_offload(lay, pool, layers, gb, dest)
         torch.cuda.synchronize()
         mma.mma_synchronize()
-        for i in sample:
-            want = W.kv_block_bytes(3, int(i), s).reshape(s.layers, 2, s.piece_bytes)
-            assert np.array_equal(pool_v[dest[i]], want), int(i)
+        want = okv.kv_offload(before, views, gb, dest, LAY, geom)
+        del before, views
+        assert np.array_equal(pool_v, want)
+        log(f"  {gpu_layout} offload: the whole pool matches the oracle")
+        del want
         st = mma.mma_get_stats()
         pool.free()
     assert st["failed_transfers"] == 0

@@ -4,7 +4,7 @@ One schedule of ~150 operations is drawn from a seed: single copies and tensor l
 directions (1 byte to 12 MiB, odd offsets, self-contained launches, whole-CU transfers, early
 starts on idle streams, multipath transfers with merged copy-engine commands) and paged-KV
 fetches and offloads in all three GPU block layouts, a third of them with the pool in HBM (pool
-launches in the piece layout, the ring otherwise), issued in random order over four streams
+launches in the piece and head-major layouts, the ring for x-packed), issued in random order over four streams
 (including the legacy default stream). Every operation writes its own destination range and
 reads a read-only source, so the final state is unique whatever the interleaving; each
 destination (and the poison around it) is compared byte-exact with oracle.copy / oracle.kv.
@@ -111,7 +111,7 @@ def test_random_mixed_schedule(seed, control):
                 lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
                                     s.host_num_slots, xp)
                 pool_np = r.integers(0, 256, (s.host_num_slots, s.slot_bytes), dtype=np.uint8)
-                if r.integers(3) == 0:  # a pool in HBM: one pool-kernel launch (piece layout) or the ring
+                if r.integers(3) == 0:  # a pool in HBM: one pool-kernel launch (piece, head-major) or the ring
                     pool = torch.from_numpy(pool_np.reshape(-1).copy()).cuda()
                 else:
                     pool = mma.PinnedBuffer(pool_np.size)

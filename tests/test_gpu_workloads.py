@@ -1,8 +1,9 @@
-"""Full-size parity of the model wake-up and mixed-contention workloads.
+"""Full-size parity of the model wake-up, fall-asleep and mixed-contention workloads.
 
 Model wake-up: 291 Llama-3-8B-shaped bf16 tensors (16,060,522,496 B) from one pinned
 arena into separate device tensors as one logical transfer; every destination byte
-is compared with its source (oracle.copy: dst = src) and with oracle.digest.
+is compared with its source (oracle.copy: dst = src) and with oracle.digest. Fall
+asleep: the same list from device tensors back into a pinned arena.
 
 Mixed contention: the same kind of tensor list loaded on stream A as 34 groups,
 each followed on A by the dependent digest kernel over that group, while a 50%-dirty
@@ -76,6 +77,49 @@ def test_weights_wakeup_full():
         assert not bad, bad
         del dst
         arena.free()
+
+
+def test_weights_sleep_full():
+    """Model fall-asleep (Section 5.2.2, the other direction of a model switch): the same
+    291-tensor list (16,060,522,496 B) from device tensors into a poisoned pinned arena as one
+    logical device->host transfer. Each tensor's bytes must equal its source (oracle.copy:
+    dst = src) and its digest the source's, and the alignment gaps between tensors in the arena
+    must keep their poison."""
+    t0 = time.time()
+    with session("both"):
+        src_arena, sizes, offs = weights_arena(2)
+        # device tensors written by the runtime's copy, independent of this library
+        dev = [torch.from_numpy(src_arena.array[offs[t]:offs[t] + sizes[t]]).to("cuda") for t in range(len(sizes))]
+        dst_arena = mma.PinnedBuffer(src_arena.nbytes)
+        dst_arena.array[:] = W.WEIGHT_POISON
+        torch.cuda.synchronize()
+        log(f"  inputs ready in {time.time() - t0:.1f}s")
+        stream = torch.cuda.Stream()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        mma.mma_weights_load([(dst_arena.ptr + offs[t], dev[t], sizes[t]) for t in range(len(sizes))],
+                             mma.MMA_D2H, stream)
+        b.record(stream)
+        stream.synchronize()
+        mma.mma_synchronize()
+        ms = a.elapsed_time(b)
+        st = mma.mma_get_stats()
+        log(f"  fall-asleep: {ms:.1f} ms, {sum(sizes) / ms / 1e6:.2f} GB/s; cu={st['path_bytes'][16]} "
+            f"sdma={st['path_bytes'][:2]}")
+        assert st["failed_transfers"] == 0 and sum(st["path_bytes"]) == sum(sizes)
+        del dev
+
+        def check(t):
+            got = dst_arena.array[offs[t]:offs[t] + sizes[t]]
+            want = src_arena.array[offs[t]:offs[t] + sizes[t]]
+            gap_end = offs[t + 1] if t + 1 < len(sizes) else dst_arena.nbytes
+            gap_ok = bool(np.all(dst_arena.array[offs[t] + sizes[t]:gap_end] == W.WEIGHT_POISON))
+            return bool(np.array_equal(got, want)) and odigest.digest(got) == odigest.digest(want) and gap_ok
+
+        bad = [t for t, ok in enumerate(POOL.map(check, range(len(sizes)))) if not ok]
+        assert not bad, bad
+        dst_arena.free()
+        src_arena.free()
 
 
 def test_mixed_contention_full():
