@@ -198,6 +198,8 @@ struct SdmaSlot {
   int path = 0;
   uint64_t t_submit = 0;  // current copy-engine command: submission time and size
   uint64_t op_bytes = 0;
+  uint64_t ahead = 0;     // the other direction's bytes on the same engine at submission: the engine
+                          // runs one in-order queue, so they may all run before this command
 };
 
 struct SdmaPath {
@@ -218,6 +220,7 @@ struct Config {
   uint64_t whole[2];    // per direction: transfers up to this size may be taken whole by the CU path (0: never)
   uint32_t device;      // 1: device control (no engine thread in the loop)
   uint32_t device_cu_percent;  // device control: the CU path's share of a linear transfer's bytes
+  uint32_t overdue_gbs;        // link rate the overdue rule assumes, GB/s (0: 50)
 };
 
 struct Stats {
@@ -433,6 +436,21 @@ class Engine {
   }
   bool cu_enabled() const { return (cfg_.mask[dir_] & MMA_PATH_CU) != 0; }
   bool device_control() const { return cfg_.device != 0; }
+  // Both directions at once on one link (Section 5.1.2, concurrent flows):
+  // the two directions' engines share the copy engines, and each copy engine
+  // runs the commands of both directions from one in-order queue. The other
+  // direction's commands on a copy engine (peer) are neither foreign work nor
+  // congestion: a command of ours only waits behind those that were queued
+  // before it. On the mixed workload (a device-to-host KV offload beside a
+  // host-to-device weight load, whose merged commands run for milliseconds),
+  // counting that wait as congestion backed the offload's engines off about 66
+  // times per run (each command 2.3-3.4 ms at the head of this engine's view of
+  // the queue, while the other direction's commands ahead of it ran); allowing
+  // for the bytes queued ahead at submission, 0-2 times.
+  void set_peer(const Engine* peer) { peer_ = peer; }
+  // Bytes of the other direction's commands in flight on copy engine e.
+  uint64_t peer_bytes_on(int e) const { return peer_ ? peer_->eng_bytes_[e].load(std::memory_order_relaxed) : 0; }
+
   // Transfers tracked by the submitting threads are in flight (see track).
   bool tracked() const { return n_tracked_.load(std::memory_order_acquire) != 0; }
   bool has_sdma() const { return !paths_.empty(); }
@@ -1180,11 +1198,18 @@ class Engine {
     if (!s.x->t_first_sdma) s.x->t_first_sdma = now_ns();
     s.t_submit = now_ns();
     s.op_bytes = bytes;
+    s.ahead = peer_bytes_on(paths_[s.path].engine);
     SdmaPath& path = paths_[s.path];
     if (engine_ops(path) == 0) path.t_head = s.t_submit;  // (s is not in an engine state yet)
     be_->signal_store(s.sig, 1);
-    const bool ok = be_->copy(paths_[s.path].engine, dst, dst_on_device, src, src_on_device, bytes, s.sig);
-    if (ok) st_->sdma_commands += 1;
+    // counted before the command is queued, so that the other direction never
+    // sees the engine in use with none of these bytes on it
+    eng_bytes_[path.engine].fetch_add(bytes, std::memory_order_relaxed);
+    const bool ok = be_->copy(path.engine, dst, dst_on_device, src, src_on_device, bytes, s.sig);
+    if (ok)
+      st_->sdma_commands += 1;
+    else
+      eng_bytes_[path.engine].fetch_sub(bytes, std::memory_order_relaxed);
     return ok;
   }
 
@@ -1286,6 +1311,7 @@ class Engine {
       x->progress = true;
       // The engine runs our commands in order: the next one is at the head now.
       paths_[s.path].t_head = now_ns();
+      eng_bytes_[paths_[s.path].engine].fetch_sub(s.op_bytes, std::memory_order_relaxed);
       if (v < 0) {
         x->failed = true;
         if (s.state == kH2DStage) --x->sdma_cu_pending;
@@ -1376,8 +1402,8 @@ class Engine {
 
   // A path is overdue when its oldest command has been at the head of the
   // engine's queue for four times what its size needs at an equal share of a
-  // 50 GB/s link among all paths, plus 0.5 ms of slack. (Timing from
-  // submission would count the wait behind the path's own earlier commands.)
+  // 50 GB/s link (overdue_gbs) among all paths, plus 0.5 ms of slack. (Timing
+  // from submission would count the wait behind the path's own earlier commands.)
   bool overdue(const SdmaPath& path, uint64_t now) const {
     const SdmaSlot* head = nullptr;
     for (int id : path.slots) {
@@ -1387,7 +1413,11 @@ class Engine {
     if (!head) return false;
     const uint64_t npaths = paths_.size() + (cu_enabled() ? 1 : 0);
     const uint64_t since = std::max(path.t_head, head->t_submit);
-    return now > since && now - since > 4 * npaths * head->op_bytes / 50 + 500000;  // ns
+    // the other direction's commands that were on this engine when the head
+    // command was submitted may run first
+    const uint64_t bytes = head->op_bytes + head->ahead;
+    const uint64_t gbs = cfg_.overdue_gbs ? cfg_.overdue_gbs : 50;  // 1 GB/s = 1 byte per ns
+    return now > since && now - since > 4 * npaths * bytes / gbs + 500000;  // ns
   }
 
   // Paths that can make progress take work (Section 2.2; Section 3.4 contention
@@ -1417,7 +1447,8 @@ class Engine {
           free_mask = be_->engines_idle(dir_);
           have_mask = true;
         }
-        if (!(free_mask & (1u << path.engine))) {
+        // busy with work of the other direction of this library: not foreign
+        if (!(free_mask & (1u << path.engine)) && peer_bytes_on(path.engine) == 0) {
           st_->foreign_skips += 1;
           continue;
         }
@@ -1697,6 +1728,10 @@ class Engine {
   std::deque<std::unique_ptr<Transfer>> tracked_;
   std::atomic<uint64_t> n_tracked_{0};
   uint64_t inflight_ = 0;
+  // Bytes of this engine's commands in flight per copy engine; read by the
+  // other direction's engine thread.
+  std::atomic<uint64_t> eng_bytes_[MMA_MAX_SDMA] = {};
+  const Engine* peer_ = nullptr;          // the other direction's engine
   bool stop_ = false;
   bool engine_waiting_ = false;  // the engine thread waits on cv_ (guarded by mu_)
   std::atomic<bool> stop_flag_{false};

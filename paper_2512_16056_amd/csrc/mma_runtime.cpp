@@ -624,6 +624,8 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
     }
     set_affinity_local(rt->eng[d]->native_handle(), hip_device);
   }
+  rt->eng[MMA_D2H]->set_peer(rt->eng[MMA_H2D].get());
+  rt->eng[MMA_H2D]->set_peer(rt->eng[MMA_D2H].get());
   if (env_u64("MMA_TRACE", 0)) g_trace = 1;
   g_rt = rt.release();
   return MMA_OK;
@@ -637,6 +639,8 @@ mma_status_t mma_finalize(void) {
   if (!drained) return fail(MMA_ERR_TIMEOUT, "in-flight transfers did not drain");
   {
     DeviceGuard dg(g_rt->dev);
+    // each engine thread reads the other engine's counters: stop both before freeing either
+    for (auto& e : g_rt->eng) e->shutdown();
     for (auto& e : g_rt->eng) e.reset();
   }
   if (g_rt->hsa_up) hsa_shut_down();

@@ -133,13 +133,24 @@ class FakeBackend final : public Backend {
     Eng* e = engines_[engine].get();
     {
       std::lock_guard<std::mutex> g(e->mu);
-      e->q.push_back({dst, src, bytes, sig});
+      e->q.push_back({dst, src, bytes, sig, 0});
       e->pending.fetch_add(1);
       e->bytes_total += bytes;
       e->commands += 1;
     }
     e->cv.notify_all();
     return true;
+  }
+  // Another component's command on engine e (not this library's): it keeps the
+  // engine busy for hold_ns and signals nothing.
+  void foreign(int e, uint64_t hold_ns) {
+    Eng* p = engines_[e].get();
+    {
+      std::lock_guard<std::mutex> g(p->mu);
+      p->q.push_back({nullptr, nullptr, 0, 0, hold_ns});
+      p->pending.fetch_add(1);
+    }
+    p->cv.notify_all();
   }
   uint32_t engines_idle(int) override {
     uint32_t m = 0;
@@ -158,6 +169,7 @@ class FakeBackend final : public Backend {
     const void* src;
     uint64_t bytes;
     uint64_t sig;
+    uint64_t hold_ns;  // foreign work: no copy, no signal
   };
   struct Eng {
     double rate = 1000;
@@ -179,8 +191,16 @@ class FakeBackend final : public Backend {
         c = e->q.front();
         e->q.pop_front();
       }
-      sleep_ns(cmd_ns_ + static_cast<uint64_t>(c.bytes * 1000.0 / e->rate));
+      if (c.hold_ns) {
+        sleep_ns(c.hold_ns);
+        e->pending.fetch_sub(1);
+        continue;
+      }
+      // the command lands after its modelled time; the host's memcpy runs inside it
+      const auto end = std::chrono::steady_clock::now() +
+                       std::chrono::nanoseconds(cmd_ns_ + static_cast<uint64_t>(c.bytes * 1000.0 / e->rate));
       std::memcpy(c.dst, c.src, c.bytes);
+      std::this_thread::sleep_until(end);
       e->pending.fetch_sub(1);
       signal_sub(c.sig, 1);  // a landed command decrements its signal
     }
@@ -408,6 +428,7 @@ struct Setup {
   double wave_rate = 250;                          // bytes/us per wave
   uint64_t cmd_ns = 20000;
   uint32_t mask = MMA_PATH_CU | 0x3;
+  uint32_t mask_d2h = 0;  // device-to-host paths, when not `mask` (copy engines a subset of mask's)
   Config cfg{};
 };
 
@@ -433,19 +454,23 @@ class Harness {
  public:
   explicit Harness(const Setup& s) : s_(s), be_(s.engine_rates, s.cmd_ns) {
     Config c = s.cfg;
-    c.mask[0] = c.mask[1] = s.mask;
+    c.mask[MMA_H2D] = s.mask;
+    c.mask[MMA_D2H] = s.mask_d2h ? s.mask_d2h : s.mask;
     stage_bytes_ = std::max<uint64_t>(c.chunk, 2 * 1024 * 1024);
     const uint32_t engines = static_cast<uint32_t>(__builtin_popcount(s.mask & 0xFFFFu));
     staging_.assign(2 * engines * c.depth * stage_bytes_ + 1, 0);
     for (int d = 0; d < 2; ++d) {
       eng_[d].reset(new Engine(d, c, &be_, &stats_));
       void* base = engines ? staging_.data() + d * engines * c.depth * stage_bytes_ : nullptr;
-      const mma_status_t rc = eng_[d]->init(s.mask & 0xFFFFu, stage_bytes_, base);
+      const mma_status_t rc = eng_[d]->init(c.mask[d] & 0xFFFFu, stage_bytes_, base);
       CHECK(rc == MMA_OK, "engine init %d: %s", rc, t_err.c_str());
     }
+    eng_[MMA_D2H]->set_peer(eng_[MMA_H2D].get());  // as mma_init
+    eng_[MMA_H2D]->set_peer(eng_[MMA_D2H].get());
     cfg_ = c;
   }
   ~Harness() {
+    for (auto& e : eng_) e->shutdown();  // each engine thread reads the other's counters
     for (auto& e : eng_) e.reset();
   }
   // The runtime's submit(), with the fake stream in place of the kernel launch.
@@ -1325,26 +1350,103 @@ double timed_copy(double cu_rate, double eng_rate, uint32_t static_cu_percent, b
   return ms;
 }
 
+// Another component's command on a copy engine: a path whose engine is in use
+// while none of our commands is on it takes no work until the engine is free.
+void foreign_work_skipped() {
+  Setup s;
+  s.cfg = default_config();
+  s.engine_rates = {4000, 4000};
+  s.cmd_ns = 5000;
+  Harness h(s);
+  FakeStream st;
+  h.backend().foreign(0, 1500ull * 1000 * 1000);  // engine 0 busy for 1.5 s
+  const uint64_t n = 8 * 1024 * 1024 + 7;
+  auto src = random_bytes(n, 41);
+  std::vector<uint8_t> dst(n);
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, st);
+  st.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst == src, "bytes differ");
+  CHECK(h.stats().foreign_skips.load() > 0, "engine 0 busy with foreign work was not skipped");
+  CHECK(h.stats().path_tasks[0].load() == 0, "engine 0 took %llu micro-tasks while busy with foreign work",
+        (unsigned long long)h.stats().path_tasks[0].load());
+  std::printf("ok   a copy engine busy with foreign work is skipped (%llu skips; engine 1 %llu, CU %llu tasks)\n",
+              (unsigned long long)h.stats().foreign_skips.load(), (unsigned long long)h.stats().path_tasks[1].load(),
+              (unsigned long long)h.stats().path_tasks[16].load());
+}
+
+// Both directions on the same two copy engines, each engine running the
+// commands of both from one in-order queue (Section 5.1.2, concurrent flows): a
+// large host-to-device copy keeps merged 8 MiB commands queued on both engines
+// while device-to-host copies (copy engines only) arrive one by one. The other
+// direction's commands on an engine are neither foreign work (no skip) nor
+// congestion: a device-to-host command waits for the 16 MiB queued before it,
+// about four times the allowance for its own size, and within the allowance once
+// those bytes count. Modelled engines at 2 GB/s, the overdue rule set for an
+// 8 GB/s link, so that the host's memcpy stays inside the modelled times.
+void duplex_peer_commands() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.chunk = 512 * 1024;
+  s.cfg.fallback = 512 * 1024;
+  s.cfg.merge = 16;  // commands up to 8 MiB
+  s.cfg.overdue_gbs = 8;
+  s.engine_rates = {2000, 2000};
+  s.cmd_ns = 2000;
+  s.mask = MMA_PATH_CU | 0x3;
+  s.mask_d2h = 0x3;
+  Harness h(s);
+  FakeStream a, b;
+  const uint64_t n = 192ull * 1024 * 1024 + 3, m = 1536 * 1024 + 5;
+  const int k = 16;
+  auto src = random_bytes(n, 51);
+  std::vector<uint8_t> dst(n);
+  std::vector<std::vector<uint8_t>> dsrc, ddst;
+  for (int i = 0; i < k; ++i) {
+    dsrc.push_back(random_bytes(m, 60 + i));
+    ddst.emplace_back(m, 0);
+  }
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, a);
+  sleep_ns(5000000);  // its commands are on both engines
+  for (int i = 0; i < k; ++i) {  // arriving one by one while the large copy runs
+    h.submit(linear(MMA_D2H, ddst[i].data(), dsrc[i].data(), m, h.cfg()), m, b);
+    sleep_ns(1000000);
+  }
+  a.synchronize();
+  b.synchronize();
+  CHECK(h.sync(), "sync");
+  CHECK(dst == src, "host-to-device bytes differ");
+  for (int i = 0; i < k; ++i) CHECK(ddst[i] == dsrc[i], "device-to-host copy %d differs", i);
+  const uint64_t skips = h.stats().foreign_skips.load(), backoffs = h.stats().congestion_backoffs.load();
+  std::printf("     duplex: foreign skips %llu, congestion back-offs %llu\n", (unsigned long long)skips,
+              (unsigned long long)backoffs);
+  CHECK(skips == 0, "the other direction's commands counted as foreign work (%llu skips)",
+        (unsigned long long)skips);
+  CHECK(backoffs <= 1, "the other direction's commands counted as congestion (%llu back-offs; about 8 when they are)",
+        (unsigned long long)backoffs);
+  std::printf("ok   the other direction's commands on a shared copy engine are neither foreign work nor congestion\n");
+}
+
 void pull_tracks_best_static_split() {
   for (double ratio : {1.0, 2.0}) {
     const double eng = 1000, cu = 1000 * ratio;  // CU path ratio x faster
     double best = 1e30;
     std::printf("     rate ratio CU:SDMA = %g:1 -- static", ratio);
-    // best of three runs each: the fake paths are host threads that sleep
-    auto best_of3 = [&](uint32_t pct, bool pull) {
+    // best of five runs each: the fake paths are host threads that sleep
+    auto best_of5 = [&](uint32_t pct, bool pull) {
       double t = 1e30;
-      for (int r = 0; r < 3; ++r) t = std::min(t, timed_copy(cu, eng, pct, pull));
+      for (int r = 0; r < 5; ++r) t = std::min(t, timed_copy(cu, eng, pct, pull));
       return t;
     };
     for (uint32_t pct : {0u, 33u, 50u, 67u, 100u}) {
-      const double t = best_of3(pct, false);
+      const double t = best_of5(pct, false);
       best = std::min(best, t);
       std::printf(" %u%%=%.1fms", pct, t);
     }
-    const double p = best_of3(0, true);
+    const double p = best_of5(0, true);
     std::printf(" | pull=%.1fms\n", p);
-    // Quiet machines give pull <= best static; the bound leaves room for a busy host's sleep jitter.
-    CHECK(p <= best * 1.15, "pull %.1f ms vs best static %.1f ms at ratio %g", p, best, ratio);
+    // Quiet machines give pull <= best static (0.92-1.02 here); 5% allows for a busy host.
+    CHECK(p <= best * 1.05, "pull %.1f ms vs best static %.1f ms at ratio %g", p, best, ratio);
     std::printf("     pull / best static = %.3f\n", p / best);
   }
   std::printf("ok   pull-based selection tracks the best fixed split at 1:1 and 2:1\n");
@@ -1379,8 +1481,10 @@ int main(int argc, char** argv) {
     device_recycling_and_refusals();
     device_unlaunched_and_whole();
     shutdown_in_flight_keeps_shared_memory();
+    foreign_work_skipped();
   }
   if (timing) {
+    duplex_peer_commands();
     slow_engine_gets_fewer_tasks();
     pull_tracks_best_static_split();
   }

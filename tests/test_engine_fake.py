@@ -5,8 +5,11 @@ are host threads with a set rate and per-command cost, the dummy-task kernel is 
 host threads that follow the record protocol, device memory is host memory. It checks
 byte-exact copies, tensor lists and paged-KV fetch/offload through staging, that every
 micro-task is retired once, merged copy-engine commands, re-routed submit failures, two
-streams in flight, that a slower engine pulls fewer micro-tasks, and that pull-based
-selection tracks the best fixed split (the paper's static-split comparison, Section 5.1.2).
+streams in flight, that an engine busy with another component's work is skipped, that the
+other direction's commands on a shared engine count as neither foreign work nor congestion
+(Section 5.1.2, concurrent flows), that a slower engine pulls fewer micro-tasks, and that
+pull-based selection comes within 5% of the best fixed split (the paper's static-split
+comparison, Section 5.1.2).
 Under device control (no engine thread in the loop) it checks exact copies on idle streams
 (copy engines and CU path) and busy ones (CU path only), KV fetch and offload, records
 recycled by later submissions, refused commands re-routed, a transfer larger than a ring
@@ -46,8 +49,9 @@ def test_engine_on_fake_paths(tmp_path):
     exe = str(tmp_path / "engine_fake")
     _build(cxx, exe, ["-O2", "-Wall"])
     _run(exe, ["--no-timing"])
-    # The rate-dependent scenarios (a slower engine pulls fewer micro-tasks; pull vs the best
-    # fixed split) emulate path rates with sleeps; one re-measurement absorbs a noisy host.
+    # The rate-dependent scenarios (both directions on shared engines; a slower engine pulls
+    # fewer micro-tasks; pull vs the best fixed split) model path rates with timed sleeps; one
+    # re-measurement absorbs a noisy host.
     for attempt in range(2):
         r = subprocess.run([exe, "--timing-only"], capture_output=True, text=True, timeout=600)
         print(r.stdout)
