@@ -221,7 +221,9 @@ mma_status_t mma_config_default(mma_config_t* out);
  * D2H engines). cfg == NULL: defaults, then MMA_* environment overrides
  * (MMA_CHUNK_BYTES, MMA_FALLBACK_BYTES, MMA_SMALL_BYTES, MMA_QUEUE_DEPTH,
  * MMA_CU_QUEUE_DEPTH, MMA_BACKOFF_DEPTH, MMA_PATHS_H2D, MMA_PATHS_D2H,
- * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS, MMA_SDMA_MERGE_TASKS, MMA_TRACE).
+ * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS, MMA_SDMA_MERGE_TASKS,
+ * MMA_CU_WHOLE_BYTES, MMA_CU_WHOLE_BYTES_D2H, MMA_CONTROL, MMA_STATIC_CU_PERCENT,
+ * MMA_TRACE).
  * Errors: MMA_ERR_ALREADY_INITIALIZED, MMA_ERR_INVALID_ARG (bad device or
  * config), MMA_ERR_HIP / MMA_ERR_HSA. */
 mma_status_t mma_init(int hip_device, const mma_config_t* cfg);

@@ -6,7 +6,8 @@ scope, where the preloaded library comes first), move seeded bytes in each direc
 its own. Each result is compared with oracle.copy and read back over a route that stays
 with the runtime (pageable host memory). Per call, the library's statistics tell whether
 the copy went through it (and which paths carried it). With the argument "faults", the
-failure handling is checked with host-forced faults instead. Prints one JSON line.
+failure handling is checked with host-forced faults instead, and with "defaults" which copies go
+through the library when MMA_INTERPOSE_SYNC is not set. Prints one JSON line.
 """
 import ctypes
 import json
@@ -141,6 +142,24 @@ def faults(mma):
     return out
 
 
+def defaults(mma):
+    """The interposer's defaults: an asynchronous pinned copy goes through the library, a blocking one
+    stays with the runtime (MMA_INTERPOSE_SYNC unset); both exact."""
+    out = {}
+    n = (40 << 20) + 3
+    stream = torch.cuda.current_stream().cuda_stream
+    src_np = seeded(n, 202)
+    src = torch.from_numpy(src_np).pin_memory()
+    for route in ("hipMemcpyAsync", "hipMemcpy", "hipMemcpyWithStream"):
+        dst = torch.full((n,), POISON, dtype=torch.uint8, device="cuda")
+        before = stats(mma)
+        rc = call(route, dst, src, n, H2D, stream)
+        torch.cuda.synchronize()
+        mma.mma_synchronize()
+        out[route] = {"rc": rc, "exact": bool(np.array_equal(dst.cpu().numpy(), src_np)), **delta(before, stats(mma))}
+    return out
+
+
 def main():
     torch.cuda.set_device(0)
     import paper_2512_16056_amd as mma  # the library the interposer loaded (same path, same instance)
@@ -150,6 +169,8 @@ def main():
     torch.cuda.synchronize()
     if len(sys.argv) > 1 and sys.argv[1] == "faults":
         res = faults(mma)
+    elif len(sys.argv) > 1 and sys.argv[1] == "defaults":
+        res = defaults(mma)
     else:
         res = routes(mma)
     print(json.dumps(res), flush=True)

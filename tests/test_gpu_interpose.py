@@ -27,10 +27,13 @@ LIB = os.path.join(ROOT, "paper_2512_16056_amd", "libmma_interpose.so")
 THRESHOLD = 32 * 1024
 
 
-def run_child(control: str, *args):
+def run_child(control: str, *args, sync: bool = True):
     assert os.path.exists(LIB), "build with python paper_2512_16056_amd/build.py"
     env = dict(os.environ)
     env["MMA_CONTROL"] = control  # the interposer initialises the library from the environment
+    env.pop("MMA_INTERPOSE_SYNC", None)
+    if sync:  # blocking copies through the library too (off by default)
+        env["MMA_INTERPOSE_SYNC"] = "1"
     # keep whatever is preloaded already; add the interposer after it
     env["LD_PRELOAD"] = (env.get("LD_PRELOAD", "") + " " + LIB).strip()
     env["MMA_WATCHDOG_MS"] = "2000"
@@ -74,3 +77,12 @@ def test_interposed_failures():
     assert "an earlier copy through libmma failed" in err
     # the state is cleared: copies go through libmma again
     assert res["after_rc"] == 0 and res["after_exact"] and res["after"]["transfers"] == 1, res
+
+
+def test_interposer_defaults():
+    """Without MMA_INTERPOSE_SYNC, blocking copies stay with the runtime (on one GPU a blocking caller
+    does not wait less through the library); asynchronous ones go through it."""
+    res, _ = run_child("0", "defaults", sync=False)
+    assert all(r["rc"] == 0 and r["exact"] for r in res.values()), res
+    assert res["hipMemcpyAsync"]["transfers"] == 1, res
+    assert res["hipMemcpy"]["transfers"] == 0 and res["hipMemcpyWithStream"]["transfers"] == 0, res
