@@ -13,7 +13,7 @@ the same workload, native hipMemcpyAsync comparators, and the 64 MiB single-copy
 workload.
 
 Usage: python bench.py [--gpus 1] [--steps 10] [--warmup 2]
-       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint|control|hbmpool|misaligned
+       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint|control|hbmpool|misaligned|mixed
                                                                 (JSON per point)
        python bench.py --calib                                  (counter-scaling kernels)
 """
@@ -52,8 +52,12 @@ def parse():
     p.add_argument("--control", choices=["host", "device"], default=None,
                    help="who drives transfers after submission (default: the library's, MMA_CONTROL)")
     p.add_argument("--sweep", choices=["sizes", "idle", "chunks", "contention", "duplex", "paths", "footprint",
-                                       "control", "hbmpool", "misaligned"],
+                                       "control", "hbmpool", "misaligned", "mixed"],
                    help="instead of the benchmark, print one JSON line per point of a parameter sweep")
+    p.add_argument("--oracle-cores", default=None,
+                   help=argparse.SUPPRESS)  # the all-cores oracle baseline's worker process (CPU only)
+    p.add_argument("--sizes", default=None,
+                   help="comma-separated transfer sizes in bytes for --sweep idle (default: 32 KiB to 8 GiB)")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
     return p.parse_args()
@@ -194,12 +198,165 @@ def link_peaks(mma, nat, stream, sdma_mask):
                      **{k: (round(v, 2) if v else None) for k, v in rates.items()},
                      "zero_copy_best_grid": best_grid,
                      "sdma_mask": hex(sdma_mask)}
-    del dbuf
+    # Both directions at once: one hipMemcpyAsync of 1 GiB each way on two streams (median of 3);
+    # the aggregate is the reference for transfers that overlap in both directions.
+    hbuf2 = mma.PinnedBuffer(n)
+    hbuf2.array[::4096] = 1
+    dbuf2 = torch.empty(n, dtype=torch.uint8, device="cuda")
+    s2 = torch.cuda.Stream()
+    D1, S1, Z = (ctypes.c_void_p * 1)(dbuf.data_ptr()), (ctypes.c_void_p * 1)(hbuf.ptr), (ctypes.c_uint64 * 1)(n)
+    D2, S2 = (ctypes.c_void_p * 1)(hbuf2.ptr), (ctypes.c_void_p * 1)(dbuf2.data_ptr())
+    agg = []
+    for _ in range(4):
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        e[2].record(s2)
+        nat.native_list(D1, S1, Z, 1, 0, ctypes.c_void_p(stream.cuda_stream))
+        nat.native_list(D2, S2, Z, 1, 1, ctypes.c_void_p(s2.cuda_stream))
+        e[1].record(stream)
+        e[3].record(s2)
+        torch.cuda.synchronize()
+        agg.append(n / e[0].elapsed_time(e[1]) / 1e6 + n / e[2].elapsed_time(e[3]) / 1e6)
+    res["duplex_GBs"] = round(sorted(agg[1:])[1], 2)
+    del dbuf, dbuf2
     hbuf.free()
+    hbuf2.free()
     return res
 
 
-def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_step, total, out):
+def gpu_local_cpus(torch):
+    """(NUMA node, its CPUs) of GPU 0, from sysfs; (None, []) when unknown."""
+    p = torch.cuda.get_device_properties(0)
+    dev = f"/sys/bus/pci/devices/{p.pci_domain_id:04x}:{p.pci_bus_id:02x}:{p.pci_device_id:02x}.0"
+    try:
+        node = int(open(os.path.join(dev, "numa_node")).read().strip())
+        cpus = []
+        for part in open(os.path.join(dev, "local_cpulist")).read().strip().split(","):
+            a, _, b = part.partition("-")
+            cpus.extend(range(int(a), int(b or a) + 1))
+        return node, cpus
+    except (OSError, ValueError):
+        return None, []
+
+
+# One GPU's job on these hosts gets a 16-CPU share of the machine, whatever the node holds.
+HOST_CPU_SHARE = 16
+
+
+def oracle_all_cores(torch, seconds):
+    """The oracle KV fetch spread over one process per core: the CPUs of the GPU's NUMA node that
+    this process may use (at most the job's CPU share), each process pinned to one of them and
+    working on its own disjoint slices of the 4096-entry block table (64 blocks x one layer per
+    call). Aggregate payload GB/s over the slowest worker's time."""
+    import subprocess
+    node, local = gpu_local_cpus(torch)
+    allowed = sorted(os.sched_getaffinity(0))
+    use = [c for c in local if c in set(allowed)] or allowed
+    use = use[:HOST_CPU_SHARE]
+    r = subprocess.run([sys.executable, os.path.abspath(__file__), "--oracle-cores", ",".join(map(str, use)),
+                        "--cpu-seconds", str(seconds)], capture_output=True, text=True, timeout=600)
+    lines = [x for x in r.stdout.splitlines() if x.startswith("{")]
+    if r.returncode != 0 or not lines:
+        return {"value": None, "error": f"exit {r.returncode}: {r.stderr[-300:]}"}
+    res = json.loads(lines[-1])
+    res.update({"numa_node": node, "node_cpus": len(local), "cpus_allowed": len(allowed),
+                "cpu_share_cap": HOST_CPU_SHARE})
+    return res
+
+
+def oracle_cores_worker(cores, seconds):
+    """Child of oracle_all_cores (no GPU in this process): a pageable copy of the pool's shape,
+    then one forked worker per core, released together, each running oracle.kv.kv_fetch_layer
+    over its own (layer, 64-block slice) tasks until the deadline; one JSON line."""
+    import numpy as np
+
+    import workloads as W
+    from oracle import kv as okv
+    s = W.KV64K
+    hs, _ = W.kv_fetch_tables(s, cfg=3)
+    pool = np.empty((s.host_num_slots, s.slot_bytes), np.uint8)
+    with ThreadPoolExecutor(len(cores)) as ex:  # touch every page before the workers fork
+        list(ex.map(lambda i: pool[i:i + 64].fill(0x3C), range(0, s.host_num_slots, 64)))
+    span = 64
+    tasks = [(l, a) for l in range(s.layers) for a in range(0, s.n_blocks, span)]
+    poison = np.full((2, span, s.piece_bytes), W.GPU_POISON, np.uint8)
+    local_blocks = np.arange(span, dtype=np.int32)
+    go_r, go_w = os.pipe()
+    res_r, res_w = os.pipe()
+    kids = []
+    for k, core in enumerate(cores):
+        pid = os.fork()
+        if pid == 0:
+            os.close(go_w)
+            os.close(res_r)
+            os.sched_setaffinity(0, {core})
+            mine = tasks[k::len(cores)]
+            okv.kv_fetch_layer(pool, poison, mine[0][0], s.layers, hs[mine[0][1]:mine[0][1] + span], local_blocks)
+            os.read(go_r, 1)  # released together
+            t0 = time.perf_counter()
+            done = 0
+            while True:
+                for l, a in mine:
+                    okv.kv_fetch_layer(pool, poison, l, s.layers, hs[a:a + span], local_blocks)
+                    done += span * 2 * s.piece_bytes
+                if time.perf_counter() - t0 >= seconds:
+                    break
+            os.write(res_w, f"{done} {time.perf_counter() - t0}\n".encode())
+            os._exit(0)
+        kids.append(pid)
+    os.close(go_r)
+    os.close(res_w)
+    os.write(go_w, b"x" * len(cores))
+    out = b""
+    while True:
+        chunk = os.read(res_r, 4096)
+        if not chunk:
+            break
+        out += chunk
+    for pid in kids:
+        os.waitpid(pid, 0)
+    rows = [x.split() for x in out.decode().splitlines() if x.strip()]
+    moved = sum(int(a) for a, _ in rows)
+    wall = max(float(b) for _, b in rows)
+    print(json.dumps({"value": round(moved / wall / 1e9, 3), "unit": "GB/s", "cores": len(rows), "kind": "oracle",
+                      "cpus": cores, "sample": f"{moved / s.slot_bytes / s.n_blocks:.1f} x the 64k-token fetch "
+                      f"(oracle.kv.kv_fetch_layer on (layer, 64-block) slices of the table), {len(rows)} processes "
+                      f"pinned one per CPU, {wall:.1f} s"}), flush=True)
+
+
+def run_native_batch(s, hs, gb):
+    """One hipMemcpyBatchAsync of the 262,144 pieces of the 64k-token fetch, from the standalone
+    comparator program (it links the system ROCm runtime, which exports the call), run as its
+    own process with the same block tables. Its JSON line, or the reason it has none."""
+    import subprocess
+    import tempfile
+
+    import numpy as np
+    exe = os.path.join(ROOT, "paper_2512_16056_amd", "native_batch")
+    if not os.path.exists(exe):
+        return {"available": False, "error": "native_batch not built"}
+    with tempfile.NamedTemporaryFile(suffix=".i32", delete=False) as f:
+        f.write(np.concatenate([hs, gb]).astype(np.int32).tobytes())
+        path = f.name
+    try:
+        r = subprocess.run([exe, path, str(s.n_blocks), str(s.layers), str(s.piece_bytes), str(s.gpu_num_blocks),
+                            str(s.host_num_slots), "3"], capture_output=True, text=True, timeout=300)
+    except subprocess.TimeoutExpired:
+        return {"available": False, "error": "timed out after 300 s"}
+    finally:
+        os.unlink(path)
+    if r.returncode < 0 or r.returncode >= 128:
+        # the comparator died (a signal, e.g. a fault): touch the GPU no further in this process
+        raise SystemExit(f"native_batch ended with status {r.returncode}: {r.stderr[-500:]}")
+    lines = [x for x in r.stdout.splitlines() if x.startswith("{")]
+    if r.returncode != 0 or not lines:
+        return {"available": False, "error": f"exit {r.returncode}: {(r.stderr or r.stdout)[-300:]}"}
+    return json.loads(lines[-1])
+
+
+def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_step, total, out,
+               native_batch=None):
     import ctypes
     extras = {}
     nat = native_lib()
@@ -212,18 +369,24 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
     out["roofline"]["frac_of_measured"] = round(out["roofline"]["achieved"] / m_h2d, 4)
     log("measured link:", peaks)
 
-    # native per-piece hipMemcpyAsync KV fetch (262,144 copies), and the batched call if present
+    # native KV fetch comparators: (n1) 262,144 per-piece hipMemcpyAsync calls, host-timed from the
+    # first call to the stream's completion; (n2) one hipMemcpyBatchAsync with the same 262,144
+    # entries, event-timed in its own process (run_native_batch). "Native" is the best of the two.
     lp = (ctypes.c_void_p * s.layers)(*[t.data_ptr() for t in layers])
     hs_c, gb_c = hs.ctypes.data_as(ctypes.c_void_p), gb.ctypes.data_as(ctypes.c_void_p)
-    for fn_name in ("native_kv_fetch", "native_kv_fetch_batch"):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        rc = getattr(nat, fn_name)(pool.ptr, lp, hs_c, gb_c, s.n_blocks, s.layers, s.piece_bytes, s.gpu_num_blocks,
-                                   ctypes.c_void_p(stream.cuda_stream))
-        stream.synchronize()
-        extras[f"{fn_name}_ms"] = round((time.perf_counter() - t0) * 1e3, 2) if rc == 0 else None
-    if extras.get("native_kv_fetch_ms"):
-        extras["kv_fetch_speedup_vs_native"] = round(extras["native_kv_fetch_ms"] / ms_per_step, 2)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    rc = nat.native_kv_fetch(pool.ptr, lp, hs_c, gb_c, s.n_blocks, s.layers, s.piece_bytes, s.gpu_num_blocks,
+                             ctypes.c_void_p(stream.cuda_stream))
+    stream.synchronize()
+    extras["native_kv_fetch_ms"] = round((time.perf_counter() - t0) * 1e3, 2) if rc == 0 else None
+    nb = native_batch or {"available": False, "error": "not run"}
+    extras["native_kv_fetch_batch"] = nb
+    extras["native_kv_fetch_batch_ms"] = nb.get("ms_median") if nb.get("ok") else None
+    natives = [v for v in (extras["native_kv_fetch_ms"], extras["native_kv_fetch_batch_ms"]) if v]
+    if natives:
+        extras["native_kv_fetch_best_ms"] = min(natives)
+        extras["kv_fetch_speedup_vs_native"] = round(min(natives) / ms_per_step, 3)
 
     # the 64 MiB single-copy workload: MMA vs one hipMemcpyAsync, 50 runs each after 5 warm-ups
     n = W.COPY64_BYTES
@@ -360,11 +523,91 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
     # digest kernel over the group, while the 2048-block offload runs on stream B; 256 KiB chunks.
     extras["mixed_contention"] = mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan,
                                                   arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
+    mc = extras["mixed_contention"]
+    mc["duplex_probe_GBs"] = peaks.get("duplex_GBs")
+    if mc["mma"].get("overlap_aggregate_GBs") and peaks.get("duplex_GBs"):
+        mc["overlap_frac_of_duplex_probe"] = round(mc["mma"]["overlap_aggregate_GBs"] / peaks["duplex_GBs"], 3)
+
+    # All five workloads under both control modes, with the engine threads' CPU time per call.
+    extras["control_modes"] = control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_blocks, plan,
+                                            arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
+    extras["device_control"] = extras["control_modes"]["device"]["kv_fetch_64k"]
     del wdst
     arena.free()
-
-    extras["device_control"] = device_control_leg(mma, torch, pool, layers, lay, hs, gb, stream, total)
     return extras
+
+
+def control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_blocks, plan, arena, offs, sizes, wdst,
+                  Dw, Sw, Zw, lp):
+    """The five workloads under host control (engine threads pull for every path) and device control
+    (the calling thread plans each transfer, the dummy-task kernel alone tracks it), each on a
+    stream of its own: median time and GB/s, and the engine threads' CPU time per call (their
+    CPU-time delta over the timed calls, read after they have gone idle)."""
+    import ctypes
+    stream = torch.cuda.Stream()
+    n64 = W.COPY64_BYTES
+    src64 = mma.PinnedBuffer(n64)
+    src64.array[:] = W.uniform_bytes(1, W.TAG_DATA, 0, n64)
+    dst64 = torch.empty(n64, dtype=torch.uint8, device="cuda")
+    wtotal = sum(sizes)
+    lst = [(wdst[t], arena.ptr + offs[t], sizes[t]) for t in range(len(sizes))]
+    off_bytes = len(src_blocks) * s.slot_bytes
+    total = s.n_blocks * s.slot_bytes
+    margs = (ctypes.c_void_p(dst64.data_ptr()), ctypes.c_void_p(src64.ptr), ctypes.c_uint64(n64), mma.MMA_H2D,
+             ctypes.c_void_p(stream.cuda_stream))
+
+    def cpu_ns():
+        mma.mma_synchronize()
+        time.sleep(0.005)  # past the engine threads' spin after their last transfer
+        return mma.mma_get_stats()["engine_cpu_ns"]
+
+    def leg(fn, reps, warm, nbytes):
+        for _ in range(warm):
+            fn()
+        stream.synchronize()
+        c0 = cpu_ns()
+        t = _timed(stream, fn, reps=reps, warm=0)
+        c1 = cpu_ns()
+        return {"ms": round(t["p50"], 3), "GBs": round(nbytes / t["p50"] / 1e6, 2),
+                "engine_cpu_ms_per_call": round((c1 - c0) / 1e6 / reps, 3)}
+
+    out = {}
+    cfg0 = mma.mma_get_config()
+    mma.mma_finalize()
+    try:
+        for mode, code in (("host", mma.MMA_CONTROL_HOST), ("device", mma.MMA_CONTROL_DEVICE)):
+            c = mma.mma_config_default()
+            c.control = code
+            mma.mma_init(0, c)
+            r = {"copy_64mib": leg(lambda: _ok(mma.lib.mma_memcpy_async(*margs)), 20, 3, n64),
+                 "weights_wakeup_291": leg(lambda: mma.mma_weights_load(lst, mma.MMA_H2D, stream), 2, 1, wtotal),
+                 "kv_fetch_64k": leg(lambda: mma.mma_kv_fetch(lay, pool, layers, hs, gb, stream), 3, 1, total),
+                 "kv_offload_2048": leg(lambda: mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, stream),
+                                        3, 1, off_bytes)}
+            ok64 = bool(np.array_equal(dst64[:1 << 20].cpu().numpy(), src64.array[:1 << 20]))
+            r["copy_64mib"]["sampled_parity"] = ok64
+            r["kv_fetch_64k"]["sampled_parity"] = sampled_fetch_parity(
+                s, pool.array.reshape(s.host_num_slots, s.slot_bytes), layers, hs, gb, lay.gpu_layout, samples=16,
+                seed=3)
+            r["failed_transfers"] = mma.mma_get_stats()["failed_transfers"]
+            mma.mma_finalize()
+            c.chunk_bytes = 256 << 10
+            mma.mma_init(0, c)
+            c0 = cpu_ns()
+            a_ms, b_ms = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan,
+                                                    arena, offs, sizes, wdst, Dw, Sw, Zw, lp, reps=1)
+            c1 = cpu_ns()
+            r["mixed_contention"] = {"stream_a_weights_digests_ms": round(a_ms, 1),
+                                     "stream_b_offload_ms": round(b_ms, 1),
+                                     "engine_cpu_ms_per_schedule": round((c1 - c0) / 1e6 / 2, 3)}
+            r["failed_transfers"] += mma.mma_get_stats()["failed_transfers"]
+            mma.mma_finalize()
+            out[mode] = r
+            log(f"control {mode}:", r)
+    finally:
+        mma.mma_init(0, cfg0)
+    src64.free()
+    return out
 
 
 def sampled_fetch_parity(s, pv, layers, hs, gb, gpu_layout, samples=64, seed=0):
@@ -388,37 +631,6 @@ def sampled_fetch_parity(s, pv, layers, hs, gb, gpu_layout, samples=64, seed=0):
             want = want.reshape(B_, H_, D_ * E_).transpose(1, 0, 2).reshape(-1)
         ok &= bool(np.array_equal(got, want))
     return ok
-
-
-def device_control_leg(mma, torch, pool, layers, lay, hs, gb, stream, total):
-    """The 64k-token fetch again under device control (the calling thread plans the transfer, the
-    dummy-task kernel alone tracks it; the stream has the start event pending, so the CU path
-    carries it), with the engine threads' CPU time per step; then the default session again."""
-    mma.mma_synchronize()
-    mma.mma_finalize()
-    cfg = mma.mma_config_default()
-    cfg.control = mma.MMA_CONTROL_DEVICE
-    mma.mma_init(0, cfg)
-    try:
-        import workloads as W
-        for t_ in layers:  # poison the cache so that the parity check sees this leg's bytes
-            t_.fill_(W.GPU_POISON)
-        torch.cuda.synchronize()
-        t = _timed(stream, lambda: mma.mma_kv_fetch(lay, pool, layers, hs, gb, stream), reps=5, warm=1)
-        mma.mma_synchronize()
-        st = mma.mma_get_stats()
-        s = W.KV64K
-        pv = pool.array.reshape(s.host_num_slots, s.slot_bytes)
-        ok = sampled_fetch_parity(s, pv, layers, hs, gb, lay.gpu_layout, seed=1)
-        res = {"kv_fetch_ms": round(t["p50"], 3), "kv_fetch_ms_p10_p90": [round(t["p10"], 3), round(t["p90"], 3)],
-               "kv_fetch_GBs": round(total / t["p50"] / 1e6, 2),
-               "engine_cpu_ms_per_step": round(st["engine_cpu_ns"] / 1e6 / 6, 3),
-               "failed_transfers": st["failed_transfers"], "sampled_parity": ok}
-    finally:
-        mma.mma_finalize()
-        mma.mma_init(0)
-    log("device control:", res)
-    return res
 
 
 def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan, arena, offs, sizes, wdst,
@@ -473,9 +685,13 @@ def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, p
         ok = True
         for t in [int(x) for x in r.integers(len(sizes), size=8)]:
             ok &= bool(np.array_equal(wdst[t][:65536].cpu().numpy(), arena.array[offs[t]:offs[t] + min(65536, sizes[t])]))
+        wtotal, off_bytes = sum(sizes), len(src_blocks) * s.slot_bytes
+        # both directions over the offload's time: its bytes, plus the weight bytes moved meanwhile
+        # at stream A's average rate
+        agg = (off_bytes + wtotal / a_ms * b_ms) / b_ms / 1e6 if b_ms <= a_ms else None
         res["mma"] = {"stream_a_weights_digests_ms": round(a_ms, 1), "stream_b_offload_ms": round(b_ms, 1),
-                      "makespan_ms": round(max(a_ms, b_ms), 1), "sampled_parity": ok,
-                      "failed_transfers": mma.mma_get_stats()["failed_transfers"]}
+                      "makespan_ms": round(max(a_ms, b_ms), 1), "overlap_aggregate_GBs": round(agg, 1) if agg else None,
+                      "sampled_parity": ok, "failed_transfers": mma.mma_get_stats()["failed_transfers"]}
     finally:
         mma.mma_finalize()
         mma.mma_init(0, cfg)
@@ -483,6 +699,8 @@ def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, p
     res["native"] = {"stream_a_weights_digests_ms": round(a_ms, 1), "stream_b_offload_ms": round(b_ms, 1),
                      "makespan_ms": round(max(a_ms, b_ms), 1)}
     res["makespan_speedup_vs_native"] = round(res["native"]["makespan_ms"] / res["mma"]["makespan_ms"], 3)
+    res["stream_a_ratio_vs_native"] = round(res["native"]["stream_a_weights_digests_ms"] /
+                                            res["mma"]["stream_a_weights_digests_ms"], 3)
     res["chunk_bytes"] = 256 << 10
     return res
 
@@ -566,46 +784,73 @@ def sweep_misaligned():
     mma.mma_finalize()
 
 
-def sweep_idle():
+def sweep_idle(sizes=None):
     """Host wall time from the call to the return of hipStreamSynchronize, on a stream with nothing
     pending (the case of the idle-stream early start), for the default multipath configuration and
-    one hipMemcpyAsync, alternating; median of 50 after 10 discarded. Also the share of transfers
-    whose copy engines started before the kernel's start signal (trace: started < 3 us after
-    submission)."""
+    one hipMemcpyAsync, alternating; the median after discarded warm-up calls (50 of 60 up to
+    64 MiB, fewer above). Also the share of transfers whose copy engines started before the
+    kernel's start signal (trace: started < 3 us after submission)."""
     import ctypes
     import numpy as np
     mma, torch, nat, st = _sweep_env()
     mma.mma_init(0)
-    top = 64 << 20
+    sizes = sizes or [32 << 10, 64 << 10, 256 << 10, 1 << 20, 4 << 20, 8 << 20, 16 << 20, 32 << 20, 64 << 20,
+                      256 << 20, 1 << 30, 8 << 30]
+    top = max(sizes)
     h = mma.PinnedBuffer(top)
     h.array[::4096] = 1
     d = torch.empty(top, dtype=torch.uint8, device="cuda")
     sp = ctypes.c_void_p(st.cuda_stream)
-    for n in (4 << 20, 8 << 20, 16 << 20, 32 << 20, 64 << 20):
+    # The platform's own round trips on an idle stream: a one-workgroup kernel (the digest kernel over
+    # 4 bytes) and a 4-byte hipMemcpyAsync, each from the call to the return of hipStreamSynchronize.
+    out8 = torch.zeros(1, dtype=torch.int64, device="cuda")
+    D4, S4, Z4 = (ctypes.c_void_p * 1)(d.data_ptr()), (ctypes.c_void_p * 1)(h.ptr), (ctypes.c_uint64 * 1)(4)
+    tk, tc = [], []
+    for _ in range(60):
+        st.synchronize()
+        t0 = time.perf_counter()
+        _ok(mma.lib.mma_digest_u32(ctypes.c_void_p(d.data_ptr()), ctypes.c_uint64(4), ctypes.c_void_p(out8.data_ptr()),
+                                   sp))
+        st.synchronize()
+        tk.append((time.perf_counter() - t0) * 1e6)
+        t0 = time.perf_counter()
+        nat.native_list(D4, S4, Z4, 1, 0, sp)
+        st.synchronize()
+        tc.append((time.perf_counter() - t0) * 1e6)
+    _emit(sweep="idle", reference="round trips of the platform, idle stream",
+          tiny_kernel_us=round(float(np.median(tk[10:])), 1), tiny_copy_us=round(float(np.median(tc[10:])), 1))
+    for n in sizes:
+        reps, skip = (60, 10) if n <= (64 << 20) else ((14, 4) if n <= (1 << 30) else (5, 1))
         row = {"bytes": n}
         for dr, name in ((0, "h2d"), (1, "d2h")):
             dst, src = (d.data_ptr(), h.ptr) if dr == 0 else (h.ptr, d.data_ptr())
             D, S, Z = (ctypes.c_void_p * 1)(dst), (ctypes.c_void_p * 1)(src), (ctypes.c_uint64 * 1)(n)
             margs = (ctypes.c_void_p(dst), ctypes.c_void_p(src), ctypes.c_uint64(n), dr, sp)
-            tn, tm = [], []
+            tn, tm, an, am = [], [], [], []
             mma.mma_trace_enable(True)
-            for _ in range(60):
+            for _ in range(reps):
                 st.synchronize()
                 t0 = time.perf_counter()
                 nat.native_list(D, S, Z, 1, dr, sp)
+                t1 = time.perf_counter()
                 st.synchronize()
                 tn.append((time.perf_counter() - t0) * 1e6)
+                an.append((t1 - t0) * 1e6)
                 time.sleep(0.0002)
                 t0 = time.perf_counter()
                 _ok(mma.lib.mma_memcpy_async(*margs))
+                t1 = time.perf_counter()
                 st.synchronize()
                 tm.append((time.perf_counter() - t0) * 1e6)
+                am.append((t1 - t0) * 1e6)
             mma.mma_synchronize()
-            tr = mma.mma_trace_read()[-60:]
+            tr = mma.mma_trace_read()[-reps:]
             mma.mma_trace_enable(False)
             early = sum(1 for r in tr if r["t_started_ns"] and r["t_started_ns"] - r["t_submit_ns"] < 3000)
-            m, nt = float(np.median(tm[10:])), float(np.median(tn[10:]))
+            m, nt = float(np.median(tm[skip:])), float(np.median(tn[skip:]))
             row[name] = {"mma_us": round(m, 1), "native_us": round(nt, 1), "ratio_vs_native": round(nt / m, 3),
+                         "mma_call_us": round(float(np.median(am[skip:])), 1),
+                         "native_call_us": round(float(np.median(an[skip:])), 1),
                          "early_start_frac": round(early / max(1, len(tr)), 2)}
         _emit(sweep="idle", **row)
     h.free()
@@ -909,6 +1154,115 @@ def sweep_duplex():
     pool.free()
 
 
+def sweep_mixed(sizes=None, rounds=6):
+    """The mixed-contention workload (the 291-tensor list as 34 groups on stream A, each followed by
+    the dependent digest kernel; the 2048-block KV offload on stream B; 256 KiB micro-tasks) under
+    path assignments per direction, against the same schedule with native copies. The cases are
+    interleaved over `rounds` rounds (a fresh library per run, one warm-up schedule, one timed), and
+    every run is reported: both streams' times and the link aggregate while both directions run
+    (bytes of B plus the bytes A moved meanwhile at its average rate, over B's time)."""
+    import ctypes
+
+    import numpy as np
+
+    import workloads as W
+    mma, torch, nat, _ = _sweep_env()
+    s = W.KV64K
+    plan = W.kv_offload_plan(s, cfg=4)
+    mma.mma_init(0)
+    pool = mma.PinnedBuffer(s.host_num_slots * s.slot_bytes)
+    pool.array[::4096] = 1
+    sizes_w = W.weight_tensor_bytes()
+    offs, wtotal = W.arena_offsets(sizes_w, 256)
+    arena = mma.PinnedBuffer(wtotal)
+    arena.array[::4096] = 0x3C
+    mma.mma_finalize()
+    layers = [torch.zeros(s.layer_bytes, dtype=torch.uint8, device="cuda") for _ in range(s.layers)]
+    lay = mma.kv_layout(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                        s.host_num_slots)
+    hs, gb = W.kv_fetch_tables(s, cfg=3)
+    src_blocks = gb[plan.dirty].astype(np.int32)
+    off_bytes = len(plan.dirty) * s.slot_bytes
+    wdst = [torch.empty(k, dtype=torch.uint8, device="cuda") for k in sizes_w]
+    Dw = (ctypes.c_void_p * len(sizes_w))(*[t.data_ptr() for t in wdst])
+    Sw = (ctypes.c_void_p * len(sizes_w))(*[arena.ptr + o for o in offs])
+    Zw = (ctypes.c_uint64 * len(sizes_w))(*sizes_w)
+    lp = (ctypes.c_void_p * s.layers)(*[t.data_ptr() for t in layers])
+    CU = mma.MMA_PATH_CU
+    cases = [("default", {}),
+             ("h2d cu + engine 0, d2h engine 1", dict(path_mask_h2d=CU | 1, path_mask_d2h=2)),
+             ("d2h engines 2-5", dict(path_mask_d2h=0x3C)),
+             ("native", None)]
+    for rnd in range(rounds):
+        for name, kv in cases[rnd % len(cases):] + cases[:rnd % len(cases)]:
+            c = mma.mma_config_default()
+            c.chunk_bytes = 256 << 10
+            for k, v in (kv or {}).items():
+                setattr(c, k, v)
+            mma.mma_init(0, c)
+            mma.mma_trace_enable(True)
+            a, b = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
+                                              offs, sizes_w, wdst, Dw, Sw, Zw, lp, native=kv is None, reps=1)
+            mma.mma_synchronize()
+            st = mma.mma_get_stats()
+            tr = mma.mma_trace_read()
+            mma.mma_trace_enable(False)
+            mma.mma_finalize()
+            # micro-tasks per path of the timed schedule's transfers (the second half of the records)
+            tr = tr[len(tr) // 2:]
+            paths = {}
+            for d, key in ((0, "h2d_tasks"), (1, "d2h_tasks")):
+                tot = [0] * 17
+                for r_ in tr:
+                    if r_["dir"] == d:
+                        tot = [x + y for x, y in zip(tot, r_["path_tasks"])]
+                paths[key] = {("cu" if i == 16 else f"e{i}"): v for i, v in enumerate(tot) if v}
+            agg = (off_bytes + wtotal / a * b) / b / 1e6 if b <= a else None
+            _emit(sweep="mixed", round=rnd, case=name, stream_a_weights_digests_ms=round(a, 1),
+                  stream_b_offload_ms=round(b, 1), overlap_aggregate_GBs=round(agg, 1) if agg else None,
+                  failed=st["failed_transfers"], backoffs=st["sdma_congestion_backoffs"], **paths)
+    arena.free()
+    pool.free()
+
+
+def mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena, offs, sizes,
+                               wdst, Dw, Sw, Zw, lp, native=False, reps=1):
+    """The mixed-contention schedule (stream A: 34 groups, each loaded and then digested; stream B:
+    the offload), once to warm up and then `reps` times; the median stream times in ms."""
+    import ctypes
+    groups = W.weight_groups()
+    digests = torch.zeros(len(sizes), dtype=torch.int64, device="cuda")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    out = []
+    for _ in range(reps + 1):
+        ea = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        eb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ea[0].record(sa)
+        for g in groups:
+            if not native:
+                mma.mma_weights_load([(wdst[t], arena.ptr + offs[t], sizes[t]) for t in g], mma.MMA_H2D, sa)
+            else:
+                o = 8 * g[0]
+                nat.native_list(ctypes.addressof(Dw) + o, ctypes.addressof(Sw) + o, ctypes.addressof(Zw) + o,
+                                len(g), 0, ctypes.c_void_p(sa.cuda_stream))
+            for t in g:
+                mma.mma_digest_u32(wdst[t], sizes[t], digests.data_ptr() + 8 * t, sa)
+        ea[1].record(sa)
+        eb[0].record(sb)
+        if not native:
+            mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, sb)
+        else:
+            nat.native_kv_offload(pool.ptr, lp, src_blocks.ctypes.data_as(ctypes.c_void_p),
+                                  plan.dest.ctypes.data_as(ctypes.c_void_p), len(src_blocks), s.layers,
+                                  s.piece_bytes, s.gpu_num_blocks, ctypes.c_void_p(sb.cuda_stream))
+        eb[1].record(sb)
+        torch.cuda.synchronize()
+        out.append((ea[0].elapsed_time(ea[1]), eb[0].elapsed_time(eb[1])))
+    out = out[1:]
+    return sorted(x[0] for x in out)[len(out) // 2], sorted(x[1] for x in out)[len(out) // 2]
+
+
 def sweep_paths():
     """Bandwidth against the path set (single-GPU analog of the paper's bandwidth-vs-paths study):
     a 1 GiB copy each way and a 1024-block (2 GiB) KV fetch with one engine, both host-facing
@@ -1098,7 +1452,7 @@ def sweep_hbmpool():
 
 SWEEPS = {"sizes": sweep_sizes, "idle": sweep_idle, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
           "paths": sweep_paths, "footprint": sweep_footprint, "control": sweep_control, "hbmpool": sweep_hbmpool,
-          "misaligned": sweep_misaligned}
+          "misaligned": sweep_misaligned, "mixed": sweep_mixed}
 
 
 def main():
@@ -1108,8 +1462,14 @@ def main():
     if args.calib:
         calibration_kernels()
         return
+    if args.oracle_cores:
+        oracle_cores_worker([int(c) for c in args.oracle_cores.split(",")], args.cpu_seconds)
+        return
     if args.sweep:
-        SWEEPS[args.sweep]()
+        if args.sizes:
+            SWEEPS[args.sweep](sizes=[int(x, 0) for x in args.sizes.split(",")])
+        else:
+            SWEEPS[args.sweep]()
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the multipath path here is the single-GPU share (SDMA engines + "
@@ -1120,15 +1480,21 @@ def main():
     import ctypes
 
     import numpy as np
-    import torch
 
-    import paper_2512_16056_amd as mma
     import workloads as W
 
-    torch.cuda.set_device(0)
     s = W.KV64K
     hs, gb = W.kv_fetch_tables(s, cfg=3)
     total = s.n_blocks * s.slot_bytes
+    # The batched native comparator runs as its own process, before this one touches the GPU.
+    native_batch = None if args.no_extras else run_native_batch(s, hs, gb)
+    log("native hipMemcpyBatchAsync:", native_batch)
+
+    import torch
+
+    import paper_2512_16056_amd as mma
+
+    torch.cuda.set_device(0)
 
     mma.mma_init(0)  # defaults, then MMA_* environment overrides
     cfg = mma.mma_get_config().as_dict()
@@ -1186,6 +1552,17 @@ def main():
     ok = sampled_fetch_parity(s, pv, layers, hs, gb, lay.gpu_layout)
     log(f"sampled parity: {'ok' if ok else 'MISMATCH'}")
 
+    # ---- host-observed latency: the call to the return of hipStreamSynchronize, stream idle
+    host_ms = []
+    for _ in range(5):
+        stream.synchronize()
+        t0 = time.perf_counter()
+        mma.mma_kv_fetch(lay, pool, layers, hs, gb, stream)
+        stream.synchronize()
+        host_ms.append((time.perf_counter() - t0) * 1e3)
+    hp = _pcts(host_ms)
+    log(f"host-observed fetch latency: {hp['p50']:.3f} ms (p10 {hp['p10']:.3f}, p90 {hp['p90']:.3f})")
+
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -1215,6 +1592,8 @@ def main():
         },
         "kv_fetch_latency_ms": round(avg_kernel_ms, 3),
         "kv_fetch_latency_ms_p10_p50_p90": [round(kp[k], 3) for k in ("p10", "p50", "p90")],
+        "kv_fetch_host_latency_ms": round(hp["p50"], 3),
+        "kv_fetch_host_latency_ms_p10_p50_p90": [round(hp[k], 3) for k in ("p10", "p50", "p90")],
         "sampled_parity": ok,
         "path_bytes": {"cu": stats["path_bytes"][16],
                        **{f"sdma{e}": stats["path_bytes"][e] for e in range(16) if stats["path_bytes"][e]}},
@@ -1240,7 +1619,8 @@ def main():
 
     extras = {}
     if not args.no_extras:
-        extras = run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_step, total, out)
+        extras = run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_step, total, out,
+                            native_batch)
         log("extras:", extras)
     out["extras"] = extras
 
@@ -1259,25 +1639,10 @@ def main():
                                "kind": "oracle",
                                "sample": f"{reps} x the full 4096-block 64k-token KV fetch (oracle.kv.kv_fetch_layer "
                                          f"over 32 layers, numpy slice copies, one thread), {dt:.1f} s"}
-        # The same oracle calls spread over every core this process may use (one layer per task):
-        # context for the host's own copy bandwidth.
-        ncores = min(16, len(os.sched_getaffinity(0)))
-
-        def layer_task(l_):
-            okv.kv_fetch_layer(pv, poison, l_, s.layers, hs, gb)
-
-        reps, t0 = 0, time.perf_counter()
-        with ThreadPoolExecutor(ncores) as ex:
-            while True:
-                list(ex.map(layer_task, range(s.layers)))
-                reps += 1
-                if time.perf_counter() - t0 >= args.cpu_seconds / 2:
-                    break
-        dt = time.perf_counter() - t0
-        out["cpu_baseline_all_cores"] = {"value": round(total * reps / dt / 1e9, 3), "unit": "GB/s",
-                                         "cores": ncores, "kind": "oracle",
-                                         "sample": f"{reps} x the full fetch, 32 layer tasks over {ncores} threads, "
-                                                   f"{dt:.1f} s"}
+        # The same oracle over the cores near the GPU, one process per core, each on its own
+        # disjoint slices of the block table: context for the host's own copy bandwidth. It runs
+        # in a process of its own, which never touches the GPU (it forks its workers).
+        out["cpu_baseline_all_cores"] = oracle_all_cores(torch, args.cpu_seconds / 2)
     print(json.dumps(out), flush=True)
     pool.free()
     mma.mma_finalize()

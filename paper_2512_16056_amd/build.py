@@ -17,6 +17,7 @@ OBJ = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(HERE, "libmma.so")
 NATIVE_LIB = os.path.join(HERE, "libmma_native.so")  # hipMemcpyAsync comparators for the benchmark
 INTERPOSE_LIB = os.path.join(HERE, "libmma_interpose.so")  # LD_PRELOAD: hipMemcpy* -> libmma
+NATIVE_BATCH = os.path.join(HERE, "native_batch")  # hipMemcpyBatchAsync comparator (its own process)
 CXX = os.environ.get("CXX", "g++")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
@@ -70,6 +71,13 @@ def build(verbose: bool = False) -> str:
           f"-I{os.path.join(ROCM, 'include')}", f"-I{os.path.join(ROOT, 'include')}",
           os.path.join(CSRC, "mma_interpose.cpp"), "-o", tmp, "-ldl"])
     os.replace(tmp, INTERPOSE_LIB)
+    # The batched comparator links the system ROCm runtime (the one torch bundles does not export
+    # hipMemcpyBatchAsync); DT_RPATH, so that no LD_LIBRARY_PATH entry can swap it for another.
+    tmp = NATIVE_BATCH + ".tmp"
+    _run([CXX, "-std=c++17", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__", f"-I{os.path.join(ROCM, 'include')}",
+          os.path.join(CSRC, "native_batch.cpp"), "-o", tmp, f"-L{os.path.join(ROCM, 'lib')}", "-lamdhip64",
+          f"-Wl,-rpath,{os.path.join(ROCM, 'lib')}", "-Wl,--disable-new-dtags"])
+    os.replace(tmp, NATIVE_BATCH)
     return LIB
 
 
