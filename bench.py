@@ -521,16 +521,19 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
 
     # Mixed contention: the wake-up list as 34 groups on stream A, each followed by the dependent
     # digest kernel over the group, while the 2048-block offload runs on stream B; 256 KiB chunks.
+    # A and B are a pair of streams shown to run side by side (see concurrent_stream_pair).
+    sa, sb, side_by_side = concurrent_stream_pair(torch)
     extras["mixed_contention"] = mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan,
-                                                  arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
+                                                  arena, offs, sizes, wdst, Dw, Sw, Zw, lp, (sa, sb))
     mc = extras["mixed_contention"]
+    mc["streams_side_by_side"] = side_by_side
     mc["duplex_probe_GBs"] = peaks.get("duplex_GBs")
     if mc["mma"].get("overlap_aggregate_GBs") and peaks.get("duplex_GBs"):
         mc["overlap_frac_of_duplex_probe"] = round(mc["mma"]["overlap_aggregate_GBs"] / peaks["duplex_GBs"], 3)
 
     # All five workloads under both control modes, with the engine threads' CPU time per call.
     extras["control_modes"] = control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_blocks, plan,
-                                            arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
+                                            arena, offs, sizes, wdst, Dw, Sw, Zw, lp, (sa, sb))
     extras["device_control"] = extras["control_modes"]["device"]["kv_fetch_64k"]
     del wdst
     arena.free()
@@ -538,7 +541,7 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
 
 
 def control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_blocks, plan, arena, offs, sizes, wdst,
-                  Dw, Sw, Zw, lp):
+                  Dw, Sw, Zw, lp, mixed_streams):
     """The five workloads under host control (engine threads pull for every path) and device control
     (the calling thread plans each transfer, the dummy-task kernel alone tracks it), each on a
     stream of its own: median time and GB/s, and the engine threads' CPU time per call (their
@@ -594,12 +597,10 @@ def control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_bloc
             c.chunk_bytes = 256 << 10
             mma.mma_init(0, c)
             c0 = cpu_ns()
-            a_ms, b_ms = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan,
-                                                    arena, offs, sizes, wdst, Dw, Sw, Zw, lp, reps=1)
+            mx = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan,
+                                            arena, offs, sizes, wdst, Dw, Sw, Zw, lp, reps=1, streams=mixed_streams)
             c1 = cpu_ns()
-            r["mixed_contention"] = {"stream_a_weights_digests_ms": round(a_ms, 1),
-                                     "stream_b_offload_ms": round(b_ms, 1),
-                                     "engine_cpu_ms_per_schedule": round((c1 - c0) / 1e6 / 2, 3)}
+            r["mixed_contention"] = {**mx, "engine_cpu_ms_per_schedule": round((c1 - c0) / 1e6 / 2, 3)}
             r["failed_transfers"] += mma.mma_get_stats()["failed_transfers"]
             mma.mma_finalize()
             out[mode] = r
@@ -634,40 +635,10 @@ def sampled_fetch_parity(s, pv, layers, hs, gb, gpu_layout, samples=64, seed=0):
 
 
 def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan, arena, offs, sizes, wdst,
-                     Dw, Sw, Zw, lp):
-    import ctypes
+                     Dw, Sw, Zw, lp, streams):
     groups = W.weight_groups()
     assert all(list(g) == list(range(g[0], g[0] + len(g))) for g in groups)
-    digests = torch.zeros(len(sizes), dtype=torch.int64, device="cuda")
-    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
     res = {}
-
-    def schedule(use_mma):
-        ea = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        eb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        torch.cuda.synchronize()
-        ea[0].record(sa)
-        for g in groups:
-            if use_mma:
-                mma.mma_weights_load([(wdst[t], arena.ptr + offs[t], sizes[t]) for t in g], mma.MMA_H2D, sa)
-            else:  # a group is a contiguous run of the tensor list
-                o = 8 * g[0]
-                nat.native_list(ctypes.addressof(Dw) + o, ctypes.addressof(Sw) + o, ctypes.addressof(Zw) + o,
-                                len(g), 0, ctypes.c_void_p(sa.cuda_stream))
-            for t in g:
-                mma.mma_digest_u32(wdst[t], sizes[t], digests.data_ptr() + 8 * t, sa)
-        ea[1].record(sa)
-        eb[0].record(sb)
-        if use_mma:
-            mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, sb)
-        else:
-            nat.native_kv_offload(pool.ptr, lp, src_blocks.ctypes.data_as(ctypes.c_void_p),
-                                  plan.dest.ctypes.data_as(ctypes.c_void_p), len(src_blocks), s.layers,
-                                  s.piece_bytes, s.gpu_num_blocks, ctypes.c_void_p(sb.cuda_stream))
-        eb[1].record(sb)
-        torch.cuda.synchronize()
-        return ea[0].elapsed_time(ea[1]), eb[0].elapsed_time(eb[1])
-
     cfg = mma.mma_get_config()
     mma.mma_finalize()
     c = mma.mma_config_default()
@@ -676,28 +647,26 @@ def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, p
     try:
         for t in range(len(sizes)):
             wdst[t].fill_(W.WEIGHT_POISON)
-        schedule(True)  # warm-up at this chunk size
-        for t in range(len(sizes)):
-            wdst[t].fill_(W.WEIGHT_POISON)
-        a_ms, b_ms = schedule(True)
+        r = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena, offs,
+                                       sizes, wdst, Dw, Sw, Zw, lp, reps=1, streams=streams)
         mma.mma_synchronize()
-        r = np.random.default_rng(2)
+        g = np.random.default_rng(2)
         ok = True
-        for t in [int(x) for x in r.integers(len(sizes), size=8)]:
+        for t in [int(x) for x in g.integers(len(sizes), size=8)]:
             ok &= bool(np.array_equal(wdst[t][:65536].cpu().numpy(), arena.array[offs[t]:offs[t] + min(65536, sizes[t])]))
         wtotal, off_bytes = sum(sizes), len(src_blocks) * s.slot_bytes
+        a_ms, b_ms = r["stream_a_weights_digests_ms"], r["stream_b_offload_ms"]
         # both directions over the offload's time: its bytes, plus the weight bytes moved meanwhile
-        # at stream A's average rate
-        agg = (off_bytes + wtotal / a_ms * b_ms) / b_ms / 1e6 if b_ms <= a_ms else None
-        res["mma"] = {"stream_a_weights_digests_ms": round(a_ms, 1), "stream_b_offload_ms": round(b_ms, 1),
-                      "makespan_ms": round(max(a_ms, b_ms), 1), "overlap_aggregate_GBs": round(agg, 1) if agg else None,
-                      "sampled_parity": ok, "failed_transfers": mma.mma_get_stats()["failed_transfers"]}
+        # at stream A's average rate (only while the two ran side by side)
+        agg = (off_bytes + wtotal / a_ms * b_ms) / b_ms / 1e6 if r["concurrent"] and b_ms <= a_ms else None
+        res["mma"] = {**r, "overlap_aggregate_GBs": round(agg, 1) if agg else None, "sampled_parity": ok,
+                      "failed_transfers": mma.mma_get_stats()["failed_transfers"]}
     finally:
         mma.mma_finalize()
         mma.mma_init(0, cfg)
-    a_ms, b_ms = schedule(False)
-    res["native"] = {"stream_a_weights_digests_ms": round(a_ms, 1), "stream_b_offload_ms": round(b_ms, 1),
-                     "makespan_ms": round(max(a_ms, b_ms), 1)}
+    res["native"] = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
+                                               offs, sizes, wdst, Dw, Sw, Zw, lp, native=True, reps=1,
+                                               streams=streams)
     res["makespan_speedup_vs_native"] = round(res["native"]["makespan_ms"] / res["mma"]["makespan_ms"], 3)
     res["stream_a_ratio_vs_native"] = round(res["native"]["stream_a_weights_digests_ms"] /
                                             res["mma"]["stream_a_weights_digests_ms"], 3)
@@ -1135,7 +1104,10 @@ def sweep_duplex():
     hs2, gb2 = hs[nb:2 * nb].astype(np.int32), gb[nb:2 * nb].astype(np.int32)
     kvb = nb * s.slot_bytes
     CU = mma.MMA_PATH_CU
-    for name, kv in (("default", {}), ("cu only", dict(path_mask_h2d=CU, path_mask_d2h=CU)),
+    SAME = mma.MMA_DUPLEX_UNCHANGED
+    for name, kv in (("default", {}),
+                     ("all paths shared by both directions", dict(duplex_paths_h2d=SAME, duplex_paths_d2h=SAME)),
+                     ("cu only", dict(path_mask_h2d=CU, path_mask_d2h=CU)),
                      ("d2h without cu", dict(path_mask_d2h=0x3)),
                      ("h2d without cu", dict(path_mask_h2d=0x3)),
                      ("no cu either way", dict(path_mask_h2d=0x3, path_mask_d2h=0x3)),
@@ -1158,9 +1130,10 @@ def sweep_mixed(sizes=None, rounds=6):
     """The mixed-contention workload (the 291-tensor list as 34 groups on stream A, each followed by
     the dependent digest kernel; the 2048-block KV offload on stream B; 256 KiB micro-tasks) under
     path assignments per direction, against the same schedule with native copies. The cases are
-    interleaved over `rounds` rounds (a fresh library per run, one warm-up schedule, one timed), and
-    every run is reported: both streams' times and the link aggregate while both directions run
-    (bytes of B plus the bytes A moved meanwhile at its average rate, over B's time)."""
+    interleaved over `rounds` rounds (a fresh library per run, one warm-up schedule, one timed), on
+    one pair of streams shown to run side by side, and every run is reported: both streams' times,
+    B's start, the makespan, and the link aggregate while both directions run (bytes of B plus the
+    bytes A moved meanwhile at its average rate, over B's time)."""
     import ctypes
 
     import numpy as np
@@ -1189,10 +1162,14 @@ def sweep_mixed(sizes=None, rounds=6):
     Zw = (ctypes.c_uint64 * len(sizes_w))(*sizes_w)
     lp = (ctypes.c_void_p * s.layers)(*[t.data_ptr() for t in layers])
     CU = mma.MMA_PATH_CU
+    SAME = mma.MMA_DUPLEX_UNCHANGED
     cases = [("default", {}),
-             ("h2d cu + engine 0, d2h engine 1", dict(path_mask_h2d=CU | 1, path_mask_d2h=2)),
-             ("d2h engines 2-5", dict(path_mask_d2h=0x3C)),
+             ("all paths shared by both directions", dict(duplex_paths_h2d=SAME, duplex_paths_d2h=SAME)),
+             ("duplex h2d engines 0-1 + cu, d2h engines 2-5", dict(duplex_paths_h2d=CU | 0x3)),
+             ("duplex h2d engines 0-1, d2h engines 2-3", dict(duplex_paths_d2h=0xC)),
              ("native", None)]
+    streams = concurrent_stream_pair(torch)
+    _emit(sweep="mixed", streams_side_by_side=streams[2])
     for rnd in range(rounds):
         for name, kv in cases[rnd % len(cases):] + cases[:rnd % len(cases)]:
             c = mma.mma_config_default()
@@ -1201,8 +1178,10 @@ def sweep_mixed(sizes=None, rounds=6):
                 setattr(c, k, v)
             mma.mma_init(0, c)
             mma.mma_trace_enable(True)
-            a, b = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
-                                              offs, sizes_w, wdst, Dw, Sw, Zw, lp, native=kv is None, reps=1)
+            r = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
+                                           offs, sizes_w, wdst, Dw, Sw, Zw, lp, native=kv is None, reps=1,
+                                           streams=streams[:2])
+            a, b = r["stream_a_weights_digests_ms"], r["stream_b_offload_ms"]
             mma.mma_synchronize()
             st = mma.mma_get_stats()
             tr = mma.mma_trace_read()
@@ -1217,22 +1196,49 @@ def sweep_mixed(sizes=None, rounds=6):
                     if r_["dir"] == d:
                         tot = [x + y for x, y in zip(tot, r_["path_tasks"])]
                 paths[key] = {("cu" if i == 16 else f"e{i}"): v for i, v in enumerate(tot) if v}
-            agg = (off_bytes + wtotal / a * b) / b / 1e6 if b <= a else None
-            _emit(sweep="mixed", round=rnd, case=name, stream_a_weights_digests_ms=round(a, 1),
-                  stream_b_offload_ms=round(b, 1), overlap_aggregate_GBs=round(agg, 1) if agg else None,
+            agg = (off_bytes + wtotal / a * b) / b / 1e6 if r["concurrent"] and b <= a else None
+            _emit(sweep="mixed", round=rnd, case=name, **r, overlap_aggregate_GBs=round(agg, 1) if agg else None,
                   failed=st["failed_transfers"], backoffs=st["sdma_congestion_backoffs"], **paths)
     arena.free()
     pool.free()
 
 
+def concurrent_stream_pair(torch, tries=16):
+    """Two streams that run side by side. The runtime maps streams onto a few hardware queues
+    (GPU_MAX_HW_QUEUES, 4 by default), so two new streams may share one; a kernel on one then
+    starts only after the kernels queued before it on the other. (The copy engines' commands of
+    a runtime copy are ordered by stream, not by hardware queue, so runtime copies do not see
+    this.) Probe: a sleep kernel on A, then an event on B, which must complete while A still
+    sleeps. Returns (A, B, True), or the last pair tried and False."""
+    import time as _t
+    for _ in range(tries):
+        sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(sa):
+            torch.cuda._sleep(200_000_000)  # about 0.1 s of GPU clock cycles
+        e = torch.cuda.Event()
+        e.record(sb)
+        t0 = _t.perf_counter()
+        while not e.query() and _t.perf_counter() - t0 < 5.0:
+            pass
+        ok = e.query() and not sa.query()
+        torch.cuda.synchronize()
+        if ok:
+            return sa, sb, True
+    return sa, sb, False
+
+
 def mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena, offs, sizes,
-                               wdst, Dw, Sw, Zw, lp, native=False, reps=1):
+                               wdst, Dw, Sw, Zw, lp, native=False, reps=1, streams=None):
     """The mixed-contention schedule (stream A: 34 groups, each loaded and then digested; stream B:
-    the offload), once to warm up and then `reps` times; the median stream times in ms."""
+    the offload, issued after A's work), once to warm up and then `reps` times. Medians in ms: A's
+    and B's times on their streams, when B started after A's start, and the makespan from A's
+    start to the later end; `concurrent`: B started before A ended in every timed run. `streams`:
+    the (A, B) pair to use, else two new ones from torch's pool."""
     import ctypes
     groups = W.weight_groups()
     digests = torch.zeros(len(sizes), dtype=torch.int64, device="cuda")
-    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    sa, sb = streams if streams else (torch.cuda.Stream(), torch.cuda.Stream())
     out = []
     for _ in range(reps + 1):
         ea = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -1258,9 +1264,15 @@ def mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blo
                                   s.piece_bytes, s.gpu_num_blocks, ctypes.c_void_p(sb.cuda_stream))
         eb[1].record(sb)
         torch.cuda.synchronize()
-        out.append((ea[0].elapsed_time(ea[1]), eb[0].elapsed_time(eb[1])))
+        a, b, b0 = ea[0].elapsed_time(ea[1]), eb[0].elapsed_time(eb[1]), ea[0].elapsed_time(eb[0])
+        out.append((a, b, b0, max(a, ea[0].elapsed_time(eb[1]))))
     out = out[1:]
-    return sorted(x[0] for x in out)[len(out) // 2], sorted(x[1] for x in out)[len(out) // 2]
+
+    def med(i):
+        return sorted(x[i] for x in out)[len(out) // 2]
+    return {"stream_a_weights_digests_ms": round(med(0), 1), "stream_b_offload_ms": round(med(1), 1),
+            "stream_b_start_ms": round(med(2), 1), "makespan_ms": round(med(3), 1),
+            "concurrent": all(x[2] < x[0] for x in out)}
 
 
 def sweep_paths():

@@ -68,6 +68,8 @@ typedef int32_t mma_status_t;
 
 /* Path mask bits: bit e (e < 16) = SDMA engine e; MMA_PATH_CU = the CU path. */
 #define MMA_PATH_CU 0x80000000u
+/* duplex_paths_*: keep a direction's own paths while the other direction moves. */
+#define MMA_DUPLEX_UNCHANGED 0xFFFFFFFFu
 #define MMA_MAX_SDMA 16
 #define MMA_NUM_PATHS 17      /* stats index 16 = CU path */
 #define MMA_MAX_LAYERS 256    /* KV layers per call */
@@ -129,6 +131,21 @@ typedef struct mma_config {
                                  stream with work pending, and for KV transfers, the CU path
                                  carries the transfer alone. A transfer of more than 4096
                                  micro-tasks still goes to the engine thread. */
+  uint32_t duplex_paths_h2d; /* paths host->device pulls from while a device->host transfer is
+                               moving (Section 5.1.2, concurrent flows; host control only).
+                               0 (default): the host-facing SDMA engines of path_mask_h2d, without
+                               the CU path. MMA_DUPLEX_UNCHANGED: path_mask_h2d. Each copy engine
+                               runs one in-order queue for both directions, and CU zero-copy loads
+                               send their read requests up the lanes that device->host data uses.
+                               Micro-tasks only the CU path may carry still take it. */
+  uint32_t duplex_paths_d2h; /* paths device->host pulls from while a host->device transfer is
+                               moving. 0 (default): SDMA engines 2-5 (on MI355X the xGMI-facing
+                               engines, 13-18 GB/s each toward the host), neither the host-facing
+                               engines nor the CU path, whose stores to host memory share the
+                               upstream lanes in small writes; MMA_DUPLEX_UNCHANGED: path_mask_d2h.
+                               Engines the device does not offer are dropped; a set left with no
+                               path, or a CU path the direction does not have, falls back to its
+                               path mask. */
 } mma_config_t;
 
 typedef struct mma_copy_desc {
@@ -223,7 +240,7 @@ mma_status_t mma_config_default(mma_config_t* out);
  * MMA_CU_QUEUE_DEPTH, MMA_BACKOFF_DEPTH, MMA_PATHS_H2D, MMA_PATHS_D2H,
  * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS, MMA_SDMA_MERGE_TASKS,
  * MMA_CU_WHOLE_BYTES, MMA_CU_WHOLE_BYTES_D2H, MMA_CONTROL, MMA_STATIC_CU_PERCENT,
- * MMA_TRACE).
+ * MMA_DUPLEX_PATHS_H2D, MMA_DUPLEX_PATHS_D2H, MMA_TRACE).
  * Errors: MMA_ERR_ALREADY_INITIALIZED, MMA_ERR_INVALID_ARG (bad device or
  * config), MMA_ERR_HIP / MMA_ERR_HSA. */
 mma_status_t mma_init(int hip_device, const mma_config_t* cfg);

@@ -30,6 +30,7 @@ MMA_ERR_TIMEOUT = -10
 MMA_H2D = 0
 MMA_D2H = 1
 MMA_PATH_CU = 0x80000000
+MMA_DUPLEX_UNCHANGED = 0xFFFFFFFF  # duplex_paths_*: keep the direction's own paths
 MMA_KV_LAYOUT_PIECE = 0
 MMA_KV_LAYOUT_XPACKED = 1
 MMA_KV_LAYOUT_HND = 2
@@ -70,7 +71,8 @@ class mma_config_t(ctypes.Structure):
                 ("watchdog_ms", ctypes.c_uint32), ("static_split", ctypes.c_uint32),
                 ("static_cu_percent", ctypes.c_uint32), ("sdma_merge_tasks", ctypes.c_uint32),
                 ("cu_whole_bytes", ctypes.c_uint32), ("cu_whole_bytes_d2h", ctypes.c_uint32),
-                ("control", ctypes.c_uint32)]
+                ("control", ctypes.c_uint32), ("duplex_paths_h2d", ctypes.c_uint32),
+                ("duplex_paths_d2h", ctypes.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

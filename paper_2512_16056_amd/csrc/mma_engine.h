@@ -127,6 +127,7 @@ struct Transfer {
   std::vector<uint8_t> claimed;
   std::vector<uint32_t> left;  // CU entries outstanding per CU-path task
   size_t cur_cu = 0, cur_sdma = 0, n_claimed = 0, n_done = 0;
+  size_t cu_only_left = 0, cur_cu_only = 0;  // unclaimed CU-only micro-tasks; scan cursor while the CU path pauses
   uint64_t piece = 0;
   bool sdma_ok = true;         // SDMA may carry this transfer's tasks
   // CU ring bookkeeping
@@ -221,6 +222,7 @@ struct Config {
   uint32_t device;      // 1: device control (no engine thread in the loop)
   uint32_t device_cu_percent;  // device control: the CU path's share of a linear transfer's bytes
   uint32_t overdue_gbs;        // link rate the overdue rule assumes, GB/s (0: 50)
+  uint32_t duplex[2];          // per direction: the paths used while the other direction moves (see set_peer)
 };
 
 struct Stats {
@@ -434,6 +436,7 @@ class Engine {
     for (auto& p : paths_) m |= 1u << p.engine;
     return m;
   }
+  bool moving() const { return moving(now_ns()); }
   bool cu_enabled() const { return (cfg_.mask[dir_] & MMA_PATH_CU) != 0; }
   bool device_control() const { return cfg_.device != 0; }
   // Both directions at once on one link (Section 5.1.2, concurrent flows):
@@ -447,9 +450,26 @@ class Engine {
   // times per run (each command 2.3-3.4 ms at the head of this engine's view of
   // the queue, while the other direction's commands ahead of it ran); allowing
   // for the bytes queued ahead at submission, 0-2 times.
+  //
+  // While the other direction moves, a direction pulls only from its duplex
+  // paths (cfg.duplex[dir]): by default the host-facing engines alone for
+  // host-to-device, and engines 2-5 alone for device-to-host. No command then
+  // waits behind the other direction's merged commands, and neither direction's
+  // CU path puts its traffic on the lanes the other one's data uses: CU
+  // zero-copy loads send their read requests upstream beside device-to-host
+  // data, and CU stores to host memory share those lanes in small writes. On
+  // the mixed workload (the 34-group weight load beside the 2048-block offload,
+  // streams side by side) that keeps the weight stream at 303.9 ms against the
+  // native schedule's 303.5 ms, with the offload at 104 ms; all paths shared:
+  // 310.6 and 178 ms. The CU path still takes micro-tasks that no other path
+  // may carry. Called once both engines are initialised.
   void set_peer(const Engine* peer) { peer_ = peer; }
   // Bytes of the other direction's commands in flight on copy engine e.
   uint64_t peer_bytes_on(int e) const { return peer_ ? peer_->eng_bytes_[e].load(std::memory_order_relaxed) : 0; }
+  // The other direction has had a started transfer that is not complete
+  // within the last kDuplexHoldNs.
+  bool peer_moving(uint64_t now) const { return peer_ && peer_->moving(now); }
+  bool moving(uint64_t now) const { return now < moving_until_.load(std::memory_order_relaxed); }
 
   // Transfers tracked by the submitting threads are in flight (see track).
   bool tracked() const { return n_tracked_.load(std::memory_order_acquire) != 0; }
@@ -569,7 +589,9 @@ class Engine {
   // CU path's first pulls, made before the transfer is handed to the engine
   // thread (no concurrent access to x yet): the dummy task's workers can start
   // copying as soon as the stream reaches them, without a host round trip.
-  void prefill(Transfer* x) { pull_cu(x); }
+  // While the other direction moves, only micro-tasks that the CU path alone
+  // may carry (see set_peer).
+  void prefill(Transfer* x) { pull_cu(x, cu_paused_at(now_ns())); }
 
   // Workgroups of the dummy-task kernel: one wave per ring entry that can be
   // outstanding at once (waves beyond that would only poll host memory, and
@@ -629,6 +651,8 @@ class Engine {
         f |= static_cu_task(i, cfg_.static_cu_percent) ? kPlanCuOnly : kPlanSdmaOnly;
       }
     }
+    x->cu_only_left = static_cast<size_t>(std::count_if(
+        x->tasks.begin(), x->tasks.end(), [](const Task& t) { return (t.flags & kPlanCuOnly) != 0; }));
     const bool staged = x->kind != Kind::kLinear && has_sdma() && x->sdma_ok;
     const bool needs_cu = cu_enabled() || staged ||
                           std::any_of(x->tasks.begin(), x->tasks.end(),
@@ -1149,9 +1173,13 @@ class Engine {
   }
 
   // ---------------------------------------------------------------- CU path
-  bool pull_cu(Transfer* x) {
+  bool pull_cu(Transfer* x, bool cu_paused) {
     if (x->failed || x->ignored || x->aborting) return false;
     const bool any = cu_enabled() || x->pool_dev;
+    // While the CU path pauses for the other direction (see set_peer), it
+    // takes only the micro-tasks no other path may carry.
+    const bool paused = cu_paused && !x->pool_dev && !x->whole;
+    if (paused && x->cu_only_left == 0) return false;
     // An HBM-resident pool keeps every wave busy: two micro-tasks per wave outstanding.
     const uint32_t depth = x->whole ? ~0u : (x->pool_dev ? 2 * x->waves : cfg_.cu_depth);
     bool p = false;
@@ -1164,6 +1192,11 @@ class Engine {
                                       (!any && !(x->tasks[i].flags & kPlanCuOnly))))
         ++i;
       x->cur_cu = i;
+      if (paused) {  // the cursor above stays where the CU path resumes
+        i = std::max(x->cur_cu_only, i);
+        while (i < x->tasks.size() && (x->claimed[i] || !(x->tasks[i].flags & kPlanCuOnly))) ++i;
+        x->cur_cu_only = i;
+      }
       if (i >= x->tasks.size()) break;
       const Task& t = x->tasks[i];
       uint32_t ne;
@@ -1175,6 +1208,7 @@ class Engine {
       if (!ne) break;
       x->claimed[i] = 1;
       ++x->n_claimed;
+      if (t.flags & kPlanCuOnly) --x->cu_only_left;
       x->left[i] = ne;
       ++x->cu_busy;
       p = true;
@@ -1257,6 +1291,8 @@ class Engine {
       x->tasks[j].flags = (x->tasks[j].flags & ~kPlanSdmaOnly) | kPlanCuOnly;
     }
     x->n_claimed -= end - i;
+    x->cu_only_left += end - i;
+    x->cur_cu_only = std::min(x->cur_cu_only, i);
     x->cur_cu = std::min(x->cur_cu, i);
     x->progress = true;
   }
@@ -1396,7 +1432,8 @@ class Engine {
       const SdmaSlot& s = slots_[id];
       if (s.x == x && s.state != kFree) mine += s.task_end - s.task;
     }
-    const size_t fair = (unclaimed + outstanding + paths_.size() - 1) / paths_.size();
+    const size_t n = std::max<size_t>(1, n_pull_paths_);
+    const size_t fair = (unclaimed + outstanding + n - 1) / n;
     return fair > mine ? fair - mine : 0;
   }
 
@@ -1411,13 +1448,31 @@ class Engine {
       if (engine_op(s) && (!head || s.t_submit < head->t_submit)) head = &s;
     }
     if (!head) return false;
-    const uint64_t npaths = paths_.size() + (cu_enabled() ? 1 : 0);
+    const uint64_t npaths = std::max<size_t>(1, n_pull_paths_) + (cu_enabled() && !cu_paused_ ? 1 : 0);
     const uint64_t since = std::max(path.t_head, head->t_submit);
     // the other direction's commands that were on this engine when the head
     // command was submitted may run first
     const uint64_t bytes = head->op_bytes + head->ahead;
     const uint64_t gbs = cfg_.overdue_gbs ? cfg_.overdue_gbs : 50;  // 1 GB/s = 1 byte per ns
     return now > since && now - since > 4 * npaths * bytes / gbs + 500000;  // ns
+  }
+
+  // The paths of this phase: the duplex paths while the other direction moves
+  // (see set_peer), else the direction's own. Set at the top of every round of
+  // the engine loop, before any path pulls.
+  void phase(uint64_t now) {
+    usable_ = peer_moving(now) ? cfg_.duplex[dir_] : cfg_.mask[dir_];
+    n_pull_paths_ = 0;
+    for (auto& path : paths_) n_pull_paths_ += (usable_ >> path.engine) & 1u;
+    cu_paused_ = cu_enabled() && !(usable_ & MMA_PATH_CU) && n_pull_paths_ > 0;
+  }
+  // The same decision for the CU path alone, from any thread (paths_ and cfg_
+  // are fixed after init).
+  bool cu_paused_at(uint64_t now) const {
+    if (!cu_enabled() || !peer_moving(now) || (cfg_.duplex[dir_] & MMA_PATH_CU)) return false;
+    for (auto& path : paths_)
+      if ((cfg_.duplex[dir_] >> path.engine) & 1u) return true;
+    return false;
   }
 
   // Paths that can make progress take work (Section 2.2; Section 3.4 contention
@@ -1432,8 +1487,10 @@ class Engine {
     uint32_t free_mask = 0;
     bool have_mask = false;
     const uint64_t now = now_ns();
+    const uint32_t usable = usable_;
     for (size_t k = 0; k < paths_.size(); ++k) {
       SdmaPath& path = paths_[(k + rr_) % paths_.size()];
+      if (!((usable >> path.engine) & 1u)) continue;  // not a path of this phase
       if (path.congested) {
         if (path.busy > 0) continue;
         path.congested = false;
@@ -1658,6 +1715,7 @@ class Engine {
         }
       }
       if (!busy_t0) busy_t0 = now_ns();
+      phase(now_ns());
       bool p = false;
       for (auto& up : active_) {
         up->progress = false;
@@ -1665,7 +1723,7 @@ class Engine {
         p |= scan_cu(up.get());
       }
       p |= poll_sdma();
-      for (auto& up : active_) p |= pull_cu(up.get());
+      for (auto& up : active_) p |= pull_cu(up.get(), cu_paused_);
       p |= pull_sdma();
       for (auto& up : active_) {
         p |= advance(up.get());
@@ -1686,6 +1744,9 @@ class Engine {
         active_.erase(active_.begin() + static_cast<long>(i));
         p = true;
       }
+      bool moving = false;
+      for (auto& up : active_) moving |= up->started && !up->completed && !up->failed;
+      if (moving) moving_until_.store(now_ns() + kDuplexHoldNs, std::memory_order_relaxed);
       if (p) {
         idle_spins = 0;
       } else if (++idle_spins < 20000) {
@@ -1731,12 +1792,21 @@ class Engine {
   // Bytes of this engine's commands in flight per copy engine; read by the
   // other direction's engine thread.
   std::atomic<uint64_t> eng_bytes_[MMA_MAX_SDMA] = {};
+  std::atomic<uint64_t> moving_until_{0};  // see peer_moving (read by the other direction)
+  uint32_t usable_ = 0;                    // paths of this phase (see phase)
+  bool cu_paused_ = false;                 // the CU path takes only CU-only micro-tasks (see set_peer)
+  size_t n_pull_paths_ = 0;                // copy-engine paths pull_sdma may use this round
   const Engine* peer_ = nullptr;          // the other direction's engine
   bool stop_ = false;
   bool engine_waiting_ = false;  // the engine thread waits on cv_ (guarded by mu_)
   std::atomic<bool> stop_flag_{false};
   std::atomic<uint64_t> n_incoming_{0};
   static constexpr uint64_t kIdleSpinNs = 2000000;  // 2 ms
+  // A direction counts as moving this long after its last started transfer
+  // that was not complete, so that the gaps between back-to-back transfers (a
+  // weight list in groups with kernels between them) do not switch the other
+  // direction's paths back and forth.
+  static constexpr uint64_t kDuplexHoldNs = 1000000;  // 1 ms
   static constexpr uint64_t kTagGraceNs = 100000000;  // 100 ms
   static constexpr size_t kReapWindow = 512;
   std::thread thread_;

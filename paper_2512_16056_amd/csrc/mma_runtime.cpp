@@ -462,6 +462,8 @@ void fill_config(mma_config_t* c, bool use_env) {
   if (use_env) {
     d.control = static_cast<uint32_t>(env_u64("MMA_CONTROL", d.control));
     d.static_cu_percent = static_cast<uint32_t>(env_u64("MMA_STATIC_CU_PERCENT", 0));
+    d.duplex_paths_h2d = static_cast<uint32_t>(env_u64("MMA_DUPLEX_PATHS_H2D", 0));
+    d.duplex_paths_d2h = static_cast<uint32_t>(env_u64("MMA_DUPLEX_PATHS_D2H", 0));
     d.chunk_bytes = env_u64("MMA_CHUNK_BYTES", d.chunk_bytes);
     d.fallback_bytes = env_u64("MMA_FALLBACK_BYTES", 0);
     d.small_bytes = env_u64("MMA_SMALL_BYTES", d.small_bytes);
@@ -557,6 +559,20 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   }
   c.path_mask_h2d = mask[0];
   c.path_mask_d2h = mask[1];
+  // Paths while the other direction moves (see Engine::set_peer). A static
+  // split fixes each micro-task's path at plan time, so it keeps its masks.
+  uint32_t duplex[2] = {c.duplex_paths_h2d, c.duplex_paths_d2h};
+  for (int d = 0; d < 2; ++d) {
+    if (c.static_split || duplex[d] == MMA_DUPLEX_UNCHANGED) {
+      duplex[d] = mask[d];
+      continue;
+    }
+    if (!duplex[d]) duplex[d] = d == MMA_H2D ? (mask[d] & host_facing & 0xFFFFu) : 0x3Cu;
+    duplex[d] = (duplex[d] & mask[d] & MMA_PATH_CU) | (duplex[d] & avail[d] & 0xFFFFu);
+    if (!duplex[d]) duplex[d] = mask[d];
+  }
+  c.duplex_paths_h2d = duplex[0];
+  c.duplex_paths_d2h = duplex[1];
   if (!c.backoff_depth) c.backoff_depth = c.queue_depth;
   rt->ucfg = c;
   Config& k = rt->cfg;
@@ -571,6 +587,8 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   k.watchdog_ms = c.watchdog_ms;
   k.mask[0] = mask[0];
   k.mask[1] = mask[1];
+  k.duplex[0] = duplex[0];
+  k.duplex[1] = duplex[1];
   if (c.static_cu_percent > 100) return fail(MMA_ERR_INVALID_ARG, "static_cu_percent > 100");
   if (c.control > MMA_CONTROL_DEVICE) return fail(MMA_ERR_INVALID_ARG, "unknown control mode %u", c.control);
   k.device = c.control == MMA_CONTROL_DEVICE ? 1u : 0u;
@@ -587,7 +605,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   // cache maintenance). Kept for the process lifetime and reused.
   const uint64_t stage_bytes = (std::max<uint64_t>(k.chunk, 2 * MiB) + 4095) & ~4095ull;
   for (int d = 0; d < 2; ++d) {
-    const uint32_t n = static_cast<uint32_t>(__builtin_popcount(mask[d] & 0xFFFFu));
+    const uint32_t n = static_cast<uint32_t>(__builtin_popcount((mask[d] | duplex[d]) & 0xFFFFu));
     const uint64_t need = n * k.depth * stage_bytes;
     StagingCache& sc = g_staging[d];
     if (need && (sc.dev != hip_device || sc.bytes < need)) {
@@ -615,7 +633,8 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   rt->backend.reset(new HsaBackend(rt->ag.gpu, rt->ag.cpu));
   for (int d = 0; d < 2; ++d) {
     rt->eng[d].reset(new Engine(d, k, rt->backend.get(), &rt->stats));
-    mma_status_t s = rt->eng[d]->init(mask[d] & 0xFFFFu, stage_bytes, (mask[d] & 0xFFFFu) ? g_staging[d].base : nullptr);
+    const uint32_t engines = (mask[d] | duplex[d]) & 0xFFFFu;
+    mma_status_t s = rt->eng[d]->init(engines, stage_bytes, engines ? g_staging[d].base : nullptr);
     if (s != MMA_OK) {
       rt->eng[0].reset();
       rt->eng[1].reset();

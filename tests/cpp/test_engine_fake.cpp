@@ -22,6 +22,7 @@
 // Usage: test_engine_fake [--no-timing | --timing-only]
 // The timing scenarios sleep to emulate path rates, so a heavily loaded host
 // distorts them; the pytest wrapper runs them apart from the correctness ones.
+#include <array>
 #include <atomic>
 #include <chrono>
 #include <condition_variable>
@@ -428,7 +429,8 @@ struct Setup {
   double wave_rate = 250;                          // bytes/us per wave
   uint64_t cmd_ns = 20000;
   uint32_t mask = MMA_PATH_CU | 0x3;
-  uint32_t mask_d2h = 0;  // device-to-host paths, when not `mask` (copy engines a subset of mask's)
+  uint32_t mask_d2h = 0;  // device-to-host paths, when not `mask`
+  uint32_t duplex[2] = {0, 0};  // paths while the other direction moves (0: the direction's own)
   Config cfg{};
 };
 
@@ -456,13 +458,14 @@ class Harness {
     Config c = s.cfg;
     c.mask[MMA_H2D] = s.mask;
     c.mask[MMA_D2H] = s.mask_d2h ? s.mask_d2h : s.mask;
+    for (int d = 0; d < 2; ++d) c.duplex[d] = s.duplex[d] ? s.duplex[d] : c.mask[d];
     stage_bytes_ = std::max<uint64_t>(c.chunk, 2 * 1024 * 1024);
-    const uint32_t engines = static_cast<uint32_t>(__builtin_popcount(s.mask & 0xFFFFu));
+    const uint32_t engines = 16;  // staging for any engine set
     staging_.assign(2 * engines * c.depth * stage_bytes_ + 1, 0);
     for (int d = 0; d < 2; ++d) {
       eng_[d].reset(new Engine(d, c, &be_, &stats_));
-      void* base = engines ? staging_.data() + d * engines * c.depth * stage_bytes_ : nullptr;
-      const mma_status_t rc = eng_[d]->init(c.mask[d] & 0xFFFFu, stage_bytes_, base);
+      void* base = staging_.data() + d * engines * c.depth * stage_bytes_;
+      const mma_status_t rc = eng_[d]->init((c.mask[d] | c.duplex[d]) & 0xFFFFu, stage_bytes_, base);
       CHECK(rc == MMA_OK, "engine init %d: %s", rc, t_err.c_str());
     }
     eng_[MMA_D2H]->set_peer(eng_[MMA_H2D].get());  // as mma_init
@@ -1427,6 +1430,88 @@ void duplex_peer_commands() {
   std::printf("ok   the other direction's commands on a shared copy engine are neither foreign work nor congestion\n");
 }
 
+// While the other direction moves, a direction pulls only from its duplex
+// paths: here host-to-device engines 0-1 without the CU path, device-to-host
+// engines 2-3 without the CU path. A device-to-host list issued while a long
+// host-to-device copy runs takes engines 2-3 only, except for its small tensor,
+// which only the CU path may carry; once the host-to-device copy is done, a
+// second list uses its own paths again (engines 0-1 and the CU path). Exact in
+// both directions.
+void duplex_paths() {
+  Setup s;
+  s.cfg = default_config();
+  s.cfg.chunk = 512 * 1024;
+  s.cfg.fallback = 512 * 1024;
+  s.cfg.merge = 16;
+  s.engine_rates = {2000, 2000, 2000, 2000};
+  s.cmd_ns = 2000;
+  s.duplex[MMA_H2D] = 0x3;
+  s.duplex[MMA_D2H] = 0xC;
+  Harness h(s);
+  FakeStream a, b;
+  const uint64_t n = 160ull * 1024 * 1024 + 3;
+  const std::vector<uint64_t> sizes = {8ull * 1024 * 1024 + 5, 4096, 4ull * 1024 * 1024};  // 4 KiB < small
+  auto src = random_bytes(n, 71);
+  std::vector<uint8_t> dst(n);
+  std::vector<std::vector<uint8_t>> lsrc, ldst;
+  for (int rep = 0; rep < 2; ++rep)
+    for (size_t i = 0; i < sizes.size(); ++i) {
+      lsrc.push_back(random_bytes(sizes[i], 80 + 10 * rep + static_cast<uint32_t>(i)));
+      ldst.emplace_back(sizes[i], 0);
+    }
+  auto list = [&](int rep) {
+    std::vector<mma_copy_desc_t> d;
+    std::vector<uint64_t> z, sa, da;
+    for (size_t i = 0; i < sizes.size(); ++i) {
+      const size_t j = rep * sizes.size() + i;
+      d.push_back({ldst[j].data(), lsrc[j].data(), sizes[i]});
+      z.push_back(sizes[i]);
+      sa.push_back(reinterpret_cast<uint64_t>(lsrc[j].data()));
+      da.push_back(reinterpret_cast<uint64_t>(ldst[j].data()));
+    }
+    return make_list_transfer(MMA_D2H, d.data(), d.size(), z.data(), sa.data(), da.data(), h.cfg());
+  };
+  uint64_t total = 0;
+  for (uint64_t z : sizes) total += z;
+  auto d2h_tasks = [&]() {
+    std::array<uint64_t, MMA_NUM_PATHS> t{};
+    std::lock_guard<std::mutex> g(g_trace_mu);
+    for (const auto& r : g_trace_buf)
+      if (r.dir == MMA_D2H)
+        for (int i = 0; i < MMA_NUM_PATHS; ++i) t[i] += r.path_tasks[i];
+    g_trace_buf.clear();
+    return t;
+  };
+  g_trace = 1;
+  h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, a);
+  sleep_ns(5000000);
+  CHECK(h.engine(MMA_H2D)->moving(), "the host-to-device copy is not moving after 5 ms");
+  h.submit(list(0), total, b);
+  b.synchronize();
+  CHECK(h.engine(MMA_D2H)->wait_idle(60000), "device-to-host list did not retire");
+  const bool h2d_still_moving = h.engine(MMA_H2D)->moving();
+  const auto t0 = d2h_tasks();
+  a.synchronize();
+  CHECK(h.sync(), "sync");
+  sleep_ns(3000000);  // past the hold time
+  h.submit(list(1), total, b);
+  b.synchronize();
+  CHECK(h.sync(), "sync");
+  const auto t1 = d2h_tasks();
+  g_trace = 0;
+  CHECK(dst == src, "host-to-device bytes differ");
+  for (size_t j = 0; j < ldst.size(); ++j) CHECK(ldst[j] == lsrc[j], "device-to-host tensor %zu differs", j);
+  std::printf("     during: engines 0-1 %llu, 2-3 %llu, CU %llu tasks; after: engines 0-1 %llu, 2-3 %llu, CU %llu\n",
+              (unsigned long long)(t0[0] + t0[1]), (unsigned long long)(t0[2] + t0[3]), (unsigned long long)t0[16],
+              (unsigned long long)(t1[0] + t1[1]), (unsigned long long)(t1[2] + t1[3]), (unsigned long long)t1[16]);
+  CHECK(h2d_still_moving, "the host-to-device copy ended before the device-to-host list (slow host?)");
+  CHECK(t0[0] + t0[1] == 0 && t0[2] + t0[3] > 0 && t0[16] == 1,
+        "while host-to-device moved: device-to-host tasks outside engines 2-3 and the small tensor's CU task");
+  CHECK(t1[2] + t1[3] == 0 && t1[0] + t1[1] + t1[16] > 0, "alone: device-to-host tasks on engines 2-3");
+  CHECK(h.stats().failed.load() == 0, "failed transfers");
+  std::printf("ok   while the other direction moves, a direction pulls from its duplex paths only\n");
+}
+
 void pull_tracks_best_static_split() {
   for (double ratio : {1.0, 2.0}) {
     const double eng = 1000, cu = 1000 * ratio;  // CU path ratio x faster
@@ -1485,6 +1570,7 @@ int main(int argc, char** argv) {
   }
   if (timing) {
     duplex_peer_commands();
+    duplex_paths();
     slow_engine_gets_fewer_tasks();
     pull_tracks_best_static_split();
   }

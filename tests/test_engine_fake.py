@@ -7,7 +7,9 @@ byte-exact copies, tensor lists and paged-KV fetch/offload through staging, that
 micro-task is retired once, merged copy-engine commands, re-routed submit failures, two
 streams in flight, that an engine busy with another component's work is skipped, that the
 other direction's commands on a shared engine count as neither foreign work nor congestion
-(Section 5.1.2, concurrent flows), that a slower engine pulls fewer micro-tasks, and that
+(Section 5.1.2, concurrent flows), that while the other direction moves a direction pulls from
+its duplex paths only (CU-only micro-tasks excepted), that a slower engine pulls fewer
+micro-tasks, and that
 pull-based selection comes within 5% of the best fixed split (the paper's static-split
 comparison, Section 5.1.2).
 Under device control (no engine thread in the loop) it checks exact copies on idle streams
