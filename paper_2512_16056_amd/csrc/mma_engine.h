@@ -607,8 +607,15 @@ class Engine {
     }
     const uint64_t total = (bytes + sub - 1) / sub;
     const uint64_t per_task = (cfg_.chunk + sub - 1) / sub;
-    uint64_t inflight = cu_enabled() ? cfg_.cu_depth * per_task : 0;
-    if (staged) inflight += static_cast<uint64_t>(__builtin_popcount(sdma_mask())) * cfg_.depth * per_task;
+    // Entries in flight with a phase's paths (the direction's own, or its
+    // duplex paths while the other direction moves; see set_peer): the CU
+    // path's depth, and for staged transfers each engine's staging.
+    const auto inflight_with = [&](uint32_t paths) {
+      uint64_t f = (paths & MMA_PATH_CU) && cu_enabled() ? cfg_.cu_depth * per_task : 0;
+      if (staged) f += static_cast<uint64_t>(__builtin_popcount(paths & sdma_mask())) * cfg_.depth * per_task;
+      return f;
+    };
+    const uint64_t inflight = std::max(inflight_with(cfg_.mask[dir_]), inflight_with(cfg_.duplex[dir_]));
     uint64_t g = (std::max<uint64_t>(1, std::min(total, inflight)) + kWavesPerWG - 1) / kWavesPerWG;
     g = std::max<uint64_t>(1, std::min<uint64_t>(g, wg_cap(wide)));
     return static_cast<uint32_t>(g);
