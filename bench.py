@@ -521,19 +521,17 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
 
     # Mixed contention: the wake-up list as 34 groups on stream A, each followed by the dependent
     # digest kernel over the group, while the 2048-block offload runs on stream B; 256 KiB chunks.
-    # A and B are a pair of streams shown to run side by side (see concurrent_stream_pair).
-    sa, sb, side_by_side = concurrent_stream_pair(torch)
+    # A and B run side by side (see side_by_side_schedules).
     extras["mixed_contention"] = mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan,
-                                                  arena, offs, sizes, wdst, Dw, Sw, Zw, lp, (sa, sb))
+                                                  arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
     mc = extras["mixed_contention"]
-    mc["streams_side_by_side"] = side_by_side
     mc["duplex_probe_GBs"] = peaks.get("duplex_GBs")
     if mc["mma"].get("overlap_aggregate_GBs") and peaks.get("duplex_GBs"):
         mc["overlap_frac_of_duplex_probe"] = round(mc["mma"]["overlap_aggregate_GBs"] / peaks["duplex_GBs"], 3)
 
     # All five workloads under both control modes, with the engine threads' CPU time per call.
     extras["control_modes"] = control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_blocks, plan,
-                                            arena, offs, sizes, wdst, Dw, Sw, Zw, lp, (sa, sb))
+                                            arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
     extras["device_control"] = extras["control_modes"]["device"]["kv_fetch_64k"]
     del wdst
     arena.free()
@@ -541,7 +539,7 @@ def run_extras(mma, W, np, torch, s, pool, layers, lay, hs, gb, stream, ms_per_s
 
 
 def control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_blocks, plan, arena, offs, sizes, wdst,
-                  Dw, Sw, Zw, lp, mixed_streams):
+                  Dw, Sw, Zw, lp):
     """The five workloads under host control (engine threads pull for every path) and device control
     (the calling thread plans each transfer, the dummy-task kernel alone tracks it), each on a
     stream of its own: median time and GB/s, and the engine threads' CPU time per call (their
@@ -597,10 +595,11 @@ def control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_bloc
             c.chunk_bytes = 256 << 10
             mma.mma_init(0, c)
             c0 = cpu_ns()
-            mx = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan,
-                                            arena, offs, sizes, wdst, Dw, Sw, Zw, lp, reps=1, streams=mixed_streams)
+            mx, _, tried = side_by_side_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan,
+                                                  arena, offs, sizes, wdst, Dw, Sw, Zw, lp)
             c1 = cpu_ns()
-            r["mixed_contention"] = {**mx, "engine_cpu_ms_per_schedule": round((c1 - c0) / 1e6 / 2, 3)}
+            r["mixed_contention"] = {**mx, "stream_pairs_tried": tried,
+                                     "engine_cpu_ms_per_schedule": round((c1 - c0) / 1e6 / (4 * tried), 3)}
             r["failed_transfers"] += mma.mma_get_stats()["failed_transfers"]
             mma.mma_finalize()
             out[mode] = r
@@ -635,7 +634,7 @@ def sampled_fetch_parity(s, pv, layers, hs, gb, gpu_layout, samples=64, seed=0):
 
 
 def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, plan, arena, offs, sizes, wdst,
-                     Dw, Sw, Zw, lp, streams):
+                     Dw, Sw, Zw, lp):
     groups = W.weight_groups()
     assert all(list(g) == list(range(g[0], g[0] + len(g))) for g in groups)
     res = {}
@@ -647,8 +646,9 @@ def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, p
     try:
         for t in range(len(sizes)):
             wdst[t].fill_(W.WEIGHT_POISON)
-        r = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena, offs,
-                                       sizes, wdst, Dw, Sw, Zw, lp, reps=1, streams=streams)
+        r, streams, tried = side_by_side_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
+                                                   offs, sizes, wdst, Dw, Sw, Zw, lp)
+        r["stream_pairs_tried"] = tried
         mma.mma_synchronize()
         g = np.random.default_rng(2)
         ok = True
@@ -664,9 +664,9 @@ def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, p
     finally:
         mma.mma_finalize()
         mma.mma_init(0, cfg)
-    res["native"] = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
-                                               offs, sizes, wdst, Dw, Sw, Zw, lp, native=True, reps=1,
-                                               streams=streams)
+    res["native"], _, tried = side_by_side_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan,
+                                                     arena, offs, sizes, wdst, Dw, Sw, Zw, lp, native=True)
+    res["native"]["stream_pairs_tried"] = tried
     res["makespan_speedup_vs_native"] = round(res["native"]["makespan_ms"] / res["mma"]["makespan_ms"], 3)
     res["stream_a_ratio_vs_native"] = round(res["native"]["stream_a_weights_digests_ms"] /
                                             res["mma"]["stream_a_weights_digests_ms"], 3)
@@ -1168,8 +1168,13 @@ def sweep_mixed(sizes=None, rounds=6):
              ("duplex h2d engines 0-1 + cu, d2h engines 2-5", dict(duplex_paths_h2d=CU | 0x3)),
              ("duplex h2d engines 0-1, d2h engines 2-3", dict(duplex_paths_d2h=0xC)),
              ("native", None)]
-    streams = concurrent_stream_pair(torch)
-    _emit(sweep="mixed", streams_side_by_side=streams[2])
+    c = mma.mma_config_default()
+    c.chunk_bytes = 256 << 10
+    mma.mma_init(0, c)
+    r, streams, tried = side_by_side_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
+                                               offs, sizes_w, wdst, Dw, Sw, Zw, lp, reps=1)
+    mma.mma_finalize()
+    _emit(sweep="mixed", streams_side_by_side=r["concurrent"], stream_pairs_tried=tried)
     for rnd in range(rounds):
         for name, kv in cases[rnd % len(cases):] + cases[:rnd % len(cases)]:
             c = mma.mma_config_default()
@@ -1180,7 +1185,7 @@ def sweep_mixed(sizes=None, rounds=6):
             mma.mma_trace_enable(True)
             r = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
                                            offs, sizes_w, wdst, Dw, Sw, Zw, lp, native=kv is None, reps=1,
-                                           streams=streams[:2])
+                                           streams=streams)
             a, b = r["stream_a_weights_digests_ms"], r["stream_b_offload_ms"]
             mma.mma_synchronize()
             st = mma.mma_get_stats()
@@ -1203,29 +1208,24 @@ def sweep_mixed(sizes=None, rounds=6):
     pool.free()
 
 
-def concurrent_stream_pair(torch, tries=16):
-    """Two streams that run side by side. The runtime maps streams onto a few hardware queues
-    (GPU_MAX_HW_QUEUES, 4 by default), so two new streams may share one; a kernel on one then
-    starts only after the kernels queued before it on the other. (The copy engines' commands of
-    a runtime copy are ordered by stream, not by hardware queue, so runtime copies do not see
-    this.) Probe: a sleep kernel on A, then an event on B, which must complete while A still
-    sleeps. Returns (A, B, True), or the last pair tried and False."""
-    import time as _t
-    for _ in range(tries):
-        sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
-        torch.cuda.synchronize()
-        with torch.cuda.stream(sa):
-            torch.cuda._sleep(200_000_000)  # about 0.1 s of GPU clock cycles
-        e = torch.cuda.Event()
-        e.record(sb)
-        t0 = _t.perf_counter()
-        while not e.query() and _t.perf_counter() - t0 < 5.0:
-            pass
-        ok = e.query() and not sa.query()
-        torch.cuda.synchronize()
-        if ok:
-            return sa, sb, True
-    return sa, sb, False
+def side_by_side_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena, offs, sizes, wdst,
+                           Dw, Sw, Zw, lp, native=False, tries=6, reps=3):
+    """mixed_contention_schedules on a pair of new streams that ran side by side. The runtime maps
+    streams onto a few hardware queues (GPU_MAX_HW_QUEUES, 4 by default), and two streams may
+    share one: a kernel or timing marker on one then waits for what was queued before it on the
+    other, so the offload (and its first timing event) starts only when stream A has ended. The
+    copy engines' commands of a runtime copy are ordered by stream, not by hardware queue, but
+    the native schedule's timing events see the same wait. No separate probe predicts it (a sleep
+    kernel on A beside an event or a kernel on B passed for pairs that then ran one after the
+    other), so the schedule itself is the test: a pair whose offload started only after A ended
+    is replaced by two new streams, up to `tries` times. Returns (result, streams, pairs tried)."""
+    for k in range(tries):
+        pair = (torch.cuda.Stream(), torch.cuda.Stream())
+        r = mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena, offs, sizes,
+                                       wdst, Dw, Sw, Zw, lp, native=native, reps=reps, streams=pair)
+        if r["concurrent"]:
+            break
+    return r, pair, k + 1
 
 
 def mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena, offs, sizes,
@@ -1244,6 +1244,7 @@ def mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blo
         ea = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         eb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         torch.cuda.synchronize()
+        t_host = time.perf_counter()
         ea[0].record(sa)
         for g in groups:
             if not native:
@@ -1255,6 +1256,7 @@ def mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blo
             for t in g:
                 mma.mma_digest_u32(wdst[t], sizes[t], digests.data_ptr() + 8 * t, sa)
         ea[1].record(sa)
+        b_host = (time.perf_counter() - t_host) * 1e3  # when the host got to issue B's work
         eb[0].record(sb)
         if not native:
             mma.mma_kv_offload(lay, pool, layers, src_blocks, plan.dest, sb)
@@ -1265,14 +1267,14 @@ def mixed_contention_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blo
         eb[1].record(sb)
         torch.cuda.synchronize()
         a, b, b0 = ea[0].elapsed_time(ea[1]), eb[0].elapsed_time(eb[1]), ea[0].elapsed_time(eb[0])
-        out.append((a, b, b0, max(a, ea[0].elapsed_time(eb[1]))))
+        out.append((a, b, b0, max(a, ea[0].elapsed_time(eb[1])), b_host))
     out = out[1:]
 
     def med(i):
         return sorted(x[i] for x in out)[len(out) // 2]
     return {"stream_a_weights_digests_ms": round(med(0), 1), "stream_b_offload_ms": round(med(1), 1),
             "stream_b_start_ms": round(med(2), 1), "makespan_ms": round(med(3), 1),
-            "concurrent": all(x[2] < x[0] for x in out)}
+            "stream_b_issued_host_ms": round(med(4), 1), "concurrent": all(x[2] < x[0] for x in out)}
 
 
 def sweep_paths():
