@@ -133,16 +133,18 @@ typedef struct mma_config {
                                  micro-tasks still goes to the engine thread. */
   uint32_t duplex_paths_h2d; /* paths host->device pulls from while a device->host transfer is
                                moving (Section 5.1.2, concurrent flows; host control only).
-                               0 (default): the host-facing SDMA engines of path_mask_h2d, without
-                               the CU path. MMA_DUPLEX_UNCHANGED: path_mask_h2d. Each copy engine
+                               0 (default): the SDMA engines of path_mask_h2d, without the CU
+                               path. MMA_DUPLEX_UNCHANGED: path_mask_h2d. Each copy engine
                                runs one in-order queue for both directions, and CU zero-copy loads
                                send their read requests up the lanes that device->host data uses.
                                Micro-tasks only the CU path may carry still take it. */
   uint32_t duplex_paths_d2h; /* paths device->host pulls from while a host->device transfer is
-                               moving. 0 (default): SDMA engines 2-5 (on MI355X the xGMI-facing
-                               engines, 13-18 GB/s each toward the host), neither the host-facing
-                               engines nor the CU path, whose stores to host memory share the
-                               upstream lanes in small writes; MMA_DUPLEX_UNCHANGED: path_mask_d2h.
+                               moving. 0 (default): with the default path_mask_d2h, SDMA engines
+                               2-5 (on MI355X the xGMI-facing engines, 13-18 GB/s each toward the
+                               host), neither the host-facing engines nor the CU path, whose stores
+                               to host memory share the upstream lanes in small writes; with a
+                               path_mask_d2h given, its SDMA engines without the CU path.
+                               MMA_DUPLEX_UNCHANGED: path_mask_d2h.
                                Engines the device does not offer are dropped; a set left with no
                                path, or a CU path the direction does not have, falls back to its
                                path mask. */

@@ -552,6 +552,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   hsa_agent_get_info(rt->ag.gpu, static_cast<hsa_agent_info_t>(HSA_AMD_AGENT_INFO_NUM_SDMA_ENG), &nsdma);
   const uint32_t host_facing = nsdma >= 16 ? 0xFFFFu : ((1u << nsdma) - 1u);
   uint32_t mask[2] = {c.path_mask_h2d, c.path_mask_d2h};
+  const bool mask_given[2] = {c.path_mask_h2d != 0, c.path_mask_d2h != 0};
   for (int d = 0; d < 2; ++d) {
     if (!mask[d]) mask[d] = MMA_PATH_CU | (avail[d] & host_facing);
     mask[d] = (mask[d] & MMA_PATH_CU) | (mask[d] & avail[d] & 0xFFFFu);
@@ -567,7 +568,9 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
       duplex[d] = mask[d];
       continue;
     }
-    if (!duplex[d]) duplex[d] = d == MMA_H2D ? (mask[d] & host_facing & 0xFFFFu) : 0x3Cu;
+    // Default: the direction's engines without the CU path; for device-to-host
+    // with the default path mask, engines 2-5 instead of the host-facing ones.
+    if (!duplex[d]) duplex[d] = d == MMA_H2D || mask_given[d] ? (mask[d] & 0xFFFFu) : 0x3Cu;
     duplex[d] = (duplex[d] & mask[d] & MMA_PATH_CU) | (duplex[d] & avail[d] & 0xFFFFu);
     if (!duplex[d]) duplex[d] = mask[d];
   }
