@@ -1567,10 +1567,10 @@ int main(int argc, char** argv) {
     device_unlaunched_and_whole();
     shutdown_in_flight_keeps_shared_memory();
     foreign_work_skipped();
+    duplex_paths();
   }
   if (timing) {
     duplex_peer_commands();
-    duplex_paths();
     slow_engine_gets_fewer_tasks();
     pull_tracks_best_static_split();
   }
