@@ -459,10 +459,12 @@ class Engine {
   // zero-copy loads send their read requests upstream beside device-to-host
   // data, and CU stores to host memory share those lanes in small writes. On
   // the mixed workload (the 34-group weight load beside the 2048-block offload,
-  // streams side by side) that keeps the weight stream at 303.9 ms against the
-  // native schedule's 303.5 ms, with the offload at 104 ms; all paths shared:
-  // 310.6 and 178 ms. The CU path still takes micro-tasks that no other path
-  // may carry. Called once both engines are initialised.
+  // streams side by side) that keeps the weight stream within 0.4% of the
+  // native schedule (304.3-305.2 ms against 303.4-303.7 ms), with the offload
+  // at 102-104 ms; all paths shared: 309-312 and 170-174 ms. The CU path still
+  // takes micro-tasks that no other path may carry. Device control has no
+  // phases: its copy-engine share stays on the direction's own path mask.
+  // Called once both engines are initialised.
   void set_peer(const Engine* peer) { peer_ = peer; }
   // Bytes of the other direction's commands in flight on copy engine e.
   uint64_t peer_bytes_on(int e) const { return peer_ ? peer_->eng_bytes_[e].load(std::memory_order_relaxed) : 0; }
@@ -852,9 +854,14 @@ class Engine {
     r->h.status = 0;
     __atomic_thread_fence(__ATOMIC_RELEASE);
 
-    // The copy engines' share: the last micro-tasks, by bytes.
+    // The copy engines' share: the last micro-tasks, by bytes, on the
+    // engines of the direction's own path mask (its duplex-only engines are
+    // for the engine thread's phases; see set_peer).
+    std::vector<int> dev_paths;
+    for (size_t k = 0; k < paths_.size(); ++k)
+      if ((cfg_.mask[dir_] >> paths_[k].engine) & 1u) dev_paths.push_back(static_cast<int>(k));
     std::vector<size_t> eng_tasks;
-    if (stream_idle && linear && x->sdma_ok && !dev_sig_.empty()) {
+    if (stream_idle && linear && x->sdma_ok && !dev_sig_.empty() && !dev_paths.empty()) {
       const uint64_t cu_pct = cu_enabled() ? cfg_.device_cu_percent : 0;
       const uint64_t want = payload_bytes / 100 * (100 - cu_pct) + payload_bytes % 100 * (100 - cu_pct) / 100;
       uint64_t got = 0;
@@ -870,9 +877,9 @@ class Engine {
     x->pushed = 0;
     for (size_t i = 0; i < n; ++i)
       if (!x->claimed[i]) push_device(x, i);
-    // Engine k takes the engine tasks whose first byte falls in the k-th equal
-    // part of their bytes; runs that follow each other in both address spaces
-    // go as one command.
+    // Engine k of dev_paths takes the engine tasks whose first byte falls in
+    // the k-th equal part of their bytes; runs that follow each other in both
+    // address spaces go as one command.
     struct Cmd {
       int path;
       size_t first, end;
@@ -884,7 +891,7 @@ class Engine {
     for (size_t k = 0; k < eng_tasks.size(); ++k) {
       const size_t i = eng_tasks[k];
       const Task& t = x->tasks[i];
-      const int path = static_cast<int>(at * paths_.size() / std::max<uint64_t>(total, 1));
+      const int path = dev_paths[at * dev_paths.size() / std::max<uint64_t>(total, 1)];
       at += t.bytes;
       if (!cmds.empty()) {
         Cmd& c = cmds.back();

@@ -1153,6 +1153,34 @@ void device_copies(bool idle) {
               (unsigned long long)sum_tasks(h.stats(), 0, 16));
 }
 
+// Device control has no engine-thread phases, so a direction's duplex-only
+// engines (here device-to-host engines 2-3) never take its copy-engine share:
+// idle-stream copies in both directions use engines 0-1 alone.
+void device_copies_keep_own_engines() {
+  Setup s = device_setup();
+  s.engine_rates = {2000, 2000, 2000, 2000};
+  s.duplex[MMA_D2H] = 0xC;
+  Harness h(s);
+  FakeStream st;
+  uint64_t init_bytes[4];  // each engine's warm-up command at init
+  for (int e = 0; e < 4; ++e) init_bytes[e] = h.backend().engine_bytes(e);
+  for (int dir = 0; dir < 2; ++dir) {
+    const uint64_t n = 6ull * 1024 * 1024 + 9;
+    auto src = random_bytes(n, static_cast<uint32_t>(31 + dir));
+    std::vector<uint8_t> dst(n);
+    h.submit_device(linear(dir, dst.data(), src.data(), n, h.cfg()), n, st, nullptr, true);
+    st.synchronize();
+    CHECK(h.sync(), "sync");
+    CHECK(dst == src, "device dir=%d: bytes differ", dir);
+  }
+  const uint64_t e01 = h.backend().engine_bytes(0) + h.backend().engine_bytes(1) - init_bytes[0] - init_bytes[1];
+  const uint64_t e23 = h.backend().engine_bytes(2) + h.backend().engine_bytes(3) - init_bytes[2] - init_bytes[3];
+  CHECK(e01 > 0 && e23 == 0, "device control: engines 0-1 %llu bytes, duplex-only engines 2-3 %llu bytes",
+        (unsigned long long)e01, (unsigned long long)e23);
+  std::printf("ok   device control keeps to the direction's own engines (engines 0-1 %llu bytes, 2-3 none)\n",
+              (unsigned long long)e01);
+}
+
 // Paged-KV fetch then offload under device control: the CU path alone.
 void device_kv_roundtrip() {
   Setup s = device_setup();
@@ -1562,6 +1590,7 @@ int main(int argc, char** argv) {
     two_streams_both_directions();
     device_copies(true);
     device_copies(false);
+    device_copies_keep_own_engines();
     device_kv_roundtrip();
     device_recycling_and_refusals();
     device_unlaunched_and_whole();
