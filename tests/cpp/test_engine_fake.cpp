@@ -1512,8 +1512,10 @@ void duplex_paths() {
   };
   g_trace = 1;
   h.submit(linear(MMA_H2D, dst.data(), src.data(), n, h.cfg()), n, a);
-  sleep_ns(5000000);
-  CHECK(h.engine(MMA_H2D)->moving(), "the host-to-device copy is not moving after 5 ms");
+  // the fake stream starts the transfer on a host thread: wait for it (a loaded host,
+  // or a sanitizer build, can take several milliseconds)
+  for (int i = 0; i < 2000 && !h.engine(MMA_H2D)->moving(); ++i) sleep_ns(1000000);
+  CHECK(h.engine(MMA_H2D)->moving(), "the host-to-device copy is not moving after 2 s");
   h.submit(list(0), total, b);
   b.synchronize();
   CHECK(h.engine(MMA_D2H)->wait_idle(60000), "device-to-host list did not retire");
