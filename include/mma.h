@@ -148,7 +148,14 @@ typedef struct mma_config {
                                Engines the device does not offer are dropped; a set left with no
                                path, or a CU path the direction does not have, falls back to its
                                path mask. */
+  uint32_t engine_nap_us;   /* host control: the longest a direction's engine thread sleeps between
+                               two rounds of its loop (Section 5.3, CPU overhead). It sleeps only
+                               while every path has work queued for longer than the nap and no
+                               transfer is near its end, and a submission wakes it at once.
+                               Default 50; MMA_ENGINE_NAP_OFF: poll without sleeping while a
+                               transfer is in flight (the paper's engine); at most 1000. */
 } mma_config_t;
+#define MMA_ENGINE_NAP_OFF 0xFFFFFFFFu
 
 typedef struct mma_copy_desc {
   void* dst;
@@ -212,6 +219,8 @@ typedef struct mma_stats {
   uint32_t reserved;
   uint64_t pool_launches;                 /* KV transfers with the pool in this GPU's memory carried by
                                              one pool-kernel launch (the others took the ring path) */
+  uint64_t engine_naps;                   /* sleeps of the engine threads between rounds of their loop
+                                             while transfers were in flight (engine_nap_us) */
 } mma_stats_t;
 
 /* One micro-task of a plan (host-only planner, exposed for verification).

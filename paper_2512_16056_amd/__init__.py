@@ -31,6 +31,7 @@ MMA_H2D = 0
 MMA_D2H = 1
 MMA_PATH_CU = 0x80000000
 MMA_DUPLEX_UNCHANGED = 0xFFFFFFFF  # duplex_paths_*: keep the direction's own paths
+MMA_ENGINE_NAP_OFF = 0xFFFFFFFF  # engine_nap_us: the engine threads poll without sleeping
 MMA_KV_LAYOUT_PIECE = 0
 MMA_KV_LAYOUT_XPACKED = 1
 MMA_KV_LAYOUT_HND = 2
@@ -72,7 +73,7 @@ class mma_config_t(ctypes.Structure):
                 ("static_cu_percent", ctypes.c_uint32), ("sdma_merge_tasks", ctypes.c_uint32),
                 ("cu_whole_bytes", ctypes.c_uint32), ("cu_whole_bytes_d2h", ctypes.c_uint32),
                 ("control", ctypes.c_uint32), ("duplex_paths_h2d", ctypes.c_uint32),
-                ("duplex_paths_d2h", ctypes.c_uint32)]
+                ("duplex_paths_d2h", ctypes.c_uint32), ("engine_nap_us", ctypes.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -98,7 +99,7 @@ class mma_stats_t(ctypes.Structure):
                 ("sdma_commands", ctypes.c_uint64),
                 ("sdma_engines_h2d", ctypes.c_uint32), ("sdma_engines_d2h", ctypes.c_uint32),
                 ("cu_path_enabled", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
-                ("pool_launches", ctypes.c_uint64)]
+                ("pool_launches", ctypes.c_uint64), ("engine_naps", ctypes.c_uint64)]
 
     def as_dict(self):
         d = {k: getattr(self, k) for k, _ in self._fields_ if k not in ("reserved", "path_bytes", "path_tasks")}

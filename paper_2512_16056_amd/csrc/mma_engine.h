@@ -21,6 +21,7 @@
 #define MMA_ENGINE_H_
 
 #include <pthread.h>
+#include <sys/prctl.h>
 #include <time.h>
 
 #include <algorithm>
@@ -162,12 +163,14 @@ struct Transfer {
   std::unique_ptr<int32_t[]> owner;  // >= 0: CU-path task; < 0: -(1 + SDMA slot id)
   std::unique_ptr<uint8_t[]> tdone;  // its done tag has been seen
   uint32_t cu_busy = 0;
+  uint64_t cu_entries = 0;     // ring entries of CU-path micro-tasks appended and not seen done
   bool cu_full = false;
   int sdma_cu_pending = 0;     // SDMA slots that may still append ring entries (a staging step, or a
                                // re-route of their micro-tasks to the CU path)
   int sdma_refs = 0;           // SDMA slots referencing this transfer
   uint64_t heartbeat = 0;
   uint64_t bytes = 0;          // payload bytes
+  uint64_t done_bytes = 0;     // payload bytes of the micro-tasks landed so far (engine thread)
   // trace timestamps (CLOCK_MONOTONIC ns)
   uint64_t t_api = 0, t_submit = 0, t_started = 0, t_first_sdma = 0, t_last_task = 0, t_complete = 0;
   uint64_t t_released = 0;     // when the kernel was seen to release the record with tags still missing
@@ -210,6 +213,7 @@ struct SdmaPath {
   bool full = false;
   bool congested = false;  // a command is long overdue: pull nothing more until the engine drains
   uint64_t t_head = 0;     // when the path's oldest command in flight reached the head of its queue
+  double ns_per_byte = 0;  // measured time per byte of its commands (moving average; 0: none yet)
 };
 
 struct Config {
@@ -223,11 +227,14 @@ struct Config {
   uint32_t device_cu_percent;  // device control: the CU path's share of a linear transfer's bytes
   uint32_t overdue_gbs;        // link rate the overdue rule assumes, GB/s (0: 50)
   uint32_t duplex[2];          // per direction: the paths used while the other direction moves (see set_peer)
+  uint64_t nap_ns;             // longest sleep of the engine thread between rounds (see nap); 0: poll
+  uint64_t duplex_hold_ns;     // a direction counts as moving this long after it was last seen moving
+                               // (0: kDuplexHoldNs)
 };
 
 struct Stats {
   std::atomic<uint64_t> transfers{0}, failed{0}, staging_bytes{0}, submit_failures{0}, busy_ns{0};
-  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0}, sdma_commands{0}, pool_launches{0};
+  std::atomic<uint64_t> foreign_skips{0}, congestion_backoffs{0}, sdma_commands{0}, pool_launches{0}, naps{0};
   std::atomic<uint64_t> path_bytes[MMA_NUM_PATHS], path_tasks[MMA_NUM_PATHS];
   Stats() {
     for (auto& v : path_bytes) v = 0;
@@ -235,7 +242,7 @@ struct Stats {
   }
   void reset() {
     transfers = failed = staging_bytes = submit_failures = busy_ns = foreign_skips = congestion_backoffs = 0;
-    sdma_commands = pool_launches = 0;
+    sdma_commands = pool_launches = naps = 0;
     for (auto& v : path_bytes) v = 0;
     for (auto& v : path_tasks) v = 0;
   }
@@ -356,7 +363,12 @@ class Engine {
     }
     mma_status_t w = warm_up();
     if (w != MMA_OK) return w;
-    thread_ = std::thread([this] { loop(); });
+    thread_ = std::thread([this] {
+      // Naps of tens of microseconds (see nap): wake within 1 us of the
+      // deadline instead of the default 50 us of timer slack.
+      prctl(PR_SET_TIMERSLACK, 1000UL, 0UL, 0UL, 0UL);
+      loop();
+    });
     return MMA_OK;
   }
 
@@ -1025,7 +1037,7 @@ class Engine {
       wake = engine_waiting_;
     }
     n_incoming_.fetch_add(1, std::memory_order_release);
-    if (wake) cv_.notify_all();  // the engine thread sleeps only after 2 ms without work
+    if (wake) cv_.notify_all();  // the engine thread sleeps after 2 ms without work, or naps
   }
 
   bool wait_idle(uint64_t timeout_ms) {
@@ -1101,6 +1113,7 @@ class Engine {
     if (x->n_done == x->tasks.size()) x->t_last_task = now_ns();
     const Task& t = x->tasks[i];
     const uint64_t bytes = x->kind == Kind::kLinear ? t.bytes : t.bytes * x->piece;
+    x->done_bytes += bytes;
     st_->path_bytes[path_stat] += bytes;
     st_->path_tasks[path_stat] += 1;
     x->progress = true;
@@ -1116,6 +1129,7 @@ class Engine {
       p = true;
       const int32_t own = x->owner[slot];
       if (own >= 0) {
+        --x->cu_entries;
         if (--x->left[own] == 0) {
           --x->cu_busy;
           task_done(x, static_cast<size_t>(own), MMA_NUM_PATHS - 1);
@@ -1224,6 +1238,7 @@ class Engine {
       ++x->n_claimed;
       if (t.flags & kPlanCuOnly) --x->cu_only_left;
       x->left[i] = ne;
+      x->cu_entries += ne;
       ++x->cu_busy;
       p = true;
     }
@@ -1360,7 +1375,13 @@ class Engine {
       Transfer* x = s.x;
       x->progress = true;
       // The engine runs our commands in order: the next one is at the head now.
-      paths_[s.path].t_head = now_ns();
+      SdmaPath& path = paths_[s.path];
+      const uint64_t now = now_ns(), start = std::max(path.t_head, s.t_submit);
+      if (v == 0 && now > start && s.op_bytes >= kRateMinBytes) {
+        const double obs = static_cast<double>(now - start) / static_cast<double>(s.op_bytes);
+        path.ns_per_byte = path.ns_per_byte > 0 ? 0.75 * path.ns_per_byte + 0.25 * obs : obs;
+      }
+      path.t_head = now;
       eng_bytes_[paths_[s.path].engine].fetch_sub(s.op_bytes, std::memory_order_relaxed);
       if (v < 0) {
         x->failed = true;
@@ -1678,6 +1699,91 @@ class Engine {
     return n;
   }
 
+  // How long the engine thread may sleep before its next round (Section 5.3,
+  // CPU overhead): 0 to poll on. A nap must delay neither a path's next
+  // micro-task nor a transfer's completion. With R the link rate the overdue
+  // rule assumes, it is bounded by:
+  //  - each copy engine with commands of ours in flight: half the time until
+  //    the last of them could end at the fastest rate the engine may run --
+  //    1.5 times its measured rate, at most R -- counted from when the first
+  //    reached the head of the queue, and kLateNapNs once that time has
+  //    passed; so the thread looks often when they land and when the engine
+  //    needs its next command;
+  //  - a transfer waiting for its start signal: a 256th of its bytes at R
+  //    (the copy engines join at most that late; the CU path starts with the
+  //    kernel, from its prefilled entries);
+  //  - a started transfer: a 64th, at R, of its bytes that are neither landed
+  //    nor in a copy-engine command, so naps shrink to nothing as the CU path
+  //    finishes it, and stop once copy-engine commands hold all that is left;
+  //  - its CU path, while micro-tasks remain that the CU path may take: half
+  //    the time its outstanding ring entries beyond one per wave (which may
+  //    be nearly done) take at R -- none if there are no more than that.
+  // Nor does the thread nap with a transfer submitted but not yet taken in, a
+  // transfer completed or failed but not retired, a staging step waiting for
+  // ring room, or a copy engine idle while a staging step of its own runs.
+  uint64_t nap() const {
+    if (!cfg_.nap_ns || n_incoming_.load(std::memory_order_relaxed)) return 0;
+    const uint64_t gbs = cfg_.overdue_gbs ? cfg_.overdue_gbs : 50;  // 1 GB/s = 1 byte per ns
+    const uint64_t now = now_ns();
+    uint64_t ns = cfg_.nap_ns;
+    // payload bytes in copy-engine commands, per transfer (few are active)
+    auto& on_engines = nap_scratch_;
+    on_engines.clear();
+    for (const auto& path : paths_) {
+      const SdmaSlot* q[64];
+      size_t n = 0;
+      bool staging = false;
+      for (int id : path.slots) {
+        const SdmaSlot& sl = slots_[id];
+        if (sl.state == kH2DScatterPush || sl.state == kD2HGatherPush) return 0;
+        if (engine_op(sl) && n < 64)
+          q[n++] = &sl;
+        else if (sl.state != kFree)
+          staging = true;
+      }
+      if (!n) {
+        if (staging) return 0;
+        continue;
+      }
+      std::sort(q, q + n, [](const SdmaSlot* a, const SdmaSlot* b) { return a->t_submit < b->t_submit; });
+      const double fast = std::max(path.ns_per_byte / 1.5, 1.0 / static_cast<double>(gbs));
+      double end = static_cast<double>(std::max(path.t_head, q[0]->t_submit));
+      for (size_t k = 0; k < n; ++k) {
+        end += fast * static_cast<double>(q[k]->op_bytes);
+        const Transfer* x = q[k]->x;
+        const uint64_t b = x->kind == Kind::kLinear ? q[k]->count : q[k]->count * x->piece;
+        auto it = std::find_if(on_engines.begin(), on_engines.end(), [x](const auto& e) { return e.first == x; });
+        if (it == on_engines.end())
+          on_engines.push_back({x, b});
+        else
+          it->second += b;
+      }
+      ns = std::min(ns, end > static_cast<double>(now) ? static_cast<uint64_t>((end - static_cast<double>(now)) / 2)
+                                                        : kLateNapNs);
+    }
+    for (const auto& up : active_) {
+      const Transfer* x = up.get();
+      if (x->completed || x->failed || x->ignored || x->aborting || x->unlaunched.load(std::memory_order_relaxed))
+        return 0;
+      if (!x->started) {
+        ns = std::min(ns, x->bytes / gbs / 256);
+        continue;
+      }
+      uint64_t eng = 0;
+      for (const auto& e : on_engines)
+        if (e.first == x) eng = e.second;
+      ns = std::min(ns, (x->bytes - std::min(x->bytes, x->done_bytes + eng)) / gbs / 64);
+      const bool cu_takes = (cu_enabled() && !cu_paused_) || x->pool_dev || x->cu_only_left > 0;
+      if (cu_takes && x->n_claimed < x->tasks.size()) {
+        if (x->cu_entries <= x->waves) return 0;
+        const uint64_t per_entry = x->kind == Kind::kLinear ? x->sub
+                                   : (x->kv_per ? x->kv_per : std::max<uint64_t>(1, cfg_.sub / x->piece)) * x->piece;
+        ns = std::min(ns, (x->cu_entries - x->waves) * per_entry / gbs / 2);
+      }
+    }
+    return ns;
+  }
+
   bool retire_ready(Transfer* x) {
     // A self-contained kernel's done tags are its last accesses to the record.
     if (x->self_contained) return x->n_done == x->tasks.size();
@@ -1760,8 +1866,21 @@ class Engine {
       }
       bool moving = false;
       for (auto& up : active_) moving |= up->started && !up->completed && !up->failed;
-      if (moving) moving_until_.store(now_ns() + kDuplexHoldNs, std::memory_order_relaxed);
-      if (p) {
+      if (moving)
+        moving_until_.store(now_ns() + (cfg_.duplex_hold_ns ? cfg_.duplex_hold_ns : kDuplexHoldNs),
+                            std::memory_order_relaxed);
+      const uint64_t nap_ns = active_.empty() ? 0 : nap();
+      if (nap_ns >= kMinNapNs) {
+        // A submission wakes the thread (engine_waiting_), as in the idle wait.
+        idle_spins = 0;
+        std::unique_lock<std::mutex> lk(mu_);
+        if (incoming_.empty() && !stop_) {
+          st_->naps += 1;
+          engine_waiting_ = true;
+          cv_.wait_for(lk, std::chrono::nanoseconds(nap_ns));
+          engine_waiting_ = false;
+        }
+      } else if (p) {
         idle_spins = 0;
       } else if (++idle_spins < 20000) {
         cpu_relax();
@@ -1808,6 +1927,7 @@ class Engine {
   std::atomic<uint64_t> eng_bytes_[MMA_MAX_SDMA] = {};
   std::atomic<uint64_t> moving_until_{0};  // see peer_moving (read by the other direction)
   uint32_t usable_ = 0;                    // paths of this phase (see phase)
+  mutable std::vector<std::pair<const Transfer*, uint64_t>> nap_scratch_;  // see nap (engine thread)
   bool cu_paused_ = false;                 // the CU path takes only CU-only micro-tasks (see set_peer)
   size_t n_pull_paths_ = 0;                // copy-engine paths pull_sdma may use this round
   const Engine* peer_ = nullptr;          // the other direction's engine
@@ -1822,6 +1942,9 @@ class Engine {
   // direction's paths back and forth.
   static constexpr uint64_t kDuplexHoldNs = 1000000;  // 1 ms
   static constexpr uint64_t kTagGraceNs = 100000000;  // 100 ms
+  static constexpr uint64_t kMinNapNs = 4000;  // shorter naps cost more than the polls they save
+  static constexpr uint64_t kRateMinBytes = 256 * 1024;  // commands that time an engine's rate
+  static constexpr uint64_t kLateNapNs = 10000;  // nap once a copy engine's commands may have landed
   static constexpr size_t kReapWindow = 512;
   std::thread thread_;
 };

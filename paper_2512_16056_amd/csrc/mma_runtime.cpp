@@ -459,7 +459,9 @@ void fill_config(mma_config_t* c, bool use_env) {
   d.cu_whole_bytes = static_cast<uint32_t>(kPrefill * kWholeMaxSub);
   d.cu_whole_bytes_d2h = static_cast<uint32_t>(8 * MiB);
   d.control = MMA_CONTROL_HOST;
+  d.engine_nap_us = 50;
   if (use_env) {
+    d.engine_nap_us = static_cast<uint32_t>(env_u64("MMA_ENGINE_NAP_US", d.engine_nap_us));
     d.control = static_cast<uint32_t>(env_u64("MMA_CONTROL", d.control));
     d.static_cu_percent = static_cast<uint32_t>(env_u64("MMA_STATIC_CU_PERCENT", 0));
     d.duplex_paths_h2d = static_cast<uint32_t>(env_u64("MMA_DUPLEX_PATHS_H2D", 0));
@@ -518,6 +520,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
     if (!c.watchdog_ms) c.watchdog_ms = d.watchdog_ms;
     if (!c.cu_whole_bytes) c.cu_whole_bytes = d.cu_whole_bytes;
     if (!c.cu_whole_bytes_d2h) c.cu_whole_bytes_d2h = d.cu_whole_bytes_d2h;
+    if (!c.engine_nap_us) c.engine_nap_us = d.engine_nap_us;
   } else {
     fill_config(&c, true);
   }
@@ -526,6 +529,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   // reserve of one slot per wave.
   if (c.cu_sub_bytes % 16 || c.cu_sub_bytes < 256 || c.chunk_bytes % 16 || c.queue_depth > 16 ||
       c.cu_workgroups > kMaxWorkgroups || c.cu_queue_depth > 64 ||
+      (c.engine_nap_us > 1000 && c.engine_nap_us != MMA_ENGINE_NAP_OFF) ||
       (c.chunk_bytes + c.cu_sub_bytes - 1) / c.cu_sub_bytes > kRingSize / 2)
     return fail(MMA_ERR_INVALID_ARG, "invalid configuration");
 
@@ -600,6 +604,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   k.static_cu_percent = c.static_cu_percent;
   k.whole[MMA_H2D] = c.cu_whole_bytes;
   k.whole[MMA_D2H] = c.cu_whole_bytes_d2h;
+  k.nap_ns = c.engine_nap_us == MMA_ENGINE_NAP_OFF ? 0 : 1000ull * c.engine_nap_us;
   k.merge = c.sdma_merge_tasks ? c.sdma_merge_tasks
                               : static_cast<uint32_t>(std::max<uint64_t>(1, 64 * MiB / c.chunk_bytes));
 
@@ -1056,6 +1061,7 @@ mma_status_t mma_get_stats(mma_stats_t* out) {
   out->sdma_foreign_busy_skips = st.foreign_skips;
   out->sdma_commands = st.sdma_commands;
   out->pool_launches = st.pool_launches;
+  out->engine_naps = st.naps;
   out->sdma_congestion_backoffs = st.congestion_backoffs;
   uint64_t cpu = 0;
   for (auto& e : g_rt->eng) {

@@ -596,14 +596,20 @@ std::unique_ptr<Transfer> linear(int dir, void* dst, const void* src, uint64_t n
 }
 
 // ------------------------------------------------------------ scenarios
-void copies_are_exact(uint32_t mask, const char* name, bool early = false) {
+// nap_ns > 0: the engine thread naps between rounds; the fake paths are slow,
+// so the nap bounds assume a 1 GB/s link instead of 50.
+void copies_are_exact(uint32_t mask, const char* name, bool early = false, uint64_t nap_ns = 0) {
   Setup s;
   s.cfg = default_config();
+  s.cfg.nap_ns = nap_ns;
+  s.cfg.overdue_gbs = nap_ns ? 1 : 0;
   s.mask = mask;
   Harness h(s);
   FakeStream st;
   for (int dir = 0; dir < 2; ++dir) {
-    for (uint64_t n : {1ull, 777ull, 64ull * 1024, 300ull * 1024 + 5, 3ull * 1024 * 1024 + 123}) {
+    for (uint64_t n : {1ull, 777ull, 64ull * 1024, 300ull * 1024 + 5, 3ull * 1024 * 1024 + 123,
+                       nap_ns ? 24ull * 1024 * 1024 + 9 : 0ull}) {
+      if (!n) continue;
       auto src = random_bytes(n, static_cast<uint32_t>(n + dir));
       std::vector<uint8_t> dst(n + 64, 0xA5);
       auto x = linear(dir, dst.data() + 32, src.data(), n, h.cfg());
@@ -620,8 +626,10 @@ void copies_are_exact(uint32_t mask, const char* name, bool early = false) {
     }
   }
   CHECK(h.stats().failed.load() == 0, "%s: failed transfers", name);
-  std::printf("ok   copies exact, every micro-task retired once (%s): cu tasks %llu, sdma tasks %llu\n", name,
-              (unsigned long long)h.stats().path_tasks[16].load(), (unsigned long long)sum_tasks(h.stats(), 0, 16));
+  CHECK(!nap_ns || h.stats().naps.load() > 0, "%s: the engine thread never napped", name);
+  std::printf("ok   copies exact, every micro-task retired once (%s): cu tasks %llu, sdma tasks %llu, naps %llu\n",
+              name, (unsigned long long)h.stats().path_tasks[16].load(), (unsigned long long)sum_tasks(h.stats(), 0, 16),
+              (unsigned long long)h.stats().naps.load());
 }
 
 void list_with_merging() {
@@ -659,10 +667,12 @@ void list_with_merging() {
               (unsigned long long)cmds, (unsigned long long)sdma_tasks);
 }
 
-void kv_roundtrip(uint32_t mask, const char* name, bool early = false) {
+void kv_roundtrip(uint32_t mask, const char* name, bool early = false, uint64_t nap_ns = 0) {
   Setup s;
   s.cfg = default_config();
   s.cfg.chunk = 8 * 1024;  // 4 pieces per micro-task
+  s.cfg.nap_ns = nap_ns;
+  s.cfg.overdue_gbs = nap_ns ? 1 : 0;
   s.mask = mask;
   Harness h(s);
   FakeStream st;
@@ -1475,6 +1485,9 @@ void duplex_paths() {
   s.cmd_ns = 2000;
   s.duplex[MMA_H2D] = 0x3;
   s.duplex[MMA_D2H] = 0xC;
+  // A long hold: a loaded host (or a sanitizer build) may leave the
+  // host-to-device engine thread unscheduled for more than the default 1 ms.
+  s.cfg.duplex_hold_ns = 300000000;
   Harness h(s);
   FakeStream a, b;
   const uint64_t n = 160ull * 1024 * 1024 + 3;
@@ -1523,7 +1536,7 @@ void duplex_paths() {
   const auto t0 = d2h_tasks();
   a.synchronize();
   CHECK(h.sync(), "sync");
-  sleep_ns(3000000);  // past the hold time
+  sleep_ns(350000000);  // past the hold time
   h.submit(list(1), total, b);
   b.synchronize();
   CHECK(h.sync(), "sync");
@@ -1582,6 +1595,9 @@ int main(int argc, char** argv) {
     copies_are_exact(MMA_PATH_CU | 0x3, "CU + 2 engines, idle-stream early start", true);
     copies_are_exact(0x3, "2 engines, idle-stream early start", true);
     kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging, idle-stream early start", true);
+    copies_are_exact(MMA_PATH_CU | 0x3, "CU + 2 engines, engine naps", false, 50000);
+    copies_are_exact(0x3, "2 engines, engine naps", false, 50000);
+    kv_roundtrip(MMA_PATH_CU | 0x3, "CU + 2 engines, staging, engine naps", false, 50000);
     unlaunched_transfer_drains();
     whole_transfers_on_cu();
     whole_kv_transfers();

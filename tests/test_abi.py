@@ -43,6 +43,7 @@ def test_status_strings_and_defaults():
     assert c.chunk_bytes == 2 << 20 and c.queue_depth == 2 and c.cu_sub_bytes == 64 << 10
     assert c.small_bytes == 64 << 10 and c.cu_workgroups > 0 and c.watchdog_ms > 0
     assert c.control == mma.MMA_CONTROL_HOST  # the engine thread drives transfers unless asked otherwise
+    assert c.engine_nap_us == 50  # and naps between rounds while every path has work queued
 
 
 def test_calls_before_init_fail_cleanly():

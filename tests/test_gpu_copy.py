@@ -102,6 +102,47 @@ def test_copy_64mib(paths, direction):
     log(f"  path bytes: cu={stats['path_bytes'][16]} sdma={stats['path_bytes'][:4]}")
 
 
+@pytest.mark.parametrize("nap", ["default", "off"])
+def test_engine_naps(nap):
+    """The engine thread naps between rounds while every path has work queued (Section 5.3, CPU
+    overhead; engine_nap_us), or polls throughout (MMA_ENGINE_NAP_OFF). 1 GiB copies in both
+    directions, three each, are the oracle's bytes either way; the statistics count the naps."""
+    log(f"engine naps: {nap}")
+    n = 1 << 30
+    src_np = np.ascontiguousarray(W.uniform_bytes(1, W.TAG_DATA, 7, n))
+    over = {} if nap == "default" else {"engine_nap_us": mma.MMA_ENGINE_NAP_OFF}
+    with session("both", **over) as cfg:
+        assert cfg.engine_nap_us == (50 if nap == "default" else mma.MMA_ENGINE_NAP_OFF)
+        h = mma.PinnedBuffer(n)
+        d = device_bytes(n)
+        for direction in (mma.MMA_H2D, mma.MMA_D2H):
+            for rep in range(3):
+                if direction == mma.MMA_H2D:
+                    h.array[:] = src_np
+                    d.fill_(W.WEIGHT_POISON)
+                    mma.mma_memcpy_async(d, h, n, direction)
+                    torch.cuda.synchronize()
+                    got = to_host(d)
+                else:
+                    d.copy_(torch.from_numpy(src_np))
+                    h.array[:] = W.WEIGHT_POISON
+                    torch.cuda.synchronize()
+                    mma.mma_memcpy_async(h, d, n, direction)
+                    torch.cuda.synchronize()
+                    got = h.array.copy()
+                assert np.array_equal(got, ocopy.memcpy(np.full(n, W.WEIGHT_POISON, np.uint8), 0, src_np, 0, n)), \
+                    (direction, rep)
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+        h.free()
+    assert stats["failed_transfers"] == 0
+    log(f"  naps {stats['engine_naps']}, engine CPU {stats['engine_cpu_ns'] / 1e6:.1f} ms")
+    if nap == "default":
+        assert stats["engine_naps"] > 0
+    else:
+        assert stats["engine_naps"] == 0
+
+
 @pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
 def test_whole_transfers_on_cu_path(direction):
     """Default configuration around the size limit of transfers taken whole by the CU path
