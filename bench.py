@@ -37,6 +37,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+_ENGINE_NAP_US = None  # --engine-nap-us
+
+
+def _default_config():
+    """The library's default configuration, with --engine-nap-us applied."""
+    import paper_2512_16056_amd as mma
+    c = mma.mma_config_default()
+    if _ENGINE_NAP_US is not None:
+        c.engine_nap_us = _ENGINE_NAP_US
+    return c
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=int(os.environ.get("WORLD_SIZE", "1")))
@@ -60,6 +72,9 @@ def parse():
                    help="comma-separated transfer sizes in bytes for --sweep idle (default: 32 KiB to 8 GiB)")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
+    p.add_argument("--engine-nap-us", type=int, default=None,
+                   help="engine_nap_us of every configuration the run uses (default: the library's; "
+                        "4294967295 = MMA_ENGINE_NAP_OFF, the engine threads poll without sleeping)")
     return p.parse_args()
 
 
@@ -577,7 +592,7 @@ def control_modes(mma, W, np, torch, nat, s, pool, layers, lay, hs, gb, src_bloc
     mma.mma_finalize()
     try:
         for mode, code in (("host", mma.MMA_CONTROL_HOST), ("device", mma.MMA_CONTROL_DEVICE)):
-            c = mma.mma_config_default()
+            c = _default_config()
             c.control = code
             mma.mma_init(0, c)
             r = {"copy_64mib": leg(lambda: _ok(mma.lib.mma_memcpy_async(*margs)), 20, 3, n64),
@@ -640,7 +655,7 @@ def mixed_contention(mma, W, np, torch, s, nat, pool, layers, lay, src_blocks, p
     res = {}
     cfg = mma.mma_get_config()
     mma.mma_finalize()
-    c = mma.mma_config_default()
+    c = _default_config()
     c.chunk_bytes = 256 << 10
     mma.mma_init(0, c)
     try:
@@ -878,7 +893,7 @@ def sweep_control():
 
     rows = {}
     for mode, name in ((mma.MMA_CONTROL_HOST, "host"), (mma.MMA_CONTROL_DEVICE, "device")):
-        cfg = mma.mma_config_default()
+        cfg = _default_config()
         cfg.control = mode
         mma.mma_init(0, cfg)
         h = mma.PinnedBuffer(top)
@@ -906,7 +921,7 @@ def sweep_control():
         _emit(sweep="control", bytes=n, dir=dname, **r)
 
     for pct in (40, 50, 60, 70, 80, 100):
-        cfg = mma.mma_config_default()
+        cfg = _default_config()
         cfg.control = mma.MMA_CONTROL_DEVICE
         cfg.static_cu_percent = pct
         mma.mma_init(0, cfg)
@@ -937,7 +952,7 @@ def sweep_chunks():
     mma.mma_finalize()
     for chunk in (256 << 10, 512 << 10, 1 << 20, 2 << 20, 4 << 20, 8 << 20, 16 << 20):
         for depth in (1, 2, 4):
-            c = mma.mma_config_default()
+            c = _default_config()
             c.chunk_bytes, c.queue_depth = chunk, depth
             mma.mma_init(0, c)
             r = {}
@@ -997,7 +1012,7 @@ def sweep_contention():
                 ("static_cu100", dict(path_mask_h2d=CU))]
     for kind in ("none", "gemm", "hbm", "native_h2d"):
         for policy, kv in policies:
-            c = mma.mma_config_default()
+            c = _default_config()
             for k, v in kv.items():
                 setattr(c, k, v)
             mma.mma_init(0, c)
@@ -1114,7 +1129,7 @@ def sweep_duplex():
                      ("engine 0 h2d, engine 1 d2h, no cu", dict(path_mask_h2d=1, path_mask_d2h=2)),
                      ("engine 0 + cu h2d, engine 1 + cu d2h", dict(path_mask_h2d=CU | 1, path_mask_d2h=CU | 2)),
                      ("engine 0 h2d, engine 1 + cu d2h", dict(path_mask_h2d=1, path_mask_d2h=CU | 2))):
-        c = mma.mma_config_default()
+        c = _default_config()
         for k, v in kv.items():
             setattr(c, k, v)
         mma.mma_init(0, c)
@@ -1168,7 +1183,7 @@ def sweep_mixed(sizes=None, rounds=6):
              ("duplex h2d engines 0-1 + cu, d2h engines 2-5", dict(duplex_paths_h2d=CU | 0x3)),
              ("duplex h2d engines 0-1, d2h engines 2-3", dict(duplex_paths_d2h=0xC)),
              ("native", None)]
-    c = mma.mma_config_default()
+    c = _default_config()
     c.chunk_bytes = 256 << 10
     mma.mma_init(0, c)
     r, streams, tried = side_by_side_schedules(mma, torch, nat, s, W, pool, layers, lay, src_blocks, plan, arena,
@@ -1177,7 +1192,7 @@ def sweep_mixed(sizes=None, rounds=6):
     _emit(sweep="mixed", streams_side_by_side=r["concurrent"], stream_pairs_tried=tried)
     for rnd in range(rounds):
         for name, kv in cases[rnd % len(cases):] + cases[:rnd % len(cases)]:
-            c = mma.mma_config_default()
+            c = _default_config()
             c.chunk_bytes = 256 << 10
             for k, v in (kv or {}).items():
                 setattr(c, k, v)
@@ -1299,7 +1314,7 @@ def sweep_paths():
     CU = mma.MMA_PATH_CU
     for name, mask in (("sdma0", 0x1), ("sdma1", 0x2), ("sdma0+1", 0x3), ("cu", CU), ("cu+sdma0", CU | 0x1),
                        ("cu+sdma0+1", CU | 0x3), ("cu+all16", CU | 0xFFFF)):
-        c = mma.mma_config_default()
+        c = _default_config()
         c.path_mask_h2d = c.path_mask_d2h = mask
         mma.mma_init(0, c)
         used = mma.mma_get_stats()
@@ -1386,9 +1401,38 @@ def sweep_footprint():
     g = a.elapsed_time(b)
     _emit(sweep="footprint", case="stream held by the command processor (event wait, no wave)", gemm_ms=round(g, 2),
           gemm_slowdown=round(g / alone - 1, 4))
+    # hipStreamWaitValue64 on signal memory (the documented form), released by a host store once the
+    # matmuls are done: does the runtime hold the stream without a wave?
+    vp, u64 = ctypes.c_void_p, ctypes.c_uint64
+    hip.hipExtMallocWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_size_t, ctypes.c_uint]
+    hip.hipStreamWaitValue64.argtypes = [vp, vp, u64, ctypes.c_uint, u64]
+    hip.hipStreamWriteValue64.argtypes = [vp, vp, u64, ctypes.c_uint]
+    hip.hipStreamQuery.argtypes = [vp]
+    hip.hipFree.argtypes = [vp]
+    sig = vp()
+    if hip.hipExtMallocWithFlags(ctypes.byref(sig), 8, 2) == 0:  # hipMallocSignalMemory
+        val = ctypes.cast(sig, ctypes.POINTER(u64))
+        torch.cuda.synchronize()
+        val[0] = 0
+        rc = hip.hipStreamWaitValue64(vp(st.cuda_stream), sig, 5, 0, (1 << 64) - 1)  # hipStreamWaitValueGte
+        held = hip.hipStreamQuery(vp(st.cuda_stream)) != 0
+        a, b = gemms()
+        b.synchronize()
+        g = a.elapsed_time(b)
+        val[0] = 5
+        t0 = time.perf_counter()
+        while hip.hipStreamQuery(vp(st.cuda_stream)) != 0 and time.perf_counter() - t0 < 2.0:
+            pass
+        if hip.hipStreamQuery(vp(st.cuda_stream)) != 0:  # the store was not seen: the documented release
+            hip.hipStreamWriteValue64(vp(s3.cuda_stream), sig, 6, 0)
+        torch.cuda.synchronize()
+        _emit(sweep="footprint", case="stream held by hipStreamWaitValue64 (signal memory)", wait_rc=rc,
+              held=held, gemm_ms=round(g, 2), gemm_slowdown=round(g / alone - 1, 4),
+              release_us=round((time.perf_counter() - t0) * 1e6, 1))
+        hip.hipFree(sig)
     for name, mask in (("copy engines only (dummy task = 1 waiting wave)", 0x3),
                        ("default paths (16 CU-path workgroups)", 0)):
-        c = mma.mma_config_default()
+        c = _default_config()
         c.path_mask_h2d = mask
         mma.mma_init(0, c)
         mma.mma_memcpy_async(d, h, n, mma.MMA_H2D, st)
@@ -1470,7 +1514,11 @@ SWEEPS = {"sizes": sweep_sizes, "idle": sweep_idle, "chunks": sweep_chunks, "con
 
 
 def main():
+    global _ENGINE_NAP_US
     args = parse()
+    if args.engine_nap_us is not None:  # configurations built here, and mma_init without one
+        _ENGINE_NAP_US = args.engine_nap_us
+        os.environ["MMA_ENGINE_NAP_US"] = str(args.engine_nap_us)
     if args.control:
         os.environ["MMA_CONTROL"] = "1" if args.control == "device" else "0"
     if args.calib:
@@ -1602,6 +1650,7 @@ def main():
             "paths_h2d": hex(cfg["path_mask_h2d"]),
             "cu_workgroups": cfg["cu_workgroups"],
             "control": "device" if cfg["control"] == mma.MMA_CONTROL_DEVICE else "host",
+            "engine_nap_us": "off" if cfg["engine_nap_us"] == mma.MMA_ENGINE_NAP_OFF else cfg["engine_nap_us"],
             "parallelism": "1 GPU (SDMA engines + CU zero-copy on its own PCIe link)",
         },
         "kv_fetch_latency_ms": round(avg_kernel_ms, 3),
@@ -1612,6 +1661,7 @@ def main():
         "path_bytes": {"cu": stats["path_bytes"][16],
                        **{f"sdma{e}": stats["path_bytes"][e] for e in range(16) if stats["path_bytes"][e]}},
         "engine_cpu_ms_per_step": round(stats["engine_cpu_ns"] / 1e6 / max(1, args.steps + args.warmup), 3),
+        "engine_naps_per_step": round(stats["engine_naps"] / max(1, args.steps + args.warmup)),
         # SDMA share of the fetch: host slot -> HBM staging (copy engine), then the CU scatter
         # staging -> paged blocks reads and writes each byte once more in HBM.
         "staging_scatter": {
