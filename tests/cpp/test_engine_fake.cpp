@@ -608,7 +608,7 @@ void copies_are_exact(uint32_t mask, const char* name, bool early = false, uint6
   FakeStream st;
   for (int dir = 0; dir < 2; ++dir) {
     for (uint64_t n : {1ull, 777ull, 64ull * 1024, 300ull * 1024 + 5, 3ull * 1024 * 1024 + 123,
-                       nap_ns ? 24ull * 1024 * 1024 + 9 : 0ull}) {
+                       nap_ns ? 8ull * 1024 * 1024 + 9 : 0ull}) {
       if (!n) continue;
       auto src = random_bytes(n, static_cast<uint32_t>(n + dir));
       std::vector<uint8_t> dst(n + 64, 0xA5);
