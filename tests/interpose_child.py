@@ -7,7 +7,8 @@ its own. Each result is compared with oracle.copy and read back over a route tha
 with the runtime (pageable host memory). Per call, the library's statistics tell whether
 the copy went through it (and which paths carried it). With the argument "faults", the
 failure handling is checked with host-forced faults instead, and with "defaults" which copies go
-through the library when MMA_INTERPOSE_SYNC is not set. Prints one JSON line.
+through the library when neither MMA_INTERPOSE_SYNC nor MMA_INTERPOSE_IDLE is set. Prints one JSON
+line.
 """
 import ctypes
 import json
@@ -143,20 +144,62 @@ def faults(mma):
 
 
 def defaults(mma):
-    """The interposer's defaults: an asynchronous pinned copy goes through the library, a blocking one
-    stays with the runtime (MMA_INTERPOSE_SYNC unset); both exact."""
+    """The interposer's defaults (MMA_INTERPOSE_SYNC and MMA_INTERPOSE_IDLE unset): an asynchronous
+    pinned copy queued behind other work goes through the library, one on a stream with nothing
+    pending and the blocking ones stay with the runtime; all exact. Then an asynchronous copy that
+    fails in the library (host-forced: the engine thread ignores it, the watchdog releases the
+    stream) is reported by the next call, a copy on an idle stream that copies nothing, and the
+    one after that goes to the runtime again."""
     out = {}
     n = (40 << 20) + 3
     stream = torch.cuda.current_stream().cuda_stream
     src_np = seeded(n, 202)
     src = torch.from_numpy(src_np).pin_memory()
-    for route in ("hipMemcpyAsync", "hipMemcpy", "hipMemcpyWithStream"):
+
+    def busy():  # about 50 ms of other work queued on the stream before the copy
+        torch.cuda._sleep(int(2.4e9 * 0.05))
+
+    for name, route, pre in (("hipMemcpyAsync/busy", "hipMemcpyAsync", busy),
+                             ("hipMemcpyAsync/idle", "hipMemcpyAsync", None),
+                             ("hipMemcpy", "hipMemcpy", None), ("hipMemcpyWithStream", "hipMemcpyWithStream", None)):
         dst = torch.full((n,), POISON, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
         before = stats(mma)
+        if pre:
+            pre()
         rc = call(route, dst, src, n, H2D, stream)
         torch.cuda.synchronize()
         mma.mma_synchronize()
-        out[route] = {"rc": rc, "exact": bool(np.array_equal(dst.cpu().numpy(), src_np)), **delta(before, stats(mma))}
+        out[name] = {"rc": rc, "exact": bool(np.array_equal(dst.cpu().numpy(), src_np)), **delta(before, stats(mma))}
+
+    rep = {}
+    want = ocopy.memcpy(np.full(n, POISON, np.uint8), 0, src_np, 0, n)
+    mma.mma_test_set_fault(mma.MMA_FAULT_ENGINE_IGNORE, 1)
+    dst = torch.full((n,), POISON, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    before = stats(mma)
+    print("defaults: hipMemcpyAsync behind other work while the engine ignores transfers", file=sys.stderr,
+          flush=True)
+    busy()
+    rep["failed_rc"] = _rt.hipMemcpyAsync(dst.data_ptr(), src.data_ptr(), n, H2D, stream)
+    torch.cuda.synchronize()  # released by the watchdog
+    mma.mma_test_set_fault(mma.MMA_FAULT_ENGINE_IGNORE, 0)
+    mma.lib.mma_synchronize(20000)  # retire it: the failure is now sticky
+    rep["failed"] = delta(before, stats(mma))
+    small = (1 << 20) + 7
+    dst3 = torch.full((small,), POISON, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    print("defaults: the next interposed call, on an idle stream, reports the failure", file=sys.stderr, flush=True)
+    rep["next_rc"] = _rt.hipMemcpyAsync(dst3.data_ptr(), src.data_ptr(), small, H2D, stream)
+    torch.cuda.synchronize()
+    rep["next_untouched"] = bool(np.all(dst3.cpu().numpy() == POISON))
+    before = stats(mma)
+    rep["after_rc"] = _rt.hipMemcpyAsync(dst3.data_ptr(), src.data_ptr(), small, H2D, stream)
+    torch.cuda.synchronize()
+    mma.mma_synchronize()
+    rep["after_exact"] = bool(np.array_equal(dst3.cpu().numpy(), want[:small]))
+    rep["after"] = delta(before, stats(mma))
+    out["idle_report"] = rep
     return out
 
 

@@ -7,7 +7,10 @@ own, compared with the oracle. Pinned copies at or above the threshold go throug
 multipath library (one transfer each, copy engines included above the whole-launch
 limit under host control); copies below it stay with the runtime. Under host-forced
 faults, a failed blocking copy still delivers its bytes and says so on stderr, and a
-failed asynchronous copy is reported by the next interposed call.
+failed asynchronous copy is reported by the next interposed call. These tests send every
+eligible copy through the library (MMA_INTERPOSE_SYNC=1, MMA_INTERPOSE_IDLE=1); the last
+one checks the defaults: blocking copies, and asynchronous ones on a stream with nothing
+pending, stay with the runtime, whose copy is the faster there.
 """
 import json
 import os
@@ -27,13 +30,16 @@ LIB = os.path.join(ROOT, "paper_2512_16056_amd", "libmma_interpose.so")
 THRESHOLD = 32 * 1024
 
 
-def run_child(control: str, *args, sync: bool = True):
+def run_child(control: str, *args, sync: bool = True, idle: bool = True):
     assert os.path.exists(LIB), "build with python paper_2512_16056_amd/build.py"
     env = dict(os.environ)
     env["MMA_CONTROL"] = control  # the interposer initialises the library from the environment
     env.pop("MMA_INTERPOSE_SYNC", None)
     if sync:  # blocking copies through the library too (off by default)
         env["MMA_INTERPOSE_SYNC"] = "1"
+    env.pop("MMA_INTERPOSE_IDLE", None)
+    if idle:  # asynchronous copies on an idle stream through the library too (off by default)
+        env["MMA_INTERPOSE_IDLE"] = "1"
     # keep whatever is preloaded already; add the interposer after it
     env["LD_PRELOAD"] = (env.get("LD_PRELOAD", "") + " " + LIB).strip()
     env["MMA_WATCHDOG_MS"] = "2000"
@@ -80,9 +86,19 @@ def test_interposed_failures():
 
 
 def test_interposer_defaults():
-    """Without MMA_INTERPOSE_SYNC, blocking copies stay with the runtime (on one GPU a blocking caller
-    does not wait less through the library); asynchronous ones go through it."""
-    res, _ = run_child("0", "defaults", sync=False)
-    assert all(r["rc"] == 0 and r["exact"] for r in res.values()), res
-    assert res["hipMemcpyAsync"]["transfers"] == 1, res
+    """Without MMA_INTERPOSE_SYNC and MMA_INTERPOSE_IDLE: blocking copies stay with the runtime (on
+    one GPU a blocking caller does not wait less through the library), and so do asynchronous ones
+    on a stream with nothing pending (the runtime's copy engine starts sooner than a kernel); an
+    asynchronous copy queued behind other work goes through the library. An earlier asynchronous
+    failure is reported by the next call even when that call's copy would stay with the runtime."""
+    res, err = run_child("0", "defaults", sync=False, idle=False)
+    copies = {k: v for k, v in res.items() if k != "idle_report"}
+    assert all(r["rc"] == 0 and r["exact"] for r in copies.values()), res
+    assert res["hipMemcpyAsync/busy"]["transfers"] == 1, res
+    assert res["hipMemcpyAsync/idle"]["transfers"] == 0, res
     assert res["hipMemcpy"]["transfers"] == 0 and res["hipMemcpyWithStream"]["transfers"] == 0, res
+    rep = res["idle_report"]
+    assert rep["failed_rc"] == 0 and rep["failed"]["failed"] == 1, res  # the busy-stream copy failed (watchdog)
+    assert rep["next_rc"] == 999 and rep["next_untouched"], res  # reported by the idle-stream call
+    assert "an earlier copy through libmma failed" in err
+    assert rep["after_rc"] == 0 and rep["after_exact"] and rep["after"]["transfers"] == 0, res
