@@ -11,7 +11,8 @@ other direction's commands on a shared engine count as neither foreign work nor 
 its duplex paths only (CU-only micro-tasks excepted), that a slower engine pulls fewer
 micro-tasks, and that
 pull-based selection comes within 5% of the best fixed split (the paper's static-split
-comparison, Section 5.1.2).
+comparison, Section 5.1.2), with the engine thread polling and with it napping between rounds;
+and that naps between rounds keep copies and KV transfers exact.
 Under device control (no engine thread in the loop) it checks exact copies on idle streams
 (copy engines and CU path) and busy ones (CU path only), KV fetch and offload, records
 recycled by later submissions, refused commands re-routed, a transfer larger than a ring
