@@ -1736,10 +1736,11 @@ class Engine {
       for (int id : path.slots) {
         const SdmaSlot& sl = slots_[id];
         if (sl.state == kH2DScatterPush || sl.state == kD2HGatherPush) return 0;
-        if (engine_op(sl) && n < 64)
-          q[n++] = &sl;
-        else if (sl.state != kFree)
+        if (engine_op(sl)) {
+          if (n < 64) q[n++] = &sl;  // a path has at most queue_depth (<= 16) slots
+        } else if (sl.state != kFree) {
           staging = true;
+        }
       }
       if (!n) {
         if (staging) return 0;
