@@ -1,9 +1,9 @@
 """Child process of test_gpu_interpose.py, run with libmma_interpose.so in LD_PRELOAD.
 
 An unmodified torch program's copies, and direct calls of the interposed HIP functions
-(hipMemcpyAsync, hipMemcpy, hipMemcpyWithStream, resolved from the process's global
-scope, where the preloaded library comes first), move seeded bytes in each direction on
-its own. Each result is compared with oracle.copy and read back over a route that stays
+(hipMemcpyAsync, with an explicit kind and with hipMemcpyDefault, hipMemcpy and
+hipMemcpyWithStream, resolved from the process's global scope, where the preloaded library
+comes first), move seeded bytes in each direction on its own. Each result is compared with oracle.copy and read back over a route that stays
 with the runtime (pageable host memory). Per call, the library's statistics tell whether
 the copy went through it (and which paths carried it). With the argument "faults", the
 failure handling is checked with host-forced faults instead, and with "defaults" which copies go
@@ -21,7 +21,7 @@ import torch
 sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 from oracle import copy as ocopy  # noqa: E402
 
-H2D, D2H = 1, 2  # hipMemcpyKind
+H2D, D2H, DEFAULT = 1, 2, 4  # hipMemcpyKind (hipMemcpyDefault: the runtime infers the direction)
 HIP_ERROR_UNKNOWN = 999
 POISON = 0xA5
 SIZES = [(3 << 20) + 5, (40 << 20) + 3, 4096]  # whole CU launch, multipath engine, below the threshold
@@ -62,6 +62,10 @@ def call(route, dst, src, n, kind, stream):
     d, s = dst.data_ptr(), src.data_ptr()
     if route == "hipMemcpy":
         return _rt.hipMemcpy(d, s, n, kind)
+    if route == "hipMemcpyAsync/default":  # direction from the pointers' attributes
+        rc = _rt.hipMemcpyAsync(d, s, n, DEFAULT, stream)
+        torch.cuda.current_stream().synchronize()
+        return rc
     if route == "hipMemcpyWithStream":
         return _rt.hipMemcpyWithStream(d, s, n, kind, stream)
     rc = _rt.hipMemcpyAsync(d, s, n, kind, stream)
@@ -73,7 +77,8 @@ def routes(mma):
     out = {}
     stream = torch.cuda.current_stream().cuda_stream
     seed = 0
-    for route in ("torch_async", "torch_sync", "hipMemcpyAsync", "hipMemcpy", "hipMemcpyWithStream"):
+    for route in ("torch_async", "torch_sync", "hipMemcpyAsync", "hipMemcpyAsync/default", "hipMemcpy",
+                  "hipMemcpyWithStream"):
         for n in SIZES:
             for kind in (H2D, D2H):
                 seed += 1
