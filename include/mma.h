@@ -129,8 +129,9 @@ typedef struct mma_config {
                                  kernel alone tracks completion; no host thread works on the
                                  transfer afterwards (records are recycled by later calls). On a
                                  stream with work pending, and for KV transfers, the CU path
-                                 carries the transfer alone. A transfer of more than 4096
-                                 micro-tasks still goes to the engine thread. */
+                                 carries the transfer alone. A copy or tensor list of more than
+                                 4096 micro-tasks is planned again at twice chunk_bytes until it
+                                 fits; a KV transfer of more goes to the engine thread. */
   uint32_t duplex_paths_h2d; /* paths host->device pulls from while a device->host transfer is
                                moving (Section 5.1.2, concurrent flows; host control only).
                                0 (default): the SDMA engines of path_mask_h2d, without the CU

@@ -92,6 +92,10 @@ constexpr uint64_t kWholeMaxSub = 512 * KiB;
 // 1 GiB copies, 40% to 70% land within 0.2% of each other; 40% was best in
 // both directions.
 constexpr uint32_t kDeviceCuPercent = 40;
+// Device control: a copy or tensor list with more micro-tasks than a ring is
+// planned again at twice the chunk size, up to this chunk (a CU entry's byte
+// count is 32 bits).
+constexpr uint64_t kDeviceMaxChunk = 1ull << 30;
 
 // ------------------------------------------------------------------ transfer
 enum class Kind : uint8_t { kLinear, kKvFetch, kKvOffload };

@@ -791,6 +791,17 @@ mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t d
   if (!total) return MMA_OK;
   if (!ranges_disjoint(dsts)) return fail(MMA_ERR_INVALID_ARG, "destination ranges overlap");
   std::unique_ptr<Transfer> x = make_list_transfer(dir, list, n, sizes.data(), src_cu.data(), dst_cu.data(), rt->cfg);
+  // Device control plans a transfer into one ring of kRingSize micro-tasks. A
+  // copy or list with more is planned again at twice the chunk size until it
+  // fits, rather than handed to the engine thread (the model wake-up list has
+  // 7,723 micro-tasks at 2 MiB, 3,890 at 4 MiB).
+  if (rt->cfg.device) {
+    Config c = rt->cfg;
+    while (x->tasks.size() > kRingSize && c.chunk < kDeviceMaxChunk) {
+      c.chunk *= 2;
+      x = make_list_transfer(dir, list, n, sizes.data(), src_cu.data(), dst_cu.data(), c);
+    }
+  }
   x->t_api = t_api;
   return submit(std::move(x), total, stream, nullptr);
 }

@@ -11,8 +11,9 @@ byte against oracle.copy / oracle.kv on seeded inputs:
   - paged-KV fetch and offload in both GPU block layouts (CU path only);
   - stream ordering: a dependent kernel on the stream sees every byte of the copy, including
     the copy engines' share;
-  - more transfers than there are records, the blocking mma_memcpy, and a transfer with more
-    micro-tasks than a ring holds (handed to the engine thread).
+  - more transfers than there are records, the blocking mma_memcpy, a tensor list with more
+    micro-tasks than a ring holds (planned again at a larger chunk, still under device control),
+    and a KV transfer with more (handed to the engine thread).
 """
 import numpy as np
 import pytest
@@ -285,6 +286,42 @@ def test_device_many_transfers_and_sync_copy():
         back.array[:] = 0
         mma.mma_memcpy(back.ptr, dmid.data_ptr() + 7, m, mma.MMA_D2H)
         assert np.array_equal(back.array, src_np[7:7 + m])
+
+
+@pytest.mark.parametrize("idle", [True, False])
+def test_device_list_beyond_ring_replanned(idle):
+    """A tensor list with more micro-tasks than a ring holds (10 x 481 at 64 KiB chunks) is planned
+    again at twice the chunk size and stays under device control: byte-exact, copy engines
+    included on an idle stream, and the engine thread never takes it."""
+    sizes = [(30 << 20) + 1 + 4096 * k for k in range(10)]
+    stream = torch.cuda.Stream()
+    offs, off = [], 0
+    for z in sizes:
+        offs.append(off)
+        off += (z + 255) // 256 * 256
+    src_np = np.ascontiguousarray(W.uniform_bytes(23, 0, int(idle), off))
+    with session("both", chunk_bytes=64 << 10, **DEVICE):
+        src = mma.PinnedBuffer(off)
+        src.array[:] = src_np
+        dsts = [device_bytes(z, W.WEIGHT_POISON) for z in sizes]
+        torch.cuda.synchronize()
+        busy0 = mma.mma_get_stats()["engine_wall_busy_ns"]
+        if not idle:
+            _busy(stream)
+        mma.mma_weights_load([(d, src.ptr + o, z) for d, o, z in zip(dsts, offs, sizes)], mma.MMA_H2D, stream)
+        stream.synchronize()
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+        for d, o, z in zip(dsts, offs, sizes):
+            assert np.array_equal(to_host(d)[:z], ocopy.memcpy(np.full(z, W.WEIGHT_POISON, np.uint8), 0,
+                                                                src_np[o:o + z], 0, z)), z
+    assert stats["failed_transfers"] == 0
+    assert sum(stats["path_bytes"]) == sum(sizes)
+    assert stats["engine_wall_busy_ns"] == busy0, "the engine thread took the transfer"
+    if idle:
+        assert sum(stats["path_bytes"][:16]) > 0, "the copy engines took no share on an idle stream"
+    else:
+        assert sum(stats["path_bytes"][:16]) == 0
 
 
 def test_device_beyond_ring_goes_to_engine_thread():
