@@ -223,6 +223,7 @@ struct SdmaPath {
 struct Config {
   uint64_t chunk, fallback, small, sub;
   uint32_t depth, cu_depth, backoff, cu_wgs, watchdog_ms;
+  uint32_t cu_backoff;  // the CU path's back-off depth (0: cu_depth, no extra back-off); `backoff` is the engines'
   uint32_t mask[2];
   uint32_t static_split, static_cu_percent;
   uint32_t merge;       // max micro-tasks per copy-engine command
@@ -1217,7 +1218,7 @@ class Engine {
     bool p = false;
     while (true) {
       if (x->cu_busy >= depth) x->cu_full = true;
-      if (x->cu_full && x->cu_busy < std::min(cfg_.backoff, depth)) x->cu_full = false;
+      if (x->cu_full && x->cu_busy < std::min(cfg_.cu_backoff ? cfg_.cu_backoff : depth, depth)) x->cu_full = false;
       if (x->cu_full) break;
       size_t i = x->cur_cu;
       while (i < x->tasks.size() && (x->claimed[i] || (x->tasks[i].flags & kPlanSdmaOnly) ||

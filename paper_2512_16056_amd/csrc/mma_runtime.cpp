@@ -580,6 +580,9 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   }
   c.duplex_paths_h2d = duplex[0];
   c.duplex_paths_d2h = duplex[1];
+  // Back-off depth: given, it applies to every path; by default each path
+  // pulls again as soon as it is below its own queue depth.
+  const uint32_t backoff_given = c.backoff_depth;
   if (!c.backoff_depth) c.backoff_depth = c.queue_depth;
   rt->ucfg = c;
   Config& k = rt->cfg;
@@ -590,6 +593,7 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   k.depth = c.queue_depth;
   k.cu_depth = c.cu_queue_depth;
   k.backoff = c.backoff_depth;
+  k.cu_backoff = backoff_given;
   k.cu_wgs = c.cu_workgroups;
   k.watchdog_ms = c.watchdog_ms;
   k.mask[0] = mask[0];
