@@ -1711,9 +1711,10 @@ class Engine {
   //  - each copy engine with commands of ours in flight: half the time until
   //    the last of them could end at the fastest rate the engine may run --
   //    1.5 times its measured rate, at most R -- counted from when the first
-  //    reached the head of the queue, and kLateNapNs once that time has
-  //    passed; so the thread looks often when they land and when the engine
-  //    needs its next command;
+  //    reached the head of the queue, and kLateNapNs once that time is near
+  //    or past; so the thread looks often when they land and when the engine
+  //    needs its next command. An engine idle while a staging step of its own
+  //    runs (its next command waits for the CU side): kLateNapNs;
   //  - a transfer waiting for its start signal: a 256th of its bytes at R
   //    (the copy engines join at most that late; the CU path starts with the
   //    kernel, from its prefilled entries);
@@ -1722,10 +1723,12 @@ class Engine {
   //    finishes it, and stop once copy-engine commands hold all that is left;
   //  - its CU path, while micro-tasks remain that the CU path may take: half
   //    the time its outstanding ring entries beyond one per wave (which may
-  //    be nearly done) take at R -- none if there are no more than that.
+  //    be nearly done) take at R; with no more entries than that, kLateNapNs
+  //    if the CU path is full (it takes nothing until a micro-task lands),
+  //    else none.
   // Nor does the thread nap with a transfer submitted but not yet taken in, a
-  // transfer completed or failed but not retired, a staging step waiting for
-  // ring room, or a copy engine idle while a staging step of its own runs.
+  // transfer completed or failed but not retired, or a staging step waiting
+  // for ring room.
   uint64_t nap() const {
     if (!cfg_.nap_ns || n_incoming_.load(std::memory_order_relaxed)) return 0;
     const uint64_t gbs = cfg_.overdue_gbs ? cfg_.overdue_gbs : 50;  // 1 GB/s = 1 byte per ns
@@ -1748,7 +1751,7 @@ class Engine {
         }
       }
       if (!n) {
-        if (staging) return 0;
+        if (staging) ns = std::min(ns, kLateNapNs);  // idle until a staging step of its own lands
         continue;
       }
       std::sort(q, q + n, [](const SdmaSlot* a, const SdmaSlot* b) { return a->t_submit < b->t_submit; });
@@ -1764,8 +1767,9 @@ class Engine {
         else
           it->second += b;
       }
-      ns = std::min(ns, end > static_cast<double>(now) ? static_cast<uint64_t>((end - static_cast<double>(now)) / 2)
-                                                        : kLateNapNs);
+      ns = std::min(ns, end > static_cast<double>(now + 2 * kLateNapNs)
+                            ? static_cast<uint64_t>((end - static_cast<double>(now)) / 2)
+                            : kLateNapNs);
     }
     for (const auto& up : active_) {
       const Transfer* x = up.get();
@@ -1781,7 +1785,12 @@ class Engine {
       ns = std::min(ns, (x->bytes - std::min(x->bytes, x->done_bytes + eng)) / gbs / 64);
       const bool cu_takes = (cu_enabled() && !cu_paused_) || x->pool_dev || x->cu_only_left > 0;
       if (cu_takes && x->n_claimed < x->tasks.size()) {
-        if (x->cu_entries <= x->waves) return 0;
+        if (x->cu_entries <= x->waves) {
+          // Full, the CU path takes nothing more until one of its micro-tasks lands.
+          if (x->cu_busy < (x->pool_dev ? 2 * x->waves : cfg_.cu_depth)) return 0;
+          ns = std::min(ns, kLateNapNs);
+          continue;
+        }
         const uint64_t per_entry = x->kind == Kind::kLinear ? x->sub
                                    : (x->kv_per ? x->kv_per : std::max<uint64_t>(1, cfg_.sub / x->piece)) * x->piece;
         ns = std::min(ns, (x->cu_entries - x->waves) * per_entry / gbs / 2);
