@@ -85,7 +85,8 @@ typedef struct mma_config {
   uint32_t cu_queue_depth;  /* outstanding micro-tasks on the CU path; default 4 */
   uint32_t backoff_depth;   /* once a path's queue is full it pulls again only when its depth
                                drops below this (Section 3.4 contention back-off);
-                               default = its queue depth (no extra back-off) */
+                               default: each path's own queue depth (no extra back-off);
+                               a value given applies to every path */
   uint32_t path_mask_h2d;   /* paths used host->device; default: CU path + the host-facing
                                SDMA engines reported by ROCr */
   uint32_t path_mask_d2h;   /* paths used device->host; same default */
@@ -252,7 +253,7 @@ mma_status_t mma_config_default(mma_config_t* out);
  * MMA_CU_QUEUE_DEPTH, MMA_BACKOFF_DEPTH, MMA_PATHS_H2D, MMA_PATHS_D2H,
  * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS, MMA_SDMA_MERGE_TASKS,
  * MMA_CU_WHOLE_BYTES, MMA_CU_WHOLE_BYTES_D2H, MMA_CONTROL, MMA_STATIC_CU_PERCENT,
- * MMA_DUPLEX_PATHS_H2D, MMA_DUPLEX_PATHS_D2H, MMA_TRACE).
+ * MMA_DUPLEX_PATHS_H2D, MMA_DUPLEX_PATHS_D2H, MMA_ENGINE_NAP_US, MMA_TRACE).
  * Errors: MMA_ERR_ALREADY_INITIALIZED, MMA_ERR_INVALID_ARG (bad device or
  * config), MMA_ERR_HIP / MMA_ERR_HSA. */
 mma_status_t mma_init(int hip_device, const mma_config_t* cfg);
