@@ -419,9 +419,11 @@ mma_status_t submit(std::unique_ptr<Transfer> x, uint64_t payload_bytes, void* s
   if (!x->self_contained && x->sdma_ok && e->has_sdma() && x->n_claimed < x->tasks.size() && stream_idle(hs)) {
     x->early = true;
     // If the launch fails, the copy engines may already hold part of the
-    // transfer: the call returns only after they have drained.
-    std::shared_ptr<Waiter> w = std::make_shared<Waiter>();
-    x->waiter = w;
+    // transfer: the call returns only after they have drained. A blocking
+    // caller's waiter (mma_memcpy_stream) serves for that wait too, so that
+    // the caller is still told when the transfer retires.
+    if (!x->waiter) x->waiter = std::make_shared<Waiter>();
+    std::shared_ptr<Waiter> w = x->waiter;
     Transfer* raw = x.get();  // the engine retires it only after the kernel (or `unlaunched`) releases it
     e->submit(std::move(x));
     const hipError_t err = launch_transfer(a, grid, hs);

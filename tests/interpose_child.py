@@ -2,7 +2,7 @@
 
 An unmodified torch program's copies, and direct calls of the interposed HIP functions
 (hipMemcpyAsync, with an explicit kind and with hipMemcpyDefault, hipMemcpy and
-hipMemcpyWithStream, resolved from the process's global scope, where the preloaded library
+hipMemcpyWithStream, the latter also on a stream of its own with nothing pending, resolved from the process's global scope, where the preloaded library
 comes first), move seeded bytes in each direction on its own. Each result is compared with oracle.copy and read back over a route that stays
 with the runtime (pageable host memory). Per call, the library's statistics tell whether
 the copy went through it (and which paths carried it). With the argument "faults", the
@@ -50,6 +50,15 @@ def delta(a, b):
     return {k: b[k] - a[k] for k in a}
 
 
+_SIDE = []
+
+
+def _side_stream():
+    if not _SIDE:
+        _SIDE.append(torch.cuda.Stream())
+    return _SIDE[0]
+
+
 def call(route, dst, src, n, kind, stream):
     """One interposed copy; returns the HIP status."""
     if route == "torch_sync":  # copy_ with non_blocking=False: hipMemcpyWithStream in torch on ROCm
@@ -68,6 +77,9 @@ def call(route, dst, src, n, kind, stream):
         return rc
     if route == "hipMemcpyWithStream":
         return _rt.hipMemcpyWithStream(d, s, n, kind, stream)
+    if route == "hipMemcpyWithStream/idle":  # a stream of its own with nothing pending: early start
+        torch.cuda.synchronize()
+        return _rt.hipMemcpyWithStream(d, s, n, kind, _side_stream().cuda_stream)
     rc = _rt.hipMemcpyAsync(d, s, n, kind, stream)
     torch.cuda.current_stream().synchronize()
     return rc
@@ -78,7 +90,7 @@ def routes(mma):
     stream = torch.cuda.current_stream().cuda_stream
     seed = 0
     for route in ("torch_async", "torch_sync", "hipMemcpyAsync", "hipMemcpyAsync/default", "hipMemcpy",
-                  "hipMemcpyWithStream"):
+                  "hipMemcpyWithStream", "hipMemcpyWithStream/idle"):
         for n in SIZES:
             for kind in (H2D, D2H):
                 seed += 1

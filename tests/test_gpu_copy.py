@@ -410,6 +410,51 @@ def test_sync_memcpy(direction):
         mma.mma_synchronize()
 
 
+@pytest.mark.parametrize("control", [mma.MMA_CONTROL_HOST, mma.MMA_CONTROL_DEVICE])
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+def test_sync_memcpy_stream_idle(direction, control):
+    """mma_memcpy_stream on a stream with nothing pending. Above the whole-launch limit the copy
+    engines are handed the copy before the kernel is launched (the idle-stream early start); the
+    blocking call must still be told when it retires, and return MMA_COPY_RETIRED at once rather
+    than fail at its time limit. A whole launch, a one-byte and a zero-byte copy on the same
+    stream too; every byte against the oracle, read without further synchronisation."""
+    sizes = [(40 << 20) + 3, (3 << 20) + 5, 1, 0]
+    top = max(sizes)
+    src_np = np.ascontiguousarray(W.uniform_bytes(41, direction, 0, top))
+    st = torch.cuda.Stream()
+    with session("both", cu_whole_bytes=0, cu_whole_bytes_d2h=0, control=control):
+        if direction == mma.MMA_H2D:
+            src = mma.PinnedBuffer(top)
+            src.array[:] = src_np
+        else:
+            src = from_host(src_np)
+        for n in sizes:
+            for rep in range(2):
+                log(f"sync stream idle control={control} dir={direction} n={n} rep={rep}")
+                if direction == mma.MMA_H2D:
+                    dst = device_bytes(top, W.WEIGHT_POISON)
+                    dptr, sptr = dst.data_ptr(), src.ptr
+                else:
+                    dst = mma.PinnedBuffer(top)
+                    dst.array[:] = W.WEIGHT_POISON
+                    dptr, sptr = dst.ptr, src.data_ptr()
+                torch.cuda.synchronize()  # the stream and the legacy default stream have nothing pending
+                t0 = time.perf_counter()
+                outcome = mma.mma_memcpy_stream(dptr, sptr, n, direction, st)
+                dt = time.perf_counter() - t0
+                got = to_host(dst) if direction == mma.MMA_H2D else dst.array.copy()
+                if direction == mma.MMA_D2H:
+                    dst.free()
+                assert outcome == mma.MMA_COPY_RETIRED, (n, outcome)
+                assert dt < 2.0, (n, dt)
+                want = ocopy.memcpy(np.full(top, W.WEIGHT_POISON, np.uint8), 0, src_np, 0, n)
+                assert np.array_equal(got, want), n
+        mma.mma_synchronize()
+        assert mma.mma_get_stats()["failed_transfers"] == 0
+        if direction == mma.MMA_H2D:
+            src.free()
+
+
 MISALIGNED = [(1, 0), (0, 1), (5, 9), (15, 2)]  # (source, destination) offsets modulo 16
 
 

@@ -3,7 +3,8 @@ program run with libmma_interpose.so in LD_PRELOAD.
 
 Every interposed route -- torch's asynchronous and blocking copies, and direct calls of
 hipMemcpyAsync (with an explicit kind, and with hipMemcpyDefault, where the interposer reads the
-direction from the pointers), hipMemcpy and hipMemcpyWithStream -- moves bytes in each direction
+direction from the pointers), hipMemcpy and hipMemcpyWithStream (also on an idle stream of its
+own, where the copy engines start before the kernel launch) -- moves bytes in each direction
 on its own, compared with the oracle. Pinned copies at or above the threshold go through the
 multipath library (one transfer each, copy engines included above the whole-launch
 limit under host control); copies below it stay with the runtime. Under host-forced
@@ -56,7 +57,7 @@ def run_child(control: str, *args, sync: bool = True, idle: bool = True):
 @pytest.mark.parametrize("control", ["0", "1"])
 def test_interposed_routes(control):
     res, _ = run_child(control)
-    assert len(res) == 6 * 3 * 2
+    assert len(res) == 7 * 3 * 2
     for key, r in res.items():
         route, direction, n = key.rsplit("/", 2)
         n = int(n)
