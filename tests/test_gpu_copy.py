@@ -410,27 +410,37 @@ def test_sync_memcpy(direction):
         mma.mma_synchronize()
 
 
+HIP_STREAM_PER_THREAD = 2  # hipStreamPerThread
+
+
+@pytest.mark.parametrize("kind", ["idle", "busy", "per_thread", "legacy"])
 @pytest.mark.parametrize("control", [mma.MMA_CONTROL_HOST, mma.MMA_CONTROL_DEVICE])
 @pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
-def test_sync_memcpy_stream_idle(direction, control):
-    """mma_memcpy_stream on a stream with nothing pending. Above the whole-launch limit the copy
-    engines are handed the copy before the kernel is launched (the idle-stream early start); the
-    blocking call must still be told when it retires, and return MMA_COPY_RETIRED at once rather
-    than fail at its time limit. A whole launch, a one-byte and a zero-byte copy on the same
-    stream too; every byte against the oracle, read without further synchronisation."""
+def test_sync_memcpy_stream(direction, control, kind):
+    """mma_memcpy_stream returns MMA_COPY_RETIRED once the data has arrived, on
+    - idle: a stream of its own with nothing pending. Above the whole-launch limit the copy engines
+      are handed the copy before the kernel is launched (the idle-stream early start); the call
+      must still be told when it retires, rather than fail at its time limit;
+    - busy: the same stream behind a spin kernel; device to host, the source is written on that
+      stream after the spin, right before the call, so the copy must be ordered after it;
+    - per_thread: hipStreamPerThread; legacy: the legacy default stream.
+    An engine-driven copy, a whole launch, a one-byte and a zero-byte copy each; every byte against
+    the oracle, read without further synchronisation."""
     sizes = [(40 << 20) + 3, (3 << 20) + 5, 1, 0]
     top = max(sizes)
     src_np = np.ascontiguousarray(W.uniform_bytes(41, direction, 0, top))
-    st = torch.cuda.Stream()
+    side = torch.cuda.Stream()
+    stream = {"idle": side, "busy": side, "per_thread": HIP_STREAM_PER_THREAD, "legacy": 0}[kind]
     with session("both", cu_whole_bytes=0, cu_whole_bytes_d2h=0, control=control):
         if direction == mma.MMA_H2D:
             src = mma.PinnedBuffer(top)
             src.array[:] = src_np
         else:
-            src = from_host(src_np)
+            fresh = from_host(src_np)
+            src = device_bytes(top, 0)
         for n in sizes:
             for rep in range(2):
-                log(f"sync stream idle control={control} dir={direction} n={n} rep={rep}")
+                log(f"sync stream kind={kind} control={control} dir={direction} n={n} rep={rep}")
                 if direction == mma.MMA_H2D:
                     dst = device_bytes(top, W.WEIGHT_POISON)
                     dptr, sptr = dst.data_ptr(), src.ptr
@@ -438,9 +448,17 @@ def test_sync_memcpy_stream_idle(direction, control):
                     dst = mma.PinnedBuffer(top)
                     dst.array[:] = W.WEIGHT_POISON
                     dptr, sptr = dst.ptr, src.data_ptr()
-                torch.cuda.synchronize()  # the stream and the legacy default stream have nothing pending
+                    src.zero_()
+                    if kind != "busy":
+                        src.copy_(fresh)
+                torch.cuda.synchronize()  # every stream has nothing pending
+                if kind == "busy":
+                    with torch.cuda.stream(side):
+                        torch.cuda._sleep(1_000_000)
+                        if direction == mma.MMA_D2H:
+                            src.copy_(fresh)  # the producer, on the copy's stream
                 t0 = time.perf_counter()
-                outcome = mma.mma_memcpy_stream(dptr, sptr, n, direction, st)
+                outcome = mma.mma_memcpy_stream(dptr, sptr, n, direction, stream)
                 dt = time.perf_counter() - t0
                 got = to_host(dst) if direction == mma.MMA_H2D else dst.array.copy()
                 if direction == mma.MMA_D2H:
@@ -449,6 +467,7 @@ def test_sync_memcpy_stream_idle(direction, control):
                 assert dt < 2.0, (n, dt)
                 want = ocopy.memcpy(np.full(top, W.WEIGHT_POISON, np.uint8), 0, src_np, 0, n)
                 assert np.array_equal(got, want), n
+        torch.cuda.synchronize()
         mma.mma_synchronize()
         assert mma.mma_get_stats()["failed_transfers"] == 0
         if direction == mma.MMA_H2D:
