@@ -271,10 +271,14 @@ def _ragged_list(seed, count, max_size):
     return sizes
 
 
+@pytest.mark.parametrize("stream", ["legacy", "idle"])
 @pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
 @pytest.mark.parametrize("paths", list(PATHS))
-def test_tensor_list_ragged(paths, direction):
-    log(f"tensor list paths={paths} dir={direction}")
+def test_tensor_list_ragged(paths, direction, stream):
+    """A ragged list of 40 tensors up to 3 MiB, on the legacy default stream and on a stream of its
+    own with nothing pending (where the copy engines may start before the kernel launch)."""
+    log(f"tensor list paths={paths} dir={direction} stream={stream}")
+    st = torch.cuda.Stream() if stream == "idle" else None
     sizes = _ragged_list(7 + direction, 40, 3 * 1024 * 1024)
     src_offs, total = W.arena_offsets(sizes, 16)
     # destinations interleaved with untouched 4 KiB gaps, some misaligned by 16 B
@@ -290,16 +294,18 @@ def test_tensor_list_ragged(paths, direction):
             src = mma.PinnedBuffer(total)
             src.array[:] = src_np
             dst = from_host(poison)
+            torch.cuda.synchronize()
             mma.mma_weights_load([(dst.data_ptr() + d, src.ptr + s, n) for d, s, n in zip(dst_offs, src_offs, sizes)],
-                                 direction)
+                                 direction, st)
             torch.cuda.synchronize()
             got = to_host(dst)
         else:
             src = from_host(src_np)
             dst = mma.PinnedBuffer(dtotal)
             dst.array[:] = poison
+            torch.cuda.synchronize()
             mma.mma_weights_load([(dst.ptr + d, src.data_ptr() + s, n) for d, s, n in zip(dst_offs, src_offs, sizes)],
-                                 direction)
+                                 direction, st)
             torch.cuda.synchronize()
             got = dst.array.copy()
         mma.mma_synchronize()

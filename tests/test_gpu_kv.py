@@ -68,18 +68,27 @@ SHAPES = {
 }
 
 
+def _stream_of(kind):
+    """None: the legacy default stream; else a stream of its own, on which nothing is pending once
+    the caller has synchronised (the copy engines may then start before the kernel launch)."""
+    return torch.cuda.Stream() if kind == "idle" else None
+
+
+@pytest.mark.parametrize("stream", ["legacy", "idle"])
 @pytest.mark.parametrize("chunk", [4096, 65536])
 @pytest.mark.parametrize("shape", list(SHAPES))
 @pytest.mark.parametrize("paths", list(PATHS))
-def test_kv_fetch_small(paths, shape, chunk):
+def test_kv_fetch_small(paths, shape, chunk, stream):
     s = SHAPES[shape]
-    log(f"kv fetch paths={paths} shape={shape} chunk={chunk}")
+    log(f"kv fetch paths={paths} shape={shape} chunk={chunk} stream={stream}")
     hs, gb = W.kv_fetch_tables(s, cfg=3)
+    st = _stream_of(stream)
     with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
         pool = _pool(s, 1)
         layers = _layers(s, W.GPU_POISON)
         before = _layer_views(s, layers)
-        mma.mma_kv_fetch(layout_of(s), pool, layers, hs, gb)
+        torch.cuda.synchronize()
+        mma.mma_kv_fetch(layout_of(s), pool, layers, hs, gb, st)
         torch.cuda.synchronize()
         mma.mma_synchronize()
         stats = mma.mma_get_stats()
@@ -88,19 +97,22 @@ def test_kv_fetch_small(paths, shape, chunk):
     assert sum(stats["path_bytes"]) == s.n_blocks * s.slot_bytes
 
 
+@pytest.mark.parametrize("stream", ["legacy", "idle"])
 @pytest.mark.parametrize("chunk", [4096, 65536])
 @pytest.mark.parametrize("shape", list(SHAPES))
 @pytest.mark.parametrize("paths", list(PATHS))
-def test_kv_offload_small(paths, shape, chunk):
+def test_kv_offload_small(paths, shape, chunk, stream):
     s = SHAPES[shape]
-    log(f"kv offload paths={paths} shape={shape} chunk={chunk}")
+    log(f"kv offload paths={paths} shape={shape} chunk={chunk} stream={stream}")
     plan = W.kv_offload_plan(s, cfg=4)
+    st = _stream_of(stream)
     with session(paths, chunk_bytes=chunk, cu_sub_bytes=1024):
         pool = _pool(s, 2)
         before = pool.array.copy()
         layers = _layers(s, seed=100)
         views = _layer_views(s, layers)
-        mma.mma_kv_offload(layout_of(s), pool, layers, plan.src_blocks, plan.dest)
+        torch.cuda.synchronize()
+        mma.mma_kv_offload(layout_of(s), pool, layers, plan.src_blocks, plan.dest, st)
         torch.cuda.synchronize()
         mma.mma_synchronize()
         want = okv.kv_offload(before.reshape(s.host_num_slots, -1), views, plan.src_blocks, plan.dest)
