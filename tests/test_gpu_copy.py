@@ -115,6 +115,7 @@ def test_engine_naps(nap):
         assert cfg.engine_nap_us == (50 if nap == "default" else mma.MMA_ENGINE_NAP_OFF)
         h = mma.PinnedBuffer(n)
         d = device_bytes(n)
+        dsrc = from_host(src_np)
         for direction in (mma.MMA_H2D, mma.MMA_D2H):
             for rep in range(3):
                 if direction == mma.MMA_H2D:
@@ -124,7 +125,7 @@ def test_engine_naps(nap):
                     torch.cuda.synchronize()
                     got = to_host(d)
                 else:
-                    d.copy_(torch.from_numpy(src_np))
+                    d.copy_(dsrc)
                     h.array[:] = W.WEIGHT_POISON
                     torch.cuda.synchronize()
                     mma.mma_memcpy_async(h, d, n, direction)

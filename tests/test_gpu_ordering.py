@@ -156,9 +156,10 @@ def test_kv_fetch_then_dependent_kernel():
 def test_concurrent_submitters(control):
     """Four host threads, each with its own stream, submit interleaved H2D copies, D2H copies and
     tensor lists of mixed sizes (self-contained, CU+SDMA and SDMA-merged ones) at the same time;
-    each transfer is followed on its stream by the dependent digest kernel. Every destination and
-    every digest must equal the oracle's (submissions are serialised inside the library; streams
-    are independent)."""
+    each transfer is followed on its stream by the dependent digest kernel, and in the last round by
+    a blocking device->host copy (mma_memcpy_stream) whose result is read at once. Every destination
+    and every digest must equal the oracle's (submissions are serialised inside the library;
+    streams are independent; each blocking caller waits for its own copy)."""
     from concurrent.futures import ThreadPoolExecutor
     sizes = [12345, 1 << 20, (3 << 20) + 17, 9 << 20, 64 << 10]
     with session("both", chunk_bytes=1 << 20, control=control):
@@ -168,7 +169,7 @@ def test_concurrent_submitters(control):
                 return _submitter(tid, stream)
 
         def _submitter(tid, stream):
-            results = []
+            results, bad = [], []
             for rep in range(3):
                 for k, n in enumerate(sizes):
                     src_np = np.ascontiguousarray(W.uniform_bytes(40 + tid, rep, k, n))
@@ -187,8 +188,14 @@ def test_concurrent_submitters(control):
                     mma.mma_digest_u32(d, n, out, stream)
                     mma.mma_memcpy_async(back, d, n, mma.MMA_D2H, stream)
                     results.append((src_np, h, d, out, back))
+                    if rep == 2:  # a blocking copy behind that work, read at once
+                        back2 = mma.PinnedBuffer(n)
+                        back2.array[:] = W.WEIGHT_POISON
+                        outcome = mma.mma_memcpy_stream(back2, d, n, mma.MMA_D2H, stream)
+                        if outcome != mma.MMA_COPY_RETIRED or not np.array_equal(back2.array, src_np):
+                            bad.append(("blocking", tid, k, outcome))
+                        back2.free()
             stream.synchronize()
-            bad = []
             for i, (src_np, h, d, out, back) in enumerate(results):
                 if not np.array_equal(back.array, src_np):
                     bad.append(("d2h", i))
