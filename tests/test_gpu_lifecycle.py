@@ -1,4 +1,5 @@
-"""Process lifecycle: a program that copies through the library and exits without mma_finalize
+"""Process lifecycle: mma_finalize with transfers still in flight waits for them; a program that
+copies through the library and exits without mma_finalize
 must exit cleanly (the engine threads are stopped when the library is unloaded, before the HIP
 runtime's own teardown), with the data exact."""
 import os
@@ -40,3 +41,41 @@ def test_exit_without_finalize_is_clean():
     print(r.stdout[-1000:], r.stderr[-2000:])
     assert "copied" in r.stdout
     assert r.returncode == 0
+
+
+@pytest.mark.parametrize("control", [0, 1])
+def test_finalize_waits_for_transfers_in_flight(control):
+    """mma_finalize right after enqueuing, with nothing synchronised: a 256 MiB host->device copy
+    queued behind a spin kernel on a stream of its own (the engine thread drives it under host
+    control) and a 3 MiB whole launch. finalize waits until both have retired and returns MMA_OK;
+    the bytes are exact, and the library initialises again."""
+    import numpy as np
+
+    import paper_2512_16056_amd as mma
+    from gpu_helpers import log
+    from oracle import copy as ocopy
+    import workloads as W
+
+    n, m = 256 << 20, (3 << 20) + 5
+    src_np = np.ascontiguousarray(W.uniform_bytes(51, control, 0, n))
+    log(f"finalize with transfers in flight, control={control}")
+    mma.mma_init(0, control=control, watchdog_ms=5000)
+    try:
+        src = mma.PinnedBuffer(n)
+        src.array[:] = src_np
+        dst = torch.full((n,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
+        dst2 = torch.full((m,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
+        st = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(st):
+            torch.cuda._sleep(2_000_000)
+        mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D, st)
+        mma.mma_memcpy_async(dst2, src.ptr + 7, m, mma.MMA_H2D, st)
+    finally:
+        mma.mma_finalize()
+    torch.cuda.synchronize()
+    assert np.array_equal(dst.cpu().numpy(), ocopy.memcpy(np.full(n, W.WEIGHT_POISON, np.uint8), 0, src_np, 0, n))
+    assert np.array_equal(dst2.cpu().numpy(), ocopy.memcpy(np.full(m, W.WEIGHT_POISON, np.uint8), 0, src_np, 7, m))
+    src.free()
+    mma.mma_init(0)
+    mma.mma_finalize()
