@@ -426,6 +426,16 @@ mma_status_t mma_plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, ui
 mma_status_t mma_plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t piece_bytes, uint64_t chunk,
                          mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out);
 
+/* Byte sizes a KV layout implies (the layout described at mma_kv_layout_t): one
+ * piece, one host slot (2 * num_layers pieces), the host pool (host_num_slots
+ * slots) and one GPU layer tensor (2 * gpu_num_blocks pieces), i.e. what a caller
+ * allocates. Any output pointer may be NULL. MMA_ERR_INVALID_ARG, and nothing
+ * written, if a field is 0, num_layers > MMA_MAX_LAYERS, the piece is above
+ * 4 GiB or a size does not fit 64 bits; the KV calls apply the same check. The
+ * GPU block layout's own conditions are checked by the KV calls alone. */
+mma_status_t mma_kv_layout_sizes(const mma_kv_layout_t* layout, uint64_t* piece_bytes, uint64_t* slot_bytes,
+                                 uint64_t* pool_bytes, uint64_t* layer_bytes);
+
 /* Block-table check applied by mma_kv_fetch/offload: equal lengths implied,
  * src[i] in [0, src_count), dst[i] in [0, dst_count), dst entries distinct.
  * MMA_OK or MMA_ERR_INVALID_ARG. */

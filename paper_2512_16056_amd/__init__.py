@@ -162,6 +162,8 @@ _SIGNATURES = {
                        ctypes.POINTER(_U64)], _S),
     "mma_plan_kv": ([_U64, _U32, _U64, _U64, ctypes.POINTER(mma_plan_entry_t), _U64, ctypes.POINTER(_U64)], _S),
     "mma_validate_kv_tables": ([ctypes.POINTER(_I32), _U32, ctypes.POINTER(_I32), _U32, _U64], _S),
+    "mma_kv_layout_sizes": ([ctypes.POINTER(mma_kv_layout_t), ctypes.POINTER(_U64), ctypes.POINTER(_U64),
+                             ctypes.POINTER(_U64), ctypes.POINTER(_U64)], _S),
     "mma_trace_enable": ([_I32], _S),
     "mma_trace_read": ([ctypes.POINTER(mma_trace_rec_t), _U64, ctypes.POINTER(_U64)], _S),
     "mma_test_set_fault": ([_I32, _U64], _S),
@@ -422,3 +424,11 @@ def mma_validate_kv_tables(src, src_count: int, dst, dst_count: int) -> bool:
     st = lib.mma_validate_kv_tables(s.ctypes.data_as(ctypes.POINTER(_I32)), src_count,
                                     d.ctypes.data_as(ctypes.POINTER(_I32)), dst_count, s.size)
     return st == MMA_OK
+
+
+def mma_kv_layout_sizes(layout: mma_kv_layout_t) -> dict:
+    """Bytes of one piece, one host slot, the host pool and one GPU layer tensor; MMAError if the
+    layout is invalid or a size does not fit 64 bits."""
+    out = [_U64() for _ in range(4)]
+    _check(lib.mma_kv_layout_sizes(ctypes.byref(layout), *[ctypes.byref(v) for v in out]), "mma_kv_layout_sizes")
+    return dict(zip(("piece", "slot", "pool", "layer"), (v.value for v in out)))

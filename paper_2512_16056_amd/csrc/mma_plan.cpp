@@ -49,6 +49,24 @@ bool ranges_disjoint(std::vector<std::pair<uint64_t, uint64_t>> r) {
   return true;
 }
 
+bool kv_sizes(uint32_t num_layers, uint32_t block_tokens, uint32_t kv_heads, uint32_t head_dim, uint32_t elem_bytes,
+              uint32_t gpu_num_blocks, uint32_t host_num_slots, uint32_t max_layers, KvSizes* out) {
+  if (!num_layers || num_layers > max_layers || !block_tokens || !kv_heads || !head_dim || !elem_bytes ||
+      !gpu_num_blocks || !host_num_slots)
+    return false;
+  uint64_t piece = block_tokens, slot = 0, pool = 0, layer = 0;
+  if (__builtin_mul_overflow(piece, static_cast<uint64_t>(kv_heads), &piece) ||
+      __builtin_mul_overflow(piece, static_cast<uint64_t>(head_dim), &piece) ||
+      __builtin_mul_overflow(piece, static_cast<uint64_t>(elem_bytes), &piece) || piece > (1ull << 32))
+    return false;
+  slot = piece * 2 * num_layers;  // at most 2^32 * 2 * max_layers
+  if (__builtin_mul_overflow(slot, static_cast<uint64_t>(host_num_slots), &pool) ||
+      __builtin_mul_overflow(2 * piece, static_cast<uint64_t>(gpu_num_blocks), &layer))
+    return false;
+  *out = {piece, slot, pool, layer};
+  return true;
+}
+
 }  // namespace mma
 
 extern "C" {
@@ -74,6 +92,20 @@ mma_status_t mma_plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t 
   if (!out) return cap == 0 ? MMA_OK : MMA_ERR_INVALID_ARG;
   if (cap < v.size()) return MMA_ERR_BUFFER_TOO_SMALL;
   for (size_t i = 0; i < v.size(); ++i) out[i] = {v[i].item, v[i].offset, v[i].bytes, v[i].flags, 0u};
+  return MMA_OK;
+}
+
+mma_status_t mma_kv_layout_sizes(const mma_kv_layout_t* layout, uint64_t* piece_bytes, uint64_t* slot_bytes,
+                                 uint64_t* pool_bytes, uint64_t* layer_bytes) {
+  mma::KvSizes z;
+  if (!layout || !mma::kv_sizes(layout->num_layers, layout->block_tokens, layout->kv_heads, layout->head_dim,
+                                layout->elem_bytes, layout->gpu_num_blocks, layout->host_num_slots,
+                                MMA_MAX_LAYERS, &z))
+    return MMA_ERR_INVALID_ARG;
+  if (piece_bytes) *piece_bytes = z.piece;
+  if (slot_bytes) *slot_bytes = z.slot;
+  if (pool_bytes) *pool_bytes = z.pool;
+  if (layer_bytes) *layer_bytes = z.layer;
   return MMA_OK;
 }
 

@@ -40,6 +40,17 @@ bool tables_valid(const int32_t* src, uint32_t src_count, const int32_t* dst, ui
 // Half-open [begin, end) ranges pairwise disjoint (empty ranges ignored).
 bool ranges_disjoint(std::vector<std::pair<uint64_t, uint64_t>> ranges);
 
+// Byte sizes that a paged-KV layout implies (one piece, one host slot, the host
+// pool, one GPU layer tensor). False if a field is 0, there are more than
+// max_layers layers, a piece exceeds 4 GiB, or a size does not fit 64 bits:
+// every size is a product of caller-given fields, and a wrapped product would
+// let range checks pass for a smaller footprint than the kernels address.
+struct KvSizes {
+  uint64_t piece, slot, pool, layer;
+};
+bool kv_sizes(uint32_t num_layers, uint32_t block_tokens, uint32_t kv_heads, uint32_t head_dim, uint32_t elem_bytes,
+              uint32_t gpu_num_blocks, uint32_t host_num_slots, uint32_t max_layers, KvSizes* out);
+
 }  // namespace mma
 
 #endif  // MMA_PLAN_H_

@@ -834,11 +834,12 @@ static mma_status_t kv_check(const mma_kv_layout_t* lay, const void* host_pool, 
   mma_status_t s;
   if (!lay || !host_pool || !layers || !host_slots || !gpu_blocks)
     return fail(MMA_ERR_INVALID_ARG, "NULL argument");
-  if (!lay->num_layers || lay->num_layers > kMaxLayers || !lay->block_tokens || !lay->kv_heads || !lay->head_dim ||
-      !lay->elem_bytes || !lay->gpu_num_blocks || !lay->host_num_slots)
-    return fail(MMA_ERR_INVALID_ARG, "invalid KV layout");
-  const uint64_t piece = static_cast<uint64_t>(lay->block_tokens) * lay->kv_heads * lay->head_dim * lay->elem_bytes;
-  if (piece > (1ull << 32)) return fail(MMA_ERR_INVALID_ARG, "KV piece too large");
+  KvSizes sz;
+  if (!kv_sizes(lay->num_layers, lay->block_tokens, lay->kv_heads, lay->head_dim, lay->elem_bytes,
+                lay->gpu_num_blocks, lay->host_num_slots, kMaxLayers, &sz))
+    return fail(MMA_ERR_INVALID_ARG, "invalid KV layout: a field is 0, more than %u layers, a piece above 4 GiB, "
+                                     "or a pool or layer size beyond 64 bits", kMaxLayers);
+  const uint64_t piece = sz.piece;
   KvGeom& kv = out->kv;
   kv.layout = lay->gpu_layout;
   if (lay->gpu_layout == MMA_KV_LAYOUT_XPACKED) {
@@ -876,9 +877,7 @@ static mma_status_t kv_check(const mma_kv_layout_t* lay, const void* host_pool, 
     return fail(MMA_ERR_INVALID_ARG, "unknown GPU KV layout %u", lay->gpu_layout);
   }
   const uint32_t ppb = 2 * lay->num_layers;
-  const uint64_t slot_bytes = piece * ppb;
-  const uint64_t pool_bytes = slot_bytes * lay->host_num_slots;
-  const uint64_t layer_bytes = 2 * piece * lay->gpu_num_blocks;
+  const uint64_t slot_bytes = sz.slot, pool_bytes = sz.pool, layer_bytes = sz.layer;
   bool ok = dir == MMA_H2D ? tables(host_slots, lay->host_num_slots, gpu_blocks, lay->gpu_num_blocks, n)
                            : tables(gpu_blocks, lay->gpu_num_blocks, host_slots, lay->host_num_slots, n);
   if (!ok) return fail(MMA_ERR_INVALID_ARG, "block table entry out of range or duplicate destination");

@@ -107,6 +107,46 @@ def test_validate_tables_matches_oracle():
         assert mma.mma_validate_kv_tables([0, 1, 2, 3], 4, perm, 4)
 
 
+def test_kv_layout_sizes():
+    """The sizes a KV layout implies, and the rejection of layouts whose sizes wrap 64 bits (the KV
+    calls apply the same check before any range check)."""
+    def sizes(*f):
+        return mma.mma_kv_layout_sizes(mma.kv_layout(*f))
+
+    # the 64k-token workload: 16 tokens x 8 heads x 128 x bf16 pieces, 32 layers, 4096 slots, 4352 GPU blocks
+    assert sizes(32, 16, 8, 128, 2, 4352, 4096) == {"piece": 32768, "slot": 2 << 20, "pool": 8 << 30,
+                                                    "layer": 285212672}
+    for s in (W.small_kv_shape(), W.KVShape(layers=3, block_tokens=1, kv_heads=1, head_dim=5, elem_bytes=2,
+                                            gpu_num_blocks=50, host_num_slots=40, n_blocks=37)):
+        got = sizes(s.layers, s.block_tokens, s.kv_heads, s.head_dim, s.elem_bytes, s.gpu_num_blocks,
+                    s.host_num_slots)
+        assert got == {"piece": s.piece_bytes, "slot": s.slot_bytes, "pool": s.slot_bytes * s.host_num_slots,
+                       "layer": s.layer_bytes}
+    # a 4 GiB piece is the largest accepted
+    assert sizes(1, 1 << 16, 1 << 16, 1, 1, 1, 1) == {"piece": 1 << 32, "slot": 1 << 33, "pool": 1 << 33,
+                                                       "layer": 1 << 33}
+    # 256 layers of 4 GiB pieces: a 2 TiB slot; 2^23 - 1 slots fit 64 bits, 2^23 wrap to 0
+    assert sizes(256, 1 << 16, 1 << 16, 1, 1, 1, (1 << 23) - 1)["pool"] == (1 << 64) - (1 << 41)
+    # a layer of 2^31 - 1 blocks of two 4 GiB pieces fits, 2^31 blocks wrap to 0
+    assert sizes(1, 1 << 16, 1 << 16, 1, 1, (1 << 31) - 1, 1)["layer"] == (1 << 64) - (1 << 33)
+    assert sizes(256, 1, 1, 1, 1, 1, 1)["slot"] == 512
+    bad = [(256, 1 << 16, 1 << 16, 1, 1, 1, 1 << 23),       # pool size wraps to 0
+           (1, 1 << 16, 1 << 16, 1, 1, 1 << 31, 1),          # layer size wraps to 0
+           (1, 1 << 16, 1 << 16, 1 << 16, 1 << 16, 1, 1),    # piece wraps to 0
+           (1, 1 << 16, (1 << 16) + 1, 1, 1, 1, 1),          # piece above 4 GiB
+           (1, 0xFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF, 16, 1, 1),  # piece product beyond 64 bits
+           (257, 1, 1, 1, 1, 1, 1)]                          # more layers than a call takes
+    bad += [tuple(0 if k == z else 1 for k in range(7)) for z in range(7)]  # each field 0 in turn
+    for f in bad:
+        with pytest.raises(mma.MMAError) as e:
+            sizes(*f)
+        assert e.value.name == "MMA_ERR_INVALID_ARG", f
+    out = (mma._U64 * 1)(7)
+    assert mma.lib.mma_kv_layout_sizes(None, out, None, None, None) == mma.MMA_ERR_INVALID_ARG and out[0] == 7
+    assert mma.lib.mma_kv_layout_sizes(mma.kv_layout(*bad[0]), out, None, None, None) == mma.MMA_ERR_INVALID_ARG
+    assert out[0] == 7  # nothing written on rejection
+
+
 def test_struct_layouts_match_header(tmp_path):
     """Every ctypes mirror has the size and field offsets that a C compiler gives the header's struct."""
     import ctypes

@@ -273,6 +273,13 @@ def test_kv_rejects_bad_tables():
             assert e.value.name == "MMA_ERR_INVALID_ARG"
         with pytest.raises(mma.MMAError):  # duplicate destination slot on offload
             mma.mma_kv_offload(lay, pool, layers, [0, 1], [2, 2])
+        # layouts whose pool or layer size wraps 64 bits (to 0, which every range check would pass):
+        # rejected before anything else, with tables that are in range
+        for f in [(256, 1 << 16, 1 << 16, 1, 1, 1, 1 << 23), (1, 1 << 16, 1 << 16, 1, 1, 1 << 31, 1)]:
+            for call in (mma.mma_kv_fetch, mma.mma_kv_offload, mma.mma_kv_fetch_noalloc):
+                with pytest.raises(mma.MMAError) as e:
+                    call(mma.kv_layout(*f), pool, [layers[0]] * f[0], [0], [0])
+                assert e.value.name == "MMA_ERR_INVALID_ARG", (f, call)
         mma.mma_kv_fetch(lay, pool, layers, [], [])  # empty: no-op
         torch.cuda.synchronize()
 
