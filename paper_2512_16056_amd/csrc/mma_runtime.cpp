@@ -223,9 +223,13 @@ mma_status_t check_ready() {
 // the same buffer id. (The runtime's RANGE_SIZE attribute is not used: it is
 // truncated to 32 bits for allocations of 4 GiB and more.)
 bool within_allocation(const void* p, uint64_t bytes) {
+  // A range that wraps the address space would put its last byte below p,
+  // possibly inside the same allocation.
+  const uint64_t span = bytes ? bytes : 1;
+  if (span - 1 > UINT64_MAX - reinterpret_cast<uint64_t>(p)) return false;
   uint64_t id0 = 0, id1 = 0;
   hipDeviceptr_t first = const_cast<void*>(p);
-  hipDeviceptr_t last = static_cast<uint8_t*>(const_cast<void*>(p)) + (bytes - 1);
+  hipDeviceptr_t last = static_cast<uint8_t*>(const_cast<void*>(p)) + (span - 1);
   if (hipPointerGetAttribute(&id0, HIP_POINTER_ATTRIBUTE_BUFFER_ID, first) != hipSuccess ||
       hipPointerGetAttribute(&id1, HIP_POINTER_ATTRIBUTE_BUFFER_ID, last) != hipSuccess) {
     (void)hipGetLastError();
@@ -248,7 +252,7 @@ class RangeCache {
   bool find(uint64_t id, bool host, uint64_t p, uint64_t bytes, Entry* out) {
     std::lock_guard<std::mutex> g(mu_);
     for (const Entry& e : e_)
-      if (e.id == id && e.host == host && p >= e.base && p + bytes <= e.base + e.size) {
+      if (e.id == id && e.host == host && p >= e.base && bytes <= e.size && p - e.base <= e.size - bytes) {
         *out = e;
         return true;
       }
@@ -289,7 +293,7 @@ void remember(uint64_t id, bool host, const void* p, uint64_t bytes, int64_t dev
     return;
   }
   const uint64_t b = reinterpret_cast<uint64_t>(base), q = reinterpret_cast<uint64_t>(p);
-  if (q < b || q + bytes > b + size) return;  // inconsistent answer: do not rely on it
+  if (q < b || bytes > size || q - b > size - bytes) return;  // inconsistent answer: do not rely on it
   RangeCache::Entry e;
   e.id = id;
   e.base = b;

@@ -383,9 +383,24 @@ def test_rejects_bad_arguments():
         with pytest.raises(mma.MMAError) as e:          # overlapping destinations
             mma.mma_weights_load([(dst, src, 64), (dst.data_ptr() + 32, src, 64)], mma.MMA_H2D)
         assert e.value.name == "MMA_ERR_INVALID_ARG"
+        # sizes whose range wraps the address space (a negative length cast to unsigned, or one that
+        # ends just past 2^64), from inside allocations that earlier calls validated and cached
+        mma.mma_memcpy_async(dst, src, 4096, mma.MMA_H2D)
+        mma.mma_memcpy_async(src, dst, 4096, mma.MMA_D2H)
+        torch.cuda.synchronize()
+        h, d = src.ptr + 64, dst.data_ptr() + 64
+        for n in ((1 << 64) - 1, (1 << 64) - h + 16, (1 << 64) - d + 16):
+            for dr, a, b in ((mma.MMA_H2D, d, h), (mma.MMA_D2H, h, d)):
+                with pytest.raises(mma.MMAError) as e:
+                    mma.mma_memcpy_async(a, b, n, dr)
+                assert e.value.name in ("MMA_ERR_NOT_PINNED", "MMA_ERR_INVALID_ARG"), (n, dr)
+            with pytest.raises(mma.MMAError) as e:
+                mma.mma_digest_u32(d, n & ~3, device_bytes(8, 0))
+            assert e.value.name == "MMA_ERR_INVALID_ARG", n
         mma.mma_memcpy_async(dst, src, 0, mma.MMA_H2D)   # zero bytes: no-op
         mma.mma_weights_load([], mma.MMA_H2D)
         torch.cuda.synchronize()
+        assert mma.mma_get_stats()["failed_transfers"] == 0
         src.free()
 
 
