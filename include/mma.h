@@ -18,7 +18,8 @@
  *
  * Conventions for every call:
  *   - Returns mma_status_t: MMA_OK (0) or a negative error code. No call
- *     aborts the process; details of the last error: mma_last_error().
+ *     aborts the process or lets a C++ exception out (host memory exhaustion
+ *     is MMA_ERR_NO_MEMORY); details of the last error: mma_last_error().
  *   - Argument validation happens before anything is enqueued: a call that
  *     fails validation has no effect.
  *   - bytes == 0 / n == 0 is an MMA_OK no-op (nothing is enqueued).
@@ -60,6 +61,8 @@ typedef int32_t mma_status_t;
 #define MMA_ERR_NO_MEMORY (-8)
 #define MMA_ERR_BUFFER_TOO_SMALL (-9)
 #define MMA_ERR_TIMEOUT (-10)
+#define MMA_ERR_INTERNAL (-11) /* a C++ exception inside the library other than host memory
+                                  exhaustion (MMA_ERR_NO_MEMORY); mma_last_error() names it */
 
 /* Direction of a transfer. Only host<->device copies are handled (Section 3.2:
  * GPU-to-GPU traffic is not intercepted). */

@@ -27,6 +27,8 @@ MMA_ERR_NOT_PINNED = -3
 MMA_ERR_HIP = -4
 MMA_ERR_TRANSFER_FAILED = -6
 MMA_ERR_TIMEOUT = -10
+MMA_ERR_NO_MEMORY = -8
+MMA_ERR_INTERNAL = -11
 MMA_H2D = 0
 MMA_D2H = 1
 MMA_PATH_CU = 0x80000000
@@ -52,7 +54,7 @@ MMA_TASK_SDMA_ONLY = 2
 STATUS = {
     0: "MMA_OK", -1: "MMA_ERR_NOT_INITIALIZED", -2: "MMA_ERR_INVALID_ARG", -3: "MMA_ERR_NOT_PINNED",
     -4: "MMA_ERR_HIP", -5: "MMA_ERR_HSA", -6: "MMA_ERR_TRANSFER_FAILED", -7: "MMA_ERR_ALREADY_INITIALIZED",
-    -8: "MMA_ERR_NO_MEMORY", -9: "MMA_ERR_BUFFER_TOO_SMALL", -10: "MMA_ERR_TIMEOUT",
+    -8: "MMA_ERR_NO_MEMORY", -9: "MMA_ERR_BUFFER_TOO_SMALL", -10: "MMA_ERR_TIMEOUT", -11: "MMA_ERR_INTERNAL",
 }
 
 

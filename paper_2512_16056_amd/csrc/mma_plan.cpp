@@ -2,13 +2,27 @@
 #include "mma_plan.h"
 
 #include <algorithm>
+#include <new>
 
 #include "../../include/mma.h"
 
 namespace mma {
 
+// Room for `count` more items, or std::bad_alloc at once: a count beyond what
+// memory can hold fails here instead of after growing the vector for a while.
+static void reserve_more(std::vector<PlanItem>& out, uint64_t count) {
+  if (count > out.max_size() - out.size()) throw std::bad_alloc();
+  out.reserve(out.size() + count);
+}
+
 void plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, uint64_t fallback, uint64_t small,
                std::vector<PlanItem>& out) {
+  uint64_t count = 0;  // saturates: only compared with what a vector can hold
+  for (uint64_t t = 0; t < n; ++t) {
+    const uint64_t sz = sizes[t], c = sz == 0 ? 0 : sz < fallback ? 1 : sz / chunk + (sz % chunk != 0);
+    count = c > UINT64_MAX - count ? UINT64_MAX : count + c;
+  }
+  reserve_more(out, count);
   for (uint64_t t = 0; t < n; ++t) {
     const uint64_t sz = sizes[t];
     if (sz == 0) continue;
@@ -17,7 +31,11 @@ void plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, uint64_t fallb
       out.push_back({t, 0, sz, flags});
       continue;
     }
-    for (uint64_t o = 0; o < sz; o += chunk) out.push_back({t, o, std::min(chunk, sz - o), flags});
+    for (uint64_t o = 0; o < sz;) {  // advances by what is left at the end: o never wraps
+      const uint64_t b = std::min(chunk, sz - o);
+      out.push_back({t, o, b, flags});
+      o += b;
+    }
   }
 }
 
@@ -25,6 +43,8 @@ void plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t piece_bytes,
              std::vector<PlanItem>& out) {
   uint64_t per = piece_bytes ? chunk / piece_bytes : 1;
   if (per < 1) per = 1;
+  const uint64_t groups = pieces_per_block / per + (pieces_per_block % per != 0);
+  reserve_more(out, groups && n_blocks > UINT64_MAX / groups ? UINT64_MAX : n_blocks * groups);
   for (uint64_t i = 0; i < n_blocks; ++i)
     for (uint64_t p = 0; p < pieces_per_block; p += per)
       out.push_back({i, p, std::min<uint64_t>(per, pieces_per_block - p), 0u});
@@ -69,10 +89,13 @@ bool kv_sizes(uint32_t num_layers, uint32_t block_tokens, uint32_t kv_heads, uin
 
 }  // namespace mma
 
+// A C++ exception never leaves these calls (a C caller cannot catch it): the
+// planners and the table check allocate, and running out of host memory is
+// MMA_ERR_NO_MEMORY.
 extern "C" {
 
 mma_status_t mma_plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, uint64_t fallback, uint64_t small,
-                           mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out) {
+                           mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out) try {
   if (!n_out || chunk == 0 || (n && !sizes)) return MMA_ERR_INVALID_ARG;
   std::vector<mma::PlanItem> v;
   mma::plan_list(sizes, n, chunk, fallback, small, v);
@@ -81,10 +104,14 @@ mma_status_t mma_plan_list(const uint64_t* sizes, uint64_t n, uint64_t chunk, ui
   if (cap < v.size()) return MMA_ERR_BUFFER_TOO_SMALL;
   for (size_t i = 0; i < v.size(); ++i) out[i] = {v[i].item, v[i].offset, v[i].bytes, v[i].flags, 0u};
   return MMA_OK;
+} catch (const std::bad_alloc&) {
+  return MMA_ERR_NO_MEMORY;
+} catch (...) {
+  return MMA_ERR_INTERNAL;
 }
 
 mma_status_t mma_plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t piece_bytes, uint64_t chunk,
-                         mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out) {
+                         mma_plan_entry_t* out, uint64_t cap, uint64_t* n_out) try {
   if (!n_out || chunk == 0 || piece_bytes == 0) return MMA_ERR_INVALID_ARG;
   std::vector<mma::PlanItem> v;
   mma::plan_kv(n_blocks, pieces_per_block, piece_bytes, chunk, v);
@@ -93,6 +120,10 @@ mma_status_t mma_plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t 
   if (cap < v.size()) return MMA_ERR_BUFFER_TOO_SMALL;
   for (size_t i = 0; i < v.size(); ++i) out[i] = {v[i].item, v[i].offset, v[i].bytes, v[i].flags, 0u};
   return MMA_OK;
+} catch (const std::bad_alloc&) {
+  return MMA_ERR_NO_MEMORY;
+} catch (...) {
+  return MMA_ERR_INTERNAL;
 }
 
 mma_status_t mma_kv_layout_sizes(const mma_kv_layout_t* layout, uint64_t* piece_bytes, uint64_t* slot_bytes,
@@ -110,9 +141,13 @@ mma_status_t mma_kv_layout_sizes(const mma_kv_layout_t* layout, uint64_t* piece_
 }
 
 mma_status_t mma_validate_kv_tables(const int32_t* src, uint32_t src_count, const int32_t* dst, uint32_t dst_count,
-                                    uint64_t n) {
+                                    uint64_t n) try {
   if (n && (!src || !dst)) return MMA_ERR_INVALID_ARG;
   return mma::tables_valid(src, src_count, dst, dst_count, n) ? MMA_OK : MMA_ERR_INVALID_ARG;
+} catch (const std::bad_alloc&) {
+  return MMA_ERR_NO_MEMORY;
+} catch (...) {
+  return MMA_ERR_INTERNAL;
 }
 
 }  // extern "C"

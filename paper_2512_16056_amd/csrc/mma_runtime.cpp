@@ -10,6 +10,9 @@
 #include <pthread.h>
 #include <sched.h>
 
+#include <exception>
+#include <new>
+
 #include "mma_engine.h"
 
 namespace mma {
@@ -490,6 +493,33 @@ void fill_config(mma_config_t* c, bool use_env) {
   *c = d;
 }
 
+// No C++ exception may cross the C ABI (a C caller cannot catch it, and it
+// would end the process): the entry points that allocate on the host end in a
+// handler that turns the exception in flight into a status. Host memory
+// exhaustion is MMA_ERR_NO_MEMORY, anything else MMA_ERR_INTERNAL. A call that
+// fails this way may have taken a transfer record or light slot it does not
+// give back; a later call then waits for another.
+void note_exception(mma_status_t s, const char* api, const char* what) noexcept {
+  try {
+    fail(s, "%s: %s", api, what);
+  } catch (...) {
+  }
+}
+
+mma_status_t boundary_error(const char* api) noexcept {
+  try {
+    throw;
+  } catch (const std::bad_alloc&) {
+    note_exception(MMA_ERR_NO_MEMORY, api, "out of host memory");
+    return MMA_ERR_NO_MEMORY;
+  } catch (const std::exception& e) {
+    note_exception(MMA_ERR_INTERNAL, api, e.what());
+  } catch (...) {
+    note_exception(MMA_ERR_INTERNAL, api, "unknown C++ exception");
+  }
+  return MMA_ERR_INTERNAL;
+}
+
 }  // namespace
 }  // namespace mma
 
@@ -503,7 +533,7 @@ mma_status_t mma_config_default(mma_config_t* out) {
   return MMA_OK;
 }
 
-mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
+mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
   std::lock_guard<std::mutex> g(g_init_mu);
   if (g_rt) return fail(MMA_ERR_ALREADY_INITIALIZED, "already initialised");
   g_ranges.clear();  // device entries were checked against the previous device
@@ -666,9 +696,11 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) {
   if (env_u64("MMA_TRACE", 0)) g_trace = 1;
   g_rt = rt.release();
   return MMA_OK;
+} catch (...) {
+  return boundary_error("mma_init");
 }
 
-mma_status_t mma_finalize(void) {
+mma_status_t mma_finalize(void) try {
   std::lock_guard<std::mutex> g(g_init_mu);
   if (!g_rt) return fail(MMA_ERR_NOT_INITIALIZED, "not initialised");
   bool drained = true;
@@ -684,6 +716,8 @@ mma_status_t mma_finalize(void) {
   delete g_rt;
   g_rt = nullptr;
   return MMA_OK;
+} catch (...) {
+  return boundary_error("mma_finalize");
 }
 
 mma_status_t mma_get_config(mma_config_t* out) {
@@ -693,11 +727,13 @@ mma_status_t mma_get_config(mma_config_t* out) {
   return MMA_OK;
 }
 
-mma_status_t mma_synchronize(uint32_t timeout_ms) {
+mma_status_t mma_synchronize(uint32_t timeout_ms) try {
   if (!g_rt) return fail(MMA_ERR_NOT_INITIALIZED, "not initialised");
   for (auto& e : g_rt->eng)
     if (!e->wait_idle(timeout_ms)) return fail(MMA_ERR_TIMEOUT, "transfers still in flight");
   return g_sticky.load() ? fail(MMA_ERR_TRANSFER_FAILED, "a transfer failed") : MMA_OK;
+} catch (...) {
+  return boundary_error("mma_synchronize");
 }
 
 mma_status_t mma_host_alloc(uint64_t bytes, void** out) {
@@ -732,7 +768,7 @@ mma_status_t mma_memcpy_async(void* dst, const void* src, uint64_t bytes, int32_
 }
 
 mma_status_t mma_memcpy_stream(void* dst, const void* src, uint64_t bytes, int32_t dir, void* stream,
-                               int32_t* outcome) {
+                               int32_t* outcome) try {
   if (outcome) *outcome = MMA_COPY_NOT_ENQUEUED;
   std::shared_ptr<Waiter> w = std::make_shared<Waiter>();
   tl_waiter = w;
@@ -765,13 +801,15 @@ mma_status_t mma_memcpy_stream(void* dst, const void* src, uint64_t bytes, int32
   }
   if (outcome) *outcome = MMA_COPY_RETIRED;
   return w->failed ? fail(MMA_ERR_TRANSFER_FAILED, "the copy failed") : MMA_OK;
+} catch (...) {
+  return boundary_error("mma_memcpy_stream");
 }
 
 mma_status_t mma_memcpy(void* dst, const void* src, uint64_t bytes, int32_t dir) {
   return mma_memcpy_stream(dst, src, bytes, dir, nullptr, nullptr);
 }
 
-mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t dir, void* stream) {
+mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t dir, void* stream) try {
   const uint64_t t_api = now_ns();
   mma_status_t s = check_ready();
   if (s) return s;
@@ -814,6 +852,8 @@ mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t d
   }
   x->t_api = t_api;
   return submit(std::move(x), total, stream, nullptr);
+} catch (...) {
+  return boundary_error("mma_weights_load");
 }
 
 // A validated KV call: geometry handed to the kernels, and where the pool is.
@@ -916,7 +956,7 @@ static mma_status_t kv_check(const mma_kv_layout_t* lay, const void* host_pool, 
 
 static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool, const void* const* layers,
                               const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n, int dir,
-                              void* stream) {
+                              void* stream) try {
   const uint64_t t_api = now_ns();
   mma_status_t s = check_ready();
   if (s) return s;
@@ -935,6 +975,8 @@ static mma_status_t kv_common(const mma_kv_layout_t* lay, const void* host_pool,
   x->pool_launch = c.pool_dev && (c.kv.layout == MMA_KV_LAYOUT_PIECE || c.kv.layout == MMA_KV_LAYOUT_HND);
   x->t_api = t_api;
   return submit(std::move(x), n * c.slot_bytes, stream, &c.kv);
+} catch (...) {
+  return boundary_error("mma_kv_fetch/mma_kv_offload");
 }
 
 // Table check of the no-alloc KV fetch: the same rule as tables_valid, with
@@ -986,7 +1028,7 @@ mma_status_t mma_kv_offload(const mma_kv_layout_t* layout, void* host_pool, cons
 
 mma_status_t mma_kv_fetch_noalloc(const mma_kv_layout_t* layout, const void* host_pool, void* const* gpu_layers,
                                   const int32_t* host_slots, const int32_t* gpu_blocks, uint64_t n_blocks,
-                                  void* stream) {
+                                  void* stream) try {
   mma_status_t s = check_ready();
   if (s) return s;
   if (!n_blocks) return MMA_OK;
@@ -1045,6 +1087,8 @@ mma_status_t mma_kv_fetch_noalloc(const mma_kv_layout_t* layout, const void* hos
       static_cast<uint32_t>(std::max<uint64_t>(1, std::min<uint64_t>((claims + kWavesPerWG - 1) / kWavesPerWG, cap)));
   const hipError_t err = launch_noalloc(a, grid, hs);
   return err == hipSuccess ? MMA_OK : fail(MMA_ERR_HIP, "no-alloc KV fetch launch failed: %s", hipGetErrorString(err));
+} catch (...) {
+  return boundary_error("mma_kv_fetch_noalloc");
 }
 
 mma_status_t mma_digest_u32(const void* dev_ptr, uint64_t bytes, uint64_t* dev_out, void* stream) {
@@ -1061,7 +1105,7 @@ mma_status_t mma_digest_u32(const void* dev_ptr, uint64_t bytes, uint64_t* dev_o
   return e == hipSuccess ? MMA_OK : fail(MMA_ERR_HIP, "digest launch: %s", hipGetErrorString(e));
 }
 
-mma_status_t mma_get_stats(mma_stats_t* out) {
+mma_status_t mma_get_stats(mma_stats_t* out) try {
   if (!out) return fail(MMA_ERR_INVALID_ARG, "NULL out");
   if (!g_rt) return fail(MMA_ERR_NOT_INITIALIZED, "not initialised");
   // Transfers that the submitting threads track are retired when a thread
@@ -1095,6 +1139,8 @@ mma_status_t mma_get_stats(mma_stats_t* out) {
   out->sdma_engines_d2h = g_rt->eng[MMA_D2H]->sdma_mask();
   out->cu_path_enabled = (g_rt->eng[MMA_H2D]->cu_enabled() ? 1u : 0u) | (g_rt->eng[MMA_D2H]->cu_enabled() ? 2u : 0u);
   return MMA_OK;
+} catch (...) {
+  return boundary_error("mma_get_stats");
 }
 
 mma_status_t mma_reset_stats(void) {
@@ -1116,6 +1162,7 @@ const char* mma_status_str(mma_status_t s) {
     case MMA_ERR_NO_MEMORY: return "MMA_ERR_NO_MEMORY";
     case MMA_ERR_BUFFER_TOO_SMALL: return "MMA_ERR_BUFFER_TOO_SMALL";
     case MMA_ERR_TIMEOUT: return "MMA_ERR_TIMEOUT";
+    case MMA_ERR_INTERNAL: return "MMA_ERR_INTERNAL";
     default: return "MMA_ERR_UNKNOWN";
   }
 }
@@ -1128,14 +1175,16 @@ mma_status_t mma_clear_error(void) {
   return MMA_OK;
 }
 
-mma_status_t mma_trace_enable(int32_t on) {
+mma_status_t mma_trace_enable(int32_t on) try {
   std::lock_guard<std::mutex> g(g_trace_mu);
   if (on && !g_trace.load()) g_trace_buf.clear();
   g_trace = on ? 1 : 0;
   return MMA_OK;
+} catch (...) {
+  return boundary_error("mma_trace_enable");
 }
 
-mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out) {
+mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out) try {
   if (!n_out || (cap && !out)) return fail(MMA_ERR_INVALID_ARG, "NULL argument");
   if (g_rt)
     for (auto& e : g_rt->eng) e->reap();  // records of tracked transfers are written when they retire
@@ -1145,6 +1194,8 @@ mma_status_t mma_trace_read(mma_trace_rec_t* out, uint64_t cap, uint64_t* n_out)
   g_trace_buf.erase(g_trace_buf.begin(), g_trace_buf.begin() + static_cast<long>(n));
   *n_out = n;
   return MMA_OK;
+} catch (...) {
+  return boundary_error("mma_trace_read");
 }
 
 mma_status_t mma_test_set_fault(int32_t kind, uint64_t value) {

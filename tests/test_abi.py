@@ -95,6 +95,19 @@ def test_plan_linear_covers_exactly_once():
             assert (n == 0 and got == []) or oplan.covers_exactly_once([(o, b) for _, o, b, _ in got], n)
 
 
+def test_plan_limits():
+    """Plans too large for memory fail at once with MMA_ERR_NO_MEMORY (a count computed before any
+    item is stored), and a tensor whose last chunk ends at 2^64 - 1 is split without wrapping."""
+    for call in (lambda: mma.mma_plan_list([1 << 60], 1, 2, 1),
+                 lambda: mma.mma_plan_kv(1 << 62, 64, 1, 1)):
+        with pytest.raises(mma.MMAError) as e:
+            call()
+        assert e.value.name == "MMA_ERR_NO_MEMORY"
+    top = (1 << 64) - 1
+    assert mma.mma_plan_list([top], 1 << 63, 2, 1) == [(0, 0, 1 << 63, 0), (0, 1 << 63, top - (1 << 63), 0)]
+    assert mma.mma_status_str(-11) == "MMA_ERR_INTERNAL" and mma.mma_status_str(-8) == "MMA_ERR_NO_MEMORY"
+
+
 def test_validate_tables_matches_oracle():
     r = np.random.default_rng(4)
     for _ in range(300):
