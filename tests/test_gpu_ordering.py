@@ -22,7 +22,7 @@ if not torch.cuda.is_available():
     pytest.skip("no GPU", allow_module_level=True)
 
 import paper_2512_16056_amd as mma  # noqa: E402
-from gpu_helpers import PATHS, device_bytes, log, session, to_host  # noqa: E402
+from gpu_helpers import PATHS, device_bytes, from_host, log, session, to_host  # noqa: E402
 from test_gpu_kv import layout_of  # noqa: E402
 
 
@@ -30,7 +30,7 @@ def test_digest_kernel_matches_oracle():
     with session("both"):
         for n in (4, 8, 12, 1000, 4096, 65536 + 12, (1 << 22) + 4):
             src = np.ascontiguousarray(W.uniform_bytes(9, 0, n, n))
-            d = torch.from_numpy(src).cuda()
+            d = from_host(src)
             out = torch.zeros(1, dtype=torch.int64, device="cuda")
             mma.mma_digest_u32(d, n, out)
             torch.cuda.synchronize()
@@ -38,7 +38,7 @@ def test_digest_kernel_matches_oracle():
             assert got == odigest.digest(src), n
         # unaligned start (4-byte aligned only) and ragged tail
         src = np.ascontiguousarray(W.uniform_bytes(9, 1, 0, 4096))
-        d = torch.from_numpy(src).cuda()
+        d = from_host(src)
         out = torch.zeros(1, dtype=torch.int64, device="cuda")
         mma.mma_digest_u32(d.data_ptr() + 4, 4000 + 3, out)
         torch.cuda.synchronize()
@@ -104,7 +104,7 @@ def test_two_streams_concurrent(control):
         sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
         src = mma.PinnedBuffer(n)
         src.array[:] = W.uniform_bytes(11, 0, 0, n)
-        dev_b = torch.from_numpy(np.ascontiguousarray(W.uniform_bytes(11, 0, 1, n))).cuda()
+        dev_b = from_host(W.uniform_bytes(11, 0, 1, n))
         torch.cuda.synchronize()
         outs, hosts = [], []
         for rep in range(4):
