@@ -562,12 +562,15 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
   }
   if (!c.fallback_bytes) c.fallback_bytes = 2 * c.chunk_bytes;
   // A micro-task's ring entries must fit the ring next to the end-marker
-  // reserve of one slot per wave.
+  // reserve of one slot per wave (counted without forming chunk + sub, which
+  // could wrap).
   if (c.cu_sub_bytes % 16 || c.cu_sub_bytes < 256 || c.chunk_bytes % 16 || c.queue_depth > 16 ||
       c.cu_workgroups > kMaxWorkgroups || c.cu_queue_depth > 64 ||
       (c.engine_nap_us > 1000 && c.engine_nap_us != MMA_ENGINE_NAP_OFF) ||
-      (c.chunk_bytes + c.cu_sub_bytes - 1) / c.cu_sub_bytes > kRingSize / 2)
+      c.chunk_bytes / c.cu_sub_bytes + (c.chunk_bytes % c.cu_sub_bytes != 0) > kRingSize / 2)
     return fail(MMA_ERR_INVALID_ARG, "invalid configuration");
+  if (c.static_cu_percent > 100) return fail(MMA_ERR_INVALID_ARG, "static_cu_percent > 100");
+  if (c.control > MMA_CONTROL_DEVICE) return fail(MMA_ERR_INVALID_ARG, "unknown control mode %u", c.control);
 
   std::unique_ptr<Runtime> rt(new Runtime());
   rt->dev = hip_device;
@@ -578,12 +581,24 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
   if (hipDeviceGetAttribute(&wclk, hipDeviceAttributeWallClockRate, hip_device) == hipSuccess && wclk > 0)
     rt->wallclock_khz = static_cast<uint32_t>(wclk);
   if (hsa_init() != HSA_STATUS_SUCCESS) return fail(MMA_ERR_HSA, "hsa_init failed");
+  // Every way out of this call but success (an error return, an exception)
+  // gives the ROCr reference back, after the engines (their threads and
+  // signals) are gone.
+  struct HsaRef {
+    Runtime* rt;
+    bool held = true;
+    ~HsaRef() {
+      if (!held) return;
+      rt->eng[0].reset();
+      rt->eng[1].reset();
+      hsa_shut_down();
+    }
+  } hsa_ref{rt.get()};
   rt->hsa_up = true;
   rt->ag.want_bdf = static_cast<uint32_t>((prop.pciBusID << 8) | (prop.pciDeviceID << 3));
   rt->ag.want_domain = static_cast<uint32_t>(prop.pciDomainID);
   hsa_iterate_agents(agent_cb, &rt->ag);
   if (!rt->ag.have_gpu || !rt->ag.have_cpu) {
-    hsa_shut_down();
     return fail(MMA_ERR_HSA, "no ROCr agent for HIP device %d", hip_device);
   }
   uint32_t avail[2] = {0, 0}, nsdma = 0;
@@ -636,8 +651,6 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
   k.mask[1] = mask[1];
   k.duplex[0] = duplex[0];
   k.duplex[1] = duplex[1];
-  if (c.static_cu_percent > 100) return fail(MMA_ERR_INVALID_ARG, "static_cu_percent > 100");
-  if (c.control > MMA_CONTROL_DEVICE) return fail(MMA_ERR_INVALID_ARG, "unknown control mode %u", c.control);
   k.device = c.control == MMA_CONTROL_DEVICE ? 1u : 0u;
   k.device_cu_percent = c.static_cu_percent ? c.static_cu_percent : kDeviceCuPercent;
   k.static_split = c.static_split;
@@ -660,7 +673,6 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
       void* p = nullptr;
       if (hipExtMallocWithFlags(&p, need, hipDeviceMallocUncached) != hipSuccess) {
         (void)hipGetLastError();
-        hsa_shut_down();
         return fail(MMA_ERR_HIP, "staging allocation of %llu bytes failed", static_cast<unsigned long long>(need));
       }
       sc.dev = hip_device;
@@ -674,7 +686,6 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
     const hipError_t e = noalloc_setup(hip_device);
     if (e != hipSuccess) {
       (void)hipGetLastError();
-      hsa_shut_down();
       return fail(MMA_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
     }
   }
@@ -683,17 +694,13 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
     rt->eng[d].reset(new Engine(d, k, rt->backend.get(), &rt->stats));
     const uint32_t engines = (mask[d] | duplex[d]) & 0xFFFFu;
     mma_status_t s = rt->eng[d]->init(engines, stage_bytes, engines ? g_staging[d].base : nullptr);
-    if (s != MMA_OK) {
-      rt->eng[0].reset();
-      rt->eng[1].reset();
-      hsa_shut_down();
-      return s;
-    }
+    if (s != MMA_OK) return s;  // hsa_ref stops the engines created so far
     set_affinity_local(rt->eng[d]->native_handle(), hip_device);
   }
   rt->eng[MMA_D2H]->set_peer(rt->eng[MMA_H2D].get());
   rt->eng[MMA_H2D]->set_peer(rt->eng[MMA_D2H].get());
   if (env_u64("MMA_TRACE", 0)) g_trace = 1;
+  hsa_ref.held = false;  // mma_finalize gives it back
   g_rt = rt.release();
   return MMA_OK;
 } catch (...) {

@@ -79,3 +79,33 @@ def test_finalize_waits_for_transfers_in_flight(control):
     src.free()
     mma.mma_init(0)
     mma.mma_finalize()
+
+
+def test_init_rejects_invalid_configurations():
+    """mma_init refuses each invalid configuration with MMA_ERR_INVALID_ARG and stays uninitialised
+    (a chunk size near 2^64 among them, whose ring-entry count would wrap if formed as chunk + sub);
+    a second mma_init is MMA_ERR_ALREADY_INITIALIZED; a device index out of range is refused."""
+    import paper_2512_16056_amd as mma
+
+    bad = [dict(cu_sub_bytes=100), dict(cu_sub_bytes=128), dict(chunk_bytes=17),
+           dict(chunk_bytes=(1 << 64) - 16), dict(chunk_bytes=1 << 40), dict(queue_depth=17),
+           dict(cu_workgroups=257), dict(cu_queue_depth=65), dict(engine_nap_us=1001),
+           dict(static_cu_percent=101), dict(control=2)]
+    for over in bad:
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_init(0, **over)
+        assert e.value.name == "MMA_ERR_INVALID_ARG", over
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_get_config()
+        assert e.value.name == "MMA_ERR_NOT_INITIALIZED", over
+    with pytest.raises(mma.MMAError) as e:
+        mma.mma_init(torch.cuda.device_count())
+    assert e.value.name == "MMA_ERR_INVALID_ARG"
+    mma.mma_init(0)
+    try:
+        with pytest.raises(mma.MMAError) as e:
+            mma.mma_init(0)
+        assert e.value.name == "MMA_ERR_ALREADY_INITIALIZED"
+        assert mma.mma_get_config().chunk_bytes == 2 << 20
+    finally:
+        mma.mma_finalize()
