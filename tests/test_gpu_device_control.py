@@ -349,3 +349,47 @@ def test_device_beyond_ring_goes_to_engine_thread():
             assert np.array_equal(to_host(layers[l]).reshape(2, s.gpu_num_blocks, s.piece_bytes), want)
     assert stats["failed_transfers"] == 0
     assert stats["engine_wall_busy_ns"] > busy0, "the engine thread did not take the transfer"
+
+
+@pytest.mark.parametrize("direction", [mma.MMA_H2D, mma.MMA_D2H])
+def test_device_list_of_more_tensors_than_a_ring(direction):
+    """A tensor list of 5000 small tensors has more micro-tasks than a ring at any chunk size (one
+    per tensor): after the re-planning gives up it goes to the engine thread; byte-exact, gaps
+    between destinations untouched."""
+    sizes = [4096 + (k % 7) * 3 for k in range(5000)]
+    src_offs, total = W.arena_offsets(sizes, 16)
+    dst_offs, cur = [], 0
+    for z in sizes:
+        dst_offs.append(cur)
+        cur += z + 48
+    dtotal = cur
+    src_np = np.ascontiguousarray(W.uniform_bytes(61, direction, 0, total))
+    poison = np.full(dtotal, W.WEIGHT_POISON, np.uint8)
+    stream = torch.cuda.Stream()
+    with session("both", **DEVICE):
+        torch.cuda.synchronize()
+        busy0 = mma.mma_get_stats()["engine_wall_busy_ns"]
+        if direction == mma.MMA_H2D:
+            src = mma.PinnedBuffer(total)
+            src.array[:] = src_np
+            dst = from_host(poison)
+            torch.cuda.synchronize()
+            mma.mma_weights_load([(dst.data_ptr() + d, src.ptr + o, z) for d, o, z in zip(dst_offs, src_offs, sizes)],
+                                 direction, stream)
+            stream.synchronize()
+            got = to_host(dst)
+        else:
+            src = from_host(src_np)
+            dst = mma.PinnedBuffer(dtotal)
+            dst.array[:] = poison
+            torch.cuda.synchronize()
+            mma.mma_weights_load([(dst.ptr + d, src.data_ptr() + o, z) for d, o, z in zip(dst_offs, src_offs, sizes)],
+                                 direction, stream)
+            stream.synchronize()
+            got = dst.array.copy()
+        mma.mma_synchronize()
+        stats = mma.mma_get_stats()
+    want = ocopy.tensor_list(poison, src_np, list(zip(dst_offs, src_offs, sizes)))
+    assert np.array_equal(got, want)
+    assert stats["failed_transfers"] == 0
+    assert stats["engine_wall_busy_ns"] > busy0, "the engine thread did not take the transfer"
