@@ -849,8 +849,10 @@ mma_status_t mma_weights_load(const mma_copy_desc_t* list, uint64_t n, int32_t d
   // Device control plans a transfer into one ring of kRingSize micro-tasks. A
   // copy or list with more is planned again at twice the chunk size until it
   // fits, rather than handed to the engine thread (the model wake-up list has
-  // 7,723 micro-tasks at 2 MiB, 3,890 at 4 MiB).
-  if (rt->cfg.device) {
+  // 7,723 micro-tasks at 2 MiB, 3,890 at 4 MiB). A list of more tensors than
+  // that never fits (each tensor is at least one micro-task) and is not
+  // planned again.
+  if (rt->cfg.device && dsts.size() <= kRingSize) {
     Config c = rt->cfg;
     while (x->tasks.size() > kRingSize && c.chunk < kDeviceMaxChunk) {
       c.chunk *= 2;
