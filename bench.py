@@ -13,7 +13,7 @@ the same workload, native hipMemcpyAsync comparators, and the 64 MiB single-copy
 workload.
 
 Usage: python bench.py [--gpus 1] [--steps 10] [--warmup 2]
-       python bench.py --sweep sizes|idle|chunks|contention|duplex|paths|footprint|control|hbmpool|misaligned|mixed
+       python bench.py --sweep sizes|idle|blocking|chunks|contention|duplex|paths|footprint|control|hbmpool|misaligned|mixed
                                                                 (JSON per point)
        python bench.py --calib                                  (counter-scaling kernels)
 """
@@ -64,12 +64,13 @@ def parse():
     p.add_argument("--control", choices=["host", "device"], default=None,
                    help="who drives transfers after submission (default: the library's, MMA_CONTROL)")
     p.add_argument("--sweep", choices=["sizes", "idle", "chunks", "contention", "duplex", "paths", "footprint",
-                                       "control", "hbmpool", "misaligned", "mixed"],
+                                       "control", "hbmpool", "misaligned", "mixed", "blocking"],
                    help="instead of the benchmark, print one JSON line per point of a parameter sweep")
     p.add_argument("--oracle-cores", default=None,
                    help=argparse.SUPPRESS)  # the all-cores oracle baseline's worker process (CPU only)
     p.add_argument("--sizes", default=None,
-                   help="comma-separated transfer sizes in bytes for --sweep idle (default: 32 KiB to 8 GiB)")
+                   help="comma-separated transfer sizes in bytes for --sweep idle (default: 32 KiB to 8 GiB) "
+                        "or --sweep blocking (default: 64 KiB to 64 MiB)")
     p.add_argument("--calib", action="store_true",
                    help="only run plain kernels of known traffic (1 GiB fill, read, copy) for counter scaling")
     p.add_argument("--engine-nap-us", type=int, default=None,
@@ -841,6 +842,72 @@ def sweep_idle(sizes=None):
     mma.mma_finalize()
 
 
+def sweep_blocking(sizes=None):
+    """Blocking copies on a stream with nothing pending: host wall time from the call to its return,
+    median of the last 30 of 40 calls, alternating one hipMemcpyAsync + hipStreamSynchronize
+    (native), mma_memcpy_async + hipStreamSynchronize, and the blocking mma_memcpy_stream. Run for
+    the default configuration ("default") and with every copy kept off the whole-launch route
+    ("engine": cu_whole_bytes[_d2h] = 1). From the trace of the asynchronous calls, for transfers
+    the engine thread drives: when it published `complete` and when it retired the transfer,
+    counted from the call."""
+    import ctypes
+    import numpy as np
+    mma, torch, nat, st = _sweep_env()
+    sizes = sizes or [64 << 10, 256 << 10, 1 << 20, 4 << 20, 8 << 20, 16 << 20, 64 << 20]
+    top = max(sizes)
+    for mode in ("default", "engine"):
+        cfg = _default_config()
+        if mode == "engine":
+            cfg.cu_whole_bytes = cfg.cu_whole_bytes_d2h = 1
+        mma.mma_init(0, cfg)
+        h = mma.PinnedBuffer(top)
+        h.array[::4096] = 1
+        d = torch.empty(top, dtype=torch.uint8, device="cuda")
+        sp = ctypes.c_void_p(st.cuda_stream)
+        outcome = ctypes.c_int32(0)
+        for n in sizes:
+            row = {"mode": mode, "bytes": n}
+            for dr, name in ((0, "h2d"), (1, "d2h")):
+                dst, src = (d.data_ptr(), h.ptr) if dr == 0 else (h.ptr, d.data_ptr())
+                D, S, Z = (ctypes.c_void_p * 1)(dst), (ctypes.c_void_p * 1)(src), (ctypes.c_uint64 * 1)(n)
+                margs = (ctypes.c_void_p(dst), ctypes.c_void_p(src), ctypes.c_uint64(n), dr, sp)
+                tn, ta, tb, starts = [], [], [], []
+                mma.mma_trace_enable(True)
+                for _ in range(40):
+                    st.synchronize()
+                    t0 = time.perf_counter_ns()
+                    nat.native_list(D, S, Z, 1, dr, sp)
+                    st.synchronize()
+                    tn.append(time.perf_counter_ns() - t0)
+                    time.sleep(0.0002)
+                    t0 = time.perf_counter_ns()
+                    _ok(mma.lib.mma_memcpy_async(*margs))
+                    st.synchronize()
+                    ta.append(time.perf_counter_ns() - t0)
+                    starts.append(t0)
+                    mma.mma_synchronize()
+                    time.sleep(0.0002)
+                    t0 = time.perf_counter_ns()
+                    _ok(mma.lib.mma_memcpy_stream(*margs, ctypes.byref(outcome)))
+                    tb.append(time.perf_counter_ns() - t0)
+                    time.sleep(0.0002)
+                mma.mma_synchronize()
+                recs = mma.mma_trace_read()[-80:][0::2]  # the asynchronous calls' records
+                mma.mma_trace_enable(False)
+                got = mma.mma_get_config()
+                limit = got.cu_whole_bytes if dr == 0 else got.cu_whole_bytes_d2h
+                eng = list(zip(recs, starts))[10:] if n > limit else []  # engine-driven transfers only
+                med = lambda v: round(float(np.median(v[10:])) / 1e3, 1)
+                row[name] = {"native_us": med(tn), "async_sync_us": med(ta), "blocking_us": med(tb),
+                             "complete_us": round(float(np.median([(r["t_complete_ns"] - t) / 1e3 for r, t in eng])), 1)
+                             if eng else None,
+                             "retire_us": round(float(np.median([(r["t_retire_ns"] - t) / 1e3 for r, t in eng])), 1)
+                             if eng else None}
+            _emit(sweep="blocking", **row)
+        h.free()
+        mma.mma_finalize()
+
+
 def _busy_timed(torch, st, fn, reps, warm):
     """HIP-event time of fn() queued behind about a millisecond of other work on `st`: the
     stream has work pending when fn is called. Median and the list, in ms."""
@@ -1510,7 +1577,7 @@ def sweep_hbmpool():
 
 SWEEPS = {"sizes": sweep_sizes, "idle": sweep_idle, "chunks": sweep_chunks, "contention": sweep_contention, "duplex": sweep_duplex,
           "paths": sweep_paths, "footprint": sweep_footprint, "control": sweep_control, "hbmpool": sweep_hbmpool,
-          "misaligned": sweep_misaligned, "mixed": sweep_mixed}
+          "misaligned": sweep_misaligned, "mixed": sweep_mixed, "blocking": sweep_blocking}
 
 
 def main():
