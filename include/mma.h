@@ -257,7 +257,8 @@ mma_status_t mma_config_default(mma_config_t* out);
  * MMA_CU_WGS, MMA_CU_SUB_BYTES, MMA_WATCHDOG_MS, MMA_SDMA_MERGE_TASKS,
  * MMA_CU_WHOLE_BYTES, MMA_CU_WHOLE_BYTES_D2H, MMA_CONTROL, MMA_STATIC_CU_PERCENT,
  * MMA_DUPLEX_PATHS_H2D, MMA_DUPLEX_PATHS_D2H, MMA_ENGINE_NAP_US, MMA_TRACE).
- * Errors: MMA_ERR_ALREADY_INITIALIZED, MMA_ERR_INVALID_ARG (bad device or
+ * As in cfg, 0 selects a field's default; an environment value that does not
+ * parse as a number reads as 0. Errors: MMA_ERR_ALREADY_INITIALIZED, MMA_ERR_INVALID_ARG (bad device or
  * config), MMA_ERR_HIP / MMA_ERR_HSA. */
 mma_status_t mma_init(int hip_device, const mma_config_t* cfg);
 

@@ -542,24 +542,25 @@ mma_status_t mma_init(int hip_device, const mma_config_t* user_cfg) try {
     (void)hipGetLastError();
     return fail(MMA_ERR_INVALID_ARG, "invalid HIP device %d (%d devices)", hip_device, ndev);
   }
-  mma_config_t c;
-  if (user_cfg) {
-    mma_config_t d;
-    fill_config(&d, false);
+  // Zero selects a field's default, whether it came in the caller's
+  // configuration or from the environment (where an unparsable value reads
+  // as 0).
+  mma_config_t c, d;
+  fill_config(&d, false);
+  if (user_cfg)
     c = *user_cfg;
-    if (!c.chunk_bytes) c.chunk_bytes = d.chunk_bytes;
-    if (!c.small_bytes) c.small_bytes = d.small_bytes;
-    if (!c.queue_depth) c.queue_depth = d.queue_depth;
-    if (!c.cu_queue_depth) c.cu_queue_depth = d.cu_queue_depth;
-    if (!c.cu_workgroups) c.cu_workgroups = d.cu_workgroups;
-    if (!c.cu_sub_bytes) c.cu_sub_bytes = d.cu_sub_bytes;
-    if (!c.watchdog_ms) c.watchdog_ms = d.watchdog_ms;
-    if (!c.cu_whole_bytes) c.cu_whole_bytes = d.cu_whole_bytes;
-    if (!c.cu_whole_bytes_d2h) c.cu_whole_bytes_d2h = d.cu_whole_bytes_d2h;
-    if (!c.engine_nap_us) c.engine_nap_us = d.engine_nap_us;
-  } else {
+  else
     fill_config(&c, true);
-  }
+  if (!c.chunk_bytes) c.chunk_bytes = d.chunk_bytes;
+  if (!c.small_bytes) c.small_bytes = d.small_bytes;
+  if (!c.queue_depth) c.queue_depth = d.queue_depth;
+  if (!c.cu_queue_depth) c.cu_queue_depth = d.cu_queue_depth;
+  if (!c.cu_workgroups) c.cu_workgroups = d.cu_workgroups;
+  if (!c.cu_sub_bytes) c.cu_sub_bytes = d.cu_sub_bytes;
+  if (!c.watchdog_ms) c.watchdog_ms = d.watchdog_ms;
+  if (!c.cu_whole_bytes) c.cu_whole_bytes = d.cu_whole_bytes;
+  if (!c.cu_whole_bytes_d2h) c.cu_whole_bytes_d2h = d.cu_whole_bytes_d2h;
+  if (!c.engine_nap_us) c.engine_nap_us = d.engine_nap_us;
   if (!c.fallback_bytes) c.fallback_bytes = 2 * c.chunk_bytes;
   // A micro-task's ring entries must fit the ring next to the end-marker
   // reserve of one slot per wave (counted without forming chunk + sub, which

@@ -109,3 +109,42 @@ def test_init_rejects_invalid_configurations():
         assert mma.mma_get_config().chunk_bytes == 2 << 20
     finally:
         mma.mma_finalize()
+
+
+def test_environment_zero_selects_defaults():
+    """Configured from the environment (mma_init without a configuration), 0 and values that do not
+    parse select the defaults as 0 does in a configuration; a copy then runs byte-exact."""
+    import numpy as np
+
+    import paper_2512_16056_amd as mma
+    from oracle import copy as ocopy
+    import workloads as W
+
+    keys = {"MMA_CHUNK_BYTES": "0", "MMA_CU_WGS": "0", "MMA_QUEUE_DEPTH": "x", "MMA_CU_QUEUE_DEPTH": "0",
+            "MMA_CU_SUB_BYTES": "0", "MMA_WATCHDOG_MS": "none", "MMA_CU_WHOLE_BYTES": "0"}
+    saved = {k: os.environ.get(k) for k in keys}
+    os.environ.update(keys)
+    try:
+        mma.mma_init(0)
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    try:
+        c, d = mma.mma_get_config(), mma.mma_config_default()
+        for f in ("chunk_bytes", "cu_workgroups", "queue_depth", "cu_queue_depth", "cu_sub_bytes", "watchdog_ms",
+                  "cu_whole_bytes"):
+            assert getattr(c, f) == getattr(d, f), f
+        n = (40 << 20) + 5
+        src_np = np.ascontiguousarray(W.uniform_bytes(71, 0, 0, n))
+        src = mma.PinnedBuffer(n)
+        src.array[:] = src_np
+        dst = torch.full((n,), W.WEIGHT_POISON, dtype=torch.uint8, device="cuda")
+        mma.mma_memcpy_async(dst, src, n, mma.MMA_H2D)
+        torch.cuda.synchronize()
+        assert np.array_equal(dst.cpu().numpy(), ocopy.memcpy(np.full(n, W.WEIGHT_POISON, np.uint8), 0, src_np, 0, n))
+        src.free()
+    finally:
+        mma.mma_finalize()
