@@ -1,7 +1,8 @@
 /* A plain C program that uses the library through include/mma.h alone: no
  * Python, no torch. It copies a ragged buffer host -> device -> host on its
- * own non-blocking stream, loads a three-tensor list, reads the stats, and
- * checks every byte against the source (a copy's definition). The library is
+ * own non-blocking stream, loads a three-tensor list, reads the stats, fetches
+ * paged-KV blocks into buffers sized with mma_kv_layout_sizes, and checks every
+ * byte against the source (a copy's and the KV layout's definition). The library is
  * initialised from the environment (MMA_* variables), so the same program
  * runs under either control mode. Prints "ALL OK" and exits 0 on success.
  */
@@ -113,6 +114,55 @@ int main(void) {
     expect(st.transfers == 6, "transfer count");
     expect(total == 2 * n + 2 * ((3u << 20) + (17u << 20) + 8), "payload bytes");
   }
+  /* a paged-KV fetch, its buffers sized with mma_kv_layout_sizes: every piece of every moved
+   * block must equal its slot's piece in the pool (the layout's definition), the other GPU
+   * blocks keep their fill */
+  {
+    mma_kv_layout_t lay = {2, 16, 2, 64, 2, 10, 8, MMA_KV_LAYOUT_PIECE};
+    const int32_t slots[5] = {3, 0, 7, 5, 1}, blocks[5] = {9, 2, 4, 0, 6};
+    uint64_t piece = 0, slot = 0, pool_bytes = 0, layer_bytes = 0;
+    uint8_t *pool = NULL, *layer_host = NULL;
+    void* layers[2] = {NULL, NULL};
+    uint32_t l, k, j, b;
+    mma_kv_layout_t wrap = {256, 1u << 16, 1u << 16, 1, 1, 1, 1u << 23, MMA_KV_LAYOUT_PIECE};
+    expect(mma_kv_layout_sizes(&wrap, NULL, NULL, &pool_bytes, NULL) == MMA_ERR_INVALID_ARG,
+           "a layout whose pool size wraps 64 bits was accepted");
+    CHECK_MMA(mma_kv_layout_sizes(&lay, &piece, &slot, &pool_bytes, &layer_bytes));
+    expect(piece == 4096 && slot == 4 * 4096 && pool_bytes == 8 * slot && layer_bytes == 2 * 10 * 4096,
+           "layout sizes");
+    CHECK_MMA(mma_host_alloc(pool_bytes, (void**)&pool));
+    layer_host = (uint8_t*)malloc(layer_bytes);
+    for (i = 0; i < pool_bytes; ++i) pool[i] = (uint8_t)(i * 40503u >> 7);
+    for (l = 0; l < 2; ++l) {
+      CHECK_HIP(hipMalloc(&layers[l], layer_bytes));
+      CHECK_HIP(hipMemset(layers[l], 0x5A, layer_bytes));
+    }
+    CHECK_HIP(hipDeviceSynchronize());
+    CHECK_MMA(mma_kv_fetch(&lay, pool, layers, slots, blocks, 5, stream));
+    CHECK_HIP(hipStreamSynchronize(stream));
+    for (l = 0; l < 2; ++l) {
+      CHECK_HIP(hipMemcpy(layer_host, layers[l], layer_bytes, hipMemcpyDeviceToHost));
+      for (k = 0; k < 2; ++k)
+        for (b = 0; b < 10; ++b) {
+          const uint8_t* got = layer_host + (k * 10 + b) * piece;
+          int moved = -1;
+          for (j = 0; j < 5; ++j)
+            if ((uint32_t)blocks[j] == b) moved = (int)j;
+          if (moved >= 0) {
+            expect(memcmp(got, pool + slots[moved] * slot + (2 * l + k) * piece, piece) == 0,
+                   "fetched KV piece differs from its pool slot");
+          } else {
+            for (i = 0; i < piece; ++i)
+              if (got[i] != 0x5A) break;
+            expect(i == piece, "a GPU block outside the table was written");
+          }
+        }
+      CHECK_HIP(hipFree(layers[l]));
+    }
+    free(layer_host);
+    CHECK_MMA(mma_host_free(pool));
+  }
+
   CHECK_HIP(hipStreamDestroy(stream));
   CHECK_HIP(hipFree(dev));
   CHECK_MMA(mma_host_free(src));
