@@ -51,10 +51,21 @@ void plan_kv(uint64_t n_blocks, uint32_t pieces_per_block, uint64_t piece_bytes,
 }
 
 bool tables_valid(const int32_t* src, uint32_t src_count, const int32_t* dst, uint32_t dst_count, uint64_t n) {
-  std::vector<uint8_t> seen(dst_count, 0);
   for (uint64_t i = 0; i < n; ++i) {
     if (src[i] < 0 || static_cast<uint32_t>(src[i]) >= src_count) return false;
     if (dst[i] < 0 || static_cast<uint32_t>(dst[i]) >= dst_count) return false;
+  }
+  if (n < 2) return true;
+  // Distinct destinations. A short table against a large cache (a few blocks
+  // fetched into millions) sorts a copy of its n entries rather than clearing
+  // a flag per destination block on every call.
+  if (n < dst_count / 64) {
+    std::vector<int32_t> d(dst, dst + n);
+    std::sort(d.begin(), d.end());
+    return std::adjacent_find(d.begin(), d.end()) == d.end();
+  }
+  std::vector<uint8_t> seen(dst_count, 0);
+  for (uint64_t i = 0; i < n; ++i) {
     if (seen[dst[i]]) return false;
     seen[dst[i]] = 1;
   }

@@ -118,6 +118,18 @@ def test_validate_tables_matches_oracle():
         assert mma.mma_validate_kv_tables(src, sc, dst, dc) == okv.validate_tables(src, sc, dst, dc)
     for perm in itertools.permutations(range(4)):
         assert mma.mma_validate_kv_tables([0, 1, 2, 3], 4, perm, 4)
+    # short tables against large destination counts (the sorted check) and long ones (the bitmap)
+    for _ in range(200):
+        dc = int(r.choice([1000, 100_000, 5_000_000]))
+        n = int(r.integers(2, 40)) if r.random() < 0.7 else int(r.integers(dc // 64, dc // 64 + 50))
+        dst = r.choice(dc, n, replace=False) if dc <= 100_000 else r.permutation(np.unique(r.integers(0, dc, 2 * n)))[:n]
+        n = len(dst)
+        if r.random() < 0.5:
+            dst[int(r.integers(1, n))] = dst[int(r.integers(0, n))]  # a duplicate (or, rarely, the same slot)
+        if r.random() < 0.1:
+            dst[int(r.integers(0, n))] = dc  # out of range
+        src = r.integers(0, 8, n)
+        assert mma.mma_validate_kv_tables(src, 8, dst, dc) == okv.validate_tables(src, 8, dst, dc), (dc, n)
 
 
 def test_kv_layout_sizes():
